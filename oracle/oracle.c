@@ -1,0 +1,261 @@
+/*
+ * CPU oracle for one synchronous SGD step of a convnet replica.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, obviously correct
+ * reference that the HIP kernels are checked against.  Only the tests, the
+ * smoke check and the bench's CPU-baseline leg may load it; the product path
+ * never does.  It shares no code, header or constant with the HIP library.
+ *
+ * Every array is dense and float64.  Activations are NHWC row-major
+ * (x[n][h][w][c]); filters are HWIO row-major (w[kh][kw][ci][co]); pool argmax
+ * is int32.  Every sum runs in a fixed order inside one output element, and
+ * OpenMP only splits *independent* output elements across threads, so results
+ * are bitwise identical for any thread count.
+ *
+ * The paper (Section 3.1) treats a mini-batch 2-D convolution as an operation
+ * from two 4-D tensors to a 4-D tensor, and (Section 6.1) puts convolution and
+ * pooling on the critical path of training; it does not spell out their
+ * arithmetic.  The definitions below use the conventions of the paper's
+ * system: cross-correlation (no filter flip), explicit padding, max-pooling
+ * over in-bounds taps only, gradient = sum of the partial gradients of every
+ * path (Section 4.1), and the update W' = W - alpha * dL/dW (Section 4.1).
+ *
+ * Parity pins (what fixes each function independently of this file) live in
+ * the CPU tests: brute-force finite differences, adjoint identities, delta
+ * kernels, library convolution and matmul, closed forms and brute-force
+ * window scans.
+ */
+#include <stdint.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+typedef int64_t i64;
+
+int orc_num_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+void orc_set_num_threads(int n) {
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
+/* Number of windows along one axis with explicit padding: floor((n+p0+p1-k)/s)+1. */
+int orc_out_len(int n, int k, int s, int p0, int p1) {
+    int span = n + p0 + p1 - k;
+    if (span < 0 || s <= 0) return 0;
+    return span / s + 1;
+}
+
+/*
+ * Conv2D forward (cross-correlation):
+ *   y[n,oh,ow,co] = sum_{kh,kw,ci} X[n, oh*sh+kh-pt, ow*sw+kw-pl, ci] * w[kh,kw,ci,co]
+ * with X = 0 outside [0,H) x [0,W).  Sum order: kh, kw, ci.
+ */
+void orc_conv2d_fwd(const double *x, int N, int H, int W, int C,
+                    const double *w, int KH, int KW, int K,
+                    int sh, int sw, int pt, int pl,
+                    double *y, int OH, int OW) {
+    i64 npix = (i64)N * OH * OW;
+#pragma omp parallel for schedule(static)
+    for (i64 p = 0; p < npix; ++p) {
+        int n = (int)(p / ((i64)OH * OW));
+        int oh = (int)((p / OW) % OH);
+        int ow = (int)(p % OW);
+        double *out = y + p * K;
+        for (int co = 0; co < K; ++co) out[co] = 0.0;
+        for (int kh = 0; kh < KH; ++kh) {
+            int ih = oh * sh + kh - pt;
+            if (ih < 0 || ih >= H) continue;
+            for (int kw = 0; kw < KW; ++kw) {
+                int iw = ow * sw + kw - pl;
+                if (iw < 0 || iw >= W) continue;
+                const double *xin = x + (((i64)n * H + ih) * W + iw) * C;
+                for (int ci = 0; ci < C; ++ci) {
+                    const double xv = xin[ci];
+                    const double *wr = w + (((i64)kh * KW + kw) * C + ci) * K;
+                    for (int co = 0; co < K; ++co) out[co] += xv * wr[co];
+                }
+            }
+        }
+    }
+}
+
+/*
+ * Conv2DBackpropInput: the adjoint of the forward map in x.
+ *   dx[n,h,w,ci] = sum over (kh,kw,co) and the unique (oh,ow) with
+ *                  oh*sh + kh - pt = h and ow*sw + kw - pl = w
+ *                  (0 <= oh < OH, 0 <= ow < OW) of dy[n,oh,ow,co] * w[kh,kw,ci,co].
+ * Written as a gather per dx element; input positions no window reaches get 0.
+ * beta == 0: dx is overwritten; beta == 1: the sum is added to dx.
+ * Sum order: kh, kw, co (after the old value when beta == 1).
+ */
+void orc_conv2d_bwd_input(const double *dy, int N, int OH, int OW, int K,
+                          const double *w, int KH, int KW,
+                          int sh, int sw, int pt, int pl,
+                          double *dx, int H, int W, int C, int beta) {
+    i64 npix = (i64)N * H * W;
+#pragma omp parallel for schedule(static)
+    for (i64 p = 0; p < npix; ++p) {
+        int n = (int)(p / ((i64)H * W));
+        int h = (int)((p / W) % H);
+        int wi = (int)(p % W);
+        for (int ci = 0; ci < C; ++ci) {
+            double acc = beta ? dx[p * C + ci] : 0.0;
+            for (int kh = 0; kh < KH; ++kh) {
+                int th = h + pt - kh;            /* = oh*sh */
+                if (th < 0 || th % sh != 0) continue;
+                int oh = th / sh;
+                if (oh >= OH) continue;
+                for (int kw = 0; kw < KW; ++kw) {
+                    int tw = wi + pl - kw;       /* = ow*sw */
+                    if (tw < 0 || tw % sw != 0) continue;
+                    int ow = tw / sw;
+                    if (ow >= OW) continue;
+                    const double *g = dy + (((i64)n * OH + oh) * OW + ow) * K;
+                    const double *wr = w + (((i64)kh * KW + kw) * C + ci) * K;
+                    for (int co = 0; co < K; ++co) acc += g[co] * wr[co];
+                }
+            }
+            dx[p * C + ci] = acc;
+        }
+    }
+}
+
+/*
+ * Conv2DBackpropFilter: the adjoint of the forward map in w.
+ *   dw[kh,kw,ci,co] = sum_{n,oh,ow} X[n, oh*sh+kh-pt, ow*sw+kw-pl, ci] * dy[n,oh,ow,co]
+ * (padding contributes nothing).  dw is overwritten.  Sum order: n, oh, ow.
+ */
+void orc_conv2d_bwd_filter(const double *x, int N, int H, int W, int C,
+                           const double *dy, int OH, int OW, int K,
+                           int KH, int KW, int sh, int sw, int pt, int pl,
+                           double *dw) {
+    i64 rows = (i64)KH * KW * C;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (i64 r = 0; r < rows; ++r) {
+        int kh = (int)(r / ((i64)KW * C));
+        int kw = (int)((r / C) % KW);
+        int ci = (int)(r % C);
+        double *out = dw + r * K;
+        for (int co = 0; co < K; ++co) out[co] = 0.0;
+        for (int n = 0; n < N; ++n)
+            for (int oh = 0; oh < OH; ++oh) {
+                int ih = oh * sh + kh - pt;
+                if (ih < 0 || ih >= H) continue;
+                for (int ow = 0; ow < OW; ++ow) {
+                    int iw = ow * sw + kw - pl;
+                    if (iw < 0 || iw >= W) continue;
+                    const double xv = x[(((i64)n * H + ih) * W + iw) * C + ci];
+                    const double *g = dy + (((i64)n * OH + oh) * OW + ow) * K;
+                    for (int co = 0; co < K; ++co) out[co] += xv * g[co];
+                }
+            }
+    }
+}
+
+/*
+ * Fused BiasAdd + ReLU forward over P pixels of C channels:
+ *   y = pre + b[c];  y = (y > 0) ? y : +0.0
+ * (the paper's hand-fused ReLU kernels, Section 5).  y may equal pre.
+ */
+void orc_bias_relu_fwd(const double *pre, const double *b, i64 P, int C, double *y) {
+#pragma omp parallel for schedule(static)
+    for (i64 p = 0; p < P; ++p)
+        for (int c = 0; c < C; ++c) {
+            double v = pre[p * C + c] + b[c];
+            y[p * C + c] = v > 0.0 ? v : 0.0;
+        }
+}
+
+/*
+ * ReLU backward + bias gradient:
+ *   dpre = (y > 0) ? dy : 0            (mask from the stored output y)
+ *   db[c] = sum_p dpre[p, c]           (ascending p)
+ * dpre may equal dy.
+ */
+void orc_bias_relu_bwd(const double *y, const double *dy, i64 P, int C,
+                       double *dpre, double *db) {
+#pragma omp parallel for schedule(static)
+    for (i64 p = 0; p < P; ++p)
+        for (int c = 0; c < C; ++c)
+            dpre[p * C + c] = y[p * C + c] > 0.0 ? dy[p * C + c] : 0.0;
+#pragma omp parallel for schedule(static)
+    for (int c = 0; c < C; ++c) {
+        double s = 0.0;
+        for (i64 p = 0; p < P; ++p) s += dpre[p * C + c];
+        db[c] = s;
+    }
+}
+
+/*
+ * MaxPool forward with argmax.  For each output (n,oh,ow,c) the window taps
+ * are scanned kh outer, kw inner, skipping taps outside [0,H) x [0,W).  The
+ * first in-bounds tap seeds the maximum; a later tap replaces it only if
+ * strictly greater, so the first maximum in scan order wins.  argmax is the
+ * flat dense NHWC index ((n*H + h)*W + w)*C + c into x.  A window with no
+ * in-bounds tap yields y = 0 and argmax = -1 (the HIP library rejects such
+ * windows before launching).
+ */
+void orc_maxpool_fwd(const double *x, int N, int H, int W, int C,
+                     int KH, int KW, int sh, int sw, int pt, int pl,
+                     double *y, int32_t *argmax, int OH, int OW) {
+    i64 total = (i64)N * OH * OW * C;
+#pragma omp parallel for schedule(static)
+    for (i64 o = 0; o < total; ++o) {
+        int c = (int)(o % C);
+        i64 pix = o / C;
+        int ow = (int)(pix % OW);
+        int oh = (int)((pix / OW) % OH);
+        int n = (int)(pix / ((i64)OW * OH));
+        int have = 0;
+        double best = 0.0;
+        i64 besti = -1;
+        for (int kh = 0; kh < KH; ++kh) {
+            int ih = oh * sh + kh - pt;
+            if (ih < 0 || ih >= H) continue;
+            for (int kw = 0; kw < KW; ++kw) {
+                int iw = ow * sw + kw - pl;
+                if (iw < 0 || iw >= W) continue;
+                i64 idx = (((i64)n * H + ih) * W + iw) * C + c;
+                double v = x[idx];
+                if (!have || v > best) {
+                    best = v;
+                    besti = idx;
+                    have = 1;
+                }
+            }
+        }
+        y[o] = best;
+        argmax[o] = (int32_t)besti;
+    }
+}
+
+/*
+ * MaxPool backward: dx[i] = (beta ? dx[i] : 0) + sum_{o : argmax[o] == i} dy[o],
+ * the routed contributions added in ascending o.  nx = number of x elements,
+ * ny = number of pooled elements.  Indices outside [0, nx) are ignored.
+ */
+void orc_maxpool_bwd(const double *dy, const int32_t *argmax, i64 ny,
+                     double *dx, i64 nx, int beta) {
+    if (!beta) memset(dx, 0, sizeof(double) * (size_t)nx);
+    for (i64 o = 0; o < ny; ++o) {
+        i64 i = argmax[o];
+        if (i >= 0 && i < nx) dx[i] += dy[o];
+    }
+}
+
+/* ApplyGradientDescent, in place: var <- var - lr * grad (Section 4.1). */
+void orc_apply_sgd(double *var, const double *grad, i64 n, double lr) {
+#pragma omp parallel for schedule(static)
+    for (i64 i = 0; i < n; ++i) var[i] = var[i] - lr * grad[i];
+}

@@ -1,0 +1,218 @@
+"""The CPU oracle pinned to the mathematics (no GPU).
+
+Bars: exact or ~1e-12 for the identities that hold in fp64, and the 1e-6
+relative bar for brute-force finite differences.
+"""
+import os
+import shutil
+import subprocess
+import tempfile
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1605_08695_amd import workloads as W
+from tests import pins
+
+FD_BAR = 1e-6
+
+
+def test_conv_fwd_matches_library_conv():
+    assert pins.check_conv_vs_torch() < 1e-12
+
+
+def test_conv_shifted_delta_fixes_no_flip():
+    assert pins.check_shifted_delta(1) == 0.0
+    assert pins.check_shifted_delta(2) == 0.0
+
+
+def test_conv_delta_kernel_is_identity():
+    assert pins.check_delta_identity(3) == 0.0
+    assert pins.check_delta_identity(5) == 0.0
+
+
+def test_conv_1x1_is_matmul():
+    assert pins.check_one_by_one_is_matmul() < 1e-13
+
+
+def test_full_window_conv_is_fc_layer():
+    assert pins.check_full_window_is_fc() < 1e-13
+
+
+def test_conv_padding_closed_form():
+    assert pins.check_all_ones_closed_form() == 0.0
+
+
+def test_conv_adjoint_identities():
+    assert pins.check_adjoints() < 1e-12
+
+
+def test_conv_bwd_input_unused_rows_zero():
+    assert pins.check_unused_rows_get_zero() == 0.0
+
+
+def test_conv_gradients_finite_differences():
+    assert pins.check_conv_fd() < FD_BAR
+
+
+def test_conv_bwd_input_beta_accumulates():
+    rng = np.random.default_rng(20)
+    w = rng.standard_normal((3, 3, 2, 4))
+    g = rng.standard_normal((1, 4, 4, 4))
+    base = rng.standard_normal((1, 4, 4, 2))
+    d0 = oracle.conv2d_bwd_input(g, w, base.shape, 1, (1, 1, 1, 1))
+    d1 = oracle.conv2d_bwd_input(g, w, base.shape, 1, (1, 1, 1, 1), dx=base, beta=1)
+    assert pins.rel(d1, base + d0) < 1e-14
+
+
+def test_pool_matches_bruteforce_scan_with_ties():
+    assert pins.check_pool_bruteforce() == 0.0
+
+
+def test_pool_nonoverlapping_is_reshape_max():
+    assert pins.check_pool_reshape_max() == 0.0
+
+
+def test_pool_bwd_mass_support_fd():
+    assert pins.check_pool_bwd() < FD_BAR
+
+
+def test_pool_bwd_beta():
+    assert pins.check_pool_bwd_beta() < 1e-15
+
+
+def test_pool_all_zero_window_picks_first_tap():
+    x = np.zeros((1, 4, 4, 2))
+    _, am = oracle.maxpool_fwd(x, (3, 3), 1, (1, 1, 1, 1))
+    # window at (0,0) starts at padded (-1,-1): first in-bounds tap is (0,0)
+    assert am[0, 0, 0, 0] == 0 and am[0, 0, 0, 1] == 1
+    # window at (2,2) starts at (1,1)
+    assert am[0, 2, 2, 0] == ((0 * 4 + 1) * 4 + 1) * 2
+
+
+def test_bias_relu():
+    assert pins.check_bias_relu() < FD_BAR
+
+
+def test_sgd_linear_loss_decrease():
+    assert pins.check_sgd_decrease() < 1e-10
+
+
+def test_single_layer_step_finite_differences():
+    net = W.single_layer(batch=2, hw=8, cin=3, cout=4)
+    inp = W.make_inputs(net, seed=3)
+    assert pins.check_step_fd(net, inp) < FD_BAR
+
+
+def test_single_layer_step_first_order_decrease():
+    net = W.single_layer(batch=2, hw=8, cin=3, cout=4)
+    inp = W.make_inputs(net, seed=4)
+    assert pins.check_step_decrease(net, inp) < 1e-6
+
+
+def test_inception_style_step_sums_fanout_gradients():
+    """A two-branch module with concat: FD of the whole step in a filter of each branch."""
+    b = W._Builder("tiny_inception", "f32", 0.01, True, (1, 5, 5, 3))
+    cat = b.concat_buffer("x", (5, 5), 4 + 2 + 3)
+    b.conv("x", 4, 1, dst=cat, c0=0, name="a")
+    r = b.conv("x", 2, 1, name="r")
+    b.conv(r, 2, 3, pads=(1, 1, 1, 1), dst=cat, c0=4, name="b")
+    p = b.pool("x", 3, 1, pads=(1, 1, 1, 1), name="p")
+    b.conv(p, 3, 1, dst=cat, c0=6, name="c")
+    net = b.done(cat)
+    inp = W.make_inputs(net, seed=5)
+    from oracle import net as onet
+    res = onet.step(net, inp.x, inp.weights, inp.biases, inp.g)
+    rng = np.random.default_rng(0)
+    h = 1e-6
+    worst = 0.0
+    for name in ("a", "r", "b", "c"):
+        Wt = inp.weights[name]
+        for _ in range(6):
+            idx = tuple(int(rng.integers(0, d)) for d in Wt.shape)
+            ws_p = dict(inp.weights)
+            ws_m = dict(inp.weights)
+            ws_p[name] = Wt.copy()
+            ws_m[name] = Wt.copy()
+            ws_p[name][idx] += h
+            ws_m[name][idx] -= h
+            fd = (onet.loss(net, inp.x, ws_p, inp.biases, inp.g) -
+                  onet.loss(net, inp.x, ws_m, inp.biases, inp.g)) / (2 * h)
+            worst = max(worst, abs(fd - res["dW"][name][idx]) / max(1.0, abs(fd)))
+    # dx sums four paths (three 1x1 branches and the pool branch)
+    for _ in range(6):
+        idx = tuple(int(rng.integers(0, d)) for d in inp.x.shape)
+        xp, xm = inp.x.copy(), inp.x.copy()
+        xp[idx] += h
+        xm[idx] -= h
+        fd = (onet.loss(net, xp, inp.weights, inp.biases, inp.g) -
+              onet.loss(net, xm, inp.weights, inp.biases, inp.g)) / (2 * h)
+        worst = max(worst, abs(fd - res["grads"]["x"][idx]) / max(1.0, abs(fd)))
+    assert worst < FD_BAR
+
+
+def test_oracle_deterministic_across_thread_counts():
+    rng = np.random.default_rng(30)
+    x = rng.standard_normal((2, 9, 9, 8))
+    w = rng.standard_normal((3, 3, 8, 16))
+    n0 = oracle.num_threads()
+    try:
+        oracle.set_num_threads(1)
+        a = oracle.conv2d_bwd_filter(x, oracle.conv2d_fwd(x, w, 1, (1, 1, 1, 1)), (3, 3), 1, (1, 1, 1, 1))
+        oracle.set_num_threads(max(2, n0))
+        b = oracle.conv2d_bwd_filter(x, oracle.conv2d_fwd(x, w, 1, (1, 1, 1, 1)), (3, 3), 1, (1, 1, 1, 1))
+    finally:
+        oracle.set_num_threads(n0)
+    assert np.array_equal(a, b)
+
+
+# ----------------------------------------------------------------------------- mutations
+# Each mutation plants one plausible mistake in a copy of oracle.c; the pins above must
+# catch it.  The copy is built in a temp dir and loaded in place of the real oracle.
+MUTATIONS = [
+    ("conv fwd flips the filter", "const double *wr = w + (((i64)kh * KW + kw) * C + ci) * K;\n"
+     "                    for (int co = 0; co < K; ++co) out[co] += xv * wr[co];",
+     "const double *wr = w + (((i64)(KH - 1 - kh) * KW + (KW - 1 - kw)) * C + ci) * K;\n"
+     "                    for (int co = 0; co < K; ++co) out[co] += xv * wr[co];",
+     "check_conv_vs_torch"),
+    ("bwd_input ignores the stride phase", "if (th < 0 || th % sh != 0) continue;",
+     "if (th < 0) continue;", "check_adjoints"),
+    ("bwd_filter uses the wrong pad", "int iw = ow * sw + kw - pl;\n                    if (iw < 0 || iw >= W) continue;\n"
+     "                    const double xv = x[",
+     "int iw = ow * sw + kw - pt;\n                    if (iw < 0 || iw >= W) continue;\n"
+     "                    const double xv = x[", "check_adjoints"),
+    ("maxpool keeps the last maximum", "if (!have || v > best) {", "if (!have || v >= best) {",
+     "check_pool_bruteforce"),
+    ("relu bwd passes the gradient at zero", "dpre[p * C + c] = y[p * C + c] > 0.0 ? dy[p * C + c] : 0.0;",
+     "dpre[p * C + c] = y[p * C + c] >= 0.0 ? dy[p * C + c] : 0.0;", "check_bias_relu"),
+    ("sgd adds the gradient", "var[i] = var[i] - lr * grad[i];", "var[i] = var[i] + lr * grad[i];",
+     "check_sgd_decrease"),
+    ("bias grad drops the last pixel", "for (i64 p = 0; p < P; ++p) s += dpre[p * C + c];",
+     "for (i64 p = 0; p + 1 < P; ++p) s += dpre[p * C + c];", "check_bias_relu"),
+    ("pool bwd drops beta", "if (!beta) memset(dx, 0, sizeof(double) * (size_t)nx);",
+     "memset(dx, 0, sizeof(double) * (size_t)nx);", "check_pool_bwd_beta"),
+]
+
+
+@pytest.mark.parametrize("label,old,new,check", MUTATIONS, ids=[m[0] for m in MUTATIONS])
+def test_pins_catch_planted_mistakes(label, old, new, check):
+    src = open(os.path.join(os.path.dirname(oracle.__file__), "oracle.c")).read()
+    assert src.count(old) == 1, label
+    tmp = tempfile.mkdtemp(prefix="orc_mut_")
+    try:
+        path = os.path.join(tmp, "oracle.c")
+        with open(path, "w") as f:
+            f.write(src.replace(old, new))
+        so = os.path.join(tmp, "libmut.so")
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c99",
+                               "-o", so, path, "-lm"])
+        real = oracle._lib
+        oracle.use_library(so)
+        try:
+            err = getattr(pins, check)()
+        finally:
+            oracle._lib = real
+        assert err > 1e-3, (label, err)
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
