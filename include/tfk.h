@@ -1,0 +1,220 @@
+/*
+ * tfk.h -- C ABI of the MI355X (gfx950) convnet training-step library.
+ *
+ * The library implements the dataflow operations of one synchronous SGD step
+ * of a convolutional network replica (the paper's single-replica hot path,
+ * Sections 4.1, 4.4 and 6.1): Conv2D forward, Conv2DBackpropInput,
+ * Conv2DBackpropFilter, fused bias+ReLU forward/backward, MaxPool
+ * forward/backward with argmax, and in-place ApplyGradientDescent.  The paper
+ * separates client languages from the core by a thin C API (Section 5); this
+ * header is that boundary for these operations.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensors are dense device arrays (hipMalloc'd or equivalent).  Activations
+ *    are NHWC row-major: element (n,h,w,c) lives at
+ *      base[((n*H + h)*W + w) * pixel_stride + c].
+ *    pixel_stride == 0 means "dense" (= c).  pixel_stride > c describes a
+ *    channel slice of a wider buffer (concat without copies).
+ *  - Filters are HWIO row-major: w[kh][kw][ci][co], always dense.
+ *  - Element types: TFK_F32 (float) or TFK_BF16 (bfloat16 stored as uint16,
+ *    round-to-nearest-even on store).  Accumulation is always fp32.  Filter
+ *    gradients, bias, bias gradients and variables are always fp32.
+ *  - Convolution is cross-correlation (no filter flip) with explicit stride and
+ *    padding (top, bottom, left, right).  Output extent along an axis:
+ *      OH = floor((H + pad_top + pad_bottom - KH) / stride_h) + 1.
+ *    The library never infers SAME/VALID padding; callers pass the pads.
+ *  - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *    stream) and returns its status synchronously.  Arguments are validated
+ *    before anything is launched: on a non-OK status nothing was enqueued and
+ *    no buffer was touched.  tfk_last_error() then holds a message.
+ *  - Ownership: the caller owns every buffer.  The library allocates no
+ *    device memory and keeps no pointer after the call returns; buffers must
+ *    stay valid until the stream has passed the operation.  Operations that
+ *    need scratch memory take a caller-provided workspace sized by the
+ *    matching *_workspace_bytes query.
+ *  - Aliasing: outputs must not overlap inputs except where an argument is
+ *    documented as in-place.  A detected overlap returns TFK_ERR_ALIAS.
+ *  - An empty batch (n == 0) is valid: nothing is read; reductions over the
+ *    batch (filter and bias gradients) are written as zeros.  Pointers of
+ *    empty tensors may be NULL.
+ *  - Results are deterministic: no floating-point atomics; every reduction has
+ *    a fixed order for a given shape.
+ */
+#ifndef TFK_H_
+#define TFK_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TFK_ABI_VERSION 1
+
+#if defined(__GNUC__)
+#define TFK_API __attribute__((visibility("default")))
+#else
+#define TFK_API
+#endif
+
+typedef enum {
+    TFK_OK = 0,
+    TFK_ERR_NULL = 1,       /* a required pointer is NULL                          */
+    TFK_ERR_SHAPE = 2,      /* non-positive extent, mismatched shapes, bad window  */
+    TFK_ERR_DTYPE = 3,      /* unknown element type                                */
+    TFK_ERR_ALIGN = 4,      /* pointer not aligned to its element size             */
+    TFK_ERR_OVERFLOW = 5,   /* an index would not fit its integer type             */
+    TFK_ERR_ALIAS = 6,      /* an output overlaps an input it may not overlap      */
+    TFK_ERR_WORKSPACE = 7,  /* workspace missing or smaller than the query says    */
+    TFK_ERR_HIP = 8,        /* the HIP runtime reported an error at launch         */
+    TFK_ERR_ARG = 9         /* any other invalid argument (beta, lr, count, ...)   */
+} tfk_status;
+
+typedef enum { TFK_F32 = 0, TFK_BF16 = 1 } tfk_dtype;
+
+/* An NHWC tensor view: extents and the distance between consecutive pixels,
+ * in elements (0 = c, i.e. dense). */
+typedef struct {
+    int32_t n, h, w, c;
+    int64_t pixel_stride;
+} tfk_nhwc;
+
+/* A sliding window: extent, stride and explicit padding. */
+typedef struct {
+    int32_t kh, kw;
+    int32_t stride_h, stride_w;
+    int32_t pad_top, pad_bottom, pad_left, pad_right;
+} tfk_window;
+
+/* ---------------------------------------------------------------- convolution
+ * Conv2D forward (the mini-batch 2-D convolution of Section 3.1):
+ *   y[n,oh,ow,co] = sum_{kh,kw,ci} X[n, oh*sh+kh-pt, ow*sw+kw-pl, ci] * w[kh,kw,ci,co]
+ * with X = 0 outside the image.
+ *   x   : xd-shaped input, element type dt.
+ *   w   : dense HWIO filter [kh][kw][xd.c][cout], element type dt.
+ *   y   : yd-shaped output, element type dt, overwritten.  yd.n == xd.n,
+ *         yd.h/yd.w must equal the output extents, yd.c == cout.
+ *   ws  : workspace of at least tfk_conv2d_workspace_bytes(0, ...) bytes
+ *         (may be NULL when that is 0).
+ * Requirements: pad < kernel extent on every side.
+ */
+TFK_API tfk_status tfk_conv2d_fwd(const void *x, tfk_nhwc xd, const void *w, int32_t cout,
+                          tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
+                          void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Conv2DBackpropInput: the gradient of the forward map with respect to x
+ * (Section 4.1 backpropagation through the convolution):
+ *   dx[n,h,w,ci] = sum over (kh,kw,co) and the (oh,ow) with
+ *                  oh*sh+kh-pt == h, ow*sw+kw-pl == w of dy[n,oh,ow,co]*w[kh,kw,ci,co].
+ * Input positions reached by no window receive 0.
+ *   dy  : dyd-shaped upstream gradient (the forward output's shape), type dt.
+ *   w   : dense HWIO filter [kh][kw][dxd.c][dyd.c], type dt.
+ *   dx  : dxd-shaped gradient (the forward input's shape: with stride > 1 it
+ *         cannot be recovered from dy, so the caller states it), type dt.
+ *   beta: 0 overwrites dx; 1 adds to it (summing the partial gradients of
+ *         several paths, Section 4.1).  With beta == 1, dx is read and written.
+ */
+TFK_API tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void *w, tfk_window p,
+                                tfk_dtype dt, void *dx, tfk_nhwc dxd, float beta,
+                                void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Conv2DBackpropFilter: the gradient with respect to the filter:
+ *   dw[kh,kw,ci,co] = sum_{n,oh,ow} X[n, oh*sh+kh-pt, ow*sw+kw-pl, ci] * dy[n,oh,ow,co]
+ *   x   : xd-shaped forward input, type dt.
+ *   dy  : dyd-shaped upstream gradient, type dt.
+ *   dw  : dense fp32 HWIO [p.kh][p.kw][xd.c][dyd.c], overwritten.
+ *   ws  : at least tfk_conv2d_workspace_bytes(2, ...) bytes (split-K partial sums,
+ *         reduced in a fixed order).
+ */
+TFK_API tfk_status tfk_conv2d_bwd_filter(const void *x, tfk_nhwc xd, const void *dy, tfk_nhwc dyd,
+                                 tfk_window p, tfk_dtype dt, float *dw,
+                                 void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace needed by a convolution: op 0 = forward, 1 = backprop-input,
+ * 2 = backprop-filter; xd is the forward input, cout the filter's output
+ * channels.  Returns 0 for invalid arguments (the operation itself then
+ * reports the error). */
+TFK_API size_t tfk_conv2d_workspace_bytes(int32_t op, tfk_nhwc xd, int32_t cout, tfk_window p,
+                                  tfk_dtype dt);
+
+/* ---------------------------------------------------------------- bias + ReLU
+ * Fused BiasAdd + ReLU forward, in place (the hand-fused ReLU kernels of
+ * Section 5):  y[p,c] <- max(y[p,c] + bias[c], +0).
+ *   y    : yd-shaped, type dt, read and written.
+ *   bias : fp32 [yd.c].
+ */
+TFK_API tfk_status tfk_bias_relu_fwd(void *y, tfk_nhwc yd, const float *bias, tfk_dtype dt,
+                             void *stream);
+
+/*
+ * ReLU backward fused with the bias gradient:
+ *   dpre[p,c] = (y[p,c] > 0) ? dy[p,c] : 0        (mask from the stored y)
+ *   dbias[c]  = sum over all pixels p of dpre[p,c]  (fp32, fixed order)
+ *   y, dy, dpre : share the view yd (same extents and pixel stride), type dt.
+ *                 dpre may equal dy (in place); any other overlap is an error.
+ *   dbias       : fp32 [yd.c], overwritten.
+ *   ws          : at least tfk_bias_relu_bwd_workspace_bytes(yd, dt) bytes.
+ * Requirements: yd.c <= 16384.
+ */
+TFK_API tfk_status tfk_bias_relu_bwd(const void *y, const void *dy, tfk_nhwc yd, void *dpre,
+                             float *dbias, tfk_dtype dt, void *ws, size_t ws_bytes,
+                             void *stream);
+
+TFK_API size_t tfk_bias_relu_bwd_workspace_bytes(tfk_nhwc yd, tfk_dtype dt);
+
+/* ---------------------------------------------------------------- max-pool
+ * MaxPool forward with argmax.  Each window scans kh (outer) and kw (inner),
+ * skipping padded taps; the first maximum in that order wins (a later tap
+ * replaces the running maximum only if strictly greater).
+ *   x      : xd-shaped input, type dt.
+ *   y      : yd-shaped output, type dt, overwritten.
+ *   argmax : dense int32 [yd.n][yd.h][yd.w][yd.c]: the flat dense NHWC index
+ *            ((n*H + h)*W + w)*C + c into x of the selected tap.
+ * Requirements: every window holds at least one in-bounds tap (pad < kernel
+ * extent); xd.n*xd.h*xd.w*xd.c <= INT32_MAX (else TFK_ERR_OVERFLOW).
+ */
+TFK_API tfk_status tfk_maxpool_fwd(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype dt,
+                           void *y, tfk_nhwc yd, int32_t *argmax, void *stream);
+
+/*
+ * MaxPool backward: dx[i] = beta*dx[i] + sum over outputs o with argmax[o] == i of dy[o]
+ * (overlapping windows may route several outputs to one input; all are summed).
+ *   dy, argmax : yd-shaped (argmax dense), from tfk_maxpool_fwd.
+ *   dx         : xd-shaped, type dt; beta 0 overwrites, 1 accumulates.
+ */
+TFK_API tfk_status tfk_maxpool_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p,
+                           tfk_dtype dt, void *dx, tfk_nhwc xd, float beta, void *stream);
+
+/* ---------------------------------------------------------------- update
+ * ApplyGradientDescent, in place (Section 4.1: W' = W - alpha * dL/dW written
+ * with "-=" into the variable's buffer; Section 3.1 variables are mutable
+ * buffers updated in place):
+ *   var[i] <- fma(-lr, grad[i], var[i])      for 0 <= i < n   (fp32)
+ *   var_bf16, if not NULL, receives the bf16 (RNE) copy of the updated var,
+ *   used as the next step's low-precision weights.
+ * var must not overlap grad or var_bf16.
+ */
+TFK_API tfk_status tfk_apply_sgd(float *var, const float *grad, int64_t n, float lr,
+                         uint16_t *var_bf16, void *stream);
+
+/* The same update over `count` independent (var, grad, n, shadow) tuples in one
+ * launch per batch of tensors.  shadows may be NULL (no shadows) or hold NULL
+ * entries.  The pointer arrays are host memory and are read during the call. */
+TFK_API tfk_status tfk_apply_sgd_multi(int32_t count, float *const *vars, const float *const *grads,
+                               const int64_t *ns, float lr, uint16_t *const *shadows,
+                               void *stream);
+
+/* ---------------------------------------------------------------- misc */
+TFK_API const char *tfk_status_string(tfk_status s);
+/* Detail of the last non-OK status returned on the calling thread ("" if none). */
+TFK_API const char *tfk_last_error(void);
+TFK_API int32_t tfk_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TFK_H_ */

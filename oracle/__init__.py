@@ -13,8 +13,10 @@ Parity status of each function (pins are in tests/test_oracle_pins.py):
 * conv2d_fwd        pinned: library conv (torch float64 CPU), 1x1 conv = matmul,
                     delta / shifted-delta kernels, all-ones closed form.
 * conv2d_bwd_input  pinned: finite differences, adjoint identity, delta kernel.
+* conv2d_bwd_input  also pinned against torch autograd (float64 CPU).
 * conv2d_bwd_filter pinned: finite differences, adjoint identity, full-window
-                    VALID conv = outer-product matmul.
+                    VALID conv = outer-product matmul, torch autograd.
+* conv2d_bwd_filter_at  pinned: torch autograd at the selected entries.
 * bias_relu_fwd/bwd pinned: finite differences off the kink, numpy column sums.
 * maxpool_fwd       pinned: reshape-max for non-overlapping windows, brute-force
                     numpy argmax (first maximum) for any window, planted ties.
@@ -73,6 +75,8 @@ def _declare(lib):
                                          _dp, _i, _i, _i, _i]
     lib.orc_conv2d_bwd_filter.argtypes = [_dp, _i, _i, _i, _i, _dp, _i, _i, _i,
                                           _i, _i, _i, _i, _i, _i, _dp]
+    lib.orc_conv2d_bwd_filter_at.argtypes = [_dp, _i, _i, _i, _i, _dp, _i, _i, _i, _i, _i, _i, _i, _i, _i,
+                                             ctypes.POINTER(ctypes.c_int64), _l, _dp]
     lib.orc_bias_relu_fwd.argtypes = [_dp, _dp, _l, _i, _dp]
     lib.orc_bias_relu_bwd.argtypes = [_dp, _dp, _l, _i, _dp, _dp]
     lib.orc_maxpool_fwd.argtypes = [_dp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _dp, _ip, _i, _i]
@@ -160,6 +164,25 @@ def conv2d_bwd_filter(x, dy, kernel_hw, stride, pads):
     lib.orc_conv2d_bwd_filter(_ptr(x), N, H, W, C, _ptr(dy), OH, OW, K, KH, KW, sh, sw, pt, pl,
                               _ptr(dw))
     return dw
+
+
+def conv2d_bwd_filter_at(x, dy, kernel_hw, stride, pads, flat_idx):
+    """Selected entries dW.flat[flat_idx] of conv2d_bwd_filter (HWIO flat indices)."""
+    lib = _load()
+    x, dy = _f64(x), _f64(dy)
+    N, H, W, C = x.shape
+    N2, OH, OW, K = dy.shape
+    assert N2 == N
+    KH, KW = kernel_hw
+    sh, sw = (stride, stride) if np.isscalar(stride) else stride
+    pt, pb, pl, pr = pads
+    assert OH == out_len(H, KH, sh, pt, pb) and OW == out_len(W, KW, sw, pl, pr)
+    idx = np.ascontiguousarray(flat_idx, dtype=np.int64)
+    assert idx.min() >= 0 and idx.max() < KH * KW * C * K
+    out = np.empty(idx.size)
+    lib.orc_conv2d_bwd_filter_at(_ptr(x), N, H, W, C, _ptr(dy), OH, OW, K, KH, KW, sh, sw, pt, pl,
+                                 idx.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), idx.size, _ptr(out))
+    return out
 
 
 def bias_relu_fwd(pre, b):

@@ -164,6 +164,38 @@ void orc_conv2d_bwd_filter(const double *x, int N, int H, int W, int C,
 }
 
 /*
+ * Selected elements of Conv2DBackpropFilter (same definition and sum order as
+ * above): out[i] = dw[idx[i]] for flat HWIO indices idx[i].  Lets a check
+ * evaluate a handful of filter-gradient entries of a full-size problem.
+ */
+void orc_conv2d_bwd_filter_at(const double *x, int N, int H, int W, int C,
+                              const double *dy, int OH, int OW, int K,
+                              int KH, int KW, int sh, int sw, int pt, int pl,
+                              const int64_t *idx, i64 count, double *out) {
+#pragma omp parallel for schedule(dynamic, 1)
+    for (i64 i = 0; i < count; ++i) {
+        i64 f = idx[i];
+        int co = (int)(f % K);
+        int ci = (int)((f / K) % C);
+        int kw = (int)((f / ((i64)K * C)) % KW);
+        int kh = (int)(f / ((i64)K * C * KW));
+        double s = 0.0;
+        for (int n = 0; n < N; ++n)
+            for (int oh = 0; oh < OH; ++oh) {
+                int ih = oh * sh + kh - pt;
+                if (ih < 0 || ih >= H) continue;
+                for (int ow = 0; ow < OW; ++ow) {
+                    int iw = ow * sw + kw - pl;
+                    if (iw < 0 || iw >= W) continue;
+                    s += x[(((i64)n * H + ih) * W + iw) * C + ci] *
+                         dy[(((i64)n * OH + oh) * OW + ow) * K + co];
+                }
+            }
+        out[i] = s;
+    }
+}
+
+/*
  * Fused BiasAdd + ReLU forward over P pixels of C channels:
  *   y = pre + b[c];  y = (y > 0) ? y : +0.0
  * (the paper's hand-fused ReLU kernels, Section 5).  y may equal pre.

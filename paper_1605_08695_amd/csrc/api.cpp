@@ -1,0 +1,427 @@
+// C ABI of the gfx950 convnet training-step library (declared in include/tfk.h).
+//
+// Every entry point validates its arguments completely before anything is
+// enqueued; on failure it returns a status, records a message for
+// tfk_last_error() and leaves every buffer untouched.  Validation is plain
+// host code: it makes no HIP call.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+
+#include "../../include/tfk.h"
+#include "kernels.h"
+
+using namespace tfk;
+
+namespace {
+
+thread_local std::string g_err;
+
+tfk_status fail(tfk_status s, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+tfk_status ok() {
+    g_err.clear();
+    return TFK_OK;
+}
+
+tfk_status hip_status(hipError_t e, const char *what) {
+    if (e == hipSuccess) return ok();
+    return fail(TFK_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool valid_dt(tfk_dtype dt) { return dt == TFK_F32 || dt == TFK_BF16; }
+int64_t esize(tfk_dtype dt) { return dt == TFK_F32 ? 4 : 2; }
+
+// Checks extents, resolves pixel_stride == 0 to c.
+tfk_status check_view(const char *name, tfk_nhwc &d) {
+    if (d.n < 0 || d.h <= 0 || d.w <= 0 || d.c <= 0)
+        return fail(TFK_ERR_SHAPE, "%s: extents must be n >= 0 and h, w, c >= 1 (got %d,%d,%d,%d)", name, d.n,
+                    d.h, d.w, d.c);
+    if (d.pixel_stride == 0) d.pixel_stride = d.c;
+    if (d.pixel_stride < d.c)
+        return fail(TFK_ERR_SHAPE, "%s: pixel_stride %lld < c %d", name, (long long)d.pixel_stride, d.c);
+    const int64_t pix = (int64_t)d.n * d.h * d.w;
+    if (pix > INT32_MAX) return fail(TFK_ERR_OVERFLOW, "%s: n*h*w = %lld exceeds 2^31-1", name, (long long)pix);
+    if (d.pixel_stride > ((int64_t)1 << 40))
+        return fail(TFK_ERR_OVERFLOW, "%s: pixel_stride too large", name);
+    return TFK_OK;
+}
+
+int64_t view_bytes(const tfk_nhwc &d, int64_t es) {
+    const int64_t pix = (int64_t)d.n * d.h * d.w;
+    if (pix == 0) return 0;
+    return ((pix - 1) * d.pixel_stride + d.c) * es;
+}
+
+tfk_status check_window(const tfk_window &p) {
+    if (p.kh < 1 || p.kw < 1) return fail(TFK_ERR_SHAPE, "window: kh, kw must be >= 1");
+    if (p.stride_h < 1 || p.stride_w < 1 || p.stride_h > 255 || p.stride_w > 255)
+        return fail(TFK_ERR_SHAPE, "window: strides must be in [1, 255]");
+    if (p.pad_top < 0 || p.pad_bottom < 0 || p.pad_left < 0 || p.pad_right < 0)
+        return fail(TFK_ERR_SHAPE, "window: pads must be >= 0");
+    if (p.pad_top >= p.kh || p.pad_bottom >= p.kh || p.pad_left >= p.kw || p.pad_right >= p.kw)
+        return fail(TFK_ERR_SHAPE, "window: every pad must be smaller than the kernel extent");
+    return TFK_OK;
+}
+
+// Output extent along one axis, or 0 when no window fits.
+int out_len(int n, int k, int s, int p0, int p1) {
+    const int64_t span = (int64_t)n + p0 + p1 - k;
+    if (span < 0) return 0;
+    return (int)(span / s + 1);
+}
+
+bool overlap(const void *a, int64_t abytes, const void *b, int64_t bbytes) {
+    if (!a || !b || abytes <= 0 || bbytes <= 0) return false;
+    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + (uintptr_t)bbytes && b0 < a0 + (uintptr_t)abytes;
+}
+
+bool aligned(const void *p, int64_t a) { return ((uintptr_t)p % (uintptr_t)a) == 0; }
+
+tfk_status need_ptr(const void *p, const char *name) {
+    if (!p) return fail(TFK_ERR_NULL, "%s is NULL", name);
+    return TFK_OK;
+}
+
+tfk_status need_align(const void *p, int64_t a, const char *name) {
+    if (p && !aligned(p, a)) return fail(TFK_ERR_ALIGN, "%s is not %lld-byte aligned", name, (long long)a);
+    return TFK_OK;
+}
+
+#define TRY(expr)                         \
+    do {                                  \
+        tfk_status _s = (expr);           \
+        if (_s != TFK_OK) return _s;      \
+    } while (0)
+
+// Shared validation of a convolution: input view xd, filter (KH,KW,C,cout), output view yd.
+tfk_status check_conv(tfk_nhwc &xd, int32_t cout, const tfk_window &p, tfk_dtype dt, tfk_nhwc &yd,
+                      const char *xname, const char *yname, ConvShape &s) {
+    if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
+    TRY(check_view(xname, xd));
+    TRY(check_view(yname, yd));
+    TRY(check_window(p));
+    if (cout < 1) return fail(TFK_ERR_SHAPE, "cout must be >= 1");
+    const int oh = out_len(xd.h, p.kh, p.stride_h, p.pad_top, p.pad_bottom);
+    const int ow = out_len(xd.w, p.kw, p.stride_w, p.pad_left, p.pad_right);
+    if (oh < 1 || ow < 1) return fail(TFK_ERR_SHAPE, "window does not fit the padded input");
+    if (yd.n != xd.n || yd.h != oh || yd.w != ow || yd.c != cout)
+        return fail(TFK_ERR_SHAPE, "%s must be [%d,%d,%d,%d], got [%d,%d,%d,%d]", yname, xd.n, oh, ow, cout, yd.n,
+                    yd.h, yd.w, yd.c);
+    const int64_t kred = (int64_t)p.kh * p.kw * xd.c;
+    if (kred > INT32_MAX / 2 || (int64_t)kred * cout > INT32_MAX)
+        return fail(TFK_ERR_OVERFLOW, "filter too large");
+    s.N = xd.n; s.H = xd.h; s.W = xd.w; s.C = xd.c;
+    s.OH = oh; s.OW = ow; s.K = cout;
+    s.KH = p.kh; s.KW = p.kw; s.sh = p.stride_h; s.sw = p.stride_w; s.pt = p.pad_top; s.pl = p.pad_left;
+    return TFK_OK;
+}
+
+int64_t filter_bytes(const ConvShape &s, int64_t es) { return (int64_t)s.KH * s.KW * s.C * s.K * es; }
+
+tfk_status check_ws(void *ws, size_t ws_bytes, size_t need) {
+    if (need == 0) return TFK_OK;
+    if (!ws) return fail(TFK_ERR_WORKSPACE, "workspace of %zu bytes required, got NULL", need);
+    if (ws_bytes < need) return fail(TFK_ERR_WORKSPACE, "workspace of %zu bytes required, got %zu", need, ws_bytes);
+    if (!aligned(ws, 16)) return fail(TFK_ERR_ALIGN, "workspace must be 16-byte aligned");
+    return TFK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t tfk_abi_version(void) { return TFK_ABI_VERSION; }
+
+const char *tfk_last_error(void) { return g_err.c_str(); }
+
+const char *tfk_status_string(tfk_status s) {
+    switch (s) {
+        case TFK_OK: return "ok";
+        case TFK_ERR_NULL: return "null pointer";
+        case TFK_ERR_SHAPE: return "invalid shape";
+        case TFK_ERR_DTYPE: return "invalid dtype";
+        case TFK_ERR_ALIGN: return "misaligned pointer";
+        case TFK_ERR_OVERFLOW: return "index overflow";
+        case TFK_ERR_ALIAS: return "illegal aliasing";
+        case TFK_ERR_WORKSPACE: return "workspace too small";
+        case TFK_ERR_HIP: return "HIP runtime error";
+        case TFK_ERR_ARG: return "invalid argument";
+    }
+    return "unknown status";
+}
+
+// ------------------------------------------------------------------ convolution
+size_t tfk_conv2d_workspace_bytes(int32_t op, tfk_nhwc xd, int32_t cout, tfk_window p, tfk_dtype dt) {
+    if (op != 2) return 0;
+    if (!valid_dt(dt) || check_view("x", xd) != TFK_OK || check_window(p) != TFK_OK || cout < 1) return 0;
+    const int oh = out_len(xd.h, p.kh, p.stride_h, p.pad_top, p.pad_bottom);
+    const int ow = out_len(xd.w, p.kw, p.stride_w, p.pad_left, p.pad_right);
+    if (oh < 1 || ow < 1 || xd.n == 0) return 0;
+    ConvShape s{xd.n, xd.h, xd.w, xd.c, oh, ow, cout, p.kh, p.kw, p.stride_h, p.stride_w, p.pad_top, p.pad_left};
+    return conv_bwd_filter_ws_bytes(dt == TFK_F32 ? 0 : 1, s);
+}
+
+tfk_status tfk_conv2d_fwd(const void *x, tfk_nhwc xd, const void *w, int32_t cout, tfk_window p, tfk_dtype dt,
+                          void *y, tfk_nhwc yd, void *ws, size_t ws_bytes, void *stream) {
+    (void)ws;
+    (void)ws_bytes;
+    ConvShape s;
+    TRY(check_conv(xd, cout, p, dt, yd, "x", "y", s));
+    if (xd.n == 0) return ok();
+    const int64_t es = esize(dt);
+    TRY(need_ptr(x, "x"));
+    TRY(need_ptr(w, "w"));
+    TRY(need_ptr(y, "y"));
+    TRY(need_align(x, es, "x"));
+    TRY(need_align(w, es, "w"));
+    TRY(need_align(y, es, "y"));
+    const int64_t yb = view_bytes(yd, es);
+    if (overlap(y, yb, x, view_bytes(xd, es)) || overlap(y, yb, w, filter_bytes(s, es)))
+        return fail(TFK_ERR_ALIAS, "y overlaps x or w");
+    return hip_status(launch_conv_fwd(dt == TFK_F32 ? 0 : 1, x, xd.pixel_stride, w, y, yd.pixel_stride, s,
+                                      (hipStream_t)stream),
+                      "conv2d_fwd");
+}
+
+tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void *w, tfk_window p, tfk_dtype dt, void *dx,
+                                tfk_nhwc dxd, float beta, void *ws, size_t ws_bytes, void *stream) {
+    (void)ws;
+    (void)ws_bytes;
+    ConvShape s;
+    TRY(check_conv(dxd, dyd.c, p, dt, dyd, "dx", "dy", s));
+    if (!(beta == 0.f || beta == 1.f)) return fail(TFK_ERR_ARG, "beta must be 0 or 1");
+    if (dxd.n == 0) return ok();
+    const int64_t es = esize(dt);
+    TRY(need_ptr(dy, "dy"));
+    TRY(need_ptr(w, "w"));
+    TRY(need_ptr(dx, "dx"));
+    TRY(need_align(dy, es, "dy"));
+    TRY(need_align(w, es, "w"));
+    TRY(need_align(dx, es, "dx"));
+    const int64_t xb = view_bytes(dxd, es);
+    if (overlap(dx, xb, dy, view_bytes(dyd, es)) || overlap(dx, xb, w, filter_bytes(s, es)))
+        return fail(TFK_ERR_ALIAS, "dx overlaps dy or w");
+    return hip_status(launch_conv_bwd_data(dt == TFK_F32 ? 0 : 1, dy, dyd.pixel_stride, w, dx, dxd.pixel_stride,
+                                           beta, s, (hipStream_t)stream),
+                      "conv2d_bwd_input");
+}
+
+tfk_status tfk_conv2d_bwd_filter(const void *x, tfk_nhwc xd, const void *dy, tfk_nhwc dyd, tfk_window p,
+                                 tfk_dtype dt, float *dw, void *ws, size_t ws_bytes, void *stream) {
+    ConvShape s;
+    TRY(check_conv(xd, dyd.c, p, dt, dyd, "x", "dy", s));
+    TRY(need_ptr(dw, "dw"));
+    TRY(need_align(dw, 4, "dw"));
+    const int64_t wb = filter_bytes(s, 4);
+    hipStream_t st = (hipStream_t)stream;
+    if (xd.n == 0) return hip_status(launch_fill_zero(dw, wb / 4, st), "conv2d_bwd_filter");
+    const int64_t es = esize(dt);
+    TRY(need_ptr(x, "x"));
+    TRY(need_ptr(dy, "dy"));
+    TRY(need_align(x, es, "x"));
+    TRY(need_align(dy, es, "dy"));
+    const int dti = dt == TFK_F32 ? 0 : 1;
+    const size_t need = conv_bwd_filter_ws_bytes(dti, s);
+    TRY(check_ws(ws, ws_bytes, need));
+    const int64_t xb = view_bytes(xd, es), yb = view_bytes(dyd, es);
+    if (overlap(dw, wb, x, xb) || overlap(dw, wb, dy, yb))
+        return fail(TFK_ERR_ALIAS, "dw overlaps x or dy");
+    if (need && (overlap(ws, (int64_t)need, x, xb) || overlap(ws, (int64_t)need, dy, yb) ||
+                 overlap(ws, (int64_t)need, dw, wb)))
+        return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
+    return hip_status(launch_conv_bwd_filter(dti, x, xd.pixel_stride, dy, dyd.pixel_stride, dw, s, ws, st),
+                      "conv2d_bwd_filter");
+}
+
+// ------------------------------------------------------------------ bias + ReLU
+tfk_status tfk_bias_relu_fwd(void *y, tfk_nhwc yd, const float *bias, tfk_dtype dt, void *stream) {
+    if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
+    TRY(check_view("y", yd));
+    if (yd.n == 0) return ok();
+    const int64_t es = esize(dt);
+    TRY(need_ptr(y, "y"));
+    TRY(need_ptr(bias, "bias"));
+    TRY(need_align(y, es, "y"));
+    TRY(need_align(bias, 4, "bias"));
+    if (overlap(y, view_bytes(yd, es), bias, (int64_t)yd.c * 4)) return fail(TFK_ERR_ALIAS, "bias overlaps y");
+    const int64_t P = (int64_t)yd.n * yd.h * yd.w;
+    return hip_status(launch_bias_relu_fwd(dt == TFK_F32 ? 0 : 1, y, P, yd.c, yd.pixel_stride, bias,
+                                           (hipStream_t)stream),
+                      "bias_relu_fwd");
+}
+
+size_t tfk_bias_relu_bwd_workspace_bytes(tfk_nhwc yd, tfk_dtype dt) {
+    if (!valid_dt(dt) || check_view("y", yd) != TFK_OK || yd.n == 0) return 0;
+    int G;
+    int64_t ppb;
+    relu_bwd_plan(dt == TFK_F32 ? 0 : 1, (int64_t)yd.n * yd.h * yd.w, yd.c, yd.pixel_stride, &G, &ppb);
+    return (size_t)G * yd.c * sizeof(float);
+}
+
+tfk_status tfk_bias_relu_bwd(const void *y, const void *dy, tfk_nhwc yd, void *dpre, float *dbias, tfk_dtype dt,
+                             void *ws, size_t ws_bytes, void *stream) {
+    if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
+    TRY(check_view("y", yd));
+    TRY(need_ptr(dbias, "dbias"));
+    TRY(need_align(dbias, 4, "dbias"));
+    hipStream_t st = (hipStream_t)stream;
+    const int64_t es = esize(dt);
+    const int64_t vb = view_bytes(yd, es);
+    const int64_t bb = (int64_t)yd.c * 4;
+    if (yd.c > 16384) return fail(TFK_ERR_SHAPE, "bias_relu_bwd supports at most 16384 channels");
+    if (yd.n == 0) return hip_status(launch_fill_zero(dbias, yd.c, st), "bias_relu_bwd");
+    TRY(need_ptr(y, "y"));
+    TRY(need_ptr(dy, "dy"));
+    TRY(need_ptr(dpre, "dpre"));
+    TRY(need_align(y, es, "y"));
+    TRY(need_align(dy, es, "dy"));
+    TRY(need_align(dpre, es, "dpre"));
+    if (dpre != dy && overlap(dpre, vb, dy, vb)) return fail(TFK_ERR_ALIAS, "dpre partially overlaps dy");
+    if (overlap(dpre, vb, y, vb)) return fail(TFK_ERR_ALIAS, "dpre overlaps y");
+    if (overlap(dbias, bb, y, vb) || overlap(dbias, bb, dy, vb) || overlap(dbias, bb, dpre, vb))
+        return fail(TFK_ERR_ALIAS, "dbias overlaps a tensor");
+    const size_t need = tfk_bias_relu_bwd_workspace_bytes(yd, dt);
+    TRY(check_ws(ws, ws_bytes, need));
+    if (overlap(ws, (int64_t)need, y, vb) || overlap(ws, (int64_t)need, dy, vb) ||
+        overlap(ws, (int64_t)need, dpre, vb) || overlap(ws, (int64_t)need, dbias, bb))
+        return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
+    const int64_t P = (int64_t)yd.n * yd.h * yd.w;
+    return hip_status(launch_bias_relu_bwd(dt == TFK_F32 ? 0 : 1, y, dy, dpre, P, yd.c, yd.pixel_stride, dbias,
+                                           (float *)ws, st),
+                      "bias_relu_bwd");
+}
+
+// ------------------------------------------------------------------ max-pool
+static tfk_status check_pool(tfk_nhwc &xd, const tfk_window &p, tfk_dtype dt, tfk_nhwc &yd, const char *xname,
+                             const char *yname, PoolGeom &g) {
+    if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
+    TRY(check_view(xname, xd));
+    TRY(check_view(yname, yd));
+    TRY(check_window(p));
+    const int oh = out_len(xd.h, p.kh, p.stride_h, p.pad_top, p.pad_bottom);
+    const int ow = out_len(xd.w, p.kw, p.stride_w, p.pad_left, p.pad_right);
+    if (oh < 1 || ow < 1) return fail(TFK_ERR_SHAPE, "window does not fit the padded input");
+    if (yd.n != xd.n || yd.h != oh || yd.w != ow || yd.c != xd.c)
+        return fail(TFK_ERR_SHAPE, "%s must be [%d,%d,%d,%d], got [%d,%d,%d,%d]", yname, xd.n, oh, ow, xd.c, yd.n,
+                    yd.h, yd.w, yd.c);
+    if ((int64_t)xd.n * xd.h * xd.w * xd.c > INT32_MAX)
+        return fail(TFK_ERR_OVERFLOW, "%s has more than 2^31-1 elements: argmax would overflow int32", xname);
+    g.N = xd.n; g.H = xd.h; g.W = xd.w; g.C = xd.c;
+    g.OH = oh; g.OW = ow;
+    g.KH = p.kh; g.KW = p.kw; g.sh = p.stride_h; g.sw = p.stride_w; g.pt = p.pad_top; g.pl = p.pad_left;
+    g.xs = xd.pixel_stride;
+    g.ys = yd.pixel_stride;
+    return TFK_OK;
+}
+
+tfk_status tfk_maxpool_fwd(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
+                           int32_t *argmax, void *stream) {
+    PoolGeom g;
+    TRY(check_pool(xd, p, dt, yd, "x", "y", g));
+    if (xd.n == 0) return ok();
+    const int64_t es = esize(dt);
+    TRY(need_ptr(x, "x"));
+    TRY(need_ptr(y, "y"));
+    TRY(need_ptr(argmax, "argmax"));
+    TRY(need_align(x, es, "x"));
+    TRY(need_align(y, es, "y"));
+    TRY(need_align(argmax, 4, "argmax"));
+    const int64_t xb = view_bytes(xd, es), yb = view_bytes(yd, es);
+    const int64_t ab = (int64_t)yd.n * yd.h * yd.w * yd.c * 4;
+    if (overlap(y, yb, x, xb) || overlap(argmax, ab, x, xb) || overlap(argmax, ab, y, yb))
+        return fail(TFK_ERR_ALIAS, "y / argmax overlap");
+    return hip_status(launch_maxpool_fwd(dt == TFK_F32 ? 0 : 1, x, g, y, argmax, (hipStream_t)stream),
+                      "maxpool_fwd");
+}
+
+tfk_status tfk_maxpool_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
+                           void *dx, tfk_nhwc xd, float beta, void *stream) {
+    PoolGeom g;
+    TRY(check_pool(xd, p, dt, yd, "dx", "dy", g));
+    if (!(beta == 0.f || beta == 1.f)) return fail(TFK_ERR_ARG, "beta must be 0 or 1");
+    if (xd.n == 0) return ok();
+    const int64_t es = esize(dt);
+    TRY(need_ptr(dy, "dy"));
+    TRY(need_ptr(argmax, "argmax"));
+    TRY(need_ptr(dx, "dx"));
+    TRY(need_align(dy, es, "dy"));
+    TRY(need_align(dx, es, "dx"));
+    TRY(need_align(argmax, 4, "argmax"));
+    const int64_t xb = view_bytes(xd, es), yb = view_bytes(yd, es);
+    const int64_t ab = (int64_t)yd.n * yd.h * yd.w * yd.c * 4;
+    if (overlap(dx, xb, dy, yb) || overlap(dx, xb, argmax, ab)) return fail(TFK_ERR_ALIAS, "dx overlaps dy or argmax");
+    return hip_status(launch_maxpool_bwd(dt == TFK_F32 ? 0 : 1, dy, argmax, g, beta, dx, (hipStream_t)stream),
+                      "maxpool_bwd");
+}
+
+// ------------------------------------------------------------------ SGD
+static tfk_status check_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh) {
+    if (n < 0) return fail(TFK_ERR_SHAPE, "n must be >= 0");
+    if (!isfinite(lr)) return fail(TFK_ERR_ARG, "lr must be finite");
+    if (n == 0) return TFK_OK;
+    TRY(need_ptr(var, "var"));
+    TRY(need_ptr(grad, "grad"));
+    TRY(need_align(var, 4, "var"));
+    TRY(need_align(grad, 4, "grad"));
+    TRY(need_align(sh, 2, "var_bf16"));
+    if (n > ((int64_t)1 << 40)) return fail(TFK_ERR_OVERFLOW, "n too large");
+    if (overlap(var, n * 4, grad, n * 4) || overlap(var, n * 4, sh, n * 2) || overlap(grad, n * 4, sh, n * 2))
+        return fail(TFK_ERR_ALIAS, "var, grad and var_bf16 must not overlap");
+    return TFK_OK;
+}
+
+tfk_status tfk_apply_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *var_bf16, void *stream) {
+    TRY(check_sgd(var, grad, n, lr, var_bf16));
+    if (n == 0) return ok();
+    return hip_status(launch_sgd(var, grad, n, lr, var_bf16, (hipStream_t)stream), "apply_sgd");
+}
+
+tfk_status tfk_apply_sgd_multi(int32_t count, float *const *vars, const float *const *grads, const int64_t *ns,
+                               float lr, uint16_t *const *shadows, void *stream) {
+    if (count < 0) return fail(TFK_ERR_ARG, "count must be >= 0");
+    if (count == 0) return ok();
+    TRY(need_ptr(vars, "vars"));
+    TRY(need_ptr(grads, "grads"));
+    TRY(need_ptr(ns, "ns"));
+    for (int i = 0; i < count; ++i) {
+        tfk_status s = check_sgd(vars[i], grads[i], ns[i], lr, shadows ? shadows[i] : nullptr);
+        if (s != TFK_OK) return fail(s, "tensor %d: %s", i, g_err.c_str());
+    }
+    hipStream_t st = (hipStream_t)stream;
+    int i = 0;
+    while (i < count) {
+        SgdBatch b;
+        b.count = 0;
+        b.blk_start[0] = 0;
+        for (; i < count && b.count < kSgdBatch; ++i) {
+            if (ns[i] == 0) continue;
+            const int k = b.count++;
+            b.var[k] = vars[i];
+            b.grad[k] = grads[i];
+            b.shadow[k] = shadows ? shadows[i] : nullptr;
+            b.n[k] = ns[i];
+            b.blk_start[k + 1] = b.blk_start[k] + (ns[i] + 1023) / 1024;
+        }
+        if (b.count == 0) continue;
+        if (b.blk_start[b.count] > INT32_MAX) return fail(TFK_ERR_OVERFLOW, "too many elements in one batch");
+        hipError_t e = launch_sgd_multi(b, lr, st);
+        if (e != hipSuccess) return hip_status(e, "apply_sgd_multi");
+    }
+    return ok();
+}
+
+}  // extern "C"

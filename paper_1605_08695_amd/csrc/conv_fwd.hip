@@ -1,0 +1,28 @@
+// Conv2D forward on gfx950 MFMA: Out[p][co] = sum_k im2col(x)[p][k] * w[k][co].
+#include "igemm_launch.h"
+
+namespace tfk {
+
+template <typename T>
+static hipError_t conv_fwd_t(const void *x, int64_t xs, const void *w, void *y, int64_t ys, const ConvShape &s,
+                             hipStream_t st) {
+    constexpr int EPC = Elem<T>::kPerChunk;
+    IgArgs a;
+    fill_geom(a, s);
+    a.src_i = w;
+    a.src_j = x;
+    a.out = y;
+    a.xs = xs;
+    a.ys = ys;
+    a.NI = s.K;
+    const bool vi = s.K % EPC == 0 && aligned16p(w);
+    const bool vj = s.C % EPC == 0 && xs % EPC == 0 && aligned16p(x);
+    return igemm_launch<T, DIR_FWD>(a, s.N * s.OH * s.OW, 1, vi, vj, st);
+}
+
+hipError_t launch_conv_fwd(int dt, const void *x, int64_t xs, const void *w, void *y, int64_t ys,
+                           const ConvShape &s, hipStream_t st) {
+    return dt == 0 ? conv_fwd_t<float>(x, xs, w, y, ys, s, st) : conv_fwd_t<bf16_t>(x, xs, w, y, ys, s, st);
+}
+
+}  // namespace tfk

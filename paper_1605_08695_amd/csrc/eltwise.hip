@@ -1,0 +1,474 @@
+// Bandwidth-bound kernels of the training step on gfx950: fused bias+ReLU
+// forward/backward with the bias-gradient reduction, max-pool forward/backward
+// with argmax, the in-place SGD update, and the split-K sum of bwd-filter.
+//
+// Every kernel moves 16-byte chunks (8 bf16 or 4 fp32 channels) when the
+// channel count, pixel stride and base pointers allow it, and falls back to
+// one element per thread otherwise.  Reductions are two-pass with a fixed
+// order, so results do not depend on scheduling.
+#include "common.h"
+#include "kernels.h"
+
+namespace tfk {
+
+static inline int grid_for(int64_t work, int per_block = 256, int cap = 65536) {
+    int64_t g = (work + per_block - 1) / per_block;
+    if (g < 1) g = 1;
+    if (g > cap) g = cap;
+    return (int)g;
+}
+
+// ------------------------------------------------------------------ chunk helpers
+template <typename T>
+__device__ __forceinline__ void chunk_to_f32(const U4 &v, float *f) {
+    if constexpr (sizeof(T) == 4) {
+        f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
+        f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
+    } else {
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            f[2 * j] = __uint_as_float(w[j] << 16);
+            f[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+        }
+    }
+}
+
+template <typename T>
+__device__ __forceinline__ U4 f32_to_chunk(const float *f) {
+    U4 v;
+    if constexpr (sizeof(T) == 4) {
+        v.x = __float_as_uint(f[0]); v.y = __float_as_uint(f[1]);
+        v.z = __float_as_uint(f[2]); v.w = __float_as_uint(f[3]);
+    } else {
+        v.x = pack_bf16x2(f[0], f[1]); v.y = pack_bf16x2(f[2], f[3]);
+        v.z = pack_bf16x2(f[4], f[5]); v.w = pack_bf16x2(f[6], f[7]);
+    }
+    return v;
+}
+
+// ------------------------------------------------------------------ bias + ReLU forward
+template <typename T, bool VEC>
+__global__ __launch_bounds__(256) void bias_relu_fwd_kernel(T *__restrict__ y, int64_t P, int C,
+                                                            int64_t ys, const float *__restrict__ bias,
+                                                            FastDiv dCV) {
+    constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
+    const int CV = C / EPC;
+    const int64_t total = P * CV;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
+         t += (int64_t)gridDim.x * blockDim.x) {
+        int64_t p;
+        int cv;
+        if (total < (1ll << 31)) {
+            uint32_t q, r;
+            dCV.divmod((uint32_t)t, q, r);
+            p = q;
+            cv = (int)r;
+        } else {
+            p = t / CV;
+            cv = (int)(t - p * CV);
+        }
+        T *ptr = y + p * ys + (int64_t)cv * EPC;
+        if constexpr (VEC) {
+            float f[EPC];
+            chunk_to_f32<T>(*reinterpret_cast<const U4 *>(ptr), f);
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                const float v = f[e] + bias[cv * EPC + e];
+                f[e] = v > 0.f ? v : 0.f;
+            }
+            *reinterpret_cast<U4 *>(ptr) = f32_to_chunk<T>(f);
+        } else {
+            const float v = Elem<T>::load(ptr) + bias[cv];
+            Elem<T>::store(ptr, v > 0.f ? v : 0.f);
+        }
+    }
+}
+
+// ------------------------------------------------------------------ ReLU backward + bias gradient
+// Pass 1: block b owns pixels [b*ppb, min(P, (b+1)*ppb)).  Thread t owns channel
+// chunks cv = t % CVB (+ CVB, ...) and pixel rows t / CVB (+ R, ...).  It writes
+// dpre and keeps fp32 per-channel sums; the block then reduces its R row groups
+// in LDS in a fixed order and writes partial[b][c].
+template <typename T, bool VEC>
+__global__ __launch_bounds__(256) void relu_bwd_partial_kernel(const T *__restrict__ y, const T *dy,
+                                                               T *dpre, int64_t P, int C, int64_t ys,
+                                                               int64_t ppb, float *__restrict__ partial) {
+    constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
+    extern __shared__ float red[];                 // [R][C]
+    const int CV = C / EPC;
+    const int CVB = CV < 256 ? CV : 256;
+    const int R = 256 / CVB;
+    const int t = threadIdx.x;
+    const int lane_cv = t % CVB;
+    const int row = t / CVB;
+    const int64_t p0 = (int64_t)blockIdx.x * ppb;
+    const int64_t p1 = min(P, p0 + ppb);
+    const bool active = row < R;
+    for (int cv = lane_cv; cv < CV; cv += CVB) {
+        float s[EPC];
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) s[e] = 0.f;
+        if (active) {
+            for (int64_t p = p0 + row; p < p1; p += R) {
+                const int64_t off = p * ys + (int64_t)cv * EPC;
+                if constexpr (VEC) {
+                    float fy[EPC], fd[EPC];
+                    chunk_to_f32<T>(*reinterpret_cast<const U4 *>(y + off), fy);
+                    chunk_to_f32<T>(*reinterpret_cast<const U4 *>(dy + off), fd);
+#pragma unroll
+                    for (int e = 0; e < EPC; ++e) {
+                        fd[e] = fy[e] > 0.f ? fd[e] : 0.f;
+                        s[e] += fd[e];
+                    }
+                    *reinterpret_cast<U4 *>(dpre + off) = f32_to_chunk<T>(fd);
+                } else {
+                    const float fy = Elem<T>::load(y + off);
+                    const float fd = fy > 0.f ? Elem<T>::load(dy + off) : 0.f;
+                    s[0] += fd;
+                    Elem<T>::store(dpre + off, fd);
+                }
+            }
+            // The stored dpre equals the value summed here: with bf16 storage the
+            // masked dy is already a bf16 value, so rounding on store is exact.
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) red[row * C + cv * EPC + e] = s[e];
+        }
+    }
+    __syncthreads();
+    for (int c = t; c < C; c += 256) {
+        float acc = 0.f;
+        for (int r = 0; r < R; ++r) acc += red[r * C + c];
+        partial[(int64_t)blockIdx.x * C + c] = acc;
+    }
+}
+
+__global__ __launch_bounds__(256) void sum_partials_kernel(const float *__restrict__ partial, int G, int C,
+                                                           float *__restrict__ out) {
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= C) return;
+    float acc = 0.f;
+    for (int b = 0; b < G; ++b) acc += partial[(int64_t)b * C + c];
+    out[c] = acc;
+}
+
+// ------------------------------------------------------------------ max-pool forward
+template <typename T, bool VEC>
+__global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T *__restrict__ x, PoolGeom g,
+                                                          T *__restrict__ y, int32_t *__restrict__ argmax) {
+    constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
+    const int CV = g.C / EPC;
+    const int64_t total = (int64_t)g.N * g.OH * g.OW * CV;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
+         t += (int64_t)gridDim.x * blockDim.x) {
+        const int cv = (int)(t % CV);
+        const int64_t pix = t / CV;
+        const int ow = (int)(pix % g.OW);
+        const int oh = (int)((pix / g.OW) % g.OH);
+        const int n = (int)(pix / ((int64_t)g.OW * g.OH));
+        float best[EPC];
+        int32_t bi[EPC];
+        bool have = false;
+        for (int kh = 0; kh < g.KH; ++kh) {
+            const int ih = oh * g.sh + kh - g.pt;
+            if ((unsigned)ih >= (unsigned)g.H) continue;
+            for (int kw = 0; kw < g.KW; ++kw) {
+                const int iw = ow * g.sw + kw - g.pl;
+                if ((unsigned)iw >= (unsigned)g.W) continue;
+                const int64_t pidx = ((int64_t)n * g.H + ih) * g.W + iw;
+                const int32_t dense = (int32_t)(pidx * g.C + cv * EPC);
+                float v[EPC];
+                if constexpr (VEC) {
+                    chunk_to_f32<T>(*reinterpret_cast<const U4 *>(x + pidx * g.xs + cv * EPC), v);
+                } else {
+                    v[0] = Elem<T>::load(x + pidx * g.xs + cv);
+                }
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    if (!have || v[e] > best[e]) {
+                        best[e] = v[e];
+                        bi[e] = dense + e;
+                    }
+                }
+                have = true;
+            }
+        }
+        const int64_t opix = ((int64_t)n * g.OH + oh) * g.OW + ow;
+        if constexpr (VEC) {
+            *reinterpret_cast<U4 *>(y + opix * g.ys + cv * EPC) = f32_to_chunk<T>(best);
+            int32_t *am = argmax + opix * g.C + cv * EPC;
+#pragma unroll
+            for (int e = 0; e < EPC; e += 4) {
+                int4 q;
+                q.x = bi[e]; q.y = bi[e + 1]; q.z = bi[e + 2]; q.w = bi[e + 3];
+                *reinterpret_cast<int4 *>(am + e) = q;
+            }
+        } else {
+            Elem<T>::store(y + opix * g.ys + cv, best[0]);
+            argmax[opix * g.C + cv] = bi[0];
+        }
+    }
+}
+
+// ------------------------------------------------------------------ max-pool backward
+// Gather form: each input element visits the windows that contain it in
+// ascending output order and adds the gradients routed to it.
+template <typename T, bool VEC>
+__global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T *__restrict__ dy,
+                                                          const int32_t *__restrict__ argmax, PoolGeom g,
+                                                          float beta, T *dx) {
+    constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
+    const int CV = g.C / EPC;
+    const int64_t total = (int64_t)g.N * g.H * g.W * CV;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
+         t += (int64_t)gridDim.x * blockDim.x) {
+        const int cv = (int)(t % CV);
+        const int64_t pix = t / CV;
+        const int w = (int)(pix % g.W);
+        const int h = (int)((pix / g.W) % g.H);
+        const int n = (int)(pix / ((int64_t)g.W * g.H));
+        const int32_t self = (int32_t)(pix * g.C + cv * EPC);
+        // windows oh with oh*sh - pt <= h <= oh*sh - pt + KH - 1
+        const int hp = h + g.pt, wp = w + g.pl;
+        const int oh_lo = hp - g.KH + 1 <= 0 ? 0 : (hp - g.KH + 1 + g.sh - 1) / g.sh;
+        const int oh_hi = min(g.OH - 1, hp / g.sh);
+        const int ow_lo = wp - g.KW + 1 <= 0 ? 0 : (wp - g.KW + 1 + g.sw - 1) / g.sw;
+        const int ow_hi = min(g.OW - 1, wp / g.sw);
+        float s[EPC];
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) s[e] = 0.f;
+        for (int oh = oh_lo; oh <= oh_hi; ++oh) {
+            for (int ow = ow_lo; ow <= ow_hi; ++ow) {
+                const int64_t opix = ((int64_t)n * g.OH + oh) * g.OW + ow;
+                if constexpr (VEC) {
+                    const int32_t *am = argmax + opix * g.C + cv * EPC;
+                    int32_t ai[EPC];
+#pragma unroll
+                    for (int e = 0; e < EPC; e += 4) {
+                        const int4 q = *reinterpret_cast<const int4 *>(am + e);
+                        ai[e] = q.x; ai[e + 1] = q.y; ai[e + 2] = q.z; ai[e + 3] = q.w;
+                    }
+                    bool any = false;
+#pragma unroll
+                    for (int e = 0; e < EPC; ++e) any |= (ai[e] == self + e);
+                    if (any) {
+                        float v[EPC];
+                        chunk_to_f32<T>(*reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC), v);
+#pragma unroll
+                        for (int e = 0; e < EPC; ++e)
+                            if (ai[e] == self + e) s[e] += v[e];
+                    }
+                } else {
+                    if (argmax[opix * g.C + cv] == self) s[0] += Elem<T>::load(dy + opix * g.ys + cv);
+                }
+            }
+        }
+        T *out = dx + pix * g.xs + cv * EPC;
+        if constexpr (VEC) {
+            if (beta != 0.f) {
+                float o[EPC];
+                chunk_to_f32<T>(*reinterpret_cast<const U4 *>(out), o);
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) s[e] += beta * o[e];
+            }
+            *reinterpret_cast<U4 *>(out) = f32_to_chunk<T>(s);
+        } else {
+            if (beta != 0.f) s[0] += beta * Elem<T>::load(out);
+            Elem<T>::store(out, s[0]);
+        }
+    }
+}
+
+// ------------------------------------------------------------------ SGD
+__device__ __forceinline__ void sgd_one(float *var, const float *grad, uint16_t *sh, int64_t i, float lr) {
+    const float v = fmaf(-lr, grad[i], var[i]);
+    var[i] = v;
+    if (sh) sh[i] = (uint16_t)f32_to_bf16(v);
+}
+
+__global__ __launch_bounds__(256) void sgd_kernel(float *__restrict__ var, const float *__restrict__ grad,
+                                                  int64_t n, float lr, uint16_t *__restrict__ sh, bool vec) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (vec) {
+        const int64_t n4 = n / 4;
+        for (int64_t t = t0; t < n4; t += stride) {
+            float4 v = reinterpret_cast<const float4 *>(var)[t];
+            const float4 g = reinterpret_cast<const float4 *>(grad)[t];
+            v.x = fmaf(-lr, g.x, v.x); v.y = fmaf(-lr, g.y, v.y);
+            v.z = fmaf(-lr, g.z, v.z); v.w = fmaf(-lr, g.w, v.w);
+            reinterpret_cast<float4 *>(var)[t] = v;
+            if (sh) {
+                uint2 b;
+                b.x = pack_bf16x2(v.x, v.y);
+                b.y = pack_bf16x2(v.z, v.w);
+                reinterpret_cast<uint2 *>(sh)[t] = b;
+            }
+        }
+        for (int64_t i = n4 * 4 + t0; i < n; i += stride) sgd_one(var, grad, sh, i, lr);
+    } else {
+        for (int64_t i = t0; i < n; i += stride) sgd_one(var, grad, sh, i, lr);
+    }
+}
+
+__global__ __launch_bounds__(256) void sgd_multi_kernel(SgdBatch b, float lr) {
+    int k = 0;
+    while (k + 1 < b.count && (int64_t)blockIdx.x >= b.blk_start[k + 1]) ++k;
+    const int64_t first = ((int64_t)blockIdx.x - b.blk_start[k]) * 256 * 4;
+    float *var = b.var[k];
+    const float *grad = b.grad[k];
+    uint16_t *sh = b.shadow[k];
+    const int64_t n = b.n[k];
+    for (int r = 0; r < 4; ++r) {
+        const int64_t i = first + r * 256 + threadIdx.x;
+        if (i < n) sgd_one(var, grad, sh, i, lr);
+    }
+}
+
+// ------------------------------------------------------------------ split-K sum / zero fill
+__global__ __launch_bounds__(256) void sum_splits_kernel(const float *__restrict__ part, int splits,
+                                                         int64_t mn, float *__restrict__ out) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < mn; i += stride) {
+        float acc = 0.f;
+        for (int s = 0; s < splits; ++s) acc += part[(int64_t)s * mn + i];
+        out[i] = acc;
+    }
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(float *__restrict__ out, int64_t n) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) out[i] = 0.f;
+}
+
+// ------------------------------------------------------------------ host launchers
+static bool aligned16(const void *p) { return ((uintptr_t)p & 15) == 0; }
+
+template <typename T>
+static hipError_t bias_relu_fwd_t(void *y, int64_t P, int C, int64_t ys, const float *bias, hipStream_t st) {
+    constexpr int EPC = Elem<T>::kPerChunk;
+    const bool vec = C % EPC == 0 && ys % EPC == 0 && aligned16(y);
+    const int CV = vec ? C / EPC : C;
+    const int g = grid_for(P * CV, 256, 8192);
+    FastDiv d((uint32_t)CV);
+    if (vec)
+        hipLaunchKernelGGL((bias_relu_fwd_kernel<T, true>), dim3(g), dim3(256), 0, st, (T *)y, P, C, ys, bias, d);
+    else
+        hipLaunchKernelGGL((bias_relu_fwd_kernel<T, false>), dim3(g), dim3(256), 0, st, (T *)y, P, C, ys, bias, d);
+    return hipGetLastError();
+}
+
+hipError_t launch_bias_relu_fwd(int dt, void *y, int64_t P, int C, int64_t ys, const float *bias, hipStream_t st) {
+    return dt == 0 ? bias_relu_fwd_t<float>(y, P, C, ys, bias, st)
+                   : bias_relu_fwd_t<bf16_t>(y, P, C, ys, bias, st);
+}
+
+// Partial-sum grid of the bias-gradient reduction (shared with the workspace query).
+void relu_bwd_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *ppb) {
+    const int EPC = dt == 0 ? 4 : 8;
+    const bool vec = C % EPC == 0 && ys % EPC == 0;
+    const int CV = vec ? C / EPC : C;
+    const int CVB = CV < 256 ? CV : 256;
+    const int R = 256 / CVB;
+    int64_t g = (P + (int64_t)R * 8 - 1) / ((int64_t)R * 8);    // >= 8 pixel rows per thread
+    const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(1024, (1 << 21) / std::max(C, 1)));
+    if (g > cap) g = cap;
+    if (g < 1) g = 1;
+    *G = (int)g;
+    *ppb = (P + g - 1) / g;
+}
+
+template <typename T>
+static hipError_t relu_bwd_t(const void *y, const void *dy, void *dpre, int64_t P, int C, int64_t ys,
+                             float *db, float *ws, hipStream_t st) {
+    constexpr int EPC = Elem<T>::kPerChunk;
+    const bool vec = C % EPC == 0 && ys % EPC == 0 && aligned16(y) && aligned16(dy) && aligned16(dpre);
+    int G;
+    int64_t ppb;
+    relu_bwd_plan(sizeof(T) == 4 ? 0 : 1, P, C, ys, &G, &ppb);
+    const int CV = vec ? C / EPC : C;
+    const int CVB = CV < 256 ? CV : 256;
+    const int R = 256 / CVB;
+    const size_t smem = (size_t)R * C * sizeof(float);
+    if (vec)
+        hipLaunchKernelGGL((relu_bwd_partial_kernel<T, true>), dim3(G), dim3(256), smem, st,
+                           (const T *)y, (const T *)dy, (T *)dpre, P, C, ys, ppb, ws);
+    else
+        hipLaunchKernelGGL((relu_bwd_partial_kernel<T, false>), dim3(G), dim3(256), smem, st,
+                           (const T *)y, (const T *)dy, (T *)dpre, P, C, ys, ppb, ws);
+    hipLaunchKernelGGL(sum_partials_kernel, dim3((C + 255) / 256), dim3(256), 0, st, ws, G, C, db);
+    return hipGetLastError();
+}
+
+hipError_t launch_bias_relu_bwd(int dt, const void *y, const void *dy, void *dpre, int64_t P, int C,
+                                int64_t ys, float *db, float *ws, hipStream_t st) {
+    return dt == 0 ? relu_bwd_t<float>(y, dy, dpre, P, C, ys, db, ws, st)
+                   : relu_bwd_t<bf16_t>(y, dy, dpre, P, C, ys, db, ws, st);
+}
+
+template <typename T>
+static hipError_t maxpool_fwd_t(const void *x, const PoolGeom &g, void *y, int32_t *am, hipStream_t st) {
+    constexpr int EPC = Elem<T>::kPerChunk;
+    const bool vec = g.C % EPC == 0 && g.xs % EPC == 0 && g.ys % EPC == 0 && aligned16(x) &&
+                     aligned16(y) && aligned16(am);
+    const int64_t work = (int64_t)g.N * g.OH * g.OW * (vec ? g.C / EPC : g.C);
+    const int grid = grid_for(work, 256, 16384);
+    if (vec)
+        hipLaunchKernelGGL((maxpool_fwd_kernel<T, true>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am);
+    else
+        hipLaunchKernelGGL((maxpool_fwd_kernel<T, false>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am);
+    return hipGetLastError();
+}
+
+hipError_t launch_maxpool_fwd(int dt, const void *x, const PoolGeom &g, void *y, int32_t *am, hipStream_t st) {
+    return dt == 0 ? maxpool_fwd_t<float>(x, g, y, am, st) : maxpool_fwd_t<bf16_t>(x, g, y, am, st);
+}
+
+template <typename T>
+static hipError_t maxpool_bwd_t(const void *dy, const int32_t *am, const PoolGeom &g, float beta, void *dx,
+                                hipStream_t st) {
+    constexpr int EPC = Elem<T>::kPerChunk;
+    const bool vec = g.C % EPC == 0 && g.xs % EPC == 0 && g.ys % EPC == 0 && aligned16(dx) &&
+                     aligned16(dy) && aligned16(am);
+    const int64_t work = (int64_t)g.N * g.H * g.W * (vec ? g.C / EPC : g.C);
+    const int grid = grid_for(work, 256, 16384);
+    if (vec)
+        hipLaunchKernelGGL((maxpool_bwd_kernel<T, true>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g, beta, (T *)dx);
+    else
+        hipLaunchKernelGGL((maxpool_bwd_kernel<T, false>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g, beta, (T *)dx);
+    return hipGetLastError();
+}
+
+hipError_t launch_maxpool_bwd(int dt, const void *dy, const int32_t *am, const PoolGeom &g, float beta, void *dx,
+                              hipStream_t st) {
+    return dt == 0 ? maxpool_bwd_t<float>(dy, am, g, beta, dx, st) : maxpool_bwd_t<bf16_t>(dy, am, g, beta, dx, st);
+}
+
+hipError_t launch_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh, hipStream_t st) {
+    const bool vec = aligned16(var) && aligned16(grad) && (sh == nullptr || ((uintptr_t)sh & 7) == 0);
+    const int grid = grid_for(vec ? (n + 3) / 4 : n, 256, 8192);
+    hipLaunchKernelGGL(sgd_kernel, dim3(grid), dim3(256), 0, st, var, grad, n, lr, sh, vec);
+    return hipGetLastError();
+}
+
+hipError_t launch_sgd_multi(const SgdBatch &b, float lr, hipStream_t st) {
+    const int64_t blocks = b.blk_start[b.count];
+    if (blocks <= 0) return hipSuccess;
+    hipLaunchKernelGGL(sgd_multi_kernel, dim3((unsigned)blocks), dim3(256), 0, st, b, lr);
+    return hipGetLastError();
+}
+
+hipError_t launch_sum_splits(const float *part, int splits, int64_t mn, float *out, hipStream_t st) {
+    const int grid = grid_for(mn, 256, 8192);
+    hipLaunchKernelGGL(sum_splits_kernel, dim3(grid), dim3(256), 0, st, part, splits, mn, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(float *out, int64_t n, hipStream_t st) {
+    if (n <= 0) return hipSuccess;
+    const int grid = grid_for(n, 256, 8192);
+    hipLaunchKernelGGL(fill_zero_kernel, dim3(grid), dim3(256), 0, st, out, n);
+    return hipGetLastError();
+}
+
+}  // namespace tfk

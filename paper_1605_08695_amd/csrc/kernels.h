@@ -1,0 +1,58 @@
+// Internal interface between the C ABI (api.cpp) and the gfx950 kernels.
+// Everything here is validated by the caller before it is reached.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+namespace tfk {
+
+// Geometry of one forward convolution (input N,H,W,C; output OH,OW,K).
+struct ConvShape {
+    int N, H, W, C;
+    int OH, OW, K;
+    int KH, KW, sh, sw, pt, pl;
+};
+
+struct PoolGeom {
+    int N, H, W, C;      // input
+    int OH, OW;          // output
+    int KH, KW, sh, sw, pt, pl;
+    int64_t xs, ys;      // pixel strides of x (dx) and y (dy)
+};
+
+constexpr int kSgdBatch = 16;
+struct SgdBatch {
+    int count;
+    float *var[kSgdBatch];
+    const float *grad[kSgdBatch];
+    uint16_t *shadow[kSgdBatch];
+    int64_t n[kSgdBatch];
+    int64_t blk_start[kSgdBatch + 1];   // prefix sums of ceil(n / 1024)
+};
+
+// dt: 0 = fp32, 1 = bf16
+hipError_t launch_conv_fwd(int dt, const void *x, int64_t xs, const void *w, void *y, int64_t ys,
+                           const ConvShape &s, hipStream_t st);
+hipError_t launch_conv_bwd_data(int dt, const void *dy, int64_t dys, const void *w, void *dx, int64_t dxs,
+                                float beta, const ConvShape &s, hipStream_t st);
+hipError_t launch_conv_bwd_filter(int dt, const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,
+                                  const ConvShape &s, void *ws, hipStream_t st);
+// Split-K plan of bwd-filter: number of splits and reduction elements per split.
+void conv_bwd_filter_plan(int dt, const ConvShape &s, int *splits, int *k_split);
+size_t conv_bwd_filter_ws_bytes(int dt, const ConvShape &s);
+
+hipError_t launch_bias_relu_fwd(int dt, void *y, int64_t P, int C, int64_t ys, const float *bias, hipStream_t st);
+void relu_bwd_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *ppb);
+hipError_t launch_bias_relu_bwd(int dt, const void *y, const void *dy, void *dpre, int64_t P, int C,
+                                int64_t ys, float *db, float *ws, hipStream_t st);
+hipError_t launch_maxpool_fwd(int dt, const void *x, const PoolGeom &g, void *y, int32_t *am, hipStream_t st);
+hipError_t launch_maxpool_bwd(int dt, const void *dy, const int32_t *am, const PoolGeom &g, float beta, void *dx,
+                              hipStream_t st);
+hipError_t launch_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh, hipStream_t st);
+hipError_t launch_sgd_multi(const SgdBatch &b, float lr, hipStream_t st);
+hipError_t launch_sum_splits(const float *part, int splits, int64_t mn, float *out, hipStream_t st);
+hipError_t launch_fill_zero(float *out, int64_t n, hipStream_t st);
+
+}  // namespace tfk

@@ -1,0 +1,205 @@
+"""Python binding of the tfk_* C ABI over torch device tensors.
+
+Argument marshalling only: every step runs in the HIP kernels of libtfk.so.
+Tensors are NHWC torch tensors on the GPU; a 4-D tensor may be a channel
+slice of a wider NHWC buffer (its pixel stride is passed to the library).
+Filters are dense HWIO.  Every call is enqueued on ``stream`` (default: torch's
+current stream) and raises TfkError on a non-OK status.  There is no CPU path.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional, Sequence, Tuple
+
+import torch
+
+from ._lib import Nhwc, TfkError, Window, TFK_BF16, TFK_F32, check, load
+
+__all__ = ["conv2d_fwd", "conv2d_bwd_input", "conv2d_bwd_filter", "conv2d_workspace_bytes", "bias_relu_fwd",
+           "bias_relu_bwd", "bias_relu_bwd_workspace_bytes", "maxpool_fwd", "maxpool_bwd", "apply_sgd",
+           "apply_sgd_multi", "out_len", "nhwc", "window", "TfkError", "abi_version"]
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return TFK_F32
+    if t.dtype == torch.bfloat16:
+        return TFK_BF16
+    raise TypeError("tfk supports float32 and bfloat16 tensors, got %s" % t.dtype)
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> ctypes.c_void_p:
+    return ctypes.c_void_p(t.data_ptr() if t is not None else 0)
+
+
+def nhwc(t: torch.Tensor) -> Nhwc:
+    """Describes a 4-D NHWC tensor (or a channel slice of one) for the library."""
+    if t.dim() != 4:
+        raise ValueError("expected a 4-D NHWC tensor, got shape %s" % (tuple(t.shape),))
+    n, h, w, c = t.shape
+    s0, s1, s2, s3 = t.stride()
+    if n * h * w > 0:
+        ps = s2 if w > 1 else (s1 if h > 1 else (s0 if n > 1 else c))
+        if s3 != 1 or (w > 1 and s2 != ps) or (h > 1 and s1 != w * ps) or (n > 1 and s0 != h * w * ps):
+            raise ValueError("tensor is not an NHWC view with unit channel stride: strides %s" % (t.stride(),))
+    else:
+        ps = c
+    return Nhwc(n, h, w, c, ps)
+
+
+def window(kh, kw, stride, pads) -> Window:
+    sh, sw = (stride, stride) if isinstance(stride, int) else stride
+    pt, pb, pl, pr = pads
+    return Window(kh, kw, sh, sw, pt, pb, pl, pr)
+
+
+def out_len(n, k, s, p0, p1) -> int:
+    return (n + p0 + p1 - k) // s + 1
+
+
+def abi_version() -> int:
+    return load().tfk_abi_version()
+
+
+def _ws(nbytes: int, device) -> Optional[torch.Tensor]:
+    if nbytes == 0:
+        return None
+    return torch.empty((nbytes + 15) // 16 * 16, dtype=torch.uint8, device=device)
+
+
+# ----------------------------------------------------------------------------- convolution
+def conv2d_workspace_bytes(op: int, x: torch.Tensor, cout: int, kh, kw, stride, pads) -> int:
+    return load().tfk_conv2d_workspace_bytes(op, nhwc(x), cout, window(kh, kw, stride, pads), _dt(x))
+
+
+def conv2d_fwd(x, w, stride, pads, y=None, stream=None):
+    """y = x (*) w (cross-correlation).  x NHWC, w HWIO, pads (top, bottom, left, right)."""
+    lib = load()
+    kh, kw, cin, cout = w.shape
+    win = window(kh, kw, stride, pads)
+    if y is None:
+        n, h, ww, _ = x.shape
+        y = torch.empty((n, out_len(h, kh, win.stride_h, pads[0], pads[1]),
+                         out_len(ww, kw, win.stride_w, pads[2], pads[3]), cout), dtype=x.dtype, device=x.device)
+    if w.dtype != x.dtype or y.dtype != x.dtype:
+        raise TypeError("x, w and y must share one dtype")
+    check(lib.tfk_conv2d_fwd(_ptr(x), nhwc(x), _ptr(w), cout, win, _dt(x), _ptr(y), nhwc(y), None, 0,
+                             _stream(stream)))
+    return y
+
+
+def conv2d_bwd_input(dy, w, dx, stride, pads, beta=0.0, stream=None):
+    """dx (= or +=) conv2d_fwd^T(dy).  dx gives the forward input's shape (it is written)."""
+    lib = load()
+    kh, kw, cin, cout = w.shape
+    if not (w.dtype == dy.dtype == dx.dtype):
+        raise TypeError("dy, w and dx must share one dtype")
+    check(lib.tfk_conv2d_bwd_input(_ptr(dy), nhwc(dy), _ptr(w), window(kh, kw, stride, pads), _dt(dy), _ptr(dx),
+                                   nhwc(dx), float(beta), None, 0, _stream(stream)))
+    return dx
+
+
+def conv2d_bwd_filter(x, dy, kernel_hw, stride, pads, dw=None, ws=None, stream=None):
+    """dW (fp32 HWIO) = sum over pixels of x-gather * dy."""
+    lib = load()
+    kh, kw = kernel_hw
+    cout = dy.shape[3]
+    if dw is None:
+        dw = torch.empty((kh, kw, x.shape[3], cout), dtype=torch.float32, device=x.device)
+    if dy.dtype != x.dtype or dw.dtype != torch.float32:
+        raise TypeError("x and dy share one dtype; dw is float32")
+    win = window(kh, kw, stride, pads)
+    need = lib.tfk_conv2d_workspace_bytes(2, nhwc(x), cout, win, _dt(x))
+    if ws is None or ws.numel() < need:
+        ws = _ws(need, x.device)
+    check(lib.tfk_conv2d_bwd_filter(_ptr(x), nhwc(x), _ptr(dy), nhwc(dy), win, _dt(x), _ptr(dw), _ptr(ws),
+                                    need, _stream(stream)))
+    return dw
+
+
+# ----------------------------------------------------------------------------- bias + relu
+def bias_relu_fwd(y, bias, stream=None):
+    """In place: y <- max(y + bias, 0)."""
+    check(load().tfk_bias_relu_fwd(_ptr(y), nhwc(y), _ptr(bias), _dt(y), _stream(stream)))
+    return y
+
+
+def bias_relu_bwd_workspace_bytes(y) -> int:
+    return load().tfk_bias_relu_bwd_workspace_bytes(nhwc(y), _dt(y))
+
+
+def bias_relu_bwd(y, dy, dpre=None, dbias=None, ws=None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """dpre = dy * (y > 0) (dpre may be dy), dbias = column sums of dpre (fp32)."""
+    lib = load()
+    if dpre is None:
+        dpre = torch.empty_like(dy)
+    if dbias is None:
+        dbias = torch.empty(y.shape[3], dtype=torch.float32, device=y.device)
+    need = lib.tfk_bias_relu_bwd_workspace_bytes(nhwc(y), _dt(y))
+    if ws is None or ws.numel() < need:
+        ws = _ws(need, y.device)
+    d_y, d_dy, d_dp = nhwc(y), nhwc(dy), nhwc(dpre)
+    if (d_y.pixel_stride, d_y.c) != (d_dy.pixel_stride, d_dy.c) or (d_y.pixel_stride, d_y.c) != (d_dp.pixel_stride, d_dp.c):
+        raise ValueError("y, dy and dpre must share one view (extents and pixel stride)")
+    check(lib.tfk_bias_relu_bwd(_ptr(y), _ptr(dy), d_y, _ptr(dpre), _ptr(dbias), _dt(y), _ptr(ws), need,
+                                _stream(stream)))
+    return dpre, dbias
+
+
+# ----------------------------------------------------------------------------- max-pool
+def maxpool_fwd(x, kernel_hw, stride, pads, y=None, argmax=None, stream=None):
+    lib = load()
+    kh, kw = kernel_hw
+    win = window(kh, kw, stride, pads)
+    n, h, w, c = x.shape
+    oh = out_len(h, kh, win.stride_h, pads[0], pads[1])
+    ow = out_len(w, kw, win.stride_w, pads[2], pads[3])
+    if y is None:
+        y = torch.empty((n, oh, ow, c), dtype=x.dtype, device=x.device)
+    if argmax is None:
+        argmax = torch.empty((n, oh, ow, c), dtype=torch.int32, device=x.device)
+    check(lib.tfk_maxpool_fwd(_ptr(x), nhwc(x), win, _dt(x), _ptr(y), nhwc(y), _ptr(argmax), _stream(stream)))
+    return y, argmax
+
+
+def maxpool_bwd(dy, argmax, dx, kernel_hw, stride, pads, beta=0.0, stream=None):
+    kh, kw = kernel_hw
+    if not argmax.is_contiguous() or argmax.dtype != torch.int32:
+        raise ValueError("argmax must be a dense int32 tensor")
+    check(load().tfk_maxpool_bwd(_ptr(dy), _ptr(argmax), nhwc(dy), window(kh, kw, stride, pads), _dt(dy),
+                                 _ptr(dx), nhwc(dx), float(beta), _stream(stream)))
+    return dx
+
+
+# ----------------------------------------------------------------------------- update
+def apply_sgd(var, grad, lr, shadow=None, stream=None):
+    """In place: var <- fma(-lr, grad, var); shadow (bf16) <- bf16(var) if given."""
+    if var.dtype != torch.float32 or grad.dtype != torch.float32:
+        raise TypeError("var and grad are float32")
+    if not (var.is_contiguous() and grad.is_contiguous()) or var.numel() != grad.numel():
+        raise ValueError("var and grad must be contiguous with the same size")
+    if shadow is not None and (shadow.dtype != torch.bfloat16 or shadow.numel() != var.numel()
+                               or not shadow.is_contiguous()):
+        raise ValueError("shadow must be a contiguous bfloat16 tensor of var's size")
+    check(load().tfk_apply_sgd(_ptr(var), _ptr(grad), var.numel(), float(lr), _ptr(shadow), _stream(stream)))
+    return var
+
+
+def apply_sgd_multi(vars_: Sequence[torch.Tensor], grads: Sequence[torch.Tensor], lr,
+                    shadows: Optional[Sequence[Optional[torch.Tensor]]] = None, stream=None):
+    count = len(vars_)
+    VP = ctypes.c_void_p * max(count, 1)
+    NS = ctypes.c_int64 * max(count, 1)
+    v = VP(*[t.data_ptr() for t in vars_])
+    g = VP(*[t.data_ptr() for t in grads])
+    ns = NS(*[t.numel() for t in vars_])
+    sh = None
+    if shadows is not None:
+        sh = VP(*[(t.data_ptr() if t is not None else 0) for t in shadows])
+    check(load().tfk_apply_sgd_multi(count, v, g, ns, float(lr), sh, _stream(stream)))

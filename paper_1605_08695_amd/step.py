@@ -1,0 +1,191 @@
+"""One worker replica's synchronous SGD step, driven through the tfk_* ops.
+
+The schedule follows the paper's single-replica semantics (Sections 4.1 and
+4.4): a forward pass over every op; the upstream gradient ``g`` of the output
+tensor seeds a backward pass that visits the ops in reverse order and sums the
+partial gradients of every path into a tensor (``beta = 1`` for every
+contribution after the first); no gradient is formed for the step input
+unless the workload asks for it; then every variable is updated in place with
+W' = W - lr * dW, all from gradients computed with the same pre-update
+parameters.
+
+Memory layout (all on one GPU):
+
+* Variables: one flat fp32 buffer holding every filter (HWIO) and bias, each
+  at a 256-byte aligned offset, and a flat fp32 gradient buffer with the same
+  layout, so the whole update is one ApplyGradientDescent launch.  For bf16
+  workloads a flat bf16 shadow of the variables (written by that same launch)
+  holds the filters the convolutions read.
+* Activations: one NHWC buffer per tensor in the workload's storage type.
+  Inception concat buffers are written by their branches as channel slices
+  and read back the same way, so no concat or split is ever copied.
+* Gradients: one NHWC buffer per tensor (ReLU-backward writes its result over
+  the incoming gradient, except for the seed ``g`` which stays intact).
+"""
+from __future__ import annotations
+
+from typing import Dict, Optional
+
+import numpy as np
+import torch
+
+from . import ops
+from .workloads import Conv, Inputs, Net, Pool
+
+_ALIGN = 64   # elements: 256 bytes of fp32
+
+
+def _align(n: int) -> int:
+    return (n + _ALIGN - 1) // _ALIGN * _ALIGN
+
+
+class Replica:
+    """Device state of one replica of ``net`` and its training step."""
+
+    def __init__(self, net: Net, inputs: Inputs, device: str = "cuda"):
+        self.net = net
+        self.device = torch.device(device)
+        self.dtype = torch.float32 if net.dtype == "f32" else torch.bfloat16
+        self.lr = float(np.float32(net.lr))
+        dev, dt = self.device, self.dtype
+
+        # ---- variables
+        off = 0
+        self._layout = {}
+        for c in net.convs:
+            cin = net.tensors[c.src][3]
+            wn = c.kh * c.kw * cin * c.cout
+            self._layout[c.name] = (off, (c.kh, c.kw, cin, c.cout), off + _align(wn), c.cout)
+            off += _align(wn) + _align(c.cout)
+        self.n_params = off
+        self.params = torch.zeros(off, dtype=torch.float32, device=dev)
+        self.grads = torch.zeros(off, dtype=torch.float32, device=dev)
+        self.shadow = torch.zeros(off, dtype=torch.bfloat16, device=dev) if dt == torch.bfloat16 else None
+        host = np.zeros(off, dtype=np.float32)
+        for c in net.convs:
+            wo, wshape, bo, bn = self._layout[c.name]
+            host[wo:wo + int(np.prod(wshape))] = inputs.weights[c.name].astype(np.float32).ravel()
+            host[bo:bo + bn] = inputs.biases[c.name].astype(np.float32)
+        p = torch.from_numpy(host)
+        if dt == torch.bfloat16:
+            p = p.to(torch.bfloat16).to(torch.float32)      # master weights start at the bf16 values
+        self.params.copy_(p.to(dev))
+        if self.shadow is not None:
+            self.shadow.copy_(self.params.to(torch.bfloat16))
+        self.W, self.b, self.dW, self.db, self.Wlp = {}, {}, {}, {}, {}
+        for c in net.convs:
+            wo, wshape, bo, bn = self._layout[c.name]
+            wn = int(np.prod(wshape))
+            self.W[c.name] = self.params[wo:wo + wn].view(wshape)
+            self.dW[c.name] = self.grads[wo:wo + wn].view(wshape)
+            self.b[c.name] = self.params[bo:bo + bn]
+            self.db[c.name] = self.grads[bo:bo + bn]
+            self.Wlp[c.name] = (self.shadow[wo:wo + wn].view(wshape) if self.shadow is not None
+                                else self.W[c.name])
+
+        # ---- activations, gradients, argmax
+        self.act: Dict[str, torch.Tensor] = {}
+        for name, shape in net.tensors.items():
+            if name == "x":
+                self.act["x"] = torch.from_numpy(inputs.x).to(dt).to(dev)
+            else:
+                self.act[name] = torch.zeros(shape, dtype=dt, device=dev)
+        self.g = torch.from_numpy(inputs.g).to(dt).to(dev)
+        self.grad: Dict[str, torch.Tensor] = {net.output: self.g}
+        for name, shape in net.tensors.items():
+            if name == net.output or (name == "x" and not net.input_grad):
+                continue
+            self.grad[name] = torch.zeros(shape, dtype=dt, device=dev)
+        # ReLU-backward of the ops that write the output tensor must not overwrite the seed g
+        self.dpre_out = torch.zeros(net.tensors[net.output], dtype=dt, device=dev)
+        self.argmax = {op.name: torch.zeros(net.tensors[op.dst][:3] + (net.tensors[op.src][3],),
+                                            dtype=torch.int32, device=dev)
+                       for op in net.ops if isinstance(op, Pool)}
+        # ---- one workspace big enough for every op
+        need = 0
+        for c in net.convs:
+            x = self.act[c.src]
+            need = max(need, ops.conv2d_workspace_bytes(2, x, c.cout, c.kh, c.kw, (c.sh, c.sw), c.pads))
+            need = max(need, ops.bias_relu_bwd_workspace_bytes(self._slice(self.act, c)))
+        self.ws = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=dev)
+
+    # ------------------------------------------------------------------ helpers
+    def _width(self, op) -> int:
+        return op.cout if isinstance(op, Conv) else self.net.tensors[op.src][3]
+
+    def _slice(self, bufs, op):
+        t = bufs[op.dst]
+        return t[..., op.dst_c0:op.dst_c0 + self._width(op)]
+
+    # ------------------------------------------------------------------ the step
+    def forward(self, trace=None, stream=None):
+        for op in self.net.ops:
+            x = self.act[op.src]
+            y = self._slice(self.act, op)
+            if isinstance(op, Conv):
+                if trace: trace("conv_fwd", op, x=x, w=self.Wlp[op.name], y=y)
+                ops.conv2d_fwd(x, self.Wlp[op.name], (op.sh, op.sw), op.pads, y=y, stream=stream)
+                if trace: trace("conv_fwd:end", op, y=y)
+                if trace: trace("bias_relu_fwd", op, y=y, b=self.b[op.name])
+                ops.bias_relu_fwd(y, self.b[op.name], stream=stream)
+                if trace: trace("bias_relu_fwd:end", op, y=y)
+            else:
+                if trace: trace("maxpool_fwd", op, x=x, y=y, argmax=self.argmax[op.name])
+                ops.maxpool_fwd(x, (op.kh, op.kw), (op.sh, op.sw), op.pads, y=y, argmax=self.argmax[op.name],
+                                stream=stream)
+                if trace: trace("maxpool_fwd:end", op, y=y, argmax=self.argmax[op.name])
+
+    def backward(self, trace=None, stream=None):
+        net = self.net
+        written = set()
+        for op in reversed(net.ops):
+            dy = self._slice(self.grad, op)
+            src_grad = op.src != "x" or net.input_grad
+            beta = 1.0 if op.src in written else 0.0
+            if isinstance(op, Conv):
+                y = self._slice(self.act, op)
+                dpre = self._slice({op.dst: self.dpre_out}, op) if op.dst == net.output else dy
+                if trace: trace("bias_relu_bwd", op, y=y, dy=dy)
+                ops.bias_relu_bwd(y, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
+                if trace: trace("bias_relu_bwd:end", op, dpre=dpre, db=self.db[op.name])
+                x = self.act[op.src]
+                if trace: trace("conv_bwd_filter", op, x=x, dy=dpre)
+                ops.conv2d_bwd_filter(x, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, dw=self.dW[op.name],
+                                      ws=self.ws, stream=stream)
+                if trace: trace("conv_bwd_filter:end", op, dw=self.dW[op.name])
+                if src_grad:
+                    dx = self.grad[op.src]
+                    if trace: trace("conv_bwd_input", op, dy=dpre, w=self.Wlp[op.name], dx=dx, beta=beta)
+                    ops.conv2d_bwd_input(dpre, self.Wlp[op.name], dx, (op.sh, op.sw), op.pads, beta=beta,
+                                         stream=stream)
+                    if trace: trace("conv_bwd_input:end", op, dx=dx)
+            else:
+                if src_grad:
+                    dx = self.grad[op.src]
+                    am = self.argmax[op.name]
+                    if trace: trace("maxpool_bwd", op, dy=dy, argmax=am, dx=dx, beta=beta)
+                    ops.maxpool_bwd(dy, am, dx, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
+                                    stream=stream)
+                    if trace: trace("maxpool_bwd:end", op, dx=dx)
+            if src_grad:
+                written.add(op.src)
+
+    def update(self, trace=None, stream=None):
+        if trace: trace("apply_sgd", None, var=self.params, grad=self.grads)
+        ops.apply_sgd(self.params, self.grads, self.lr, shadow=self.shadow, stream=stream)
+        if trace: trace("apply_sgd:end", None, var=self.params)
+
+    def step(self, trace=None, stream=None):
+        self.forward(trace, stream)
+        self.backward(trace, stream)
+        self.update(trace, stream)
+
+    # ------------------------------------------------------------------ state
+    def snapshot(self):
+        """Copies of the variables (master and shadow), for restore-and-rerun checks."""
+        return (self.params.clone(), None if self.shadow is None else self.shadow.clone())
+
+    def restore(self, snap):
+        self.params.copy_(snap[0])
+        if self.shadow is not None:
+            self.shadow.copy_(snap[1])

@@ -1,0 +1,171 @@
+"""Parity harness between the HIP path and the CPU oracle (GPU tests only).
+
+Error metric (fixed for every floating-point comparison):
+    err(a, r) = max_i |a_i - r_i| / RMS(r)
+i.e. the worst absolute error in units of the reference's root-mean-square
+value.  Bars: fp32 path <= 1e-4; bf16 storage with fp32 accumulation <= 2e-2.
+Argmax indices must match exactly.  SGD results must be within 1 ulp of the
+fp32 rounding of the fp64 oracle.
+
+Comparisons are teacher-forced: the oracle receives the exact values the GPU
+op consumed (bf16 widened to fp64), so kernel error is isolated from the
+compounding of bf16 storage across layers.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+
+BAR = {torch.float32: 1e-4, torch.bfloat16: 2e-2}
+
+
+def f64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().to(torch.float64).cpu().numpy()
+
+
+def err(a, r) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    r = np.asarray(r, dtype=np.float64)
+    if r.size == 0:
+        return 0.0
+    rms = float(np.sqrt(np.mean(r * r)))
+    d = float(np.max(np.abs(a - r)))
+    return d / rms if rms > 0 else d
+
+
+def ulp_diff_f32(a: np.ndarray, r64: np.ndarray) -> int:
+    """Max distance in fp32 ulps between fp32 array a and fp32(r64)."""
+    a = np.ascontiguousarray(a, dtype=np.float32).view(np.int32).astype(np.int64)
+    b = np.ascontiguousarray(r64.astype(np.float32)).view(np.int32).astype(np.int64)
+    a = np.where(a < 0, -(a & 0x7fffffff), a)
+    b = np.where(b < 0, -(b & 0x7fffffff), b)
+    return int(np.max(np.abs(a - b))) if a.size else 0
+
+
+def say(*args):
+    print(*args, flush=True)
+    sys.stdout.flush()
+
+
+class ParityTracer:
+    """Step-driver hook: snapshots each op's inputs, then checks its outputs.
+
+    ``sample_images``: None checks whole tensors; a list of image indices checks
+    only those images (outputs of every op but the filter/bias gradients depend
+    on one image each) and evaluates ``filter_samples`` filter-gradient entries
+    through the oracle's sampled entry point.
+    """
+
+    def __init__(self, dtype, sample_images=None, filter_samples=256, seed=0, label=""):
+        self.dtype = dtype
+        self.bar = BAR[dtype]
+        self.sample = sample_images
+        self.filter_samples = filter_samples
+        self.rng = np.random.default_rng(seed)
+        self.pending = None
+        self.results = []           # (kind, op name, metric, value, bar, ok)
+        self.label = label
+
+    # -------------------------------------------------------------- helpers
+    def _imgs(self, a: np.ndarray) -> np.ndarray:
+        return a if self.sample is None else a[self.sample]
+
+    def _x64(self, t: torch.Tensor) -> np.ndarray:
+        if self.sample is None:
+            return f64(t)
+        idx = torch.tensor(self.sample, device=t.device)
+        return f64(t.index_select(0, idx))
+
+    def record(self, kind, name, metric, value, bar):
+        ok = value <= bar
+        self.results.append((kind, name, metric, value, bar, ok))
+
+    def failures(self):
+        return [r for r in self.results if not r[5]]
+
+    def summary(self):
+        worst = {}
+        for kind, name, metric, value, bar, ok in self.results:
+            key = (kind, metric)
+            score = value / bar if bar > 0 else value
+            if key not in worst or score > worst[key][3]:
+                worst[key] = (value, bar, name, score)
+        return worst
+
+    # -------------------------------------------------------------- hook
+    def __call__(self, event, op, **t):
+        if not event.endswith(":end"):
+            snap = {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in t.items()}
+            self.pending = (event, op, snap)
+            return
+        kind, op0, inp = self.pending
+        assert kind == event[:-4] and op0 is op
+        torch.cuda.synchronize()
+        getattr(self, "_check_" + kind)(op, inp, t)
+        self.pending = None
+
+    # -------------------------------------------------------------- checks
+    def _check_conv_fwd(self, op, inp, out):
+        ref = oracle.conv2d_fwd(self._x64(inp["x"]), f64(inp["w"]), (op.sh, op.sw), op.pads)
+        self.record("conv_fwd", op.name, "err", err(self._x64(out["y"]), ref), self.bar)
+
+    def _check_bias_relu_fwd(self, op, inp, out):
+        ref = oracle.bias_relu_fwd(self._x64(inp["y"]), f64(inp["b"]))
+        y = self._x64(out["y"])
+        self.record("bias_relu_fwd", op.name, "err", err(y, ref), self.bar)
+        self.record("bias_relu_fwd", op.name, "negatives", float(np.sum(np.signbit(y))), 0.0)
+
+    def _check_maxpool_fwd(self, op, inp, out):
+        x = self._x64(inp["x"])
+        ref, am = oracle.maxpool_fwd(x, (op.kh, op.kw), (op.sh, op.sw), op.pads)
+        got_am = out["argmax"].cpu().numpy().astype(np.int64)
+        if self.sample is not None:
+            n, h, w, c = inp["x"].shape
+            got_am = got_am[self.sample] - (np.asarray(self.sample) * (h * w * c))[:, None, None, None]
+        self.record("maxpool_fwd", op.name, "err", err(self._x64(out["y"]), ref), 0.0)
+        self.record("maxpool_fwd", op.name, "argmax_mismatch", float(np.sum(got_am != am)), 0.0)
+
+    def _check_bias_relu_bwd(self, op, inp, out):
+        y, dy = f64(inp["y"]), f64(inp["dy"])
+        ref_dpre, ref_db = oracle.bias_relu_bwd(y, dy)
+        self.record("bias_relu_bwd", op.name, "err_dpre", err(f64(out["dpre"]), ref_dpre), self.bar)
+        self.record("bias_relu_bwd", op.name, "err_db", err(f64(out["db"]), ref_db), self.bar)
+
+    def _check_conv_bwd_filter(self, op, inp, out):
+        dw = f64(out["dw"])
+        if self.sample is None:
+            ref = oracle.conv2d_bwd_filter(f64(inp["x"]), f64(inp["dy"]), (op.kh, op.kw), (op.sh, op.sw), op.pads)
+            self.record("conv_bwd_filter", op.name, "err", err(dw, ref), self.bar)
+        else:
+            idx = self.rng.integers(0, dw.size, size=min(self.filter_samples, dw.size))
+            ref = oracle.conv2d_bwd_filter_at(f64(inp["x"]), f64(inp["dy"]), (op.kh, op.kw), (op.sh, op.sw),
+                                              op.pads, idx)
+            self.record("conv_bwd_filter", op.name, "err_sampled", err(dw.ravel()[idx], ref), self.bar)
+
+    def _check_conv_bwd_input(self, op, inp, out):
+        dy = self._x64(inp["dy"])
+        dx_old = self._x64(inp["dx"])
+        ref = oracle.conv2d_bwd_input(dy, f64(inp["w"]), dx_old.shape, (op.sh, op.sw), op.pads,
+                                      dx=dx_old, beta=inp["beta"])
+        self.record("conv_bwd_input", op.name, "err", err(self._x64(out["dx"]), ref), self.bar)
+
+    def _check_maxpool_bwd(self, op, inp, out):
+        dy = self._x64(inp["dy"])
+        am = inp["argmax"].cpu().numpy().astype(np.int64)
+        dx_old = self._x64(inp["dx"])
+        if self.sample is not None:
+            n, h, w, c = inp["dx"].shape
+            am = am[self.sample] - (np.asarray(self.sample) * (h * w * c))[:, None, None, None]
+        ref = oracle.maxpool_bwd(dy, am.astype(np.int32), dx_old.shape, dx=dx_old, beta=inp["beta"])
+        self.record("maxpool_bwd", op.name, "err", err(self._x64(out["dx"]), ref), self.bar)
+
+    def _check_apply_sgd(self, op, inp, out):
+        var, grad = inp["var"].cpu().numpy(), inp["grad"].cpu().numpy()
+        ref = oracle.apply_sgd(var.astype(np.float64), grad.astype(np.float64), self.lr)
+        self.record("apply_sgd", "all", "ulp", float(ulp_diff_f32(out["var"].cpu().numpy(), ref)), 1.0)
+
+    lr = 0.01

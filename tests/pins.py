@@ -204,6 +204,30 @@ def check_conv_fd(seed=7, samples=12):
     return worst
 
 
+def check_conv_bwd_vs_autograd(seed=15, cases=25):
+    """Library pin: torch float64 autograd of conv2d gives dX and dW of <g, conv(x, w)>;
+    also checks the sampled filter-gradient entry point at random entries."""
+    rng = np.random.default_rng(seed)
+    worst = 0.0
+    for _ in range(cases):
+        x, w, s, pads = random_conv_case(rng)
+        y = torch_conv(x, w, s, pads)
+        g = rng.standard_normal(y.shape)
+        pt, pb, pl, pr = pads
+        xt = torch.from_numpy(np.ascontiguousarray(x.transpose(0, 3, 1, 2))).requires_grad_(True)
+        wt = torch.from_numpy(np.ascontiguousarray(w.transpose(3, 2, 0, 1))).requires_grad_(True)
+        yt = F.conv2d(F.pad(xt, (pl, pr, pt, pb)), wt, stride=s)
+        (yt * torch.from_numpy(np.ascontiguousarray(g.transpose(0, 3, 1, 2)))).sum().backward()
+        dx_ref = xt.grad.numpy().transpose(0, 2, 3, 1)
+        dw_ref = wt.grad.numpy().transpose(2, 3, 1, 0)
+        dx = oracle.conv2d_bwd_input(g, w, x.shape, s, pads)
+        dw = oracle.conv2d_bwd_filter(x, g, w.shape[:2], s, pads)
+        idx = rng.integers(0, w.size, size=8)
+        dw_at = oracle.conv2d_bwd_filter_at(x, g, w.shape[:2], s, pads, idx)
+        worst = max(worst, rel(dx, dx_ref), rel(dw, dw_ref), rel(dw_at, dw_ref.ravel()[idx]))
+    return worst
+
+
 # ----------------------------------------------------------------------------- pool
 def windows(x_shape, kh, kw, s, pads):
     """Brute-force window enumeration: for each output position, the in-bounds taps in

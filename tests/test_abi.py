@@ -1,0 +1,187 @@
+"""C ABI checks that need no GPU: the library loads, exports what include/tfk.h
+declares, and rejects invalid arguments before launching anything.
+
+Every call here fails validation (a GPU-free code path); pointers are fake
+addresses that are never dereferenced.
+"""
+import ctypes
+import os
+import re
+import subprocess
+import tempfile
+
+import pytest
+import torch
+
+from paper_1605_08695_amd import _lib, ops
+from paper_1605_08695_amd._lib import Nhwc, Window
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tfk.h")
+
+F32, BF16 = 0, 1
+OK, NULL, SHAPE, DTYPE, ALIGN, OVERFLOW, ALIAS, WORKSPACE, HIP, ARG = range(10)
+P = 0x10000000          # fake, 256-byte aligned device addresses (never dereferenced)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def vp(a):
+    return ctypes.c_void_p(a)
+
+
+def test_header_symbols_exported(lib):
+    decl = re.findall(r"TFK_API\s+[^;]*?\b(tfk_\w+)\s*\(", open(HEADER).read())
+    assert sorted(set(decl)) == sorted(_lib.EXPORTS)
+    out = subprocess.check_output(["nm", "-D", "--defined-only", _lib.LIB_PATH], text=True)
+    exported = set(re.findall(r"\bT (tfk_\w+)", out))
+    assert set(decl) == exported
+    for name in decl:
+        assert hasattr(lib, name)
+
+
+def test_abi_version_and_status_strings(lib):
+    assert lib.tfk_abi_version() == 1
+    assert lib.tfk_status_string(0) == b"ok"
+    assert lib.tfk_status_string(6) == b"illegal aliasing"
+    assert lib.tfk_status_string(99) == b"unknown status"
+
+
+def conv_fwd(lib, x=P, xd=(2, 8, 8, 16, 0), w=P + 0x100000, cout=32, win=(3, 3, 1, 1, 1, 1, 1, 1), dt=F32,
+             y=P + 0x200000, yd=(2, 8, 8, 32, 0)):
+    return lib.tfk_conv2d_fwd(vp(x), Nhwc(*xd), vp(w), cout, Window(*win), dt, vp(y), Nhwc(*yd), None, 0, None)
+
+
+def test_conv_fwd_validation(lib):
+    assert conv_fwd(lib, x=0) == NULL
+    assert conv_fwd(lib, dt=7) == DTYPE
+    assert conv_fwd(lib, yd=(2, 7, 8, 32, 0)) == SHAPE                 # wrong output extent
+    assert conv_fwd(lib, yd=(2, 8, 8, 16, 0)) == SHAPE                 # wrong cout
+    assert conv_fwd(lib, win=(3, 3, 1, 1, 3, 1, 1, 1)) == SHAPE        # pad == kernel extent
+    assert conv_fwd(lib, win=(3, 3, 0, 1, 1, 1, 1, 1)) == SHAPE        # zero stride
+    assert conv_fwd(lib, xd=(2, 8, 8, 16, 8)) == SHAPE                 # pixel stride < c
+    assert conv_fwd(lib, x=P + 2) == ALIGN                             # fp32 needs 4-byte alignment
+    assert conv_fwd(lib, y=P + 0x100) == ALIAS                         # y overlaps x
+    assert conv_fwd(lib, xd=(2, 1, 1, 16, 0), yd=(2, 1, 1, 32, 0), win=(3, 3, 1, 1, 0, 0, 0, 0)) == SHAPE
+    assert b"must be" in lib.tfk_last_error() or len(lib.tfk_last_error()) > 0
+
+
+def test_conv_bwd_validation(lib):
+    W = Window(3, 3, 1, 1, 1, 1, 1, 1)
+    st = lib.tfk_conv2d_bwd_input(vp(P), Nhwc(2, 8, 8, 32, 0), vp(P + 0x100000), W, F32, vp(P + 0x200000),
+                                  Nhwc(2, 8, 8, 16, 0), ctypes.c_float(0.5), None, 0, None)
+    assert st == ARG                                                   # beta must be 0 or 1
+    st = lib.tfk_conv2d_bwd_input(vp(P), Nhwc(2, 8, 8, 32, 0), vp(P + 0x100000), W, F32, vp(P + 0x100),
+                                  Nhwc(2, 8, 8, 16, 0), ctypes.c_float(0.0), None, 0, None)
+    assert st == ALIAS                                                 # dx overlaps dy
+    # bwd-filter with splits needs a workspace
+    xd = Nhwc(64, 56, 56, 64, 0)
+    need = lib.tfk_conv2d_workspace_bytes(2, xd, 64, W, BF16)
+    assert need > 0
+    st = lib.tfk_conv2d_bwd_filter(vp(P), xd, vp(P + 0x40000000), Nhwc(64, 56, 56, 64, 0), W, BF16,
+                                   vp(P + 0x80000000), vp(P + 0xC0000000), need - 1, None)
+    assert st == WORKSPACE
+    st = lib.tfk_conv2d_bwd_filter(vp(P), xd, vp(P + 0x40000000), Nhwc(64, 56, 56, 64, 0), W, BF16,
+                                   vp(0), vp(P + 0xC0000000), need, None)
+    assert st == NULL
+
+
+def test_pool_validation(lib):
+    W = Window(3, 3, 2, 2, 0, 0, 0, 0)
+    st = lib.tfk_maxpool_fwd(vp(P), Nhwc(2, 7, 7, 8, 0), W, BF16, vp(P + 0x100000), Nhwc(2, 4, 4, 8, 0),
+                             vp(P + 0x200000), None)
+    assert st == SHAPE                                                 # 7 -> 3, not 4
+    big = Nhwc(1 << 12, 1 << 10, 1 << 8, 4, 0)                         # 2^32 elements: argmax overflows
+    st = lib.tfk_maxpool_fwd(vp(P), big, Window(2, 2, 2, 2, 0, 0, 0, 0), BF16, vp(P), Nhwc(1 << 12, 512, 128, 4, 0),
+                             vp(P), None)
+    assert st == OVERFLOW
+    st = lib.tfk_maxpool_bwd(vp(P), vp(P + 0x100000), Nhwc(2, 3, 3, 8, 0), W, BF16, vp(P + 0x200000),
+                             Nhwc(2, 7, 7, 8, 0), ctypes.c_float(2.0), None)
+    assert st == ARG
+
+
+def test_bias_relu_validation(lib):
+    yd = Nhwc(4, 8, 8, 64, 0)
+    need = lib.tfk_bias_relu_bwd_workspace_bytes(yd, BF16)
+    assert need >= 64 * 4
+    st = lib.tfk_bias_relu_bwd(vp(P), vp(P + 0x100000), yd, vp(P + 0x100010), vp(P + 0x300000), BF16,
+                               vp(P + 0x400000), need, None)
+    assert st == ALIAS                                                 # dpre partially overlaps dy
+    st = lib.tfk_bias_relu_bwd(vp(P), vp(P + 0x100000), yd, vp(P + 0x100000), vp(P + 0x300000), BF16,
+                               vp(P + 0x400000), need - 4, None)
+    assert st == WORKSPACE
+    st = lib.tfk_bias_relu_fwd(vp(P), yd, vp(0), BF16, None)
+    assert st == NULL
+
+
+def test_sgd_validation(lib):
+    assert lib.tfk_apply_sgd(vp(P), vp(P + 0x10), 100, ctypes.c_float(0.01), None, None) == ALIAS
+    assert lib.tfk_apply_sgd(vp(P), vp(P + 0x1000), -1, ctypes.c_float(0.01), None, None) == SHAPE
+    assert lib.tfk_apply_sgd(vp(P), vp(P + 0x1000), 10, ctypes.c_float(float("nan")), None, None) == ARG
+    assert lib.tfk_apply_sgd(vp(P + 1), vp(P + 0x1000), 10, ctypes.c_float(0.01), None, None) == ALIGN
+    assert lib.tfk_apply_sgd(vp(0), vp(P), 10, ctypes.c_float(0.01), None, None) == NULL
+    # empty update is a no-op that needs no pointers
+    assert lib.tfk_apply_sgd(vp(0), vp(0), 0, ctypes.c_float(0.01), None, None) == OK
+    VP = ctypes.c_void_p * 2
+    NS = ctypes.c_int64 * 2
+    st = lib.tfk_apply_sgd_multi(2, VP(P, P + 0x1000), VP(P + 0x2000, P + 0x1000), NS(16, 16),
+                                 ctypes.c_float(0.01), None, None)
+    assert st == ALIAS                                                 # second var == its grad
+    assert b"tensor 1" in lib.tfk_last_error()
+
+
+def test_empty_batch_conv_fwd_is_noop(lib):
+    # n == 0: nothing to read or write, so no launch and no pointers needed
+    assert conv_fwd(lib, x=0, w=0, y=0, xd=(0, 8, 8, 16, 0), yd=(0, 8, 8, 32, 0)) == OK
+
+
+def test_nhwc_view_of_channel_slice():
+    buf = torch.zeros(2, 5, 6, 48)
+    d = ops.nhwc(buf[..., 16:40])
+    assert (d.n, d.h, d.w, d.c, d.pixel_stride) == (2, 5, 6, 24, 48)
+    d = ops.nhwc(buf)
+    assert (d.c, d.pixel_stride) == (48, 48)
+    with pytest.raises(ValueError):
+        ops.nhwc(buf.permute(0, 3, 1, 2))
+
+
+FASTDIV_TEST = r"""
+#include <stdio.h>
+#include <stdint.h>
+#include "fastdiv.h"
+int main() {
+    const uint32_t ds[] = {1, 2, 3, 5, 6, 7, 11, 13, 27, 55, 169, 729, 3025, 50176, 65535, 65536, 65537,
+                           1000003, 46340u * 46340u, 0x7fffffffu};
+    uint64_t bad = 0;
+    for (uint32_t d : ds) {
+        FastDiv f(d);
+        for (uint64_t n = 0; n < (1ull << 31); n += (n < 1000000 ? 1 : 7919 + (n >> 20))) {
+            uint32_t q, r;
+            f.divmod((uint32_t)n, q, r);
+            if (q != n / d || r != n % d) ++bad;
+        }
+        const uint32_t edge[] = {0x7fffffffu, 0x7ffffffeu, d - 1, d, d + 1, 2 * d - 1};
+        for (uint32_t n : edge) {
+            if (n >= 0x80000000u) continue;
+            uint32_t q, r;
+            f.divmod(n, q, r);
+            if (q != n / d || r != n % d) ++bad;
+        }
+    }
+    printf("%llu\n", (unsigned long long)bad);
+    return bad != 0;
+}
+"""
+
+
+def test_fastdiv_host_exhaustive_sample():
+    with tempfile.TemporaryDirectory() as td:
+        src = os.path.join(td, "t.cpp")
+        open(src, "w").write(FASTDIV_TEST)
+        exe = os.path.join(td, "t")
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-I",
+                               os.path.join(ROOT, "paper_1605_08695_amd", "csrc"), src, "-o", exe])
+        assert subprocess.run([exe], capture_output=True, text=True).stdout.strip() == "0"

@@ -1,0 +1,238 @@
+"""Per-op parity of the HIP kernels against the CPU oracle on seeded inputs (GPU).
+
+Shapes span several tiles with ragged tails, odd channel counts (scalar
+gather paths), strided and asymmetric windows, channel-slice views (concat
+buffers), the stride-phase cases of bwd-input (including a phase with no
+taps), empty batches, ties in max-pool and both element types.
+"""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1605_08695_amd import ops
+from tests.gpu_parity import BAR, err, f64, say, ulp_diff_f32
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+DTYPES = [torch.float32, torch.bfloat16]
+
+# N, H, W, Cin, Cout, KH, KW, sh, sw, pads
+CONV_CASES = [
+    ("single_layer", 8, 32, 32, 16, 32, 3, 3, 1, 1, (1, 1, 1, 1)),
+    ("ragged_tiles", 3, 13, 11, 24, 136, 3, 3, 1, 1, (1, 1, 1, 1)),
+    ("cin3_11x11s4", 2, 35, 35, 3, 64, 11, 11, 4, 4, (2, 2, 2, 2)),
+    ("3x3s2_valid", 2, 17, 17, 32, 48, 3, 3, 2, 2, (0, 0, 0, 0)),
+    ("1x7_asym", 2, 9, 9, 16, 24, 1, 7, 1, 1, (0, 0, 3, 3)),
+    ("7x1_asym", 2, 9, 9, 16, 24, 7, 1, 1, 1, (3, 3, 0, 0)),
+    ("1x1s2_empty_phase", 2, 8, 8, 16, 32, 1, 1, 2, 2, (0, 0, 0, 0)),
+    ("odd_channels", 2, 7, 7, 5, 7, 3, 3, 1, 1, (1, 1, 1, 1)),
+    ("5x5_cout192", 2, 14, 14, 64, 192, 5, 5, 1, 1, (2, 2, 2, 2)),
+    ("long_reduction", 16, 28, 28, 64, 64, 3, 3, 1, 1, (1, 1, 1, 1)),
+    ("3x3s2_pad_odd", 3, 10, 9, 8, 16, 3, 3, 2, 2, (1, 0, 1, 0)),
+]
+
+
+def _mk(shape, dtype, rng, scale=1.0):
+    a = rng.standard_normal(shape) * scale
+    return torch.from_numpy(a).to(dtype).to(DEV)
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
+@pytest.mark.parametrize("case", CONV_CASES, ids=[c[0] for c in CONV_CASES])
+def test_conv_three_directions(case, dtype):
+    name, N, H, W, C, K, KH, KW, sh, sw, pads = case
+    say("conv case", name, dtype)
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    x = _mk((N, H, W, C), dtype, rng)
+    w = _mk((KH, KW, C, K), dtype, rng, np.sqrt(2.0 / (KH * KW * C)))
+    y = ops.conv2d_fwd(x, w, (sh, sw), pads)
+    torch.cuda.synchronize()
+    ref = oracle.conv2d_fwd(f64(x), f64(w), (sh, sw), pads)
+    assert y.shape == ref.shape
+    e = err(f64(y), ref)
+    say("  fwd err %.2e" % e)
+    assert e <= BAR[dtype]
+
+    dy = _mk(y.shape, dtype, rng)
+    for beta in (0.0, 1.0):
+        dx = _mk(x.shape, dtype, rng)
+        dx_old = f64(dx)
+        ops.conv2d_bwd_input(dy, w, dx, (sh, sw), pads, beta=beta)
+        torch.cuda.synchronize()
+        ref = oracle.conv2d_bwd_input(f64(dy), f64(w), x.shape, (sh, sw), pads, dx=dx_old, beta=beta)
+        e = err(f64(dx), ref)
+        say("  bwd_input beta=%g err %.2e" % (beta, e))
+        assert e <= BAR[dtype]
+
+    dw = ops.conv2d_bwd_filter(x, dy, (KH, KW), (sh, sw), pads)
+    torch.cuda.synchronize()
+    ref = oracle.conv2d_bwd_filter(f64(x), f64(dy), (KH, KW), (sh, sw), pads)
+    e = err(f64(dw), ref)
+    say("  bwd_filter err %.2e" % e)
+    assert e <= BAR[dtype]
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
+def test_conv_channel_slice_views(dtype):
+    """Input read from and output written into channel slices of wider buffers."""
+    rng = np.random.default_rng(7)
+    big_in = _mk((2, 9, 9, 48), dtype, rng)
+    x = big_in[..., 8:40]                                    # 32 channels, pixel stride 48
+    w = _mk((3, 3, 32, 24), dtype, rng, 0.1)
+    out = torch.full((2, 9, 9, 64), 7.0, dtype=dtype, device=DEV)
+    y = out[..., 16:40]
+    ops.conv2d_fwd(x, w, 1, (1, 1, 1, 1), y=y)
+    torch.cuda.synchronize()
+    ref = oracle.conv2d_fwd(f64(x), f64(w), 1, (1, 1, 1, 1))
+    assert err(f64(y), ref) <= BAR[dtype]
+    rest = torch.cat([out[..., :16], out[..., 40:]], dim=-1)
+    assert bool(torch.all(rest == 7.0))                      # neighbours untouched
+    dyb = _mk((2, 9, 9, 64), dtype, rng)
+    dy = dyb[..., 16:40]
+    dxb = torch.zeros((2, 9, 9, 48), dtype=dtype, device=DEV)
+    dx = dxb[..., 8:40]
+    ops.conv2d_bwd_input(dy, w, dx, 1, (1, 1, 1, 1))
+    dw = ops.conv2d_bwd_filter(x, dy, (3, 3), 1, (1, 1, 1, 1))
+    torch.cuda.synchronize()
+    assert err(f64(dx), oracle.conv2d_bwd_input(f64(dy), f64(w), x.shape, 1, (1, 1, 1, 1))) <= BAR[dtype]
+    assert err(f64(dw), oracle.conv2d_bwd_filter(f64(x), f64(dy), (3, 3), 1, (1, 1, 1, 1))) <= BAR[dtype]
+    assert bool(torch.all(dxb[..., :8] == 0)) and bool(torch.all(dxb[..., 40:] == 0))
+
+
+def test_conv_empty_batch_filter_grad_is_zero():
+    x = torch.zeros((0, 8, 8, 16), dtype=torch.bfloat16, device=DEV)
+    dy = torch.zeros((0, 8, 8, 32), dtype=torch.bfloat16, device=DEV)
+    dw = torch.full((3, 3, 16, 32), 5.0, device=DEV)
+    ops.conv2d_bwd_filter(x, dy, (3, 3), 1, (1, 1, 1, 1), dw=dw)
+    torch.cuda.synchronize()
+    assert bool(torch.all(dw == 0))
+
+
+def test_conv_misaligned_base_uses_scalar_path():
+    """A view whose base is not 16-byte aligned still computes correctly."""
+    rng = np.random.default_rng(9)
+    flat = _mk((1 + 2 * 6 * 6 * 16,), torch.bfloat16, rng)
+    x = flat[1:].view(2, 6, 6, 16)                           # 2-byte offset
+    w = _mk((3, 3, 16, 16), torch.bfloat16, rng, 0.2)
+    y = ops.conv2d_fwd(x, w, 1, (1, 1, 1, 1))
+    torch.cuda.synchronize()
+    assert err(f64(y), oracle.conv2d_fwd(f64(x), f64(w), 1, (1, 1, 1, 1))) <= BAR[torch.bfloat16]
+
+
+# ----------------------------------------------------------------------------- bias + relu
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
+@pytest.mark.parametrize("shape,slice_", [((2, 7, 7, 64), None), ((3, 5, 5, 13), None),
+                                          ((2, 6, 6, 96), (32, 80)), ((64, 13, 13, 384), None)],
+                         ids=["c64", "c13_odd", "slice", "alexnet_conv3"])
+def test_bias_relu(dtype, shape, slice_):
+    rng = np.random.default_rng(11)
+    buf = _mk(shape, dtype, rng)
+    y = buf if slice_ is None else buf[..., slice_[0]:slice_[1]]
+    C = y.shape[-1]
+    b = torch.from_numpy(rng.standard_normal(C) * 0.5).float().to(DEV)
+    pre = f64(y)
+    ops.bias_relu_fwd(y, b)
+    torch.cuda.synchronize()
+    got = f64(y)
+    assert err(got, oracle.bias_relu_fwd(pre, f64(b))) <= BAR[dtype]
+    assert not np.any(np.signbit(got))
+    dybuf = _mk(buf.shape, dtype, rng)
+    dy = dybuf if slice_ is None else dybuf[..., slice_[0]:slice_[1]]
+    dy0 = f64(dy)
+    dpre, db = ops.bias_relu_bwd(y, dy, dpre=dy)          # in place
+    torch.cuda.synchronize()
+    ref_dpre, ref_db = oracle.bias_relu_bwd(got, dy0)
+    assert err(f64(dpre), ref_dpre) <= BAR[dtype]
+    assert err(f64(db), ref_db) <= BAR[dtype]
+    # exact: masked entries are exactly zero, passed entries exactly dy
+    assert np.array_equal(f64(dpre), ref_dpre)
+
+
+# ----------------------------------------------------------------------------- max-pool
+POOL_CASES = [
+    ("alexnet_pool1", (2, 55, 55, 64), 3, 2, (0, 0, 0, 0)),
+    ("same_3s2", (2, 28, 28, 192), 3, 2, (0, 1, 0, 1)),
+    ("branch_3s1", (2, 6, 5, 8), 3, 1, (1, 1, 1, 1)),
+    ("odd_c", (2, 8, 8, 5), 2, 2, (0, 0, 0, 0)),
+    ("vgg_2s2", (2, 14, 14, 128), 2, 2, (0, 0, 0, 0)),
+]
+
+
+@pytest.mark.parametrize("ties", [False, True], ids=["random", "ties"])
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
+@pytest.mark.parametrize("case", POOL_CASES, ids=[c[0] for c in POOL_CASES])
+def test_maxpool(case, dtype, ties):
+    name, shape, k, s, pads = case
+    rng = np.random.default_rng(13)
+    a = rng.standard_normal(shape)
+    if ties:
+        a = np.maximum(np.round(a * 2), 0.0)                 # many exact zeros and repeats
+    x = torch.from_numpy(a).to(dtype).to(DEV)
+    y, am = ops.maxpool_fwd(x, (k, k), s, pads)
+    torch.cuda.synchronize()
+    ref_y, ref_am = oracle.maxpool_fwd(f64(x), (k, k), s, pads)
+    assert np.array_equal(f64(y), ref_y)
+    assert np.array_equal(am.cpu().numpy(), ref_am)
+    dy = _mk(y.shape, dtype, rng)
+    for beta in (0.0, 1.0):
+        dx = _mk(shape, dtype, rng)
+        old = f64(dx)
+        ops.maxpool_bwd(dy, am, dx, (k, k), s, pads, beta=beta)
+        torch.cuda.synchronize()
+        ref = oracle.maxpool_bwd(f64(dy), ref_am, shape, dx=old, beta=beta)
+        assert err(f64(dx), ref) <= BAR[dtype]
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
+def test_maxpool_slice_views(dtype):
+    """Pool output written into a concat slice; its gradient read from one."""
+    rng = np.random.default_rng(17)
+    x = _mk((2, 9, 9, 32), dtype, rng)
+    cat = torch.zeros((2, 4, 4, 80), dtype=dtype, device=DEV)
+    y = cat[..., 40:72]
+    _, am = ops.maxpool_fwd(x, (3, 3), 2, (0, 0, 0, 0), y=y)
+    torch.cuda.synchronize()
+    ref_y, ref_am = oracle.maxpool_fwd(f64(x), (3, 3), 2, (0, 0, 0, 0))
+    assert np.array_equal(f64(y), ref_y) and np.array_equal(am.cpu().numpy(), ref_am)
+    gcat = _mk((2, 4, 4, 80), dtype, rng)
+    dy = gcat[..., 40:72]
+    dx = torch.empty_like(x)
+    ops.maxpool_bwd(dy, am, dx, (3, 3), 2, (0, 0, 0, 0))
+    torch.cuda.synchronize()
+    assert err(f64(dx), oracle.maxpool_bwd(f64(dy), ref_am, x.shape)) <= BAR[dtype]
+
+
+# ----------------------------------------------------------------------------- sgd
+@pytest.mark.parametrize("n", [1, 1001, 2469696])
+def test_apply_sgd_one_ulp_and_shadow(n):
+    rng = np.random.default_rng(19)
+    v = torch.from_numpy(rng.standard_normal(n).astype(np.float32)).to(DEV)
+    g = torch.from_numpy(rng.standard_normal(n).astype(np.float32) * 10).to(DEV)
+    v0, g0 = v.cpu().numpy().astype(np.float64), g.cpu().numpy().astype(np.float64)
+    sh = torch.empty(n, dtype=torch.bfloat16, device=DEV)
+    lr = float(np.float32(0.01))
+    ops.apply_sgd(v, g, lr, shadow=sh)
+    torch.cuda.synchronize()
+    ref = oracle.apply_sgd(v0, g0, lr)
+    assert ulp_diff_f32(v.cpu().numpy(), ref) <= 1
+    assert torch.equal(sh, v.to(torch.bfloat16))            # bf16 shadow = RNE of the new value
+
+
+def test_apply_sgd_multi():
+    rng = np.random.default_rng(23)
+    sizes = [0, 5, 1024, 1025, 3000] + [17] * 20               # more than one launch batch
+    vs = [torch.from_numpy(rng.standard_normal(n).astype(np.float32)).to(DEV) for n in sizes]
+    gs = [torch.from_numpy(rng.standard_normal(n).astype(np.float32)).to(DEV) for n in sizes]
+    shs = [torch.empty(n, dtype=torch.bfloat16, device=DEV) if i % 2 else None for i, n in enumerate(sizes)]
+    before = [v.cpu().numpy().astype(np.float64) for v in vs]
+    ops.apply_sgd_multi(vs, gs, 0.045, shs)
+    torch.cuda.synchronize()
+    for v, g, b, sh in zip(vs, gs, before, shs):
+        ref = oracle.apply_sgd(b, g.cpu().numpy().astype(np.float64), float(np.float32(0.045)))
+        assert ulp_diff_f32(v.cpu().numpy(), ref) <= 1
+        if sh is not None:
+            assert torch.equal(sh, v.to(torch.bfloat16))

@@ -56,6 +56,10 @@ def test_conv_gradients_finite_differences():
     assert pins.check_conv_fd() < FD_BAR
 
 
+def test_conv_gradients_match_library_autograd():
+    assert pins.check_conv_bwd_vs_autograd() < 1e-12
+
+
 def test_conv_bwd_input_beta_accumulates():
     rng = np.random.default_rng(20)
     w = rng.standard_normal((3, 3, 2, 4))
