@@ -1,0 +1,253 @@
+"""Benchmark: one replica's synchronous SGD step of the AlexNet-shaped convnet.
+
+Workload: batch 128, 224x224x3 synthetic N(0,1) images, bf16 storage with fp32
+accumulation, conv 11x11/4 64 -> pool 3/2 -> 5x5 192 -> pool -> 3x3 384 ->
+3x3 256 -> 3x3 256 -> pool, bias+ReLU after each conv, He-normal filters, an
+N(0,1) upstream gradient of the last pool, plain SGD (lr 0.01) of every filter
+and bias.  All inputs are resident in HBM before timing starts.
+
+    python bench.py [--steps K] [--warmup W] [--eager] [--no-cpu-baseline]
+
+Prints one JSON line: ms per step (the timed region is K whole steps between
+two device synchronisations), conv TFLOP/s against the bf16 MFMA peak, the
+roofline entry of the convolution kernels measured with HIP events on the
+stream they run on, and the CPU oracle timed on a bounded batch slice.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA: 256 CU x 4096 FLOP/clk x 2.4 GHz
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+METRIC = "ms per training step + conv TFLOP/s (% bf16 MFMA peak), AlexNet-shape b=128"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--batch", type=int, default=128)
+    ap.add_argument("--eager", action="store_true", help="launch every op from Python instead of a HIP graph")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=128, help="images of the batch the oracle steps through")
+    ap.add_argument("--seed", type=int, default=0)
+    return ap.parse_args()
+
+
+def elementwise_bytes(net, op_kind, op, D):
+    """Algorithmic HBM bytes of one elementwise op (read + write of its operands)."""
+    t = net.tensors
+    if op_kind == "bias_relu_fwd":
+        n = int(np.prod(t[op.dst][:3])) * op.cout
+        return 2 * n * D
+    if op_kind == "bias_relu_bwd":
+        n = int(np.prod(t[op.dst][:3])) * op.cout
+        return 3 * n * D
+    if op_kind == "maxpool_fwd":
+        nx = int(np.prod(t[op.src]))
+        ny = int(np.prod(t[op.dst][:3])) * t[op.src][3]
+        return nx * D + ny * (D + 4)
+    if op_kind == "maxpool_bwd":
+        nx = int(np.prod(t[op.src]))
+        ny = int(np.prod(t[op.dst][:3])) * t[op.src][3]
+        return ny * (D + 4) + nx * D
+    raise KeyError(op_kind)
+
+
+def conv_flops(net, op):
+    n, oh, ow, _ = net.tensors[op.dst]
+    cin = net.tensors[op.src][3]
+    return 2.0 * n * oh * ow * op.kh * op.kw * cin * op.cout
+
+
+class EventTrace:
+    """Step-driver hook that brackets every op with HIP events on the current stream."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.open = None
+        self.rec = []           # (kind, op, start, end)
+
+    def __call__(self, event, op, **t):
+        if event.endswith(":end"):
+            e = self.torch.cuda.Event(enable_timing=True)
+            e.record()
+            kind, op0, s = self.open
+            self.rec.append((kind, op0, s, e))
+            self.open = None
+        else:
+            s = self.torch.cuda.Event(enable_timing=True)
+            s.record()
+            self.open = (event, op, s)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs one replica on one GPU; multi-GPU data parallelism is not built "
+              "(requested --gpus %d)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1605_08695_amd import workloads as W
+    from paper_1605_08695_amd.step import Replica
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    net = W.alexnet(batch=args.batch)
+    inp = W.make_inputs(net, seed=args.seed)
+    rep = Replica(net, inp)
+    D = 2
+    torch.cuda.synchronize()
+    print("bench: %s, %d params, %.1f GFLOP/step" % (net.name, rep.n_params, W.conv_flops(net) / 1e9),
+          file=sys.stderr, flush=True)
+
+    # ---------------------------------------------------------------- timed region
+    graph = None
+    if not args.eager:
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for _ in range(2):
+                rep.step()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            rep.step()
+        run = graph.replay
+    else:
+        run = rep.step
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    step_ms = []
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record()
+    for i in range(args.steps):
+        run()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    print("bench: timed %d steps, %.3f ms/step (median %.3f)" % (args.steps, ms_per_step, np.median(step_ms)),
+          file=sys.stderr, flush=True)
+
+    # ---------------------------------------------------------------- per-op events (eager)
+    tr = EventTrace(torch)
+    reps = max(3, min(10, args.steps))
+    per_kind = {}
+    per_layer = {}
+    for r in range(reps):
+        tr.rec.clear()
+        rep.step(trace=tr)
+        torch.cuda.synchronize()
+        for kind, op, s, e in tr.rec:
+            ms = s.elapsed_time(e)
+            per_kind.setdefault(kind, 0.0)
+            per_kind[kind] += ms / reps
+            key = (kind, op.name if op is not None else "all")
+            per_layer[key] = per_layer.get(key, 0.0) + ms / reps
+    conv_kinds = ("conv_fwd", "conv_bwd_input", "conv_bwd_filter")
+    conv_ms = sum(per_kind.get(k, 0.0) for k in conv_kinds)
+    flops = {k: 0.0 for k in conv_kinds}
+    launches = 0
+    for op in net.convs:
+        f = conv_flops(net, op)
+        flops["conv_fwd"] += f
+        flops["conv_bwd_filter"] += f
+        launches += 2
+        if op.src != "x" or net.input_grad:
+            flops["conv_bwd_input"] += f
+            launches += 1
+    conv_flop = sum(flops.values())
+    conv_tflops = conv_flop / (conv_ms * 1e-3) / 1e12
+    ew_kinds = ("bias_relu_fwd", "bias_relu_bwd", "maxpool_fwd", "maxpool_bwd")
+    ew_bytes = {k: 0.0 for k in ew_kinds}
+    for op in net.ops:
+        for k in ew_kinds:
+            if (k.startswith("bias") and hasattr(op, "cout")) or (k.startswith("maxpool") and not hasattr(op, "cout")):
+                if k == "maxpool_bwd" and op.src == "x":
+                    continue
+                ew_bytes[k] += elementwise_bytes(net, k, op, D)
+    sgd_bytes = rep.n_params * 14.0
+    ew_ms = sum(per_kind.get(k, 0.0) for k in ew_kinds) + per_kind.get("apply_sgd", 0.0)
+    ew_gbs = (sum(ew_bytes.values()) + sgd_bytes) / (ew_ms * 1e-3) / 1e9
+
+    # ---------------------------------------------------------------- CPU baseline: the oracle
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        from oracle import net as onet
+        oracle.build()
+        k = max(1, min(args.cpu_sample, args.batch))
+        snet = W.alexnet(batch=k)
+        sinp = W.make_inputs(net, seed=args.seed, batch_slice=k)
+        print("bench: oracle step on %d images ..." % k, file=sys.stderr, flush=True)
+        c0 = time.perf_counter()
+        onet.step(snet, sinp.x, sinp.weights, sinp.biases, sinp.g)
+        c1 = time.perf_counter()
+        cpu = {"value": round((c1 - c0) * 1e3 * args.batch / k, 1), "unit": "ms/step",
+               "cores": oracle.num_threads(), "kind": "oracle",
+               "sample": "%d of the %d images of one step (fp64 loop nests, %.1f s); oracle cost is linear "
+                         "in batch, scaled x%g" % (k, args.batch, c1 - c0, args.batch / k)}
+
+    dom = max(conv_kinds, key=lambda k: per_kind.get(k, 0.0))
+    n_dom = sum(1 for op in net.convs if dom != "conv_bwd_input" or op.src != "x" or net.input_grad)
+    out = {
+        "metric": METRIC,
+        "value": round(ms_per_step, 4),
+        "unit": "ms/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "alexnet_b%d" % args.batch, "global_batch": args.batch, "image": [224, 224, 3],
+                   "layers": "conv11x11/4-64,pool3/2,conv5x5-192,pool3/2,conv3x3-384,conv3x3-256,conv3x3-256,pool3/2",
+                   "launch": "eager" if args.eager else "hip_graph"},
+        "step_ms_median": round(float(np.median(step_ms)), 4),
+        "step_ms_p10": round(float(np.percentile(step_ms, 10)), 4),
+        "step_ms_p90": round(float(np.percentile(step_ms, 90)), 4),
+        "images_per_s": round(args.batch / (ms_per_step * 1e-3), 1),
+        "conv_gflop_per_step": round(conv_flop / 1e9, 2),
+        "conv_tflops": round(conv_tflops, 1),
+        "conv_pct_bf16_peak": round(100 * conv_tflops / PEAK_BF16_TFLOPS, 2),
+        "conv_tflops_by_direction": {k: round(flops[k] / (per_kind[k] * 1e-3) / 1e12, 1) for k in conv_kinds},
+        "eltwise_gbs": round(ew_gbs, 1),
+        "eltwise_pct_hbm_peak": round(100 * ew_gbs / PEAK_HBM_GBS, 2),
+        "per_op_ms": {k: round(v, 4) for k, v in sorted(per_kind.items())},
+        "roofline": {"kernel": "implicit-GEMM convolution (%s, %d launches/step)" % (dom, n_dom),
+                     "bound": "mfma",
+                     "achieved": round(flops[dom] / (per_kind[dom] * 1e-3) / 1e12, 1),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(flops[dom] / (per_kind[dom] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None,
+                     "avg_launch_us": round(per_kind[dom] * 1e3 / n_dom, 2),
+                     "flop_per_launch": round(flops[dom] / n_dom)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+    print("per-layer ms:", json.dumps({"%s/%s" % k: round(v, 4) for k, v in sorted(per_layer.items())}),
+          file=sys.stderr)
+
+
+if __name__ == "__main__":
+    main()

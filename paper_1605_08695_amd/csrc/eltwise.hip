@@ -89,7 +89,7 @@ __global__ __launch_bounds__(256) void bias_relu_fwd_kernel(T *__restrict__ y, i
 // Pass 1: block b owns pixels [b*ppb, min(P, (b+1)*ppb)).  Thread t owns channel
 // chunks cv = t % CVB (+ CVB, ...) and pixel rows t / CVB (+ R, ...).  It writes
 // dpre and keeps fp32 per-channel sums; the block then reduces its R row groups
-// in LDS in a fixed order and writes partial[b][c].
+// in LDS in a fixed order and writes partial[c][b].
 template <typename T, bool VEC>
 __global__ __launch_bounds__(256) void relu_bwd_partial_kernel(const T *__restrict__ y, const T *dy,
                                                                T *dpre, int64_t P, int C, int64_t ys,
@@ -139,17 +139,27 @@ __global__ __launch_bounds__(256) void relu_bwd_partial_kernel(const T *__restri
     for (int c = t; c < C; c += 256) {
         float acc = 0.f;
         for (int r = 0; r < R; ++r) acc += red[r * C + c];
-        partial[(int64_t)blockIdx.x * C + c] = acc;
+        partial[(int64_t)c * gridDim.x + blockIdx.x] = acc;
     }
 }
 
+// Pass 2: one block per channel sums its G partials (stored channel-major, so
+// the reads are contiguous): thread t takes b = t, t + 256, ... in order, then
+// a fixed-shape tree combines the 256 running sums.
 __global__ __launch_bounds__(256) void sum_partials_kernel(const float *__restrict__ partial, int G, int C,
                                                            float *__restrict__ out) {
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C) return;
+    __shared__ float red[256];
+    const int c = blockIdx.x;
+    const float *row = partial + (int64_t)c * G;
     float acc = 0.f;
-    for (int b = 0; b < G; ++b) acc += partial[(int64_t)b * C + c];
-    out[c] = acc;
+    for (int b = threadIdx.x; b < G; b += 256) acc += row[b];
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+        if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) out[c] = red[0];
 }
 
 // ------------------------------------------------------------------ max-pool forward
@@ -396,7 +406,7 @@ static hipError_t relu_bwd_t(const void *y, const void *dy, void *dpre, int64_t 
     else
         hipLaunchKernelGGL((relu_bwd_partial_kernel<T, false>), dim3(G), dim3(256), smem, st,
                            (const T *)y, (const T *)dy, (T *)dpre, P, C, ys, ppb, ws);
-    hipLaunchKernelGGL(sum_partials_kernel, dim3((C + 255) / 256), dim3(256), 0, st, ws, G, C, db);
+    hipLaunchKernelGGL(sum_partials_kernel, dim3(C), dim3(256), 0, st, ws, G, C, db);
     return hipGetLastError();
 }
 

@@ -1,11 +1,28 @@
 """Parity harness between the HIP path and the CPU oracle (GPU tests only).
 
-Error metric (fixed for every floating-point comparison):
-    err(a, r) = max_i |a_i - r_i| / RMS(r)
-i.e. the worst absolute error in units of the reference's root-mean-square
-value.  Bars: fp32 path <= 1e-4; bf16 storage with fp32 accumulation <= 2e-2.
-Argmax indices must match exactly.  SGD results must be within 1 ulp of the
-fp32 rounding of the fp64 oracle.
+Error metrics (fixed for every floating-point comparison; ``r`` is the fp64
+oracle result, ``a`` the GPU result):
+
+    rel_l2(a, r) = ||a - r||_2 / ||r||_2          relative error normalised by
+                                                  the tensor's L2 norm
+    err(a, r)    = max_i |a_i - r_i| / RMS(r)     worst element in units of
+                                                  the reference's RMS
+    ulp(a, r)    = max_i |a_i - r_i| / (2^-7 |r_i| + 1e-3 RMS(r))
+
+Gates:
+* outputs stored in fp32 by an fp32 path: err <= 1e-4 (this also bounds
+  rel_l2 by 1e-4);
+* outputs stored in fp32 by a bf16-input path (filter and bias gradients):
+  err <= 2e-2;
+* outputs stored in bf16: rel_l2 <= 2e-2 and ulp <= 1, i.e. every element is
+  within one bf16 ulp of the exact value (round-to-nearest on store costs half
+  an ulp; a different fp32 summation order can move a value across a rounding
+  midpoint), plus a slack of 1e-3 RMS for cancellation.  A max-over-RMS gate
+  would count the storage rounding itself as error: on a sparse or
+  heavy-tailed tensor half a bf16 ulp of its largest element alone exceeds
+  2e-2 RMS.
+Argmax indices and max-pool values must match exactly.  SGD results must be
+within 1 ulp of the fp32 rounding of the fp64 oracle.
 
 Comparisons are teacher-forced: the oracle receives the exact values the GPU
 op consumed (bf16 widened to fp64), so kernel error is isolated from the
@@ -35,6 +52,43 @@ def err(a, r) -> float:
     rms = float(np.sqrt(np.mean(r * r)))
     d = float(np.max(np.abs(a - r)))
     return d / rms if rms > 0 else d
+
+
+def rel_l2(a, r) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    r = np.asarray(r, dtype=np.float64)
+    nr = float(np.linalg.norm(r.ravel()))
+    d = float(np.linalg.norm((a - r).ravel()))
+    return d / nr if nr > 0 else d
+
+
+def ulp_bf16(a, r) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    r = np.asarray(r, dtype=np.float64)
+    if r.size == 0:
+        return 0.0
+    rms = float(np.sqrt(np.mean(r * r)))
+    tol = 2.0 ** -7 * np.abs(r) + 1e-3 * rms
+    tol = np.where(tol > 0, tol, 1e-30)
+    return float(np.max(np.abs(a - r) / tol))
+
+
+def compare(a, r, storage, path=None):
+    """Gate of one output tensor; returns (ok, metrics)."""
+    path = storage if path is None else path
+    m = {"err": err(a, r), "rel_l2": rel_l2(a, r)}
+    if storage == torch.bfloat16:
+        m["ulp"] = ulp_bf16(a, r)
+        ok = m["rel_l2"] <= 2e-2 and m["ulp"] <= 1.0
+    else:
+        ok = m["err"] <= BAR[path]
+    return ok, m
+
+
+def assert_close(a, r, storage, path=None, label=""):
+    ok, m = compare(a, r, storage, path)
+    say("  %-28s %s" % (label, " ".join("%s=%.2e" % kv for kv in m.items())))
+    assert ok, (label, m)
 
 
 def ulp_diff_f32(a: np.ndarray, r64: np.ndarray) -> int:
@@ -80,9 +134,25 @@ class ParityTracer:
         idx = torch.tensor(self.sample, device=t.device)
         return f64(t.index_select(0, idx))
 
+    def _index_shift(self, x_shape):
+        """Argmax indices of image sample[j] in the full batch minus those of image j of the slice."""
+        n, h, w, c = x_shape
+        j = np.arange(len(self.sample))
+        return ((np.asarray(self.sample) - j) * (h * w * c))[:, None, None, None]
+
     def record(self, kind, name, metric, value, bar):
         ok = value <= bar
         self.results.append((kind, name, metric, value, bar, ok))
+
+    def record_tensor(self, kind, name, a, r, storage, path=None):
+        path = self.dtype if path is None else path
+        ok, m = compare(a, r, storage, path)
+        if storage == torch.bfloat16:
+            self.record(kind, name, "rel_l2", m["rel_l2"], 2e-2)
+            self.record(kind, name, "ulp", m["ulp"], 1.0)
+            self.results.append((kind, name, "err(info)", m["err"], float("inf"), True))
+        else:
+            self.record(kind, name, "err", m["err"], BAR[path])
 
     def failures(self):
         return [r for r in self.results if not r[5]]
@@ -111,12 +181,12 @@ class ParityTracer:
     # -------------------------------------------------------------- checks
     def _check_conv_fwd(self, op, inp, out):
         ref = oracle.conv2d_fwd(self._x64(inp["x"]), f64(inp["w"]), (op.sh, op.sw), op.pads)
-        self.record("conv_fwd", op.name, "err", err(self._x64(out["y"]), ref), self.bar)
+        self.record_tensor("conv_fwd", op.name, self._x64(out["y"]), ref, self.dtype)
 
     def _check_bias_relu_fwd(self, op, inp, out):
         ref = oracle.bias_relu_fwd(self._x64(inp["y"]), f64(inp["b"]))
         y = self._x64(out["y"])
-        self.record("bias_relu_fwd", op.name, "err", err(y, ref), self.bar)
+        self.record_tensor("bias_relu_fwd", op.name, y, ref, self.dtype)
         self.record("bias_relu_fwd", op.name, "negatives", float(np.sum(np.signbit(y))), 0.0)
 
     def _check_maxpool_fwd(self, op, inp, out):
@@ -124,44 +194,42 @@ class ParityTracer:
         ref, am = oracle.maxpool_fwd(x, (op.kh, op.kw), (op.sh, op.sw), op.pads)
         got_am = out["argmax"].cpu().numpy().astype(np.int64)
         if self.sample is not None:
-            n, h, w, c = inp["x"].shape
-            got_am = got_am[self.sample] - (np.asarray(self.sample) * (h * w * c))[:, None, None, None]
+            got_am = got_am[self.sample] - self._index_shift(inp["x"].shape)
         self.record("maxpool_fwd", op.name, "err", err(self._x64(out["y"]), ref), 0.0)
         self.record("maxpool_fwd", op.name, "argmax_mismatch", float(np.sum(got_am != am)), 0.0)
 
     def _check_bias_relu_bwd(self, op, inp, out):
         y, dy = f64(inp["y"]), f64(inp["dy"])
         ref_dpre, ref_db = oracle.bias_relu_bwd(y, dy)
-        self.record("bias_relu_bwd", op.name, "err_dpre", err(f64(out["dpre"]), ref_dpre), self.bar)
-        self.record("bias_relu_bwd", op.name, "err_db", err(f64(out["db"]), ref_db), self.bar)
+        self.record("bias_relu_bwd", op.name, "dpre_mismatch", float(np.sum(f64(out["dpre"]) != ref_dpre)), 0.0)
+        self.record_tensor("bias_relu_bwd:db", op.name, f64(out["db"]), ref_db, torch.float32)
 
     def _check_conv_bwd_filter(self, op, inp, out):
         dw = f64(out["dw"])
         if self.sample is None:
             ref = oracle.conv2d_bwd_filter(f64(inp["x"]), f64(inp["dy"]), (op.kh, op.kw), (op.sh, op.sw), op.pads)
-            self.record("conv_bwd_filter", op.name, "err", err(dw, ref), self.bar)
+            self.record_tensor("conv_bwd_filter", op.name, dw, ref, torch.float32)
         else:
             idx = self.rng.integers(0, dw.size, size=min(self.filter_samples, dw.size))
             ref = oracle.conv2d_bwd_filter_at(f64(inp["x"]), f64(inp["dy"]), (op.kh, op.kw), (op.sh, op.sw),
                                               op.pads, idx)
-            self.record("conv_bwd_filter", op.name, "err_sampled", err(dw.ravel()[idx], ref), self.bar)
+            self.record_tensor("conv_bwd_filter:sampled", op.name, dw.ravel()[idx], ref, torch.float32)
 
     def _check_conv_bwd_input(self, op, inp, out):
         dy = self._x64(inp["dy"])
         dx_old = self._x64(inp["dx"])
         ref = oracle.conv2d_bwd_input(dy, f64(inp["w"]), dx_old.shape, (op.sh, op.sw), op.pads,
                                       dx=dx_old, beta=inp["beta"])
-        self.record("conv_bwd_input", op.name, "err", err(self._x64(out["dx"]), ref), self.bar)
+        self.record_tensor("conv_bwd_input", op.name, self._x64(out["dx"]), ref, self.dtype)
 
     def _check_maxpool_bwd(self, op, inp, out):
         dy = self._x64(inp["dy"])
         am = inp["argmax"].cpu().numpy().astype(np.int64)
         dx_old = self._x64(inp["dx"])
         if self.sample is not None:
-            n, h, w, c = inp["dx"].shape
-            am = am[self.sample] - (np.asarray(self.sample) * (h * w * c))[:, None, None, None]
+            am = am[self.sample] - self._index_shift(inp["dx"].shape)
         ref = oracle.maxpool_bwd(dy, am.astype(np.int32), dx_old.shape, dx=dx_old, beta=inp["beta"])
-        self.record("maxpool_bwd", op.name, "err", err(self._x64(out["dx"]), ref), self.bar)
+        self.record_tensor("maxpool_bwd", op.name, self._x64(out["dx"]), ref, self.dtype)
 
     def _check_apply_sgd(self, op, inp, out):
         var, grad = inp["var"].cpu().numpy(), inp["grad"].cpu().numpy()

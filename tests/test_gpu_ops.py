@@ -13,7 +13,7 @@ import torch
 
 import oracle
 from paper_1605_08695_amd import ops
-from tests.gpu_parity import BAR, err, f64, say, ulp_diff_f32
+from tests.gpu_parity import BAR, assert_close, err, f64, say, ulp_diff_f32
 
 pytestmark = pytest.mark.gpu
 
@@ -53,9 +53,7 @@ def test_conv_three_directions(case, dtype):
     torch.cuda.synchronize()
     ref = oracle.conv2d_fwd(f64(x), f64(w), (sh, sw), pads)
     assert y.shape == ref.shape
-    e = err(f64(y), ref)
-    say("  fwd err %.2e" % e)
-    assert e <= BAR[dtype]
+    assert_close(f64(y), ref, dtype, label="fwd")
 
     dy = _mk(y.shape, dtype, rng)
     for beta in (0.0, 1.0):
@@ -64,16 +62,12 @@ def test_conv_three_directions(case, dtype):
         ops.conv2d_bwd_input(dy, w, dx, (sh, sw), pads, beta=beta)
         torch.cuda.synchronize()
         ref = oracle.conv2d_bwd_input(f64(dy), f64(w), x.shape, (sh, sw), pads, dx=dx_old, beta=beta)
-        e = err(f64(dx), ref)
-        say("  bwd_input beta=%g err %.2e" % (beta, e))
-        assert e <= BAR[dtype]
+        assert_close(f64(dx), ref, dtype, label="bwd_input beta=%g" % beta)
 
     dw = ops.conv2d_bwd_filter(x, dy, (KH, KW), (sh, sw), pads)
     torch.cuda.synchronize()
     ref = oracle.conv2d_bwd_filter(f64(x), f64(dy), (KH, KW), (sh, sw), pads)
-    e = err(f64(dw), ref)
-    say("  bwd_filter err %.2e" % e)
-    assert e <= BAR[dtype]
+    assert_close(f64(dw), ref, torch.float32, dtype, label="bwd_filter")
 
 
 @pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
@@ -88,7 +82,7 @@ def test_conv_channel_slice_views(dtype):
     ops.conv2d_fwd(x, w, 1, (1, 1, 1, 1), y=y)
     torch.cuda.synchronize()
     ref = oracle.conv2d_fwd(f64(x), f64(w), 1, (1, 1, 1, 1))
-    assert err(f64(y), ref) <= BAR[dtype]
+    assert_close(f64(y), ref, dtype, label="fwd slice")
     rest = torch.cat([out[..., :16], out[..., 40:]], dim=-1)
     assert bool(torch.all(rest == 7.0))                      # neighbours untouched
     dyb = _mk((2, 9, 9, 64), dtype, rng)
@@ -98,8 +92,10 @@ def test_conv_channel_slice_views(dtype):
     ops.conv2d_bwd_input(dy, w, dx, 1, (1, 1, 1, 1))
     dw = ops.conv2d_bwd_filter(x, dy, (3, 3), 1, (1, 1, 1, 1))
     torch.cuda.synchronize()
-    assert err(f64(dx), oracle.conv2d_bwd_input(f64(dy), f64(w), x.shape, 1, (1, 1, 1, 1))) <= BAR[dtype]
-    assert err(f64(dw), oracle.conv2d_bwd_filter(f64(x), f64(dy), (3, 3), 1, (1, 1, 1, 1))) <= BAR[dtype]
+    assert_close(f64(dx), oracle.conv2d_bwd_input(f64(dy), f64(w), x.shape, 1, (1, 1, 1, 1)), dtype,
+                 label="bwd_input slice")
+    assert_close(f64(dw), oracle.conv2d_bwd_filter(f64(x), f64(dy), (3, 3), 1, (1, 1, 1, 1)), torch.float32,
+                 dtype, label="bwd_filter slice")
     assert bool(torch.all(dxb[..., :8] == 0)) and bool(torch.all(dxb[..., 40:] == 0))
 
 
@@ -120,7 +116,7 @@ def test_conv_misaligned_base_uses_scalar_path():
     w = _mk((3, 3, 16, 16), torch.bfloat16, rng, 0.2)
     y = ops.conv2d_fwd(x, w, 1, (1, 1, 1, 1))
     torch.cuda.synchronize()
-    assert err(f64(y), oracle.conv2d_fwd(f64(x), f64(w), 1, (1, 1, 1, 1))) <= BAR[torch.bfloat16]
+    assert_close(f64(y), oracle.conv2d_fwd(f64(x), f64(w), 1, (1, 1, 1, 1)), torch.bfloat16, label="misaligned")
 
 
 # ----------------------------------------------------------------------------- bias + relu
@@ -138,7 +134,7 @@ def test_bias_relu(dtype, shape, slice_):
     ops.bias_relu_fwd(y, b)
     torch.cuda.synchronize()
     got = f64(y)
-    assert err(got, oracle.bias_relu_fwd(pre, f64(b))) <= BAR[dtype]
+    assert_close(got, oracle.bias_relu_fwd(pre, f64(b)), dtype, label="bias_relu_fwd")
     assert not np.any(np.signbit(got))
     dybuf = _mk(buf.shape, dtype, rng)
     dy = dybuf if slice_ is None else dybuf[..., slice_[0]:slice_[1]]
@@ -146,8 +142,7 @@ def test_bias_relu(dtype, shape, slice_):
     dpre, db = ops.bias_relu_bwd(y, dy, dpre=dy)          # in place
     torch.cuda.synchronize()
     ref_dpre, ref_db = oracle.bias_relu_bwd(got, dy0)
-    assert err(f64(dpre), ref_dpre) <= BAR[dtype]
-    assert err(f64(db), ref_db) <= BAR[dtype]
+    assert_close(f64(db), ref_db, torch.float32, dtype, label="db")
     # exact: masked entries are exactly zero, passed entries exactly dy
     assert np.array_equal(f64(dpre), ref_dpre)
 
@@ -184,7 +179,7 @@ def test_maxpool(case, dtype, ties):
         ops.maxpool_bwd(dy, am, dx, (k, k), s, pads, beta=beta)
         torch.cuda.synchronize()
         ref = oracle.maxpool_bwd(f64(dy), ref_am, shape, dx=old, beta=beta)
-        assert err(f64(dx), ref) <= BAR[dtype]
+        assert_close(f64(dx), ref, dtype, label="maxpool_bwd beta=%g" % beta)
 
 
 @pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
@@ -203,7 +198,7 @@ def test_maxpool_slice_views(dtype):
     dx = torch.empty_like(x)
     ops.maxpool_bwd(dy, am, dx, (3, 3), 2, (0, 0, 0, 0))
     torch.cuda.synchronize()
-    assert err(f64(dx), oracle.maxpool_bwd(f64(dy), ref_am, x.shape)) <= BAR[dtype]
+    assert_close(f64(dx), oracle.maxpool_bwd(f64(dy), ref_am, x.shape), dtype, label="maxpool_bwd slice")
 
 
 # ----------------------------------------------------------------------------- sgd

@@ -21,9 +21,13 @@ from tests.gpu_parity import ParityTracer, err, f64, say, ulp_diff_f32
 pytestmark = pytest.mark.gpu
 
 
+def bitwise_equal(a, b):
+    return torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
 def _report(tr):
     for (kind, metric), (value, bar, name, _) in sorted(tr.summary().items()):
-        say("  %-16s %-16s worst %.3e (bar %.0e) at %s" % (kind, metric, value, bar, name))
+        say("  %-24s %-14s worst %.3e (bar %.0e) at %s" % (kind, metric, value, bar, name))
     bad = tr.failures()
     for b in bad[:20]:
         say("  FAIL", b)
@@ -60,7 +64,8 @@ def test_single_layer_step_end_to_end():
     say("  argmax mismatches (near-ties only):", len(mism))
     # the update, given the GPU's own gradients: within 1 ulp of the fp64 rule
     lr = float(np.float32(net.lr))
-    w_new = oracle.apply_sgd(inp.weights[c], f64(rep.dW[c]), lr)
+    w0 = inp.weights[c].astype(np.float32).astype(np.float64)     # the replica's fp32 start
+    w_new = oracle.apply_sgd(w0, f64(rep.dW[c]), lr)
     assert ulp_diff_f32(rep.W[c].cpu().numpy(), w_new) <= 1
 
 
@@ -107,6 +112,7 @@ def test_alexnet_full_size_sampled():
                          ids=["single_layer", "googlenet_b4"])
 def test_step_deterministic_and_restorable(make):
     net = make()
+    net.lr = 1e-6            # keep the linear surrogate loss from driving values to inf
     inp = W.make_inputs(net, seed=1)
     rep = Replica(net, inp)
     snap = rep.snapshot()
@@ -115,13 +121,15 @@ def test_step_deterministic_and_restorable(make):
     rep.restore(snap)
     rep.step()
     torch.cuda.synchronize()
-    assert torch.equal(p1, rep.params) and torch.equal(g1, rep.grads)
+    assert bool(torch.isfinite(rep.params).all())
+    assert bitwise_equal(p1, rep.params) and bitwise_equal(g1, rep.grads)
 
 
 def test_graph_capture_replays_match_eager():
     """The whole step captured once in a HIP graph; every replay (with eager steps and
     synchronisations in between) must equal the eager step from the same state."""
     net = W.alexnet(batch=8)
+    net.lr = 1e-6            # keep the linear surrogate loss from driving values to inf
     inp = W.make_inputs(net, seed=2)
     eager = Replica(net, inp)
     graphed = Replica(net, inp)
@@ -132,7 +140,7 @@ def test_graph_capture_replays_match_eager():
     torch.cuda.current_stream().wait_stream(s)
     eager.step()
     torch.cuda.synchronize()
-    assert torch.equal(eager.params, graphed.params)
+    assert bitwise_equal(eager.params, graphed.params)
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         graphed.step()
@@ -140,6 +148,7 @@ def test_graph_capture_replays_match_eager():
         eager.step()
         g.replay()
         torch.cuda.synchronize()
-        assert torch.equal(eager.params, graphed.params), r
-        assert torch.equal(eager.grads, graphed.grads), r
+        assert bool(torch.isfinite(eager.params).all()), r
+        assert bitwise_equal(eager.params, graphed.params), r
+        assert bitwise_equal(eager.grads, graphed.grads), r
         _ = torch.ones(1024, device="cuda").sum().item()      # unrelated eager work between replays
