@@ -17,12 +17,12 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libtfk.so")
 
-SOURCES = ["api.cpp", "eltwise.hip", "conv_fwd.hip", "conv_bwd_data.hip", "conv_bwd_filter.hip"]
+SOURCES = ["api.cpp", "eltwise.hip", "conv_fwd.hip", "conv_bwd_data.hip", "conv_bwd_filter.hip", "conv_fold.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed fp32 instructions are kept out of the generated code on purpose.
-COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function", "-fvisibility=hidden",
+COMMON = ["-O3", "-fPIC", "-std=c++20", "-Wall", "-Wno-unused-function", "-fvisibility=hidden",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-I", os.path.join(ROOT, "include")]
 

@@ -166,19 +166,19 @@ const char *tfk_status_string(tfk_status s) {
 
 // ------------------------------------------------------------------ convolution
 size_t tfk_conv2d_workspace_bytes(int32_t op, tfk_nhwc xd, int32_t cout, tfk_window p, tfk_dtype dt) {
-    if (op != 2) return 0;
+    if (op != 0 && op != 2) return 0;
     if (!valid_dt(dt) || check_view("x", xd) != TFK_OK || check_window(p) != TFK_OK || cout < 1) return 0;
     const int oh = out_len(xd.h, p.kh, p.stride_h, p.pad_top, p.pad_bottom);
     const int ow = out_len(xd.w, p.kw, p.stride_w, p.pad_left, p.pad_right);
     if (oh < 1 || ow < 1 || xd.n == 0) return 0;
     ConvShape s{xd.n, xd.h, xd.w, xd.c, oh, ow, cout, p.kh, p.kw, p.stride_h, p.stride_w, p.pad_top, p.pad_left};
-    return conv_bwd_filter_ws_bytes(dt == TFK_F32 ? 0 : 1, s);
+    const int dti = dt == TFK_F32 ? 0 : 1;
+    if (op == 0) return conv_fold_applies(dti, s) ? conv_fold_ws_bytes(0, s) : 0;
+    return conv_bwd_filter_ws_bytes(dti, s);
 }
 
 tfk_status tfk_conv2d_fwd(const void *x, tfk_nhwc xd, const void *w, int32_t cout, tfk_window p, tfk_dtype dt,
                           void *y, tfk_nhwc yd, void *ws, size_t ws_bytes, void *stream) {
-    (void)ws;
-    (void)ws_bytes;
     ConvShape s;
     TRY(check_conv(xd, cout, p, dt, yd, "x", "y", s));
     if (xd.n == 0) return ok();
@@ -192,7 +192,13 @@ tfk_status tfk_conv2d_fwd(const void *x, tfk_nhwc xd, const void *w, int32_t cou
     const int64_t yb = view_bytes(yd, es);
     if (overlap(y, yb, x, view_bytes(xd, es)) || overlap(y, yb, w, filter_bytes(s, es)))
         return fail(TFK_ERR_ALIAS, "y overlaps x or w");
-    return hip_status(launch_conv_fwd(dt == TFK_F32 ? 0 : 1, x, xd.pixel_stride, w, y, yd.pixel_stride, s,
+    const int dti = dt == TFK_F32 ? 0 : 1;
+    const size_t need = conv_fold_applies(dti, s) ? conv_fold_ws_bytes(0, s) : 0;
+    TRY(check_ws(ws, ws_bytes, need));
+    if (need && (overlap(ws, (int64_t)need, x, view_bytes(xd, es)) || overlap(ws, (int64_t)need, w, filter_bytes(s, es)) ||
+                 overlap(ws, (int64_t)need, y, yb)))
+        return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
+    return hip_status(launch_conv_fwd(dti, x, xd.pixel_stride, w, y, yd.pixel_stride, s, need ? ws : nullptr,
                                       (hipStream_t)stream),
                       "conv2d_fwd");
 }

@@ -21,6 +21,13 @@ static hipError_t conv_bwd_data_t(const void *dy, int64_t dys, const void *w, vo
     const bool vj = s.K % EPC == 0 && dys % EPC == 0 && aligned16p(dy);
     // largest phase: ceil(H / sh) x ceil(W / sw) pixels per image
     const int mj = s.N * ((s.H + s.sh - 1) / s.sh) * ((s.W + s.sw - 1) / s.sw);
+    if constexpr (sizeof(T) == 2) {
+        if (vi && vj && s.C % 8 == 0 && dxs % 8 == 0 && aligned16p(dx)) {
+            int bi, bj;
+            igemm2_tiles(a.NI, mj, s.sh * s.sw, &bi, &bj);
+            return igemm2_launch<DIR_BWD_DATA>(a, mj, s.sh * s.sw, bi, bj, st);
+        }
+    }
     return igemm_launch<T, DIR_BWD_DATA>(a, mj, s.sh * s.sw, vi, vj, st);
 }
 

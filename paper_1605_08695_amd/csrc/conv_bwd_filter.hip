@@ -4,55 +4,104 @@
 
 namespace tfk {
 
-void conv_bwd_filter_plan(int dt, const ConvShape &s, int *splits, int *k_split) {
+namespace {
+
+struct BwfPlan {
+    int bi, bj, splits, k_split;
+};
+
+// Tiles and split-K of one bwd-filter launch.  The pipelined bf16 kernel (v2)
+// runs one block per CU, so it aims at about one block per CU in total; the
+// register-staged kernel runs two per CU.
+BwfPlan bwf_plan(int dt, const ConvShape &s, bool v2) {
+    BwfPlan p;
     const int bk = dt == 0 ? 32 : 64;
     const int m = s.KH * s.KW * s.C;
-    const int bi = igemm_bi(s.K);
-    const int tiles = ((s.K + bi - 1) / bi) * ((m + 127) / 128);
+    if (v2) {
+        p.bi = s.K <= 64 ? 64 : 128;
+        p.bj = m >= 2048 ? 256 : 128;
+    } else {
+        p.bi = igemm_bi(s.K);
+        p.bj = 128;
+    }
+    const int tiles = ((s.K + p.bi - 1) / p.bi) * ((m + p.bj - 1) / p.bj);
     const int64_t ktot = (int64_t)s.N * s.OH * s.OW;
     const int64_t ktiles = (ktot + bk - 1) / bk;
-    int64_t sp = (512 + tiles - 1) / tiles;            // about two blocks per CU
+    const int target = v2 ? 256 : 512;
+    int64_t sp = (target + tiles - 1) / tiles;
     const int64_t max_sp = std::max<int64_t>(1, ktiles / 8);   // at least 8 K tiles per split
     sp = std::max<int64_t>(1, std::min<int64_t>(sp, max_sp));
     sp = std::min<int64_t>(sp, 4096);
-    int64_t per = (ktiles + sp - 1) / sp;              // K tiles per split
-    *k_split = (int)(per * bk);
-    *splits = (int)((ktiles + per - 1) / per);
+    const int64_t per = (ktiles + sp - 1) / sp;                 // K tiles per split
+    p.k_split = (int)(per * bk);
+    p.splits = (int)((ktiles + per - 1) / per);
+    return p;
+}
+
+size_t plan_ws(const ConvShape &s, const BwfPlan &p) {
+    if (p.splits <= 1) return 0;
+    return (size_t)p.splits * (size_t)s.KH * s.KW * s.C * s.K * sizeof(float);
+}
+
+}  // namespace
+
+void conv_bwd_filter_plan(int dt, const ConvShape &s, int *splits, int *k_split) {
+    const BwfPlan p = bwf_plan(dt, s, false);
+    *splits = p.splits;
+    *k_split = p.k_split;
 }
 
 size_t conv_bwd_filter_ws_bytes(int dt, const ConvShape &s) {
-    int splits, k_split;
-    conv_bwd_filter_plan(dt, s, &splits, &k_split);
-    if (splits <= 1) return 0;
-    return (size_t)splits * (size_t)s.KH * s.KW * s.C * s.K * sizeof(float);
+    size_t need = plan_ws(s, bwf_plan(dt, s, false));
+    if (dt == 1) need = std::max(need, plan_ws(s, bwf_plan(dt, s, true)));
+    if (conv_fold_applies(dt, s)) need = std::max(need, conv_fold_ws_bytes(2, s));
+    return need;
 }
 
 template <typename T>
 static hipError_t conv_bwd_filter_t(const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,
                                     const ConvShape &s, void *ws, hipStream_t st) {
     constexpr int EPC = Elem<T>::kPerChunk;
+    const int dti = sizeof(T) == 4 ? 0 : 1;
     IgArgs a;
     fill_geom(a, s);
-    int splits, k_split;
-    conv_bwd_filter_plan(sizeof(T) == 4 ? 0 : 1, s, &splits, &k_split);
     const int64_t mn = (int64_t)s.KH * s.KW * s.C * s.K;
+    const int m = s.KH * s.KW * s.C;
     a.src_i = dy;
     a.src_j = x;
-    a.out = splits > 1 ? ws : (void *)dw;
     a.xs = xs;
     a.ys = dys;
     a.NI = s.K;
-    a.k_split = k_split;
     a.split_stride = mn;
     const bool vi = s.K % EPC == 0 && dys % EPC == 0 && aligned16p(dy);
     const bool vj = s.C % EPC == 0 && xs % EPC == 0 && aligned16p(x);
-    hipError_t e = igemm_launch<T, DIR_BWD_FILTER>(a, s.KH * s.KW * s.C, splits, vi, vj, st);
-    if (e != hipSuccess || splits <= 1) return e;
-    return launch_sum_splits(reinterpret_cast<const float *>(ws), splits, mn, dw, st);
+    hipError_t e;
+    BwfPlan p;
+    bool v2 = false;
+    if constexpr (sizeof(T) == 2) {
+        if (vi && vj) {
+            p = bwf_plan(dti, s, true);
+            v2 = p.splits > 1 || aligned16p(dw);
+        }
+    }
+    if (v2) {
+        a.out = p.splits > 1 ? ws : (void *)dw;
+        a.k_split = p.k_split;
+        e = igemm2_launch<DIR_BWD_FILTER>(a, m, p.splits, p.bi, p.bj, st);
+    } else {
+        p = bwf_plan(dti, s, false);
+        a.out = p.splits > 1 ? ws : (void *)dw;
+        a.k_split = p.k_split;
+        e = igemm_launch<T, DIR_BWD_FILTER>(a, m, p.splits, vi, vj, st);
+    }
+    if (e != hipSuccess || p.splits <= 1) return e;
+    return launch_sum_splits(reinterpret_cast<const float *>(ws), p.splits, mn, dw, st);
 }
 
 hipError_t launch_conv_bwd_filter(int dt, const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,
                                   const ConvShape &s, void *ws, hipStream_t st) {
+    if (conv_fold_applies(dt, s) && dys % 8 == 0 && ((uintptr_t)dy & 15) == 0 && ((uintptr_t)ws & 15) == 0)
+        return launch_conv_bwd_filter_folded(x, xs, dy, dys, dw, s, ws, st);
     return dt == 0 ? conv_bwd_filter_t<float>(x, xs, dy, dys, dw, s, ws, st)
                    : conv_bwd_filter_t<bf16_t>(x, xs, dy, dys, dw, s, ws, st);
 }

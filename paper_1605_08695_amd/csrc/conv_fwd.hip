@@ -17,11 +17,21 @@ static hipError_t conv_fwd_t(const void *x, int64_t xs, const void *w, void *y, 
     a.NI = s.K;
     const bool vi = s.K % EPC == 0 && aligned16p(w);
     const bool vj = s.C % EPC == 0 && xs % EPC == 0 && aligned16p(x);
-    return igemm_launch<T, DIR_FWD>(a, s.N * s.OH * s.OW, 1, vi, vj, st);
+    const int mj = s.N * s.OH * s.OW;
+    if constexpr (sizeof(T) == 2) {
+        if (vi && vj && ys % 8 == 0 && aligned16p(y)) {
+            int bi, bj;
+            igemm2_tiles(a.NI, mj, 1, &bi, &bj);
+            return igemm2_launch<DIR_FWD>(a, mj, 1, bi, bj, st);
+        }
+    }
+    return igemm_launch<T, DIR_FWD>(a, mj, 1, vi, vj, st);
 }
 
 hipError_t launch_conv_fwd(int dt, const void *x, int64_t xs, const void *w, void *y, int64_t ys,
-                           const ConvShape &s, hipStream_t st) {
+                           const ConvShape &s, void *ws, hipStream_t st) {
+    if (ws != nullptr && conv_fold_applies(dt, s) && ((uintptr_t)y & 15) == 0 && ys % 8 == 0)
+        return launch_conv_fwd_folded(x, xs, w, y, ys, s, ws, st);
     return dt == 0 ? conv_fwd_t<float>(x, xs, w, y, ys, s, st) : conv_fwd_t<bf16_t>(x, xs, w, y, ys, s, st);
 }
 

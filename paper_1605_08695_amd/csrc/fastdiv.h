@@ -17,10 +17,10 @@ struct FastDiv {
     uint32_t mul;    // magic multiplier
     uint32_t shift;  // post-shift
 
-    FastDiv() : d(1), mul(1), shift(0) {}
-    explicit FastDiv(uint32_t divisor) { init(divisor); }
+    TFK_HD FastDiv() : d(1), mul(1), shift(0) {}
+    TFK_HD explicit FastDiv(uint32_t divisor) { init(divisor); }
 
-    void init(uint32_t divisor) {
+    TFK_HD void init(uint32_t divisor) {
         d = divisor ? divisor : 1;
         uint32_t l = 0;
         while ((1ull << l) < d) ++l;                       // l = ceil(log2 d)

@@ -60,7 +60,7 @@ struct IgArgs {
     int tiles_i;         // number of I tiles (blockIdx.x = tj * tiles_i + ti)
     int k_split;         // BWD_FILTER: reduction elements per split (multiple of the K tile)
     int64_t split_stride;// BWD_FILTER: floats between consecutive partial outputs
-    FastDiv dC, dKW, dOW, dOH;
+    FastDiv dC, dKW, dOW, dOH, dK;
 };
 
 template <typename T> struct Mfma;

@@ -2,6 +2,7 @@
 // selection and grid shape.
 #pragma once
 #include "igemm.h"
+#include "igemm2.h"
 #include "kernels.h"
 
 namespace tfk {
@@ -36,6 +37,31 @@ static hipError_t igemm_launch(IgArgs &a, int mj, int zdim, bool vi, bool vj, hi
     return hipGetLastError();
 }
 
+// Pipelined bf16 kernel: I tile of 64 or 128 channels, J tile of 128 or 256 rows
+// (the larger J tile when it still yields about one block per CU).
+static inline void igemm2_tiles(int ni, int mj, int zdim, int *bi, int *bj) {
+    *bi = ni <= 64 ? 64 : 128;
+    const int ti = (ni + *bi - 1) / *bi;
+    const int64_t blocks256 = (int64_t)ti * ((mj + 255) / 256) * zdim;
+    *bj = blocks256 >= 240 ? 256 : 128;
+}
+
+template <int DIR>
+static hipError_t igemm2_launch(IgArgs &a, int mj, int zdim, int bi, int bj, hipStream_t st) {
+    a.tiles_i = (a.NI + bi - 1) / bi;
+    const int tiles_j = (mj + bj - 1) / bj;
+    const dim3 grid((unsigned)(a.tiles_i * tiles_j), 1, (unsigned)zdim);
+    if (bi == 64 && bj == 128)
+        hipLaunchKernelGGL((igemm2_kernel<DIR, 64, 128>), grid, dim3(512), 0, st, a);
+    else if (bi == 64)
+        hipLaunchKernelGGL((igemm2_kernel<DIR, 64, 256>), grid, dim3(512), 0, st, a);
+    else if (bj == 128)
+        hipLaunchKernelGGL((igemm2_kernel<DIR, 128, 128>), grid, dim3(512), 0, st, a);
+    else
+        hipLaunchKernelGGL((igemm2_kernel<DIR, 128, 256>), grid, dim3(512), 0, st, a);
+    return hipGetLastError();
+}
+
 static inline void fill_geom(IgArgs &a, const ConvShape &s) {
     a.N = s.N; a.H = s.H; a.W = s.W; a.C = s.C;
     a.OH = s.OH; a.OW = s.OW; a.K = s.K;
@@ -44,6 +70,7 @@ static inline void fill_geom(IgArgs &a, const ConvShape &s) {
     a.dKW.init((uint32_t)s.KW);
     a.dOW.init((uint32_t)s.OW);
     a.dOH.init((uint32_t)s.OH);
+    a.dK.init((uint32_t)s.K);
     a.beta = 0.f;
     a.k_split = 0;
     a.split_stride = 0;

@@ -34,7 +34,7 @@ struct SgdBatch {
 
 // dt: 0 = fp32, 1 = bf16
 hipError_t launch_conv_fwd(int dt, const void *x, int64_t xs, const void *w, void *y, int64_t ys,
-                           const ConvShape &s, hipStream_t st);
+                           const ConvShape &s, void *ws, hipStream_t st);
 hipError_t launch_conv_bwd_data(int dt, const void *dy, int64_t dys, const void *w, void *dx, int64_t dxs,
                                 float beta, const ConvShape &s, hipStream_t st);
 hipError_t launch_conv_bwd_filter(int dt, const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,
@@ -42,6 +42,13 @@ hipError_t launch_conv_bwd_filter(int dt, const void *x, int64_t xs, const void 
 // Split-K plan of bwd-filter: number of splits and reduction elements per split.
 void conv_bwd_filter_plan(int dt, const ConvShape &s, int *splits, int *k_split);
 size_t conv_bwd_filter_ws_bytes(int dt, const ConvShape &s);
+// bf16 convolutions with C % 8 != 0 run as an equivalent 8-channel convolution (conv_fold.hip).
+bool conv_fold_applies(int dt, const ConvShape &s);
+size_t conv_fold_ws_bytes(int op, const ConvShape &s);
+hipError_t launch_conv_fwd_folded(const void *x, int64_t xs, const void *w, void *y, int64_t ys, const ConvShape &s,
+                                  void *ws, hipStream_t st);
+hipError_t launch_conv_bwd_filter_folded(const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,
+                                         const ConvShape &s, void *ws, hipStream_t st);
 
 hipError_t launch_bias_relu_fwd(int dt, void *y, int64_t P, int C, int64_t ys, const float *bias, hipStream_t st);
 void relu_bwd_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *ppb);

@@ -78,19 +78,22 @@ def conv2d_workspace_bytes(op: int, x: torch.Tensor, cout: int, kh, kw, stride, 
     return load().tfk_conv2d_workspace_bytes(op, nhwc(x), cout, window(kh, kw, stride, pads), _dt(x))
 
 
-def conv2d_fwd(x, w, stride, pads, y=None, stream=None):
+def conv2d_fwd(x, w, stride, pads, y=None, ws=None, stream=None):
     """y = x (*) w (cross-correlation).  x NHWC, w HWIO, pads (top, bottom, left, right)."""
     lib = load()
     kh, kw, cin, cout = w.shape
     win = window(kh, kw, stride, pads)
+    need = lib.tfk_conv2d_workspace_bytes(0, nhwc(x), cout, win, _dt(x))
+    if need and (ws is None or ws.numel() < need):
+        ws = _ws(need, x.device)
     if y is None:
         n, h, ww, _ = x.shape
         y = torch.empty((n, out_len(h, kh, win.stride_h, pads[0], pads[1]),
                          out_len(ww, kw, win.stride_w, pads[2], pads[3]), cout), dtype=x.dtype, device=x.device)
     if w.dtype != x.dtype or y.dtype != x.dtype:
         raise TypeError("x, w and y must share one dtype")
-    check(lib.tfk_conv2d_fwd(_ptr(x), nhwc(x), _ptr(w), cout, win, _dt(x), _ptr(y), nhwc(y), None, 0,
-                             _stream(stream)))
+    check(lib.tfk_conv2d_fwd(_ptr(x), nhwc(x), _ptr(w), cout, win, _dt(x), _ptr(y), nhwc(y),
+                             _ptr(ws) if need else None, need, _stream(stream)))
     return y
 
 

@@ -105,7 +105,8 @@ class Replica:
         need = 0
         for c in net.convs:
             x = self.act[c.src]
-            need = max(need, ops.conv2d_workspace_bytes(2, x, c.cout, c.kh, c.kw, (c.sh, c.sw), c.pads))
+            for op_kind in (0, 2):
+                need = max(need, ops.conv2d_workspace_bytes(op_kind, x, c.cout, c.kh, c.kw, (c.sh, c.sw), c.pads))
             need = max(need, ops.bias_relu_bwd_workspace_bytes(self._slice(self.act, c)))
         self.ws = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=dev)
 
@@ -124,7 +125,7 @@ class Replica:
             y = self._slice(self.act, op)
             if isinstance(op, Conv):
                 if trace: trace("conv_fwd", op, x=x, w=self.Wlp[op.name], y=y)
-                ops.conv2d_fwd(x, self.Wlp[op.name], (op.sh, op.sw), op.pads, y=y, stream=stream)
+                ops.conv2d_fwd(x, self.Wlp[op.name], (op.sh, op.sw), op.pads, y=y, ws=self.ws, stream=stream)
                 if trace: trace("conv_fwd:end", op, y=y)
                 if trace: trace("bias_relu_fwd", op, y=y, b=self.b[op.name])
                 ops.bias_relu_fwd(y, self.b[op.name], stream=stream)

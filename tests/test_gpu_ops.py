@@ -25,6 +25,8 @@ CONV_CASES = [
     ("single_layer", 8, 32, 32, 16, 32, 3, 3, 1, 1, (1, 1, 1, 1)),
     ("ragged_tiles", 3, 13, 11, 24, 136, 3, 3, 1, 1, (1, 1, 1, 1)),
     ("cin3_11x11s4", 2, 35, 35, 3, 64, 11, 11, 4, 4, (2, 2, 2, 2)),
+    ("cin3_11x11s4_pairfold", 2, 36, 40, 3, 64, 11, 11, 4, 4, (2, 2, 2, 2)),
+    ("cin3_3x3s2_valid_oddw", 2, 15, 17, 3, 32, 3, 3, 2, 2, (0, 0, 0, 0)),
     ("3x3s2_valid", 2, 17, 17, 32, 48, 3, 3, 2, 2, (0, 0, 0, 0)),
     ("1x7_asym", 2, 9, 9, 16, 24, 1, 7, 1, 1, (0, 0, 3, 3)),
     ("7x1_asym", 2, 9, 9, 16, 24, 7, 1, 1, 1, (3, 3, 0, 0)),
