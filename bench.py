@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=128, help="images of the batch the oracle steps through")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="only run a plain copy kernel over this many MiB (HBM counter calibration) and exit")
     return ap.parse_args()
 
 
@@ -63,6 +65,31 @@ def elementwise_bytes(net, op_kind, op, D):
         ny = int(np.prod(t[op.dst][:3])) * t[op.src][3]
         return ny * (D + 4) + nx * D
     raise KeyError(op_kind)
+
+
+def kernel_source_sha():
+    """Hash of the HIP sources: HBM counters recorded for other sources are not reported."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1605_08695_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            h.update(name.encode())
+            h.update(open(os.path.join(csrc, name), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(kind):
+    """HBM bytes per launch of the dominant kernel measured with rocprofv3 --pmc (FETCH_SIZE and
+    WRITE_SIZE, scaled by a plain-copy calibration), if recorded for the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", "alexnet_b128_conv_traffic.json")
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha") != kernel_source_sha():
+        return None
+    return rec.get("bytes_per_launch", {}).get(kind)
 
 
 def conv_flops(net, op):
@@ -104,6 +131,16 @@ def main():
     from paper_1605_08695_amd.step import Replica
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.calibrate_copy_mib:
+        # A plain elementwise copy of known size: reads and writes n * 4 bytes per launch.
+        n = args.calibrate_copy_mib * (1 << 20) // 4
+        a = torch.ones(n, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            torch.neg(a, out=b)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration_copy_bytes_read": n * 4, "calibration_copy_bytes_written": n * 4}))
+        return
     net = W.alexnet(batch=args.batch)
     inp = W.make_inputs(net, seed=args.seed)
     rep = Replica(net, inp)
@@ -239,7 +276,7 @@ def main():
                      "achieved": round(flops[dom] / (per_kind[dom] * 1e-3) / 1e12, 1),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(flops[dom] / (per_kind[dom] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None,
+                     "traffic": recorded_traffic(dom),
                      "avg_launch_us": round(per_kind[dom] * 1e3 / n_dom, 2),
                      "flop_per_launch": round(flops[dom] / n_dom)},
         "cpu_baseline": cpu,
