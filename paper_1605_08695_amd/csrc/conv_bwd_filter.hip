@@ -10,16 +10,17 @@ struct BwfPlan {
     int bi, bj, splits, k_split;
 };
 
-// Tiles and split-K of one bwd-filter launch.  The pipelined bf16 kernel (v2)
-// runs one block per CU, so it aims at about one block per CU in total; the
-// register-staged kernel runs two per CU.
+// Tiles and split-K of one bwd-filter launch.  The pipelined bf16 kernel (v2) runs
+// one block per CU; a sweep over the AlexNet/VGG shapes favours 128-row tap tiles and
+// about two blocks per CU in total (splitting the pixel reduction further than one
+// round hides the copies of one block behind the MFMAs of the next).
 BwfPlan bwf_plan(int dt, const ConvShape &s, bool v2) {
     BwfPlan p;
     const int bk = dt == 0 ? 32 : 64;
     const int m = s.KH * s.KW * s.C;
     if (v2) {
-        p.bi = s.K <= 64 ? 64 : 128;
-        p.bj = m >= 2048 ? 256 : 128;
+        p.bi = (s.K % 128 == 0) ? 128 : 64;
+        p.bj = 128;
     } else {
         p.bi = igemm_bi(s.K);
         p.bj = 128;
@@ -27,7 +28,7 @@ BwfPlan bwf_plan(int dt, const ConvShape &s, bool v2) {
     const int tiles = ((s.K + p.bi - 1) / p.bi) * ((m + p.bj - 1) / p.bj);
     const int64_t ktot = (int64_t)s.N * s.OH * s.OW;
     const int64_t ktiles = (ktot + bk - 1) / bk;
-    const int target = v2 ? 256 : 512;
+    const int target = 512;
     int64_t sp = (target + tiles - 1) / tiles;
     const int64_t max_sp = std::max<int64_t>(1, ktiles / 8);   // at least 8 K tiles per split
     sp = std::max<int64_t>(1, std::min<int64_t>(sp, max_sp));

@@ -92,7 +92,78 @@ __global__ __launch_bounds__(256) void unfold_filter_grad_kernel(const float *__
     }
 }
 
+// Dense input, 8 pixels per thread: 8 C elements arrive as C 16-byte loads and leave
+// as Cp 16-byte stores (C, Cp <= 8); the last npix % 8 pixels take the kernel above.
+template <int C, int Cp>
+__global__ __launch_bounds__(256) void pad_channels_vec_kernel(const bf16_t *__restrict__ x, int64_t groups,
+                                                               bf16_t *__restrict__ xp) {
+    for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < groups;
+         g += (int64_t)gridDim.x * blockDim.x) {
+        uint32_t in[32];
+        const U4 *src = reinterpret_cast<const U4 *>(x + g * 8 * C);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            if (q < C) {
+                const U4 v = src[q];
+                in[4 * q] = v.x; in[4 * q + 1] = v.y; in[4 * q + 2] = v.z; in[4 * q + 3] = v.w;
+            }
+        }
+        U4 *dst = reinterpret_cast<U4 *>(xp + g * 8 * Cp);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            if (q < Cp) {
+                uint32_t o[4];
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    uint32_t word = 0;
+#pragma unroll
+                    for (int half = 0; half < 2; ++half) {
+                        const int e = (q * 4 + h) * 2 + half;       // output element within the 8 pixels
+                        const int pix = e / Cp, c = e % Cp;
+                        if (c < C) {
+                            const int i = pix * C + c;              // input element
+                            const uint32_t bits = (in[i >> 1] >> ((i & 1) * 16)) & 0xffffu;
+                            word |= bits << (half * 16);
+                        }
+                    }
+                    o[h] = word;
+                }
+                U4 v;
+                v.x = o[0]; v.y = o[1]; v.z = o[2]; v.w = o[3];
+                dst[q] = v;
+            }
+        }
+    }
+}
+
 int grid_of(int64_t n) { return (int)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, 16384)); }
+
+template <int C, int Cp>
+bool pad_vec(const bf16_t *x, int64_t groups, bf16_t *xp, hipStream_t st) {
+    hipLaunchKernelGGL((pad_channels_vec_kernel<C, Cp>), dim3(grid_of(groups)), dim3(256), 0, st, x, groups, xp);
+    return true;
+}
+
+// The 16-byte path for the channel counts of image inputs.
+bool pad_vec_dispatch(int C, int Cp, const bf16_t *x, int64_t groups, bf16_t *xp, hipStream_t st) {
+    if (C == 3 && Cp == 4) return pad_vec<3, 4>(x, groups, xp, st);
+    if (C == 3 && Cp == 8) return pad_vec<3, 8>(x, groups, xp, st);
+    if (C == 1 && Cp == 8) return pad_vec<1, 8>(x, groups, xp, st);
+    if (C == 1 && Cp == 1) return pad_vec<1, 1>(x, groups, xp, st);
+    if (C == 4 && Cp == 8) return pad_vec<4, 8>(x, groups, xp, st);
+    return false;
+}
+
+void pad_channels(const void *x, int64_t npix, int C, int64_t xs, int Cp, bf16_t *xp, hipStream_t st) {
+    const bf16_t *xb = reinterpret_cast<const bf16_t *>(x);
+    int64_t done = 0;
+    const int64_t groups = npix / 8;
+    if (xs == C && ((uintptr_t)x & 15) == 0 && groups > 0 && pad_vec_dispatch(C, Cp, xb, groups, xp, st))
+        done = groups * 8;
+    if (done < npix)
+        hipLaunchKernelGGL(pad_channels_kernel, dim3(grid_of((npix - done) * Cp)), dim3(256), 0, st,
+                           xb + done * xs, npix - done, C, xs, Cp, xp + done * Cp);
+}
 
 }  // namespace
 
@@ -119,8 +190,7 @@ hipError_t launch_conv_fwd_folded(const void *x, int64_t xs, const void *w, void
     bf16_t *xp = reinterpret_cast<bf16_t *>(base);
     bf16_t *wv = reinterpret_cast<bf16_t *>(base + align256((size_t)s.N * s.H * s.W * f.Cp * 2));
     const int64_t npix = (int64_t)s.N * s.H * s.W;
-    hipLaunchKernelGGL(pad_channels_kernel, dim3(grid_of(npix * f.Cp)), dim3(256), 0, st,
-                       reinterpret_cast<const bf16_t *>(x), npix, s.C, xs, f.Cp, xp);
+    pad_channels(x, npix, s.C, xs, f.Cp, xp, st);
     hipLaunchKernelGGL(fold_filter_kernel, dim3(grid_of((int64_t)s.KH * f.v.KW * 8 * s.K)), dim3(256), 0, st,
                        reinterpret_cast<const bf16_t *>(w), s.KH, s.KW, s.C, s.K, f.F, f.Cp, f.v.KW, wv);
     hipError_t e = hipGetLastError();
@@ -139,8 +209,7 @@ hipError_t launch_conv_bwd_filter_folded(const void *x, int64_t xs, const void *
     float *dwv = reinterpret_cast<float *>(base + xb);
     void *ws2 = base + xb + align256(wvn * 4);
     const int64_t npix = (int64_t)s.N * s.H * s.W;
-    hipLaunchKernelGGL(pad_channels_kernel, dim3(grid_of(npix * f.Cp)), dim3(256), 0, st,
-                       reinterpret_cast<const bf16_t *>(x), npix, s.C, xs, f.Cp, xp);
+    pad_channels(x, npix, s.C, xs, f.Cp, xp, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     e = launch_conv_bwd_filter(1, xp, 8, dy, dys, dwv, f.v, ws2, st);

@@ -19,7 +19,7 @@
 //    XOR-swizzled by (row & 7) and read with ds_read_b128.  Operands that are
 //    contiguous along the row axis (the filter in the forward pass, both
 //    operands of bwd-filter) are kept k-major, [k][row], exactly as they sit
-//    in memory, with chunks swizzled by 2 (k & 3); the MFMA fragment (eight
+//    in memory, with chunks swizzled by k (kmajor_swz); the MFMA fragment (eight
 //    consecutive k of one row per lane) is assembled by two ds_read_b64_tr_b16
 //    transposing reads.  No operand is transposed in registers.
 //
@@ -68,18 +68,30 @@ __device__ __forceinline__ U4 lds_tr_pair(const unsigned char *p0, const unsigne
         (__attribute__((address_space(3))) s16x4_t *)(p0));
     const s16x4_t b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
         (__attribute__((address_space(3))) s16x4_t *)(p1));
+    // Four 16-bit elements already packed in two dwords (element 0 in the low half).
+    const uint2 ua = __builtin_bit_cast(uint2, a);
+    const uint2 ub = __builtin_bit_cast(uint2, b);
     U4 r;
-    r.x = (uint32_t)(uint16_t)a[0] | ((uint32_t)(uint16_t)a[1] << 16);
-    r.y = (uint32_t)(uint16_t)a[2] | ((uint32_t)(uint16_t)a[3] << 16);
-    r.z = (uint32_t)(uint16_t)b[0] | ((uint32_t)(uint16_t)b[1] << 16);
-    r.w = (uint32_t)(uint16_t)b[2] | ((uint32_t)(uint16_t)b[3] << 16);
+    r.x = ua.x; r.y = ua.y; r.z = ub.x; r.w = ub.y;
     return r;
 }
 
-// Byte offset of element (k, row) of a k-major tile with R rows (row even, in-chunk aligned by 4).
+// Chunk swizzle of k-row k in a k-major tile with R rows.  A transposing read of a
+// 16-lane group touches 32 bytes (two chunks) of 4 consecutive k-rows, and two groups
+// (k-rows 8g + 0..3 and 8g + 8..11) are served together: 2 (k & 3) spreads the 4 rows
+// of a group over distinct chunk pairs and bit 3 of k moves the second group to the
+// other half of the banks (for 64-row tiles, whose k-rows are 128 bytes, it moves the
+// group to the free chunk pairs instead).
+template <int R>
+__device__ __forceinline__ int kmajor_swz(int k) {
+    if constexpr (R == 64) return ((k & 3) ^ ((k >> 3) & 1)) << 1;
+    else return ((k & 3) << 1) ^ (((k >> 3) & 1) << 3);
+}
+
+// Byte offset of element (k, row) of a k-major tile with R rows (row a multiple of 4).
 template <int R>
 __device__ __forceinline__ int kmajor_off(int k, int row) {
-    return k * (R * 2) + ((((row >> 3) ^ ((k & 3) << 1))) << 4) + ((row & 7) << 1);
+    return k * (R * 2) + (((row >> 3) ^ kmajor_swz<R>(k)) << 4) + ((row & 7) << 1);
 }
 
 template <int DIR, int BI, int BJ>
@@ -143,7 +155,7 @@ __global__ __launch_bounds__(512, 1) void igemm2_kernel(const IgArgs a) {
     // [row][k] operands: copy r of this thread covers row 8 slot + lane/8, slot = wave*NL_op + r,
     // and the logical chunk (lane & 7) ^ (lane >> 3); it lands at byte 1024 slot of the tile.
     // k-major operands with R rows: copy r covers k-row slot (512/R) + lane / (R/8) and row
-    // chunk (lane % (R/8)) ^ 2 (k-row & 3).  Everything that does not depend on the K tile is
+    // chunk (lane % (R/8)) ^ kmajor_swz(k-row).  Everything that does not depend on the K tile is
     // computed here once.
     const int dchunk = (lane & 7) ^ (lane >> 3);
 
@@ -195,7 +207,7 @@ __global__ __launch_bounds__(512, 1) void igemm2_kernel(const IgArgs a) {
 #pragma unroll
         for (int r = 0; r < NLI; ++r) {
             const int krow = (wave * NLI + r) * (512 / BI) + lane / CPR;
-            const int co = i0 + ((lane % CPR) ^ ((krow & 3) << 1)) * 8;
+            const int co = i0 + ((lane % CPR) ^ kmajor_swz<BI>(krow)) * 8;
             iok[r] = co < a.NI;
             tik[r] = krow;
             iptr[r] = srcI + (int64_t)(k_beg + krow) * ld + (iok[r] ? co : 0);
@@ -209,7 +221,7 @@ __global__ __launch_bounds__(512, 1) void igemm2_kernel(const IgArgs a) {
 #pragma unroll
         for (int r = 0; r < NLJ; ++r) {
             const int krow = (wave * NLJ + r) * (512 / BJ) + lane / CPR;
-            const int c = (lane % CPR) ^ ((krow & 3) << 1);
+            const int c = (lane % CPR) ^ kmajor_swz<BJ>(krow);
             const int r0 = j0 + c * 8;
             fr_ok[r] = r0 < MJ_ext;
             const int rr = fr_ok[r] ? r0 : 0;

@@ -37,13 +37,19 @@ static hipError_t igemm_launch(IgArgs &a, int mj, int zdim, bool vi, bool vj, hi
     return hipGetLastError();
 }
 
-// Pipelined bf16 kernel: I tile of 64 or 128 channels, J tile of 128 or 256 rows
-// (the larger J tile when it still yields about one block per CU).
+// Tiles of the pipelined bf16 kernel (one block per CU), chosen from a sweep over the
+// AlexNet/VGG layer shapes on MI355X: 128-channel I tiles when the channel count is a
+// multiple of 128 (else 64, so 192 channels waste nothing), paired with 256-row J tiles;
+// 64-channel tiles take 256 rows only when that fits one round of blocks on the 256 CUs.
 static inline void igemm2_tiles(int ni, int mj, int zdim, int *bi, int *bj) {
-    *bi = ni <= 64 ? 64 : 128;
-    const int ti = (ni + *bi - 1) / *bi;
+    *bi = (ni % 128 == 0) ? 128 : 64;
+    if (*bi == 128) {
+        *bj = 256;
+        return;
+    }
+    const int ti = (ni + 63) / 64;
     const int64_t blocks256 = (int64_t)ti * ((mj + 255) / 256) * zdim;
-    *bj = blocks256 >= 240 ? 256 : 128;
+    *bj = blocks256 <= 256 ? 256 : 128;
 }
 
 template <int DIR>
