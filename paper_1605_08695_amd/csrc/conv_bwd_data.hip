@@ -23,9 +23,9 @@ static hipError_t conv_bwd_data_t(const void *dy, int64_t dys, const void *w, vo
     const int mj = s.N * ((s.H + s.sh - 1) / s.sh) * ((s.W + s.sw - 1) / s.sw);
     if constexpr (sizeof(T) == 2) {
         if (vi && vj && s.C % 8 == 0 && dxs % 8 == 0 && aligned16p(dx)) {
-            int bi, bj;
-            igemm2_tiles(a.NI, mj, s.sh * s.sw, &bi, &bj);
-            return igemm2_launch<DIR_BWD_DATA>(a, mj, s.sh * s.sw, bi, bj, st);
+            const int z = s.sh * s.sw;
+            if (!igemm2_launch<DIR_BWD_DATA>(a, mj, z, igemm2_tiles(a.NI, mj, z), st)) return hipErrorInvalidValue;
+            return hipGetLastError();
         }
     }
     return igemm_launch<T, DIR_BWD_DATA>(a, mj, s.sh * s.sw, vi, vj, st);

@@ -8,19 +8,20 @@ namespace {
 
 struct BwfPlan {
     int bi, bj, splits, k_split;
+    Igemm2Tile t;      // configuration of the pipelined bf16 kernel
 };
 
-// Tiles and split-K of one bwd-filter launch.  The pipelined bf16 kernel (v2) runs
-// one block per CU; a sweep over the AlexNet/VGG shapes favours 128-row tap tiles and
-// about two blocks per CU in total (splitting the pixel reduction further than one
-// round hides the copies of one block behind the MFMAs of the next).
+// Tiles and split-K of one bwd-filter launch, chosen from sweeps over the AlexNet/VGG
+// shapes: 128-row tap tiles, and the pixel reduction split until there are about two
+// rounds of blocks (one round leaves the last copies of every block exposed).
 BwfPlan bwf_plan(int dt, const ConvShape &s, bool v2) {
     BwfPlan p;
     const int bk = dt == 0 ? 32 : 64;
     const int m = s.KH * s.KW * s.C;
     if (v2) {
-        p.bi = (s.K % 128 == 0) ? 128 : 64;
-        p.bj = 128;
+        p.t = (s.K % 128 == 0) ? Igemm2Tile{128, 128, 4, 2} : Igemm2Tile{64, 128, 4, 2};
+        p.bi = p.t.bi;
+        p.bj = p.t.bj;
     } else {
         p.bi = igemm_bi(s.K);
         p.bj = 128;
@@ -28,7 +29,7 @@ BwfPlan bwf_plan(int dt, const ConvShape &s, bool v2) {
     const int tiles = ((s.K + p.bi - 1) / p.bi) * ((m + p.bj - 1) / p.bj);
     const int64_t ktot = (int64_t)s.N * s.OH * s.OW;
     const int64_t ktiles = (ktot + bk - 1) / bk;
-    const int target = 512;
+    const int target = v2 ? 1024 : 512;
     int64_t sp = (target + tiles - 1) / tiles;
     const int64_t max_sp = std::max<int64_t>(1, ktiles / 8);   // at least 8 K tiles per split
     sp = std::max<int64_t>(1, std::min<int64_t>(sp, max_sp));
@@ -88,7 +89,7 @@ static hipError_t conv_bwd_filter_t(const void *x, int64_t xs, const void *dy, i
     if (v2) {
         a.out = p.splits > 1 ? ws : (void *)dw;
         a.k_split = p.k_split;
-        e = igemm2_launch<DIR_BWD_FILTER>(a, m, p.splits, p.bi, p.bj, st);
+        e = igemm2_launch<DIR_BWD_FILTER>(a, m, p.splits, p.t, st) ? hipGetLastError() : hipErrorInvalidValue;
     } else {
         p = bwf_plan(dti, s, false);
         a.out = p.splits > 1 ? ws : (void *)dw;

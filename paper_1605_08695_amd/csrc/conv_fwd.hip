@@ -20,9 +20,8 @@ static hipError_t conv_fwd_t(const void *x, int64_t xs, const void *w, void *y, 
     const int mj = s.N * s.OH * s.OW;
     if constexpr (sizeof(T) == 2) {
         if (vi && vj && ys % 8 == 0 && aligned16p(y)) {
-            int bi, bj;
-            igemm2_tiles(a.NI, mj, 1, &bi, &bj);
-            return igemm2_launch<DIR_FWD>(a, mj, 1, bi, bj, st);
+            if (!igemm2_launch<DIR_FWD>(a, mj, 1, igemm2_tiles(a.NI, mj, 1), st)) return hipErrorInvalidValue;
+            return hipGetLastError();
         }
     }
     return igemm_launch<T, DIR_FWD>(a, mj, 1, vi, vj, st);

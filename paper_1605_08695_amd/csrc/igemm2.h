@@ -94,28 +94,51 @@ __device__ __forceinline__ int kmajor_off(int k, int row) {
     return k * (R * 2) + (((row >> 3) ^ kmajor_swz<R>(k)) << 4) + ((row & 7) << 1);
 }
 
-template <int DIR, int BI, int BJ>
-__global__ __launch_bounds__(512, 1) void igemm2_kernel(const IgArgs a) {
+// Workgroups are dealt to the 8 XCDs of the chip round-robin by linear id, and each XCD
+// has its own L2.  Renumber them so that XCD x runs one contiguous range of logical
+// blocks: neighbouring tiles (which read the same input rows) then share an L2.  Any
+// bijection is correct; this one only decides where data is cached.
+__device__ __forceinline__ int xcd_order(int linear, int total) {
+    constexpr int kXcd = 8;
+    const int q = total / kXcd, r = total % kXcd;
+    const int x = linear % kXcd;
+    return x * q + min(x, r) + linear / kXcd;
+}
+
+// BI x BJ output tile, NW waves (a 2 x NW/2 grid of wave tiles), NS LDS stages.  Every
+// SIMD runs two waves: one 8-wave block per CU, or two 4-wave blocks per CU when NS
+// stages fit twice in the 160 KiB of LDS.  Two independent blocks keep a CU's MFMAs busy
+// while the other block waits at its barrier for a slow copy.
+template <int DIR, int BI, int BJ, int NW, int NS>
+__global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     constexpr int BK = 64;
-    constexpr int NW = 8;                             // waves per block, two per SIMD
-    constexpr int WGJ = NW / 2;                       // wave grid 2 (I) x 4 (J)
+    constexpr int WGJ = NW / 2;                       // wave grid 2 (I) x NW/2 (J)
     constexpr bool TI = DIR != DIR_BWD_DATA;          // I operand kept k-major
     constexpr bool TJ = DIR == DIR_BWD_FILTER;        // J operand kept k-major
     constexpr int IB = BI * 128, JB = BJ * 128, SB = IB + JB;
     constexpr int NLI = BI / (8 * NW), NLJ = BJ / (8 * NW), NL = NLI + NLJ;   // copies per thread per tile
     constexpr int WI = BI / 2, WJ = BJ / WGJ;
     constexpr int MI = WI / 16, MJ = WJ / 16;
+    static_assert(NW == 4 || NW == 8, "waves");
+    static_assert(NS == 2 || NS == 3, "stages");
     static_assert(NLI >= 1 && NLJ >= 1 && MI >= 1 && MJ >= 1, "tile");
+    static_assert(NS * SB <= 160 * 1024, "LDS");
 
     __shared__ __attribute__((aligned(1024))) unsigned char lds0[SB];
     __shared__ __attribute__((aligned(1024))) unsigned char lds1[SB];
-    __shared__ __attribute__((aligned(1024))) unsigned char lds2[SB];
+    __shared__ __attribute__((aligned(1024))) unsigned char lds2[NS == 3 ? SB : 16];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int ti = blockIdx.x % a.tiles_i;
-    const int tj = blockIdx.x / a.tiles_i;
+    // (bwd-filter keeps the hardware order: its splits read disjoint pixel ranges, and
+    // spreading one split's tiles over all XCDs measured faster than concentrating them.)
+    const int lin_hw = (int)(blockIdx.x + gridDim.x * blockIdx.z);
+    const int lin = DIR == DIR_BWD_FILTER ? lin_hw : xcd_order(lin_hw, (int)(gridDim.x * gridDim.z));
+    const int bx = lin % (int)gridDim.x;
+    const int bz = lin / (int)gridDim.x;
+    const int ti = bx % a.tiles_i;
+    const int tj = bx / a.tiles_i;
     const int i0 = ti * BI;
     const int j0 = tj * BJ;
 
@@ -130,7 +153,7 @@ __global__ __launch_bounds__(512, 1) void igemm2_kernel(const IgArgs a) {
         MJ_ext = a.N * a.OH * a.OW;
         k_end = a.KH * a.KW * a.C;
     } else if constexpr (DIR == DIR_BWD_DATA) {
-        const int z = blockIdx.z;
+        const int z = bz;
         rh = z / a.sw;
         rw = z - rh * a.sw;
         h0 = ((rh - a.pt) % a.sh + a.sh) % a.sh;
@@ -145,7 +168,7 @@ __global__ __launch_bounds__(512, 1) void igemm2_kernel(const IgArgs a) {
         k_end = KHp * KWp * a.K;
     } else {
         MJ_ext = a.KH * a.KW * a.C;
-        k_beg = blockIdx.z * a.k_split;
+        k_beg = bz * a.k_split;
         k_end = min(a.N * a.OH * a.OW, k_beg + a.k_split);
     }
     if (j0 >= MJ_ext) return;
@@ -240,8 +263,27 @@ __global__ __launch_bounds__(512, 1) void igemm2_kernel(const IgArgs a) {
     if constexpr (DIR == DIR_FWD) { dInner = a.dC; dMid = a.dKW; }
     if constexpr (DIR == DIR_BWD_DATA) { dInner = a.dK; dMid.init((uint32_t)(KWp > 0 ? KWp : 1)); }
 
+    // K-tile order.  With 64 | channels, every 64-wide K-tile lies inside one filter tap,
+    // and the tiles are visited channel-chunk outer, tap inner: consecutive tiles then read
+    // the same input rows shifted by one tap, which stay in L1/L2.  issue() is called for
+    // kt = 0, 1, 2, ... in order, so the (chunk, tap) position advances by one per call.
+    int perm_T = 1, perm_CC = 0;
+    if constexpr (DIR == DIR_FWD) {
+        if (a.C % BK == 0 && a.KH * a.KW > 1) { perm_T = a.KH * a.KW; perm_CC = a.C / BK; }
+    } else if constexpr (DIR == DIR_BWD_DATA) {
+        if (a.K % BK == 0 && KHp * KWp > 1) { perm_T = KHp * KWp; perm_CC = a.K / BK; }
+    }
+    int perm_tap = 0, perm_cc = 0;
+
     // Issue the copies of K-tile kt into LDS stage `st`.
-    auto issue = [&](int kt, unsigned char *st) __attribute__((always_inline)) {
+    auto issue = [&](int kt_seq, unsigned char *st) __attribute__((always_inline)) {
+        int kt = kt_seq;
+        if constexpr (DIR != DIR_BWD_FILTER) {
+            if (perm_CC > 0) {
+                kt = perm_tap * perm_CC + perm_cc;
+                if (++perm_tap == perm_T) { perm_tap = 0; ++perm_cc; }
+            }
+        }
         const int kt0 = k_beg + kt * BK;
         unsigned char *stI = st;
         unsigned char *stJ = st + IB;
@@ -349,27 +391,35 @@ __global__ __launch_bounds__(512, 1) void igemm2_kernel(const IgArgs a) {
         }
     };
 
-    // One pipeline step on stage S: wait for tile kt, free the oldest stage for tile kt + 2.
+    // One pipeline step on stage S = kt % NS: wait for tile kt (the copies of the later
+    // tiles already issued may stay in flight), then refill the stage that tile kt - 1 used
+    // (every wave has passed the barrier, so none still reads it) with tile kt + NS - 1.
+    auto stage = [&](auto S_) __attribute__((always_inline)) -> unsigned char * {
+        constexpr int S = decltype(S_)::value % NS;
+        return S == 0 ? lds0 : (S == 1 ? lds1 : lds2);
+    };
     auto step = [&](auto S_, int kt) __attribute__((always_inline)) {
         constexpr int S = decltype(S_)::value;
-        unsigned char *cur = S == 0 ? lds0 : (S == 1 ? lds1 : lds2);
-        unsigned char *nxt = S == 0 ? lds2 : (S == 1 ? lds0 : lds1);   // stage (S + 2) % 3
-        if (kt + 1 < nk) wait_barrier<NL>(); else wait_barrier<0>();
-        if (kt + 2 < nk) issue(kt + 2, nxt);
-        compute(cur);
+        if constexpr (NS == 3) {
+            if (kt + 1 < nk) wait_barrier<NL>(); else wait_barrier<0>();
+        } else {
+            wait_barrier<0>();
+        }
+        if (kt + NS - 1 < nk) issue(kt + NS - 1, stage(std::integral_constant<int, S + NS - 1>{}));
+        compute(stage(S_));
     };
 
     if (nk > 0) {
         issue(0, lds0);
-        if (nk > 1) issue(1, lds1);
+        if (NS == 3 && nk > 1) issue(1, lds1);
         int kt = 0;
-        for (; kt + 3 <= nk; kt += 3) {
+        for (; kt + NS <= nk; kt += NS) {
             step(std::integral_constant<int, 0>{}, kt);
             step(std::integral_constant<int, 1>{}, kt + 1);
-            step(std::integral_constant<int, 2>{}, kt + 2);
+            if constexpr (NS == 3) step(std::integral_constant<int, 2>{}, kt + 2);
         }
         if (kt < nk) step(std::integral_constant<int, 0>{}, kt);
-        if (kt + 1 < nk) step(std::integral_constant<int, 1>{}, kt + 1);
+        if (NS == 3 && kt + 1 < nk) step(std::integral_constant<int, 1>{}, kt + 1);
     }
 
     // ------------------------------------------------------------ epilogue
@@ -387,7 +437,7 @@ __global__ __launch_bounds__(512, 1) void igemm2_kernel(const IgArgs a) {
             const int n = t / Hp;
             rowoff = (((int64_t)n * a.H + h0 + a.sh * th) * a.W + w0 + a.sw * tw) * a.xs;
         } else {
-            rowoff = (int64_t)blockIdx.z * a.split_stride + (int64_t)j * a.K;
+            rowoff = (int64_t)bz * a.split_stride + (int64_t)j * a.K;
         }
 #pragma unroll
         for (int x = 0; x < MI; ++x) {

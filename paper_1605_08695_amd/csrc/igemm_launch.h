@@ -37,35 +37,45 @@ static hipError_t igemm_launch(IgArgs &a, int mj, int zdim, bool vi, bool vj, hi
     return hipGetLastError();
 }
 
-// Tiles of the pipelined bf16 kernel (one block per CU), chosen from a sweep over the
-// AlexNet/VGG layer shapes on MI355X: 128-channel I tiles when the channel count is a
-// multiple of 128 (else 64, so 192 channels waste nothing), paired with 256-row J tiles;
-// 64-channel tiles take 256 rows only when that fits one round of blocks on the 256 CUs.
-static inline void igemm2_tiles(int ni, int mj, int zdim, int *bi, int *bj) {
-    *bi = (ni % 128 == 0) ? 128 : 64;
-    if (*bi == 128) {
-        *bj = 256;
-        return;
-    }
-    const int ti = (ni + 63) / 64;
-    const int64_t blocks256 = (int64_t)ti * ((mj + 255) / 256) * zdim;
-    *bj = blocks256 <= 256 ? 256 : 128;
+// Tile configuration of the pipelined bf16 kernel: BI x BJ output tile, waves per block,
+// LDS stages.
+struct Igemm2Tile {
+    int bi, bj, nw, ns;
+};
+
+// Chosen from sweeps over the AlexNet/VGG layer shapes on MI355X.  Two 4-wave blocks
+// share each CU (two LDS stages each); 128-channel tiles only pay when the channel count
+// is a multiple of 128 and there are still enough of them to fill both block slots of
+// every CU (about 460 blocks), otherwise 64-channel tiles.
+static inline Igemm2Tile igemm2_tiles(int ni, int mj, int zdim) {
+    const int64_t blocks128 = (int64_t)(ni / 128) * ((mj + 127) / 128) * zdim;
+    if (ni % 128 == 0 && blocks128 >= 460) return {128, 128, 4, 2};
+    return {64, 128, 4, 2};
 }
 
+template <int DIR, int BI, int BJ, int NW, int NS>
+static void igemm2_go(const IgArgs &a, dim3 grid, hipStream_t st) {
+    hipLaunchKernelGGL((igemm2_kernel<DIR, BI, BJ, NW, NS>), grid, dim3(NW * 64), 0, st, a);
+}
+
+// Launches one of the compiled configurations; false if t is not one of them.
 template <int DIR>
-static hipError_t igemm2_launch(IgArgs &a, int mj, int zdim, int bi, int bj, hipStream_t st) {
-    a.tiles_i = (a.NI + bi - 1) / bi;
-    const int tiles_j = (mj + bj - 1) / bj;
+static bool igemm2_launch(IgArgs &a, int mj, int zdim, const Igemm2Tile &t, hipStream_t st) {
+    a.tiles_i = (a.NI + t.bi - 1) / t.bi;
+    const int tiles_j = (mj + t.bj - 1) / t.bj;
     const dim3 grid((unsigned)(a.tiles_i * tiles_j), 1, (unsigned)zdim);
-    if (bi == 64 && bj == 128)
-        hipLaunchKernelGGL((igemm2_kernel<DIR, 64, 128>), grid, dim3(512), 0, st, a);
-    else if (bi == 64)
-        hipLaunchKernelGGL((igemm2_kernel<DIR, 64, 256>), grid, dim3(512), 0, st, a);
-    else if (bj == 128)
-        hipLaunchKernelGGL((igemm2_kernel<DIR, 128, 128>), grid, dim3(512), 0, st, a);
-    else
-        hipLaunchKernelGGL((igemm2_kernel<DIR, 128, 256>), grid, dim3(512), 0, st, a);
-    return hipGetLastError();
+    const int key = ((t.bi / 64) << 12) | ((t.bj / 64) << 8) | (t.nw << 4) | t.ns;
+    switch (key) {
+    case (1 << 12) | (2 << 8) | (8 << 4) | 3: igemm2_go<DIR, 64, 128, 8, 3>(a, grid, st); return true;
+    case (1 << 12) | (4 << 8) | (8 << 4) | 3: igemm2_go<DIR, 64, 256, 8, 3>(a, grid, st); return true;
+    case (2 << 12) | (2 << 8) | (8 << 4) | 3: igemm2_go<DIR, 128, 128, 8, 3>(a, grid, st); return true;
+    case (2 << 12) | (4 << 8) | (8 << 4) | 3: igemm2_go<DIR, 128, 256, 8, 3>(a, grid, st); return true;
+    case (2 << 12) | (2 << 8) | (4 << 4) | 2: igemm2_go<DIR, 128, 128, 4, 2>(a, grid, st); return true;
+    case (1 << 12) | (2 << 8) | (4 << 4) | 3: igemm2_go<DIR, 64, 128, 4, 3>(a, grid, st); return true;
+    case (1 << 12) | (2 << 8) | (4 << 4) | 2: igemm2_go<DIR, 64, 128, 4, 2>(a, grid, st); return true;
+    case (1 << 12) | (4 << 8) | (4 << 4) | 2: igemm2_go<DIR, 64, 256, 4, 2>(a, grid, st); return true;
+    default: return false;
+    }
 }
 
 static inline void fill_geom(IgArgs &a, const ConvShape &s) {
