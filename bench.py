@@ -194,6 +194,8 @@ def main():
         torch.cuda.synchronize()
         for kind, op, s, e in tr.rec:
             ms = s.elapsed_time(e)
+            if kind == "conv_bias_relu_fwd":
+                kind = "conv_fwd"       # the forward convolution with its bias + ReLU epilogue
             per_kind.setdefault(kind, 0.0)
             per_kind[kind] += ms / reps
             key = (kind, op.name if op is not None else "all")
@@ -216,6 +218,8 @@ def main():
     ew_bytes = {k: 0.0 for k in ew_kinds}
     for op in net.ops:
         for k in ew_kinds:
+            if k not in per_kind:
+                continue        # fused into another kernel (bias + ReLU forward runs in the conv epilogue)
             if (k.startswith("bias") and hasattr(op, "cout")) or (k.startswith("maxpool") and not hasattr(op, "cout")):
                 if k == "maxpool_bwd" and op.src == "x":
                     continue

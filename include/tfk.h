@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 1
+#define TFK_ABI_VERSION 2
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -103,6 +103,20 @@ typedef struct {
 TFK_API tfk_status tfk_conv2d_fwd(const void *x, tfk_nhwc xd, const void *w, int32_t cout,
                           tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
                           void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Conv2D forward with BiasAdd and ReLU fused into the same kernel (the hand-fused
+ * activation kernels of Section 5):
+ *   y[n,oh,ow,co] = max(conv(x, w)[n,oh,ow,co] + bias[co], +0)
+ * The sum is formed in fp32 and rounded to dt once, when y is stored (the unfused
+ * sequence tfk_conv2d_fwd + tfk_bias_relu_fwd rounds the convolution output first).
+ *   bias : cout fp32 values, 4-byte aligned, not overlapping y.
+ * Everything else, including the workspace query (op 0 of tfk_conv2d_workspace_bytes),
+ * is as for tfk_conv2d_fwd.  A NULL bias is TFK_ERR_NULL.
+ */
+TFK_API tfk_status tfk_conv2d_fwd_bias_relu(const void *x, tfk_nhwc xd, const void *w, int32_t cout,
+                                    const float *bias, tfk_window p, tfk_dtype dt, void *y,
+                                    tfk_nhwc yd, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * Conv2DBackpropInput: the gradient of the forward map with respect to x

@@ -177,8 +177,10 @@ size_t tfk_conv2d_workspace_bytes(int32_t op, tfk_nhwc xd, int32_t cout, tfk_win
     return conv_bwd_filter_ws_bytes(dti, s);
 }
 
-tfk_status tfk_conv2d_fwd(const void *x, tfk_nhwc xd, const void *w, int32_t cout, tfk_window p, tfk_dtype dt,
-                          void *y, tfk_nhwc yd, void *ws, size_t ws_bytes, void *stream) {
+// Shared by tfk_conv2d_fwd (bias == nullptr) and tfk_conv2d_fwd_bias_relu.
+static tfk_status conv_fwd_impl(const void *x, tfk_nhwc xd, const void *w, int32_t cout, const float *bias,
+                                tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd, void *ws, size_t ws_bytes,
+                                void *stream, const char *what) {
     ConvShape s;
     TRY(check_conv(xd, cout, p, dt, yd, "x", "y", s));
     if (xd.n == 0) return ok();
@@ -192,15 +194,31 @@ tfk_status tfk_conv2d_fwd(const void *x, tfk_nhwc xd, const void *w, int32_t cou
     const int64_t yb = view_bytes(yd, es);
     if (overlap(y, yb, x, view_bytes(xd, es)) || overlap(y, yb, w, filter_bytes(s, es)))
         return fail(TFK_ERR_ALIAS, "y overlaps x or w");
+    if (bias != nullptr && overlap(y, yb, bias, (int64_t)cout * 4)) return fail(TFK_ERR_ALIAS, "y overlaps bias");
     const int dti = dt == TFK_F32 ? 0 : 1;
     const size_t need = conv_fold_applies(dti, s) ? conv_fold_ws_bytes(0, s) : 0;
     TRY(check_ws(ws, ws_bytes, need));
     if (need && (overlap(ws, (int64_t)need, x, view_bytes(xd, es)) || overlap(ws, (int64_t)need, w, filter_bytes(s, es)) ||
                  overlap(ws, (int64_t)need, y, yb)))
         return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
-    return hip_status(launch_conv_fwd(dti, x, xd.pixel_stride, w, y, yd.pixel_stride, s, need ? ws : nullptr,
+    return hip_status(launch_conv_fwd(dti, x, xd.pixel_stride, w, y, yd.pixel_stride, s, bias, need ? ws : nullptr,
                                       (hipStream_t)stream),
-                      "conv2d_fwd");
+                      what);
+}
+
+tfk_status tfk_conv2d_fwd(const void *x, tfk_nhwc xd, const void *w, int32_t cout, tfk_window p, tfk_dtype dt,
+                          void *y, tfk_nhwc yd, void *ws, size_t ws_bytes, void *stream) {
+    return conv_fwd_impl(x, xd, w, cout, nullptr, p, dt, y, yd, ws, ws_bytes, stream, "conv2d_fwd");
+}
+
+tfk_status tfk_conv2d_fwd_bias_relu(const void *x, tfk_nhwc xd, const void *w, int32_t cout, const float *bias,
+                                    tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd, void *ws, size_t ws_bytes,
+                                    void *stream) {
+    if (xd.n > 0 && cout > 0) {
+        TRY(need_ptr(bias, "bias"));
+        TRY(need_align(bias, 4, "bias"));
+    }
+    return conv_fwd_impl(x, xd, w, cout, bias, p, dt, y, yd, ws, ws_bytes, stream, "conv2d_fwd_bias_relu");
 }
 
 tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void *w, tfk_window p, tfk_dtype dt, void *dx,

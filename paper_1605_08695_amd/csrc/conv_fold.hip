@@ -183,7 +183,7 @@ size_t conv_fold_ws_bytes(int op, const ConvShape &s) {
 }
 
 hipError_t launch_conv_fwd_folded(const void *x, int64_t xs, const void *w, void *y, int64_t ys, const ConvShape &s,
-                                  void *ws, hipStream_t st) {
+                                  const float *bias, void *ws, hipStream_t st) {
     Fold f;
     fold_plan(s, f);
     unsigned char *base = reinterpret_cast<unsigned char *>(ws);
@@ -195,7 +195,7 @@ hipError_t launch_conv_fwd_folded(const void *x, int64_t xs, const void *w, void
                        reinterpret_cast<const bf16_t *>(w), s.KH, s.KW, s.C, s.K, f.F, f.Cp, f.v.KW, wv);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    return launch_conv_fwd(1, xp, 8, wv, y, ys, f.v, nullptr, st);
+    return launch_conv_fwd(1, xp, 8, wv, y, ys, f.v, bias, nullptr, st);
 }
 
 hipError_t launch_conv_bwd_filter_folded(const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,

@@ -5,7 +5,7 @@ namespace tfk {
 
 template <typename T>
 static hipError_t conv_fwd_t(const void *x, int64_t xs, const void *w, void *y, int64_t ys, const ConvShape &s,
-                             hipStream_t st) {
+                             const float *bias, hipStream_t st) {
     constexpr int EPC = Elem<T>::kPerChunk;
     IgArgs a;
     fill_geom(a, s);
@@ -15,6 +15,7 @@ static hipError_t conv_fwd_t(const void *x, int64_t xs, const void *w, void *y, 
     a.xs = xs;
     a.ys = ys;
     a.NI = s.K;
+    a.bias = bias;
     const bool vi = s.K % EPC == 0 && aligned16p(w);
     const bool vj = s.C % EPC == 0 && xs % EPC == 0 && aligned16p(x);
     const int mj = s.N * s.OH * s.OW;
@@ -28,10 +29,11 @@ static hipError_t conv_fwd_t(const void *x, int64_t xs, const void *w, void *y, 
 }
 
 hipError_t launch_conv_fwd(int dt, const void *x, int64_t xs, const void *w, void *y, int64_t ys,
-                           const ConvShape &s, void *ws, hipStream_t st) {
+                           const ConvShape &s, const float *bias, void *ws, hipStream_t st) {
     if (ws != nullptr && conv_fold_applies(dt, s) && ((uintptr_t)y & 15) == 0 && ys % 8 == 0)
-        return launch_conv_fwd_folded(x, xs, w, y, ys, s, ws, st);
-    return dt == 0 ? conv_fwd_t<float>(x, xs, w, y, ys, s, st) : conv_fwd_t<bf16_t>(x, xs, w, y, ys, s, st);
+        return launch_conv_fwd_folded(x, xs, w, y, ys, s, bias, ws, st);
+    return dt == 0 ? conv_fwd_t<float>(x, xs, w, y, ys, s, bias, st)
+                   : conv_fwd_t<bf16_t>(x, xs, w, y, ys, s, bias, st);
 }
 
 }  // namespace tfk

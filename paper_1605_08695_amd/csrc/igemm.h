@@ -49,6 +49,7 @@ struct IgArgs {
     const void *src_j;   // FWD: x          BWD_DATA: dy         BWD_FILTER: x
     void *out;           // FWD: y          BWD_DATA: dx         BWD_FILTER: fp32 dw / partials
     float beta;          // BWD_DATA: 0 overwrite, 1 accumulate
+    const float *bias;   // FWD: when set, y = max(conv + bias[co], +0) (bias + ReLU fused)
     // forward-convolution geometry
     int N, H, W, C;      // input extents
     int OH, OW, K;       // output extents, K = output channels
@@ -529,6 +530,15 @@ __global__ __launch_bounds__(256) void igemm_kernel(const IgArgs a) {
 #pragma unroll
                         for (int q = 0; q < 4; ++q)
                             if (i + q < a.NI) r4[q] += a.beta * Elem<T>::load(o + q);
+                    }
+                }
+                if constexpr (DIR == DIR_FWD) {
+                    if (a.bias != nullptr) {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const float v = r4[q] + (i + q < a.NI ? a.bias[i + q] : 0.f);
+                            r4[q] = v > 0.f ? v : 0.f;
+                        }
                     }
                 }
                 if (i + 3 < a.NI) {

@@ -459,6 +459,15 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
                         r4[3] += a.beta * bf16_to_f32(old.y >> 16);
                     }
                 }
+                if constexpr (DIR == DIR_FWD) {
+                    if (a.bias != nullptr) {      // fused bias + ReLU, rounded once (i + 3 < NI)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const float v = r4[q] + a.bias[i + q];
+                            r4[q] = v > 0.f ? v : 0.f;
+                        }
+                    }
+                }
                 uint2 pk;
                 pk.x = pack_bf16x2(r4[0], r4[1]);
                 pk.y = pack_bf16x2(r4[2], r4[3]);

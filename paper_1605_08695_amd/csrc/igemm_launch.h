@@ -88,6 +88,7 @@ static inline void fill_geom(IgArgs &a, const ConvShape &s) {
     a.dOH.init((uint32_t)s.OH);
     a.dK.init((uint32_t)s.K);
     a.beta = 0.f;
+    a.bias = nullptr;
     a.k_split = 0;
     a.split_stride = 0;
 }

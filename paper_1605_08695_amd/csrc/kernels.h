@@ -33,8 +33,9 @@ struct SgdBatch {
 };
 
 // dt: 0 = fp32, 1 = bf16
+// bias (may be null): fused y = max(conv + bias, +0).
 hipError_t launch_conv_fwd(int dt, const void *x, int64_t xs, const void *w, void *y, int64_t ys,
-                           const ConvShape &s, void *ws, hipStream_t st);
+                           const ConvShape &s, const float *bias, void *ws, hipStream_t st);
 hipError_t launch_conv_bwd_data(int dt, const void *dy, int64_t dys, const void *w, void *dx, int64_t dxs,
                                 float beta, const ConvShape &s, hipStream_t st);
 hipError_t launch_conv_bwd_filter(int dt, const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,
@@ -46,7 +47,7 @@ size_t conv_bwd_filter_ws_bytes(int dt, const ConvShape &s);
 bool conv_fold_applies(int dt, const ConvShape &s);
 size_t conv_fold_ws_bytes(int op, const ConvShape &s);
 hipError_t launch_conv_fwd_folded(const void *x, int64_t xs, const void *w, void *y, int64_t ys, const ConvShape &s,
-                                  void *ws, hipStream_t st);
+                                  const float *bias, void *ws, hipStream_t st);
 hipError_t launch_conv_bwd_filter_folded(const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,
                                          const ConvShape &s, void *ws, hipStream_t st);
 

@@ -15,7 +15,7 @@ import torch
 
 from ._lib import Nhwc, TfkError, Window, TFK_BF16, TFK_F32, check, load
 
-__all__ = ["conv2d_fwd", "conv2d_bwd_input", "conv2d_bwd_filter", "conv2d_workspace_bytes", "bias_relu_fwd",
+__all__ = ["conv2d_fwd", "conv2d_fwd_bias_relu", "conv2d_bwd_input", "conv2d_bwd_filter", "conv2d_workspace_bytes", "bias_relu_fwd",
            "bias_relu_bwd", "bias_relu_bwd_workspace_bytes", "maxpool_fwd", "maxpool_bwd", "apply_sgd",
            "apply_sgd_multi", "out_len", "nhwc", "window", "TfkError", "abi_version"]
 
@@ -78,8 +78,7 @@ def conv2d_workspace_bytes(op: int, x: torch.Tensor, cout: int, kh, kw, stride, 
     return load().tfk_conv2d_workspace_bytes(op, nhwc(x), cout, window(kh, kw, stride, pads), _dt(x))
 
 
-def conv2d_fwd(x, w, stride, pads, y=None, ws=None, stream=None):
-    """y = x (*) w (cross-correlation).  x NHWC, w HWIO, pads (top, bottom, left, right)."""
+def _conv_fwd(x, w, bias, stride, pads, y, ws, stream):
     lib = load()
     kh, kw, cin, cout = w.shape
     win = window(kh, kw, stride, pads)
@@ -92,9 +91,26 @@ def conv2d_fwd(x, w, stride, pads, y=None, ws=None, stream=None):
                          out_len(ww, kw, win.stride_w, pads[2], pads[3]), cout), dtype=x.dtype, device=x.device)
     if w.dtype != x.dtype or y.dtype != x.dtype:
         raise TypeError("x, w and y must share one dtype")
-    check(lib.tfk_conv2d_fwd(_ptr(x), nhwc(x), _ptr(w), cout, win, _dt(x), _ptr(y), nhwc(y),
-                             _ptr(ws) if need else None, need, _stream(stream)))
+    wsp = _ptr(ws) if need else None
+    if bias is None:
+        check(lib.tfk_conv2d_fwd(_ptr(x), nhwc(x), _ptr(w), cout, win, _dt(x), _ptr(y), nhwc(y), wsp, need,
+                                 _stream(stream)))
+    else:
+        if bias.dtype != torch.float32 or bias.numel() != cout or not bias.is_contiguous():
+            raise ValueError("bias must be a contiguous float32 vector of cout values")
+        check(lib.tfk_conv2d_fwd_bias_relu(_ptr(x), nhwc(x), _ptr(w), cout, _ptr(bias), win, _dt(x), _ptr(y),
+                                           nhwc(y), wsp, need, _stream(stream)))
     return y
+
+
+def conv2d_fwd(x, w, stride, pads, y=None, ws=None, stream=None):
+    """y = x (*) w (cross-correlation).  x NHWC, w HWIO, pads (top, bottom, left, right)."""
+    return _conv_fwd(x, w, None, stride, pads, y, ws, stream)
+
+
+def conv2d_fwd_bias_relu(x, w, bias, stride, pads, y=None, ws=None, stream=None):
+    """y = max(x (*) w + bias, 0) in one kernel (bias fp32, one value per output channel)."""
+    return _conv_fwd(x, w, bias, stride, pads, y, ws, stream)
 
 
 def conv2d_bwd_input(dy, w, dx, stride, pads, beta=0.0, stream=None):

@@ -1,7 +1,8 @@
 """One worker replica's synchronous SGD step, driven through the tfk_* ops.
 
 The schedule follows the paper's single-replica semantics (Sections 4.1 and
-4.4): a forward pass over every op; the upstream gradient ``g`` of the output
+4.4): a forward pass over every op (each convolution with its bias and ReLU
+fused into one kernel, Section 5); the upstream gradient ``g`` of the output
 tensor seeds a backward pass that visits the ops in reverse order and sums the
 partial gradients of every path into a tensor (``beta = 1`` for every
 contribution after the first); no gradient is formed for the step input
@@ -124,12 +125,10 @@ class Replica:
             x = self.act[op.src]
             y = self._slice(self.act, op)
             if isinstance(op, Conv):
-                if trace: trace("conv_fwd", op, x=x, w=self.Wlp[op.name], y=y)
-                ops.conv2d_fwd(x, self.Wlp[op.name], (op.sh, op.sw), op.pads, y=y, ws=self.ws, stream=stream)
-                if trace: trace("conv_fwd:end", op, y=y)
-                if trace: trace("bias_relu_fwd", op, y=y, b=self.b[op.name])
-                ops.bias_relu_fwd(y, self.b[op.name], stream=stream)
-                if trace: trace("bias_relu_fwd:end", op, y=y)
+                if trace: trace("conv_bias_relu_fwd", op, x=x, w=self.Wlp[op.name], b=self.b[op.name], y=y)
+                ops.conv2d_fwd_bias_relu(x, self.Wlp[op.name], self.b[op.name], (op.sh, op.sw), op.pads, y=y,
+                                         ws=self.ws, stream=stream)
+                if trace: trace("conv_bias_relu_fwd:end", op, y=y)
             else:
                 if trace: trace("maxpool_fwd", op, x=x, y=y, argmax=self.argmax[op.name])
                 ops.maxpool_fwd(x, (op.kh, op.kw), (op.sh, op.sw), op.pads, y=y, argmax=self.argmax[op.name],

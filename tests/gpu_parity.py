@@ -183,6 +183,13 @@ class ParityTracer:
         ref = oracle.conv2d_fwd(self._x64(inp["x"]), f64(inp["w"]), (op.sh, op.sw), op.pads)
         self.record_tensor("conv_fwd", op.name, self._x64(out["y"]), ref, self.dtype)
 
+    def _check_conv_bias_relu_fwd(self, op, inp, out):
+        pre = oracle.conv2d_fwd(self._x64(inp["x"]), f64(inp["w"]), (op.sh, op.sw), op.pads)
+        ref = oracle.bias_relu_fwd(pre, f64(inp["b"]))
+        y = self._x64(out["y"])
+        self.record_tensor("conv_bias_relu_fwd", op.name, y, ref, self.dtype)
+        self.record("conv_bias_relu_fwd", op.name, "negatives", float(np.sum(np.signbit(y))), 0.0)
+
     def _check_bias_relu_fwd(self, op, inp, out):
         ref = oracle.bias_relu_fwd(self._x64(inp["y"]), f64(inp["b"]))
         y = self._x64(out["y"])

@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 1
+    assert lib.tfk_abi_version() == 2
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -67,6 +67,18 @@ def test_conv_fwd_validation(lib):
     assert conv_fwd(lib, y=P + 0x100) == ALIAS                         # y overlaps x
     assert conv_fwd(lib, xd=(2, 1, 1, 16, 0), yd=(2, 1, 1, 32, 0), win=(3, 3, 1, 1, 0, 0, 0, 0)) == SHAPE
     assert b"must be" in lib.tfk_last_error() or len(lib.tfk_last_error()) > 0
+
+
+def test_conv_fwd_bias_relu_validation(lib):
+    def fused(x=P, bias=P + 0x300000, y=P + 0x200000):
+        return lib.tfk_conv2d_fwd_bias_relu(vp(x), Nhwc(2, 8, 8, 16, 0), vp(P + 0x100000), 32, vp(bias),
+                                            Window(3, 3, 1, 1, 1, 1, 1, 1), F32, vp(y), Nhwc(2, 8, 8, 32, 0),
+                                            None, 0, None)
+    assert fused(bias=0) == NULL
+    assert fused(bias=P + 0x300002) == ALIGN                            # fp32 bias, 4-byte aligned
+    assert fused(bias=P + 0x200010) == ALIAS                            # bias inside y
+    assert fused(x=0) == NULL                                           # the convolution's own checks
+    assert fused(y=P + 0x100) == ALIAS
 
 
 def test_conv_bwd_validation(lib):

@@ -57,6 +57,14 @@ def test_conv_three_directions(case, dtype):
     assert y.shape == ref.shape
     assert_close(f64(y), ref, dtype, label="fwd")
 
+    # the same convolution with bias + ReLU fused into its epilogue
+    bias = torch.from_numpy(rng.standard_normal(K) * 0.5).to(torch.float32).to(DEV)
+    yf = ops.conv2d_fwd_bias_relu(x, w, bias, (sh, sw), pads)
+    torch.cuda.synchronize()
+    ref_f = oracle.bias_relu_fwd(ref, f64(bias))
+    assert_close(f64(yf), ref_f, dtype, label="fwd+bias+relu")
+    assert not bool(torch.any(torch.signbit(yf))), "fused ReLU must store +0, never -0 or negatives"
+
     dy = _mk(y.shape, dtype, rng)
     for beta in (0.0, 1.0):
         dx = _mk(x.shape, dtype, rng)
@@ -87,6 +95,12 @@ def test_conv_channel_slice_views(dtype):
     assert_close(f64(y), ref, dtype, label="fwd slice")
     rest = torch.cat([out[..., :16], out[..., 40:]], dim=-1)
     assert bool(torch.all(rest == 7.0))                      # neighbours untouched
+    bias = torch.linspace(-1, 1, 24, device=DEV, dtype=torch.float32)
+    ops.conv2d_fwd_bias_relu(x, w, bias, 1, (1, 1, 1, 1), y=y)
+    torch.cuda.synchronize()
+    assert_close(f64(y), oracle.bias_relu_fwd(ref, f64(bias)), dtype, label="fwd+bias+relu slice")
+    rest = torch.cat([out[..., :16], out[..., 40:]], dim=-1)
+    assert bool(torch.all(rest == 7.0))
     dyb = _mk((2, 9, 9, 64), dtype, rng)
     dy = dyb[..., 16:40]
     dxb = torch.zeros((2, 9, 9, 48), dtype=dtype, device=DEV)
