@@ -7,6 +7,7 @@
 #include "fastdiv.h"
 
 typedef uint16_t bf16_t;   // bfloat16 bits
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
 struct alignas(16) U4 {
     uint32_t x, y, z, w;

@@ -97,7 +97,7 @@ static hipError_t conv_bwd_filter_t(const void *x, int64_t xs, const void *dy, i
         e = igemm_launch<T, DIR_BWD_FILTER>(a, m, p.splits, vi, vj, st);
     }
     if (e != hipSuccess || p.splits <= 1) return e;
-    return launch_sum_splits(reinterpret_cast<const float *>(ws), p.splits, mn, dw, st);
+    return launch_sum_splits(reinterpret_cast<float *>(ws), p.splits, mn, dw, st);
 }
 
 hipError_t launch_conv_bwd_filter(int dt, const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,

@@ -162,20 +162,60 @@ __global__ __launch_bounds__(256) void sum_partials_kernel(const float *__restri
     if (threadIdx.x == 0) out[c] = red[0];
 }
 
+// ------------------------------------------------------------------ pixel decomposition
+// t = ((n * E2 + i2) * E1 + i1) * CV + cv.  Below 2^31 work items it is three 32-bit
+// multiply-high divisions; 64-bit division (a long instruction sequence) only beyond.
+struct Decode {
+    FastDiv dcv, d1, d2;
+    int64_t cv, e1, e2;
+    bool small;
+};
+
+static Decode make_decode(int64_t cv, int64_t e1, int64_t e2, int64_t total) {
+    Decode d;
+    d.cv = cv;
+    d.e1 = e1;
+    d.e2 = e2;
+    d.small = total < (1ll << 31);
+    d.dcv.init((uint32_t)cv);
+    d.d1.init((uint32_t)e1);
+    d.d2.init((uint32_t)e2);
+    return d;
+}
+
+__device__ __forceinline__ void decode(const Decode &d, int64_t t, int &cv, int64_t &pix, int &i1, int &i2, int &n) {
+    if (d.small) {
+        uint32_t q, r, q2, r2, q3, r3;
+        d.dcv.divmod((uint32_t)t, q, r);
+        d.d1.divmod(q, q2, r2);
+        d.d2.divmod(q2, q3, r3);
+        cv = (int)r;
+        pix = q;
+        i1 = (int)r2;
+        i2 = (int)r3;
+        n = (int)q3;
+    } else {
+        cv = (int)(t % d.cv);
+        pix = t / d.cv;
+        i1 = (int)(pix % d.e1);
+        const int64_t q = pix / d.e1;
+        i2 = (int)(q % d.e2);
+        n = (int)(q / d.e2);
+    }
+}
+
 // ------------------------------------------------------------------ max-pool forward
 template <typename T, bool VEC>
 __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T *__restrict__ x, PoolGeom g,
-                                                          T *__restrict__ y, int32_t *__restrict__ argmax) {
+                                                          T *__restrict__ y, int32_t *__restrict__ argmax, Decode dec) {
     constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
     const int CV = g.C / EPC;
     const int64_t total = (int64_t)g.N * g.OH * g.OW * CV;
     for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
          t += (int64_t)gridDim.x * blockDim.x) {
-        const int cv = (int)(t % CV);
-        const int64_t pix = t / CV;
-        const int ow = (int)(pix % g.OW);
-        const int oh = (int)((pix / g.OW) % g.OH);
-        const int n = (int)(pix / ((int64_t)g.OW * g.OH));
+        int cv, ow, oh, n;
+        int64_t pix;
+        decode(dec, t, cv, pix, ow, oh, n);
         float best[EPC];
         int32_t bi[EPC];
         bool have = false;
@@ -226,17 +266,15 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T *__restrict__ 
 template <typename T, bool VEC>
 __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T *__restrict__ dy,
                                                           const int32_t *__restrict__ argmax, PoolGeom g,
-                                                          float beta, T *dx) {
+                                                          float beta, T *dx, Decode dec) {
     constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
     const int CV = g.C / EPC;
     const int64_t total = (int64_t)g.N * g.H * g.W * CV;
     for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
          t += (int64_t)gridDim.x * blockDim.x) {
-        const int cv = (int)(t % CV);
-        const int64_t pix = t / CV;
-        const int w = (int)(pix % g.W);
-        const int h = (int)((pix / g.W) % g.H);
-        const int n = (int)(pix / ((int64_t)g.W * g.H));
+        int cv, w, h, n;
+        int64_t pix;
+        decode(dec, t, cv, pix, w, h, n);
         const int32_t self = (int32_t)(pix * g.C + cv * EPC);
         // windows oh with oh*sh - pt <= h <= oh*sh - pt + KH - 1
         const int hp = h + g.pt, wp = w + g.pl;
@@ -336,13 +374,56 @@ __global__ __launch_bounds__(256) void sgd_multi_kernel(SgdBatch b, float lr) {
 }
 
 // ------------------------------------------------------------------ split-K sum / zero fill
-__global__ __launch_bounds__(256) void sum_splits_kernel(const float *__restrict__ part, int splits,
-                                                         int64_t mn, float *__restrict__ out) {
+// The split partials part[s][i] (s < splits, i < mn) are summed in two fixed levels, so
+// the result depends only on the shape: groups of kSplitGroup consecutive splits are
+// summed in split order (in place, into the group's first split), then the group sums are
+// added in group order.  Each thread owns VEC consecutive elements of one group and issues
+// all of the group's loads before adding, so a reduction over many splits of a small
+// filter gradient still has enough loads in flight.
+constexpr int kSplitGroup = 16;
+
+template <int VEC>
+struct FVec;
+template <> struct FVec<1> { typedef float T; };
+template <> struct FVec<4> { typedef f32x4_t T; };
+
+template <int VEC>
+__global__ __launch_bounds__(256) void sum_split_groups_kernel(float *__restrict__ part, int splits, int64_t mn,
+                                                               int groups) {
+    typedef typename FVec<VEC>::T V;
+    const int64_t mv = mn / VEC;
+    const int64_t total = mv * groups;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < mn; i += stride) {
-        float acc = 0.f;
-        for (int s = 0; s < splits; ++s) acc += part[(int64_t)s * mn + i];
-        out[i] = acc;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += stride) {
+        const int g = (int)(t / mv);
+        const int64_t i = t - (int64_t)g * mv;
+        const int s0 = g * kSplitGroup;
+        const int n = min(kSplitGroup, splits - s0);
+        V *base = reinterpret_cast<V *>(part + (int64_t)s0 * mn) + i;
+        V v[kSplitGroup];
+#pragma unroll
+        for (int s = 0; s < kSplitGroup; ++s)
+            if (s < n) v[s] = base[(int64_t)s * mv];
+        V acc = v[0];
+#pragma unroll
+        for (int s = 1; s < kSplitGroup; ++s)
+            if (s < n) acc += v[s];
+        base[0] = acc;
+    }
+}
+
+template <int VEC>
+__global__ __launch_bounds__(256) void sum_groups_kernel(const float *__restrict__ part, int groups, int64_t mn,
+                                                         float *__restrict__ out) {
+    typedef typename FVec<VEC>::T V;
+    const int64_t mv = mn / VEC;
+    const int64_t gstride = (int64_t)kSplitGroup * mv;      // between the first splits of two groups
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < mv; i += stride) {
+        const V *src = reinterpret_cast<const V *>(part) + i;
+        V acc = src[0];
+        for (int g = 1; g < groups; ++g) acc += src[(int64_t)g * gstride];
+        reinterpret_cast<V *>(out)[i] = acc;
     }
 }
 
@@ -421,12 +502,14 @@ static hipError_t maxpool_fwd_t(const void *x, const PoolGeom &g, void *y, int32
     constexpr int EPC = Elem<T>::kPerChunk;
     const bool vec = g.C % EPC == 0 && g.xs % EPC == 0 && g.ys % EPC == 0 && aligned16(x) &&
                      aligned16(y) && aligned16(am);
-    const int64_t work = (int64_t)g.N * g.OH * g.OW * (vec ? g.C / EPC : g.C);
+    const int64_t cv = vec ? g.C / EPC : g.C;
+    const int64_t work = (int64_t)g.N * g.OH * g.OW * cv;
     const int grid = grid_for(work, 256, 16384);
+    const Decode dec = make_decode(cv, g.OW, g.OH, work);
     if (vec)
-        hipLaunchKernelGGL((maxpool_fwd_kernel<T, true>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am);
+        hipLaunchKernelGGL((maxpool_fwd_kernel<T, true>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am, dec);
     else
-        hipLaunchKernelGGL((maxpool_fwd_kernel<T, false>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am);
+        hipLaunchKernelGGL((maxpool_fwd_kernel<T, false>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am, dec);
     return hipGetLastError();
 }
 
@@ -440,12 +523,14 @@ static hipError_t maxpool_bwd_t(const void *dy, const int32_t *am, const PoolGeo
     constexpr int EPC = Elem<T>::kPerChunk;
     const bool vec = g.C % EPC == 0 && g.xs % EPC == 0 && g.ys % EPC == 0 && aligned16(dx) &&
                      aligned16(dy) && aligned16(am);
-    const int64_t work = (int64_t)g.N * g.H * g.W * (vec ? g.C / EPC : g.C);
+    const int64_t cv = vec ? g.C / EPC : g.C;
+    const int64_t work = (int64_t)g.N * g.H * g.W * cv;
     const int grid = grid_for(work, 256, 16384);
+    const Decode dec = make_decode(cv, g.W, g.H, work);
     if (vec)
-        hipLaunchKernelGGL((maxpool_bwd_kernel<T, true>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g, beta, (T *)dx);
+        hipLaunchKernelGGL((maxpool_bwd_kernel<T, true>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g, beta, (T *)dx, dec);
     else
-        hipLaunchKernelGGL((maxpool_bwd_kernel<T, false>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g, beta, (T *)dx);
+        hipLaunchKernelGGL((maxpool_bwd_kernel<T, false>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g, beta, (T *)dx, dec);
     return hipGetLastError();
 }
 
@@ -468,10 +553,21 @@ hipError_t launch_sgd_multi(const SgdBatch &b, float lr, hipStream_t st) {
     return hipGetLastError();
 }
 
-hipError_t launch_sum_splits(const float *part, int splits, int64_t mn, float *out, hipStream_t st) {
-    const int grid = grid_for(mn, 256, 8192);
-    hipLaunchKernelGGL(sum_splits_kernel, dim3(grid), dim3(256), 0, st, part, splits, mn, out);
+template <int VEC>
+static hipError_t sum_splits_t(float *part, int splits, int64_t mn, float *out, hipStream_t st) {
+    const int groups = (splits + kSplitGroup - 1) / kSplitGroup;
+    const int64_t mv = mn / VEC;
+    hipLaunchKernelGGL(sum_split_groups_kernel<VEC>, dim3(grid_for(mv * groups, 256, 16384)), dim3(256), 0, st, part,
+                       splits, mn, groups);
+    hipLaunchKernelGGL(sum_groups_kernel<VEC>, dim3(grid_for(mv, 256, 16384)), dim3(256), 0, st, part, groups, mn,
+                       out);
     return hipGetLastError();
+}
+
+// part is the caller's workspace and is overwritten by the first level.
+hipError_t launch_sum_splits(float *part, int splits, int64_t mn, float *out, hipStream_t st) {
+    if (mn % 4 == 0 && aligned16(part) && aligned16(out)) return sum_splits_t<4>(part, splits, mn, out, st);
+    return sum_splits_t<1>(part, splits, mn, out, st);
 }
 
 hipError_t launch_fill_zero(float *out, int64_t n, hipStream_t st) {

@@ -42,7 +42,6 @@ namespace tfk {
 enum ConvDir { DIR_FWD = 0, DIR_BWD_DATA = 1, DIR_BWD_FILTER = 2 };
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
-typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
 struct IgArgs {
     const void *src_i;   // FWD: w (HWIO)   BWD_DATA: w (HWIO)   BWD_FILTER: dy

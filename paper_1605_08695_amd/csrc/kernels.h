@@ -60,7 +60,8 @@ hipError_t launch_maxpool_bwd(int dt, const void *dy, const int32_t *am, const P
                               hipStream_t st);
 hipError_t launch_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh, hipStream_t st);
 hipError_t launch_sgd_multi(const SgdBatch &b, float lr, hipStream_t st);
-hipError_t launch_sum_splits(const float *part, int splits, int64_t mn, float *out, hipStream_t st);
+// Sums split-K partials part[splits][mn] into out; part (workspace) is overwritten.
+hipError_t launch_sum_splits(float *part, int splits, int64_t mn, float *out, hipStream_t st);
 hipError_t launch_fill_zero(float *out, int64_t n, hipStream_t st);
 
 }  // namespace tfk
