@@ -12,14 +12,16 @@ struct BwfPlan {
 };
 
 // Tiles and split-K of one bwd-filter launch, chosen from sweeps over the AlexNet/VGG
-// shapes: 128-row tap tiles, and the pixel reduction split until there are about two
-// rounds of blocks (one round leaves the last copies of every block exposed).
+// shapes: 128 x 128 tiles (even for 192 output channels, where the second channel tile
+// is half empty) and the pixel reduction split until there are about four blocks per CU;
+// 64-channel layers take 64 x 128 tiles and half as many splits (their partials are
+// the larger share of the work).
 BwfPlan bwf_plan(int dt, const ConvShape &s, bool v2) {
     BwfPlan p;
     const int bk = dt == 0 ? 32 : 64;
     const int m = s.KH * s.KW * s.C;
     if (v2) {
-        p.t = (s.K % 128 == 0) ? Igemm2Tile{128, 128, 4, 2} : Igemm2Tile{64, 128, 4, 2};
+        p.t = s.K > 64 ? Igemm2Tile{128, 128, 4, 2} : Igemm2Tile{64, 128, 4, 2};
         p.bi = p.t.bi;
         p.bj = p.t.bj;
     } else {
@@ -29,7 +31,7 @@ BwfPlan bwf_plan(int dt, const ConvShape &s, bool v2) {
     const int tiles = ((s.K + p.bi - 1) / p.bi) * ((m + p.bj - 1) / p.bj);
     const int64_t ktot = (int64_t)s.N * s.OH * s.OW;
     const int64_t ktiles = (ktot + bk - 1) / bk;
-    const int target = v2 ? 1024 : 512;
+    const int target = v2 && s.K > 64 ? 1024 : 512;
     int64_t sp = (target + tiles - 1) / tiles;
     const int64_t max_sp = std::max<int64_t>(1, ktiles / 8);   // at least 8 K tiles per split
     sp = std::max<int64_t>(1, std::min<int64_t>(sp, max_sp));

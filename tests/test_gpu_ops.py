@@ -35,6 +35,12 @@ CONV_CASES = [
     ("5x5_cout192", 2, 14, 14, 64, 192, 5, 5, 1, 1, (2, 2, 2, 2)),
     ("long_reduction", 16, 28, 28, 64, 64, 3, 3, 1, 1, (1, 1, 1, 1)),
     ("3x3s2_pad_odd", 3, 10, 9, 8, 16, 3, 3, 2, 2, (1, 0, 1, 0)),
+    # 64 | Cin: whole 64-channel K tiles, visited channel-chunk outer
+    ("tiny_images_c64", 9, 3, 3, 64, 72, 3, 3, 1, 1, (1, 1, 1, 1)),
+    ("stride2_c64", 2, 17, 15, 64, 64, 3, 3, 2, 2, (1, 1, 1, 1)),
+    ("1x7_c128", 2, 17, 17, 128, 64, 1, 7, 1, 1, (0, 0, 3, 3)),
+    ("5x5_valid_c128", 3, 12, 11, 128, 96, 5, 5, 1, 1, (0, 0, 0, 0)),
+    ("alexnet_conv3_shape", 4, 13, 13, 192, 384, 3, 3, 1, 1, (1, 1, 1, 1)),
 ]
 
 
