@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=128, help="images of the batch the oracle steps through")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--gemm-reference", action="store_true",
+                    help="only time the vendor bf16 GEMM (torch.matmul) on the GEMM shapes of the workload's convolutions "
+                         "(no im2col), as a reference point, and exit")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain copy kernel over this many MiB (HBM counter calibration) and exit")
     return ap.parse_args()
@@ -64,6 +67,10 @@ def elementwise_bytes(net, op_kind, op, D):
         nx = int(np.prod(t[op.src]))
         ny = int(np.prod(t[op.dst][:3])) * t[op.src][3]
         return ny * (D + 4) + nx * D
+    if op_kind == "maxpool_relu_bwd":         # + read the ReLU output y, write dpre
+        nx = int(np.prod(t[op.src]))
+        ny = int(np.prod(t[op.dst][:3])) * t[op.src][3]
+        return ny * (D + 4) + 2 * nx * D
     raise KeyError(op_kind)
 
 
@@ -119,6 +126,38 @@ class EventTrace:
             self.open = (event, op, s)
 
 
+def gemm_reference(net, torch):
+    """Vendor-library bf16 GEMMs with the (M, N, K) of every convolution direction, for reference only."""
+    def t(fn, it=20):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(it):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / it * 1e3
+    out = {}
+    for op in net.convs:
+        n, h, w, c = net.tensors[op.src]
+        _, oh, ow, k = net.tensors[op.dst][:3] + (op.cout,)
+        M, N, K = n * oh * ow, op.cout, op.kh * op.kw * c
+        fl = 2.0 * M * N * K
+        A = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
+        B = torch.randn(K, N, device="cuda", dtype=torch.bfloat16)
+        G = torch.randn(M, N, device="cuda", dtype=torch.bfloat16)
+        Bt, At = B.t().contiguous(), A.t().contiguous()
+        us = {"fwd [M,K]x[K,N]": t(lambda: A @ B), "bwd_input [M,N]x[N,K]": t(lambda: G @ Bt),
+              "bwd_filter [K,M]x[M,N]": t(lambda: At @ G)}
+        out[op.name] = {"M": M, "N": N, "K": K,
+                        "us": {k2: round(v, 1) for k2, v in us.items()},
+                        "tflops": {k2: round(fl / v / 1e6, 1) for k2, v in us.items()}}
+        del A, B, G, Bt, At
+    print(json.dumps({"gemm_reference": out}))
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -142,6 +181,9 @@ def main():
         print(json.dumps({"calibration_copy_bytes_read": n * 4, "calibration_copy_bytes_written": n * 4}))
         return
     net = W.alexnet(batch=args.batch)
+    if args.gemm_reference:
+        gemm_reference(net, torch)
+        return
     inp = W.make_inputs(net, seed=args.seed)
     rep = Replica(net, inp)
     D = 2
@@ -214,16 +256,21 @@ def main():
             launches += 1
     conv_flop = sum(flops.values())
     conv_tflops = conv_flop / (conv_ms * 1e-3) / 1e12
-    ew_kinds = ("bias_relu_fwd", "bias_relu_bwd", "maxpool_fwd", "maxpool_bwd")
+    ew_kinds = ("bias_relu_fwd", "bias_relu_bwd", "maxpool_fwd", "maxpool_bwd", "maxpool_relu_bwd")
     ew_bytes = {k: 0.0 for k in ew_kinds}
     for op in net.ops:
-        for k in ew_kinds:
-            if k not in per_kind:
-                continue        # fused into another kernel (bias + ReLU forward runs in the conv epilogue)
-            if (k.startswith("bias") and hasattr(op, "cout")) or (k.startswith("maxpool") and not hasattr(op, "cout")):
-                if k == "maxpool_bwd" and op.src == "x":
-                    continue
-                ew_bytes[k] += elementwise_bytes(net, k, op, D)
+        # the kinds this op actually ran as (bias + ReLU forward runs in the conv epilogue; a pool
+        # fused with the ReLU backward of its producer replaces that conv's bias_relu_bwd)
+        if hasattr(op, "cout"):
+            kinds = [] if op.name in rep.relu_fused else ["bias_relu_bwd"]
+        else:
+            kinds = ["maxpool_fwd"]
+            if op.name in rep.pool_relu:
+                kinds.append("maxpool_relu_bwd")
+            elif op.src != "x":
+                kinds.append("maxpool_bwd")
+        for k in kinds:
+            ew_bytes[k] += elementwise_bytes(net, k, op, D)
     sgd_bytes = rep.n_params * 14.0
     ew_ms = sum(per_kind.get(k, 0.0) for k in ew_kinds) + per_kind.get("apply_sgd", 0.0)
     ew_gbs = (sum(ew_bytes.values()) + sgd_bytes) / (ew_ms * 1e-3) / 1e9

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 2
+#define TFK_ABI_VERSION 3
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -202,6 +202,27 @@ TFK_API tfk_status tfk_maxpool_fwd(const void *x, tfk_nhwc xd, tfk_window p, tfk
  */
 TFK_API tfk_status tfk_maxpool_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p,
                            tfk_dtype dt, void *dx, tfk_nhwc xd, float beta, void *stream);
+
+/*
+ * MaxPool backward, ReLU backward and the bias gradient fused into one pass (the
+ * hand-fused activation-gradient kernels of Section 5), for a max-pool whose input y is the
+ * output of BiasAdd + ReLU:
+ *   g[i]     = beta * dpre[i] + sum over pool outputs o with argmax[o] == i of dy[o]
+ *   dpre[i]  = y[i] > 0 ? g[i] : +0              (element i of the pool input, dense index)
+ *   dbias[c] = sum over the pixels of dpre[., c]  (of the stored values; fp32)
+ * It equals tfk_maxpool_bwd(dy, argmax, ..., dx = dpre, beta) followed by
+ * tfk_bias_relu_bwd(y, dpre, ...), with the pool gradient rounded once instead of twice.
+ *   dy, argmax, yd, p : the max-pool's output gradient, its tfk_maxpool_fwd argmax and window.
+ *   y     : xd-shaped pool input (the ReLU output), element type dt; read only.
+ *   dpre  : xd-shaped, written (read first when beta = 1, which adds the gradient the other
+ *           consumers of y already stored there); must not overlap y, dy or argmax.
+ *   dbias : xd.c fp32 values, overwritten.
+ *   ws    : at least tfk_bias_relu_bwd_workspace_bytes(xd, dt) bytes.
+ * Requirements: beta is 0 or 1; xd.c <= 16384.  xd.n == 0 sets dbias to 0.
+ */
+TFK_API tfk_status tfk_maxpool_bwd_relu_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p,
+                                    tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd, float beta,
+                                    float *dbias, void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------- update
  * ApplyGradientDescent, in place (Section 4.1: W' = W - alpha * dL/dW written

@@ -392,6 +392,44 @@ tfk_status tfk_maxpool_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, t
                       "maxpool_bwd");
 }
 
+tfk_status tfk_maxpool_bwd_relu_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
+                                    const void *y, void *dpre, tfk_nhwc xd, float beta, float *dbias, void *ws,
+                                    size_t ws_bytes, void *stream) {
+    PoolGeom g;
+    TRY(check_pool(xd, p, dt, yd, "y", "dy", g));
+    if (!(beta == 0.f || beta == 1.f)) return fail(TFK_ERR_ARG, "beta must be 0 or 1");
+    if (xd.c > 16384) return fail(TFK_ERR_SHAPE, "maxpool_bwd_relu_bwd supports at most 16384 channels");
+    TRY(need_ptr(dbias, "dbias"));
+    TRY(need_align(dbias, 4, "dbias"));
+    hipStream_t st = (hipStream_t)stream;
+    if (xd.n == 0) return hip_status(launch_fill_zero(dbias, xd.c, st), "maxpool_bwd_relu_bwd");
+    const int64_t es = esize(dt);
+    TRY(need_ptr(dy, "dy"));
+    TRY(need_ptr(argmax, "argmax"));
+    TRY(need_ptr(y, "y"));
+    TRY(need_ptr(dpre, "dpre"));
+    TRY(need_align(dy, es, "dy"));
+    TRY(need_align(y, es, "y"));
+    TRY(need_align(dpre, es, "dpre"));
+    TRY(need_align(argmax, 4, "argmax"));
+    const int64_t xb = view_bytes(xd, es), yb = view_bytes(yd, es);
+    const int64_t ab = (int64_t)yd.n * yd.h * yd.w * yd.c * 4, bb = (int64_t)xd.c * 4;
+    if (overlap(dpre, xb, y, xb) || overlap(dpre, xb, dy, yb) || overlap(dpre, xb, argmax, ab))
+        return fail(TFK_ERR_ALIAS, "dpre overlaps y, dy or argmax");
+    if (overlap(dbias, bb, y, xb) || overlap(dbias, bb, dy, yb) || overlap(dbias, bb, dpre, xb) ||
+        overlap(dbias, bb, argmax, ab))
+        return fail(TFK_ERR_ALIAS, "dbias overlaps a tensor");
+    const size_t need = tfk_bias_relu_bwd_workspace_bytes(xd, dt);
+    TRY(check_ws(ws, ws_bytes, need));
+    if (overlap(ws, (int64_t)need, y, xb) || overlap(ws, (int64_t)need, dy, yb) ||
+        overlap(ws, (int64_t)need, dpre, xb) || overlap(ws, (int64_t)need, dbias, bb) ||
+        overlap(ws, (int64_t)need, argmax, ab))
+        return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
+    return hip_status(launch_maxpool_relu_bwd(dt == TFK_F32 ? 0 : 1, dy, argmax, g, y, dpre, beta, dbias, (float *)ws,
+                                              st),
+                      "maxpool_bwd_relu_bwd");
+}
+
 // ------------------------------------------------------------------ SGD
 static tfk_status check_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh) {
     if (n < 0) return fail(TFK_ERR_SHAPE, "n must be >= 0");

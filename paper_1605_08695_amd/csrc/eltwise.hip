@@ -263,6 +263,91 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T *__restrict__ 
 // ------------------------------------------------------------------ max-pool backward
 // Gather form: each input element visits the windows that contain it in
 // ascending output order and adds the gradients routed to it.
+// s[e] (e < EPC) = sum of dy over the windows whose argmax is input element
+// pix * C + cv * EPC + e, pixel pix = (n, h, w) of the pool input.
+template <typename T, bool VEC>
+__device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const int32_t *__restrict__ argmax,
+                                            const PoolGeom &g, int n, int h, int w, int64_t pix, int cv,
+                                            float *s) {
+    constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
+    const int32_t self = (int32_t)(pix * g.C + cv * EPC);
+    if constexpr (VEC) {
+        if (g.KH <= 2 * g.sh && g.KW <= 2 * g.sw) {
+            // At most 2 x 2 windows contain the element: issue every argmax and dy load of
+            // all four candidates first (clamped to a valid window, masked afterwards), so
+            // the gather costs one memory round trip instead of one or two per window.
+            const int hp = h + g.pt, wp = w + g.pl;
+            const int oh_lo = hp - g.KH + 1 <= 0 ? 0 : (hp - g.KH + 1 + g.sh - 1) / g.sh;
+            const int oh_hi = min(g.OH - 1, hp / g.sh);
+            const int ow_lo = wp - g.KW + 1 <= 0 ? 0 : (wp - g.KW + 1 + g.sw - 1) / g.sw;
+            const int ow_hi = min(g.OW - 1, wp / g.sw);
+            // (an element no window reaches has oh_lo > oh_hi; its loads go to the last window)
+            const int ohc = min(oh_lo, g.OH - 1), owc = min(ow_lo, g.OW - 1);
+            int32_t ai[4][EPC];
+            U4 dv[4];
+            bool valid[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int oh = oh_lo + (q >> 1), ow = ow_lo + (q & 1);
+                valid[q] = oh <= oh_hi && ow <= ow_hi;
+                const int64_t opix = ((int64_t)n * g.OH + (valid[q] ? oh : ohc)) * g.OW + (valid[q] ? ow : owc);
+                const int32_t *am = argmax + opix * g.C + cv * EPC;
+#pragma unroll
+                for (int e = 0; e < EPC; e += 4) {
+                    const int4 v = *reinterpret_cast<const int4 *>(am + e);
+                    ai[q][e] = v.x; ai[q][e + 1] = v.y; ai[q][e + 2] = v.z; ai[q][e + 3] = v.w;
+                }
+                dv[q] = *reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC);
+            }
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) s[e] = 0.f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {             // windows in ascending output order
+                float v[EPC];
+                chunk_to_f32<T>(dv[q], v);
+#pragma unroll
+                for (int e = 0; e < EPC; ++e)
+                    if (valid[q] && ai[q][e] == self + e) s[e] += v[e];
+            }
+            return;
+        }
+    }
+    // windows oh with oh*sh - pt <= h <= oh*sh - pt + KH - 1
+    const int hp = h + g.pt, wp = w + g.pl;
+    const int oh_lo = hp - g.KH + 1 <= 0 ? 0 : (hp - g.KH + 1 + g.sh - 1) / g.sh;
+    const int oh_hi = min(g.OH - 1, hp / g.sh);
+    const int ow_lo = wp - g.KW + 1 <= 0 ? 0 : (wp - g.KW + 1 + g.sw - 1) / g.sw;
+    const int ow_hi = min(g.OW - 1, wp / g.sw);
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) s[e] = 0.f;
+    for (int oh = oh_lo; oh <= oh_hi; ++oh) {
+        for (int ow = ow_lo; ow <= ow_hi; ++ow) {
+            const int64_t opix = ((int64_t)n * g.OH + oh) * g.OW + ow;
+            if constexpr (VEC) {
+                const int32_t *am = argmax + opix * g.C + cv * EPC;
+                int32_t ai[EPC];
+#pragma unroll
+                for (int e = 0; e < EPC; e += 4) {
+                    const int4 q = *reinterpret_cast<const int4 *>(am + e);
+                    ai[e] = q.x; ai[e + 1] = q.y; ai[e + 2] = q.z; ai[e + 3] = q.w;
+                }
+                bool any = false;
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) any |= (ai[e] == self + e);
+                if (any) {
+                    float v[EPC];
+                    chunk_to_f32<T>(*reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC), v);
+#pragma unroll
+                    for (int e = 0; e < EPC; ++e)
+                        if (ai[e] == self + e) s[e] += v[e];
+                }
+            } else {
+                if (argmax[opix * g.C + cv] == self) s[0] += Elem<T>::load(dy + opix * g.ys + cv);
+            }
+        }
+    }
+}
+
 template <typename T, bool VEC>
 __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T *__restrict__ dy,
                                                           const int32_t *__restrict__ argmax, PoolGeom g,
@@ -275,42 +360,8 @@ __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T *__restrict__ 
         int cv, w, h, n;
         int64_t pix;
         decode(dec, t, cv, pix, w, h, n);
-        const int32_t self = (int32_t)(pix * g.C + cv * EPC);
-        // windows oh with oh*sh - pt <= h <= oh*sh - pt + KH - 1
-        const int hp = h + g.pt, wp = w + g.pl;
-        const int oh_lo = hp - g.KH + 1 <= 0 ? 0 : (hp - g.KH + 1 + g.sh - 1) / g.sh;
-        const int oh_hi = min(g.OH - 1, hp / g.sh);
-        const int ow_lo = wp - g.KW + 1 <= 0 ? 0 : (wp - g.KW + 1 + g.sw - 1) / g.sw;
-        const int ow_hi = min(g.OW - 1, wp / g.sw);
         float s[EPC];
-#pragma unroll
-        for (int e = 0; e < EPC; ++e) s[e] = 0.f;
-        for (int oh = oh_lo; oh <= oh_hi; ++oh) {
-            for (int ow = ow_lo; ow <= ow_hi; ++ow) {
-                const int64_t opix = ((int64_t)n * g.OH + oh) * g.OW + ow;
-                if constexpr (VEC) {
-                    const int32_t *am = argmax + opix * g.C + cv * EPC;
-                    int32_t ai[EPC];
-#pragma unroll
-                    for (int e = 0; e < EPC; e += 4) {
-                        const int4 q = *reinterpret_cast<const int4 *>(am + e);
-                        ai[e] = q.x; ai[e + 1] = q.y; ai[e + 2] = q.z; ai[e + 3] = q.w;
-                    }
-                    bool any = false;
-#pragma unroll
-                    for (int e = 0; e < EPC; ++e) any |= (ai[e] == self + e);
-                    if (any) {
-                        float v[EPC];
-                        chunk_to_f32<T>(*reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC), v);
-#pragma unroll
-                        for (int e = 0; e < EPC; ++e)
-                            if (ai[e] == self + e) s[e] += v[e];
-                    }
-                } else {
-                    if (argmax[opix * g.C + cv] == self) s[0] += Elem<T>::load(dy + opix * g.ys + cv);
-                }
-            }
-        }
+        pool_gather<T, VEC>(dy, argmax, g, n, h, w, pix, cv, s);
         T *out = dx + pix * g.xs + cv * EPC;
         if constexpr (VEC) {
             if (beta != 0.f) {
@@ -324,6 +375,80 @@ __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T *__restrict__ 
             if (beta != 0.f) s[0] += beta * Elem<T>::load(out);
             Elem<T>::store(out, s[0]);
         }
+    }
+}
+
+// ------------------------------------------------------------------ max-pool + ReLU + bias backward
+// One pass over the pool input (= the ReLU output y of the convolution before it):
+//   dpre = (y > 0) ? (beta * dpre + sum of routed dy) : 0,   db[c] = sum over pixels of dpre.
+// The thread layout and the fixed-order bias-gradient reduction are those of
+// relu_bwd_partial_kernel: block b owns pixels [b ppb, (b+1) ppb), thread t channel chunk
+// t % CVB (+ CVB ...) and pixel rows t / CVB (+ R ...); db sums the stored (rounded) dpre,
+// the tensor the filter gradient is formed from.
+template <typename T, bool VEC>
+__global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *__restrict__ dy,
+                                                                       const int32_t *__restrict__ argmax,
+                                                                       PoolGeom g, const T *__restrict__ y, T *dpre,
+                                                                       float beta, int64_t ppb, FastDiv dW, FastDiv dH,
+                                                                       float *__restrict__ partial) {
+    constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
+    extern __shared__ float red[];                 // [R][C]
+    const int C = g.C;
+    const int CV = C / EPC;
+    const int CVB = CV < 256 ? CV : 256;
+    const int R = 256 / CVB;
+    const int t = threadIdx.x;
+    const int lane_cv = t % CVB;
+    const int row = t / CVB;
+    const int64_t P = (int64_t)g.N * g.H * g.W;
+    const int64_t p0 = (int64_t)blockIdx.x * ppb;
+    const int64_t p1 = min(P, p0 + ppb);
+    const bool active = row < R;
+    for (int cv = lane_cv; cv < CV; cv += CVB) {
+        float acc[EPC];
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
+        if (active) {
+            for (int64_t p = p0 + row; p < p1; p += R) {
+                uint32_t q, w, n, h;
+                dW.divmod((uint32_t)p, q, w);
+                dH.divmod(q, n, h);
+                float s[EPC];
+                pool_gather<T, VEC>(dy, argmax, g, (int)n, (int)h, (int)w, p, cv, s);
+                const int64_t off = p * g.xs + (int64_t)cv * EPC;
+                if constexpr (VEC) {
+                    float fy[EPC];
+                    chunk_to_f32<T>(*reinterpret_cast<const U4 *>(y + off), fy);
+                    if (beta != 0.f) {
+                        float o[EPC];
+                        chunk_to_f32<T>(*reinterpret_cast<const U4 *>(dpre + off), o);
+#pragma unroll
+                        for (int e = 0; e < EPC; ++e) s[e] += beta * o[e];
+                    }
+#pragma unroll
+                    for (int e = 0; e < EPC; ++e) s[e] = fy[e] > 0.f ? s[e] : 0.f;
+                    const U4 packed = f32_to_chunk<T>(s);
+                    *reinterpret_cast<U4 *>(dpre + off) = packed;
+                    float st[EPC];
+                    chunk_to_f32<T>(packed, st);           // the stored values
+#pragma unroll
+                    for (int e = 0; e < EPC; ++e) acc[e] += st[e];
+                } else {
+                    if (beta != 0.f) s[0] += beta * Elem<T>::load(dpre + off);
+                    const float v = Elem<T>::load(y + off) > 0.f ? s[0] : 0.f;
+                    Elem<T>::store(dpre + off, v);
+                    acc[0] += Elem<T>::load(dpre + off);
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) red[row * C + cv * EPC + e] = acc[e];
+        }
+    }
+    __syncthreads();
+    for (int c = t; c < C; c += 256) {
+        float a = 0.f;
+        for (int r = 0; r < R; ++r) a += red[r * C + c];
+        partial[(int64_t)c * gridDim.x + blockIdx.x] = a;
     }
 }
 
@@ -461,8 +586,10 @@ void relu_bwd_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *ppb) {
     const int CV = vec ? C / EPC : C;
     const int CVB = CV < 256 ? CV : 256;
     const int R = 256 / CVB;
-    int64_t g = (P + (int64_t)R * 8 - 1) / ((int64_t)R * 8);    // >= 8 pixel rows per thread
-    const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(1024, (1 << 21) / std::max(C, 1)));
+    // about 4 pixel rows per thread: the rows of one thread are a chain of dependent loads
+    // (with the fused max-pool gather, argmax then dy), so parallelism comes from the grid
+    int64_t g = (P + (int64_t)R * 4 - 1) / ((int64_t)R * 4);
+    const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(4096, (1 << 22) / std::max(C, 1)));
     if (g > cap) g = cap;
     if (g < 1) g = 1;
     *G = (int)g;
@@ -495,6 +622,37 @@ hipError_t launch_bias_relu_bwd(int dt, const void *y, const void *dy, void *dpr
                                 int64_t ys, float *db, float *ws, hipStream_t st) {
     return dt == 0 ? relu_bwd_t<float>(y, dy, dpre, P, C, ys, db, ws, st)
                    : relu_bwd_t<bf16_t>(y, dy, dpre, P, C, ys, db, ws, st);
+}
+
+template <typename T>
+static hipError_t maxpool_relu_bwd_t(const void *dy, const int32_t *am, const PoolGeom &g, const void *y, void *dpre,
+                                     float beta, float *db, float *ws, hipStream_t st) {
+    constexpr int EPC = Elem<T>::kPerChunk;
+    const bool vec = g.C % EPC == 0 && g.xs % EPC == 0 && g.ys % EPC == 0 && aligned16(dy) && aligned16(am) &&
+                     aligned16(y) && aligned16(dpre);
+    const int64_t P = (int64_t)g.N * g.H * g.W;
+    int G;
+    int64_t ppb;
+    relu_bwd_plan(sizeof(T) == 4 ? 0 : 1, P, g.C, g.xs, &G, &ppb);
+    const int CV = vec ? g.C / EPC : g.C;
+    const int CVB = CV < 256 ? CV : 256;
+    const int R = 256 / CVB;
+    const size_t smem = (size_t)R * g.C * sizeof(float);
+    const FastDiv dW((uint32_t)g.W), dH((uint32_t)g.H);
+    if (vec)
+        hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, true>), dim3(G), dim3(256), smem, st, (const T *)dy, am,
+                           g, (const T *)y, (T *)dpre, beta, ppb, dW, dH, ws);
+    else
+        hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, false>), dim3(G), dim3(256), smem, st, (const T *)dy,
+                           am, g, (const T *)y, (T *)dpre, beta, ppb, dW, dH, ws);
+    hipLaunchKernelGGL(sum_partials_kernel, dim3(g.C), dim3(256), 0, st, ws, G, g.C, db);
+    return hipGetLastError();
+}
+
+hipError_t launch_maxpool_relu_bwd(int dt, const void *dy, const int32_t *am, const PoolGeom &g, const void *y,
+                                   void *dpre, float beta, float *db, float *ws, hipStream_t st) {
+    return dt == 0 ? maxpool_relu_bwd_t<float>(dy, am, g, y, dpre, beta, db, ws, st)
+                   : maxpool_relu_bwd_t<bf16_t>(dy, am, g, y, dpre, beta, db, ws, st);
 }
 
 template <typename T>

@@ -16,7 +16,7 @@ import torch
 from ._lib import Nhwc, TfkError, Window, TFK_BF16, TFK_F32, check, load
 
 __all__ = ["conv2d_fwd", "conv2d_fwd_bias_relu", "conv2d_bwd_input", "conv2d_bwd_filter", "conv2d_workspace_bytes", "bias_relu_fwd",
-           "bias_relu_bwd", "bias_relu_bwd_workspace_bytes", "maxpool_fwd", "maxpool_bwd", "apply_sgd",
+           "bias_relu_bwd", "bias_relu_bwd_workspace_bytes", "maxpool_fwd", "maxpool_bwd", "maxpool_bwd_relu_bwd", "apply_sgd",
            "apply_sgd_multi", "out_len", "nhwc", "window", "TfkError", "abi_version"]
 
 
@@ -194,6 +194,29 @@ def maxpool_bwd(dy, argmax, dx, kernel_hw, stride, pads, beta=0.0, stream=None):
     check(load().tfk_maxpool_bwd(_ptr(dy), _ptr(argmax), nhwc(dy), window(kh, kw, stride, pads), _dt(dy),
                                  _ptr(dx), nhwc(dx), float(beta), _stream(stream)))
     return dx
+
+
+def maxpool_bwd_relu_bwd(dy, argmax, y, dpre, kernel_hw, stride, pads, beta=0.0, dbias=None, ws=None, stream=None):
+    """dpre = (y > 0) * (beta * dpre + max-pool gradient of dy), dbias = column sums of dpre (fp32).
+
+    y is the pool input (the ReLU output); dpre has its shape and view.
+    """
+    lib = load()
+    kh, kw = kernel_hw
+    if not argmax.is_contiguous() or argmax.dtype != torch.int32:
+        raise ValueError("argmax must be a dense int32 tensor")
+    if dbias is None:
+        dbias = torch.empty(y.shape[3], dtype=torch.float32, device=y.device)
+    d_y, d_p = nhwc(y), nhwc(dpre)
+    if (d_y.n, d_y.h, d_y.w, d_y.c, d_y.pixel_stride) != (d_p.n, d_p.h, d_p.w, d_p.c, d_p.pixel_stride):
+        raise ValueError("y and dpre must share one view (extents and pixel stride)")
+    need = lib.tfk_bias_relu_bwd_workspace_bytes(d_y, _dt(y))
+    if ws is None or ws.numel() < need:
+        ws = _ws(need, y.device)
+    check(lib.tfk_maxpool_bwd_relu_bwd(_ptr(dy), _ptr(argmax), nhwc(dy), window(kh, kw, stride, pads), _dt(dy),
+                                       _ptr(y), _ptr(dpre), d_y, float(beta), _ptr(dbias), _ptr(ws), need,
+                                       _stream(stream)))
+    return dpre, dbias
 
 
 # ----------------------------------------------------------------------------- update

@@ -22,6 +22,11 @@ Memory layout (all on one GPU):
   and read back the same way, so no concat or split is ever copied.
 * Gradients: one NHWC buffer per tensor (ReLU-backward writes its result over
   the incoming gradient, except for the seed ``g`` which stays intact).
+
+A max-pool whose input is the whole output of one convolution and is read by
+nothing else runs its backward fused with that convolution's ReLU backward and
+bias gradient (one kernel writes dL/d(pre-activation) directly, Section 5's
+fused activation gradients); that convolution then skips its own ReLU backward.
 """
 from __future__ import annotations
 
@@ -102,6 +107,19 @@ class Replica:
         self.argmax = {op.name: torch.zeros(net.tensors[op.dst][:3] + (net.tensors[op.src][3],),
                                             dtype=torch.int32, device=dev)
                        for op in net.ops if isinstance(op, Pool)}
+        # ---- max-pools fused with the ReLU backward of the convolution that feeds them
+        writers, readers = {}, {}
+        for op in net.ops:
+            writers.setdefault(op.dst, []).append(op)
+            readers.setdefault(op.src, []).append(op)
+        self.pool_relu = {}                      # pool name -> conv
+        for op in net.ops:
+            if isinstance(op, Pool):
+                w = writers.get(op.src, [])
+                if (len(w) == 1 and isinstance(w[0], Conv) and w[0].dst_c0 == 0
+                        and w[0].cout == net.tensors[op.src][3] and len(readers[op.src]) == 1):
+                    self.pool_relu[op.name] = w[0]
+        self.relu_fused = {c.name for c in self.pool_relu.values()}
         # ---- one workspace big enough for every op
         need = 0
         for c in net.convs:
@@ -143,11 +161,14 @@ class Replica:
             src_grad = op.src != "x" or net.input_grad
             beta = 1.0 if op.src in written else 0.0
             if isinstance(op, Conv):
-                y = self._slice(self.act, op)
-                dpre = self._slice({op.dst: self.dpre_out}, op) if op.dst == net.output else dy
-                if trace: trace("bias_relu_bwd", op, y=y, dy=dy)
-                ops.bias_relu_bwd(y, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
-                if trace: trace("bias_relu_bwd:end", op, dpre=dpre, db=self.db[op.name])
+                if op.name in self.relu_fused:
+                    dpre = dy                        # written by the fused max-pool backward
+                else:
+                    y = self._slice(self.act, op)
+                    dpre = self._slice({op.dst: self.dpre_out}, op) if op.dst == net.output else dy
+                    if trace: trace("bias_relu_bwd", op, y=y, dy=dy)
+                    ops.bias_relu_bwd(y, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
+                    if trace: trace("bias_relu_bwd:end", op, dpre=dpre, db=self.db[op.name])
                 x = self.act[op.src]
                 if trace: trace("conv_bwd_filter", op, x=x, dy=dpre)
                 ops.conv2d_bwd_filter(x, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, dw=self.dW[op.name],
@@ -159,6 +180,13 @@ class Replica:
                     ops.conv2d_bwd_input(dpre, self.Wlp[op.name], dx, (op.sh, op.sw), op.pads, beta=beta,
                                          stream=stream)
                     if trace: trace("conv_bwd_input:end", op, dx=dx)
+            elif op.name in self.pool_relu:
+                conv = self.pool_relu[op.name]
+                y, dpre, am = self.act[op.src], self.grad[op.src], self.argmax[op.name]
+                if trace: trace("maxpool_relu_bwd", op, dy=dy, argmax=am, y=y, dpre=dpre, beta=beta)
+                ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
+                                         dbias=self.db[conv.name], ws=self.ws, stream=stream)
+                if trace: trace("maxpool_relu_bwd:end", op, dpre=dpre, db=self.db[conv.name])
             else:
                 if src_grad:
                     dx = self.grad[op.src]

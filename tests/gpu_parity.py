@@ -238,6 +238,16 @@ class ParityTracer:
         ref = oracle.maxpool_bwd(dy, am.astype(np.int32), dx_old.shape, dx=dx_old, beta=inp["beta"])
         self.record_tensor("maxpool_bwd", op.name, self._x64(out["dx"]), ref, self.dtype)
 
+    def _check_maxpool_relu_bwd(self, op, inp, out):
+        # whole tensors: the bias gradient sums over every image
+        y = f64(inp["y"])
+        am = inp["argmax"].cpu().numpy()
+        dpre_old = f64(inp["dpre"])
+        g = oracle.maxpool_bwd(f64(inp["dy"]), am, y.shape, dx=dpre_old, beta=inp["beta"])
+        ref_dpre, ref_db = oracle.bias_relu_bwd(y, g)
+        self.record_tensor("maxpool_relu_bwd", op.name, f64(out["dpre"]), ref_dpre, self.dtype)
+        self.record_tensor("maxpool_relu_bwd:db", op.name, f64(out["db"]), ref_db, torch.float32)
+
     def _check_apply_sgd(self, op, inp, out):
         var, grad = inp["var"].cpu().numpy(), inp["grad"].cpu().numpy()
         ref = oracle.apply_sgd(var.astype(np.float64), grad.astype(np.float64), self.lr)

@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 2
+    assert lib.tfk_abi_version() == 3
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -127,6 +127,21 @@ def test_bias_relu_validation(lib):
     assert st == WORKSPACE
     st = lib.tfk_bias_relu_fwd(vp(P), yd, vp(0), BF16, None)
     assert st == NULL
+
+
+def test_maxpool_relu_bwd_validation(lib):
+    W = Window(3, 3, 2, 2, 0, 0, 0, 0)
+    yd, xd = Nhwc(2, 3, 3, 8, 0), Nhwc(2, 7, 7, 8, 0)
+    def fused(dy=P, am=P + 0x100000, y=P + 0x200000, dpre=P + 0x300000, beta=0.0, db=P + 0x400000, ws=P + 0x500000,
+              ws_bytes=1 << 20, x=xd):
+        return lib.tfk_maxpool_bwd_relu_bwd(vp(dy), vp(am), yd, W, BF16, vp(y), vp(dpre), x, ctypes.c_float(beta),
+                                            vp(db), vp(ws), ws_bytes, None)
+    assert fused(db=0) == NULL
+    assert fused(beta=0.5) == ARG
+    assert fused(dpre=P + 0x200010) == ALIAS                           # dpre overlaps y
+    assert fused(x=Nhwc(2, 9, 9, 8, 0)) == SHAPE                        # 9 -> 4 with a 3x3/2 window, not 3
+    assert fused(ws_bytes=0) == WORKSPACE
+    assert fused(ws=P + 0x300000) == ALIAS                              # workspace inside dpre
 
 
 def test_sgd_validation(lib):

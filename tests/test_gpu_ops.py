@@ -176,6 +176,9 @@ POOL_CASES = [
     ("branch_3s1", (2, 6, 5, 8), 3, 1, (1, 1, 1, 1)),
     ("odd_c", (2, 8, 8, 5), 2, 2, (0, 0, 0, 0)),
     ("vgg_2s2", (2, 14, 14, 128), 2, 2, (0, 0, 0, 0)),
+    # trailing rows/columns that no window reaches (gradient 0 there)
+    ("uncovered_tail_3s2", (2, 8, 10, 16), 3, 2, (0, 0, 0, 0)),
+    ("uncovered_tail_2s2", (2, 9, 7, 8), 2, 2, (0, 0, 0, 0)),
 ]
 
 
@@ -202,6 +205,32 @@ def test_maxpool(case, dtype, ties):
         torch.cuda.synchronize()
         ref = oracle.maxpool_bwd(f64(dy), ref_am, shape, dx=old, beta=beta)
         assert_close(f64(dx), ref, dtype, label="maxpool_bwd beta=%g" % beta)
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
+@pytest.mark.parametrize("case", POOL_CASES, ids=[c[0] for c in POOL_CASES])
+def test_maxpool_relu_bwd_fused(case, dtype):
+    """Fused max-pool backward + ReLU backward + bias gradient against the oracle's two ops."""
+    name, shape, k, s, pads = case
+    rng = np.random.default_rng(29)
+    # the pool input is a ReLU output: exact zeros (masked, and ties inside windows)
+    y = torch.from_numpy(np.maximum(rng.standard_normal(shape), 0.0)).to(dtype).to(DEV)
+    out, am = ops.maxpool_fwd(y, (k, k), s, pads)
+    dy = _mk(out.shape, dtype, rng)
+    torch.cuda.synchronize()
+    ref_am = am.cpu().numpy()
+    for beta in (0.0, 1.0):
+        dpre = _mk(shape, dtype, rng)
+        old = f64(dpre)
+        _, db = ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (k, k), s, pads, beta=beta)
+        torch.cuda.synchronize()
+        g = oracle.maxpool_bwd(f64(dy), ref_am, shape, dx=old, beta=beta)
+        ref_dpre, ref_db = oracle.bias_relu_bwd(f64(y), g)
+        assert_close(f64(dpre), ref_dpre, dtype, label="fused dpre beta=%g" % beta)
+        assert np.all(f64(dpre)[f64(y) <= 0] == 0), "masked entries must be exactly zero"
+        assert_close(f64(db), ref_db, torch.float32, dtype, label="fused db beta=%g" % beta)
+        # the bias gradient is the column sum of the stored dpre (fp32 accumulation of it)
+        assert err(f64(db), f64(dpre).sum(axis=(0, 1, 2))) <= 1e-4
 
 
 @pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
