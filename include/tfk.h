@@ -99,6 +99,11 @@ typedef struct {
  *   ws  : workspace of at least tfk_conv2d_workspace_bytes(0, ...) bytes
  *         (may be NULL when that is 0).
  * Requirements: pad < kernel extent on every side.
+ * Image inputs (bf16, 1-4 channels) run as an equivalent 8-channel convolution over the
+ * input padded to 4 (or 8) channels.  When x is already stored that way -- e.g. a
+ * 3-channel view with pixel_stride 4 of an RGBx buffer, 16-byte aligned -- it is read in
+ * place and not copied; the channels past xd.c then meet zero filter weights and must
+ * hold finite values.  The same holds for tfk_conv2d_bwd_filter.
  */
 TFK_API tfk_status tfk_conv2d_fwd(const void *x, tfk_nhwc xd, const void *w, int32_t cout,
                           tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
@@ -143,6 +148,8 @@ TFK_API tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void
  *   dw  : dense fp32 HWIO [p.kh][p.kw][xd.c][dyd.c], overwritten.
  *   ws  : at least tfk_conv2d_workspace_bytes(2, ...) bytes (split-K partial sums,
  *         reduced in a fixed order).
+ * An image input stored with its pixels 4 (or 8) channels apart is read in place as
+ * described at tfk_conv2d_fwd (the channels past xd.c must be finite).
  */
 TFK_API tfk_status tfk_conv2d_bwd_filter(const void *x, tfk_nhwc xd, const void *dy, tfk_nhwc dyd,
                                  tfk_window p, tfk_dtype dt, float *dw,

@@ -91,6 +91,7 @@ static hipError_t conv_bwd_filter_t(const void *x, int64_t xs, const void *dy, i
     if (v2) {
         a.out = p.splits > 1 ? ws : (void *)dw;
         a.k_split = p.k_split;
+        a.xcd_order = 0;
         e = igemm2_launch<DIR_BWD_FILTER>(a, m, p.splits, p.t, st) ? hipGetLastError() : hipErrorInvalidValue;
     } else {
         p = bwf_plan(dti, s, false);

@@ -2,9 +2,10 @@
 // on RGB images) in bf16, rewritten as an equivalent convolution that the
 // pipelined 16-byte-chunk kernels can run.
 //
-// The input is copied with its channels zero-padded to Cp (4 for RGB), and F =
-// 8 / Cp horizontally adjacent pixels are read as one "virtual pixel" of 8
-// channels (the same bytes: [N][H][W][Cp] is [N][H][W/F][F*Cp]).  With
+// The input is copied with its channels zero-padded to Cp (4 for RGB) -- or read in
+// place when its pixels are already Cp channels apart -- and F = 8 / Cp horizontally
+// adjacent pixels are read as one "virtual pixel" of 8 channels (the same bytes:
+// [N][H][W][Cp] is [N][H][W/F][F*Cp]).  With
 // F | stride_w, F | pad_left and F | W, the column tap kw = F j + p of output
 // column ow reads virtual column ow (stride_w/F) - pad_left/F + j, element p of
 // the pair.  So the convolution equals one over the virtual image with
@@ -154,6 +155,11 @@ bool pad_vec_dispatch(int C, int Cp, const bf16_t *x, int64_t groups, bf16_t *xp
     return false;
 }
 
+// The padded input the virtual convolution reads: x itself when its pixels are already Cp
+// channels apart (a C-channel view of a Cp-channel buffer: the channels past C meet zero
+// filter weights, so they only have to be finite), else a padded copy in the workspace.
+const bf16_t *padded_input(const void *x, int64_t npix, int C, int64_t xs, int Cp, bf16_t *xp, hipStream_t st);
+
 void pad_channels(const void *x, int64_t npix, int C, int64_t xs, int Cp, bf16_t *xp, hipStream_t st) {
     const bf16_t *xb = reinterpret_cast<const bf16_t *>(x);
     int64_t done = 0;
@@ -163,6 +169,12 @@ void pad_channels(const void *x, int64_t npix, int C, int64_t xs, int Cp, bf16_t
     if (done < npix)
         hipLaunchKernelGGL(pad_channels_kernel, dim3(grid_of((npix - done) * Cp)), dim3(256), 0, st,
                            xb + done * xs, npix - done, C, xs, Cp, xp + done * Cp);
+}
+
+const bf16_t *padded_input(const void *x, int64_t npix, int C, int64_t xs, int Cp, bf16_t *xp, hipStream_t st) {
+    if (xs == Cp && ((uintptr_t)x & 15) == 0) return reinterpret_cast<const bf16_t *>(x);
+    pad_channels(x, npix, C, xs, Cp, xp, st);
+    return xp;
 }
 
 }  // namespace
@@ -190,12 +202,12 @@ hipError_t launch_conv_fwd_folded(const void *x, int64_t xs, const void *w, void
     bf16_t *xp = reinterpret_cast<bf16_t *>(base);
     bf16_t *wv = reinterpret_cast<bf16_t *>(base + align256((size_t)s.N * s.H * s.W * f.Cp * 2));
     const int64_t npix = (int64_t)s.N * s.H * s.W;
-    pad_channels(x, npix, s.C, xs, f.Cp, xp, st);
+    const bf16_t *xin = padded_input(x, npix, s.C, xs, f.Cp, xp, st);
     hipLaunchKernelGGL(fold_filter_kernel, dim3(grid_of((int64_t)s.KH * f.v.KW * 8 * s.K)), dim3(256), 0, st,
                        reinterpret_cast<const bf16_t *>(w), s.KH, s.KW, s.C, s.K, f.F, f.Cp, f.v.KW, wv);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    return launch_conv_fwd(1, xp, 8, wv, y, ys, f.v, bias, nullptr, st);
+    return launch_conv_fwd(1, xin, 8, wv, y, ys, f.v, bias, nullptr, st);
 }
 
 hipError_t launch_conv_bwd_filter_folded(const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,
@@ -209,10 +221,10 @@ hipError_t launch_conv_bwd_filter_folded(const void *x, int64_t xs, const void *
     float *dwv = reinterpret_cast<float *>(base + xb);
     void *ws2 = base + xb + align256(wvn * 4);
     const int64_t npix = (int64_t)s.N * s.H * s.W;
-    pad_channels(x, npix, s.C, xs, f.Cp, xp, st);
+    const bf16_t *xin = padded_input(x, npix, s.C, xs, f.Cp, xp, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = launch_conv_bwd_filter(1, xp, 8, dy, dys, dwv, f.v, ws2, st);
+    e = launch_conv_bwd_filter(1, xin, 8, dy, dys, dwv, f.v, ws2, st);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(unfold_filter_grad_kernel, dim3(grid_of((int64_t)s.KH * s.KW * s.C * s.K)), dim3(256), 0, st,
                        dwv, s.KH, s.KW, s.C, s.K, f.F, f.Cp, f.v.KW, dw);

@@ -49,6 +49,7 @@ struct IgArgs {
     void *out;           // FWD: y          BWD_DATA: dx         BWD_FILTER: fp32 dw / partials
     float beta;          // BWD_DATA: 0 overwrite, 1 accumulate
     const float *bias;   // FWD: when set, y = max(conv + bias[co], +0) (bias + ReLU fused)
+    int xcd_order;       // pipelined kernel: 1 = give each XCD a contiguous range of logical blocks
     // forward-convolution geometry
     int N, H, W, C;      // input extents
     int OH, OW, K;       // output extents, K = output channels

@@ -131,10 +131,10 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    // (bwd-filter keeps the hardware order: its splits read disjoint pixel ranges, and
-    // spreading one split's tiles over all XCDs measured faster than concentrating them.)
+    // (the launcher may keep the hardware order: for bwd-filter splits of the AlexNet layers
+    // spreading one split's tiles over all XCDs measured faster than concentrating them)
     const int lin_hw = (int)(blockIdx.x + gridDim.x * blockIdx.z);
-    const int lin = DIR == DIR_BWD_FILTER ? lin_hw : xcd_order(lin_hw, (int)(gridDim.x * gridDim.z));
+    const int lin = a.xcd_order ? xcd_order(lin_hw, (int)(gridDim.x * gridDim.z)) : lin_hw;
     const int bx = lin % (int)gridDim.x;
     const int bz = lin / (int)gridDim.x;
     const int ti = bx % a.tiles_i;

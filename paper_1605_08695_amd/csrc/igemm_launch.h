@@ -89,6 +89,7 @@ static inline void fill_geom(IgArgs &a, const ConvShape &s) {
     a.dK.init((uint32_t)s.K);
     a.beta = 0.f;
     a.bias = nullptr;
+    a.xcd_order = 1;
     a.k_split = 0;
     a.split_stride = 0;
 }

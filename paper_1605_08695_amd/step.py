@@ -93,7 +93,14 @@ class Replica:
         self.act: Dict[str, torch.Tensor] = {}
         for name, shape in net.tensors.items():
             if name == "x":
-                self.act["x"] = torch.from_numpy(inputs.x).to(dt).to(dev)
+                xin = torch.from_numpy(inputs.x).to(dt).to(dev)
+                if dt == torch.bfloat16 and shape[3] == 3:
+                    # RGB images are kept as RGBx (a zero fourth channel): the first
+                    # convolution reads them in place instead of padding them per call
+                    buf = torch.zeros(shape[:3] + (4,), dtype=dt, device=dev)
+                    buf[..., :3].copy_(xin)
+                    xin = buf[..., :3]
+                self.act["x"] = xin
             else:
                 self.act[name] = torch.zeros(shape, dtype=dt, device=dev)
         self.g = torch.from_numpy(inputs.g).to(dt).to(dev)

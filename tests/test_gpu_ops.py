@@ -130,6 +130,31 @@ def test_conv_empty_batch_filter_grad_is_zero():
     assert bool(torch.all(dw == 0))
 
 
+@pytest.mark.parametrize("shape", [(2, 36, 40, 64, 11, 4, (2, 2, 2, 2)), (2, 15, 17, 32, 3, 2, (0, 0, 0, 0))],
+                         ids=["pairfold_in_place", "oddw_padded"])
+def test_conv_rgbx_input_view(shape):
+    """An RGB input given as a 3-channel view of an RGBx buffer whose fourth channel holds
+    finite garbage: read in place when it folds, padded otherwise; the result is that of
+    the 3-channel image either way."""
+    N, H, W, K, KS, s, pads = shape
+    rng = np.random.default_rng(31)
+    buf = _mk((N, H, W, 4), torch.bfloat16, rng)             # channel 3: random, finite
+    x = buf[..., :3]
+    w = _mk((KS, KS, 3, K), torch.bfloat16, rng, 0.1)
+    bias = torch.from_numpy(rng.standard_normal(K) * 0.5).to(torch.float32).to(DEV)
+    y = ops.conv2d_fwd(x, w, s, pads)
+    yf = ops.conv2d_fwd_bias_relu(x, w, bias, s, pads)
+    torch.cuda.synchronize()
+    ref = oracle.conv2d_fwd(f64(x), f64(w), s, pads)
+    assert_close(f64(y), ref, torch.bfloat16, label="fwd rgbx")
+    assert_close(f64(yf), oracle.bias_relu_fwd(ref, f64(bias)), torch.bfloat16, label="fwd+bias+relu rgbx")
+    dy = _mk(y.shape, torch.bfloat16, rng)
+    dw = ops.conv2d_bwd_filter(x, dy, (KS, KS), s, pads)
+    torch.cuda.synchronize()
+    assert_close(f64(dw), oracle.conv2d_bwd_filter(f64(x), f64(dy), (KS, KS), s, pads), torch.float32,
+                 torch.bfloat16, label="bwd_filter rgbx")
+
+
 def test_conv_misaligned_base_uses_scalar_path():
     """A view whose base is not 16-byte aligned still computes correctly."""
     rng = np.random.default_rng(9)
