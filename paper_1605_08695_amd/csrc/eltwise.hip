@@ -145,14 +145,26 @@ __global__ __launch_bounds__(256) void relu_bwd_partial_kernel(const T *__restri
 
 // Pass 2: one block per channel sums its G partials (stored channel-major, so
 // the reads are contiguous): thread t takes b = t, t + 256, ... in order, then
-// a fixed-shape tree combines the 256 running sums.
+// a fixed-shape tree combines the 256 running sums.  The loads of 16 consecutive
+// b of one thread are issued together before they are added (same order).
 __global__ __launch_bounds__(256) void sum_partials_kernel(const float *__restrict__ partial, int G, int C,
                                                            float *__restrict__ out) {
     __shared__ float red[256];
     const int c = blockIdx.x;
     const float *row = partial + (int64_t)c * G;
     float acc = 0.f;
-    for (int b = threadIdx.x; b < G; b += 256) acc += row[b];
+    constexpr int U = 16;
+    for (int b0 = threadIdx.x; b0 < G; b0 += 256 * U) {
+        float v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int b = b0 + u * 256;
+            v[u] = b < G ? row[b] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (b0 + u * 256 < G) acc += v[u];
+    }
     red[threadIdx.x] = acc;
     __syncthreads();
     for (int s = 128; s > 0; s >>= 1) {
@@ -452,6 +464,120 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *
     }
 }
 
+// Stride-2 pools with windows of at most 4 x 4 (AlexNet 3x3/2, VGG 2x2/2): thread work item =
+// one 2 x 2 "cell" of input pixels (rows 2 ch - pt + {0,1}, columns 2 cw - pl + {0,1}) and
+// one channel chunk.  Only windows ch-1, ch (rows) x cw-1, cw (columns) can hold the argmax
+// of a cell pixel, so their argmax and dy are loaded once for all four pixels (the gather
+// form reloads them for every pixel) and each window's gradient is routed to the pixel its
+// argmax names, windows in ascending order (the same sums, in the same order, as the gather).
+// Bias-gradient partials as in maxpool_relu_bwd_partial_kernel, over cells instead of pixels.
+template <typename T>
+__global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__restrict__ dy,
+                                                                    const int32_t *__restrict__ argmax, PoolGeom g,
+                                                                    const T *__restrict__ y, T *dpre, float beta,
+                                                                    int64_t cpb, int CH, int CW, FastDiv dCW,
+                                                                    FastDiv dCH, float *__restrict__ partial) {
+    constexpr int EPC = Elem<T>::kPerChunk;
+    extern __shared__ float red[];                 // [R][C]
+    const int C = g.C;
+    const int CV = C / EPC;
+    const int CVB = CV < 256 ? CV : 256;
+    const int R = 256 / CVB;
+    const int t = threadIdx.x;
+    const int lane_cv = t % CVB;
+    const int row = t / CVB;
+    const int64_t ncell = (int64_t)g.N * CH * CW;
+    const int64_t c0 = (int64_t)blockIdx.x * cpb;
+    const int64_t c1 = min(ncell, c0 + cpb);
+    const bool active = row < R;
+    for (int cv = lane_cv; cv < CV; cv += CVB) {
+        float acc[EPC];
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
+        if (active) {
+            for (int64_t cell = c0 + row; cell < c1; cell += R) {
+                uint32_t q, cw, n, ch;
+                dCW.divmod((uint32_t)cell, q, cw);
+                dCH.divmod(q, n, ch);
+                // the (up to) four windows, in ascending output order
+                int32_t ai[4][EPC];
+                U4 dv[4];
+                bool wok[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int oh = (int)ch - 1 + (k >> 1), ow = (int)cw - 1 + (k & 1);
+                    wok[k] = (unsigned)oh < (unsigned)g.OH && (unsigned)ow < (unsigned)g.OW;
+                    const int64_t opix = ((int64_t)n * g.OH + (wok[k] ? oh : 0)) * g.OW + (wok[k] ? ow : 0);
+                    const int32_t *am = argmax + opix * g.C + cv * EPC;
+#pragma unroll
+                    for (int e = 0; e < EPC; e += 4) {
+                        const int4 v = *reinterpret_cast<const int4 *>(am + e);
+                        ai[k][e] = v.x; ai[k][e + 1] = v.y; ai[k][e + 2] = v.z; ai[k][e + 3] = v.w;
+                    }
+                    dv[k] = *reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC);
+                }
+                // the four pixels of the cell
+                int64_t pix[4];
+                bool pok[4];
+                U4 yv[4], ov[4];
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const int h = 2 * (int)ch - g.pt + (m >> 1), w = 2 * (int)cw - g.pl + (m & 1);
+                    pok[m] = (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
+                    pix[m] = ((int64_t)n * g.H + (pok[m] ? h : 0)) * g.W + (pok[m] ? w : 0);
+                    yv[m] = *reinterpret_cast<const U4 *>(y + pix[m] * g.xs + cv * EPC);
+                    if (beta != 0.f) ov[m] = *reinterpret_cast<const U4 *>(dpre + pix[m] * g.xs + cv * EPC);
+                }
+                float s[4][EPC];
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+#pragma unroll
+                    for (int e = 0; e < EPC; ++e) s[m][e] = 0.f;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    float v[EPC];
+                    chunk_to_f32<T>(dv[k], v);
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) {
+                        const int32_t self = (int32_t)(pix[m] * g.C + cv * EPC);
+#pragma unroll
+                        for (int e = 0; e < EPC; ++e)
+                            if (wok[k] && ai[k][e] == self + e) s[m][e] += v[e];
+                    }
+                }
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    if (!pok[m]) continue;
+                    float fy[EPC];
+                    chunk_to_f32<T>(yv[m], fy);
+                    if (beta != 0.f) {
+                        float o[EPC];
+                        chunk_to_f32<T>(ov[m], o);
+#pragma unroll
+                        for (int e = 0; e < EPC; ++e) s[m][e] += beta * o[e];
+                    }
+#pragma unroll
+                    for (int e = 0; e < EPC; ++e) s[m][e] = fy[e] > 0.f ? s[m][e] : 0.f;
+                    const U4 packed = f32_to_chunk<T>(s[m]);
+                    *reinterpret_cast<U4 *>(dpre + pix[m] * g.xs + cv * EPC) = packed;
+                    float st[EPC];
+                    chunk_to_f32<T>(packed, st);
+#pragma unroll
+                    for (int e = 0; e < EPC; ++e) acc[e] += st[e];
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) red[row * C + cv * EPC + e] = acc[e];
+        }
+    }
+    __syncthreads();
+    for (int c = t; c < C; c += 256) {
+        float a = 0.f;
+        for (int r = 0; r < R; ++r) a += red[r * C + c];
+        partial[(int64_t)c * gridDim.x + blockIdx.x] = a;
+    }
+}
+
 // ------------------------------------------------------------------ SGD
 __device__ __forceinline__ void sgd_one(float *var, const float *grad, uint16_t *sh, int64_t i, float lr) {
     const float v = fmaf(-lr, grad[i], var[i]);
@@ -639,6 +765,21 @@ static hipError_t maxpool_relu_bwd_t(const void *dy, const int32_t *am, const Po
     const int R = 256 / CVB;
     const size_t smem = (size_t)R * g.C * sizeof(float);
     const FastDiv dW((uint32_t)g.W), dH((uint32_t)g.H);
+    if (vec && g.sh == 2 && g.sw == 2 && g.KH <= 4 && g.KW <= 4) {
+        // cell form: ceil((H + pt) / 2) x ceil((W + pl) / 2) cells cover every input pixel; its
+        // partial grid (fewer work items than pixels) fits the pixel-sized workspace
+        // (about 2 cells per thread; never more partial blocks than the pixel plan's G above)
+        const int CH = (g.H + g.pt + 1) / 2, CW = (g.W + g.pl + 1) / 2;
+        const int64_t ncell = (int64_t)g.N * CH * CW;
+        const int64_t gc = std::max<int64_t>(1, std::min<int64_t>(G, (ncell + 2 * R - 1) / (2 * R)));
+        const int Gc = (int)gc;
+        const int64_t cpb = (ncell + gc - 1) / gc;
+        hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am, g,
+                           (const T *)y, (T *)dpre, beta, cpb, CH, CW, FastDiv((uint32_t)CW), FastDiv((uint32_t)CH),
+                           ws);
+        hipLaunchKernelGGL(sum_partials_kernel, dim3(g.C), dim3(256), 0, st, ws, Gc, g.C, db);
+        return hipGetLastError();
+    }
     if (vec)
         hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, true>), dim3(G), dim3(256), smem, st, (const T *)dy, am,
                            g, (const T *)y, (T *)dpre, beta, ppb, dW, dH, ws);
