@@ -47,6 +47,9 @@ size_t plan_ws(const ConvShape &s, const BwfPlan &p) {
     return (size_t)p.splits * (size_t)s.KH * s.KW * s.C * s.K * sizeof(float);
 }
 
+// Workspace bytes ahead of the band kernel's partials: room for a 4-channel copy of x.
+size_t band_x_bytes(const ConvShape &s) { return ((size_t)s.N * s.H * s.W * 8 + 255) & ~(size_t)255; }
+
 }  // namespace
 
 void conv_bwd_filter_plan(int dt, const ConvShape &s, int *splits, int *k_split) {
@@ -59,6 +62,7 @@ size_t conv_bwd_filter_ws_bytes(int dt, const ConvShape &s) {
     size_t need = plan_ws(s, bwf_plan(dt, s, false));
     if (dt == 1) need = std::max(need, plan_ws(s, bwf_plan(dt, s, true)));
     if (conv_fold_applies(dt, s)) need = std::max(need, conv_fold_ws_bytes(2, s));
+    if (dt == 1 && conv_band_bwf_applies(s)) need = std::max(need, band_x_bytes(s) + conv_band_bwf_partial_bytes(s));
     return need;
 }
 
@@ -105,6 +109,15 @@ static hipError_t conv_bwd_filter_t(const void *x, int64_t xs, const void *dy, i
 
 hipError_t launch_conv_bwd_filter(int dt, const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,
                                   const ConvShape &s, void *ws, hipStream_t st) {
+    if (dt == 1 && conv_band_bwf_applies(s) && dys % 8 == 0 && aligned16p(dy) && aligned16p(ws)) {
+        const int64_t npix = (int64_t)s.N * s.H * s.W;
+        unsigned char *base = reinterpret_cast<unsigned char *>(ws);
+        const bf16_t *x4 = rgbx_input(x, npix, s.C, xs, reinterpret_cast<bf16_t *>(base), st);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        float *part = reinterpret_cast<float *>(base + band_x_bytes(s));
+        return launch_conv_bwd_filter_band(x4, dy, dys, dw, s, part, st);
+    }
     if (conv_fold_applies(dt, s) && dys % 8 == 0 && ((uintptr_t)dy & 15) == 0 && ((uintptr_t)ws & 15) == 0)
         return launch_conv_bwd_filter_folded(x, xs, dy, dys, dw, s, ws, st);
     return dt == 0 ? conv_bwd_filter_t<float>(x, xs, dy, dys, dw, s, ws, st)

@@ -179,6 +179,12 @@ const bf16_t *padded_input(const void *x, int64_t npix, int C, int64_t xs, int C
 
 }  // namespace
 
+const bf16_t *rgbx_input(const void *x, int64_t npix, int C, int64_t xs, bf16_t *xp, hipStream_t st) {
+    if (xs == 4 && ((uintptr_t)x & 7) == 0) return reinterpret_cast<const bf16_t *>(x);
+    pad_channels(x, npix, C, xs, 4, xp, st);
+    return xp;
+}
+
 bool conv_fold_applies(int dt, const ConvShape &s) {
     Fold f;
     return dt == 1 && s.K % 8 == 0 && fold_plan(s, f);

@@ -30,6 +30,13 @@ static hipError_t conv_fwd_t(const void *x, int64_t xs, const void *w, void *y, 
 
 hipError_t launch_conv_fwd(int dt, const void *x, int64_t xs, const void *w, void *y, int64_t ys,
                            const ConvShape &s, const float *bias, void *ws, hipStream_t st) {
+    if (dt == 1 && ws != nullptr && conv_band_fwd_applies(s) && aligned16p(w) && ((uintptr_t)y & 7) == 0 &&
+        ys % 4 == 0) {
+        const bf16_t *x4 = rgbx_input(x, (int64_t)s.N * s.H * s.W, s.C, xs, reinterpret_cast<bf16_t *>(ws), st);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        return launch_conv_fwd_band(x4, w, y, ys, s, bias, st);
+    }
     if (ws != nullptr && conv_fold_applies(dt, s) && ((uintptr_t)y & 15) == 0 && ys % 8 == 0)
         return launch_conv_fwd_folded(x, xs, w, y, ys, s, bias, ws, st);
     return dt == 0 ? conv_fwd_t<float>(x, xs, w, y, ys, s, bias, st)

@@ -51,6 +51,17 @@ hipError_t launch_conv_fwd_folded(const void *x, int64_t xs, const void *w, void
 hipError_t launch_conv_bwd_filter_folded(const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,
                                          const ConvShape &s, void *ws, hipStream_t st);
 
+// First layers with at most 4 input channels as band kernels (conv_band.hip): the input is read
+// as 4-channel pixels (an RGBx view in place, or a padded copy made by rgbx_input in xp).
+const uint16_t *rgbx_input(const void *x, int64_t npix, int C, int64_t xs, uint16_t *xp, hipStream_t st);
+bool conv_band_fwd_applies(const ConvShape &s);
+bool conv_band_bwf_applies(const ConvShape &s);
+size_t conv_band_bwf_partial_bytes(const ConvShape &s);
+hipError_t launch_conv_fwd_band(const uint16_t *x4, const void *w, void *y, int64_t ys, const ConvShape &s,
+                                const float *bias, hipStream_t st);
+hipError_t launch_conv_bwd_filter_band(const uint16_t *x4, const void *dy, int64_t dys, float *dw, const ConvShape &s,
+                                       float *part, hipStream_t st);
+
 hipError_t launch_bias_relu_fwd(int dt, void *y, int64_t P, int C, int64_t ys, const float *bias, hipStream_t st);
 void relu_bwd_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *ppb);
 hipError_t launch_bias_relu_bwd(int dt, const void *y, const void *dy, void *dpre, int64_t P, int C,

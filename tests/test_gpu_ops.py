@@ -155,6 +155,50 @@ def test_conv_rgbx_input_view(shape):
                  torch.bfloat16, label="bwd_filter rgbx")
 
 
+# First layers with at most 4 input channels (bf16) run as band kernels that stage input rows in LDS.
+# N, H, W, Cin, Cout, KH, KW, sh, sw, pads
+BAND_CASES = [
+    # AlexNet conv1 at full image size: 4-row bands, a 3-row last band, one band per workgroup
+    ("alexnet_conv1_b3", 3, 224, 224, 3, 64, 11, 11, 4, 4, (2, 2, 2, 2)),
+    # more bands than workgroups: the double-buffered band loop runs twice on some workgroups
+    ("many_bands", 300, 35, 35, 3, 64, 11, 11, 4, 4, (2, 2, 2, 2)),
+    # two output-channel blocks; a partly empty channel block
+    ("cin3_k128_5x5s2", 4, 30, 30, 3, 128, 5, 5, 2, 2, (2, 2, 2, 2)),
+    ("cin3_k48_5x5s2", 3, 27, 29, 3, 48, 5, 5, 2, 2, (1, 2, 2, 1)),
+    # odd horizontal stride (two 8-byte LDS reads per operand), odd width, asymmetric pads
+    ("cin3_7x7s1_oddw", 2, 20, 21, 3, 32, 7, 7, 1, 1, (3, 3, 3, 3)),
+    ("cin1_5x5s3", 3, 29, 31, 1, 16, 5, 5, 3, 3, (1, 2, 0, 1)),
+    ("cin4_9x9s2", 2, 40, 38, 4, 64, 9, 9, 2, 2, (4, 4, 4, 4)),
+    ("cin3_8x1_sh2", 2, 20, 12, 3, 32, 8, 1, 2, 1, (3, 4, 0, 0)),
+    # 3x3 first layers: forward band kernel, filter gradient on the folded path (too few taps)
+    ("cin3_3x3s1_same", 2, 24, 26, 3, 64, 3, 3, 1, 1, (1, 1, 1, 1)),
+    ("cin3_3x3s2_valid", 2, 33, 31, 3, 32, 3, 3, 2, 2, (0, 0, 0, 0)),
+]
+
+
+@pytest.mark.parametrize("case", BAND_CASES, ids=[c[0] for c in BAND_CASES])
+def test_conv_first_layer_band(case):
+    name, N, H, W, C, K, KH, KW, sh, sw, pads = case
+    say("band conv case", name)
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    x = _mk((N, H, W, C), torch.bfloat16, rng)
+    w = _mk((KH, KW, C, K), torch.bfloat16, rng, np.sqrt(2.0 / (KH * KW * C)))
+    bias = torch.from_numpy(rng.standard_normal(K) * 0.5).to(torch.float32).to(DEV)
+    y = ops.conv2d_fwd(x, w, (sh, sw), pads)
+    yf = ops.conv2d_fwd_bias_relu(x, w, bias, (sh, sw), pads)
+    torch.cuda.synchronize()
+    ref = oracle.conv2d_fwd(f64(x), f64(w), (sh, sw), pads)
+    assert y.shape == ref.shape
+    assert_close(f64(y), ref, torch.bfloat16, label="fwd")
+    assert_close(f64(yf), oracle.bias_relu_fwd(ref, f64(bias)), torch.bfloat16, label="fwd+bias+relu")
+    dy = _mk(y.shape, torch.bfloat16, rng)
+    dw = torch.full((KH, KW, C, K), 3.0, device=DEV)          # overwritten, never accumulated into
+    ops.conv2d_bwd_filter(x, dy, (KH, KW), (sh, sw), pads, dw=dw)
+    torch.cuda.synchronize()
+    assert_close(f64(dw), oracle.conv2d_bwd_filter(f64(x), f64(dy), (KH, KW), (sh, sw), pads), torch.float32,
+                 torch.bfloat16, label="bwd_filter")
+
+
 def test_conv_misaligned_base_uses_scalar_path():
     """A view whose base is not 16-byte aligned still computes correctly."""
     rng = np.random.default_rng(9)
