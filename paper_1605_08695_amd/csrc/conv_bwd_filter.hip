@@ -13,9 +13,11 @@ struct BwfPlan {
 
 // Tiles and split-K of one bwd-filter launch, chosen from sweeps over the AlexNet/VGG
 // shapes: 128 x 128 tiles (even for 192 output channels, where the second channel tile
-// is half empty) and the pixel reduction split until there are about four blocks per CU;
-// 64-channel layers take 64 x 128 tiles and half as many splits (their partials are
-// the larger share of the work).
+// is half empty) and the pixel reduction split into as many parts as keep the blocks within
+// one full round of two blocks per CU (512 blocks): a last round with only a few blocks
+// costs a whole block time, and more splits only add partial-sum traffic (AlexNet conv2-5:
+// 357 us with four-block rounds, 297 us with this rule).  64-channel layers take 64 x 128
+// tiles.
 BwfPlan bwf_plan(int dt, const ConvShape &s, bool v2) {
     BwfPlan p;
     const int bk = dt == 0 ? 32 : 64;
@@ -31,8 +33,8 @@ BwfPlan bwf_plan(int dt, const ConvShape &s, bool v2) {
     const int tiles = ((s.K + p.bi - 1) / p.bi) * ((m + p.bj - 1) / p.bj);
     const int64_t ktot = (int64_t)s.N * s.OH * s.OW;
     const int64_t ktiles = (ktot + bk - 1) / bk;
-    const int target = v2 && s.K > 64 ? 1024 : 512;
-    int64_t sp = (target + tiles - 1) / tiles;
+    const int target = 512;
+    int64_t sp = target / tiles;
     const int64_t max_sp = std::max<int64_t>(1, ktiles / 8);   // at least 8 K tiles per split
     sp = std::max<int64_t>(1, std::min<int64_t>(sp, max_sp));
     sp = std::min<int64_t>(sp, 4096);

@@ -625,8 +625,9 @@ __global__ __launch_bounds__(256) void sgd_multi_kernel(SgdBatch b, float lr) {
 }
 
 // ------------------------------------------------------------------ split-K sum / zero fill
-// The split partials part[s][i] (s < splits, i < mn) are summed in two fixed levels, so
-// the result depends only on the shape: groups of kSplitGroup consecutive splits are
+// The split partials part[s][i] (s < splits, i < mn) are summed in a fixed order that depends
+// only on the shape.  Large gradients: one pass, split order (sum_splits_direct_kernel).
+// Small ones, in two fixed levels: groups of kSplitGroup consecutive splits are
 // summed in split order (in place, into the group's first split), then the group sums are
 // added in group order.  Each thread owns VEC consecutive elements of one group and issues
 // all of the group's loads before adding, so a reduction over many splits of a small
@@ -852,10 +853,41 @@ hipError_t launch_sgd_multi(const SgdBatch &b, float lr, hipStream_t st) {
     return hipGetLastError();
 }
 
+// One pass when the gradient has enough elements to occupy the chip: each thread sums its VEC
+// elements over all splits in split order, eight loads in flight at a time.
+template <int VEC>
+__global__ __launch_bounds__(256) void sum_splits_direct_kernel(const float *__restrict__ part, int splits,
+                                                                int64_t mn, float *__restrict__ out) {
+    typedef typename FVec<VEC>::T V;
+    const int64_t mv = mn / VEC;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < mv; i += stride) {
+        const V *src = reinterpret_cast<const V *>(part) + i;
+        V acc = src[0];
+        int s = 1;
+        for (; s + 8 <= splits; s += 8) {
+            V v[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] = src[(int64_t)(s + q) * mv];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) acc += v[q];
+        }
+        for (; s < splits; ++s) acc += src[(int64_t)s * mv];
+        reinterpret_cast<V *>(out)[i] = acc;
+    }
+}
+
+constexpr int64_t kDirectSumMinThreads = 32768;
+
 template <int VEC>
 static hipError_t sum_splits_t(float *part, int splits, int64_t mn, float *out, hipStream_t st) {
     const int groups = (splits + kSplitGroup - 1) / kSplitGroup;
     const int64_t mv = mn / VEC;
+    if (mv >= kDirectSumMinThreads) {
+        hipLaunchKernelGGL(sum_splits_direct_kernel<VEC>, dim3(grid_for(mv, 256, 16384)), dim3(256), 0, st, part,
+                           splits, mn, out);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(sum_split_groups_kernel<VEC>, dim3(grid_for(mv * groups, 256, 16384)), dim3(256), 0, st, part,
                        splits, mn, groups);
     hipLaunchKernelGGL(sum_groups_kernel<VEC>, dim3(grid_for(mv, 256, 16384)), dim3(256), 0, st, part, groups, mn,

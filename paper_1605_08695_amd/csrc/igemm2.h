@@ -389,6 +389,17 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
 #pragma unroll
                 for (int y = 0; y < MJ; ++y) Mfma<bf16_t>::run(acc[x][y], fi[x], fj[y]);
         }
+        // Schedule: the fragment reads of the first sub-step, then the MFMAs of the first
+        // sub-step alternating with the reads of the second, then its MFMAs -- so the LDS
+        // latency of the second sub-step hides under MFMAs (about 2 % on the AlexNet layers).
+        constexpr int RD = (TI ? 2 : 1) * MI + (TJ ? 2 : 1) * MJ;     // LDS reads per sub-step
+        __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);             // DS reads
+#pragma unroll
+        for (int q = 0; q < MI * MJ; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);          // one MFMA
+            if (q < RD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, MI * MJ, 0);
     };
 
     // One pipeline step on stage S = kt % NS: wait for tile kt (the copies of the later
