@@ -272,6 +272,65 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T *__restrict__ 
     }
 }
 
+// Fixed small windows (3x3, 2x2) on the 16-byte path: the window loop is unrolled and all of a
+// thread's loads are issued before the first comparison, so their latencies overlap (the
+// run-time loop above waits for each tap in turn).  Same scan order and tie rule.
+template <typename T, int KH, int KW>
+__global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restrict__ x, PoolGeom g,
+                                                              T *__restrict__ y, int32_t *__restrict__ argmax,
+                                                              Decode dec) {
+    constexpr int EPC = Elem<T>::kPerChunk;
+    const int CV = g.C / EPC;
+    const int64_t total = (int64_t)g.N * g.OH * g.OW * CV;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
+         t += (int64_t)gridDim.x * blockDim.x) {
+        int cv, ow, oh, n;
+        int64_t pix;
+        decode(dec, t, cv, pix, ow, oh, n);
+        U4 v[KH * KW];
+        bool ok[KH * KW];
+        int64_t pidx[KH * KW];
+#pragma unroll
+        for (int kh = 0; kh < KH; ++kh) {
+#pragma unroll
+            for (int kw = 0; kw < KW; ++kw) {
+                const int q = kh * KW + kw;
+                const int ih = oh * g.sh + kh - g.pt, iw = ow * g.sw + kw - g.pl;
+                ok[q] = (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
+                pidx[q] = ((int64_t)n * g.H + (ok[q] ? ih : 0)) * g.W + (ok[q] ? iw : 0);
+                v[q] = *reinterpret_cast<const U4 *>(x + pidx[q] * g.xs + cv * EPC);
+            }
+        }
+        float best[EPC];
+        int32_t bi[EPC];
+        bool have = false;
+#pragma unroll
+        for (int q = 0; q < KH * KW; ++q) {
+            if (!ok[q]) continue;
+            float f[EPC];
+            chunk_to_f32<T>(v[q], f);
+            const int32_t dense = (int32_t)(pidx[q] * g.C + cv * EPC);
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                if (!have || f[e] > best[e]) {
+                    best[e] = f[e];
+                    bi[e] = dense + e;
+                }
+            }
+            have = true;
+        }
+        const int64_t opix = ((int64_t)n * g.OH + oh) * g.OW + ow;
+        *reinterpret_cast<U4 *>(y + opix * g.ys + cv * EPC) = f32_to_chunk<T>(best);
+        int32_t *am = argmax + opix * g.C + cv * EPC;
+#pragma unroll
+        for (int e = 0; e < EPC; e += 4) {
+            int4 q4;
+            q4.x = bi[e]; q4.y = bi[e + 1]; q4.z = bi[e + 2]; q4.w = bi[e + 3];
+            *reinterpret_cast<int4 *>(am + e) = q4;
+        }
+    }
+}
+
 // ------------------------------------------------------------------ max-pool backward
 // Gather form: each input element visits the windows that contain it in
 // ascending output order and adds the gradients routed to it.
@@ -806,7 +865,13 @@ static hipError_t maxpool_fwd_t(const void *x, const PoolGeom &g, void *y, int32
     const int64_t work = (int64_t)g.N * g.OH * g.OW * cv;
     const int grid = grid_for(work, 256, 16384);
     const Decode dec = make_decode(cv, g.OW, g.OH, work);
-    if (vec)
+    if (vec && g.KH == 3 && g.KW == 3)
+        hipLaunchKernelGGL((maxpool_fwd_win_kernel<T, 3, 3>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am,
+                           dec);
+    else if (vec && g.KH == 2 && g.KW == 2)
+        hipLaunchKernelGGL((maxpool_fwd_win_kernel<T, 2, 2>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am,
+                           dec);
+    else if (vec)
         hipLaunchKernelGGL((maxpool_fwd_kernel<T, true>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am, dec);
     else
         hipLaunchKernelGGL((maxpool_fwd_kernel<T, false>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am, dec);
