@@ -93,8 +93,9 @@ struct BandCopier {
         const int units = X16 ? (npix + 1) / 2 : 2 * npix;
         ncopies = (units + 63) / 64;
     }
-    // copies of wave w: i = w, w + 4, ...
-    __device__ __forceinline__ int count(int w) const { return ncopies > w ? (ncopies - w + 3) / 4 : 0; }
+    // copies of wave w of NW: i = w, w + NW, ...
+    template <int NW = 4>
+    __device__ __forceinline__ int count(int w) const { return ncopies > w ? (ncopies - w + NW - 1) / NW : 0; }
     __device__ __forceinline__ void copy(const BandArgs &a, int i, unsigned char *buf) const {
         const int lane = threadIdx.x & 63;
         const int u = 64 * i + lane;
@@ -112,11 +113,11 @@ struct BandCopier {
     }
 };
 
-template <bool X16>
+template <bool X16, int NW = 4>
 __device__ __forceinline__ void band_dma(const BandArgs &a, int b, unsigned char *buf) {
     const int wave = threadIdx.x >> 6;
     const BandCopier<X16> bc(a, b);
-    for (int i = wave; i < bc.ncopies; i += 4) bc.copy(a, i, buf);
+    for (int i = wave; i < bc.ncopies; i += NW) bc.copy(a, i, buf);
 }
 
 // ---------------------------------------------------------------------------------- forward
@@ -293,6 +294,170 @@ __global__ __launch_bounds__(256, 1) void band_fwd_kernel(const BandArgs a) {
     }
 #pragma unroll
     for (int x = 0; x < 4; ++x) store_row(x);
+}
+
+// ---------------------------------------------------------------------------------- forward, filter in registers
+// For filters of exactly KS reduction steps and bands of at most 32 MJ pixels.  The filter is
+// staged once through LDS (over the band buffers) and then held in registers: wave w takes the
+// band's pixel groups (w & 1) + 2 y (y < MJ) and the channel groups 2 (w >> 1) + {0, 1}, so per
+// step it reads only MJ pixel fragments from LDS for 2 MJ MFMAs (half the LDS traffic per MFMA of
+// band_fwd_kernel, which re-reads the filter every step).  Copies of the next band and the stores
+// of the previous band are issued one per step under the MFMAs, as in band_fwd_kernel.
+template <int KS, int MJ, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void band_fwd_reg_kernel(const BandArgs a) {
+    static_assert(NW == 4 || NW == 8, "waves");
+    constexpr int PS = NW / 2;                  // pixel parts: wave w takes part w % PS, channel half w / PS
+    static_assert(KS % 2 == 0 && KS * 32 * 128 <= 2 * kXBand, "filter staging");
+    __shared__ __attribute__((aligned(1024))) unsigned char xb0[kXBand];
+    __shared__ __attribute__((aligned(1024))) unsigned char xb1[kXBand];
+    unsigned char *filt = xb0;                  // staging of the filter (spans xb0 and xb1)
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lg = lane >> 4, ld = lane & 15;
+    const int ph = wave % PS, chh = wave / PS;
+    const int co0 = blockIdx.y * 64;
+    const int ntaps = a.KH * a.kwp;
+
+    // Filter rows m = (kh * kwp + kw) * 4 + c, k-major with the transposing-read swizzle.
+    for (int i = wave; i < KS * 4; i += NW) {
+        const int m = 8 * i + (lane >> 3);
+        const int ch = (lane & 7) ^ kmajor_swz<64>(m);
+        const int c = m & 3;
+        uint32_t kh, kw;
+        a.dKwp.divmod((uint32_t)(m >> 2), kh, kw);
+        const int co = co0 + ch * 8;
+        const bool ok = (int)kh < a.KH && (int)kw < a.KW && c < a.C && co < a.K;
+        dma16(ok ? (const void *)(a.w + (((int64_t)kh * a.KW + kw) * a.C + c) * a.K + co)
+                 : (const void *)g_zero_chunk,
+              filt + 1024 * i);
+    }
+    wait_barrier<0>();
+    U4 fw[KS][2];
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+        const int k = 32 * kk + 8 * lg + (ld >> 2);
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+            const int row = 16 * (2 * chh + x) + 4 * (ld & 3);
+            fw[kk][x] = lds_tr_pair(filt + kmajor_off<64>(k, row), filt + kmajor_off<64>(k + 4, row));
+        }
+    }
+    wait_barrier<0>();                          // every wave holds its filter: the staging area is free
+
+    int b = blockIdx.x;
+    if (b < a.bands) band_dma<true, NW>(a, b, xb0);
+    wait_barrier<0>();
+
+    float bv[2][4];
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+        const int co = co0 + 16 * (2 * chh + x) + 4 * lg;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) bv[x][e] = (a.bias != nullptr && co < a.K) ? a.bias[co + e] : 0.f;
+    }
+    // Outputs of the previous band, stored one per step during the next band: packed bf16 of
+    // acc[x][y] and the output offset of each of the lane's pixels (-1: no pixel).
+    uint2 held[2][MJ];
+    int hoff[MJ];
+#pragma unroll
+    for (int y = 0; y < MJ; ++y) hoff[y] = -1;
+    bf16_t *const out = reinterpret_cast<bf16_t *>(a.out);
+    auto store_one = [&](int x, int y) __attribute__((always_inline)) {
+        const int co = co0 + 16 * (2 * chh + x) + 4 * lg;
+        if (hoff[y] >= 0 && co < a.K) *reinterpret_cast<uint2 *>(out + hoff[y] + co) = held[x][y];
+    };
+
+    for (int it = 0; b < a.bands; b += gridDim.x, ++it) {
+        const unsigned char *cur = (it & 1) ? xb1 : xb0;
+        unsigned char *nxt = (it & 1) ? xb0 : xb1;
+        const int bn = b + (int)gridDim.x;
+        const BandCopier<true> bc(a, bn < a.bands ? bn : b);
+        const int nc = bn < a.bands ? bc.template count<NW>(wave) : 0;   // this wave's copies of the next band
+
+        const int n = b / a.bands_per_img;
+        const int oh0 = (b - n * a.bands_per_img) * a.R;
+        const int pb = min(a.R, a.OH - oh0) * a.OW;             // valid pixels of this band
+        int boff[MJ];                                           // pixel-pair index of the window origin
+        int coff[MJ];                                           // output offset (elements; fits int32)
+#pragma unroll
+        for (int y = 0; y < MJ; ++y) {
+            const int q = (PS * y + ph) * 16 + ld;
+            uint32_t r, ow;
+            a.dOW.divmod((uint32_t)(q < pb ? q : 0), r, ow);
+            boff[y] = ((int)r * a.sh * a.wst + (int)ow * a.sw) >> 1;
+            coff[y] = q < pb ? ((n * a.OH + oh0 + (int)r) * a.OW + (int)ow) * (int)a.ys : -1;
+        }
+        f32x4_t acc[2][MJ];
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int y = 0; y < MJ; ++y) acc[x][y] = fresh_zero4();
+
+        // Tap pair (kh, kw) = (t / kwp, t % kwp) of t = 8 kk + 2 lg, advanced by 8 taps per step.
+        int tkh = (2 * lg) / a.kwp, tkw = (2 * lg) % a.kwp;
+        auto next_tap = [&](int kk) __attribute__((always_inline)) -> int {
+            const int to = 8 * kk + 2 * lg < ntaps ? (tkh * a.wst + tkw) >> 1 : 0;     // in pixel pairs
+            tkw += 8;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                if (tkw >= a.kwp) {
+                    tkw -= a.kwp;
+                    ++tkh;
+                }
+            }
+            return to;
+        };
+        auto side = [&](int kk) __attribute__((always_inline)) {
+            if (kk < nc) bc.copy(a, wave + NW * kk, nxt);
+            if (kk < 2 * MJ) store_one(kk / MJ, kk % MJ);
+        };
+        // One fragment per pixel group: the group's fragment of step kk + 1 is read right after its
+        // MFMAs of step kk, so it has the other groups' MFMAs to arrive.
+        U4 fj[MJ];
+        {
+            const int to = next_tap(0);
+#pragma unroll
+            for (int y = 0; y < MJ; ++y) fj[y] = *reinterpret_cast<const U4 *>(cur + ((boff[y] + to) << 4));
+        }
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+            const int to = kk + 1 < KS ? next_tap(kk + 1) : 0;
+            side(kk);
+#pragma unroll
+            for (int y = 0; y < MJ; ++y) {
+#pragma unroll
+                for (int x = 0; x < 2; ++x) Mfma<bf16_t>::run(acc[x][y], fw[kk][x], fj[y]);
+                if (kk + 1 < KS) fj[y] = *reinterpret_cast<const U4 *>(cur + ((boff[y] + to) << 4));
+            }
+        }
+        for (int c = KS; c < nc; ++c) bc.copy(a, wave + NW * c, nxt);
+
+#pragma unroll
+        for (int i = KS; i < 2 * MJ; ++i) store_one(i / MJ, i % MJ);
+
+        // bias + ReLU, rounded once (lane: channels co .. co + 3 of pixel 16 g + ld)
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+#pragma unroll
+            for (int y = 0; y < MJ; ++y) {
+                float v4[4] = {acc[x][y][0], acc[x][y][1], acc[x][y][2], acc[x][y][3]};
+                if (a.bias != nullptr) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float v = v4[e] + bv[x][e];
+                        v4[e] = v > 0.f ? v : 0.f;
+                    }
+                }
+                held[x][y].x = pack_bf16x2(v4[0], v4[1]);
+                held[x][y].y = pack_bf16x2(v4[2], v4[3]);
+            }
+        }
+#pragma unroll
+        for (int y = 0; y < MJ; ++y) hoff[y] = coff[y];
+        wait_barrier<0>();
+    }
+#pragma unroll
+    for (int i = 0; i < 2 * MJ; ++i) store_one(i / MJ, i % MJ);
 }
 
 // ---------------------------------------------------------------------------------- bwd-filter
@@ -552,6 +717,19 @@ hipError_t launch_conv_fwd_band(const bf16_t *x4, const void *w, void *y, int64_
     a.ys = ys;
     const dim3 grid((unsigned)std::min(a.bands, kCUs), (unsigned)((s.K + 63) / 64));
     const bool x16 = pairs_aligned(s);
+    constexpr int kRegKS = 18, kRegMJ = 7, kRegNW = 4;    // AlexNet conv1: 11 x 12 taps x 4 channels
+    if (a.nks == kRegKS && s.sw % 2 == 0 && x16 && (int64_t)s.N * s.OH * s.OW * ys < (int64_t)1 << 31) {
+        const int R = band_rows(s, a.wst, 16 * kRegMJ * (kRegNW / 2));
+        if (R >= 1) {
+            a.R = R;
+            a.rows_in = (R - 1) * s.sh + s.KH;
+            a.bands_per_img = (s.OH + R - 1) / R;
+            a.bands = s.N * a.bands_per_img;
+            const dim3 g2((unsigned)std::min(a.bands, kCUs), (unsigned)((s.K + 63) / 64));
+            hipLaunchKernelGGL((band_fwd_reg_kernel<kRegKS, kRegMJ, kRegNW>), g2, dim3(64 * kRegNW), 0, st, a);
+            return hipGetLastError();
+        }
+    }
     if (s.sw % 2 == 0 && x16)
         hipLaunchKernelGGL((band_fwd_kernel<true, true>), grid, dim3(256), 0, st, a);
     else if (s.sw % 2 == 0)
