@@ -35,7 +35,7 @@ constexpr int kBandPix = kXBand / 8;
 constexpr int kMaxKSteps = 18;            // forward: reduction rows <= 18 * 32 (an even number of steps)
 constexpr int kFiltBytes = kMaxKSteps * 32 * 128;
 constexpr int kDyBandPix = 256;           // bwd-filter: pixels per band (dy rows of 64 channels)
-constexpr int kBwfGroupsPerWave = 9;      // bwd-filter: at most 16-row tap groups per wave (36 per filter)
+constexpr int kBwfGroups = 40;            // bwd-filter: at most 40 16-row tap groups (5 per wave)
 
 struct BandArgs {
     const bf16_t *x;        // [N][H][W] pixels of 4 bf16, pixel stride 4 elements
@@ -463,11 +463,12 @@ __global__ __launch_bounds__(NW * 64, 1) void band_fwd_reg_kernel(const BandArgs
 // ---------------------------------------------------------------------------------- bwd-filter
 // Grid: (persistent workgroups = splits, output-channel blocks of 64).  The reduction rows are
 // 16-row groups of 4 taps x 4 channels (taps t = kh * kwp + kw, kwp = KW rounded up to 4);
-// wave w owns groups w, w + 4, ..., w + 4 (NG - 1) (groups past the filter are computed on
-// valid addresses and dropped).  As in the forward kernel, the fragments of step kk + 1 are
+// wave w of NW owns groups w, w + NW, ..., w + NW (NG - 1) (groups past the filter are computed
+// on valid addresses and dropped).  Eight waves (two per SIMD) keep twice the transposing LDS reads
+// in flight of four, which the LDS needs to approach its bandwidth.  As in the forward kernel, the fragments of step kk + 1 are
 // read while the MFMAs of step kk run.
-template <int NG, bool X16>
-__global__ __launch_bounds__(256, 1) void band_bwf_kernel(const BandArgs a) {
+template <int NG, bool X16, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void band_bwf_kernel(const BandArgs a) {
     __shared__ __attribute__((aligned(1024))) unsigned char xb0[kXBand];
     __shared__ __attribute__((aligned(1024))) unsigned char xb1[kXBand];
     __shared__ __attribute__((aligned(1024))) unsigned char db0[kDyBandPix * 128];
@@ -478,11 +479,11 @@ __global__ __launch_bounds__(256, 1) void band_bwf_kernel(const BandArgs a) {
     const int co0 = blockIdx.y * 64;
     const int ngroups = a.KH * (a.kwp >> 2);
 
-    // Byte offset of this lane's tap (group g = wave + 4 y, tap 4 g + (ld & 3)) inside a staged band.
+    // Byte offset of this lane's tap (group g = wave + NW y, tap 4 g + (ld & 3)) inside a staged band.
     int tapb[NG];
 #pragma unroll
     for (int y = 0; y < NG; ++y) {
-        const int g = wave + 4 * y;
+        const int g = wave + NW * y;
         const int t = 4 * (g < ngroups ? g : 0) + (ld & 3);
         uint32_t kh, kw;
         a.dKwp.divmod((uint32_t)t, kh, kw);
@@ -490,21 +491,23 @@ __global__ __launch_bounds__(256, 1) void band_bwf_kernel(const BandArgs a) {
     }
 
     // dy of band b: pixel p of the band at k-row p of a k-major [256][64] tile (zero past the
-    // band), 8 direct-to-LDS copies per wave: copy i covers k-rows 8 i .. 8 i + 7.
-    auto dy_dma = [&](int b, unsigned char *buf) __attribute__((always_inline)) {
+    // band), 32 direct-to-LDS copies spread over the waves: copy i covers k-rows 8 i .. 8 i + 7.
+    constexpr int kDyCopies = kDyBandPix / (8 * NW);             // per wave
+    auto dy_copy = [&](int b, unsigned char *buf, int j) __attribute__((always_inline)) {
         const int n = b / a.bands_per_img;
         const int oh0 = (b - n * a.bands_per_img) * a.R;
         const int pb = min(a.R, a.OH - oh0) * a.OW;
         const bf16_t *base = a.dy + ((int64_t)n * a.OH + oh0) * a.OW * a.ys + co0;
+        const int i = wave + NW * j;
+        const int k = 8 * i + (lane >> 3);
+        const int ch = (lane & 7) ^ kmajor_swz<64>(k);
+        const bool ok = k < pb && co0 + ch * 8 < a.K;
+        dma16(ok ? (const void *)(base + (int64_t)k * a.ys + ch * 8) : (const void *)g_zero_chunk,
+              buf + 1024 * i);
+    };
+    auto dy_dma = [&](int b, unsigned char *buf) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < kDyBandPix / 32; ++j) {
-            const int i = wave + 4 * j;
-            const int k = 8 * i + (lane >> 3);
-            const int ch = (lane & 7) ^ kmajor_swz<64>(k);
-            const bool ok = k < pb && co0 + ch * 8 < a.K;
-            dma16(ok ? (const void *)(base + (int64_t)k * a.ys + ch * 8) : (const void *)g_zero_chunk,
-                  buf + 1024 * i);
-        }
+        for (int j = 0; j < kDyCopies; ++j) dy_copy(b, buf, j);
     };
 
     f32x4_t acc[4][NG];
@@ -515,7 +518,7 @@ __global__ __launch_bounds__(256, 1) void band_bwf_kernel(const BandArgs a) {
 
     int b = blockIdx.x;
     if (b < a.bands) {
-        band_dma<X16>(a, b, xb0);
+        band_dma<X16, NW>(a, b, xb0);
         dy_dma(b, db0);
     }
     wait_barrier<0>();
@@ -525,7 +528,7 @@ __global__ __launch_bounds__(256, 1) void band_bwf_kernel(const BandArgs a) {
         const unsigned char *dc = (it & 1) ? db1 : db0;
         const int bn = b + (int)gridDim.x;
         if (bn < a.bands) {
-            band_dma<X16>(a, bn, (it & 1) ? xb0 : xb1);
+            band_dma<X16, NW>(a, bn, (it & 1) ? xb0 : xb1);
             dy_dma(bn, (it & 1) ? db0 : db1);
         }
         const int n = b / a.bands_per_img;
@@ -604,7 +607,7 @@ __global__ __launch_bounds__(256, 1) void band_bwf_kernel(const BandArgs a) {
     float *part = reinterpret_cast<float *>(a.out) + (int64_t)blockIdx.x * a.KH * a.KW * a.C * a.K;
 #pragma unroll
     for (int y = 0; y < NG; ++y) {
-        const int g = wave + 4 * y;
+        const int g = wave + NW * y;
         if (g >= ngroups) continue;
         const int t = 4 * g + (ld >> 2), c = ld & 3;
         uint32_t kh, kw;
@@ -643,7 +646,7 @@ bool plan(const ConvShape &s, bool bwf, BandArgs &a) {
     int wst = (s.OW - 1) * s.sw + kwp;
     wst += wst & 1;
     if (bwf) {
-        if (s.KH * (kwp / 4) > 4 * kBwfGroupsPerWave || s.KH * (kwp / 4) < 4) return false;
+        if (s.KH * (kwp / 4) > kBwfGroups || s.KH * (kwp / 4) < 4) return false;
     } else {
         const int nks = ((s.KH * kwp * 4 + 63) / 64) * 2;     // even: the loop runs two steps at a time
         if (nks > kMaxKSteps) return false;
@@ -671,18 +674,18 @@ int bwf_splits(const BandArgs &a) { return std::min(a.bands, kCUs); }
 // 16-byte band copies need pixel pairs that never straddle the image edge.
 bool pairs_aligned(const ConvShape &s) { return s.pl % 2 == 0 && s.W % 2 == 0; }
 
+constexpr int kBwfWaves = 8;
+
 template <bool X16>
 void launch_bwf(int ng, dim3 grid, const BandArgs &a, hipStream_t st) {
+    constexpr int W = kBwfWaves;
+    const dim3 blk(64 * W);
     switch (ng) {
-    case 1: hipLaunchKernelGGL((band_bwf_kernel<1, X16>), grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((band_bwf_kernel<2, X16>), grid, dim3(256), 0, st, a); break;
-    case 3: hipLaunchKernelGGL((band_bwf_kernel<3, X16>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((band_bwf_kernel<4, X16>), grid, dim3(256), 0, st, a); break;
-    case 5: hipLaunchKernelGGL((band_bwf_kernel<5, X16>), grid, dim3(256), 0, st, a); break;
-    case 6: hipLaunchKernelGGL((band_bwf_kernel<6, X16>), grid, dim3(256), 0, st, a); break;
-    case 7: hipLaunchKernelGGL((band_bwf_kernel<7, X16>), grid, dim3(256), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((band_bwf_kernel<8, X16>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((band_bwf_kernel<9, X16>), grid, dim3(256), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((band_bwf_kernel<1, X16, W>), grid, blk, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((band_bwf_kernel<2, X16, W>), grid, blk, 0, st, a); break;
+    case 3: hipLaunchKernelGGL((band_bwf_kernel<3, X16, W>), grid, blk, 0, st, a); break;
+    case 4: hipLaunchKernelGGL((band_bwf_kernel<4, X16, W>), grid, blk, 0, st, a); break;
+    default: hipLaunchKernelGGL((band_bwf_kernel<5, X16, W>), grid, blk, 0, st, a); break;
     }
 }
 
@@ -755,7 +758,7 @@ hipError_t launch_conv_bwd_filter_band(const bf16_t *x4, const void *dy, int64_t
     a.nks = 0;
     const int splits = bwf_splits(a);
     const dim3 grid((unsigned)splits, (unsigned)((s.K + 63) / 64));
-    const int ng = (s.KH * (a.kwp / 4) + 3) / 4;     // 16-row tap groups per wave
+    const int ng = (s.KH * (a.kwp / 4) + kBwfWaves - 1) / kBwfWaves;     // 16-row tap groups per wave
     if (pairs_aligned(s))
         launch_bwf<true>(ng, grid, a, st);
     else
