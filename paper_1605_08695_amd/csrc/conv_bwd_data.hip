@@ -22,7 +22,9 @@ static hipError_t conv_bwd_data_t(const void *dy, int64_t dys, const void *w, vo
     // largest phase: ceil(H / sh) x ceil(W / sw) pixels per image
     const int mj = s.N * ((s.H + s.sh - 1) / s.sh) * ((s.W + s.sw - 1) / s.sw);
     if constexpr (sizeof(T) == 2) {
-        if (vi && vj && s.C % 8 == 0 && dxs % 8 == 0 && aligned16p(dx)) {
+        const int64_t wb = (int64_t)s.KH * s.KW * s.C * s.K * 2;
+        if (vi && vj && s.C % 8 == 0 && dxs % 8 == 0 && aligned16p(dx) &&
+            igemm2_fits(a, wb, span_bytes((int64_t)s.N * s.OH * s.OW, dys, s.K))) {
             const int z = s.sh * s.sw;
             if (!igemm2_launch<DIR_BWD_DATA>(a, mj, z, igemm2_tiles(a.NI, mj, z), st)) return hipErrorInvalidValue;
             return hipGetLastError();

@@ -89,7 +89,8 @@ static hipError_t conv_bwd_filter_t(const void *x, int64_t xs, const void *dy, i
     BwfPlan p;
     bool v2 = false;
     if constexpr (sizeof(T) == 2) {
-        if (vi && vj) {
+        if (vi && vj && igemm2_fits(a, span_bytes((int64_t)s.N * s.OH * s.OW, dys, s.K),
+                                    span_bytes((int64_t)s.N * s.H * s.W, xs, s.C))) {
             p = bwf_plan(dti, s, true);
             v2 = p.splits > 1 || aligned16p(dw);
         }

@@ -20,7 +20,9 @@ static hipError_t conv_fwd_t(const void *x, int64_t xs, const void *w, void *y, 
     const bool vj = s.C % EPC == 0 && xs % EPC == 0 && aligned16p(x);
     const int mj = s.N * s.OH * s.OW;
     if constexpr (sizeof(T) == 2) {
-        if (vi && vj && ys % 8 == 0 && aligned16p(y)) {
+        const int64_t wb = (int64_t)s.KH * s.KW * s.C * s.K * 2;
+        if (vi && vj && ys % 8 == 0 && aligned16p(y) &&
+            igemm2_fits(a, wb, span_bytes((int64_t)s.N * s.H * s.W, xs, s.C))) {
             if (!igemm2_launch<DIR_FWD>(a, mj, 1, igemm2_tiles(a.NI, mj, 1), st)) return hipErrorInvalidValue;
             return hipGetLastError();
         }

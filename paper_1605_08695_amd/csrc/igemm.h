@@ -62,6 +62,7 @@ struct IgArgs {
     int k_split;         // BWD_FILTER: reduction elements per split (multiple of the K tile)
     int64_t split_stride;// BWD_FILTER: floats between consecutive partial outputs
     FastDiv dC, dKW, dOW, dOH, dK;
+    uint32_t bytes_i, bytes_j;   // pipelined kernel: byte spans of src_i / src_j (each < 2^31)
 };
 
 template <typename T> struct Mfma;

@@ -3,12 +3,13 @@
 // Same GEMM views as igemm.h (I side = output channels, J side = rows), but
 // built for latency hiding on CDNA4:
 //
-//  * Global -> LDS copies use the gfx950 direct-to-LDS load
-//    (global_load_lds_dwordx4): no staging registers, no LDS-store
+//  * Global -> LDS copies use the direct-to-LDS buffer load
+//    (buffer_load_dwordx4 ... lds): no staging registers, no LDS-store
 //    instructions.  One wave instruction moves 64 x 16 bytes into a
 //    contiguous 1 KiB of LDS (lane l lands at base + 16 l), so each lane is
-//    given the global chunk that belongs at its LDS slot; out-of-range chunks
-//    are fetched from a 16-byte zero page.
+//    given the chunk that belongs at its LDS slot, as a 32-bit byte offset into
+//    its operand; out-of-range chunks get an offset past the operand's end,
+//    which the buffer range check turns into zeros.
 //  * A ring of three LDS stages: the copies of K-tile t+2 are in flight while
 //    the MFMAs consume tile t.  Each stage is a separate LDS object and the
 //    loop is unrolled by three, so the compiler can see which stage an LDS
@@ -25,7 +26,8 @@
 //
 // Requirements (checked by the launcher): bf16, every gathered 16-byte chunk
 // is aligned and lies within one pixel's channels (channel counts and pixel
-// strides multiples of 8, 16-byte aligned bases).
+// strides multiples of 8, 16-byte aligned bases), both operands span fewer
+// than 2^31 bytes and the filter has at most 31 rows and 31 columns.
 #pragma once
 #include <type_traits>
 
@@ -41,15 +43,51 @@ __device__ __attribute__((aligned(16))) uint32_t g_zero_chunk[4];
 // One 16-byte direct-to-LDS copy per lane: lane l's chunk lands at lds_base + 16 l.
 // Issued from inline assembly so that the compiler does not track these copies:
 // its LDS-DMA alias tracking would otherwise make every LDS read wait for every
-// copy in flight.  Completion is ordered explicitly with wait_barrier<N>().
+// copy in flight.  Completion is ordered explicitly with wait_barrier<N>().  The s_nop is the
+// wait state that an LDS DMA needs after a scalar write of M0.
 __device__ __forceinline__ void dma16(const void *src, unsigned char *lds_base) {
     const uint32_t lds_addr = __builtin_amdgcn_readfirstlane(
         (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char *)lds_base);
     uint32_t saved;
-    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
                  : "=&s"(saved)
                  : "v"(src), "s"(lds_addr)
                  : "memory");
+}
+
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+// Raw buffer resource over [base, base + bytes): no stride, no swizzle, dword data format.
+// Loads through it at byte offsets >= bytes return zeros (checked per dword).
+__device__ __forceinline__ i32x4_t buffer_rsrc(const void *base, uint32_t bytes) {
+    const uint64_t b = (uint64_t)(uintptr_t)base;
+    i32x4_t r;
+    r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)b);
+    r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(b >> 32) & 0xffffu));
+    r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+    r[3] = 0x00020000;
+    return r;
+}
+
+// LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_u32(const unsigned char *p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const unsigned char *)p;
+}
+
+// One 16-byte buffer-to-LDS copy per lane: lane l's chunk, at byte offset voff of the
+// buffer, lands at LDS address lds_addr + 16 l.  Ordered like dma16().
+__device__ __forceinline__ void bdma16(const i32x4_t rs, uint32_t voff, uint32_t lds_addr) {
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "v"(voff), "s"(rs), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
+                 : "memory");
+}
+
+// Bits lo .. hi-1 set (none when lo >= hi); hi <= 31.
+__device__ __forceinline__ uint32_t range_mask(int lo, int hi) {
+    return lo < hi ? ((1u << hi) - 1u) & ~((1u << lo) - 1u) : 0u;
 }
 
 // Wait until at most N vector-memory operations of this wave are in flight and
@@ -130,7 +168,7 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     // (the launcher may keep the hardware order: for bwd-filter splits of the AlexNet layers
     // spreading one split's tiles over all XCDs measured faster than concentrating them)
     const int lin_hw = (int)(blockIdx.x + gridDim.x * blockIdx.z);
@@ -144,14 +182,14 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
 
     const bf16_t *__restrict__ srcI = reinterpret_cast<const bf16_t *>(a.src_i);
     const bf16_t *__restrict__ srcJ = reinterpret_cast<const bf16_t *>(a.src_j);
-    const void *zero = (const void *)g_zero_chunk;
-
     // ------------------------------------------------------------ direction set-up
     int MJ_ext, k_beg = 0, k_end;
     int rh = 0, rw = 0, h0 = 0, w0 = 0, Hp = 1, Wp = 1, offh = 0, offw = 0, KHp = 1, KWp = 1;
     if constexpr (DIR == DIR_FWD) {
         MJ_ext = a.N * a.OH * a.OW;
         k_end = a.KH * a.KW * a.C;
+        KHp = a.KH;
+        KWp = a.KW;
     } else if constexpr (DIR == DIR_BWD_DATA) {
         const int z = bz;
         rh = z / a.sw;
@@ -175,70 +213,89 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     const int nk = k_end > k_beg ? (k_end - k_beg + BK - 1) / BK : 0;
 
     // ------------------------------------------------------------ copy plan
+    // Every copy is one buffer load into LDS with a 32-bit byte offset per lane.  The buffer
+    // resource of an operand spans exactly its bytes (fewer than 2^31, checked by the
+    // launcher) and the hardware range check returns zeros for offsets at or past the end, so
+    // padding taps, reduction entries past the end and rows past a tensor are given such an
+    // offset (kBad, or a pixel offset that lies past the tensor) instead of a branch.  Along
+    // the reduction axis both operands are zero past the end.  Rows past the output extent
+    // (channels beyond NI, filter taps beyond KH*KW*C) are not masked: they read other
+    // elements of the same operand into output rows that the epilogue drops.
+    //
     // [row][k] operands: copy r of this thread covers row 8 slot + lane/8, slot = wave*NL_op + r,
     // and the logical chunk (lane & 7) ^ (lane >> 3); it lands at byte 1024 slot of the tile.
     // k-major operands with R rows: copy r covers k-row slot (512/R) + lane / (R/8) and row
     // chunk (lane % (R/8)) ^ kmajor_swz(k-row).  Everything that does not depend on the K tile is
     // computed here once.
+    constexpr uint32_t kBad = 0x80000000u;
+    const i32x4_t rsI = buffer_rsrc(a.src_i, a.bytes_i);
+    const i32x4_t rsJ = buffer_rsrc(a.src_j, a.bytes_j);
     const int dchunk = (lane & 7) ^ (lane >> 3);
 
-    // [row][k] J rows (FWD: output pixels; BWD_DATA: dx pixels of the phase)
-    const bf16_t *jptr[NLJ];
-    int jy0[NLJ], jx0[NLJ];
-    bool jok[NLJ];
+    // I operand: byte offset of each copy at K-tile 0 (k-major: + kt * BK * ldI2 per tile;
+    // BWD_DATA filter rows ci: + the tile's tap and channel offset)
+    uint32_t ivo[NLI];
+    const uint32_t ldI2 = 2u * (uint32_t)((DIR == DIR_FWD) ? (int64_t)a.K : a.ys);
+    if constexpr (TI) {
+        constexpr int CPR = BI / 8;
+#pragma unroll
+        for (int r = 0; r < NLI; ++r) {
+            const int krow = (wave * NLI + r) * (512 / BI) + lane / CPR;
+            const int co = i0 + ((lane % CPR) ^ kmajor_swz<BI>(krow)) * 8;
+            ivo[r] = (uint32_t)(k_beg + krow) * ldI2 + 2u * (uint32_t)co;
+        }
+    } else {
+#pragma unroll
+        for (int r = 0; r < NLI; ++r) {
+            const int ci = i0 + 8 * (wave * NLI + r) + (lane >> 3);
+            ivo[r] = (uint32_t)ci * 2u * (uint32_t)a.K;
+        }
+    }
+
+    // J operand.  FWD / BWD_DATA ([row][k]): byte offset of the row's pixel for tap (0, 0) and
+    // the complements of the masks of filter rows / columns whose tap lies inside the image
+    // (bit 31 always set: it marks reduction entries past the end).  BWD_FILTER (k-major):
+    // per copy, the pixel (byte offset, oh * sh, ow * sw) of its k-row, advanced by BK pixels
+    // per tile, and the byte offset and (dh, dw) displacement of its chunk's filter tap.
+    uint32_t jvo[NLJ], jnh[NLJ], jnw[NLJ], tvo[NLJ];
+    int ohs[NLJ], ows[NLJ], fdh[NLJ], fdw[NLJ];
+    const uint32_t xs2 = 2u * (uint32_t)a.xs, ys2 = 2u * (uint32_t)a.ys;
     if constexpr (!TJ) {
+        const int Hlim = (DIR == DIR_FWD) ? a.H : a.OH;
+        const int Wlim = (DIR == DIR_FWD) ? a.W : a.OW;
 #pragma unroll
         for (int r = 0; r < NLJ; ++r) {
             const int m = j0 + 8 * (wave * NLJ + r) + (lane >> 3);
-            jok[r] = m < MJ_ext;
-            const int mm = jok[r] ? m : 0;
+            const bool ok = m < MJ_ext;
+            const int mm = ok ? m : 0;
+            int y0, x0, hlo, hhi, wlo, whi;
             if constexpr (DIR == DIR_FWD) {
                 const int ow = mm % a.OW;
                 const int t = mm / a.OW;
                 const int oh = t % a.OH;
                 const int n = t / a.OH;
-                jy0[r] = oh * a.sh - a.pt;
-                jx0[r] = ow * a.sw - a.pl;
-                jptr[r] = srcJ + (((int64_t)n * a.H + jy0[r]) * a.W + jx0[r]) * a.xs;
+                y0 = oh * a.sh - a.pt;     // tap kh reads row y0 + kh
+                x0 = ow * a.sw - a.pl;
+                jvo[r] = (uint32_t)(((((int64_t)n * a.H + y0) * a.W + x0) * a.xs) * 2);
+                hlo = max(0, -y0); hhi = min(KHp, Hlim - y0);
+                wlo = max(0, -x0); whi = min(KWp, Wlim - x0);
             } else {
                 const int tw = mm % Wp;
                 const int t = mm / Wp;
                 const int th = t % Hp;
                 const int n = t / Hp;
-                jy0[r] = th + offh;        // oh = jy0 - jh
-                jx0[r] = tw + offw;        // ow = jx0 - jw
-                jptr[r] = srcJ + (((int64_t)n * a.OH + jy0[r]) * a.OW + jx0[r]) * a.ys;
+                y0 = th + offh;            // tap jh reads dy row y0 - jh
+                x0 = tw + offw;
+                jvo[r] = (uint32_t)(((((int64_t)n * a.OH + y0) * a.OW + x0) * a.ys) * 2);
+                hlo = max(0, y0 - Hlim + 1); hhi = min(KHp, y0 + 1);
+                wlo = max(0, x0 - Wlim + 1); whi = min(KWp, x0 + 1);
             }
+            jnh[r] = ok ? ~range_mask(hlo, hhi) : ~0u;
+            jnw[r] = ~range_mask(wlo, whi);
         }
     }
-    // BWD_DATA I rows (filter rows ci)
-    const bf16_t *iptr[NLI];
-    bool iok[NLI];
-    if constexpr (!TI) {
-#pragma unroll
-        for (int r = 0; r < NLI; ++r) {
-            const int ci = i0 + 8 * (wave * NLI + r) + (lane >> 3);
-            iok[r] = ci < a.NI;
-            iptr[r] = srcI + (int64_t)(iok[r] ? ci : 0) * a.K;
-        }
-    }
-    // k-major I operand (FWD filter [k][co], BWD_FILTER dy [pixel][co])
-    int tik[NLI];
-    if constexpr (TI) {
-        constexpr int CPR = BI / 8;
-        const int64_t ld = (DIR == DIR_FWD) ? (int64_t)a.K : a.ys;
-#pragma unroll
-        for (int r = 0; r < NLI; ++r) {
-            const int krow = (wave * NLI + r) * (512 / BI) + lane / CPR;
-            const int co = i0 + ((lane % CPR) ^ kmajor_swz<BI>(krow)) * 8;
-            iok[r] = co < a.NI;
-            tik[r] = krow;
-            iptr[r] = srcI + (int64_t)(k_beg + krow) * ld + (iok[r] ? co : 0);
-        }
-    }
-    // BWD_FILTER J rows (filter taps, k-major): per copy, the 8 taps of its row chunk
-    int fr_dh[NLJ], fr_dw[NLJ], fr_ci[NLJ], fr_k[NLJ];
-    bool fr_ok[NLJ];
+    uint32_t adv_base = 0, adv_d1 = 0, adv_d2 = 0;
+    int adv_w = 0, adv_h = 0, lim_w = 0, lim_h = 0;
     if constexpr (TJ) {
         constexpr int CPR = BJ / 8;
 #pragma unroll
@@ -246,19 +303,32 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
             const int krow = (wave * NLJ + r) * (512 / BJ) + lane / CPR;
             const int c = (lane % CPR) ^ kmajor_swz<BJ>(krow);
             const int r0 = j0 + c * 8;
-            fr_ok[r] = r0 < MJ_ext;
-            const int rr = fr_ok[r] ? r0 : 0;
+            const int rr = r0 < MJ_ext ? r0 : 0;
             const int ci = rr % a.C;
             const int t = rr / a.C;
-            fr_ci[r] = ci;
-            fr_dw[r] = t % a.KW - a.pl;
-            fr_dh[r] = t / a.KW - a.pt;
-            fr_k[r] = krow;
+            fdw[r] = t % a.KW - a.pl;
+            fdh[r] = t / a.KW - a.pt;
+            tvo[r] = (uint32_t)(((((int64_t)fdh[r] * a.W + fdw[r]) * a.xs) + ci) * 2);
+            uint32_t q, ow, n, oh;
+            a.dOW.divmod((uint32_t)(k_beg + krow), q, ow);
+            a.dOH.divmod(q, n, oh);
+            ohs[r] = (int)oh * a.sh;
+            ows[r] = (int)ow * a.sw;
+            jvo[r] = (uint32_t)(((((int64_t)n * a.H + ohs[r]) * a.W + ows[r]) * a.xs) * 2);
         }
+        // BK pixels = dn images + ah rows + aw columns (ah < OH, aw < OW); adding them to
+        // (oh, ow) wraps each coordinate at most once.
+        const int pq = a.OH * a.OW;
+        const int dn = BK / pq, rem = BK % pq, ah = rem / a.OW, aw = rem % a.OW;
+        adv_w = aw * a.sw; lim_w = a.OW * a.sw;
+        adv_h = ah * a.sh; lim_h = a.OH * a.sh;
+        const int64_t hw = (int64_t)a.H * a.W;
+        adv_base = (uint32_t)(((int64_t)dn * hw + (int64_t)ah * a.sh * a.W + (int64_t)aw * a.sw) * a.xs * 2);
+        adv_d1 = (uint32_t)(((int64_t)a.sh * a.W - (int64_t)a.OW * a.sw) * a.xs * 2);   // column wrap
+        adv_d2 = (uint32_t)((hw - (int64_t)a.OH * a.sh * a.W) * a.xs * 2);              // row wrap
     }
-    // k decomposition of this thread's chunk for [row][k] operands, recomputed per tile
-    // with multiply-high division.  FWD J: k = (kh, kw, ci) over (KH, KW, C);
-    // BWD_DATA: k = (jh, jw, co) over (KHp, KWp, K).
+    // k decomposition of this lane's chunk for [row][k] operands.  FWD J: k = (kh, kw, ci)
+    // over (KH, KW, C); BWD_DATA: k = (jh, jw, co) over (KHp, KWp, K).
     FastDiv dInner, dMid;
     if constexpr (DIR == DIR_FWD) { dInner = a.dC; dMid = a.dKW; }
     if constexpr (DIR == DIR_BWD_DATA) { dInner = a.dK; dMid.init((uint32_t)(KWp > 0 ? KWp : 1)); }
@@ -266,81 +336,78 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     // K-tile order.  With 64 | channels, every 64-wide K-tile lies inside one filter tap,
     // and the tiles are visited channel-chunk outer, tap inner: consecutive tiles then read
     // the same input rows shifted by one tap, which stay in L1/L2.  issue() is called for
-    // kt = 0, 1, 2, ... in order, so the (chunk, tap) position advances by one per call.
-    int perm_T = 1, perm_CC = 0;
-    if constexpr (DIR == DIR_FWD) {
-        if (a.C % BK == 0 && a.KH * a.KW > 1) { perm_T = a.KH * a.KW; perm_CC = a.C / BK; }
-    } else if constexpr (DIR == DIR_BWD_DATA) {
-        if (a.K % BK == 0 && KHp * KWp > 1) { perm_T = KHp * KWp; perm_CC = a.K / BK; }
-    }
-    int perm_tap = 0, perm_cc = 0;
+    // kt = 0, 1, 2, ... in order, so the (chunk, tap) position advances by one per call; the
+    // tap and channel chunk of a tile are then the same for every lane.
+    bool perm = false;
+    int perm_CC = 0;
+    if constexpr (DIR == DIR_FWD) perm = a.C % BK == 0 && a.KH * a.KW > 1;
+    if constexpr (DIR == DIR_BWD_DATA) perm = a.K % BK == 0 && KHp * KWp > 1;
+    if constexpr (DIR != DIR_BWD_FILTER) perm_CC = (DIR == DIR_FWD ? a.C : a.K) / BK;
+    int perm_kh = 0, perm_kw = 0, perm_cc = 0;
 
     // Issue the copies of K-tile kt into LDS stage `st`.
     auto issue = [&](int kt_seq, unsigned char *st) __attribute__((always_inline)) {
+        const uint32_t stI = lds_u32(st);
+        const uint32_t stJ = stI + IB;
         int kt = kt_seq;
+        uint32_t kq0 = 0, kq1 = 0, kq2 = 0;
+        bool kin = true;
         if constexpr (DIR != DIR_BWD_FILTER) {
-            if (perm_CC > 0) {
-                kt = perm_tap * perm_CC + perm_cc;
-                if (++perm_tap == perm_T) { perm_tap = 0; ++perm_cc; }
+            if (perm) {
+                kq0 = perm_kh; kq1 = perm_kw;
+                kq2 = perm_cc * BK + dchunk * 8;
+                kt = (perm_kh * KWp + perm_kw) * perm_CC + perm_cc;
+                if (++perm_kw == KWp) {
+                    perm_kw = 0;
+                    if (++perm_kh == KHp) { perm_kh = 0; ++perm_cc; }
+                }
+            } else {
+                const int k = k_beg + kt * BK + dchunk * 8;
+                kin = k < k_end;
+                uint32_t t;
+                dInner.divmod((uint32_t)k, t, kq2);
+                dMid.divmod(t, kq0, kq1);
             }
         }
-        const int kt0 = k_beg + kt * BK;
-        unsigned char *stI = st;
-        unsigned char *stJ = st + IB;
-        uint32_t kq0 = 0, kq1 = 0, kq2 = 0;
-        if constexpr (DIR != DIR_BWD_FILTER) {
-            uint32_t t;
-            dInner.divmod((uint32_t)(kt0 + dchunk * 8), t, kq2);
-            dMid.divmod(t, kq0, kq1);
-        }
-        const bool kin = kt0 + dchunk * 8 < k_end;
         // ---------------- I operand
         if constexpr (TI) {
-            const int64_t step = (int64_t)(kt * BK) * ((DIR == DIR_FWD) ? (int64_t)a.K : a.ys);
+            const uint32_t step = (uint32_t)(kt * BK) * ldI2;
 #pragma unroll
-            for (int r = 0; r < NLI; ++r) {
-                const bool ok = iok[r] && kt0 + tik[r] < k_end;
-                dma16(ok ? (const void *)(iptr[r] + step) : zero, stI + (wave * NLI + r) * 1024);
-            }
+            for (int r = 0; r < NLI; ++r) bdma16(rsI, ivo[r] + step, stI + (wave * NLI + r) * 1024);
         } else {
             // BWD_DATA filter: w[rh + sh*jh][rw + sw*jw][ci][co..]
-            const int64_t koff = ((int64_t)(rh + a.sh * (int)kq0) * a.KW + (rw + a.sw * (int)kq1)) * a.C * a.K + kq2;
+            const uint32_t tap = (uint32_t)(rh + a.sh * (int)kq0) * (uint32_t)a.KW + (uint32_t)(rw + a.sw * (int)kq1);
+            const uint32_t koff = kin ? (tap * (uint32_t)a.C * (uint32_t)a.K + kq2) * 2u : kBad;
 #pragma unroll
-            for (int r = 0; r < NLI; ++r)
-                dma16(iok[r] && kin ? (const void *)(iptr[r] + koff) : zero, stI + (wave * NLI + r) * 1024);
+            for (int r = 0; r < NLI; ++r) bdma16(rsI, ivo[r] + koff, stI + (wave * NLI + r) * 1024);
         }
         // ---------------- J operand
         if constexpr (TJ) {
 #pragma unroll
             for (int r = 0; r < NLJ; ++r) {
-                const int k = kt0 + fr_k[r];
-                const bool kok = fr_ok[r] && k < k_end;
-                uint32_t t, ow, n, oh;
-                a.dOW.divmod((uint32_t)(kok ? k : 0), t, ow);
-                a.dOH.divmod(t, n, oh);
-                const int ih = (int)oh * a.sh + fr_dh[r];
-                const int iw = (int)ow * a.sw + fr_dw[r];
-                const bool ok = kok && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
-                dma16(ok ? (const void *)(srcJ + (((int64_t)n * a.H + ih) * a.W + iw) * a.xs + fr_ci[r]) : zero,
-                      stJ + (wave * NLJ + r) * 1024);
+                const bool ok = (unsigned)(ohs[r] + fdh[r]) < (unsigned)a.H && (unsigned)(ows[r] + fdw[r]) < (unsigned)a.W;
+                bdma16(rsJ, ok ? jvo[r] + tvo[r] : kBad, stJ + (wave * NLJ + r) * 1024);
             }
-        } else {
-            int64_t koff;
-            int dy, dx;
-            if constexpr (DIR == DIR_FWD) {
-                dy = (int)kq0; dx = (int)kq1;
-                koff = ((int64_t)dy * a.W + dx) * a.xs + kq2;
-            } else {
-                dy = -(int)kq0; dx = -(int)kq1;
-                koff = ((int64_t)dy * a.OW + dx) * a.ys + kq2;
-            }
-            const int Hlim = (DIR == DIR_FWD) ? a.H : a.OH;
-            const int Wlim = (DIR == DIR_FWD) ? a.W : a.OW;
 #pragma unroll
             for (int r = 0; r < NLJ; ++r) {
-                const bool ok = jok[r] && kin && (unsigned)(jy0[r] + dy) < (unsigned)Hlim &&
-                                (unsigned)(jx0[r] + dx) < (unsigned)Wlim;
-                dma16(ok ? (const void *)(jptr[r] + koff) : zero, stJ + (wave * NLJ + r) * 1024);
+                ows[r] += adv_w;
+                const bool c1 = ows[r] >= lim_w;
+                if (c1) ows[r] -= lim_w;
+                ohs[r] += adv_h + (c1 ? a.sh : 0);
+                const bool c2 = ohs[r] >= lim_h;
+                if (c2) ohs[r] -= lim_h;
+                jvo[r] += adv_base + (c1 ? adv_d1 : 0u) + (c2 ? adv_d2 : 0u);
+            }
+        } else {
+            uint32_t koff;
+            if constexpr (DIR == DIR_FWD) koff = (kq0 * (uint32_t)a.W + kq1) * xs2 + kq2 * 2u;
+            else koff = kq2 * 2u - (kq0 * (uint32_t)a.OW + kq1) * ys2;
+            const uint32_t khe = kin ? kq0 : 31u;
+#pragma unroll
+            for (int r = 0; r < NLJ; ++r) {
+                const uint32_t bad = (uint32_t)(__builtin_amdgcn_sbfe((int)jnh[r], khe, 1u) |
+                                                __builtin_amdgcn_sbfe((int)jnw[r], kq1, 1u));
+                bdma16(rsJ, (jvo[r] + koff) | bad, stJ + (wave * NLJ + r) * 1024);
             }
         }
     };

@@ -78,6 +78,23 @@ static bool igemm2_launch(IgArgs &a, int mj, int zdim, const Igemm2Tile &t, hipS
     }
 }
 
+// Bytes from the first element of a pixel-major bf16 operand to the end of its last
+// pixel's channels.
+static inline int64_t span_bytes(int64_t pixels, int64_t stride, int64_t ch) {
+    return pixels > 0 ? ((pixels - 1) * stride + ch) * 2 : 0;
+}
+
+// The pipelined kernel addresses each operand with 32-bit byte offsets (offsets from 2^31
+// up read as zeros) and keeps masks of a filter's valid rows and columns in 31 bits.
+// Records the spans when they fit.
+static inline bool igemm2_fits(IgArgs &a, int64_t span_i, int64_t span_j) {
+    constexpr int64_t kLim = int64_t(1) << 31;
+    if (span_i >= kLim || span_j >= kLim || a.KH > 31 || a.KW > 31) return false;
+    a.bytes_i = (uint32_t)span_i;
+    a.bytes_j = (uint32_t)span_j;
+    return true;
+}
+
 static inline void fill_geom(IgArgs &a, const ConvShape &s) {
     a.N = s.N; a.H = s.H; a.W = s.W; a.C = s.C;
     a.OH = s.OH; a.OW = s.OW; a.K = s.K;
@@ -92,6 +109,7 @@ static inline void fill_geom(IgArgs &a, const ConvShape &s) {
     a.xcd_order = 1;
     a.k_split = 0;
     a.split_stride = 0;
+    a.bytes_i = a.bytes_j = 0;
 }
 
 }  // namespace tfk
