@@ -6,12 +6,17 @@ accumulation, conv 11x11/4 64 -> pool 3/2 -> 5x5 192 -> pool -> 3x3 384 ->
 N(0,1) upstream gradient of the last pool, plain SGD (lr 0.01) of every filter
 and bias.  All inputs are resident in HBM before timing starts.
 
-    python bench.py [--steps K] [--warmup W] [--eager] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--launch streams|graph|serial] [--no-cpu-baseline]
 
 Prints one JSON line: ms per step (the timed region is K whole steps between
 two device synchronisations), conv TFLOP/s against the bf16 MFMA peak, the
 roofline entry of the convolution kernels measured with HIP events on the
 stream they run on, and the CPU oracle timed on a bounded batch slice.
+
+Launch modes: ``streams`` (default) launches every op from the host, the filter
+gradients on a second stream that overlaps the rest of the backward pass;
+``graph`` replays the same two-stream step captured as one HIP graph; ``serial``
+launches every op in order on one stream.
 """
 from __future__ import annotations
 
@@ -38,7 +43,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--batch", type=int, default=128)
-    ap.add_argument("--eager", action="store_true", help="launch every op from Python instead of a HIP graph")
+    ap.add_argument("--launch", choices=("streams", "graph", "serial"), default="streams",
+                    help="two streams launched from the host (default), the two-stream step as a HIP graph, "
+                         "or one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=128, help="images of the batch the oracle steps through")
     ap.add_argument("--seed", type=int, default=0)
@@ -106,24 +113,24 @@ def conv_flops(net, op):
 
 
 class EventTrace:
-    """Step-driver hook that brackets every op with HIP events on the current stream."""
+    """Step-driver hook that brackets every op with HIP events on the stream it runs on."""
 
     def __init__(self, torch):
         self.torch = torch
-        self.open = None
         self.rec = []           # (kind, op, start, end)
 
-    def __call__(self, event, op, **t):
+    def _event(self, stream):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record(stream if stream is not None else self.torch.cuda.current_stream())
+        return e
+
+    def __call__(self, event, op, stream=None, **t):
         if event.endswith(":end"):
-            e = self.torch.cuda.Event(enable_timing=True)
-            e.record()
             kind, op0, s = self.open
-            self.rec.append((kind, op0, s, e))
-            self.open = None
+            assert kind == event[:-4] and op0 is op
+            self.rec.append((kind, op0, s, self._event(stream)))
         else:
-            s = self.torch.cuda.Event(enable_timing=True)
-            s.record()
-            self.open = (event, op, s)
+            self.open = (event, op, self._event(stream))
 
 
 def gemm_reference(net, torch):
@@ -193,7 +200,7 @@ def main():
 
     # ---------------------------------------------------------------- timed region
     graph = None
-    if not args.eager:
+    if args.launch == "graph":
         s = torch.cuda.Stream()
         s.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(s):
@@ -206,7 +213,8 @@ def main():
             rep.step()
         run = graph.replay
     else:
-        run = rep.step
+        concurrent = args.launch == "streams"
+        run = lambda: rep.step(concurrent=concurrent)
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
@@ -225,14 +233,17 @@ def main():
     print("bench: timed %d steps, %.3f ms/step (median %.3f)" % (args.steps, ms_per_step, np.median(step_ms)),
           file=sys.stderr, flush=True)
 
-    # ---------------------------------------------------------------- per-op events (eager)
+    # ---------------------------------------------------------------- per-op events
+    # Every op launched alone, in order, on one stream and bracketed by HIP events on that
+    # stream: the duration of each kernel by itself (in the two-stream step the filter
+    # gradients share the GPU with the input gradients), from which the roofline is taken.
     tr = EventTrace(torch)
     reps = max(3, min(10, args.steps))
     per_kind = {}
     per_layer = {}
     for r in range(reps):
         tr.rec.clear()
-        rep.step(trace=tr)
+        rep.step(trace=tr, concurrent=False)
         torch.cuda.synchronize()
         for kind, op, s, e in tr.rec:
             ms = s.elapsed_time(e)
@@ -310,7 +321,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": "alexnet_b%d" % args.batch, "global_batch": args.batch, "image": [224, 224, 3],
                    "layers": "conv11x11/4-64,pool3/2,conv5x5-192,pool3/2,conv3x3-384,conv3x3-256,conv3x3-256,pool3/2",
-                   "launch": "eager" if args.eager else "hip_graph"},
+                   "launch": {"streams": "host launches, two streams", "graph": "hip_graph, two streams",
+                              "serial": "host launches, one stream"}[args.launch]},
         "step_ms_median": round(float(np.median(step_ms)), 4),
         "step_ms_p10": round(float(np.percentile(step_ms, 10)), 4),
         "step_ms_p90": round(float(np.percentile(step_ms, 90)), 4),
@@ -329,6 +341,7 @@ def main():
                      "frac": round(flops[dom] / (per_kind[dom] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
                      "traffic": recorded_traffic(dom),
                      "avg_launch_us": round(per_kind[dom] * 1e3 / n_dom, 2),
+                     "measured": "HIP events around each launch, every op alone on one stream",
                      "flop_per_launch": round(flops[dom] / n_dom)},
         "cpu_baseline": cpu,
     }

@@ -135,6 +135,13 @@ class Replica:
                 need = max(need, ops.conv2d_workspace_bytes(op_kind, x, c.cout, c.kh, c.kw, (c.sh, c.sw), c.pads))
             need = max(need, ops.bias_relu_bwd_workspace_bytes(self._slice(self.act, c)))
         self.ws = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=dev)
+        # ---- filter gradients run on a second stream, with a workspace of their own
+        need = 0
+        for c in net.convs:
+            need = max(need, ops.conv2d_workspace_bytes(2, self.act[c.src], c.cout, c.kh, c.kw, (c.sh, c.sw),
+                                                        c.pads))
+        self.ws_side = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=dev)
+        self.side = torch.cuda.Stream(device=dev)
 
     # ------------------------------------------------------------------ helpers
     def _width(self, op) -> int:
@@ -150,19 +157,26 @@ class Replica:
             x = self.act[op.src]
             y = self._slice(self.act, op)
             if isinstance(op, Conv):
-                if trace: trace("conv_bias_relu_fwd", op, x=x, w=self.Wlp[op.name], b=self.b[op.name], y=y)
+                if trace: trace("conv_bias_relu_fwd", op, stream=stream, x=x, w=self.Wlp[op.name],
+                                b=self.b[op.name], y=y)
                 ops.conv2d_fwd_bias_relu(x, self.Wlp[op.name], self.b[op.name], (op.sh, op.sw), op.pads, y=y,
                                          ws=self.ws, stream=stream)
-                if trace: trace("conv_bias_relu_fwd:end", op, y=y)
+                if trace: trace("conv_bias_relu_fwd:end", op, stream=stream, y=y)
             else:
-                if trace: trace("maxpool_fwd", op, x=x, y=y, argmax=self.argmax[op.name])
+                if trace: trace("maxpool_fwd", op, stream=stream, x=x, y=y, argmax=self.argmax[op.name])
                 ops.maxpool_fwd(x, (op.kh, op.kw), (op.sh, op.sw), op.pads, y=y, argmax=self.argmax[op.name],
                                 stream=stream)
-                if trace: trace("maxpool_fwd:end", op, y=y, argmax=self.argmax[op.name])
+                if trace: trace("maxpool_fwd:end", op, stream=stream, y=y, argmax=self.argmax[op.name])
 
-    def backward(self, trace=None, stream=None):
+    def backward(self, trace=None, stream=None, side=None):
+        """Gradients of every variable.  With ``side`` (a second stream), each convolution's
+        filter gradient runs there, concurrently with its input gradient and everything after
+        it on ``stream``: the two only read the same tensors, and the side stream joins back
+        before this returns (the dataflow executor runs independent kernels on several GPU
+        streams, Section 5)."""
         net = self.net
         written = set()
+        cur = stream if stream is not None else torch.cuda.current_stream()
         for op in reversed(net.ops):
             dy = self._slice(self.grad, op)
             src_grad = op.src != "x" or net.input_grad
@@ -173,46 +187,57 @@ class Replica:
                 else:
                     y = self._slice(self.act, op)
                     dpre = self._slice({op.dst: self.dpre_out}, op) if op.dst == net.output else dy
-                    if trace: trace("bias_relu_bwd", op, y=y, dy=dy)
+                    if trace: trace("bias_relu_bwd", op, stream=stream, y=y, dy=dy)
                     ops.bias_relu_bwd(y, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
-                    if trace: trace("bias_relu_bwd:end", op, dpre=dpre, db=self.db[op.name])
+                    if trace: trace("bias_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
                 x = self.act[op.src]
-                if trace: trace("conv_bwd_filter", op, x=x, dy=dpre)
+                if side is not None:
+                    side.wait_stream(cur)
+                fs = side if side is not None else stream
+                if trace: trace("conv_bwd_filter", op, stream=fs, x=x, dy=dpre)
                 ops.conv2d_bwd_filter(x, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, dw=self.dW[op.name],
-                                      ws=self.ws, stream=stream)
-                if trace: trace("conv_bwd_filter:end", op, dw=self.dW[op.name])
+                                      ws=self.ws if side is None else self.ws_side, stream=fs)
+                if trace: trace("conv_bwd_filter:end", op, stream=fs, dw=self.dW[op.name])
                 if src_grad:
                     dx = self.grad[op.src]
-                    if trace: trace("conv_bwd_input", op, dy=dpre, w=self.Wlp[op.name], dx=dx, beta=beta)
+                    if trace: trace("conv_bwd_input", op, stream=stream, dy=dpre, w=self.Wlp[op.name], dx=dx,
+                                    beta=beta)
                     ops.conv2d_bwd_input(dpre, self.Wlp[op.name], dx, (op.sh, op.sw), op.pads, beta=beta,
                                          stream=stream)
-                    if trace: trace("conv_bwd_input:end", op, dx=dx)
+                    if trace: trace("conv_bwd_input:end", op, stream=stream, dx=dx)
             elif op.name in self.pool_relu:
                 conv = self.pool_relu[op.name]
                 y, dpre, am = self.act[op.src], self.grad[op.src], self.argmax[op.name]
-                if trace: trace("maxpool_relu_bwd", op, dy=dy, argmax=am, y=y, dpre=dpre, beta=beta)
+                if trace: trace("maxpool_relu_bwd", op, stream=stream, dy=dy, argmax=am, y=y, dpre=dpre,
+                                beta=beta)
                 ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
                                          dbias=self.db[conv.name], ws=self.ws, stream=stream)
-                if trace: trace("maxpool_relu_bwd:end", op, dpre=dpre, db=self.db[conv.name])
+                if trace: trace("maxpool_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[conv.name])
             else:
                 if src_grad:
                     dx = self.grad[op.src]
                     am = self.argmax[op.name]
-                    if trace: trace("maxpool_bwd", op, dy=dy, argmax=am, dx=dx, beta=beta)
+                    if trace: trace("maxpool_bwd", op, stream=stream, dy=dy, argmax=am, dx=dx, beta=beta)
                     ops.maxpool_bwd(dy, am, dx, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
                                     stream=stream)
-                    if trace: trace("maxpool_bwd:end", op, dx=dx)
+                    if trace: trace("maxpool_bwd:end", op, stream=stream, dx=dx)
             if src_grad:
                 written.add(op.src)
+        if side is not None:
+            cur.wait_stream(side)
 
     def update(self, trace=None, stream=None):
-        if trace: trace("apply_sgd", None, var=self.params, grad=self.grads)
+        if trace: trace("apply_sgd", None, stream=stream, var=self.params, grad=self.grads)
         ops.apply_sgd(self.params, self.grads, self.lr, shadow=self.shadow, stream=stream)
-        if trace: trace("apply_sgd:end", None, var=self.params)
+        if trace: trace("apply_sgd:end", None, stream=stream, var=self.params)
 
-    def step(self, trace=None, stream=None):
+    def step(self, trace=None, stream=None, concurrent=True):
+        """One training step on ``stream``; the filter gradients overlap the rest of the
+        backward pass on a second stream unless ``concurrent`` is false.  ``trace(event, op,
+        stream=s, **tensors)`` is called before and after every op (``event`` ending in
+        ``:end``), with the stream the op runs on (None: the current stream)."""
         self.forward(trace, stream)
-        self.backward(trace, stream)
+        self.backward(trace, stream, side=self.side if concurrent else None)
         self.update(trace, stream)
 
     # ------------------------------------------------------------------ state

@@ -41,6 +41,12 @@ CONV_CASES = [
     ("1x7_c128", 2, 17, 17, 128, 64, 1, 7, 1, 1, (0, 0, 3, 3)),
     ("5x5_valid_c128", 3, 12, 11, 128, 96, 5, 5, 1, 1, (0, 0, 0, 0)),
     ("alexnet_conv3_shape", 4, 13, 13, 192, 384, 3, 3, 1, 1, (1, 1, 1, 1)),
+    # widest filter row the pipelined kernel's tap masks hold (31 columns), and one past it
+    # (33 columns: the non-pipelined kernel)
+    ("1x31_c16", 2, 5, 40, 16, 16, 1, 31, 1, 1, (0, 0, 15, 15)),
+    ("1x33_c16", 2, 5, 40, 16, 16, 1, 33, 1, 1, (0, 0, 16, 16)),
+    # one output pixel per image: a 64-pixel reduction tile spans 64 images
+    ("one_pixel_out_c64", 70, 3, 3, 64, 64, 3, 3, 1, 1, (0, 0, 0, 0)),
 ]
 
 

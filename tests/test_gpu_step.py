@@ -5,8 +5,8 @@
   batch (and, for VGG, reduced image size) so the oracle finishes in seconds;
 * the AlexNet-shaped step at its full size (batch 128, the bench's launch
   configuration) on sampled images and sampled filter-gradient entries;
-* determinism, restore-and-rerun, and a captured HIP graph replayed against
-  eager steps.
+* determinism, restore-and-rerun, the two-stream step against the one-stream
+  step, and a captured HIP graph replayed against eager steps.
 """
 import numpy as np
 import pytest
@@ -123,6 +123,25 @@ def test_step_deterministic_and_restorable(make):
     torch.cuda.synchronize()
     assert bool(torch.isfinite(rep.params).all())
     assert bitwise_equal(p1, rep.params) and bitwise_equal(g1, rep.grads)
+
+
+@pytest.mark.parametrize("make", [lambda: W.alexnet(batch=8), lambda: W.googlenet(batch=4)],
+                         ids=["alexnet_b8", "googlenet_b4"])
+def test_two_stream_step_matches_one_stream(make):
+    """Filter gradients on the second stream (overlapping the input gradients) must give
+    bit-identical gradients and variables to the same step with every op on one stream,
+    over several steps in a row."""
+    net = make()
+    net.lr = 1e-6
+    inp = W.make_inputs(net, seed=3)
+    one, two = Replica(net, inp), Replica(net, inp)
+    for r in range(3):
+        one.step(concurrent=False)
+        two.step(concurrent=True)
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(two.params).all()), r
+        assert bitwise_equal(one.grads, two.grads), r
+        assert bitwise_equal(one.params, two.params), r
 
 
 def test_graph_capture_replays_match_eager():
