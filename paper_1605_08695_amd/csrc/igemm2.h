@@ -270,10 +270,10 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
             const int mm = ok ? m : 0;
             int y0, x0, hlo, hhi, wlo, whi;
             if constexpr (DIR == DIR_FWD) {
-                const int ow = mm % a.OW;
-                const int t = mm / a.OW;
-                const int oh = t % a.OH;
-                const int n = t / a.OH;
+                uint32_t t, owu, n, ohu;
+                a.dOW.divmod((uint32_t)mm, t, owu);
+                a.dOH.divmod(t, n, ohu);
+                const int ow = (int)owu, oh = (int)ohu;
                 y0 = oh * a.sh - a.pt;     // tap kh reads row y0 + kh
                 x0 = ow * a.sw - a.pl;
                 jvo[r] = (uint32_t)(((((int64_t)n * a.H + y0) * a.W + x0) * a.xs) * 2);

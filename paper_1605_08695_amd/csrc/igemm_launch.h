@@ -44,12 +44,13 @@ struct Igemm2Tile {
 };
 
 // Chosen from sweeps over the AlexNet/VGG layer shapes on MI355X.  Two 4-wave blocks
-// share each CU (two LDS stages each); 128-channel tiles only pay when the channel count
-// is a multiple of 128 and there are still enough of them to fill both block slots of
-// every CU (about 460 blocks), otherwise 64-channel tiles.
+// share each CU (two LDS stages each; the 64-channel kernel fits three).  128-channel tiles
+// pay when the channel count is a multiple of 128 and they give at least one block per CU
+// (AlexNet conv4/conv5 forward: 57 -> 54 and 38 -> 36 us against 64-channel tiles),
+// otherwise 64-channel tiles.
 static inline Igemm2Tile igemm2_tiles(int ni, int mj, int zdim) {
     const int64_t blocks128 = (int64_t)(ni / 128) * ((mj + 127) / 128) * zdim;
-    if (ni % 128 == 0 && blocks128 >= 460) return {128, 128, 4, 2};
+    if (ni % 128 == 0 && blocks128 >= 256) return {128, 128, 4, 2};
     return {64, 128, 4, 2};
 }
 

@@ -169,10 +169,10 @@ class Replica:
                 if trace: trace("maxpool_fwd:end", op, stream=stream, y=y, argmax=self.argmax[op.name])
 
     def backward(self, trace=None, stream=None, side=None):
-        """Gradients of every variable.  With ``side`` (a second stream), each convolution's
-        filter gradient runs there, concurrently with its input gradient and everything after
-        it on ``stream``: the two only read the same tensors, and the side stream joins back
-        before this returns (the dataflow executor runs independent kernels on several GPU
+        """Gradients of every variable.  With ``side`` (a second stream), the filter gradient
+        of each convolution that also has an input gradient runs there, concurrently with that
+        input gradient and everything after it on ``stream``: the two only read the same
+        tensors, and the side stream joins back before this returns (the dataflow executor runs independent kernels on several GPU
         streams, Section 5)."""
         net = self.net
         written = set()
@@ -191,12 +191,15 @@ class Replica:
                     ops.bias_relu_bwd(y, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
                     if trace: trace("bias_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
                 x = self.act[op.src]
-                if side is not None:
+                # a filter gradient with no input gradient beside it (the first layer) stays
+                # on the main stream, where it is next on the critical path
+                on_side = side is not None and src_grad
+                if on_side:
                     side.wait_stream(cur)
-                fs = side if side is not None else stream
+                fs = side if on_side else stream
                 if trace: trace("conv_bwd_filter", op, stream=fs, x=x, dy=dpre)
                 ops.conv2d_bwd_filter(x, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, dw=self.dW[op.name],
-                                      ws=self.ws if side is None else self.ws_side, stream=fs)
+                                      ws=self.ws_side if on_side else self.ws, stream=fs)
                 if trace: trace("conv_bwd_filter:end", op, stream=fs, dw=self.dW[op.name])
                 if src_grad:
                     dx = self.grad[op.src]

@@ -47,6 +47,10 @@ CONV_CASES = [
     ("1x33_c16", 2, 5, 40, 16, 16, 1, 33, 1, 1, (0, 0, 16, 16)),
     # one output pixel per image: a 64-pixel reduction tile spans 64 images
     ("one_pixel_out_c64", 70, 3, 3, 64, 64, 3, 3, 1, 1, (0, 0, 0, 0)),
+    # several 64-channel reduction chunks with tiles spanning image boundaries and uneven
+    # padding; a 5x5 filter over 128 channels
+    ("chunks_c192_uneven_pad", 3, 11, 9, 192, 128, 3, 3, 1, 1, (1, 1, 0, 2)),
+    ("5x5_c128_k192", 2, 14, 14, 128, 192, 5, 5, 1, 1, (2, 2, 2, 2)),
 ]
 
 
