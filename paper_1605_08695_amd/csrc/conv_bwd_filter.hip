@@ -17,7 +17,8 @@ struct BwfPlan {
 // one full round of two blocks per CU (512 blocks): a last round with only a few blocks
 // costs a whole block time, and more splits only add partial-sum traffic (AlexNet conv2-5:
 // 357 us with four-block rounds, 297 us with this rule).  64-channel layers take 64 x 128
-// tiles.
+// tiles.  (192-channel tiles, which pay in the forward pass, need more registers here than
+// two waves per SIMD have and spill.)
 BwfPlan bwf_plan(int dt, const ConvShape &s, bool v2) {
     BwfPlan p;
     const int bk = dt == 0 ? 32 : 64;

@@ -119,11 +119,16 @@ __device__ __forceinline__ U4 lds_tr_pair(const unsigned char *p0, const unsigne
 // (k-rows 8g + 0..3 and 8g + 8..11) are served together: 2 (k & 3) spreads the 4 rows
 // of a group over distinct chunk pairs and bit 3 of k moves the second group to the
 // other half of the banks (for 64-row tiles, whose k-rows are 128 bytes, it moves the
-// group to the free chunk pairs instead).
+// group to the free chunk pairs instead).  192-row k-rows are 384 bytes, so consecutive
+// k-rows start alternately at bank 0 and bank 32: bit 1 of k moves k-rows 2 and 3 of a
+// group by one chunk pair and bit 3 of k the second group by two, which keeps every chunk
+// inside its aligned group of eight.
 template <int R>
 __device__ __forceinline__ int kmajor_swz(int k) {
+    static_assert(R == 64 || R == 128 || R == 192 || R == 256, "k-major tile rows");
     if constexpr (R == 64) return ((k & 3) ^ ((k >> 3) & 1)) << 1;
-    else return ((k & 3) << 1) ^ (((k >> 3) & 1) << 3);
+    else if constexpr (R != 192) return ((k & 3) << 1) ^ (((k >> 3) & 1) << 3);
+    else return (((k >> 1) & 1) << 1) | (((k >> 3) & 1) << 2);
 }
 
 // Byte offset of element (k, row) of a k-major tile with R rows (row a multiple of 4).
@@ -180,8 +185,6 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     const int i0 = ti * BI;
     const int j0 = tj * BJ;
 
-    const bf16_t *__restrict__ srcI = reinterpret_cast<const bf16_t *>(a.src_i);
-    const bf16_t *__restrict__ srcJ = reinterpret_cast<const bf16_t *>(a.src_j);
     // ------------------------------------------------------------ direction set-up
     int MJ_ext, k_beg = 0, k_end;
     int rh = 0, rw = 0, h0 = 0, w0 = 0, Hp = 1, Wp = 1, offh = 0, offw = 0, KHp = 1, KWp = 1;
@@ -224,8 +227,9 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     //
     // [row][k] operands: copy r of this thread covers row 8 slot + lane/8, slot = wave*NL_op + r,
     // and the logical chunk (lane & 7) ^ (lane >> 3); it lands at byte 1024 slot of the tile.
-    // k-major operands with R rows: copy r covers k-row slot (512/R) + lane / (R/8) and row
-    // chunk (lane % (R/8)) ^ kmajor_swz(k-row).  Everything that does not depend on the K tile is
+    // k-major operands with R rows: copy r fills 16-byte positions q = 64 slot + lane of the
+    // tile, position q being chunk q % (R/8) of k-row q / (R/8), which holds the logical row
+    // chunk (q % (R/8)) ^ kmajor_swz(k-row).  Everything that does not depend on the K tile is
     // computed here once.
     constexpr uint32_t kBad = 0x80000000u;
     const i32x4_t rsI = buffer_rsrc(a.src_i, a.bytes_i);
@@ -240,8 +244,9 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
         constexpr int CPR = BI / 8;
 #pragma unroll
         for (int r = 0; r < NLI; ++r) {
-            const int krow = (wave * NLI + r) * (512 / BI) + lane / CPR;
-            const int co = i0 + ((lane % CPR) ^ kmajor_swz<BI>(krow)) * 8;
+            const int pos = (wave * NLI + r) * 64 + lane;
+            const int krow = pos / CPR;
+            const int co = i0 + ((pos % CPR) ^ kmajor_swz<BI>(krow)) * 8;
             ivo[r] = (uint32_t)(k_beg + krow) * ldI2 + 2u * (uint32_t)co;
         }
     } else {
@@ -300,15 +305,17 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
         constexpr int CPR = BJ / 8;
 #pragma unroll
         for (int r = 0; r < NLJ; ++r) {
-            const int krow = (wave * NLJ + r) * (512 / BJ) + lane / CPR;
-            const int c = (lane % CPR) ^ kmajor_swz<BJ>(krow);
+            const int pos = (wave * NLJ + r) * 64 + lane;
+            const int krow = pos / CPR;
+            const int c = (pos % CPR) ^ kmajor_swz<BJ>(krow);
             const int r0 = j0 + c * 8;
             const int rr = r0 < MJ_ext ? r0 : 0;
-            const int ci = rr % a.C;
-            const int t = rr / a.C;
-            fdw[r] = t % a.KW - a.pl;
-            fdh[r] = t / a.KW - a.pt;
-            tvo[r] = (uint32_t)(((((int64_t)fdh[r] * a.W + fdw[r]) * a.xs) + ci) * 2);
+            uint32_t t, ci, kh, kw;
+            a.dC.divmod((uint32_t)rr, t, ci);
+            a.dKW.divmod(t, kh, kw);
+            fdw[r] = (int)kw - a.pl;
+            fdh[r] = (int)kh - a.pt;
+            tvo[r] = (uint32_t)(((((int64_t)fdh[r] * a.W + fdw[r]) * a.xs) + (int64_t)ci) * 2);
             uint32_t q, ow, n, oh;
             a.dOW.divmod((uint32_t)(k_beg + krow), q, ow);
             a.dOH.divmod(q, n, oh);

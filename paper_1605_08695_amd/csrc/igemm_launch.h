@@ -46,11 +46,13 @@ struct Igemm2Tile {
 // Chosen from sweeps over the AlexNet/VGG layer shapes on MI355X.  Two 4-wave blocks
 // share each CU (two LDS stages each; the 64-channel kernel fits three).  128-channel tiles
 // pay when the channel count is a multiple of 128 and they give at least one block per CU
-// (AlexNet conv4/conv5 forward: 57 -> 54 and 38 -> 36 us against 64-channel tiles),
+// (AlexNet conv4/conv5 forward: 57 -> 54 and 38 -> 36 us against 64-channel tiles), and
+// 192-channel tiles likewise for multiples of 192 (AlexNet conv2 forward: 76 -> 64 us),
 // otherwise 64-channel tiles.
 static inline Igemm2Tile igemm2_tiles(int ni, int mj, int zdim) {
-    const int64_t blocks128 = (int64_t)(ni / 128) * ((mj + 127) / 128) * zdim;
-    if (ni % 128 == 0 && blocks128 >= 256) return {128, 128, 4, 2};
+    const int64_t blocks_j = (int64_t)((mj + 127) / 128) * zdim;
+    if (ni % 128 == 0 && (ni / 128) * blocks_j >= 256) return {128, 128, 4, 2};
+    if (ni % 192 == 0 && (ni / 192) * blocks_j >= 256) return {192, 128, 4, 2};
     return {64, 128, 4, 2};
 }
 
@@ -66,6 +68,11 @@ static bool igemm2_launch(IgArgs &a, int mj, int zdim, const Igemm2Tile &t, hipS
     const int tiles_j = (mj + t.bj - 1) / t.bj;
     const dim3 grid((unsigned)(a.tiles_i * tiles_j), 1, (unsigned)zdim);
     const int key = ((t.bi / 64) << 12) | ((t.bj / 64) << 8) | (t.nw << 4) | t.ns;
+    if (t.bi == 192 && t.bj == 128 && t.nw == 4 && t.ns == 2) {
+        // (the filter-gradient direction does not fit these tiles in its registers)
+        if constexpr (DIR == DIR_BWD_FILTER) return false;
+        else { igemm2_go<DIR, 192, 128, 4, 2>(a, grid, st); return true; }
+    }
     switch (key) {
     case (1 << 12) | (2 << 8) | (8 << 4) | 3: igemm2_go<DIR, 64, 128, 8, 3>(a, grid, st); return true;
     case (1 << 12) | (4 << 8) | (8 << 4) | 3: igemm2_go<DIR, 64, 256, 8, 3>(a, grid, st); return true;

@@ -51,6 +51,11 @@ CONV_CASES = [
     # padding; a 5x5 filter over 128 channels
     ("chunks_c192_uneven_pad", 3, 11, 9, 192, 128, 3, 3, 1, 1, (1, 1, 0, 2)),
     ("5x5_c128_k192", 2, 14, 14, 128, 192, 5, 5, 1, 1, (2, 2, 2, 2)),
+    # enough output pixels (256 tiles of 128) for the 192-channel tiles of the forward pass
+    # and the filter gradient
+    ("k192_tiles", 32, 32, 32, 64, 192, 3, 3, 1, 1, (1, 1, 1, 1)),
+    # ... and of the input gradient (192 input channels)
+    ("c192_bwd_tiles", 32, 32, 32, 192, 64, 3, 3, 1, 1, (1, 1, 1, 1)),
 ]
 
 
