@@ -57,8 +57,9 @@ def parse():
     return ap.parse_args()
 
 
-def elementwise_bytes(net, op_kind, op, D):
-    """Algorithmic HBM bytes of one elementwise op (read + write of its operands)."""
+def elementwise_bytes(net, op_kind, op, D, A=4):
+    """Algorithmic HBM bytes of one elementwise op (read + write of its operands); A: bytes per
+    stored pool selection (4 for dense indices, 1 for window taps)."""
     t = net.tensors
     if op_kind == "bias_relu_fwd":
         n = int(np.prod(t[op.dst][:3])) * op.cout
@@ -69,15 +70,15 @@ def elementwise_bytes(net, op_kind, op, D):
     if op_kind == "maxpool_fwd":
         nx = int(np.prod(t[op.src]))
         ny = int(np.prod(t[op.dst][:3])) * t[op.src][3]
-        return nx * D + ny * (D + 4)
+        return nx * D + ny * (D + A)
     if op_kind == "maxpool_bwd":
         nx = int(np.prod(t[op.src]))
         ny = int(np.prod(t[op.dst][:3])) * t[op.src][3]
-        return ny * (D + 4) + nx * D
+        return ny * (D + A) + nx * D
     if op_kind == "maxpool_relu_bwd":         # + read the ReLU output y, write dpre
         nx = int(np.prod(t[op.src]))
         ny = int(np.prod(t[op.dst][:3])) * t[op.src][3]
-        return ny * (D + 4) + 2 * nx * D
+        return ny * (D + A) + 2 * nx * D
     raise KeyError(op_kind)
 
 
@@ -280,8 +281,9 @@ def main():
                 kinds.append("maxpool_relu_bwd")
             elif op.src != "x":
                 kinds.append("maxpool_bwd")
+        A = rep.argmax[op.name].element_size() if op.name in rep.argmax else 4
         for k in kinds:
-            ew_bytes[k] += elementwise_bytes(net, k, op, D)
+            ew_bytes[k] += elementwise_bytes(net, k, op, D, A)
     sgd_bytes = rep.n_params * 14.0
     ew_ms = sum(per_kind.get(k, 0.0) for k in ew_kinds) + per_kind.get("apply_sgd", 0.0)
     ew_gbs = (sum(ew_bytes.values()) + sgd_bytes) / (ew_ms * 1e-3) / 1e9

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 3
+#define TFK_ABI_VERSION 4
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -202,6 +202,16 @@ TFK_API tfk_status tfk_maxpool_fwd(const void *x, tfk_nhwc xd, tfk_window p, tfk
                            void *y, tfk_nhwc yd, int32_t *argmax, void *stream);
 
 /*
+ * The same with the selection stored compactly: taps is dense uint8
+ * [yd.n][yd.h][yd.w][yd.c] holding the selected window tap kh * p.kw + kw (the
+ * element ((n*H + oh*sh - pt + kh)*W + ow*sw - pl + kw)*C + c of x), a quarter
+ * of the int32 argmax's bytes.  Requires p.kh * p.kw <= 256.  The _taps backward
+ * entry points below take it in place of the argmax.
+ */
+TFK_API tfk_status tfk_maxpool_fwd_taps(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype dt,
+                                void *y, tfk_nhwc yd, uint8_t *taps, void *stream);
+
+/*
  * MaxPool backward: dx[i] = beta*dx[i] + sum over outputs o with argmax[o] == i of dy[o]
  * (overlapping windows may route several outputs to one input; all are summed).
  *   dy, argmax : yd-shaped (argmax dense), from tfk_maxpool_fwd.
@@ -209,6 +219,9 @@ TFK_API tfk_status tfk_maxpool_fwd(const void *x, tfk_nhwc xd, tfk_window p, tfk
  */
 TFK_API tfk_status tfk_maxpool_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p,
                            tfk_dtype dt, void *dx, tfk_nhwc xd, float beta, void *stream);
+/* tfk_maxpool_bwd with the selection from tfk_maxpool_fwd_taps. */
+TFK_API tfk_status tfk_maxpool_bwd_taps(const void *dy, const uint8_t *taps, tfk_nhwc yd, tfk_window p,
+                                tfk_dtype dt, void *dx, tfk_nhwc xd, float beta, void *stream);
 
 /*
  * MaxPool backward, ReLU backward and the bias gradient fused into one pass (the
@@ -230,6 +243,10 @@ TFK_API tfk_status tfk_maxpool_bwd(const void *dy, const int32_t *argmax, tfk_nh
 TFK_API tfk_status tfk_maxpool_bwd_relu_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p,
                                     tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd, float beta,
                                     float *dbias, void *ws, size_t ws_bytes, void *stream);
+/* tfk_maxpool_bwd_relu_bwd with the selection from tfk_maxpool_fwd_taps. */
+TFK_API tfk_status tfk_maxpool_bwd_relu_bwd_taps(const void *dy, const uint8_t *taps, tfk_nhwc yd, tfk_window p,
+                                         tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd, float beta,
+                                         float *dbias, void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------- update
  * ApplyGradientDescent, in place (Section 4.1: W' = W - alpha * dL/dW written

@@ -17,7 +17,8 @@ TFK_BF16 = 1
 # every symbol include/tfk.h declares
 EXPORTS = ["tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_maxpool_bwd_relu_bwd", "tfk_conv2d_bwd_input", "tfk_conv2d_bwd_filter", "tfk_conv2d_workspace_bytes",
            "tfk_bias_relu_fwd", "tfk_bias_relu_bwd", "tfk_bias_relu_bwd_workspace_bytes",
-           "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_apply_sgd", "tfk_apply_sgd_multi",
+           "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps",
+           "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd", "tfk_apply_sgd_multi",
            "tfk_status_string", "tfk_last_error", "tfk_abi_version"]
 
 
@@ -64,11 +65,15 @@ def load(path: str = LIB_PATH):
     lib.tfk_maxpool_fwd.argtypes = [vp, Nhwc, Window, st, vp, Nhwc, vp, vp]
     lib.tfk_maxpool_bwd.argtypes = [vp, vp, Nhwc, Window, st, vp, Nhwc, f32, vp]
     lib.tfk_maxpool_bwd_relu_bwd.argtypes = [vp, vp, Nhwc, Window, st, vp, vp, Nhwc, f32, vp, vp, sz, vp]
+    lib.tfk_maxpool_fwd_taps.argtypes = lib.tfk_maxpool_fwd.argtypes
+    lib.tfk_maxpool_bwd_taps.argtypes = lib.tfk_maxpool_bwd.argtypes
+    lib.tfk_maxpool_bwd_relu_bwd_taps.argtypes = lib.tfk_maxpool_bwd_relu_bwd.argtypes
     lib.tfk_apply_sgd.argtypes = [vp, vp, i64, f32, vp, vp]
     lib.tfk_apply_sgd_multi.argtypes = [i32, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(i64), f32,
                                         ctypes.POINTER(vp), vp]
     for name in ("tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_conv2d_bwd_input", "tfk_conv2d_bwd_filter", "tfk_bias_relu_fwd",
-                 "tfk_bias_relu_bwd", "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_bwd_relu_bwd", "tfk_apply_sgd",
+                 "tfk_bias_relu_bwd", "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_bwd_relu_bwd",
+                 "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps", "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd",
                  "tfk_apply_sgd_multi"):
         getattr(lib, name).restype = st
     lib.tfk_status_string.argtypes = [st]

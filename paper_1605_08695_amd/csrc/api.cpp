@@ -352,10 +352,13 @@ static tfk_status check_pool(tfk_nhwc &xd, const tfk_window &p, tfk_dtype dt, tf
     return TFK_OK;
 }
 
-tfk_status tfk_maxpool_fwd(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
-                           int32_t *argmax, void *stream) {
+// The three max-pool entry points take the argmax as int32 dense indices or (taps) as uint8
+// window taps; ab is its byte size.
+static tfk_status maxpool_fwd_impl(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
+                                   void *argmax, bool taps, void *stream) {
     PoolGeom g;
     TRY(check_pool(xd, p, dt, yd, "x", "y", g));
+    if (taps && (int64_t)p.kh * p.kw > 256) return fail(TFK_ERR_SHAPE, "tap argmax needs kh * kw <= 256");
     if (xd.n == 0) return ok();
     const int64_t es = esize(dt);
     TRY(need_ptr(x, "x"));
@@ -363,20 +366,31 @@ tfk_status tfk_maxpool_fwd(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype d
     TRY(need_ptr(argmax, "argmax"));
     TRY(need_align(x, es, "x"));
     TRY(need_align(y, es, "y"));
-    TRY(need_align(argmax, 4, "argmax"));
+    TRY(need_align(argmax, taps ? 1 : 4, "argmax"));
     const int64_t xb = view_bytes(xd, es), yb = view_bytes(yd, es);
-    const int64_t ab = (int64_t)yd.n * yd.h * yd.w * yd.c * 4;
+    const int64_t ab = (int64_t)yd.n * yd.h * yd.w * yd.c * (taps ? 1 : 4);
     if (overlap(y, yb, x, xb) || overlap(argmax, ab, x, xb) || overlap(argmax, ab, y, yb))
         return fail(TFK_ERR_ALIAS, "y / argmax overlap");
-    return hip_status(launch_maxpool_fwd(dt == TFK_F32 ? 0 : 1, x, g, y, argmax, (hipStream_t)stream),
+    return hip_status(launch_maxpool_fwd(dt == TFK_F32 ? 0 : 1, x, g, y, argmax, taps, (hipStream_t)stream),
                       "maxpool_fwd");
 }
 
-tfk_status tfk_maxpool_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
-                           void *dx, tfk_nhwc xd, float beta, void *stream) {
+tfk_status tfk_maxpool_fwd(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
+                           int32_t *argmax, void *stream) {
+    return maxpool_fwd_impl(x, xd, p, dt, y, yd, argmax, false, stream);
+}
+
+tfk_status tfk_maxpool_fwd_taps(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
+                                uint8_t *taps, void *stream) {
+    return maxpool_fwd_impl(x, xd, p, dt, y, yd, taps, true, stream);
+}
+
+static tfk_status maxpool_bwd_impl(const void *dy, const void *argmax, bool taps, tfk_nhwc yd, tfk_window p,
+                                   tfk_dtype dt, void *dx, tfk_nhwc xd, float beta, void *stream) {
     PoolGeom g;
     TRY(check_pool(xd, p, dt, yd, "dx", "dy", g));
     if (!(beta == 0.f || beta == 1.f)) return fail(TFK_ERR_ARG, "beta must be 0 or 1");
+    if (taps && (int64_t)p.kh * p.kw > 256) return fail(TFK_ERR_SHAPE, "tap argmax needs kh * kw <= 256");
     if (xd.n == 0) return ok();
     const int64_t es = esize(dt);
     TRY(need_ptr(dy, "dy"));
@@ -384,21 +398,32 @@ tfk_status tfk_maxpool_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, t
     TRY(need_ptr(dx, "dx"));
     TRY(need_align(dy, es, "dy"));
     TRY(need_align(dx, es, "dx"));
-    TRY(need_align(argmax, 4, "argmax"));
+    TRY(need_align(argmax, taps ? 1 : 4, "argmax"));
     const int64_t xb = view_bytes(xd, es), yb = view_bytes(yd, es);
-    const int64_t ab = (int64_t)yd.n * yd.h * yd.w * yd.c * 4;
+    const int64_t ab = (int64_t)yd.n * yd.h * yd.w * yd.c * (taps ? 1 : 4);
     if (overlap(dx, xb, dy, yb) || overlap(dx, xb, argmax, ab)) return fail(TFK_ERR_ALIAS, "dx overlaps dy or argmax");
-    return hip_status(launch_maxpool_bwd(dt == TFK_F32 ? 0 : 1, dy, argmax, g, beta, dx, (hipStream_t)stream),
+    return hip_status(launch_maxpool_bwd(dt == TFK_F32 ? 0 : 1, dy, argmax, taps, g, beta, dx, (hipStream_t)stream),
                       "maxpool_bwd");
 }
 
-tfk_status tfk_maxpool_bwd_relu_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
-                                    const void *y, void *dpre, tfk_nhwc xd, float beta, float *dbias, void *ws,
-                                    size_t ws_bytes, void *stream) {
+tfk_status tfk_maxpool_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
+                           void *dx, tfk_nhwc xd, float beta, void *stream) {
+    return maxpool_bwd_impl(dy, argmax, false, yd, p, dt, dx, xd, beta, stream);
+}
+
+tfk_status tfk_maxpool_bwd_taps(const void *dy, const uint8_t *taps, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
+                                void *dx, tfk_nhwc xd, float beta, void *stream) {
+    return maxpool_bwd_impl(dy, taps, true, yd, p, dt, dx, xd, beta, stream);
+}
+
+static tfk_status maxpool_relu_bwd_impl(const void *dy, const void *argmax, bool taps, tfk_nhwc yd, tfk_window p,
+                                        tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd, float beta,
+                                        float *dbias, void *ws, size_t ws_bytes, void *stream) {
     PoolGeom g;
     TRY(check_pool(xd, p, dt, yd, "y", "dy", g));
     if (!(beta == 0.f || beta == 1.f)) return fail(TFK_ERR_ARG, "beta must be 0 or 1");
     if (xd.c > 16384) return fail(TFK_ERR_SHAPE, "maxpool_bwd_relu_bwd supports at most 16384 channels");
+    if (taps && (int64_t)p.kh * p.kw > 256) return fail(TFK_ERR_SHAPE, "tap argmax needs kh * kw <= 256");
     TRY(need_ptr(dbias, "dbias"));
     TRY(need_align(dbias, 4, "dbias"));
     hipStream_t st = (hipStream_t)stream;
@@ -411,9 +436,9 @@ tfk_status tfk_maxpool_bwd_relu_bwd(const void *dy, const int32_t *argmax, tfk_n
     TRY(need_align(dy, es, "dy"));
     TRY(need_align(y, es, "y"));
     TRY(need_align(dpre, es, "dpre"));
-    TRY(need_align(argmax, 4, "argmax"));
+    TRY(need_align(argmax, taps ? 1 : 4, "argmax"));
     const int64_t xb = view_bytes(xd, es), yb = view_bytes(yd, es);
-    const int64_t ab = (int64_t)yd.n * yd.h * yd.w * yd.c * 4, bb = (int64_t)xd.c * 4;
+    const int64_t ab = (int64_t)yd.n * yd.h * yd.w * yd.c * (taps ? 1 : 4), bb = (int64_t)xd.c * 4;
     if (overlap(dpre, xb, y, xb) || overlap(dpre, xb, dy, yb) || overlap(dpre, xb, argmax, ab))
         return fail(TFK_ERR_ALIAS, "dpre overlaps y, dy or argmax");
     if (overlap(dbias, bb, y, xb) || overlap(dbias, bb, dy, yb) || overlap(dbias, bb, dpre, xb) ||
@@ -425,9 +450,21 @@ tfk_status tfk_maxpool_bwd_relu_bwd(const void *dy, const int32_t *argmax, tfk_n
         overlap(ws, (int64_t)need, dpre, xb) || overlap(ws, (int64_t)need, dbias, bb) ||
         overlap(ws, (int64_t)need, argmax, ab))
         return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
-    return hip_status(launch_maxpool_relu_bwd(dt == TFK_F32 ? 0 : 1, dy, argmax, g, y, dpre, beta, dbias, (float *)ws,
-                                              st),
+    return hip_status(launch_maxpool_relu_bwd(dt == TFK_F32 ? 0 : 1, dy, argmax, taps, g, y, dpre, beta, dbias,
+                                              (float *)ws, st),
                       "maxpool_bwd_relu_bwd");
+}
+
+tfk_status tfk_maxpool_bwd_relu_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
+                                    const void *y, void *dpre, tfk_nhwc xd, float beta, float *dbias, void *ws,
+                                    size_t ws_bytes, void *stream) {
+    return maxpool_relu_bwd_impl(dy, argmax, false, yd, p, dt, y, dpre, xd, beta, dbias, ws, ws_bytes, stream);
+}
+
+tfk_status tfk_maxpool_bwd_relu_bwd_taps(const void *dy, const uint8_t *taps, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
+                                         const void *y, void *dpre, tfk_nhwc xd, float beta, float *dbias, void *ws,
+                                         size_t ws_bytes, void *stream) {
+    return maxpool_relu_bwd_impl(dy, taps, true, yd, p, dt, y, dpre, xd, beta, dbias, ws, ws_bytes, stream);
 }
 
 // ------------------------------------------------------------------ SGD

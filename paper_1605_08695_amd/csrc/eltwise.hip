@@ -216,10 +216,67 @@ __device__ __forceinline__ void decode(const Decode &d, int64_t t, int &cv, int6
     }
 }
 
+// ------------------------------------------------------------------ argmax formats
+// A max-pool records, per output element, which input element its window selected: as the
+// dense NHWC index of that element (int32_t) or as the window tap kh * KW + kw (uint8_t, a
+// quarter of the bytes).  arg_enc gives the stored value of tap `tap` whose element has dense
+// index `dense`; arg_store / arg_load move the N values of one channel chunk.
+template <typename A> __device__ __forceinline__ int32_t arg_enc(int32_t dense, int tap);
+template <> __device__ __forceinline__ int32_t arg_enc<int32_t>(int32_t dense, int) { return dense; }
+template <> __device__ __forceinline__ int32_t arg_enc<uint8_t>(int32_t, int tap) { return tap; }
+
+template <typename A, int N>
+__device__ __forceinline__ void arg_store(A *p, const int32_t *v) {
+    if constexpr (sizeof(A) == 4 && N % 4 == 0) {
+#pragma unroll
+        for (int e = 0; e < N; e += 4) {
+            int4 q;
+            q.x = v[e]; q.y = v[e + 1]; q.z = v[e + 2]; q.w = v[e + 3];
+            *reinterpret_cast<int4 *>(p + e) = q;
+        }
+    } else if constexpr (sizeof(A) == 1 && N == 8) {
+        uint2 q;
+        q.x = (uint32_t)v[0] | ((uint32_t)v[1] << 8) | ((uint32_t)v[2] << 16) | ((uint32_t)v[3] << 24);
+        q.y = (uint32_t)v[4] | ((uint32_t)v[5] << 8) | ((uint32_t)v[6] << 16) | ((uint32_t)v[7] << 24);
+        *reinterpret_cast<uint2 *>(p) = q;
+    } else if constexpr (sizeof(A) == 1 && N == 4) {
+        *reinterpret_cast<uint32_t *>(p) =
+            (uint32_t)v[0] | ((uint32_t)v[1] << 8) | ((uint32_t)v[2] << 16) | ((uint32_t)v[3] << 24);
+    } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e) p[e] = (A)v[e];
+    }
+}
+
+template <typename A, int N>
+__device__ __forceinline__ void arg_load(const A *p, int32_t *v) {
+    if constexpr (sizeof(A) == 4 && N % 4 == 0) {
+#pragma unroll
+        for (int e = 0; e < N; e += 4) {
+            const int4 q = *reinterpret_cast<const int4 *>(p + e);
+            v[e] = q.x; v[e + 1] = q.y; v[e + 2] = q.z; v[e + 3] = q.w;
+        }
+    } else if constexpr (sizeof(A) == 1 && N == 8) {
+        const uint2 q = *reinterpret_cast<const uint2 *>(p);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[e] = (int32_t)((q.x >> (8 * e)) & 0xffu);
+            v[e + 4] = (int32_t)((q.y >> (8 * e)) & 0xffu);
+        }
+    } else if constexpr (sizeof(A) == 1 && N == 4) {
+        const uint32_t q = *reinterpret_cast<const uint32_t *>(p);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = (int32_t)((q >> (8 * e)) & 0xffu);
+    } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e) v[e] = (int32_t)p[e];
+    }
+}
+
 // ------------------------------------------------------------------ max-pool forward
-template <typename T, bool VEC>
+template <typename T, bool VEC, typename A>
 __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T *__restrict__ x, PoolGeom g,
-                                                          T *__restrict__ y, int32_t *__restrict__ argmax, Decode dec) {
+                                                          T *__restrict__ y, A *__restrict__ argmax, Decode dec) {
     constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
     const int CV = g.C / EPC;
     const int64_t total = (int64_t)g.N * g.OH * g.OW * CV;
@@ -239,6 +296,7 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T *__restrict__ 
                 if ((unsigned)iw >= (unsigned)g.W) continue;
                 const int64_t pidx = ((int64_t)n * g.H + ih) * g.W + iw;
                 const int32_t dense = (int32_t)(pidx * g.C + cv * EPC);
+                const int tap = kh * g.KW + kw;
                 float v[EPC];
                 if constexpr (VEC) {
                     chunk_to_f32<T>(*reinterpret_cast<const U4 *>(x + pidx * g.xs + cv * EPC), v);
@@ -249,7 +307,7 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T *__restrict__ 
                 for (int e = 0; e < EPC; ++e) {
                     if (!have || v[e] > best[e]) {
                         best[e] = v[e];
-                        bi[e] = dense + e;
+                        bi[e] = arg_enc<A>(dense + e, tap);
                     }
                 }
                 have = true;
@@ -258,16 +316,10 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T *__restrict__ 
         const int64_t opix = ((int64_t)n * g.OH + oh) * g.OW + ow;
         if constexpr (VEC) {
             *reinterpret_cast<U4 *>(y + opix * g.ys + cv * EPC) = f32_to_chunk<T>(best);
-            int32_t *am = argmax + opix * g.C + cv * EPC;
-#pragma unroll
-            for (int e = 0; e < EPC; e += 4) {
-                int4 q;
-                q.x = bi[e]; q.y = bi[e + 1]; q.z = bi[e + 2]; q.w = bi[e + 3];
-                *reinterpret_cast<int4 *>(am + e) = q;
-            }
+            arg_store<A, EPC>(argmax + opix * g.C + cv * EPC, bi);
         } else {
             Elem<T>::store(y + opix * g.ys + cv, best[0]);
-            argmax[opix * g.C + cv] = bi[0];
+            argmax[opix * g.C + cv] = (A)bi[0];
         }
     }
 }
@@ -275,9 +327,9 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T *__restrict__ 
 // Fixed small windows (3x3, 2x2) on the 16-byte path: the window loop is unrolled and all of a
 // thread's loads are issued before the first comparison, so their latencies overlap (the
 // run-time loop above waits for each tap in turn).  Same scan order and tie rule.
-template <typename T, int KH, int KW>
+template <typename T, int KH, int KW, typename A>
 __global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restrict__ x, PoolGeom g,
-                                                              T *__restrict__ y, int32_t *__restrict__ argmax,
+                                                              T *__restrict__ y, A *__restrict__ argmax,
                                                               Decode dec) {
     constexpr int EPC = Elem<T>::kPerChunk;
     const int CV = g.C / EPC;
@@ -314,20 +366,14 @@ __global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restric
             for (int e = 0; e < EPC; ++e) {
                 if (!have || f[e] > best[e]) {
                     best[e] = f[e];
-                    bi[e] = dense + e;
+                    bi[e] = arg_enc<A>(dense + e, q);
                 }
             }
             have = true;
         }
         const int64_t opix = ((int64_t)n * g.OH + oh) * g.OW + ow;
         *reinterpret_cast<U4 *>(y + opix * g.ys + cv * EPC) = f32_to_chunk<T>(best);
-        int32_t *am = argmax + opix * g.C + cv * EPC;
-#pragma unroll
-        for (int e = 0; e < EPC; e += 4) {
-            int4 q4;
-            q4.x = bi[e]; q4.y = bi[e + 1]; q4.z = bi[e + 2]; q4.w = bi[e + 3];
-            *reinterpret_cast<int4 *>(am + e) = q4;
-        }
+        arg_store<A, EPC>(argmax + opix * g.C + cv * EPC, bi);
     }
 }
 
@@ -336,12 +382,19 @@ __global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restric
 // ascending output order and adds the gradients routed to it.
 // s[e] (e < EPC) = sum of dy over the windows whose argmax is input element
 // pix * C + cv * EPC + e, pixel pix = (n, h, w) of the pool input.
-template <typename T, bool VEC>
-__device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const int32_t *__restrict__ argmax,
+// (A: argmax format.  Element e of the chunk matches window (oh, ow) when the window's stored
+// value is self + e (dense index) or this pixel's tap in that window (tap index).)
+template <typename T, bool VEC, typename A>
+__device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const A *__restrict__ argmax,
                                             const PoolGeom &g, int n, int h, int w, int64_t pix, int cv,
                                             float *s) {
     constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
+    constexpr bool TAP = sizeof(A) == 1;
     const int32_t self = (int32_t)(pix * g.C + cv * EPC);
+    auto want = [&](int oh, int ow, int e) __attribute__((always_inline)) -> int32_t {
+        if constexpr (TAP) return (h + g.pt - oh * g.sh) * g.KW + (w + g.pl - ow * g.sw);
+        else return self + e;
+    };
     if constexpr (VEC) {
         if (g.KH <= 2 * g.sh && g.KW <= 2 * g.sw) {
             // At most 2 x 2 windows contain the element: issue every argmax and dy load of
@@ -362,12 +415,7 @@ __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const int3
                 const int oh = oh_lo + (q >> 1), ow = ow_lo + (q & 1);
                 valid[q] = oh <= oh_hi && ow <= ow_hi;
                 const int64_t opix = ((int64_t)n * g.OH + (valid[q] ? oh : ohc)) * g.OW + (valid[q] ? ow : owc);
-                const int32_t *am = argmax + opix * g.C + cv * EPC;
-#pragma unroll
-                for (int e = 0; e < EPC; e += 4) {
-                    const int4 v = *reinterpret_cast<const int4 *>(am + e);
-                    ai[q][e] = v.x; ai[q][e + 1] = v.y; ai[q][e + 2] = v.z; ai[q][e + 3] = v.w;
-                }
+                arg_load<A, EPC>(argmax + opix * g.C + cv * EPC, ai[q]);
                 dv[q] = *reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC);
             }
 #pragma unroll
@@ -376,9 +424,10 @@ __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const int3
             for (int q = 0; q < 4; ++q) {             // windows in ascending output order
                 float v[EPC];
                 chunk_to_f32<T>(dv[q], v);
+                const int oh = oh_lo + (q >> 1), ow = ow_lo + (q & 1);
 #pragma unroll
                 for (int e = 0; e < EPC; ++e)
-                    if (valid[q] && ai[q][e] == self + e) s[e] += v[e];
+                    if (valid[q] && ai[q][e] == want(oh, ow, e)) s[e] += v[e];
             }
             return;
         }
@@ -395,33 +444,28 @@ __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const int3
         for (int ow = ow_lo; ow <= ow_hi; ++ow) {
             const int64_t opix = ((int64_t)n * g.OH + oh) * g.OW + ow;
             if constexpr (VEC) {
-                const int32_t *am = argmax + opix * g.C + cv * EPC;
                 int32_t ai[EPC];
-#pragma unroll
-                for (int e = 0; e < EPC; e += 4) {
-                    const int4 q = *reinterpret_cast<const int4 *>(am + e);
-                    ai[e] = q.x; ai[e + 1] = q.y; ai[e + 2] = q.z; ai[e + 3] = q.w;
-                }
+                arg_load<A, EPC>(argmax + opix * g.C + cv * EPC, ai);
                 bool any = false;
 #pragma unroll
-                for (int e = 0; e < EPC; ++e) any |= (ai[e] == self + e);
+                for (int e = 0; e < EPC; ++e) any |= (ai[e] == want(oh, ow, e));
                 if (any) {
                     float v[EPC];
                     chunk_to_f32<T>(*reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC), v);
 #pragma unroll
                     for (int e = 0; e < EPC; ++e)
-                        if (ai[e] == self + e) s[e] += v[e];
+                        if (ai[e] == want(oh, ow, e)) s[e] += v[e];
                 }
             } else {
-                if (argmax[opix * g.C + cv] == self) s[0] += Elem<T>::load(dy + opix * g.ys + cv);
+                if ((int32_t)argmax[opix * g.C + cv] == want(oh, ow, 0)) s[0] += Elem<T>::load(dy + opix * g.ys + cv);
             }
         }
     }
 }
 
-template <typename T, bool VEC>
+template <typename T, bool VEC, typename A>
 __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T *__restrict__ dy,
-                                                          const int32_t *__restrict__ argmax, PoolGeom g,
+                                                          const A *__restrict__ argmax, PoolGeom g,
                                                           float beta, T *dx, Decode dec) {
     constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
     const int CV = g.C / EPC;
@@ -432,7 +476,7 @@ __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T *__restrict__ 
         int64_t pix;
         decode(dec, t, cv, pix, w, h, n);
         float s[EPC];
-        pool_gather<T, VEC>(dy, argmax, g, n, h, w, pix, cv, s);
+        pool_gather<T, VEC, A>(dy, argmax, g, n, h, w, pix, cv, s);
         T *out = dx + pix * g.xs + cv * EPC;
         if constexpr (VEC) {
             if (beta != 0.f) {
@@ -456,9 +500,9 @@ __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T *__restrict__ 
 // relu_bwd_partial_kernel: block b owns pixels [b ppb, (b+1) ppb), thread t channel chunk
 // t % CVB (+ CVB ...) and pixel rows t / CVB (+ R ...); db sums the stored (rounded) dpre,
 // the tensor the filter gradient is formed from.
-template <typename T, bool VEC>
+template <typename T, bool VEC, typename A>
 __global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *__restrict__ dy,
-                                                                       const int32_t *__restrict__ argmax,
+                                                                       const A *__restrict__ argmax,
                                                                        PoolGeom g, const T *__restrict__ y, T *dpre,
                                                                        float beta, int64_t ppb, FastDiv dW, FastDiv dH,
                                                                        float *__restrict__ partial) {
@@ -485,7 +529,7 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *
                 dW.divmod((uint32_t)p, q, w);
                 dH.divmod(q, n, h);
                 float s[EPC];
-                pool_gather<T, VEC>(dy, argmax, g, (int)n, (int)h, (int)w, p, cv, s);
+                pool_gather<T, VEC, A>(dy, argmax, g, (int)n, (int)h, (int)w, p, cv, s);
                 const int64_t off = p * g.xs + (int64_t)cv * EPC;
                 if constexpr (VEC) {
                     float fy[EPC];
@@ -530,9 +574,9 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *
 // form reloads them for every pixel) and each window's gradient is routed to the pixel its
 // argmax names, windows in ascending order (the same sums, in the same order, as the gather).
 // Bias-gradient partials as in maxpool_relu_bwd_partial_kernel, over cells instead of pixels.
-template <typename T>
+template <typename T, typename A>
 __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__restrict__ dy,
-                                                                    const int32_t *__restrict__ argmax, PoolGeom g,
+                                                                    const A *__restrict__ argmax, PoolGeom g,
                                                                     const T *__restrict__ y, T *dpre, float beta,
                                                                     int64_t cpb, int CH, int CW, FastDiv dCW,
                                                                     FastDiv dCH, float *__restrict__ partial) {
@@ -567,12 +611,7 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
                     const int oh = (int)ch - 1 + (k >> 1), ow = (int)cw - 1 + (k & 1);
                     wok[k] = (unsigned)oh < (unsigned)g.OH && (unsigned)ow < (unsigned)g.OW;
                     const int64_t opix = ((int64_t)n * g.OH + (wok[k] ? oh : 0)) * g.OW + (wok[k] ? ow : 0);
-                    const int32_t *am = argmax + opix * g.C + cv * EPC;
-#pragma unroll
-                    for (int e = 0; e < EPC; e += 4) {
-                        const int4 v = *reinterpret_cast<const int4 *>(am + e);
-                        ai[k][e] = v.x; ai[k][e + 1] = v.y; ai[k][e + 2] = v.z; ai[k][e + 3] = v.w;
-                    }
+                    arg_load<A, EPC>(argmax + opix * g.C + cv * EPC, ai[k]);
                     dv[k] = *reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC);
                 }
                 // the four pixels of the cell
@@ -598,10 +637,13 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
                     chunk_to_f32<T>(dv[k], v);
 #pragma unroll
                     for (int m = 0; m < 4; ++m) {
-                        const int32_t self = (int32_t)(pix[m] * g.C + cv * EPC);
+                        // pixel m is tap (2 (1 - k/2) + m/2, 2 (1 - k%2) + m%2) of window k
+                        const int th = 2 * (1 - (k >> 1)) + (m >> 1), tw = 2 * (1 - (k & 1)) + (m & 1);
+                        const int32_t self = sizeof(A) == 1 ? (th < g.KH && tw < g.KW ? th * g.KW + tw : -1)
+                                                            : (int32_t)(pix[m] * g.C + cv * EPC);
 #pragma unroll
                         for (int e = 0; e < EPC; ++e)
-                            if (wok[k] && ai[k][e] == self + e) s[m][e] += v[e];
+                            if (wok[k] && ai[k][e] == self + (sizeof(A) == 1 ? 0 : e)) s[m][e] += v[e];
                     }
                 }
 #pragma unroll
@@ -810,8 +852,8 @@ hipError_t launch_bias_relu_bwd(int dt, const void *y, const void *dy, void *dpr
                    : relu_bwd_t<bf16_t>(y, dy, dpre, P, C, ys, db, ws, st);
 }
 
-template <typename T>
-static hipError_t maxpool_relu_bwd_t(const void *dy, const int32_t *am, const PoolGeom &g, const void *y, void *dpre,
+template <typename T, typename A>
+static hipError_t maxpool_relu_bwd_t(const void *dy, const A *am, const PoolGeom &g, const void *y, void *dpre,
                                      float beta, float *db, float *ws, hipStream_t st) {
     constexpr int EPC = Elem<T>::kPerChunk;
     const bool vec = g.C % EPC == 0 && g.xs % EPC == 0 && g.ys % EPC == 0 && aligned16(dy) && aligned16(am) &&
@@ -834,30 +876,33 @@ static hipError_t maxpool_relu_bwd_t(const void *dy, const int32_t *am, const Po
         const int64_t gc = std::max<int64_t>(1, std::min<int64_t>(G, (ncell + 2 * R - 1) / (2 * R)));
         const int Gc = (int)gc;
         const int64_t cpb = (ncell + gc - 1) / gc;
-        hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am, g,
+        hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am, g,
                            (const T *)y, (T *)dpre, beta, cpb, CH, CW, FastDiv((uint32_t)CW), FastDiv((uint32_t)CH),
                            ws);
         hipLaunchKernelGGL(sum_partials_kernel, dim3(g.C), dim3(256), 0, st, ws, Gc, g.C, db);
         return hipGetLastError();
     }
     if (vec)
-        hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, true>), dim3(G), dim3(256), smem, st, (const T *)dy, am,
+        hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, true, A>), dim3(G), dim3(256), smem, st, (const T *)dy, am,
                            g, (const T *)y, (T *)dpre, beta, ppb, dW, dH, ws);
     else
-        hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, false>), dim3(G), dim3(256), smem, st, (const T *)dy,
+        hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, false, A>), dim3(G), dim3(256), smem, st, (const T *)dy,
                            am, g, (const T *)y, (T *)dpre, beta, ppb, dW, dH, ws);
     hipLaunchKernelGGL(sum_partials_kernel, dim3(g.C), dim3(256), 0, st, ws, G, g.C, db);
     return hipGetLastError();
 }
 
-hipError_t launch_maxpool_relu_bwd(int dt, const void *dy, const int32_t *am, const PoolGeom &g, const void *y,
-                                   void *dpre, float beta, float *db, float *ws, hipStream_t st) {
-    return dt == 0 ? maxpool_relu_bwd_t<float>(dy, am, g, y, dpre, beta, db, ws, st)
-                   : maxpool_relu_bwd_t<bf16_t>(dy, am, g, y, dpre, beta, db, ws, st);
+hipError_t launch_maxpool_relu_bwd(int dt, const void *dy, const void *am, bool taps, const PoolGeom &g,
+                                   const void *y, void *dpre, float beta, float *db, float *ws, hipStream_t st) {
+    if (taps)
+        return dt == 0 ? maxpool_relu_bwd_t<float>(dy, (const uint8_t *)am, g, y, dpre, beta, db, ws, st)
+                       : maxpool_relu_bwd_t<bf16_t>(dy, (const uint8_t *)am, g, y, dpre, beta, db, ws, st);
+    return dt == 0 ? maxpool_relu_bwd_t<float>(dy, (const int32_t *)am, g, y, dpre, beta, db, ws, st)
+                   : maxpool_relu_bwd_t<bf16_t>(dy, (const int32_t *)am, g, y, dpre, beta, db, ws, st);
 }
 
-template <typename T>
-static hipError_t maxpool_fwd_t(const void *x, const PoolGeom &g, void *y, int32_t *am, hipStream_t st) {
+template <typename T, typename A>
+static hipError_t maxpool_fwd_t(const void *x, const PoolGeom &g, void *y, A *am, hipStream_t st) {
     constexpr int EPC = Elem<T>::kPerChunk;
     const bool vec = g.C % EPC == 0 && g.xs % EPC == 0 && g.ys % EPC == 0 && aligned16(x) &&
                      aligned16(y) && aligned16(am);
@@ -866,24 +911,29 @@ static hipError_t maxpool_fwd_t(const void *x, const PoolGeom &g, void *y, int32
     const int grid = grid_for(work, 256, 16384);
     const Decode dec = make_decode(cv, g.OW, g.OH, work);
     if (vec && g.KH == 3 && g.KW == 3)
-        hipLaunchKernelGGL((maxpool_fwd_win_kernel<T, 3, 3>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am,
-                           dec);
+        hipLaunchKernelGGL((maxpool_fwd_win_kernel<T, 3, 3, A>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y,
+                           am, dec);
     else if (vec && g.KH == 2 && g.KW == 2)
-        hipLaunchKernelGGL((maxpool_fwd_win_kernel<T, 2, 2>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am,
-                           dec);
+        hipLaunchKernelGGL((maxpool_fwd_win_kernel<T, 2, 2, A>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y,
+                           am, dec);
     else if (vec)
-        hipLaunchKernelGGL((maxpool_fwd_kernel<T, true>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am, dec);
+        hipLaunchKernelGGL((maxpool_fwd_kernel<T, true, A>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am,
+                           dec);
     else
-        hipLaunchKernelGGL((maxpool_fwd_kernel<T, false>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am, dec);
+        hipLaunchKernelGGL((maxpool_fwd_kernel<T, false, A>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am,
+                           dec);
     return hipGetLastError();
 }
 
-hipError_t launch_maxpool_fwd(int dt, const void *x, const PoolGeom &g, void *y, int32_t *am, hipStream_t st) {
-    return dt == 0 ? maxpool_fwd_t<float>(x, g, y, am, st) : maxpool_fwd_t<bf16_t>(x, g, y, am, st);
+hipError_t launch_maxpool_fwd(int dt, const void *x, const PoolGeom &g, void *y, void *am, bool taps, hipStream_t st) {
+    if (taps)
+        return dt == 0 ? maxpool_fwd_t<float>(x, g, y, (uint8_t *)am, st)
+                       : maxpool_fwd_t<bf16_t>(x, g, y, (uint8_t *)am, st);
+    return dt == 0 ? maxpool_fwd_t<float>(x, g, y, (int32_t *)am, st) : maxpool_fwd_t<bf16_t>(x, g, y, (int32_t *)am, st);
 }
 
-template <typename T>
-static hipError_t maxpool_bwd_t(const void *dy, const int32_t *am, const PoolGeom &g, float beta, void *dx,
+template <typename T, typename A>
+static hipError_t maxpool_bwd_t(const void *dy, const A *am, const PoolGeom &g, float beta, void *dx,
                                 hipStream_t st) {
     constexpr int EPC = Elem<T>::kPerChunk;
     const bool vec = g.C % EPC == 0 && g.xs % EPC == 0 && g.ys % EPC == 0 && aligned16(dx) &&
@@ -893,15 +943,21 @@ static hipError_t maxpool_bwd_t(const void *dy, const int32_t *am, const PoolGeo
     const int grid = grid_for(work, 256, 16384);
     const Decode dec = make_decode(cv, g.W, g.H, work);
     if (vec)
-        hipLaunchKernelGGL((maxpool_bwd_kernel<T, true>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g, beta, (T *)dx, dec);
+        hipLaunchKernelGGL((maxpool_bwd_kernel<T, true, A>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g, beta,
+                           (T *)dx, dec);
     else
-        hipLaunchKernelGGL((maxpool_bwd_kernel<T, false>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g, beta, (T *)dx, dec);
+        hipLaunchKernelGGL((maxpool_bwd_kernel<T, false, A>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g, beta,
+                           (T *)dx, dec);
     return hipGetLastError();
 }
 
-hipError_t launch_maxpool_bwd(int dt, const void *dy, const int32_t *am, const PoolGeom &g, float beta, void *dx,
-                              hipStream_t st) {
-    return dt == 0 ? maxpool_bwd_t<float>(dy, am, g, beta, dx, st) : maxpool_bwd_t<bf16_t>(dy, am, g, beta, dx, st);
+hipError_t launch_maxpool_bwd(int dt, const void *dy, const void *am, bool taps, const PoolGeom &g, float beta,
+                              void *dx, hipStream_t st) {
+    if (taps)
+        return dt == 0 ? maxpool_bwd_t<float>(dy, (const uint8_t *)am, g, beta, dx, st)
+                       : maxpool_bwd_t<bf16_t>(dy, (const uint8_t *)am, g, beta, dx, st);
+    return dt == 0 ? maxpool_bwd_t<float>(dy, (const int32_t *)am, g, beta, dx, st)
+                   : maxpool_bwd_t<bf16_t>(dy, (const int32_t *)am, g, beta, dx, st);
 }
 
 hipError_t launch_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh, hipStream_t st) {

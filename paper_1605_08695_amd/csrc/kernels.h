@@ -66,13 +66,14 @@ hipError_t launch_bias_relu_fwd(int dt, void *y, int64_t P, int C, int64_t ys, c
 void relu_bwd_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *ppb);
 hipError_t launch_bias_relu_bwd(int dt, const void *y, const void *dy, void *dpre, int64_t P, int C,
                                 int64_t ys, float *db, float *ws, hipStream_t st);
-hipError_t launch_maxpool_fwd(int dt, const void *x, const PoolGeom &g, void *y, int32_t *am, hipStream_t st);
-hipError_t launch_maxpool_bwd(int dt, const void *dy, const int32_t *am, const PoolGeom &g, float beta, void *dx,
-                              hipStream_t st);
+// am: int32 dense-index argmax, or with taps the uint8 window tap kh * KW + kw.
+hipError_t launch_maxpool_fwd(int dt, const void *x, const PoolGeom &g, void *y, void *am, bool taps, hipStream_t st);
+hipError_t launch_maxpool_bwd(int dt, const void *dy, const void *am, bool taps, const PoolGeom &g, float beta,
+                              void *dx, hipStream_t st);
 // Fused max-pool backward + ReLU backward + bias gradient over the pool input y (pixel stride g.xs);
 // ws holds the bias-gradient partials of relu_bwd_plan.
-hipError_t launch_maxpool_relu_bwd(int dt, const void *dy, const int32_t *am, const PoolGeom &g, const void *y,
-                                   void *dpre, float beta, float *db, float *ws, hipStream_t st);
+hipError_t launch_maxpool_relu_bwd(int dt, const void *dy, const void *am, bool taps, const PoolGeom &g,
+                                   const void *y, void *dpre, float beta, float *db, float *ws, hipStream_t st);
 hipError_t launch_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh, hipStream_t st);
 hipError_t launch_sgd_multi(const SgdBatch &b, float lr, hipStream_t st);
 // Sums split-K partials part[splits][mn] into out; part (workspace) is overwritten.

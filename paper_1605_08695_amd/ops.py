@@ -172,7 +172,9 @@ def bias_relu_bwd(y, dy, dpre=None, dbias=None, ws=None, stream=None) -> Tuple[t
 
 
 # ----------------------------------------------------------------------------- max-pool
-def maxpool_fwd(x, kernel_hw, stride, pads, y=None, argmax=None, stream=None):
+def maxpool_fwd(x, kernel_hw, stride, pads, y=None, argmax=None, stream=None, taps=False):
+    """Returns (y, argmax).  argmax is int32 dense NHWC indices into x, or with ``taps`` uint8
+    window taps kh * KW + kw (a quarter of the bytes); the backward ops accept either."""
     lib = load()
     kh, kw = kernel_hw
     win = window(kh, kw, stride, pads)
@@ -182,17 +184,24 @@ def maxpool_fwd(x, kernel_hw, stride, pads, y=None, argmax=None, stream=None):
     if y is None:
         y = torch.empty((n, oh, ow, c), dtype=x.dtype, device=x.device)
     if argmax is None:
-        argmax = torch.empty((n, oh, ow, c), dtype=torch.int32, device=x.device)
-    check(lib.tfk_maxpool_fwd(_ptr(x), nhwc(x), win, _dt(x), _ptr(y), nhwc(y), _ptr(argmax), _stream(stream)))
+        argmax = torch.empty((n, oh, ow, c), dtype=torch.uint8 if taps else torch.int32, device=x.device)
+    fn = _argmax_fn(lib, "tfk_maxpool_fwd", argmax)
+    check(fn(_ptr(x), nhwc(x), win, _dt(x), _ptr(y), nhwc(y), _ptr(argmax), _stream(stream)))
     return y, argmax
+
+
+def _argmax_fn(lib, name, argmax):
+    """The entry point for this argmax format: int32 dense indices, or uint8 taps (``_taps``)."""
+    if not argmax.is_contiguous() or argmax.dtype not in (torch.int32, torch.uint8):
+        raise ValueError("argmax must be a dense int32 (indices) or uint8 (taps) tensor")
+    return getattr(lib, name + ("_taps" if argmax.dtype == torch.uint8 else ""))
 
 
 def maxpool_bwd(dy, argmax, dx, kernel_hw, stride, pads, beta=0.0, stream=None):
     kh, kw = kernel_hw
-    if not argmax.is_contiguous() or argmax.dtype != torch.int32:
-        raise ValueError("argmax must be a dense int32 tensor")
-    check(load().tfk_maxpool_bwd(_ptr(dy), _ptr(argmax), nhwc(dy), window(kh, kw, stride, pads), _dt(dy),
-                                 _ptr(dx), nhwc(dx), float(beta), _stream(stream)))
+    fn = _argmax_fn(load(), "tfk_maxpool_bwd", argmax)
+    check(fn(_ptr(dy), _ptr(argmax), nhwc(dy), window(kh, kw, stride, pads), _dt(dy), _ptr(dx), nhwc(dx),
+             float(beta), _stream(stream)))
     return dx
 
 
@@ -203,8 +212,7 @@ def maxpool_bwd_relu_bwd(dy, argmax, y, dpre, kernel_hw, stride, pads, beta=0.0,
     """
     lib = load()
     kh, kw = kernel_hw
-    if not argmax.is_contiguous() or argmax.dtype != torch.int32:
-        raise ValueError("argmax must be a dense int32 tensor")
+    fn = _argmax_fn(lib, "tfk_maxpool_bwd_relu_bwd", argmax)
     if dbias is None:
         dbias = torch.empty(y.shape[3], dtype=torch.float32, device=y.device)
     d_y, d_p = nhwc(y), nhwc(dpre)
@@ -213,9 +221,8 @@ def maxpool_bwd_relu_bwd(dy, argmax, y, dpre, kernel_hw, stride, pads, beta=0.0,
     need = lib.tfk_bias_relu_bwd_workspace_bytes(d_y, _dt(y))
     if ws is None or ws.numel() < need:
         ws = _ws(need, y.device)
-    check(lib.tfk_maxpool_bwd_relu_bwd(_ptr(dy), _ptr(argmax), nhwc(dy), window(kh, kw, stride, pads), _dt(dy),
-                                       _ptr(y), _ptr(dpre), d_y, float(beta), _ptr(dbias), _ptr(ws), need,
-                                       _stream(stream)))
+    check(fn(_ptr(dy), _ptr(argmax), nhwc(dy), window(kh, kw, stride, pads), _dt(dy), _ptr(y), _ptr(dpre), d_y,
+             float(beta), _ptr(dbias), _ptr(ws), need, _stream(stream)))
     return dpre, dbias
 
 

@@ -111,8 +111,10 @@ class Replica:
             self.grad[name] = torch.zeros(shape, dtype=dt, device=dev)
         # ReLU-backward of the ops that write the output tensor must not overwrite the seed g
         self.dpre_out = torch.zeros(net.tensors[net.output], dtype=dt, device=dev)
+        # each max-pool's selection as uint8 window taps (windows of at most 256 taps)
         self.argmax = {op.name: torch.zeros(net.tensors[op.dst][:3] + (net.tensors[op.src][3],),
-                                            dtype=torch.int32, device=dev)
+                                            dtype=torch.uint8 if op.kh * op.kw <= 256 else torch.int32,
+                                            device=dev)
                        for op in net.ops if isinstance(op, Pool)}
         # ---- max-pools fused with the ReLU backward of the convolution that feeds them
         writers, readers = {}, {}

@@ -196,10 +196,23 @@ class ParityTracer:
         self.record_tensor("bias_relu_fwd", op.name, y, ref, self.dtype)
         self.record("bias_relu_fwd", op.name, "negatives", float(np.sum(np.signbit(y))), 0.0)
 
+    @staticmethod
+    def _dense(argmax, x_shape, op):
+        """A pool's selection as dense NHWC indices into its input: int32 argmax as stored, uint8
+        window taps kh * KW + kw decoded."""
+        a = argmax.cpu().numpy().astype(np.int64)
+        if argmax.dtype != torch.uint8:
+            return a
+        N, H, W, C = x_shape
+        n, oh, ow, c = np.indices(a.shape)
+        h = oh * op.sh - op.pads[0] + a // op.kw
+        w = ow * op.sw - op.pads[2] + a % op.kw
+        return ((n * H + h) * W + w) * C + c
+
     def _check_maxpool_fwd(self, op, inp, out):
         x = self._x64(inp["x"])
         ref, am = oracle.maxpool_fwd(x, (op.kh, op.kw), (op.sh, op.sw), op.pads)
-        got_am = out["argmax"].cpu().numpy().astype(np.int64)
+        got_am = self._dense(out["argmax"], inp["x"].shape, op)
         if self.sample is not None:
             got_am = got_am[self.sample] - self._index_shift(inp["x"].shape)
         self.record("maxpool_fwd", op.name, "err", err(self._x64(out["y"]), ref), 0.0)
@@ -231,7 +244,7 @@ class ParityTracer:
 
     def _check_maxpool_bwd(self, op, inp, out):
         dy = self._x64(inp["dy"])
-        am = inp["argmax"].cpu().numpy().astype(np.int64)
+        am = self._dense(inp["argmax"], inp["dx"].shape, op)
         dx_old = self._x64(inp["dx"])
         if self.sample is not None:
             am = am[self.sample] - self._index_shift(inp["dx"].shape)
@@ -241,7 +254,7 @@ class ParityTracer:
     def _check_maxpool_relu_bwd(self, op, inp, out):
         # whole tensors: the bias gradient sums over every image
         y = f64(inp["y"])
-        am = inp["argmax"].cpu().numpy()
+        am = self._dense(inp["argmax"], inp["y"].shape, op).astype(np.int32)
         dpre_old = f64(inp["dpre"])
         g = oracle.maxpool_bwd(f64(inp["dy"]), am, y.shape, dx=dpre_old, beta=inp["beta"])
         ref_dpre, ref_db = oracle.bias_relu_bwd(y, g)

@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 3
+    assert lib.tfk_abi_version() == 4
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -142,6 +142,25 @@ def test_maxpool_relu_bwd_validation(lib):
     assert fused(x=Nhwc(2, 9, 9, 8, 0)) == SHAPE                        # 9 -> 4 with a 3x3/2 window, not 3
     assert fused(ws_bytes=0) == WORKSPACE
     assert fused(ws=P + 0x300000) == ALIAS                              # workspace inside dpre
+
+
+def test_maxpool_taps_validation(lib):
+    """The uint8 tap form of the pool's selection: NULL, window size and aliasing checks."""
+    W = Window(3, 3, 2, 2, 0, 0, 0, 0)
+    yd, xd = Nhwc(2, 3, 3, 8, 0), Nhwc(2, 7, 7, 8, 0)
+    fwd = lambda taps, win=W, x=xd, y=yd: lib.tfk_maxpool_fwd_taps(vp(P), x, win, BF16, vp(P + 0x100000), y,
+                                                                   vp(taps), None)
+    assert fwd(0) == NULL
+    assert fwd(P + 0x100010) == ALIAS                                   # taps inside y
+    big = Window(17, 16, 1, 1, 0, 0, 0, 0)                              # 272 taps do not fit a byte
+    assert fwd(P + 0x200000, big, Nhwc(1, 17, 16, 8, 0), Nhwc(1, 1, 1, 8, 0)) == SHAPE
+    assert lib.tfk_maxpool_bwd_taps(vp(P), vp(0), yd, W, BF16, vp(P + 0x200000), xd, ctypes.c_float(0.0),
+                                    None) == NULL
+    assert lib.tfk_maxpool_bwd_taps(vp(P), vp(P + 0x100000), yd, big, BF16, vp(P + 0x200000), xd,
+                                    ctypes.c_float(0.0), None) == SHAPE
+    assert lib.tfk_maxpool_bwd_relu_bwd_taps(vp(P), vp(P + 0x100000), yd, W, BF16, vp(P + 0x200000),
+                                             vp(P + 0x200010), xd, ctypes.c_float(0.0), vp(P + 0x400000),
+                                             vp(P + 0x500000), 1 << 20, None) == ALIAS   # dpre overlaps y
 
 
 def test_sgd_validation(lib):

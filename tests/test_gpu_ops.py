@@ -254,6 +254,16 @@ def test_bias_relu(dtype, shape, slice_):
 
 
 # ----------------------------------------------------------------------------- max-pool
+def _taps_to_dense(taps, x_shape, k, s, pads):
+    """uint8 window taps kh * k + kw -> dense NHWC indices into the pool input."""
+    a = taps.cpu().numpy().astype(np.int64)
+    N, H, W, C = x_shape
+    n, oh, ow, c = np.indices(a.shape)
+    h = oh * s - pads[0] + a // k
+    w = ow * s - pads[2] + a % k
+    return ((n * H + h) * W + w) * C + c
+
+
 POOL_CASES = [
     ("alexnet_pool1", (2, 55, 55, 64), 3, 2, (0, 0, 0, 0)),
     ("same_3s2", (2, 28, 28, 192), 3, 2, (0, 1, 0, 1)),
@@ -277,32 +287,39 @@ def test_maxpool(case, dtype, ties):
         a = np.maximum(np.round(a * 2), 0.0)                 # many exact zeros and repeats
     x = torch.from_numpy(a).to(dtype).to(DEV)
     y, am = ops.maxpool_fwd(x, (k, k), s, pads)
+    y8, taps = ops.maxpool_fwd(x, (k, k), s, pads, taps=True)
     torch.cuda.synchronize()
     ref_y, ref_am = oracle.maxpool_fwd(f64(x), (k, k), s, pads)
-    assert np.array_equal(f64(y), ref_y)
+    assert np.array_equal(f64(y), ref_y) and np.array_equal(f64(y8), ref_y)
     assert np.array_equal(am.cpu().numpy(), ref_am)
+    assert taps.dtype == torch.uint8 and np.array_equal(_taps_to_dense(taps, shape, k, s, pads), ref_am)
     dy = _mk(y.shape, dtype, rng)
     for beta in (0.0, 1.0):
         dx = _mk(shape, dtype, rng)
+        dx8 = dx.clone()
         old = f64(dx)
         ops.maxpool_bwd(dy, am, dx, (k, k), s, pads, beta=beta)
+        ops.maxpool_bwd(dy, taps, dx8, (k, k), s, pads, beta=beta)
         torch.cuda.synchronize()
         ref = oracle.maxpool_bwd(f64(dy), ref_am, shape, dx=old, beta=beta)
         assert_close(f64(dx), ref, dtype, label="maxpool_bwd beta=%g" % beta)
+        assert torch.equal(dx, dx8), "the tap form routes exactly as the index form"
 
 
+@pytest.mark.parametrize("taps", [False, True], ids=["index", "taps"])
 @pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
 @pytest.mark.parametrize("case", POOL_CASES, ids=[c[0] for c in POOL_CASES])
-def test_maxpool_relu_bwd_fused(case, dtype):
-    """Fused max-pool backward + ReLU backward + bias gradient against the oracle's two ops."""
+def test_maxpool_relu_bwd_fused(case, dtype, taps):
+    """Fused max-pool backward + ReLU backward + bias gradient against the oracle's two ops,
+    with the selection stored as dense indices or as uint8 window taps."""
     name, shape, k, s, pads = case
     rng = np.random.default_rng(29)
     # the pool input is a ReLU output: exact zeros (masked, and ties inside windows)
     y = torch.from_numpy(np.maximum(rng.standard_normal(shape), 0.0)).to(dtype).to(DEV)
-    out, am = ops.maxpool_fwd(y, (k, k), s, pads)
+    out, am = ops.maxpool_fwd(y, (k, k), s, pads, taps=taps)
     dy = _mk(out.shape, dtype, rng)
     torch.cuda.synchronize()
-    ref_am = am.cpu().numpy()
+    ref_am = oracle.maxpool_fwd(f64(y), (k, k), s, pads)[1]
     for beta in (0.0, 1.0):
         dpre = _mk(shape, dtype, rng)
         old = f64(dpre)

@@ -53,7 +53,7 @@ def test_single_layer_step_end_to_end():
     say("single layer end-to-end:", {k: "%.2e" % v for k, v in e.items()})
     assert all(v <= 1e-4 for v in e.values()), e
     # argmax: mismatches allowed only where the oracle's window top-2 gap is tiny
-    am = rep.argmax[net.ops[1].name].cpu().numpy()
+    am = ParityTracer._dense(rep.argmax[net.ops[1].name], rep.act[c].shape, net.ops[1])
     ref_am = ref["argmax"][net.ops[1].name]
     mism = np.argwhere(am != ref_am)
     y = ref["acts"][c]
