@@ -250,6 +250,8 @@ def main():
             ms = s.elapsed_time(e)
             if kind == "conv_bias_relu_fwd":
                 kind = "conv_fwd"       # the forward convolution with its bias + ReLU epilogue
+            if kind == "conv_bwd_input_relu_bwd":
+                kind = "conv_bwd_input"  # the input gradient with the producer's ReLU backward epilogue
             per_kind.setdefault(kind, 0.0)
             per_kind[kind] += ms / reps
             key = (kind, op.name if op is not None else "all")

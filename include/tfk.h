@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 4
+#define TFK_ABI_VERSION 5
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -155,10 +155,30 @@ TFK_API tfk_status tfk_conv2d_bwd_filter(const void *x, tfk_nhwc xd, const void 
                                  tfk_window p, tfk_dtype dt, float *dw,
                                  void *ws, size_t ws_bytes, void *stream);
 
+/*
+ * Conv2DBackpropInput fused with the ReLU backward and bias gradient of the layer that
+ * produced x (the hand-fused activation-gradient kernels of Section 5), for an x that is the
+ * output y of BiasAdd + ReLU and feeds only this convolution:
+ *   g        = the input gradient of tfk_conv2d_bwd_input (beta 0)
+ *   dpre[i]  = y[i] > 0 ? g[i] : +0          (xd-shaped, rounded to dt once when stored)
+ *   dbias[c] = sum over the pixels of dpre[., c]   (fp32, of the stored values)
+ * It equals tfk_conv2d_bwd_input(..., dx = dpre, beta = 0) followed by tfk_bias_relu_bwd(y,
+ * dpre, ...) up to the order of the fp32 bias-gradient sums, without forming g in memory.
+ *   dy, dyd, w, p, dt : as tfk_conv2d_bwd_input.
+ *   y     : xd-shaped (the same view as dpre), the forward ReLU output; read only.
+ *   dpre  : xd-shaped, overwritten; must not overlap dy, w, y or dbias.
+ *   dbias : xd.c fp32 values, overwritten.
+ *   ws    : at least tfk_conv2d_workspace_bytes(3, xd, dyd.c, p, dt) bytes.
+ * Requirements: xd.c <= 16384.  xd.n == 0 sets dbias to 0.
+ */
+TFK_API tfk_status tfk_conv2d_bwd_input_relu_bwd(const void *dy, tfk_nhwc dyd, const void *w, tfk_window p,
+                                         tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd,
+                                         float *dbias, void *ws, size_t ws_bytes, void *stream);
+
 /* Workspace needed by a convolution: op 0 = forward, 1 = backprop-input,
- * 2 = backprop-filter; xd is the forward input, cout the filter's output
- * channels.  Returns 0 for invalid arguments (the operation itself then
- * reports the error). */
+ * 2 = backprop-filter, 3 = backprop-input fused with the ReLU backward;
+ * xd is the forward input, cout the filter's output channels.  Returns 0
+ * for invalid arguments (the operation itself then reports the error). */
 TFK_API size_t tfk_conv2d_workspace_bytes(int32_t op, tfk_nhwc xd, int32_t cout, tfk_window p,
                                   tfk_dtype dt);
 

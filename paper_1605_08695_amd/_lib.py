@@ -15,7 +15,8 @@ TFK_F32 = 0
 TFK_BF16 = 1
 
 # every symbol include/tfk.h declares
-EXPORTS = ["tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_maxpool_bwd_relu_bwd", "tfk_conv2d_bwd_input", "tfk_conv2d_bwd_filter", "tfk_conv2d_workspace_bytes",
+EXPORTS = ["tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_maxpool_bwd_relu_bwd", "tfk_conv2d_bwd_input",
+           "tfk_conv2d_bwd_input_relu_bwd", "tfk_conv2d_bwd_filter", "tfk_conv2d_workspace_bytes",
            "tfk_bias_relu_fwd", "tfk_bias_relu_bwd", "tfk_bias_relu_bwd_workspace_bytes",
            "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps",
            "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd", "tfk_apply_sgd_multi",
@@ -56,6 +57,7 @@ def load(path: str = LIB_PATH):
     lib.tfk_conv2d_fwd_bias_relu.argtypes = [vp, Nhwc, vp, i32, vp, Window, st, vp, Nhwc, vp, sz, vp]
     lib.tfk_conv2d_bwd_input.argtypes = [vp, Nhwc, vp, Window, st, vp, Nhwc, f32, vp, sz, vp]
     lib.tfk_conv2d_bwd_filter.argtypes = [vp, Nhwc, vp, Nhwc, Window, st, vp, vp, sz, vp]
+    lib.tfk_conv2d_bwd_input_relu_bwd.argtypes = [vp, Nhwc, vp, Window, st, vp, vp, Nhwc, vp, vp, sz, vp]
     lib.tfk_conv2d_workspace_bytes.argtypes = [i32, Nhwc, i32, Window, st]
     lib.tfk_conv2d_workspace_bytes.restype = sz
     lib.tfk_bias_relu_fwd.argtypes = [vp, Nhwc, vp, st, vp]
@@ -71,7 +73,8 @@ def load(path: str = LIB_PATH):
     lib.tfk_apply_sgd.argtypes = [vp, vp, i64, f32, vp, vp]
     lib.tfk_apply_sgd_multi.argtypes = [i32, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(i64), f32,
                                         ctypes.POINTER(vp), vp]
-    for name in ("tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_conv2d_bwd_input", "tfk_conv2d_bwd_filter", "tfk_bias_relu_fwd",
+    for name in ("tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_conv2d_bwd_input", "tfk_conv2d_bwd_input_relu_bwd",
+                 "tfk_conv2d_bwd_filter", "tfk_bias_relu_fwd",
                  "tfk_bias_relu_bwd", "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_bwd_relu_bwd",
                  "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps", "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd",
                  "tfk_apply_sgd_multi"):

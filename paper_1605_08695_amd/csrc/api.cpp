@@ -166,7 +166,7 @@ const char *tfk_status_string(tfk_status s) {
 
 // ------------------------------------------------------------------ convolution
 size_t tfk_conv2d_workspace_bytes(int32_t op, tfk_nhwc xd, int32_t cout, tfk_window p, tfk_dtype dt) {
-    if (op != 0 && op != 2) return 0;
+    if (op != 0 && op != 2 && op != 3) return 0;
     if (!valid_dt(dt) || check_view("x", xd) != TFK_OK || check_window(p) != TFK_OK || cout < 1) return 0;
     const int oh = out_len(xd.h, p.kh, p.stride_h, p.pad_top, p.pad_bottom);
     const int ow = out_len(xd.w, p.kw, p.stride_w, p.pad_left, p.pad_right);
@@ -174,6 +174,7 @@ size_t tfk_conv2d_workspace_bytes(int32_t op, tfk_nhwc xd, int32_t cout, tfk_win
     ConvShape s{xd.n, xd.h, xd.w, xd.c, oh, ow, cout, p.kh, p.kw, p.stride_h, p.stride_w, p.pad_top, p.pad_left};
     const int dti = dt == TFK_F32 ? 0 : 1;
     if (op == 0) return conv_fold_applies(dti, s) ? conv_fold_ws_bytes(0, s) : 0;
+    if (op == 3) return conv_bwd_data_relu_ws_bytes(dti, s, xd.pixel_stride ? xd.pixel_stride : xd.c);
     return conv_bwd_filter_ws_bytes(dti, s);
 }
 
@@ -242,6 +243,43 @@ tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void *w, tfk
     return hip_status(launch_conv_bwd_data(dt == TFK_F32 ? 0 : 1, dy, dyd.pixel_stride, w, dx, dxd.pixel_stride,
                                            beta, s, (hipStream_t)stream),
                       "conv2d_bwd_input");
+}
+
+tfk_status tfk_conv2d_bwd_input_relu_bwd(const void *dy, tfk_nhwc dyd, const void *w, tfk_window p, tfk_dtype dt,
+                                         const void *y, void *dpre, tfk_nhwc xd, float *dbias, void *ws,
+                                         size_t ws_bytes, void *stream) {
+    ConvShape s;
+    TRY(check_conv(xd, dyd.c, p, dt, dyd, "dpre", "dy", s));
+    if (xd.c > 16384) return fail(TFK_ERR_SHAPE, "conv2d_bwd_input_relu_bwd supports at most 16384 channels");
+    TRY(need_ptr(dbias, "dbias"));
+    TRY(need_align(dbias, 4, "dbias"));
+    hipStream_t st = (hipStream_t)stream;
+    if (xd.n == 0) return hip_status(launch_fill_zero(dbias, xd.c, st), "conv2d_bwd_input_relu_bwd");
+    const int64_t es = esize(dt);
+    TRY(need_ptr(dy, "dy"));
+    TRY(need_ptr(w, "w"));
+    TRY(need_ptr(y, "y"));
+    TRY(need_ptr(dpre, "dpre"));
+    TRY(need_align(dy, es, "dy"));
+    TRY(need_align(w, es, "w"));
+    TRY(need_align(y, es, "y"));
+    TRY(need_align(dpre, es, "dpre"));
+    const int64_t xb = view_bytes(xd, es), yb = view_bytes(dyd, es), wb = filter_bytes(s, es), bb = (int64_t)xd.c * 4;
+    if (overlap(dpre, xb, dy, yb) || overlap(dpre, xb, w, wb) || overlap(dpre, xb, y, xb))
+        return fail(TFK_ERR_ALIAS, "dpre overlaps dy, w or y");
+    if (overlap(dbias, bb, dy, yb) || overlap(dbias, bb, w, wb) || overlap(dbias, bb, y, xb) ||
+        overlap(dbias, bb, dpre, xb))
+        return fail(TFK_ERR_ALIAS, "dbias overlaps a tensor");
+    const int dti = dt == TFK_F32 ? 0 : 1;
+    const int64_t xs = xd.pixel_stride ? xd.pixel_stride : xd.c;
+    const size_t need = conv_bwd_data_relu_ws_bytes(dti, s, xs);
+    TRY(check_ws(ws, ws_bytes, need));
+    if (overlap(ws, (int64_t)need, dy, yb) || overlap(ws, (int64_t)need, w, wb) || overlap(ws, (int64_t)need, y, xb) ||
+        overlap(ws, (int64_t)need, dpre, xb) || overlap(ws, (int64_t)need, dbias, bb))
+        return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
+    return hip_status(launch_conv_bwd_data_relu(dti, dy, dyd.pixel_stride ? dyd.pixel_stride : dyd.c, w, dpre, xs, y,
+                                                dbias, (float *)ws, s, st),
+                      "conv2d_bwd_input_relu_bwd");
 }
 
 tfk_status tfk_conv2d_bwd_filter(const void *x, tfk_nhwc xd, const void *dy, tfk_nhwc dyd, tfk_window p,

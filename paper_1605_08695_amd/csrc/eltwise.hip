@@ -1022,6 +1022,11 @@ hipError_t launch_sum_splits(float *part, int splits, int64_t mn, float *out, hi
     return sum_splits_t<1>(part, splits, mn, out, st);
 }
 
+hipError_t launch_sum_partials(const float *partial, int G, int C, float *out, hipStream_t st) {
+    hipLaunchKernelGGL(sum_partials_kernel, dim3(C), dim3(256), 0, st, partial, G, C, out);
+    return hipGetLastError();
+}
+
 hipError_t launch_fill_zero(float *out, int64_t n, hipStream_t st) {
     if (n <= 0) return hipSuccess;
     const int grid = grid_for(n, 256, 8192);

@@ -63,6 +63,12 @@ struct IgArgs {
     int64_t split_stride;// BWD_FILTER: floats between consecutive partial outputs
     FastDiv dC, dKW, dOW, dOH, dK;
     uint32_t bytes_i, bytes_j;   // pipelined kernel: byte spans of src_i / src_j (each < 2^31)
+    // pipelined BWD_DATA with beta 0: when relu_y is set, the ReLU backward of the layer that produced
+    // x is applied (out = relu_y > 0 ? dx : +0, relu_y with dx's layout) and per-channel sums of
+    // the stored values go to db_part[c * db_rows + row] (row: block and wave column)
+    const void *relu_y;
+    float *db_part;
+    int db_rows;
 };
 
 template <typename T> struct Mfma;

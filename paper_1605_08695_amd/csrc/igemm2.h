@@ -212,7 +212,18 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
         k_beg = bz * a.k_split;
         k_end = min(a.N * a.OH * a.OW, k_beg + a.k_split);
     }
-    if (j0 >= MJ_ext) return;
+    if (j0 >= MJ_ext) {
+        // (a block past this stride phase's pixels still owns its rows of bias-gradient partials)
+        if (DIR == DIR_BWD_DATA && a.relu_y != nullptr && (lane & 15) == 0) {
+            const int row = (bz * (int)(gridDim.x / a.tiles_i) + tj) * WGJ + (wave >> 1);
+            for (int x = 0; x < MI; ++x) {
+                const int i = i0 + (wave & 1) * WI + x * 16 + 4 * (lane >> 4);
+                if (i < a.NI)
+                    for (int q = 0; q < 4; ++q) a.db_part[(int64_t)(i + q) * a.db_rows + row] = 0.f;
+            }
+        }
+        return;
+    }
     const int nk = k_end > k_beg ? (k_end - k_beg + BK - 1) / BK : 0;
 
     // ------------------------------------------------------------ copy plan
@@ -508,6 +519,15 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     }
 
     // ------------------------------------------------------------ epilogue
+    // (bwd-input with relu_y: the ReLU backward of the producing layer and the per-channel sums
+    // of the stored dpre over this wave's rows, in y order, then over the 16 lanes of a column
+    // group by a fixed xor tree)
+    const bool relu = DIR == DIR_BWD_DATA && a.relu_y != nullptr;
+    float cs[MI][4];
+#pragma unroll
+    for (int x = 0; x < MI; ++x)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) cs[x][q] = 0.f;
 #pragma unroll
     for (int y = 0; y < MJ; ++y) {
         const int j = j0 + wj * WJ + y * 16 + ld;
@@ -543,6 +563,14 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
                         r4[2] += a.beta * bf16_to_f32(old.y & 0xffffu);
                         r4[3] += a.beta * bf16_to_f32(old.y >> 16);
                     }
+                    if (relu) {
+                        const uint2 yv = *reinterpret_cast<const uint2 *>(
+                            reinterpret_cast<const bf16_t *>(a.relu_y) + rowoff + i);
+                        const float yq[4] = {bf16_to_f32(yv.x & 0xffffu), bf16_to_f32(yv.x >> 16),
+                                             bf16_to_f32(yv.y & 0xffffu), bf16_to_f32(yv.y >> 16)};
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) r4[q] = yq[q] > 0.f ? r4[q] : 0.f;
+                    }
                 }
                 if constexpr (DIR == DIR_FWD) {
                     if (a.bias != nullptr) {      // fused bias + ReLU, rounded once (i + 3 < NI)
@@ -557,6 +585,32 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
                 pk.x = pack_bf16x2(r4[0], r4[1]);
                 pk.y = pack_bf16x2(r4[2], r4[3]);
                 *reinterpret_cast<uint2 *>(o) = pk;
+                if (relu) {
+                    cs[x][0] += bf16_to_f32(pk.x & 0xffffu);
+                    cs[x][1] += bf16_to_f32(pk.x >> 16);
+                    cs[x][2] += bf16_to_f32(pk.y & 0xffffu);
+                    cs[x][3] += bf16_to_f32(pk.y >> 16);
+                }
+            }
+        }
+    }
+    if (relu) {
+        const int row = (bz * (int)(gridDim.x / a.tiles_i) + tj) * WGJ + wj;
+#pragma unroll
+        for (int x = 0; x < MI; ++x) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                float v = cs[x][q];
+                v += __shfl_xor(v, 1, 16);
+                v += __shfl_xor(v, 2, 16);
+                v += __shfl_xor(v, 4, 16);
+                v += __shfl_xor(v, 8, 16);
+                cs[x][q] = v;
+            }
+            const int i = i0 + wi * WI + x * 16 + 4 * lg;
+            if (ld == 0 && i < a.NI) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) a.db_part[(int64_t)(i + q) * a.db_rows + row] = cs[x][q];
             }
         }
     }

@@ -118,6 +118,9 @@ static inline void fill_geom(IgArgs &a, const ConvShape &s) {
     a.k_split = 0;
     a.split_stride = 0;
     a.bytes_i = a.bytes_j = 0;
+    a.relu_y = nullptr;
+    a.db_part = nullptr;
+    a.db_rows = 0;
 }
 
 }  // namespace tfk

@@ -38,6 +38,13 @@ hipError_t launch_conv_fwd(int dt, const void *x, int64_t xs, const void *w, voi
                            const ConvShape &s, const float *bias, void *ws, hipStream_t st);
 hipError_t launch_conv_bwd_data(int dt, const void *dy, int64_t dys, const void *w, void *dx, int64_t dxs,
                                 float beta, const ConvShape &s, hipStream_t st);
+// Input gradient fused with the ReLU backward + bias gradient of the layer that produced x:
+// dpre = y > 0 ? bwd_input(dy, w) : +0 (dx's view), db = column sums of dpre; ws: partials.
+hipError_t launch_conv_bwd_data_relu(int dt, const void *dy, int64_t dys, const void *w, void *dpre, int64_t dxs,
+                                     const void *y, float *db, float *ws, const ConvShape &s, hipStream_t st);
+size_t conv_bwd_data_relu_ws_bytes(int dt, const ConvShape &s, int64_t dxs);
+// Per-channel sums of partial[c][G] (G values per channel, summed in order) into out[C].
+hipError_t launch_sum_partials(const float *partial, int G, int C, float *out, hipStream_t st);
 hipError_t launch_conv_bwd_filter(int dt, const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,
                                   const ConvShape &s, void *ws, hipStream_t st);
 // Split-K plan of bwd-filter: number of splits and reduction elements per split.

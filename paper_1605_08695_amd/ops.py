@@ -124,6 +124,27 @@ def conv2d_bwd_input(dy, w, dx, stride, pads, beta=0.0, stream=None):
     return dx
 
 
+def conv2d_bwd_input_relu_bwd(dy, w, y, dpre, stride, pads, dbias=None, ws=None, stream=None):
+    """dpre = (y > 0) * conv2d_fwd^T(dy), dbias = column sums of dpre (fp32): the input gradient
+    fused with the ReLU backward of the layer that produced the input (y, dpre: its view)."""
+    lib = load()
+    kh, kw, cin, cout = w.shape
+    if not (w.dtype == dy.dtype == y.dtype == dpre.dtype):
+        raise TypeError("dy, w, y and dpre must share one dtype")
+    d_y, d_p = nhwc(y), nhwc(dpre)
+    if (d_y.n, d_y.h, d_y.w, d_y.c, d_y.pixel_stride) != (d_p.n, d_p.h, d_p.w, d_p.c, d_p.pixel_stride):
+        raise ValueError("y and dpre must share one view (extents and pixel stride)")
+    if dbias is None:
+        dbias = torch.empty(cin, dtype=torch.float32, device=y.device)
+    win = window(kh, kw, stride, pads)
+    need = lib.tfk_conv2d_workspace_bytes(3, d_p, cout, win, _dt(y))
+    if need and (ws is None or ws.numel() < need):
+        ws = _ws(need, y.device)
+    check(lib.tfk_conv2d_bwd_input_relu_bwd(_ptr(dy), nhwc(dy), _ptr(w), win, _dt(dy), _ptr(y), _ptr(dpre), d_p,
+                                            _ptr(dbias), _ptr(ws) if need else None, need, _stream(stream)))
+    return dpre, dbias
+
+
 def conv2d_bwd_filter(x, dy, kernel_hw, stride, pads, dw=None, ws=None, stream=None):
     """dW (fp32 HWIO) = sum over pixels of x-gather * dy."""
     lib = load()

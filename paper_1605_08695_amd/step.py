@@ -128,12 +128,22 @@ class Replica:
                 if (len(w) == 1 and isinstance(w[0], Conv) and w[0].dst_c0 == 0
                         and w[0].cout == net.tensors[op.src][3] and len(readers[op.src]) == 1):
                     self.pool_relu[op.name] = w[0]
-        self.relu_fused = {c.name for c in self.pool_relu.values()}
+        # ---- convolutions whose input is the whole ReLU output of another convolution and
+        # feeds nothing else: their input gradient applies that ReLU backward in its epilogue
+        self.bwi_relu = {}                       # conv name -> the conv that produced its input
+        for op in net.ops:
+            if isinstance(op, Conv) and op.src != "x" and op.src != net.output:
+                w = writers.get(op.src, [])
+                if (len(w) == 1 and isinstance(w[0], Conv) and w[0].dst_c0 == 0
+                        and w[0].cout == net.tensors[op.src][3] and len(readers[op.src]) == 1):
+                    self.bwi_relu[op.name] = w[0]
+        self.relu_fused = ({c.name for c in self.pool_relu.values()} |
+                           {c.name for c in self.bwi_relu.values()})
         # ---- one workspace big enough for every op
         need = 0
         for c in net.convs:
             x = self.act[c.src]
-            for op_kind in (0, 2):
+            for op_kind in (0, 2, 3) if c.name in self.bwi_relu else (0, 2):
                 need = max(need, ops.conv2d_workspace_bytes(op_kind, x, c.cout, c.kh, c.kw, (c.sh, c.sw), c.pads))
             need = max(need, ops.bias_relu_bwd_workspace_bytes(self._slice(self.act, c)))
         self.ws = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=dev)
@@ -174,8 +184,8 @@ class Replica:
         """Gradients of every variable.  With ``side`` (a second stream), the filter gradient
         of each convolution that also has an input gradient runs there, concurrently with that
         input gradient and everything after it on ``stream``: the two only read the same
-        tensors, and the side stream joins back before this returns (the dataflow executor runs independent kernels on several GPU
-        streams, Section 5)."""
+        tensors, and the side stream joins back before this returns (the dataflow executor runs
+        independent kernels on several GPU streams, Section 5)."""
         net = self.net
         written = set()
         cur = stream if stream is not None else torch.cuda.current_stream()
@@ -185,7 +195,7 @@ class Replica:
             beta = 1.0 if op.src in written else 0.0
             if isinstance(op, Conv):
                 if op.name in self.relu_fused:
-                    dpre = dy                        # written by the fused max-pool backward
+                    dpre = dy                        # written by the fused pool / input-gradient backward
                 else:
                     y = self._slice(self.act, op)
                     dpre = self._slice({op.dst: self.dpre_out}, op) if op.dst == net.output else dy
@@ -203,7 +213,15 @@ class Replica:
                 ops.conv2d_bwd_filter(x, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, dw=self.dW[op.name],
                                       ws=self.ws_side if on_side else self.ws, stream=fs)
                 if trace: trace("conv_bwd_filter:end", op, stream=fs, dw=self.dW[op.name])
-                if src_grad:
+                if src_grad and op.name in self.bwi_relu:
+                    prod = self.bwi_relu[op.name]
+                    dx, y = self.grad[op.src], self.act[op.src]
+                    if trace: trace("conv_bwd_input_relu_bwd", op, stream=stream, dy=dpre, w=self.Wlp[op.name],
+                                    y=y)
+                    ops.conv2d_bwd_input_relu_bwd(dpre, self.Wlp[op.name], y, dx, (op.sh, op.sw), op.pads,
+                                                  dbias=self.db[prod.name], ws=self.ws, stream=stream)
+                    if trace: trace("conv_bwd_input_relu_bwd:end", op, stream=stream, dpre=dx, db=self.db[prod.name])
+                elif src_grad:
                     dx = self.grad[op.src]
                     if trace: trace("conv_bwd_input", op, stream=stream, dy=dpre, w=self.Wlp[op.name], dx=dx,
                                     beta=beta)

@@ -242,6 +242,15 @@ class ParityTracer:
                                       dx=dx_old, beta=inp["beta"])
         self.record_tensor("conv_bwd_input", op.name, self._x64(out["dx"]), ref, self.dtype)
 
+    def _check_conv_bwd_input_relu_bwd(self, op, inp, out):
+        # the input gradient of op fused with the ReLU backward of the layer that produced its input
+        dy, y = self._x64(inp["dy"]), self._x64(inp["y"])
+        g = oracle.conv2d_bwd_input(dy, f64(inp["w"]), y.shape, (op.sh, op.sw), op.pads)
+        ref_dpre, ref_db = oracle.bias_relu_bwd(y, g)
+        self.record_tensor("conv_bwd_input_relu_bwd", op.name, self._x64(out["dpre"]), ref_dpre, self.dtype)
+        if self.sample is None:              # (the bias gradient sums over every image)
+            self.record_tensor("conv_bwd_input_relu_bwd:db", op.name, f64(out["db"]), ref_db, torch.float32)
+
     def _check_maxpool_bwd(self, op, inp, out):
         dy = self._x64(inp["dy"])
         am = self._dense(inp["argmax"], inp["dx"].shape, op)

@@ -101,6 +101,42 @@ def test_conv_three_directions(case, dtype):
     assert_close(f64(dw), ref, torch.float32, dtype, label="bwd_filter")
 
 
+RELU_BWI_CASES = ["ragged_tiles", "3x3s2_valid", "3x3s2_pad_odd", "1x1s2_empty_phase", "5x5_cout192",
+                  "alexnet_conv3_shape", "chunks_c192_uneven_pad", "c192_bwd_tiles", "one_pixel_out_c64", "odd_channels"]
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
+@pytest.mark.parametrize("name", RELU_BWI_CASES)
+def test_conv_bwd_input_relu_bwd_fused(name, dtype):
+    """Input gradient fused with the producer's ReLU backward + bias gradient against the
+    oracle's two ops (stride phases with empty phases, ragged tiles, 64/128/192-wide tiles)."""
+    case = next(c for c in CONV_CASES if c[0] == name)
+    _, N, H, W, C, K, KH, KW, sh, sw, pads = case
+    say("fused bwd-input + relu case", name, dtype)
+    rng = np.random.default_rng(zlib.crc32(("relu" + name).encode()))
+    # x is a ReLU output: exact zeros mask the gradient
+    y = torch.from_numpy(np.maximum(rng.standard_normal((N, H, W, C)), 0.0)).to(dtype).to(DEV)
+    w = _mk((KH, KW, C, K), dtype, rng, np.sqrt(2.0 / (KH * KW * C)))
+    out = ops.conv2d_fwd(y, w, (sh, sw), pads)
+    dy = _mk(out.shape, dtype, rng)
+    dpre = _mk(y.shape, dtype, rng)                            # overwritten
+    _, db = ops.conv2d_bwd_input_relu_bwd(dy, w, y, dpre, (sh, sw), pads)
+    torch.cuda.synchronize()
+    g = oracle.conv2d_bwd_input(f64(dy), f64(w), y.shape, (sh, sw), pads)
+    ref_dpre, ref_db = oracle.bias_relu_bwd(f64(y), g)
+    assert_close(f64(dpre), ref_dpre, dtype, label="fused dpre")
+    assert np.all(f64(dpre)[f64(y) <= 0] == 0) and not bool(torch.any(torch.signbit(dpre)[y <= 0]))
+    assert_close(f64(db), ref_db, torch.float32, dtype, label="fused db")
+    # the bias gradient is the column sum of the stored dpre
+    assert err(f64(db), f64(dpre).sum(axis=(0, 1, 2))) <= 1e-4
+    # and the stored dpre is bit-identical to the unfused pair's
+    dx = torch.empty_like(y)
+    ops.conv2d_bwd_input(dy, w, dx, (sh, sw), pads)
+    dp2, _ = ops.bias_relu_bwd(y, dx)
+    torch.cuda.synchronize()
+    assert torch.equal(dpre, dp2)
+
+
 @pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
 def test_conv_channel_slice_views(dtype):
     """Input read from and output written into channel slices of wider buffers."""
