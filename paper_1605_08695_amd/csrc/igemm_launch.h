@@ -51,7 +51,13 @@ struct Igemm2Tile {
 // otherwise 64-channel tiles.
 static inline Igemm2Tile igemm2_tiles(int ni, int mj, int zdim) {
     const int64_t blocks_j = (int64_t)((mj + 127) / 128) * zdim;
-    if (ni % 128 == 0 && (ni / 128) * blocks_j >= 256) return {128, 128, 4, 2};
+    if (ni % 128 == 0 && (ni / 128) * blocks_j >= 256) {
+        // 128-row tiles that leave most CUs with one block (AlexNet conv4/conv5: 338 blocks)
+        // spread better as 96-row tiles, still within one round of two blocks per CU
+        const int64_t b128 = (ni / 128) * blocks_j, b96 = (ni / 128) * (int64_t)((mj + 95) / 96) * zdim;
+        if (b128 < 448 && b96 <= 512) return {128, 96, 4, 2};
+        return {128, 128, 4, 2};
+    }
     if (ni % 192 == 0 && (ni / 192) * blocks_j >= 256) return {192, 128, 4, 2};
     return {64, 128, 4, 2};
 }
@@ -68,6 +74,11 @@ static bool igemm2_launch(IgArgs &a, int mj, int zdim, const Igemm2Tile &t, hipS
     const int tiles_j = (mj + t.bj - 1) / t.bj;
     const dim3 grid((unsigned)(a.tiles_i * tiles_j), 1, (unsigned)zdim);
     const int key = ((t.bi / 64) << 12) | ((t.bj / 64) << 8) | (t.nw << 4) | t.ns;
+    if (t.bi == 128 && t.bj == 96 && t.nw == 4 && t.ns == 2) {
+        // (96-row k-major tiles are not laid out: forward and bwd-input only)
+        if constexpr (DIR == DIR_BWD_FILTER) return false;
+        else { igemm2_go<DIR, 128, 96, 4, 2>(a, grid, st); return true; }
+    }
     if (t.bi == 192 && t.bj == 128 && t.nw == 4 && t.ns == 2) {
         // (the filter-gradient direction does not fit these tiles in its registers)
         if constexpr (DIR == DIR_BWD_FILTER) return false;

@@ -56,6 +56,9 @@ CONV_CASES = [
     ("k192_tiles", 32, 32, 32, 64, 192, 3, 3, 1, 1, (1, 1, 1, 1)),
     # ... and of the input gradient (192 input channels)
     ("c192_bwd_tiles", 32, 32, 32, 192, 64, 3, 3, 1, 1, (1, 1, 1, 1)),
+    # 288 tiles of 128 x 128 (most CUs with one block): 128 x 96 tiles, forward and input gradient
+    ("bj96_tiles_fwd", 36, 32, 32, 64, 128, 3, 3, 1, 1, (1, 1, 1, 1)),
+    ("bj96_tiles_bwd", 36, 32, 32, 128, 64, 3, 3, 1, 1, (1, 1, 1, 1)),
 ]
 
 
@@ -102,7 +105,8 @@ def test_conv_three_directions(case, dtype):
 
 
 RELU_BWI_CASES = ["ragged_tiles", "3x3s2_valid", "3x3s2_pad_odd", "1x1s2_empty_phase", "5x5_cout192",
-                  "alexnet_conv3_shape", "chunks_c192_uneven_pad", "c192_bwd_tiles", "one_pixel_out_c64", "odd_channels"]
+                  "alexnet_conv3_shape", "chunks_c192_uneven_pad", "c192_bwd_tiles", "bj96_tiles_bwd",
+                  "one_pixel_out_c64", "odd_channels"]
 
 
 @pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
