@@ -1000,13 +1000,63 @@ __global__ __launch_bounds__(256) void sum_splits_direct_kernel(const float *__r
 
 constexpr int64_t kDirectSumMinThreads = 32768;
 
+// The same sums with G threads per output: thread g of an output adds the splits
+// [g S / G, (g + 1) S / G) in order, then the G partial sums are added in g order through
+// LDS.  A block covers 256 / G consecutive outputs, so every split row is read as a
+// contiguous run; G times the threads of the one-thread form keep more loads in flight.
+template <int VEC, int G>
+__global__ __launch_bounds__(256) void sum_splits_grouped_kernel(const float *__restrict__ part, int splits,
+                                                                 int64_t mn, float *__restrict__ out) {
+    typedef typename FVec<VEC>::T V;
+    constexpr int COLS = 256 / G;
+    __shared__ V red[G][COLS];
+    const int64_t mv = mn / VEC;
+    const int c = threadIdx.x % COLS, g = threadIdx.x / COLS;
+    const int s0 = (int)((int64_t)g * splits / G), s1 = (int)((int64_t)(g + 1) * splits / G);
+    for (int64_t base = (int64_t)blockIdx.x * COLS; base < mv; base += (int64_t)gridDim.x * COLS) {
+        const int64_t i = base + c;
+        V acc = V{};
+        if (i < mv && s0 < s1) {
+            const V *src = reinterpret_cast<const V *>(part) + i;
+            acc = src[(int64_t)s0 * mv];
+            int s = s0 + 1;
+            for (; s + 8 <= s1; s += 8) {
+                V v[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) v[q] = src[(int64_t)(s + q) * mv];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) acc += v[q];
+            }
+            for (; s < s1; ++s) acc += src[(int64_t)s * mv];
+        }
+        red[g][c] = acc;
+        __syncthreads();
+        if (g == 0 && i < mv) {
+            V t = red[0][c];
+#pragma unroll
+            for (int q = 1; q < G; ++q) t += red[q][c];
+            reinterpret_cast<V *>(out)[i] = t;
+        }
+        __syncthreads();
+    }
+}
+
 template <int VEC>
 static hipError_t sum_splits_t(float *part, int splits, int64_t mn, float *out, hipStream_t st) {
     const int groups = (splits + kSplitGroup - 1) / kSplitGroup;
     const int64_t mv = mn / VEC;
     if (mv >= kDirectSumMinThreads) {
-        hipLaunchKernelGGL(sum_splits_direct_kernel<VEC>, dim3(grid_for(mv, 256, 16384)), dim3(256), 0, st, part,
-                           splits, mn, out);
+        // about 2^18 threads in flight: 4 or 8 per output when the outputs alone give fewer
+        if (splits >= 8 && mv < (1 << 17)) {
+            hipLaunchKernelGGL((sum_splits_grouped_kernel<VEC, 8>), dim3(grid_for(mv, 32, 16384)), dim3(256), 0, st,
+                               part, splits, mn, out);
+        } else if (splits >= 4 && mv < (1 << 18)) {
+            hipLaunchKernelGGL((sum_splits_grouped_kernel<VEC, 4>), dim3(grid_for(mv, 64, 16384)), dim3(256), 0, st,
+                               part, splits, mn, out);
+        } else {
+            hipLaunchKernelGGL(sum_splits_direct_kernel<VEC>, dim3(grid_for(mv, 256, 16384)), dim3(256), 0, st, part,
+                               splits, mn, out);
+        }
         return hipGetLastError();
     }
     hipLaunchKernelGGL(sum_split_groups_kernel<VEC>, dim3(grid_for(mv * groups, 256, 16384)), dim3(256), 0, st, part,
