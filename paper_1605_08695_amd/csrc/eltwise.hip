@@ -1059,6 +1059,12 @@ static hipError_t sum_splits_t(float *part, int splits, int64_t mn, float *out, 
         }
         return hipGetLastError();
     }
+    if (splits >= 64) {
+        // few outputs, many splits (a first layer's per-workgroup partials): 16 threads per output
+        hipLaunchKernelGGL((sum_splits_grouped_kernel<VEC, 16>), dim3(grid_for(mv, 16, 16384)), dim3(256), 0, st,
+                           part, splits, mn, out);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(sum_split_groups_kernel<VEC>, dim3(grid_for(mv * groups, 256, 16384)), dim3(256), 0, st, part,
                        splits, mn, groups);
     hipLaunchKernelGGL(sum_groups_kernel<VEC>, dim3(grid_for(mv, 256, 16384)), dim3(256), 0, st, part, groups, mn,
