@@ -101,6 +101,27 @@ def test_conv_bwd_validation(lib):
     assert st == NULL
 
 
+def test_conv_bwd_input_relu_bwd_validation(lib):
+    """The input gradient fused with the producer's ReLU backward: workspace query (op 3),
+    NULL, aliasing and workspace checks, before any launch."""
+    W = Window(3, 3, 1, 1, 1, 1, 1, 1)
+    xd, dyd = Nhwc(128, 13, 13, 384, 0), Nhwc(128, 13, 13, 256, 0)
+    need = lib.tfk_conv2d_workspace_bytes(3, xd, 256, W, BF16)
+    # at least one fp32 partial per channel and per 128-pixel tile of the output grid
+    assert need >= 384 * 4 * ((128 * 13 * 13 + 127) // 128)
+    assert lib.tfk_conv2d_workspace_bytes(1, xd, 256, W, BF16) == 0
+    def fused(dy=P, w=P + 0x10000000, y=P + 0x20000000, dpre=P + 0x30000000, db=P + 0x40000000,
+              ws=P + 0x50000000, ws_bytes=need):
+        return lib.tfk_conv2d_bwd_input_relu_bwd(vp(dy), dyd, vp(w), W, BF16, vp(y), vp(dpre), xd, vp(db), vp(ws),
+                                                 ws_bytes, None)
+    assert fused(db=0) == NULL
+    assert fused(y=0) == NULL
+    assert fused(dpre=P + 0x20000010) == ALIAS                         # dpre overlaps y
+    assert fused(db=P + 0x30000000) == ALIAS                           # dbias inside dpre
+    assert fused(ws_bytes=need - 1) == WORKSPACE
+    assert fused(ws=P + 0x20000000) == ALIAS                           # workspace over y
+
+
 def test_pool_validation(lib):
     W = Window(3, 3, 2, 2, 0, 0, 0, 0)
     st = lib.tfk_maxpool_fwd(vp(P), Nhwc(2, 7, 7, 8, 0), W, BF16, vp(P + 0x100000), Nhwc(2, 4, 4, 8, 0),
