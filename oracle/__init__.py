@@ -23,6 +23,10 @@ Parity status of each function (pins are in tests/test_oracle_pins.py):
 * maxpool_bwd       pinned: mass conservation, finite differences at tie-free
                     points, support only on argmax positions.
 * apply_sgd         pinned: closed form and a surrogate-loss decrease.
+* apply_momentum    pinned: constant-gradient closed forms (classical and nesterov),
+                    momentum 0 = SGD, the velocity as a geometric sum of past gradients.
+* apply_adam        pinned: constant-gradient closed form, first-step form, the moments
+                    as bias-weighted sums of past gradients, beta = 0 forms.
 * step (net.py)     pinned: finite differences of the whole single-layer loss
                     and the exact first-order decrease of a piecewise-linear net.
 """
@@ -82,6 +86,9 @@ def _declare(lib):
     lib.orc_maxpool_fwd.argtypes = [_dp, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _dp, _ip, _i, _i]
     lib.orc_maxpool_bwd.argtypes = [_dp, _ip, _l, _dp, _l, _i]
     lib.orc_apply_sgd.argtypes = [_dp, _dp, _l, ctypes.c_double]
+    lib.orc_apply_momentum.argtypes = [_dp, _dp, _dp, _l, ctypes.c_double, ctypes.c_double, ctypes.c_int]
+    lib.orc_apply_adam.argtypes = [_dp, _dp, _dp, _dp, _l, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                   ctypes.c_double, ctypes.c_int]
 
 
 def use_library(path: str):
@@ -245,3 +252,22 @@ def apply_sgd(var, grad, lr):
     assert out.shape == g.shape
     lib.orc_apply_sgd(_ptr(out), _ptr(g), out.size, float(lr))
     return out
+
+
+def apply_momentum(var, accum, grad, lr, momentum, nesterov=False):
+    """One Momentum update (fp64); returns (var', accum'), leaving the inputs untouched."""
+    lib = _load()
+    out, acc, g = _f64(var).copy(), _f64(accum).copy(), _f64(grad)
+    assert out.shape == acc.shape == g.shape
+    lib.orc_apply_momentum(_ptr(out), _ptr(acc), _ptr(g), out.size, float(lr), float(momentum), int(bool(nesterov)))
+    return out, acc
+
+
+def apply_adam(var, m, v, grad, lr, beta1, beta2, epsilon, t):
+    """One Adam update at step t >= 1 (fp64); returns (var', m', v'), inputs untouched."""
+    lib = _load()
+    out, mm, vv, g = _f64(var).copy(), _f64(m).copy(), _f64(v).copy(), _f64(grad)
+    assert out.shape == mm.shape == vv.shape == g.shape and t >= 1
+    lib.orc_apply_adam(_ptr(out), _ptr(mm), _ptr(vv), _ptr(g), out.size, float(lr), float(beta1), float(beta2),
+                       float(epsilon), int(t))
+    return out, mm, vv

@@ -25,6 +25,7 @@
  * kernels, library convolution and matmul, closed forms and brute-force
  * window scans.
  */
+#include <math.h>
 #include <stdint.h>
 #include <string.h>
 #ifdef _OPENMP
@@ -290,4 +291,39 @@ void orc_maxpool_bwd(const double *dy, const int32_t *argmax, i64 ny,
 void orc_apply_sgd(double *var, const double *grad, i64 n, double lr) {
 #pragma omp parallel for schedule(static)
     for (i64 i = 0; i < n; ++i) var[i] = var[i] - lr * grad[i];
+}
+
+/* Momentum (Section 4.1 names it: a per-parameter velocity accumulated from the gradients,
+ * from which the update is computed), in the velocity form of Sutskever et al. (2013):
+ *   accum <- momentum * accum + grad
+ *   var   <- var - lr * accum                         (classical)
+ *   var   <- var - lr * (grad + momentum * accum)     (nesterov: the look-ahead form)
+ * with accum already updated in the nesterov line. */
+void orc_apply_momentum(double *var, double *accum, const double *grad, i64 n, double lr, double momentum,
+                        int nesterov) {
+#pragma omp parallel for schedule(static)
+    for (i64 i = 0; i < n; ++i) {
+        accum[i] = momentum * accum[i] + grad[i];
+        if (nesterov)
+            var[i] = var[i] - lr * (grad[i] + momentum * accum[i]);
+        else
+            var[i] = var[i] - lr * accum[i];
+    }
+}
+
+/* Adam (named in Section 4.1), Algorithm 1 of Kingma & Ba (2015), step t >= 1:
+ *   m    <- beta1 * m + (1 - beta1) * grad
+ *   v    <- beta2 * v + (1 - beta2) * grad^2
+ *   mhat  = m / (1 - beta1^t),  vhat = v / (1 - beta2^t)
+ *   var  <- var - lr * mhat / (sqrt(vhat) + epsilon) */
+void orc_apply_adam(double *var, double *m, double *v, const double *grad, i64 n, double lr, double beta1,
+                    double beta2, double epsilon, int t) {
+    const double c1 = 1.0 - pow(beta1, (double)t), c2 = 1.0 - pow(beta2, (double)t);
+#pragma omp parallel for schedule(static)
+    for (i64 i = 0; i < n; ++i) {
+        m[i] = beta1 * m[i] + (1.0 - beta1) * grad[i];
+        v[i] = beta2 * v[i] + (1.0 - beta2) * grad[i] * grad[i];
+        const double mhat = m[i] / c1, vhat = v[i] / c2;
+        var[i] = var[i] - lr * mhat / (sqrt(vhat) + epsilon);
+    }
 }

@@ -380,6 +380,89 @@ def check_sgd_decrease(seed=13):
     return abs(dl + lr * float(np.dot(c, c))) / (lr * float(np.dot(c, c)))
 
 
+# ----------------------------------------------------------------------------- momentum, adam
+def _relerr(a, b):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    return float(np.max(np.abs(a - b) / np.maximum(1.0, np.abs(b))))
+
+
+def check_momentum_closed_form(nesterov=False, seed=16, T=7):
+    """A constant gradient g from a zero velocity: after t steps the velocity is the geometric
+    series g (1 - m^t) / (1 - m), so the parameter moves by lr g times the summed series (classical)
+    or by lr g times (T + m times the summed series) (look-ahead form).  Also momentum 0 is SGD."""
+    rng = np.random.default_rng(seed)
+    g = rng.standard_normal(257)
+    var0 = rng.standard_normal(257)
+    lr, m = 0.05, 0.9
+    var, acc = var0.copy(), np.zeros_like(g)
+    for _ in range(T):
+        var, acc = oracle.apply_momentum(var, acc, g, lr, m, nesterov)
+    series = sum((1 - m ** t) / (1 - m) for t in range(1, T + 1))
+    moved = T + m * series if nesterov else series
+    worst = _relerr(acc, g * (1 - m ** T) / (1 - m))
+    worst = max(worst, _relerr(var, var0 - lr * g * moved))
+    v1, a1 = oracle.apply_momentum(var0, rng.standard_normal(257), g, lr, 0.0, nesterov)
+    worst = max(worst, _relerr(v1, var0 - lr * g), _relerr(a1, g))
+    return worst
+
+
+def check_momentum_geometric_sum(nesterov=False, seed=17, T=6):
+    """With any gradient sequence g_1..g_T and a zero start the velocity is sum_k m^(T-k) g_k, and
+    the last parameter move is lr times it (classical) or lr (g_T + m times it) (look-ahead form)."""
+    rng = np.random.default_rng(seed)
+    gs = rng.standard_normal((T, 129))
+    lr, m = 0.03, 0.75
+    var, acc = rng.standard_normal(129), np.zeros(129)
+    prev = var
+    for g in gs:
+        prev = var
+        var, acc = oracle.apply_momentum(var, acc, g, lr, m, nesterov)
+    vel = sum(m ** (T - 1 - k) * gs[k] for k in range(T))
+    step = gs[-1] + m * vel if nesterov else vel
+    return max(_relerr(acc, vel), _relerr(var, prev - lr * step))
+
+
+def check_nesterov_closed_form():
+    return check_momentum_closed_form(nesterov=True)
+
+
+def check_adam_closed_form(seed=18, T=5):
+    """A constant gradient g from zero moments: the moments are g (1 - b1^t) and g^2 (1 - b2^t), so
+    the bias-corrected ones are exactly g and g^2 and every step moves the parameter by
+    lr g / (|g| + eps).  eps is of the order of |g| so that where it enters shows."""
+    rng = np.random.default_rng(seed)
+    g = rng.uniform(-2.0, 2.0, 301)
+    var0 = rng.standard_normal(301)
+    lr, b1, b2, eps = 0.01, 0.9, 0.999, 0.3
+    var, mm, vv = var0.copy(), np.zeros_like(g), np.zeros_like(g)
+    for t in range(1, T + 1):
+        var, mm, vv = oracle.apply_adam(var, mm, vv, g, lr, b1, b2, eps, t)
+    worst = _relerr(mm, g * (1 - b1 ** T))
+    worst = max(worst, _relerr(vv, g * g * (1 - b2 ** T)))
+    worst = max(worst, _relerr(var, var0 - T * lr * g / (np.abs(g) + eps)))
+    return worst
+
+
+def check_adam_weighted_sums(seed=19, T=6):
+    """With any gradient sequence and zero start, the moments are the exponentially weighted sums
+    (1 - b1) sum_k b1^(T-k) g_k and (1 - b2) sum_k b2^(T-k) g_k^2.  With b1 = b2 = 0 a step is
+    lr g / (|g| + eps) at every t."""
+    rng = np.random.default_rng(seed)
+    gs = rng.standard_normal((T, 131))
+    lr, b1, b2, eps = 0.002, 0.8, 0.95, 1e-3
+    var, mm, vv = rng.standard_normal(131), np.zeros(131), np.zeros(131)
+    for t, g in enumerate(gs, start=1):
+        var, mm, vv = oracle.apply_adam(var, mm, vv, g, lr, b1, b2, eps, t)
+    m_ref = (1 - b1) * sum(b1 ** (T - 1 - k) * gs[k] for k in range(T))
+    v_ref = (1 - b2) * sum(b2 ** (T - 1 - k) * gs[k] ** 2 for k in range(T))
+    worst = max(_relerr(mm, m_ref), _relerr(vv, v_ref))
+    var0 = rng.standard_normal(131)
+    v3, _, _ = oracle.apply_adam(var0, rng.standard_normal(131), np.abs(rng.standard_normal(131)), gs[0],
+                                 lr, 0.0, 0.0, eps, 3)
+    worst = max(worst, _relerr(v3, var0 - lr * gs[0] / (np.abs(gs[0]) + eps)))
+    return worst
+
+
 # ----------------------------------------------------------------------------- whole step
 def check_step_fd(net, inputs, samples=24, seed=14):
     """Finite differences of the whole single-step surrogate loss L(W, b, x) = <g, out>.

@@ -103,6 +103,17 @@ def test_sgd_linear_loss_decrease():
     assert pins.check_sgd_decrease() < 1e-10
 
 
+@pytest.mark.parametrize("nesterov", [False, True])
+def test_momentum_closed_form_and_geometric_sum(nesterov):
+    assert pins.check_momentum_closed_form(nesterov) < 1e-12
+    assert pins.check_momentum_geometric_sum(nesterov) < 1e-12
+
+
+def test_adam_closed_form_and_weighted_sums():
+    assert pins.check_adam_closed_form() < 1e-12
+    assert pins.check_adam_weighted_sums() < 1e-12
+
+
 def test_single_layer_step_finite_differences():
     net = W.single_layer(batch=2, hw=8, cin=3, cout=4)
     inp = W.make_inputs(net, seed=3)
@@ -194,6 +205,18 @@ MUTATIONS = [
      "check_sgd_decrease"),
     ("bias grad drops the last pixel", "for (i64 p = 0; p < P; ++p) s += dpre[p * C + c];",
      "for (i64 p = 0; p + 1 < P; ++p) s += dpre[p * C + c];", "check_bias_relu"),
+    ("momentum averages instead of accumulating", "accum[i] = momentum * accum[i] + grad[i];",
+     "accum[i] = momentum * accum[i] + (1.0 - momentum) * grad[i];", "check_momentum_closed_form"),
+    ("momentum steps along the gradient", "var[i] = var[i] - lr * accum[i];", "var[i] = var[i] - lr * grad[i];",
+     "check_momentum_geometric_sum"),
+    ("nesterov drops the momentum factor", "var[i] = var[i] - lr * (grad[i] + momentum * accum[i]);",
+     "var[i] = var[i] - lr * (grad[i] + accum[i]);", "check_nesterov_closed_form"),
+    ("adam skips the bias correction", "const double mhat = m[i] / c1, vhat = v[i] / c2;",
+     "const double mhat = m[i], vhat = v[i];", "check_adam_closed_form"),
+    ("adam second moment of |g|", "(1.0 - beta2) * grad[i] * grad[i];", "(1.0 - beta2) * fabs(grad[i]);",
+     "check_adam_weighted_sums"),
+    ("adam epsilon inside the root", "lr * mhat / (sqrt(vhat) + epsilon);", "lr * mhat / sqrt(vhat + epsilon);",
+     "check_adam_closed_form"),
     ("pool bwd drops beta", "if (!beta) memset(dx, 0, sizeof(double) * (size_t)nx);",
      "memset(dx, 0, sizeof(double) * (size_t)nx);", "check_pool_bwd_beta"),
 ]
