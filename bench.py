@@ -107,6 +107,42 @@ def recorded_traffic(kind):
     return rec.get("bytes_per_launch", {}).get(kind)
 
 
+# Algorithmic HBM bytes per fp32 variable of each in-place update (reads + writes, the bf16
+# shadow of the new value included): SGD var,grad -> var; Momentum var,accum,grad -> var,accum;
+# Adam var,m,v,grad -> var,m,v.
+UPDATE_BYTES = {"sgd": 4 + 4 + 4 + 2, "momentum": 12 + 8 + 2, "adam": 16 + 12 + 2}
+
+
+def time_updates(torch, ops, n, reps=20):
+    """Average launch time of each update over n fp32 variables (HIP events on the current stream)."""
+    dev = "cuda"
+    g = torch.Generator(device=dev).manual_seed(5)
+    var = torch.randn(n, device=dev, generator=g)
+    grad = torch.randn(n, device=dev, generator=g) * 1e-3
+    s1, s2 = torch.zeros(n, device=dev), torch.zeros(n, device=dev)
+    sh = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    calls = {
+        "sgd": lambda t: ops.apply_sgd(var, grad, 1e-3, shadow=sh),
+        "momentum": lambda t: ops.apply_momentum(var, s1, grad, 1e-3, 0.9, shadow=sh),
+        "adam": lambda t: ops.apply_adam(var, s1, s2, grad, 1e-3, 0.9, 0.999, 1e-8, t, shadow=sh),
+    }
+    res = {}
+    for name, fn in calls.items():
+        for t in range(1, 4):
+            fn(t)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for t in range(4, 4 + reps):
+            fn(t)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        gbs = UPDATE_BYTES[name] * n / (us * 1e-6) / 1e9
+        res[name] = {"us": round(us, 2), "gbs": round(gbs, 1), "pct_hbm_peak": round(100 * gbs / PEAK_HBM_GBS, 1)}
+    del var, grad, s1, s2, sh
+    return res
+
+
 def conv_flops(net, op):
     n, oh, ow, _ = net.tensors[op.dst]
     cin = net.tensors[op.src][3]
@@ -174,6 +210,7 @@ def main():
         sys.exit(2)
 
     import torch
+    from paper_1605_08695_amd import ops
     from paper_1605_08695_amd import workloads as W
     from paper_1605_08695_amd.step import Replica
 
@@ -290,6 +327,12 @@ def main():
     ew_ms = sum(per_kind.get(k, 0.0) for k in ew_kinds) + per_kind.get("apply_sgd", 0.0)
     ew_gbs = (sum(ew_bytes.values()) + sgd_bytes) / (ew_ms * 1e-3) / 1e9
 
+    # ---------------------------------------------------------------- in-place updates alone
+    # over this network's variables and over 61.1M variables (AlexNet with its classifier)
+    updates = {"bytes_per_variable": UPDATE_BYTES,
+               "this_net": dict(n=rep.n_params, **time_updates(torch, ops, rep.n_params)),
+               "alexnet_with_classifier": dict(n=61_100_840, **time_updates(torch, ops, 61_100_840))}
+
     # ---------------------------------------------------------------- CPU baseline: the oracle
     cpu = None
     if not args.no_cpu_baseline:
@@ -348,6 +391,7 @@ def main():
                      "measured": "HIP events around each launch, every op alone on one stream",
                      "flop_per_launch": round(flops[dom] / n_dom)},
         "cpu_baseline": cpu,
+        "updates": updates,
     }
     print(json.dumps(out))
     print("per-layer ms:", json.dumps({"%s/%s" % k: round(v, 4) for k, v in sorted(per_layer.items())}),

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 5
+#define TFK_ABI_VERSION 6
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -286,6 +286,36 @@ TFK_API tfk_status tfk_apply_sgd(float *var, const float *grad, int64_t n, float
 TFK_API tfk_status tfk_apply_sgd_multi(int32_t count, float *const *vars, const float *const *grads,
                                const int64_t *ns, float lr, uint16_t *const *shadows,
                                void *stream);
+
+/* Momentum, in place (Section 4.1 lists it among the optimizers built from
+ * Variable updates: a per-parameter velocity accumulated over the gradients
+ * drives the update).  Velocity form of Sutskever et al. (2013), fp32:
+ *   accum[i] <- fma(momentum, accum[i], grad[i])
+ *   var[i]   <- fma(-lr, accum[i], var[i])                           nesterov = 0
+ *   var[i]   <- fma(-lr, fma(momentum, accum[i], grad[i]), var[i])   nesterov = 1
+ * (the second line uses the updated accum).  var_bf16 as in tfk_apply_sgd.
+ * Errors: n < 0 (SHAPE); lr or momentum not finite, nesterov not 0/1 (ARG);
+ * a NULL buffer with n > 0 (NULL); a buffer not aligned to its element
+ * (ALIGN); any two of var, accum, grad, var_bf16 overlapping (ALIAS).  n == 0 is a no-op. */
+TFK_API tfk_status tfk_apply_momentum(float *var, float *accum, const float *grad, int64_t n, float lr,
+                              float momentum, int32_t nesterov, uint16_t *var_bf16, void *stream);
+
+/* Adam, in place (Section 4.1 lists it; Kingma & Ba (2015), Algorithm 1), step
+ * t >= 1 of the moment estimates m and v, fp32:
+ *   m[i] <- beta1 m[i] + (1 - beta1) grad[i]
+ *   v[i] <- beta2 v[i] + (1 - beta2) grad[i]^2
+ *   var[i] <- var[i] - lr / (1 - beta1^t) * m[i] / (sqrt(v[i] / (1 - beta2^t)) + epsilon)
+ * The bias corrections 1 - beta^t are computed on the host in fp64 and folded
+ * into two fp32 scalars; the per-element arithmetic is fp32 with fma.
+ * var_bf16 as in tfk_apply_sgd.  Start from m = v = 0 at t = 1.
+ * Errors: n < 0 (SHAPE); lr not finite, beta1 or beta2 outside [0, 1),
+ * epsilon negative or not finite, t < 1 (ARG); a bias-corrected scalar that
+ * overflows fp32 (OVERFLOW); a NULL buffer with n > 0 (NULL); a buffer not
+ * aligned to its element (ALIGN); any two of var, m, v, grad, var_bf16
+ * overlapping (ALIAS).  n == 0 is a no-op. */
+TFK_API tfk_status tfk_apply_adam(float *var, float *m, float *v, const float *grad, int64_t n, float lr,
+                          float beta1, float beta2, float epsilon, int64_t t, uint16_t *var_bf16,
+                          void *stream);
 
 /* ---------------------------------------------------------------- misc */
 TFK_API const char *tfk_status_string(tfk_status s);

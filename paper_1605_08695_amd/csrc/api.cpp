@@ -561,4 +561,65 @@ tfk_status tfk_apply_sgd_multi(int32_t count, float *const *vars, const float *c
     return ok();
 }
 
+// ------------------------------------------------------------------ Momentum, Adam
+static tfk_status check_slots(float *var, const float *grad, const float *s1, const float *s2, int64_t n,
+                              uint16_t *sh, const char *n1, const char *n2) {
+    if (n < 0) return fail(TFK_ERR_SHAPE, "n must be >= 0");
+    if (n == 0) return TFK_OK;
+    TRY(need_ptr(var, "var"));
+    TRY(need_ptr(grad, "grad"));
+    TRY(need_ptr(s1, n1));
+    if (n2) TRY(need_ptr(s2, n2));
+    TRY(need_align(var, 4, "var"));
+    TRY(need_align(grad, 4, "grad"));
+    TRY(need_align(s1, 4, n1));
+    if (n2) TRY(need_align(s2, 4, n2));
+    TRY(need_align(sh, 2, "var_bf16"));
+    if (n > ((int64_t)1 << 40)) return fail(TFK_ERR_OVERFLOW, "n too large");
+    const void *p[5] = {var, grad, s1, n2 ? s2 : nullptr, sh};
+    const int64_t b[5] = {n * 4, n * 4, n * 4, n * 4, n * 2};
+    for (int i = 0; i < 5; ++i)
+        for (int j = i + 1; j < 5; ++j)
+            if (overlap(p[i], b[i], p[j], b[j]))
+                return fail(TFK_ERR_ALIAS, "var, grad, %s%s%s and var_bf16 must not overlap", n1, n2 ? ", " : "",
+                            n2 ? n2 : "");
+    return TFK_OK;
+}
+
+tfk_status tfk_apply_momentum(float *var, float *accum, const float *grad, int64_t n, float lr, float momentum,
+                              int32_t nesterov, uint16_t *var_bf16, void *stream) {
+    if (!isfinite(lr)) return fail(TFK_ERR_ARG, "lr must be finite");
+    if (!isfinite(momentum)) return fail(TFK_ERR_ARG, "momentum must be finite");
+    if (nesterov != 0 && nesterov != 1) return fail(TFK_ERR_ARG, "nesterov must be 0 or 1");
+    TRY(check_slots(var, grad, accum, nullptr, n, var_bf16, "accum", nullptr));
+    if (n == 0) return ok();
+    OptParams p{};
+    p.lr = lr;
+    p.mom = momentum;
+    return hip_status(launch_opt(nesterov ? 1 : 0, var, accum, nullptr, grad, n, p, var_bf16, (hipStream_t)stream),
+                      "apply_momentum");
+}
+
+tfk_status tfk_apply_adam(float *var, float *m, float *v, const float *grad, int64_t n, float lr, float beta1,
+                          float beta2, float epsilon, int64_t t, uint16_t *var_bf16, void *stream) {
+    if (!isfinite(lr)) return fail(TFK_ERR_ARG, "lr must be finite");
+    if (!(beta1 >= 0.f && beta1 < 1.f)) return fail(TFK_ERR_ARG, "beta1 must be in [0, 1)");
+    if (!(beta2 >= 0.f && beta2 < 1.f)) return fail(TFK_ERR_ARG, "beta2 must be in [0, 1)");
+    if (!(epsilon >= 0.f) || !isfinite(epsilon)) return fail(TFK_ERR_ARG, "epsilon must be finite and >= 0");
+    if (t < 1) return fail(TFK_ERR_ARG, "t must be >= 1");
+    TRY(check_slots(var, grad, m, v, n, var_bf16, "m", "v"));
+    if (n == 0) return ok();
+    const double c1 = 1.0 - pow((double)beta1, (double)t), c2 = 1.0 - pow((double)beta2, (double)t);
+    OptParams p{};
+    p.lr = (float)((double)lr / c1);
+    p.b1 = beta1;
+    p.omb1 = (float)(1.0 - (double)beta1);
+    p.b2 = beta2;
+    p.omb2 = (float)(1.0 - (double)beta2);
+    p.rc2 = (float)(1.0 / c2);
+    p.eps = epsilon;
+    if (!isfinite(p.lr) || !isfinite(p.rc2)) return fail(TFK_ERR_OVERFLOW, "bias-corrected step overflows fp32");
+    return hip_status(launch_opt(2, var, m, v, grad, n, p, var_bf16, (hipStream_t)stream), "apply_adam");
+}
+
 }  // extern "C"

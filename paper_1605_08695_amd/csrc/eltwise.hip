@@ -725,6 +725,65 @@ __global__ __launch_bounds__(256) void sgd_multi_kernel(SgdBatch b, float lr) {
     }
 }
 
+// ------------------------------------------------------------------ Momentum, Adam
+// Both keep the SGD kernel's shape: one pass over the flat variable, float4 loads and stores of
+// every operand when all are 16-byte aligned, the optional bf16 shadow written beside the var.
+// KIND 0: Momentum (s1 = velocity), 1: Momentum look-ahead form, 2: Adam (s1 = m, s2 = v).
+template <int KIND>
+__device__ __forceinline__ float opt_elem(float var, float &s1, float &s2, float g, const OptParams &p) {
+    if (KIND == 2) {
+        const float m = fmaf(p.b1, s1, p.omb1 * g);
+        const float v = fmaf(p.b2, s2, (p.omb2 * g) * g);
+        s1 = m;
+        s2 = v;
+        const float den = sqrtf(v * p.rc2) + p.eps;
+        return fmaf(-p.lr, m / den, var);
+    }
+    const float a = fmaf(p.mom, s1, g);
+    s1 = a;
+    return fmaf(-p.lr, KIND == 1 ? fmaf(p.mom, a, g) : a, var);
+}
+
+template <int KIND>
+__global__ __launch_bounds__(256) void opt_kernel(float *__restrict__ var, float *__restrict__ s1,
+                                                  float *__restrict__ s2, const float *__restrict__ grad,
+                                                  int64_t n, OptParams p, uint16_t *__restrict__ sh, bool vec) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t tail = 0;
+    if (vec) {
+        const int64_t n4 = n / 4;
+        tail = n4 * 4;
+        for (int64_t t = t0; t < n4; t += stride) {
+            float4 v = reinterpret_cast<const float4 *>(var)[t];
+            float4 a = reinterpret_cast<const float4 *>(s1)[t];
+            float4 b = KIND == 2 ? reinterpret_cast<const float4 *>(s2)[t] : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float4 g = reinterpret_cast<const float4 *>(grad)[t];
+            v.x = opt_elem<KIND>(v.x, a.x, b.x, g.x, p);
+            v.y = opt_elem<KIND>(v.y, a.y, b.y, g.y, p);
+            v.z = opt_elem<KIND>(v.z, a.z, b.z, g.z, p);
+            v.w = opt_elem<KIND>(v.w, a.w, b.w, g.w, p);
+            reinterpret_cast<float4 *>(var)[t] = v;
+            reinterpret_cast<float4 *>(s1)[t] = a;
+            if (KIND == 2) reinterpret_cast<float4 *>(s2)[t] = b;
+            if (sh) {
+                uint2 q;
+                q.x = pack_bf16x2(v.x, v.y);
+                q.y = pack_bf16x2(v.z, v.w);
+                reinterpret_cast<uint2 *>(sh)[t] = q;
+            }
+        }
+    }
+    for (int64_t i = tail + t0; i < n; i += stride) {
+        float a = s1[i], b = KIND == 2 ? s2[i] : 0.f;
+        const float v = opt_elem<KIND>(var[i], a, b, grad[i], p);
+        var[i] = v;
+        s1[i] = a;
+        if (KIND == 2) s2[i] = b;
+        if (sh) sh[i] = (uint16_t)f32_to_bf16(v);
+    }
+}
+
 // ------------------------------------------------------------------ split-K sum / zero fill
 // The split partials part[s][i] (s < splits, i < mn) are summed in a fixed order that depends
 // only on the shape.  Large gradients: one pass, split order (sum_splits_direct_kernel).
@@ -964,6 +1023,20 @@ hipError_t launch_sgd(float *var, const float *grad, int64_t n, float lr, uint16
     const bool vec = aligned16(var) && aligned16(grad) && (sh == nullptr || ((uintptr_t)sh & 7) == 0);
     const int grid = grid_for(vec ? (n + 3) / 4 : n, 256, 8192);
     hipLaunchKernelGGL(sgd_kernel, dim3(grid), dim3(256), 0, st, var, grad, n, lr, sh, vec);
+    return hipGetLastError();
+}
+
+hipError_t launch_opt(int kind, float *var, float *s1, float *s2, const float *grad, int64_t n, const OptParams &p,
+                      uint16_t *sh, hipStream_t st) {
+    const bool vec = aligned16(var) && aligned16(s1) && (kind != 2 || aligned16(s2)) && aligned16(grad) &&
+                     (sh == nullptr || ((uintptr_t)sh & 7) == 0);
+    const int grid = grid_for(vec ? (n + 3) / 4 : n, 256, 8192);
+    switch (kind) {
+        case 0: hipLaunchKernelGGL(opt_kernel<0>, dim3(grid), dim3(256), 0, st, var, s1, s2, grad, n, p, sh, vec); break;
+        case 1: hipLaunchKernelGGL(opt_kernel<1>, dim3(grid), dim3(256), 0, st, var, s1, s2, grad, n, p, sh, vec); break;
+        case 2: hipLaunchKernelGGL(opt_kernel<2>, dim3(grid), dim3(256), 0, st, var, s1, s2, grad, n, p, sh, vec); break;
+        default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

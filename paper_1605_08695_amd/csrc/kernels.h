@@ -22,6 +22,12 @@ struct PoolGeom {
     int64_t xs, ys;      // pixel strides of x (dx) and y (dy)
 };
 
+// Scalars of the Momentum and Adam updates, rounded to fp32 on the host.  Adam's bias
+// corrections are folded in: lr = lr / (1 - b1^t), rc2 = 1 / (1 - b2^t).
+struct OptParams {
+    float lr, mom, b1, omb1, b2, omb2, rc2, eps;
+};
+
 constexpr int kSgdBatch = 16;
 struct SgdBatch {
     int count;
@@ -83,6 +89,9 @@ hipError_t launch_maxpool_relu_bwd(int dt, const void *dy, const void *am, bool 
                                    const void *y, void *dpre, float beta, float *db, float *ws, hipStream_t st);
 hipError_t launch_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh, hipStream_t st);
 hipError_t launch_sgd_multi(const SgdBatch &b, float lr, hipStream_t st);
+// Momentum (kind 0, 1 = look-ahead form) and Adam (kind 2) in place over n fp32 elements.
+hipError_t launch_opt(int kind, float *var, float *s1, float *s2, const float *grad, int64_t n, const OptParams &p,
+                      uint16_t *sh, hipStream_t st);
 // Sums split-K partials part[splits][mn] into out; part (workspace) is overwritten.
 hipError_t launch_sum_splits(float *part, int splits, int64_t mn, float *out, hipStream_t st);
 hipError_t launch_fill_zero(float *out, int64_t n, hipStream_t st);

@@ -17,7 +17,7 @@ from ._lib import Nhwc, TfkError, Window, TFK_BF16, TFK_F32, check, load
 
 __all__ = ["conv2d_fwd", "conv2d_fwd_bias_relu", "conv2d_bwd_input", "conv2d_bwd_filter", "conv2d_workspace_bytes", "bias_relu_fwd",
            "bias_relu_bwd", "bias_relu_bwd_workspace_bytes", "maxpool_fwd", "maxpool_bwd", "maxpool_bwd_relu_bwd", "apply_sgd",
-           "apply_sgd_multi", "out_len", "nhwc", "window", "TfkError", "abi_version"]
+           "apply_sgd_multi", "apply_momentum", "apply_adam", "out_len", "nhwc", "window", "TfkError", "abi_version"]
 
 
 def _dt(t: torch.Tensor) -> int:
@@ -258,6 +258,34 @@ def apply_sgd(var, grad, lr, shadow=None, stream=None):
                                or not shadow.is_contiguous()):
         raise ValueError("shadow must be a contiguous bfloat16 tensor of var's size")
     check(load().tfk_apply_sgd(_ptr(var), _ptr(grad), var.numel(), float(lr), _ptr(shadow), _stream(stream)))
+    return var
+
+
+def _check_update(var, grad, slots, shadow):
+    for t in (var, grad, *slots):
+        if t.dtype != torch.float32:
+            raise TypeError("var, grad and the optimizer slots are float32")
+        if not t.is_contiguous() or t.numel() != var.numel():
+            raise ValueError("var, grad and the optimizer slots must be contiguous with the same size")
+    if shadow is not None and (shadow.dtype != torch.bfloat16 or shadow.numel() != var.numel()
+                               or not shadow.is_contiguous()):
+        raise ValueError("shadow must be a contiguous bfloat16 tensor of var's size")
+
+
+def apply_momentum(var, accum, grad, lr, momentum, nesterov=False, shadow=None, stream=None):
+    """In place: accum <- momentum * accum + grad; var <- var - lr * accum (or, look-ahead form,
+    var <- var - lr * (grad + momentum * accum)); shadow (bf16) <- bf16(var) if given."""
+    _check_update(var, grad, (accum,), shadow)
+    check(load().tfk_apply_momentum(_ptr(var), _ptr(accum), _ptr(grad), var.numel(), float(lr), float(momentum),
+                                    int(bool(nesterov)), _ptr(shadow), _stream(stream)))
+    return var
+
+
+def apply_adam(var, m, v, grad, lr, beta1, beta2, epsilon, t, shadow=None, stream=None):
+    """In place, Adam step t >= 1: the moments m and v and var; shadow (bf16) <- bf16(var) if given."""
+    _check_update(var, grad, (m, v), shadow)
+    check(load().tfk_apply_adam(_ptr(var), _ptr(m), _ptr(v), _ptr(grad), var.numel(), float(lr), float(beta1),
+                                float(beta2), float(epsilon), int(t), _ptr(shadow), _stream(stream)))
     return var
 
 

@@ -48,8 +48,18 @@ def _align(n: int) -> int:
 class Replica:
     """Device state of one replica of ``net`` and its training step."""
 
-    def __init__(self, net: Net, inputs: Inputs, device: str = "cuda"):
+    def __init__(self, net: Net, inputs: Inputs, device: str = "cuda", optimizer: str = "sgd",
+                 momentum: float = 0.9, nesterov: bool = False, beta1: float = 0.9, beta2: float = 0.999,
+                 epsilon: float = 1e-8):
+        """``optimizer`` picks the in-place variable update that ends the step: "sgd"
+        (ApplyGradientDescent), "momentum" (velocity slot, optional look-ahead form) or "adam"
+        (two moment slots, bias-corrected by the step count)."""
+        if optimizer not in ("sgd", "momentum", "adam"):
+            raise ValueError("optimizer is 'sgd', 'momentum' or 'adam'")
         self.net = net
+        self.optimizer = optimizer
+        self.opt_args = dict(momentum=momentum, nesterov=bool(nesterov), beta1=beta1, beta2=beta2, epsilon=epsilon)
+        self.t = 0
         self.device = torch.device(device)
         self.dtype = torch.float32 if net.dtype == "f32" else torch.bfloat16
         self.lr = float(np.float32(net.lr))
@@ -67,6 +77,9 @@ class Replica:
         self.params = torch.zeros(off, dtype=torch.float32, device=dev)
         self.grads = torch.zeros(off, dtype=torch.float32, device=dev)
         self.shadow = torch.zeros(off, dtype=torch.bfloat16, device=dev) if dt == torch.bfloat16 else None
+        # optimizer slots (zero at the start of training), laid out like params
+        n_slots = {"sgd": 0, "momentum": 1, "adam": 2}[optimizer]
+        self.slots = [torch.zeros(off, dtype=torch.float32, device=dev) for _ in range(n_slots)]
         host = np.zeros(off, dtype=np.float32)
         for c in net.convs:
             wo, wshape, bo, bn = self._layout[c.name]
@@ -250,9 +263,22 @@ class Replica:
             cur.wait_stream(side)
 
     def update(self, trace=None, stream=None):
-        if trace: trace("apply_sgd", None, stream=stream, var=self.params, grad=self.grads)
-        ops.apply_sgd(self.params, self.grads, self.lr, shadow=self.shadow, stream=stream)
-        if trace: trace("apply_sgd:end", None, stream=stream, var=self.params)
+        a = self.opt_args
+        self.t += 1
+        if self.optimizer == "sgd":
+            if trace: trace("apply_sgd", None, stream=stream, var=self.params, grad=self.grads)
+            ops.apply_sgd(self.params, self.grads, self.lr, shadow=self.shadow, stream=stream)
+            if trace: trace("apply_sgd:end", None, stream=stream, var=self.params)
+        elif self.optimizer == "momentum":
+            if trace: trace("apply_momentum", None, stream=stream, var=self.params, grad=self.grads)
+            ops.apply_momentum(self.params, self.slots[0], self.grads, self.lr, a["momentum"], a["nesterov"],
+                               shadow=self.shadow, stream=stream)
+            if trace: trace("apply_momentum:end", None, stream=stream, var=self.params)
+        else:
+            if trace: trace("apply_adam", None, stream=stream, var=self.params, grad=self.grads)
+            ops.apply_adam(self.params, self.slots[0], self.slots[1], self.grads, self.lr, a["beta1"], a["beta2"],
+                           a["epsilon"], self.t, shadow=self.shadow, stream=stream)
+            if trace: trace("apply_adam:end", None, stream=stream, var=self.params)
 
     def step(self, trace=None, stream=None, concurrent=True):
         """One training step on ``stream``; the filter gradients overlap the rest of the
@@ -265,10 +291,15 @@ class Replica:
 
     # ------------------------------------------------------------------ state
     def snapshot(self):
-        """Copies of the variables (master and shadow), for restore-and-rerun checks."""
-        return (self.params.clone(), None if self.shadow is None else self.shadow.clone())
+        """Copies of the variables (master and shadow), the optimizer slots and the step count,
+        for restore-and-rerun checks."""
+        return (self.params.clone(), None if self.shadow is None else self.shadow.clone(),
+                [t.clone() for t in self.slots], self.t)
 
     def restore(self, snap):
         self.params.copy_(snap[0])
         if self.shadow is not None:
             self.shadow.copy_(snap[1])
+        for t, v in zip(self.slots, snap[2]):
+            t.copy_(v)
+        self.t = snap[3]

@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 5
+    assert lib.tfk_abi_version() == 6
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -198,6 +198,36 @@ def test_sgd_validation(lib):
                                  ctypes.c_float(0.01), None, None)
     assert st == ALIAS                                                 # second var == its grad
     assert b"tensor 1" in lib.tfk_last_error()
+
+
+def test_momentum_adam_validation(lib):
+    f = ctypes.c_float
+    mom = lambda var, acc, grad, n, lr=0.01, m=0.9, nest=0, sh=None: lib.tfk_apply_momentum(
+        vp(var), vp(acc), vp(grad), n, f(lr), f(m), nest, vp(sh) if sh else None, None)
+    assert mom(P, P + 0x1000, P + 0x2000, -1) == SHAPE
+    assert mom(P, P + 0x10, P + 0x2000, 100) == ALIAS                 # var overlaps accum
+    assert mom(P, P + 0x1000, P + 0x2000, 100, sh=P + 0x2010) == ALIAS  # shadow overlaps grad
+    assert mom(P, P + 0x1000, P + 0x2000, 10, lr=float("inf")) == ARG
+    assert mom(P, P + 0x1000, P + 0x2000, 10, m=float("nan")) == ARG
+    assert mom(P, P + 0x1000, P + 0x2000, 10, nest=2) == ARG
+    assert mom(P, 0, P + 0x2000, 10) == NULL
+    assert mom(P, P + 0x1002, P + 0x2000, 10) == ALIGN
+    assert mom(0, 0, 0, 0) == OK                                       # empty: no pointers needed
+    adam = lambda var, m, v, grad, n, lr=0.01, b1=0.9, b2=0.999, eps=1e-8, t=1: lib.tfk_apply_adam(
+        vp(var), vp(m), vp(v), vp(grad), n, f(lr), f(b1), f(b2), f(eps), t, None, None)
+    args = (P, P + 0x1000, P + 0x2000, P + 0x3000)
+    assert adam(*args, -1) == SHAPE
+    assert adam(P, P + 0x1000, P + 0x1000, P + 0x3000, 16) == ALIAS    # m is v
+    assert adam(*args, 16, b1=1.0) == ARG
+    assert adam(*args, 16, b1=-0.1) == ARG
+    assert adam(*args, 16, b2=float("nan")) == ARG
+    assert adam(*args, 16, eps=-1.0) == ARG
+    assert adam(*args, 16, t=0) == ARG
+    assert adam(*args, 16, lr=float("nan")) == ARG
+    assert adam(P, P + 0x1000, 0, P + 0x3000, 16) == NULL
+    assert adam(P, P + 0x1000, P + 0x2001, P + 0x3000, 16) == ALIGN
+    assert adam(0, 0, 0, 0, 0) == OK
+    assert b"" != lib.tfk_status_string(ARG)
 
 
 def test_empty_batch_conv_fwd_is_noop(lib):

@@ -423,3 +423,107 @@ def test_apply_sgd_multi():
         assert ulp_diff_f32(v.cpu().numpy(), ref) <= 1
         if sh is not None:
             assert torch.equal(sh, v.to(torch.bfloat16))
+
+
+# ----------------------------------------------------------------------------- momentum, adam
+# Error bounds from the fp32 arithmetic of the kernels (u = 2^-24, the unit roundoff), against the
+# fp64 oracle fed the same fp32 inputs and the fp32-rounded scalars:
+#   velocity  fma(m, a, g)                one rounding                 0.5 ulp -> at most 1 ulp after fp32(ref)
+#   var       fma(-lr, s, var)            2u|var'| + lr * (error of s)
+#   Adam m    fma(b1, m, fl(fl(1-b1) g))  three roundings              4u (|m'| + (1-b1)|g|)
+#   Adam v    sum of non-negative terms                                8u |v'|
+#   Adam step lr/(1-b1^t) m / (sqrt(v/(1-b2^t)) + eps): about eight roundings on top of m's error
+U = 2.0 ** -24
+
+
+def _momentum_case(n, seed, offset=0):
+    rng = np.random.default_rng(seed)
+    mk = lambda scale: torch.from_numpy((rng.standard_normal(n + offset) * scale).astype(np.float32)).to(DEV)[offset:]
+    return mk(1.0), mk(0.5), mk(3.0)
+
+
+@pytest.mark.parametrize("nesterov", [False, True])
+@pytest.mark.parametrize("n,offset", [(1, 0), (1001, 0), (1003, 1), (2469696, 0)])
+def test_apply_momentum_matches_oracle(n, offset, nesterov):
+    say("momentum", n, offset, nesterov)
+    var, acc, g = _momentum_case(n, 40 + n % 7, offset)
+    v0, a0, g0 = (t.cpu().numpy().astype(np.float64) for t in (var, acc, g))
+    lr, mom = float(np.float32(0.01)), float(np.float32(0.9))
+    sh = torch.empty(n, dtype=torch.bfloat16, device=DEV)
+    ops.apply_momentum(var, acc, g, lr, mom, nesterov=nesterov, shadow=sh)
+    torch.cuda.synchronize()
+    rv, ra = oracle.apply_momentum(v0, a0, g0, lr, mom, nesterov)
+    assert ulp_diff_f32(acc.cpu().numpy(), ra) <= 1
+    s_mag = np.abs(g0) + 2 * mom * np.abs(ra) if nesterov else np.abs(ra)
+    tol = 2 * U * np.abs(rv) + lr * 4 * U * s_mag + 1e-38
+    d = np.abs(var.cpu().numpy().astype(np.float64) - rv)
+    assert np.all(d <= tol), float(np.max(d / tol))
+    assert torch.equal(sh, var.to(torch.bfloat16))
+
+
+def _adam_bounds(rv, rm, rvv, g0, lr, b1, b2, eps, t):
+    tol_m = 4 * U * (np.abs(rm) + (1 - b1) * np.abs(g0)) + 1e-38
+    tol_v = 8 * U * rvv + 1e-38
+    c1, c2 = 1 - b1 ** t, 1 - b2 ** t
+    den = np.sqrt(rvv / c2) + eps
+    step = lr / c1 * np.abs(rm) / den
+    tol_var = 2 * U * np.abs(rv) + 16 * U * step + lr / c1 * tol_m / den + 1e-38
+    return tol_m, tol_v, tol_var
+
+
+@pytest.mark.parametrize("t", [1, 2, 1000])
+@pytest.mark.parametrize("n,offset", [(1, 0), (1001, 0), (1003, 1), (2469696, 0)])
+def test_apply_adam_matches_oracle(n, offset, t):
+    say("adam", n, offset, t)
+    rng = np.random.default_rng(60 + t)
+    mk = lambda x: torch.from_numpy(x.astype(np.float32)).to(DEV)[offset:]
+    var = mk(rng.standard_normal(n + offset))
+    m = mk(rng.standard_normal(n + offset) * 0.1)
+    v = mk(np.abs(rng.standard_normal(n + offset)) * 0.01)
+    g = mk(rng.standard_normal(n + offset) * 0.2)
+    v0, m0, vv0, g0 = (x.cpu().numpy().astype(np.float64) for x in (var, m, v, g))
+    f = lambda x: float(np.float32(x))
+    lr, b1, b2, eps = f(0.001), f(0.9), f(0.999), f(1e-8)
+    sh = torch.empty(n, dtype=torch.bfloat16, device=DEV)
+    ops.apply_adam(var, m, v, g, lr, b1, b2, eps, t, shadow=sh)
+    torch.cuda.synchronize()
+    rv, rm, rvv = oracle.apply_adam(v0, m0, vv0, g0, lr, b1, b2, eps, t)
+    tol_m, tol_v, tol_var = _adam_bounds(rv, rm, rvv, g0, lr, b1, b2, eps, t)
+    for name, got, ref, tol in (("m", m, rm, tol_m), ("v", v, rvv, tol_v), ("var", var, rv, tol_var)):
+        d = np.abs(got.cpu().numpy().astype(np.float64) - ref)
+        assert np.all(d <= tol), (name, float(np.max(d / tol)))
+    assert torch.equal(sh, var.to(torch.bfloat16))
+
+
+def test_adam_and_momentum_steps_from_zero_state():
+    """Five steps from zero slots, the way a training loop starts, against five oracle steps."""
+    rng = np.random.default_rng(71)
+    n = 4099
+    gs = [rng.standard_normal(n).astype(np.float32) * 0.3 for _ in range(5)]
+    x0 = rng.standard_normal(n).astype(np.float32)
+    f = lambda x: float(np.float32(x))
+    var = torch.from_numpy(x0).to(DEV)
+    m, v = torch.zeros(n, device=DEV), torch.zeros(n, device=DEV)
+    rv, rm, rvv = x0.astype(np.float64), np.zeros(n), np.zeros(n)
+    for t, g in enumerate(gs, start=1):
+        ops.apply_adam(var, m, v, torch.from_numpy(g).to(DEV), f(0.01), f(0.9), f(0.999), f(1e-8), t)
+        rv, rm, rvv = oracle.apply_adam(rv, rm, rvv, g.astype(np.float64), f(0.01), f(0.9), f(0.999), f(1e-8), t)
+    torch.cuda.synchronize()
+    # each step adds its own rounding; the first-order error growth over 5 steps stays linear
+    _, _, tol = _adam_bounds(rv, rm, rvv, gs[-1].astype(np.float64), f(0.01), f(0.9), f(0.999), f(1e-8), 5)
+    d = np.abs(var.cpu().numpy().astype(np.float64) - rv)
+    assert np.all(d <= 5 * tol + 5 * 32 * U * f(0.01)), float(np.max(d))
+    var = torch.from_numpy(x0).to(DEV)
+    acc = torch.zeros(n, device=DEV)
+    rv, ra = x0.astype(np.float64), np.zeros(n)
+    for g in gs:
+        ops.apply_momentum(var, acc, torch.from_numpy(g).to(DEV), f(0.01), f(0.9), nesterov=True)
+        rv, ra = oracle.apply_momentum(rv, ra, g.astype(np.float64), f(0.01), f(0.9), True)
+    torch.cuda.synchronize()
+    bound = 5 * (2 * U * np.abs(rv) + 0.01 * 16 * U * (np.abs(ra) * 6 + 2.0))
+    assert np.all(np.abs(var.cpu().numpy().astype(np.float64) - rv) <= bound)
+    # the velocity is a signed sum over the steps: each step's rounding (at most u times the
+    # magnitudes it adds) is carried forward, so the bound is absolute, not in ulps of the result
+    gmax = max(float(np.max(np.abs(g))) for g in gs)
+    vbound = 5 * 2 * U * (np.abs(ra) + 5 * gmax)
+    assert np.all(np.abs(acc.cpu().numpy().astype(np.float64) - ra) <= vbound)

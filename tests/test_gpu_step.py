@@ -62,11 +62,54 @@ def test_single_layer_step_end_to_end():
         win = np.sort(y[n, 2 * oh:2 * oh + 2, 2 * ow:2 * ow + 2, ch].ravel())
         assert win[-1] - win[-2] <= 1e-5 * rms
     say("  argmax mismatches (near-ties only):", len(mism))
-    # the update, given the GPU's own gradients: within 1 ulp of the fp64 rule
+    # the updated variables against the oracle's: the fp32 rounding of the update plus lr times
+    # the gradient bar (the replica starts from the fp32 values of the weights)
     lr = float(np.float32(net.lr))
-    w0 = inp.weights[c].astype(np.float32).astype(np.float64)     # the replica's fp32 start
-    w_new = oracle.apply_sgd(w0, f64(rep.dW[c]), lr)
-    assert ulp_diff_f32(rep.W[c].cpu().numpy(), w_new) <= 1
+    w0 = inp.weights[c].astype(np.float32).astype(np.float64)
+    dw_ref = ref["dW"][c]
+    w_ref = oracle.apply_sgd(w0, dw_ref, lr)
+    tol = 2.0 ** -23 * np.abs(w_ref) + lr * 1e-4 * np.sqrt(np.mean(dw_ref ** 2))
+    assert np.all(np.abs(f64(rep.W[c]) - w_ref) <= tol)
+
+
+@pytest.mark.parametrize("opt", ["momentum", "nesterov", "adam"])
+def test_single_layer_steps_with_momentum_and_adam(opt):
+    """Two fp32 single-layer steps with a Momentum or Adam update against the oracle's two steps
+    (forward, backward, then the same update rule), from zero optimizer slots."""
+    say("optimizer step", opt)
+    net = W.single_layer(batch=4, hw=16)
+    inp = W.make_inputs(net, seed=4)
+    c = net.convs[0].name
+    lr = float(np.float32(net.lr))
+    f = lambda v: float(np.float32(v))
+    g1 = onet.step(net, inp.x, inp.weights, inp.biases, inp.g)
+    # Adam's step is nearly sign(g) when eps is tiny; an eps of the gradient's size keeps the
+    # update Lipschitz in the gradient, so the gradient bar carries over to the variables
+    eps = f(max(np.sqrt(np.mean(g1["dW"][c] ** 2)), np.sqrt(np.mean(g1["db"][c] ** 2))))
+    kw = dict(momentum=f(0.9), nesterov=(opt == "nesterov"), beta1=f(0.9), beta2=f(0.999), epsilon=eps)
+    rep = Replica(net, inp, optimizer="adam" if opt == "adam" else "momentum", **kw)
+    w = {c: inp.weights[c].astype(np.float32).astype(np.float64)}
+    b = {c: inp.biases[c].astype(np.float32).astype(np.float64)}
+    slots = {k: [np.zeros_like(w[c]), np.zeros_like(w[c])] if k == "w" else [np.zeros_like(b[c])] * 2
+             for k in ("w", "b")}
+    for t in (1, 2):
+        rep.step()
+        ref = onet.step(net, inp.x, w, b, inp.g)
+        for key, var, grad in (("w", w, ref["dW"][c]), ("b", b, ref["db"][c])):
+            s0 = slots[key]
+            if opt == "adam":
+                var[c], s0[0], s0[1] = oracle.apply_adam(var[c], s0[0], s0[1], grad, lr, kw["beta1"], kw["beta2"],
+                                                         eps, t)
+            else:
+                var[c], s0[0] = oracle.apply_momentum(var[c], s0[0], grad, lr, kw["momentum"], kw["nesterov"])
+    torch.cuda.synchronize()
+    w0 = inp.weights[c].astype(np.float32).astype(np.float64)
+    b0 = inp.biases[c].astype(np.float32).astype(np.float64)
+    e_w = err(f64(rep.W[c]) - w0, w[c] - w0)
+    e_b = err(f64(rep.b[c]) - b0, b[c] - b0)
+    say("  variable change err: W %.2e  b %.2e" % (e_w, e_b))
+    assert e_w <= 1e-3 and e_b <= 1e-3, (e_w, e_b)
+    assert rep.t == 2
 
 
 SMALL = [
