@@ -24,8 +24,11 @@ Gates:
 Argmax indices and max-pool values must match exactly.  SGD results must be
 within 1 ulp of the fp32 rounding of the fp64 oracle.
 
-Comparisons are teacher-forced: the oracle receives the exact values the GPU
-op consumed (bf16 widened to fp64), so kernel error is isolated from the
+Whole-step comparisons are oracle-forced: the oracle runs the step op by op on
+the seeded inputs, and before each GPU op the harness overwrites that op's
+input buffers with the oracle's values, rounded to the buffer's storage type;
+the oracle op then runs on the same rounded values.  Values flow only from the
+oracle to the GPU, never back, and each kernel's error is isolated from the
 compounding of bf16 storage across layers.
 """
 from __future__ import annotations
@@ -106,40 +109,120 @@ def say(*args):
 
 
 class ParityTracer:
-    """Step-driver hook: snapshots each op's inputs, then checks its outputs.
+    """Step-driver hook that forces every op's inputs from the oracle and checks its outputs.
 
-    ``sample_images``: None checks whole tensors; a list of image indices checks
-    only those images (outputs of every op but the filter/bias gradients depend
-    on one image each) and evaluates ``filter_samples`` filter-gradient entries
-    through the oracle's sampled entry point.
+    ``rep`` is the Replica being stepped and ``inputs`` its seeded inputs.  With ``distinct``
+    set, the oracle runs on the first ``distinct`` images only and every input buffer holds
+    those images repeated along the batch (the batch must be a multiple): the GPU runs the
+    full-size step in its own launch configuration, per-image outputs are checked on the
+    distinct images (and must repeat bit for bit), and batch sums (filter and bias
+    gradients) are the oracle's sums times the repeat count.
     """
 
-    def __init__(self, dtype, sample_images=None, filter_samples=256, seed=0, label=""):
-        self.dtype = dtype
-        self.bar = BAR[dtype]
-        self.sample = sample_images
-        self.filter_samples = filter_samples
-        self.rng = np.random.default_rng(seed)
+    def __init__(self, rep, inputs, distinct=None, label=""):
+        self.rep = rep
+        self.dtype = rep.dtype
+        self.bar = BAR[rep.dtype]
+        n = inputs.x.shape[0]
+        self.k = n if distinct is None else distinct
+        assert n % self.k == 0
+        self.tile = n // self.k
+        self.label = label
+        self.lr = rep.lr
         self.pending = None
         self.results = []           # (kind, op name, metric, value, bar, ok)
-        self.label = label
+        net, k = rep.net, self.k
+        self.state = {("act", "x"): np.asarray(inputs.x[:k], np.float64),
+                      ("grad", net.output): np.asarray(inputs.g[:k], np.float64)}
+        for c in net.convs:
+            self.state[("W", c.name)] = np.asarray(inputs.weights[c.name], np.float64)
+            self.state[("b", c.name)] = np.asarray(inputs.biases[c.name], np.float64)
+        # every buffer an op reads or writes, under the oracle state key that mirrors it;
+        # NHWC batch buffers may be viewed as channel slices, the variables only whole
+        self.batched = [(("act", nm), t) for nm, t in rep.act.items()]
+        self.batched += [(("grad", nm), t) for nm, t in rep.grad.items()]
+        self.batched += [(("dpre_out",), rep.dpre_out)]
+        self.whole = [(("W", nm), t) for nm, t in rep.Wlp.items()]
+        self.whole += [(("b", nm), t) for nm, t in rep.b.items()]
+        self.whole += [(("dW", nm), t) for nm, t in rep.dW.items()]
+        self.whole += [(("db", nm), t) for nm, t in rep.db.items()]
 
-    # -------------------------------------------------------------- helpers
-    def _imgs(self, a: np.ndarray) -> np.ndarray:
-        return a if self.sample is None else a[self.sample]
+    # -------------------------------------------------------------- buffers
+    def _lookup(self, t):
+        """(state key, first channel, buffer shape) of the buffer t views: a channel slice of an
+        NHWC batch buffer, or a whole variable (first channel None)."""
+        p, es = t.data_ptr(), t.element_size()
+        for key, b in self.whole:
+            if b.dtype == t.dtype and p == b.data_ptr() and tuple(t.shape) == tuple(b.shape):
+                return key, None, tuple(b.shape)
+        for key, b in self.batched:
+            off = p - b.data_ptr()
+            if b.dtype != t.dtype or t.dim() != 4 or off < 0 or off % es:
+                continue
+            c0 = off // es
+            if (tuple(t.shape[:3]) == tuple(b.shape[:3]) and c0 + t.shape[3] <= b.shape[3]
+                    and t.stride() == b.stride()):
+                return key, c0, tuple(b.shape)
+        raise KeyError("tensor at %#x %s is none of the replica's buffers" % (p, tuple(t.shape)))
 
-    def _x64(self, t: torch.Tensor) -> np.ndarray:
-        if self.sample is None:
-            return f64(t)
-        idx = torch.tensor(self.sample, device=t.device)
-        return f64(t.index_select(0, idx))
+    def _get(self, t):
+        key, c0, _ = self._lookup(t)
+        v = self.state[key]
+        return v if c0 is None else v[..., c0:c0 + t.shape[3]]
 
-    def _index_shift(self, x_shape):
-        """Argmax indices of image sample[j] in the full batch minus those of image j of the slice."""
-        n, h, w, c = x_shape
-        j = np.arange(len(self.sample))
-        return ((np.asarray(self.sample) - j) * (h * w * c))[:, None, None, None]
+    def _set(self, t, v):
+        key, c0, shape = self._lookup(t)
+        if c0 is None:
+            self.state[key] = np.array(v, np.float64)
+            return
+        if key not in self.state:
+            self.state[key] = np.zeros((self.k,) + shape[1:])
+        self.state[key][..., c0:c0 + t.shape[3]] = v
 
+    def _round(self, v, dtype):
+        return torch.from_numpy(np.ascontiguousarray(v)).to(dtype)
+
+    def _write(self, t, r, batched):
+        """Copy host tensor r into t; a batch tensor of k images is repeated along the batch."""
+        if batched and self.tile > 1:
+            r = r.repeat(self.tile, 1, 1, 1)
+        t.copy_(r.to(t.device))
+
+    def _force(self, t):
+        """Overwrite t with the oracle's value of its buffer rounded to t's type; returns the
+        rounded value (k images for a batch tensor) in fp64."""
+        r = self._round(self._get(t), t.dtype)
+        self._write(t, r, self._lookup(t)[1] is not None)
+        return r.to(torch.float64).numpy()
+
+    def _force_argmax(self, t, op, x_shape):
+        """Overwrite a pool's selection buffer with the oracle's (dense indices into the k-image
+        input), in the buffer's format: uint8 window taps or int32 dense indices."""
+        dense = self.state[("argmax", op.name)].astype(np.int64)
+        _, H, W, C = x_shape
+        if t.dtype == torch.uint8:
+            n, oh, ow, c = np.indices(dense.shape)
+            h = dense // (W * C) % H
+            w = dense // C % W
+            taps = (h - (oh * op.sh - op.pads[0])) * op.kw + (w - (ow * op.sw - op.pads[2]))
+            assert np.all((taps >= 0) & (taps < op.kh * op.kw))
+            self._write(t, torch.from_numpy(taps.astype(np.uint8)), True)
+        else:
+            full = np.concatenate([dense + r * self.k * H * W * C for r in range(self.tile)])
+            t.copy_(torch.from_numpy(full.astype(np.int32)).to(t.device))
+        return dense
+
+    def _got(self, kind, name, t):
+        """GPU output of the k distinct images in fp64; with repeated images, checks that every
+        repeat of an image's output equals the first bit for bit."""
+        if t.dim() == 4 and self.tile > 1:
+            first = t[:self.k]
+            bad = sum(int((t[r * self.k:(r + 1) * self.k] != first).sum()) for r in range(1, self.tile))
+            self.record(kind, name, "repeat_mismatch", float(bad), 0.0)
+            t = first
+        return f64(t)
+
+    # -------------------------------------------------------------- results
     def record(self, kind, name, metric, value, bar):
         ok = value <= bar
         self.results.append((kind, name, metric, value, bar, ok))
@@ -166,36 +249,6 @@ class ParityTracer:
                 worst[key] = (value, bar, name, score)
         return worst
 
-    # -------------------------------------------------------------- hook
-    def __call__(self, event, op, **t):
-        if not event.endswith(":end"):
-            snap = {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in t.items()}
-            self.pending = (event, op, snap)
-            return
-        kind, op0, inp = self.pending
-        assert kind == event[:-4] and op0 is op
-        torch.cuda.synchronize()
-        getattr(self, "_check_" + kind)(op, inp, t)
-        self.pending = None
-
-    # -------------------------------------------------------------- checks
-    def _check_conv_fwd(self, op, inp, out):
-        ref = oracle.conv2d_fwd(self._x64(inp["x"]), f64(inp["w"]), (op.sh, op.sw), op.pads)
-        self.record_tensor("conv_fwd", op.name, self._x64(out["y"]), ref, self.dtype)
-
-    def _check_conv_bias_relu_fwd(self, op, inp, out):
-        pre = oracle.conv2d_fwd(self._x64(inp["x"]), f64(inp["w"]), (op.sh, op.sw), op.pads)
-        ref = oracle.bias_relu_fwd(pre, f64(inp["b"]))
-        y = self._x64(out["y"])
-        self.record_tensor("conv_bias_relu_fwd", op.name, y, ref, self.dtype)
-        self.record("conv_bias_relu_fwd", op.name, "negatives", float(np.sum(np.signbit(y))), 0.0)
-
-    def _check_bias_relu_fwd(self, op, inp, out):
-        ref = oracle.bias_relu_fwd(self._x64(inp["y"]), f64(inp["b"]))
-        y = self._x64(out["y"])
-        self.record_tensor("bias_relu_fwd", op.name, y, ref, self.dtype)
-        self.record("bias_relu_fwd", op.name, "negatives", float(np.sum(np.signbit(y))), 0.0)
-
     @staticmethod
     def _dense(argmax, x_shape, op):
         """A pool's selection as dense NHWC indices into its input: int32 argmax as stored, uint8
@@ -209,70 +262,143 @@ class ParityTracer:
         w = ow * op.sw - op.pads[2] + a % op.kw
         return ((n * H + h) * W + w) * C + c
 
-    def _check_maxpool_fwd(self, op, inp, out):
-        x = self._x64(inp["x"])
-        ref, am = oracle.maxpool_fwd(x, (op.kh, op.kw), (op.sh, op.sw), op.pads)
-        got_am = self._dense(out["argmax"], inp["x"].shape, op)
-        if self.sample is not None:
-            got_am = got_am[self.sample] - self._index_shift(inp["x"].shape)
-        self.record("maxpool_fwd", op.name, "err", err(self._x64(out["y"]), ref), 0.0)
+    # -------------------------------------------------------------- hook
+    def __call__(self, event, op, stream=None, **t):
+        torch.cuda.synchronize()
+        if not event.endswith(":end"):
+            used = getattr(self, "_force_" + event)(op, t)
+            torch.cuda.synchronize()
+            self.pending = (event, op, used)
+            return
+        kind, op0, used = self.pending
+        assert kind == event[:-4] and op0 is op
+        getattr(self, "_check_" + kind)(op, used, t)
+        self.pending = None
+
+    # -------------------------------------------------------------- forward
+    def _force_conv_bias_relu_fwd(self, op, t):
+        return {"x": self._force(t["x"]), "w": self._force(t["w"]), "b": self._force(t["b"])}
+
+    def _check_conv_bias_relu_fwd(self, op, u, out):
+        pre = oracle.conv2d_fwd(u["x"], u["w"], (op.sh, op.sw), op.pads)
+        ref = oracle.bias_relu_fwd(pre, u["b"])
+        y = self._got("conv_bias_relu_fwd", op.name, out["y"])
+        self.record_tensor("conv_bias_relu_fwd", op.name, y, ref, self.dtype)
+        self.record("conv_bias_relu_fwd", op.name, "negatives", float(np.sum(np.signbit(y))), 0.0)
+        self._set(out["y"], ref)
+
+    def _force_maxpool_fwd(self, op, t):
+        return {"x": self._force(t["x"]), "x_shape": tuple(t["x"].shape)}
+
+    def _check_maxpool_fwd(self, op, u, out):
+        ref, am = oracle.maxpool_fwd(u["x"], (op.kh, op.kw), (op.sh, op.sw), op.pads)
+        y = self._got("maxpool_fwd", op.name, out["y"])
+        got_am = self._dense(out["argmax"][:self.k], (self.k,) + u["x_shape"][1:], op)
+        self.record("maxpool_fwd", op.name, "err", err(y, ref), 0.0)
         self.record("maxpool_fwd", op.name, "argmax_mismatch", float(np.sum(got_am != am)), 0.0)
+        if out["argmax"].dtype == torch.uint8:          # (dense indices differ by the image offset)
+            self._got("maxpool_fwd:argmax", op.name, out["argmax"])
+        self._set(out["y"], ref)
+        self.state[("argmax", op.name)] = am
 
-    def _check_bias_relu_bwd(self, op, inp, out):
-        y, dy = f64(inp["y"]), f64(inp["dy"])
-        ref_dpre, ref_db = oracle.bias_relu_bwd(y, dy)
-        self.record("bias_relu_bwd", op.name, "dpre_mismatch", float(np.sum(f64(out["dpre"]) != ref_dpre)), 0.0)
-        self.record_tensor("bias_relu_bwd:db", op.name, f64(out["db"]), ref_db, torch.float32)
+    # -------------------------------------------------------------- backward
+    def _force_bias_relu_bwd(self, op, t):
+        return {"y": self._force(t["y"]), "dy": self._force(t["dy"])}
 
-    def _check_conv_bwd_filter(self, op, inp, out):
-        dw = f64(out["dw"])
-        if self.sample is None:
-            ref = oracle.conv2d_bwd_filter(f64(inp["x"]), f64(inp["dy"]), (op.kh, op.kw), (op.sh, op.sw), op.pads)
-            self.record_tensor("conv_bwd_filter", op.name, dw, ref, torch.float32)
-        else:
-            idx = self.rng.integers(0, dw.size, size=min(self.filter_samples, dw.size))
-            ref = oracle.conv2d_bwd_filter_at(f64(inp["x"]), f64(inp["dy"]), (op.kh, op.kw), (op.sh, op.sw),
-                                              op.pads, idx)
-            self.record_tensor("conv_bwd_filter:sampled", op.name, dw.ravel()[idx], ref, torch.float32)
+    def _check_bias_relu_bwd(self, op, u, out):
+        ref_dpre, ref_db = oracle.bias_relu_bwd(u["y"], u["dy"])
+        dpre = self._got("bias_relu_bwd", op.name, out["dpre"])
+        self.record("bias_relu_bwd", op.name, "dpre_mismatch", float(np.sum(dpre != ref_dpre)), 0.0)
+        self.record_tensor("bias_relu_bwd:db", op.name, f64(out["db"]), ref_db * self.tile, torch.float32)
+        self._set(out["dpre"], ref_dpre)
+        self._set(out["db"], ref_db * self.tile)
 
-    def _check_conv_bwd_input(self, op, inp, out):
-        dy = self._x64(inp["dy"])
-        dx_old = self._x64(inp["dx"])
-        ref = oracle.conv2d_bwd_input(dy, f64(inp["w"]), dx_old.shape, (op.sh, op.sw), op.pads,
-                                      dx=dx_old, beta=inp["beta"])
-        self.record_tensor("conv_bwd_input", op.name, self._x64(out["dx"]), ref, self.dtype)
+    def _force_conv_bwd_filter(self, op, t):
+        return {"x": self._force(t["x"]), "dy": self._force(t["dy"])}
 
-    def _check_conv_bwd_input_relu_bwd(self, op, inp, out):
+    def _check_conv_bwd_filter(self, op, u, out):
+        ref = oracle.conv2d_bwd_filter(u["x"], u["dy"], (op.kh, op.kw), (op.sh, op.sw), op.pads) * self.tile
+        self.record_tensor("conv_bwd_filter", op.name, f64(out["dw"]), ref, torch.float32)
+        self._set(out["dw"], ref)
+
+    def _force_conv_bwd_input(self, op, t):
+        u = {"dy": self._force(t["dy"]), "w": self._force(t["w"]), "beta": t["beta"],
+             "dx_shape": (self.k,) + tuple(t["dx"].shape[1:])}
+        u["dx"] = self._force(t["dx"]) if t["beta"] else None
+        return u
+
+    def _check_conv_bwd_input(self, op, u, out):
+        ref = oracle.conv2d_bwd_input(u["dy"], u["w"], u["dx_shape"], (op.sh, op.sw), op.pads,
+                                      dx=u["dx"], beta=u["beta"])
+        self.record_tensor("conv_bwd_input", op.name, self._got("conv_bwd_input", op.name, out["dx"]), ref,
+                           self.dtype)
+        self._set(out["dx"], ref)
+
+    def _force_conv_bwd_input_relu_bwd(self, op, t):
+        return {"dy": self._force(t["dy"]), "w": self._force(t["w"]), "y": self._force(t["y"])}
+
+    def _check_conv_bwd_input_relu_bwd(self, op, u, out):
         # the input gradient of op fused with the ReLU backward of the layer that produced its input
-        dy, y = self._x64(inp["dy"]), self._x64(inp["y"])
-        g = oracle.conv2d_bwd_input(dy, f64(inp["w"]), y.shape, (op.sh, op.sw), op.pads)
-        ref_dpre, ref_db = oracle.bias_relu_bwd(y, g)
-        self.record_tensor("conv_bwd_input_relu_bwd", op.name, self._x64(out["dpre"]), ref_dpre, self.dtype)
-        if self.sample is None:              # (the bias gradient sums over every image)
-            self.record_tensor("conv_bwd_input_relu_bwd:db", op.name, f64(out["db"]), ref_db, torch.float32)
+        g = oracle.conv2d_bwd_input(u["dy"], u["w"], u["y"].shape, (op.sh, op.sw), op.pads)
+        ref_dpre, ref_db = oracle.bias_relu_bwd(u["y"], g)
+        got = self._got("conv_bwd_input_relu_bwd", op.name, out["dpre"])
+        self.record_tensor("conv_bwd_input_relu_bwd", op.name, got, ref_dpre, self.dtype)
+        self.record("conv_bwd_input_relu_bwd", op.name, "masked_nonzero", float(np.sum(got[u["y"] <= 0] != 0)), 0.0)
+        self.record_tensor("conv_bwd_input_relu_bwd:db", op.name, f64(out["db"]), ref_db * self.tile, torch.float32)
+        self._set(out["dpre"], ref_dpre)
+        self._set(out["db"], ref_db * self.tile)
 
-    def _check_maxpool_bwd(self, op, inp, out):
-        dy = self._x64(inp["dy"])
-        am = self._dense(inp["argmax"], inp["dx"].shape, op)
-        dx_old = self._x64(inp["dx"])
-        if self.sample is not None:
-            am = am[self.sample] - self._index_shift(inp["dx"].shape)
-        ref = oracle.maxpool_bwd(dy, am.astype(np.int32), dx_old.shape, dx=dx_old, beta=inp["beta"])
-        self.record_tensor("maxpool_bwd", op.name, self._x64(out["dx"]), ref, self.dtype)
+    def _force_maxpool_bwd(self, op, t):
+        x_shape = tuple(t["dx"].shape)
+        u = {"dy": self._force(t["dy"]), "am": self._force_argmax(t["argmax"], op, x_shape), "beta": t["beta"],
+             "dx_shape": (self.k,) + x_shape[1:]}
+        u["dx"] = self._force(t["dx"]) if t["beta"] else None
+        return u
 
-    def _check_maxpool_relu_bwd(self, op, inp, out):
-        # whole tensors: the bias gradient sums over every image
-        y = f64(inp["y"])
-        am = self._dense(inp["argmax"], inp["y"].shape, op).astype(np.int32)
-        dpre_old = f64(inp["dpre"])
-        g = oracle.maxpool_bwd(f64(inp["dy"]), am, y.shape, dx=dpre_old, beta=inp["beta"])
-        ref_dpre, ref_db = oracle.bias_relu_bwd(y, g)
-        self.record_tensor("maxpool_relu_bwd", op.name, f64(out["dpre"]), ref_dpre, self.dtype)
-        self.record_tensor("maxpool_relu_bwd:db", op.name, f64(out["db"]), ref_db, torch.float32)
+    def _check_maxpool_bwd(self, op, u, out):
+        ref = oracle.maxpool_bwd(u["dy"], u["am"].astype(np.int32), u["dx_shape"], dx=u["dx"], beta=u["beta"])
+        self.record_tensor("maxpool_bwd", op.name, self._got("maxpool_bwd", op.name, out["dx"]), ref, self.dtype)
+        self._set(out["dx"], ref)
 
-    def _check_apply_sgd(self, op, inp, out):
-        var, grad = inp["var"].cpu().numpy(), inp["grad"].cpu().numpy()
-        ref = oracle.apply_sgd(var.astype(np.float64), grad.astype(np.float64), self.lr)
+    def _force_maxpool_relu_bwd(self, op, t):
+        y_shape = tuple(t["y"].shape)
+        u = {"dy": self._force(t["dy"]), "am": self._force_argmax(t["argmax"], op, y_shape), "y": self._force(t["y"]),
+             "beta": t["beta"]}
+        u["dpre"] = self._force(t["dpre"]) if t["beta"] else None
+        return u
+
+    def _check_maxpool_relu_bwd(self, op, u, out):
+        g = oracle.maxpool_bwd(u["dy"], u["am"].astype(np.int32), u["y"].shape, dx=u["dpre"], beta=u["beta"])
+        ref_dpre, ref_db = oracle.bias_relu_bwd(u["y"], g)
+        got = self._got("maxpool_relu_bwd", op.name, out["dpre"])
+        self.record_tensor("maxpool_relu_bwd", op.name, got, ref_dpre, self.dtype)
+        self.record_tensor("maxpool_relu_bwd:db", op.name, f64(out["db"]), ref_db * self.tile, torch.float32)
+        self._set(out["dpre"], ref_dpre)
+        self._set(out["db"], ref_db * self.tile)
+
+    # -------------------------------------------------------------- update
+    def _flat(self, kind_w, kind_b, wdtype):
+        """The oracle's per-layer values laid out like the replica's flat variable buffer (fp32;
+        weights first rounded to wdtype, the type the step's convolutions read them in)."""
+        rep = self.rep
+        flat = np.zeros(rep.n_params, np.float64)
+        for c in rep.net.convs:
+            wo, wshape, bo, bn = rep._layout[c.name]
+            wv = self._round(self.state[(kind_w, c.name)], wdtype).to(torch.float32)
+            flat[wo:wo + int(np.prod(wshape))] = wv.to(torch.float64).numpy().ravel()
+            flat[bo:bo + bn] = self._round(self.state[(kind_b, c.name)], torch.float32).to(torch.float64).numpy()
+        return flat
+
+    def _force_apply_sgd(self, op, t):
+        var = self._flat("W", "b", self.dtype)
+        grad = self._flat("dW", "db", torch.float32)
+        t["var"].copy_(torch.from_numpy(var).to(torch.float32).to(t["var"].device))
+        t["grad"].copy_(torch.from_numpy(grad).to(torch.float32).to(t["grad"].device))
+        return {"var": var, "grad": grad}
+
+    def _check_apply_sgd(self, op, u, out):
+        ref = oracle.apply_sgd(u["var"], u["grad"], self.lr)
         self.record("apply_sgd", "all", "ulp", float(ulp_diff_f32(out["var"].cpu().numpy(), ref)), 1.0)
-
-    lr = 0.01
+        if self.rep.shadow is not None:
+            same = torch.equal(self.rep.shadow, out["var"].to(torch.bfloat16))
+            self.record("apply_sgd", "shadow", "mismatch", 0.0 if same else 1.0, 0.0)

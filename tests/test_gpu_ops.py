@@ -282,12 +282,15 @@ def test_bias_relu(dtype, shape, slice_):
     got = f64(y)
     assert_close(got, oracle.bias_relu_fwd(pre, f64(b)), dtype, label="bias_relu_fwd")
     assert not np.any(np.signbit(got))
+    # the backward on a seeded ReLU output (exact zeros where the mask is off)
+    y_in = torch.from_numpy(np.maximum(rng.standard_normal(y.shape), 0.0)).to(dtype)
+    y.copy_(y_in.to(DEV))
     dybuf = _mk(buf.shape, dtype, rng)
     dy = dybuf if slice_ is None else dybuf[..., slice_[0]:slice_[1]]
     dy0 = f64(dy)
     dpre, db = ops.bias_relu_bwd(y, dy, dpre=dy)          # in place
     torch.cuda.synchronize()
-    ref_dpre, ref_db = oracle.bias_relu_bwd(got, dy0)
+    ref_dpre, ref_db = oracle.bias_relu_bwd(f64(y_in), dy0)
     assert_close(f64(db), ref_db, torch.float32, dtype, label="db")
     # exact: masked entries are exactly zero, passed entries exactly dy
     assert np.array_equal(f64(dpre), ref_dpre)

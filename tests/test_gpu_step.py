@@ -1,10 +1,12 @@
 """Whole-step parity of the HIP path against the CPU oracle (GPU).
 
 * single-layer fp32 step end to end against the oracle's own step;
-* every op of every workload teacher-forced against the oracle, at reduced
-  batch (and, for VGG, reduced image size) so the oracle finishes in seconds;
+* single-layer fp32 steps with Momentum and Adam updates against the oracle's;
+* every op of every workload oracle-forced (its inputs overwritten with the
+  oracle's values before it runs), at reduced batch (and, for VGG, reduced
+  image size) so the oracle finishes in seconds;
 * the AlexNet-shaped step at its full size (batch 128, the bench's launch
-  configuration) on sampled images and sampled filter-gradient entries;
+  configuration) on 4 distinct images repeated 32 times, whole tensors;
 * determinism, restore-and-rerun, the two-stream step against the one-stream
   step, and a captured HIP graph replayed against eager steps.
 """
@@ -122,13 +124,12 @@ SMALL = [
 
 
 @pytest.mark.parametrize("name,make", SMALL, ids=[s[0] for s in SMALL])
-def test_step_every_op_teacher_forced(name, make):
+def test_step_every_op_oracle_forced(name, make):
     net = make()
-    say("teacher-forced step:", net.name, "ops", len(net.ops))
+    say("oracle-forced step:", net.name, "ops", len(net.ops))
     inp = W.make_inputs(net, seed=0)
     rep = Replica(net, inp)
-    tr = ParityTracer(rep.dtype, label=name)
-    tr.lr = rep.lr
+    tr = ParityTracer(rep, inp, label=name)
     rep.step(trace=tr)
     torch.cuda.synchronize()
     bad = _report(tr)
@@ -137,14 +138,15 @@ def test_step_every_op_teacher_forced(name, make):
     assert not bad
 
 
-def test_alexnet_full_size_sampled():
-    """The bench workload at full size (batch 128) and launch configuration; images 0, 63
-    and 127 checked whole, 256 filter-gradient entries per conv."""
+def test_alexnet_full_size_repeated_images():
+    """The bench workload at full size (batch 128) and launch configuration (two streams), with
+    4 distinct images repeated 32 times: every op's output against the oracle's, per-image
+    outputs repeating bit for bit, and whole filter and bias gradients (32 times the oracle's
+    4-image sums)."""
     net = W.alexnet(batch=128)
     inp = W.make_inputs(net, seed=0)
     rep = Replica(net, inp)
-    tr = ParityTracer(rep.dtype, sample_images=[0, 63, 127], filter_samples=256, label="alexnet_b128")
-    tr.lr = rep.lr
+    tr = ParityTracer(rep, inp, distinct=4, label="alexnet_b128")
     rep.step(trace=tr)
     torch.cuda.synchronize()
     bad = _report(tr)
