@@ -680,6 +680,16 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
 }
 
 // ------------------------------------------------------------------ SGD
+// The variable updates stream each operand once: 16-byte non-temporal loads and stores (the
+// streams are not re-read by the update, so they should not displace cached activations).
+typedef float f4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ f4v stream_load(const float *p, int64_t t) {
+    return __builtin_nontemporal_load(reinterpret_cast<const f4v *>(p) + t);
+}
+__device__ __forceinline__ void stream_store(float *p, int64_t t, f4v v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<f4v *>(p) + t);
+}
+
 __device__ __forceinline__ void sgd_one(float *var, const float *grad, uint16_t *sh, int64_t i, float lr) {
     const float v = fmaf(-lr, grad[i], var[i]);
     var[i] = v;
@@ -693,11 +703,11 @@ __global__ __launch_bounds__(256) void sgd_kernel(float *__restrict__ var, const
     if (vec) {
         const int64_t n4 = n / 4;
         for (int64_t t = t0; t < n4; t += stride) {
-            float4 v = reinterpret_cast<const float4 *>(var)[t];
-            const float4 g = reinterpret_cast<const float4 *>(grad)[t];
+            f4v v = stream_load(var, t);
+            const f4v g = stream_load(grad, t);
             v.x = fmaf(-lr, g.x, v.x); v.y = fmaf(-lr, g.y, v.y);
             v.z = fmaf(-lr, g.z, v.z); v.w = fmaf(-lr, g.w, v.w);
-            reinterpret_cast<float4 *>(var)[t] = v;
+            stream_store(var, t, v);
             if (sh) {
                 uint2 b;
                 b.x = pack_bf16x2(v.x, v.y);
@@ -755,17 +765,17 @@ __global__ __launch_bounds__(256) void opt_kernel(float *__restrict__ var, float
         const int64_t n4 = n / 4;
         tail = n4 * 4;
         for (int64_t t = t0; t < n4; t += stride) {
-            float4 v = reinterpret_cast<const float4 *>(var)[t];
-            float4 a = reinterpret_cast<const float4 *>(s1)[t];
-            float4 b = KIND == 2 ? reinterpret_cast<const float4 *>(s2)[t] : make_float4(0.f, 0.f, 0.f, 0.f);
-            const float4 g = reinterpret_cast<const float4 *>(grad)[t];
-            v.x = opt_elem<KIND>(v.x, a.x, b.x, g.x, p);
-            v.y = opt_elem<KIND>(v.y, a.y, b.y, g.y, p);
-            v.z = opt_elem<KIND>(v.z, a.z, b.z, g.z, p);
-            v.w = opt_elem<KIND>(v.w, a.w, b.w, g.w, p);
-            reinterpret_cast<float4 *>(var)[t] = v;
-            reinterpret_cast<float4 *>(s1)[t] = a;
-            if (KIND == 2) reinterpret_cast<float4 *>(s2)[t] = b;
+            f4v v = stream_load(var, t), a = stream_load(s1, t);
+            f4v b = KIND == 2 ? stream_load(s2, t) : f4v{0.f, 0.f, 0.f, 0.f};
+            const f4v g = stream_load(grad, t);
+            float ax = a.x, ay = a.y, az = a.z, aw = a.w, bx = b.x, by = b.y, bz = b.z, bw = b.w;
+            v.x = opt_elem<KIND>(v.x, ax, bx, g.x, p);
+            v.y = opt_elem<KIND>(v.y, ay, by, g.y, p);
+            v.z = opt_elem<KIND>(v.z, az, bz, g.z, p);
+            v.w = opt_elem<KIND>(v.w, aw, bw, g.w, p);
+            stream_store(var, t, v);
+            stream_store(s1, t, f4v{ax, ay, az, aw});
+            if (KIND == 2) stream_store(s2, t, f4v{bx, by, bz, bw});
             if (sh) {
                 uint2 q;
                 q.x = pack_bf16x2(v.x, v.y);
@@ -1021,7 +1031,7 @@ hipError_t launch_maxpool_bwd(int dt, const void *dy, const void *am, bool taps,
 
 hipError_t launch_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh, hipStream_t st) {
     const bool vec = aligned16(var) && aligned16(grad) && (sh == nullptr || ((uintptr_t)sh & 7) == 0);
-    const int grid = grid_for(vec ? (n + 3) / 4 : n, 256, 8192);
+    const int grid = grid_for(vec ? (n + 3) / 4 : n, 256, 1 << 20);
     hipLaunchKernelGGL(sgd_kernel, dim3(grid), dim3(256), 0, st, var, grad, n, lr, sh, vec);
     return hipGetLastError();
 }
@@ -1030,7 +1040,7 @@ hipError_t launch_opt(int kind, float *var, float *s1, float *s2, const float *g
                       uint16_t *sh, hipStream_t st) {
     const bool vec = aligned16(var) && aligned16(s1) && (kind != 2 || aligned16(s2)) && aligned16(grad) &&
                      (sh == nullptr || ((uintptr_t)sh & 7) == 0);
-    const int grid = grid_for(vec ? (n + 3) / 4 : n, 256, 8192);
+    const int grid = grid_for(vec ? (n + 3) / 4 : n, 256, 1 << 20);
     switch (kind) {
         case 0: hipLaunchKernelGGL(opt_kernel<0>, dim3(grid), dim3(256), 0, st, var, s1, s2, grad, n, p, sh, vec); break;
         case 1: hipLaunchKernelGGL(opt_kernel<1>, dim3(grid), dim3(256), 0, st, var, s1, s2, grad, n, p, sh, vec); break;
