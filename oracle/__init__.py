@@ -27,6 +27,9 @@ Parity status of each function (pins are in tests/test_oracle_pins.py):
                     momentum 0 = SGD, the velocity as a geometric sum of past gradients.
 * apply_adam        pinned: constant-gradient closed form, first-step form, the moments
                     as bias-weighted sums of past gradients, beta = 0 forms.
+* softmax_xent      pinned: library cross-entropy and its autograd gradient, uniform-logit
+                    closed form, invariance to a per-row shift of 1000 (overflow),
+                    zero gradient row sums, NaN rows for out-of-range labels.
 * step (net.py)     pinned: finite differences of the whole single-layer loss
                     and the exact first-order decrease of a piecewise-linear net.
 """
@@ -87,6 +90,7 @@ def _declare(lib):
     lib.orc_maxpool_bwd.argtypes = [_dp, _ip, _l, _dp, _l, _i]
     lib.orc_apply_sgd.argtypes = [_dp, _dp, _l, ctypes.c_double]
     lib.orc_apply_momentum.argtypes = [_dp, _dp, _dp, _l, ctypes.c_double, ctypes.c_double, ctypes.c_int]
+    lib.orc_softmax_xent.argtypes = [_dp, _dp, _ip, _l, _i, ctypes.c_double, _dp, _dp]
     lib.orc_apply_adam.argtypes = [_dp, _dp, _dp, _dp, _l, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                                    ctypes.c_double, ctypes.c_int]
 
@@ -271,3 +275,21 @@ def apply_adam(var, m, v, grad, lr, beta1, beta2, epsilon, t):
     lib.orc_apply_adam(_ptr(out), _ptr(mm), _ptr(vv), _ptr(g), out.size, float(lr), float(beta1), float(beta2),
                        float(epsilon), int(t))
     return out, mm, vv
+
+
+def softmax_xent(logits, labels, scale=1.0, bias=None):
+    """Softmax cross-entropy of (n, c) logits (+ bias[c]) against int labels; returns
+    (loss per row, scale * (softmax - onehot)) in fp64."""
+    lib = _load()
+    z = _f64(logits)
+    assert z.ndim == 2
+    n, c = z.shape
+    lab = np.ascontiguousarray(labels, dtype=np.int32)
+    assert lab.shape == (n,)
+    b = None if bias is None else _f64(bias)
+    assert b is None or b.shape == (c,)
+    loss = np.zeros(n)
+    dz = np.zeros((n, c))
+    lib.orc_softmax_xent(_ptr(z), None if b is None else _ptr(b), lab.ctypes.data_as(_ip), n, c, float(scale),
+                         _ptr(loss), _ptr(dz))
+    return loss, dz

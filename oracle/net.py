@@ -10,19 +10,23 @@ gradients that reach a tensor along different paths (Section 4.1); no
 gradient is formed for the step input unless the workload asks for it.
 
 The surrogate loss is L = <g, out>, so the upstream gradient of the net's
-output tensor is the given ``g``.
+output tensor is the given ``g``.  A classifier net (``net.loss ==
+"softmax_xent"``) instead ends in logits and its loss is the batch mean of the
+softmax cross-entropy against ``labels``; the upstream gradient of the logits
+is then (softmax - onehot) / N.
 
 ``net`` is a plain description: ``net.ops`` in forward order, each op carrying
 ``name, src, dst, dst_c0, kh, kw, sh, sw, pads`` and, for convolutions,
-``cout``; ``net.tensors`` maps names to NHWC shapes; ``net.output`` names the
-output tensor.  Every convolution is followed by bias-add and ReLU.
+``cout`` and ``relu``; ``net.tensors`` maps names to NHWC shapes; ``net.output``
+names the output tensor.  Every convolution is followed by bias-add and, unless
+its ``relu`` is false (a classifier's logits), ReLU.
 """
 from __future__ import annotations
 
 import numpy as np
 
 from . import (apply_sgd, bias_relu_bwd, bias_relu_fwd, conv2d_bwd_filter, conv2d_bwd_input,
-               conv2d_fwd, maxpool_bwd, maxpool_fwd)
+               conv2d_fwd, maxpool_bwd, maxpool_fwd, softmax_xent)
 
 
 def _is_conv(op):
@@ -40,7 +44,10 @@ def forward(net, x, weights, biases):
         src = acts[op.src]
         if _is_conv(op):
             pre = conv2d_fwd(src, weights[op.name], (op.sh, op.sw), op.pads)
-            out = bias_relu_fwd(pre, biases[op.name])
+            if getattr(op, "relu", True):
+                out = bias_relu_fwd(pre, biases[op.name])
+            else:
+                out = pre + np.asarray(biases[op.name], dtype=np.float64)
         else:
             out, am = maxpool_fwd(src, (op.kh, op.kw), (op.sh, op.sw), op.pads)
             argmax[op.name] = am
@@ -67,7 +74,10 @@ def backward(net, acts, argmax, weights, g):
         src = acts[op.src]
         if _is_conv(op):
             y = acts[op.dst][..., op.dst_c0:op.dst_c0 + width]
-            dpre, db[op.name] = bias_relu_bwd(y, dy)
+            if getattr(op, "relu", True):
+                dpre, db[op.name] = bias_relu_bwd(y, dy)
+            else:
+                dpre, db[op.name] = dy, dy.sum(axis=(0, 1, 2))
             dW[op.name] = conv2d_bwd_filter(src, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads)
             if op.src != "x" or net.input_grad:
                 dx = conv2d_bwd_input(dpre, weights[op.name], src.shape, (op.sh, op.sw), op.pads)
@@ -79,19 +89,33 @@ def backward(net, acts, argmax, weights, g):
     return grads, dW, db
 
 
-def step(net, x, weights, biases, g, lr=None):
-    """One SGD step.  Returns a dict with acts, argmax, grads, dW, db, new_weights, new_biases."""
+def classifier_loss(net, acts, labels):
+    """Batch-mean softmax cross-entropy of the logits and its gradient (N, 1, 1, C)."""
+    out = acts[net.output]
+    n = out.shape[0]
+    rows, dz = softmax_xent(out.reshape(n, -1), labels, 1.0 / n)
+    return float(np.mean(rows)), dz.reshape(out.shape)
+
+
+def step(net, x, weights, biases, g, lr=None, labels=None):
+    """One SGD step.  Returns a dict with acts, argmax, grads, dW, db, new_weights, new_biases
+    (and, for a classifier, loss)."""
     # The learning rate is an fp32 attribute of the update op: use its fp32 value.
     lr = float(np.float32(net.lr if lr is None else lr))
     acts, argmax = forward(net, x, weights, biases)
+    value = None
+    if net.loss == "softmax_xent":
+        value, g = classifier_loss(net, acts, labels)
     grads, dW, db = backward(net, acts, argmax, weights, g)
     new_w = {k: apply_sgd(weights[k], dW[k], lr) for k in dW}
     new_b = {k: apply_sgd(biases[k], db[k], lr) for k in db}
     return dict(acts=acts, argmax=argmax, grads=grads, dW=dW, db=db,
-                new_weights=new_w, new_biases=new_b)
+                new_weights=new_w, new_biases=new_b, loss=value)
 
 
-def loss(net, x, weights, biases, g):
-    """Surrogate loss <g, out> of the forward pass."""
+def loss(net, x, weights, biases, g, labels=None):
+    """The loss of the forward pass: <g, out>, or a classifier's mean cross-entropy."""
     acts, _ = forward(net, x, weights, biases)
+    if net.loss == "softmax_xent":
+        return classifier_loss(net, acts, labels)[0]
     return float(np.sum(np.asarray(g, dtype=np.float64) * acts[net.output]))

@@ -327,3 +327,37 @@ void orc_apply_adam(double *var, double *m, double *v, const double *grad, i64 n
         var[i] = var[i] - lr * mhat / (sqrt(vhat) + epsilon);
     }
 }
+
+/* Softmax cross-entropy of a classifier's logits against integer labels (the paper's image
+ * models end in a softmax classifier trained by the gradient of its loss, Section 4.1).
+ * Row i of z = logits + bias (bias may be NULL), n rows of c classes:
+ *   loss[i]  = log(sum_j exp(z_ij)) - z_i,label      evaluated as m + log(sum_j exp(z_ij - m)),
+ *                                                     m = max_j z_ij, so no exp overflows
+ *   dz[i][j] = scale * (exp(z_ij - m) / sum_k exp(z_ik - m) - [j == label])
+ * A label outside [0, c) gives a NaN loss and a NaN gradient row. */
+void orc_softmax_xent(const double *logits, const double *bias, const int32_t *labels, i64 n, int c,
+                      double scale, double *loss, double *dz) {
+#pragma omp parallel for schedule(static)
+    for (i64 i = 0; i < n; ++i) {
+        const double *zr = logits + i * c;
+        double *dr = dz + i * c;
+        const int lab = labels[i];
+        if (lab < 0 || lab >= c) {
+            loss[i] = NAN;
+            for (int j = 0; j < c; ++j) dr[j] = NAN;
+            continue;
+        }
+        double m = -INFINITY;
+        for (int j = 0; j < c; ++j) {
+            const double z = zr[j] + (bias ? bias[j] : 0.0);
+            if (z > m) m = z;
+        }
+        double sum = 0.0;
+        for (int j = 0; j < c; ++j) sum += exp(zr[j] + (bias ? bias[j] : 0.0) - m);
+        loss[i] = m + log(sum) - (zr[lab] + (bias ? bias[lab] : 0.0));
+        for (int j = 0; j < c; ++j) {
+            const double p = exp(zr[j] + (bias ? bias[j] : 0.0) - m) / sum;
+            dr[j] = scale * (p - (j == lab ? 1.0 : 0.0));
+        }
+    }
+}

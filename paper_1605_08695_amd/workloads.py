@@ -49,6 +49,7 @@ class Conv:
     sh: int
     sw: int
     pads: Pads
+    relu: bool = True               # False: bias only (the logits layer of a classifier)
 
 
 @dataclass(frozen=True)
@@ -75,6 +76,8 @@ class Net:
     tensors: Dict[str, Tuple[int, int, int, int]] = field(default_factory=dict)
     ops: List[object] = field(default_factory=list)
     output: str = ""
+    loss: str = "surrogate"         # "surrogate": L = <g, out>; "softmax_xent": mean cross-entropy
+    classes: int = 0                # softmax_xent: the output tensor is (N, 1, 1, classes) logits
 
     @property
     def convs(self) -> List[Conv]:
@@ -137,6 +140,14 @@ class _Builder:
         self.net.ops.append(Conv(name, src, dst, c0, cout, kh, kw, s, s, pads))
         return dst
 
+    def fc(self, src, cout, relu=True, name=None):
+        """A fully connected layer: a VALID convolution whose window is the whole input image."""
+        n, h, w, _ = self.net.tensors[src]
+        name = name or self._fresh("fc")
+        self.net.tensors[name] = (n, 1, 1, cout)
+        self.net.ops.append(Conv(name, src, name, 0, cout, h, w, 1, 1, VALID, relu))
+        return name
+
     def pool(self, src, k, s, pads=VALID, dst=None, c0=0, name=None):
         n, oh, ow, pads = self._spatial(src, k, k, s, s, pads)
         name = name or self._fresh("pool")
@@ -159,6 +170,13 @@ class _Builder:
         self.net.output = out
         return self.net
 
+    def softmax_done(self, logits, classes):
+        self.net.output = logits
+        self.net.loss = "softmax_xent"
+        self.net.classes = classes
+        assert self.net.tensors[logits][1:] == (1, 1, classes)
+        return self.net
+
 
 # ----------------------------------------------------------------------------- C1
 def single_layer(batch=8, hw=32, cin=16, cout=32) -> Net:
@@ -170,9 +188,12 @@ def single_layer(batch=8, hw=32, cin=16, cout=32) -> Net:
 
 
 # ----------------------------------------------------------------------------- C2
-def alexnet(batch=128) -> Net:
-    """AlexNet-shaped conv stack, bf16: 11x11/4 p2 64, pool 3/2, 5x5 p2 192, pool, 3x3 384, 256, 256, pool."""
-    b = _Builder("alexnet_b%d" % batch, "bf16", 0.01, False, (batch, 224, 224, 3))
+def alexnet(batch=128, classifier=False) -> Net:
+    """AlexNet-shaped conv stack, bf16: 11x11/4 p2 64, pool 3/2, 5x5 p2 192, pool, 3x3 384, 256, 256, pool.
+    With ``classifier``: then fc 4096 + ReLU, fc 4096 + ReLU, fc 1000 logits and the softmax
+    cross-entropy of 1000 classes (no dropout)."""
+    b = _Builder("alexnet%s_b%d" % ("_cls" if classifier else "", batch), "bf16", 0.01, False,
+                 (batch, 224, 224, 3))
     t = b.conv("x", 64, 11, s=4, pads=(2, 2, 2, 2), name="conv1")
     t = b.pool(t, 3, 2, name="pool1")
     t = b.conv(t, 192, 5, pads=(2, 2, 2, 2), name="conv2")
@@ -181,7 +202,23 @@ def alexnet(batch=128) -> Net:
     t = b.conv(t, 256, 3, pads=(1, 1, 1, 1), name="conv4")
     t = b.conv(t, 256, 3, pads=(1, 1, 1, 1), name="conv5")
     t = b.pool(t, 3, 2, name="pool5")
+    if classifier:
+        t = b.fc(t, 4096, name="fc6")
+        t = b.fc(t, 4096, name="fc7")
+        t = b.fc(t, 1000, relu=False, name="fc8")
+        return b.softmax_done(t, 1000)
     return b.done(t)
+
+
+def classifier_small(batch=4, dtype="f32") -> Net:
+    """A small classifier for finite differences and parity: conv3x3 p1 8 + pool 2/2, fc 16 + ReLU,
+    fc 10 logits, softmax cross-entropy (input gradient included)."""
+    b = _Builder("classifier_small_%s" % dtype, dtype, 0.01, True, (batch, 8, 8, 4))
+    t = b.conv("x", 8, 3, pads=(1, 1, 1, 1), name="conv1")
+    t = b.pool(t, 2, 2, name="pool1")
+    t = b.fc(t, 16, name="fc1")
+    t = b.fc(t, 10, relu=False, name="fc2")
+    return b.softmax_done(t, 10)
 
 
 # ----------------------------------------------------------------------------- C3
@@ -367,11 +404,13 @@ class Inputs:
     x: np.ndarray                 # float64 NHWC
     weights: Dict[str, np.ndarray]  # conv name -> float64 HWIO
     biases: Dict[str, np.ndarray]   # conv name -> float64 zeros [Cout]
-    g: np.ndarray                 # float64 upstream gradient, shape of the output tensor
+    g: np.ndarray                 # float64 upstream gradient, shape of the output tensor (surrogate loss)
+    labels: np.ndarray | None = None  # int32 class per image (softmax cross-entropy; g is then None)
 
 
 def make_inputs(net: Net, seed: int = 0, batch_slice: int | None = None) -> Inputs:
-    """Seeded inputs in the fixed draw order: x, then filters in op order, then g.
+    """Seeded inputs in the fixed draw order: x, then filters in op order, then g (or, for a
+    softmax classifier, one uniform class label per image).
 
     ``batch_slice`` keeps only the first images of x and g (the filters are
     drawn from the same stream in the same order, so they are identical).
@@ -384,11 +423,17 @@ def make_inputs(net: Net, seed: int = 0, batch_slice: int | None = None) -> Inpu
         std = math.sqrt(2.0 / (c.kh * c.kw * cin))
         weights[c.name] = rng.standard_normal((c.kh, c.kw, cin, c.cout)) * std
         biases[c.name] = np.zeros(c.cout)
-    g = rng.standard_normal(net.tensors[net.output])
+    if net.loss == "softmax_xent":
+        g = None
+        labels = rng.integers(0, net.classes, size=net.tensors["x"][0]).astype(np.int32)
+    else:
+        g = rng.standard_normal(net.tensors[net.output])
+        labels = None
     if batch_slice is not None:
         x = x[:batch_slice].copy()
-        g = g[:batch_slice].copy()
-    return Inputs(x, weights, biases, g)
+        g = None if g is None else g[:batch_slice].copy()
+        labels = None if labels is None else labels[:batch_slice].copy()
+    return Inputs(x, weights, biases, g, labels)
 
 
 def with_batch(net_fn, batch):

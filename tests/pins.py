@@ -463,6 +463,91 @@ def check_adam_weighted_sums(seed=19, T=6):
     return worst
 
 
+# ----------------------------------------------------------------------------- softmax cross-entropy
+def check_softmax_xent_vs_torch(seed=20, n=7, c=13):
+    """Against the library: torch float64 cross_entropy per row, and the autograd gradient of the
+    batch-mean loss (scale 1/n), with a bias added to the logits."""
+    rng = np.random.default_rng(seed)
+    z = rng.standard_normal((n, c)) * 3
+    b = rng.standard_normal(c)
+    lab = rng.integers(0, c, size=n).astype(np.int32)
+    rows, dz = oracle.softmax_xent(z, lab, 1.0 / n, bias=b)
+    zt = torch.tensor(z + b, dtype=torch.float64, requires_grad=True)
+    ref_rows = F.cross_entropy(zt, torch.tensor(lab, dtype=torch.int64), reduction="none")
+    ref_rows.mean().backward()
+    return max(rel(rows, ref_rows.detach().numpy()), rel(dz, zt.grad.numpy()))
+
+
+def check_softmax_xent_closed_forms(seed=21, n=5, c=11):
+    """Equal logits give loss log(c) and gradient scale (1/c - onehot); a shift of every logit of a
+    row by +-1000 changes nothing (the max is taken out before exp); gradient rows sum to zero; a
+    label outside [0, c) gives a NaN row."""
+    rng = np.random.default_rng(seed)
+    lab = rng.integers(0, c, size=n).astype(np.int32)
+    rows, dz = oracle.softmax_xent(np.full((n, c), 0.7), lab, 0.25)
+    onehot = np.eye(c)[lab]
+    worst = max(float(np.max(np.abs(rows - np.log(c)))), float(np.max(np.abs(dz - 0.25 * (1.0 / c - onehot)))))
+    z = rng.standard_normal((n, c))
+    r0, d0 = oracle.softmax_xent(z, lab, 1.0)
+    for shift in (1000.0, -1000.0):
+        r1, d1 = oracle.softmax_xent(z + shift, lab, 1.0)
+        worst = max(worst, float(np.max(np.abs(r1 - r0))) if np.all(np.isfinite(r1)) else np.inf,
+                    float(np.max(np.abs(d1 - d0))) if np.all(np.isfinite(d1)) else np.inf)
+    worst = max(worst, float(np.max(np.abs(d0.sum(axis=1)))))
+    bad = lab.copy()
+    bad[1], bad[3] = -1, c
+    rb, db = oracle.softmax_xent(z, bad, 1.0)
+    ok = (np.isnan(rb[1]) and np.isnan(rb[3]) and np.all(np.isnan(db[[1, 3]]))
+          and np.array_equal(rb[[0, 2, 4]], r0[[0, 2, 4]]))
+    return worst if ok else np.inf
+
+
+def check_classifier_step_fd(net, inputs, samples=12, seed=22):
+    """Finite differences of the batch-mean cross-entropy of a classifier net in the filters and
+    biases of every layer and in x.  The loss is smooth apart from ReLU and max-pool kinks; entries
+    whose steps h and h/2 disagree crossed one and are skipped."""
+    rng = np.random.default_rng(seed)
+    res = onet.step(net, inputs.x, inputs.weights, inputs.biases, None, labels=inputs.labels)
+    lab = inputs.labels
+
+    def L(ws, bs, xx):
+        return onet.loss(net, xx, ws, bs, None, labels=lab)
+
+    def fd(f, arr, idx, h):
+        ap, am = arr.copy(), arr.copy()
+        ap[idx] += h
+        am[idx] -= h
+        return (f(ap) - f(am)) / (2 * h)
+    worst, checked = 0.0, 0
+    targets = []
+    for c in net.convs:
+        targets.append(("W", c.name, inputs.weights[c.name], res["dW"][c.name]))
+        targets.append(("b", c.name, inputs.biases[c.name], res["db"][c.name]))
+    targets.append(("x", "x", inputs.x, res["grads"]["x"]))
+    for kind, name, arr, ref in targets:
+        gscale = max(float(np.max(np.abs(ref))), 1e-12)
+
+        def f(a, kind=kind, name=name):
+            ws, bs, xx = dict(inputs.weights), dict(inputs.biases), inputs.x
+            if kind == "W":
+                ws[name] = a
+            elif kind == "b":
+                bs[name] = a
+            else:
+                xx = a
+            return L(ws, bs, xx)
+        h = 1e-5 * float(np.sqrt(np.mean(arr ** 2)) or 1.0)
+        for _ in range(samples):
+            idx = tuple(int(rng.integers(0, d)) for d in arr.shape)
+            d1, d2 = fd(f, arr, idx, h), fd(f, arr, idx, h / 2)
+            if abs(d1 - d2) > 1e-6 * gscale:
+                continue
+            checked += 1
+            worst = max(worst, abs(d2 - ref[idx]) / gscale)
+    assert checked >= samples * len(targets) // 2, checked
+    return worst
+
+
 # ----------------------------------------------------------------------------- whole step
 def check_step_fd(net, inputs, samples=24, seed=14):
     """Finite differences of the whole single-step surrogate loss L(W, b, x) = <g, out>.

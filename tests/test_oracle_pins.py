@@ -114,6 +114,18 @@ def test_adam_closed_form_and_weighted_sums():
     assert pins.check_adam_weighted_sums() < 1e-12
 
 
+def test_softmax_xent_library_and_closed_forms():
+    assert pins.check_softmax_xent_vs_torch() < 1e-12
+    assert pins.check_softmax_xent_closed_forms() < 1e-12
+
+
+def test_classifier_step_finite_differences():
+    net = W.classifier_small(batch=3)
+    inp = W.make_inputs(net, seed=5)
+    assert inp.g is None and inp.labels.shape == (3,)
+    assert pins.check_classifier_step_fd(net, inp) < 1e-6
+
+
 def test_single_layer_step_finite_differences():
     net = W.single_layer(batch=2, hw=8, cin=3, cout=4)
     inp = W.make_inputs(net, seed=3)
@@ -217,6 +229,12 @@ MUTATIONS = [
      "check_adam_weighted_sums"),
     ("adam epsilon inside the root", "lr * mhat / (sqrt(vhat) + epsilon);", "lr * mhat / sqrt(vhat + epsilon);",
      "check_adam_closed_form"),
+    ("softmax does not take the max out", "double m = -INFINITY;", "double m = 0.0;",
+     "check_softmax_xent_closed_forms"),
+    ("cross-entropy gradient drops the one-hot", "dr[j] = scale * (p - (j == lab ? 1.0 : 0.0));",
+     "dr[j] = scale * p;", "check_softmax_xent_vs_torch"),
+    ("cross-entropy loss of class 0", "- (zr[lab] + (bias ? bias[lab] : 0.0));", "- (zr[0] + (bias ? bias[0] : 0.0));",
+     "check_softmax_xent_vs_torch"),
     ("pool bwd drops beta", "if (!beta) memset(dx, 0, sizeof(double) * (size_t)nx);",
      "memset(dx, 0, sizeof(double) * (size_t)nx);", "check_pool_bwd_beta"),
 ]
