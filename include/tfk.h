@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 6
+#define TFK_ABI_VERSION 7
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -199,6 +199,8 @@ TFK_API tfk_status tfk_bias_relu_fwd(void *y, tfk_nhwc yd, const float *bias, tf
  *                 dpre may equal dy (in place); any other overlap is an error.
  *   dbias       : fp32 [yd.c], overwritten.
  *   ws          : at least tfk_bias_relu_bwd_workspace_bytes(yd, dt) bytes.
+ * y may be NULL: a layer with a bias and no ReLU (a classifier's logits), so
+ * dpre = dy and dbias holds the column sums of dy.
  * Requirements: yd.c <= 16384.
  */
 TFK_API tfk_status tfk_bias_relu_bwd(const void *y, const void *dy, tfk_nhwc yd, void *dpre,
@@ -286,6 +288,29 @@ TFK_API tfk_status tfk_apply_sgd(float *var, const float *grad, int64_t n, float
 TFK_API tfk_status tfk_apply_sgd_multi(int32_t count, float *const *vars, const float *const *grads,
                                const int64_t *ns, float lr, uint16_t *const *shadows,
                                void *stream);
+
+/* ---------------------------------------------------------------- classifier loss
+ * Softmax cross-entropy of a classifier's logits against integer labels (the
+ * loss whose gradient Section 4.1's backpropagation starts from in the image
+ * models the paper trains).  For each row i < n of z = logits + bias:
+ *   loss[i]       = log(sum_j exp(z[i][j])) - z[i][labels[i]]
+ *   dlogits[i][j] = scale * (softmax(z[i])[j] - (j == labels[i]))
+ * (scale = 1/n gives the gradient of the batch-mean loss).  The max of each row
+ * is taken out before exp, so no finite logit overflows; arithmetic is fp32.
+ *   logits, dlogits : n x c row-major, type dt; dlogits may equal logits (in
+ *                     place, the logits are then overwritten), any other
+ *                     overlap is an error.
+ *   bias            : fp32 [c], or NULL for none.
+ *   labels          : int32 [n], device memory.  A label outside [0, c) is not
+ *                     checked on the host: its row gets a NaN loss and NaN
+ *                     gradients.
+ *   loss            : fp32 [n], overwritten.
+ * Errors: n < 0 or c < 1 (SHAPE); scale not finite (ARG); n * c > 2^40
+ * (OVERFLOW); NULL buffers with n > 0 (NULL); misalignment (ALIGN);
+ * overlapping operands (ALIAS).  n == 0 is a no-op. */
+TFK_API tfk_status tfk_softmax_xent(const void *logits, tfk_dtype dt, int64_t n, int32_t c, const float *bias,
+                            const int32_t *labels, float scale, float *loss, void *dlogits,
+                            void *stream);
 
 /* Momentum, in place (Section 4.1 lists it among the optimizers built from
  * Variable updates: a per-parameter velocity accumulated over the gradients

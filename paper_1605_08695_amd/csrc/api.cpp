@@ -346,7 +346,6 @@ tfk_status tfk_bias_relu_bwd(const void *y, const void *dy, tfk_nhwc yd, void *d
     const int64_t bb = (int64_t)yd.c * 4;
     if (yd.c > 16384) return fail(TFK_ERR_SHAPE, "bias_relu_bwd supports at most 16384 channels");
     if (yd.n == 0) return hip_status(launch_fill_zero(dbias, yd.c, st), "bias_relu_bwd");
-    TRY(need_ptr(y, "y"));
     TRY(need_ptr(dy, "dy"));
     TRY(need_ptr(dpre, "dpre"));
     TRY(need_align(y, es, "y"));
@@ -559,6 +558,38 @@ tfk_status tfk_apply_sgd_multi(int32_t count, float *const *vars, const float *c
         if (e != hipSuccess) return hip_status(e, "apply_sgd_multi");
     }
     return ok();
+}
+
+// ------------------------------------------------------------------ softmax cross-entropy
+tfk_status tfk_softmax_xent(const void *logits, tfk_dtype dt, int64_t n, int32_t c, const float *bias,
+                            const int32_t *labels, float scale, float *loss, void *dlogits, void *stream) {
+    if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
+    if (n < 0 || c < 1) return fail(TFK_ERR_SHAPE, "need n >= 0 and c >= 1 (n=%lld, c=%d)", (long long)n, c);
+    if (!isfinite(scale)) return fail(TFK_ERR_ARG, "scale must be finite");
+    if (n == 0) return ok();
+    if (n > ((int64_t)1 << 40) / c) return fail(TFK_ERR_OVERFLOW, "n * c too large");
+    const int64_t es = esize(dt), zb = n * c * es;
+    TRY(need_ptr(logits, "logits"));
+    TRY(need_ptr(labels, "labels"));
+    TRY(need_ptr(loss, "loss"));
+    TRY(need_ptr(dlogits, "dlogits"));
+    TRY(need_align(logits, es, "logits"));
+    TRY(need_align(dlogits, es, "dlogits"));
+    TRY(need_align(bias, 4, "bias"));
+    TRY(need_align(labels, 4, "labels"));
+    TRY(need_align(loss, 4, "loss"));
+    if (dlogits != logits && overlap(dlogits, zb, logits, zb))
+        return fail(TFK_ERR_ALIAS, "dlogits partially overlaps logits");
+    const void *p[5] = {dlogits, bias, labels, loss, logits};
+    const int64_t b[5] = {zb, (int64_t)c * 4, n * 4, n * 4, zb};
+    for (int i = 0; i < 4; ++i)
+        for (int j = i + 1; j < 5; ++j)
+            if (!(i == 0 && j == 4) && overlap(p[i], b[i], p[j], b[j]))
+                return fail(TFK_ERR_ALIAS, "softmax_xent operands overlap");
+    if ((n + 3) / 4 > INT32_MAX) return fail(TFK_ERR_OVERFLOW, "too many rows");
+    return hip_status(launch_softmax_xent(dt == TFK_F32 ? 0 : 1, logits, bias, labels, n, c, scale, loss, dlogits,
+                                          (hipStream_t)stream),
+                      "softmax_xent");
 }
 
 // ------------------------------------------------------------------ Momentum, Adam

@@ -114,7 +114,12 @@ __global__ __launch_bounds__(256) void relu_bwd_partial_kernel(const T *__restri
                 const int64_t off = p * ys + (int64_t)cv * EPC;
                 if constexpr (VEC) {
                     float fy[EPC], fd[EPC];
-                    chunk_to_f32<T>(*reinterpret_cast<const U4 *>(y + off), fy);
+                    if (y != nullptr) {
+                        chunk_to_f32<T>(*reinterpret_cast<const U4 *>(y + off), fy);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < EPC; ++e) fy[e] = 1.f;
+                    }
                     chunk_to_f32<T>(*reinterpret_cast<const U4 *>(dy + off), fd);
 #pragma unroll
                     for (int e = 0; e < EPC; ++e) {
@@ -123,7 +128,7 @@ __global__ __launch_bounds__(256) void relu_bwd_partial_kernel(const T *__restri
                     }
                     *reinterpret_cast<U4 *>(dpre + off) = f32_to_chunk<T>(fd);
                 } else {
-                    const float fy = Elem<T>::load(y + off);
+                    const float fy = y != nullptr ? Elem<T>::load(y + off) : 1.f;
                     const float fd = fy > 0.f ? Elem<T>::load(dy + off) : 0.f;
                     s[0] += fd;
                     Elem<T>::store(dpre + off, fd);
@@ -792,6 +797,64 @@ __global__ __launch_bounds__(256) void opt_kernel(float *__restrict__ var, float
         if (KIND == 2) s2[i] = b;
         if (sh) sh[i] = (uint16_t)f32_to_bf16(v);
     }
+}
+
+// ------------------------------------------------------------------ softmax cross-entropy
+// One wave per row of n x c logits (z = logits + bias): the row max, then the sum of exp(z - max),
+// both reduced across the wave by a fixed xor tree, then the loss and the gradient
+// scale * (softmax - onehot).  Each lane reads and writes only its own columns, so dz may be the
+// logits buffer itself.
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void softmax_xent_kernel(const T *z, const float *__restrict__ bias,
+                                                           const int32_t *__restrict__ labels, int64_t n, int c,
+                                                           float scale, float *__restrict__ loss, T *dz) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= n) return;
+    const T *zr = z + row * c;
+    T *dr = dz + row * c;
+    const int lab = labels[row];
+    if (lab < 0 || lab >= c) {
+        for (int j = lane; j < c; j += 64) Elem<T>::store(dr + j, __builtin_nanf(""));
+        if (lane == 0) loss[row] = __builtin_nanf("");
+        return;
+    }
+    float m = -INFINITY;
+    for (int j = lane; j < c; j += 64) m = fmaxf(m, Elem<T>::load(zr + j) + (bias ? bias[j] : 0.f));
+    m = wave_max(m);
+    float sum = 0.f;
+    for (int j = lane; j < c; j += 64) sum += expf(Elem<T>::load(zr + j) + (bias ? bias[j] : 0.f) - m);
+    sum = wave_sum(sum);
+    const float zl = Elem<T>::load(zr + lab) + (bias ? bias[lab] : 0.f);
+    if (lane == 0) loss[row] = m + logf(sum) - zl;
+    const float inv = 1.f / sum;
+    for (int j = lane; j < c; j += 64) {
+        const float p = expf(Elem<T>::load(zr + j) + (bias ? bias[j] : 0.f) - m) * inv;
+        Elem<T>::store(dr + j, scale * (j == lab ? p - 1.f : p));
+    }
+}
+
+hipError_t launch_softmax_xent(int dt, const void *z, const float *bias, const int32_t *labels, int64_t n, int c,
+                               float scale, float *loss, void *dz, hipStream_t st) {
+    const int64_t blocks = (n + 3) / 4;
+    if (dt == 0)
+        hipLaunchKernelGGL(softmax_xent_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, (const float *)z, bias,
+                           labels, n, c, scale, loss, (float *)dz);
+    else
+        hipLaunchKernelGGL(softmax_xent_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st, (const bf16_t *)z,
+                           bias, labels, n, c, scale, loss, (bf16_t *)dz);
+    return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ split-K sum / zero fill

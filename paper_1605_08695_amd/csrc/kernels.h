@@ -89,6 +89,10 @@ hipError_t launch_maxpool_relu_bwd(int dt, const void *dy, const void *am, bool 
                                    const void *y, void *dpre, float beta, float *db, float *ws, hipStream_t st);
 hipError_t launch_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh, hipStream_t st);
 hipError_t launch_sgd_multi(const SgdBatch &b, float lr, hipStream_t st);
+// Softmax cross-entropy of n x c logits (+ bias) against labels: per-row loss and
+// dz = scale * (softmax - onehot); dz may be z.
+hipError_t launch_softmax_xent(int dt, const void *z, const float *bias, const int32_t *labels, int64_t n, int c,
+                               float scale, float *loss, void *dz, hipStream_t st);
 // Momentum (kind 0, 1 = look-ahead form) and Adam (kind 2) in place over n fp32 elements.
 hipError_t launch_opt(int kind, float *var, float *s1, float *s2, const float *grad, int64_t n, const OptParams &p,
                       uint16_t *sh, hipStream_t st);

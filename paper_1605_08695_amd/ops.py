@@ -17,7 +17,7 @@ from ._lib import Nhwc, TfkError, Window, TFK_BF16, TFK_F32, check, load
 
 __all__ = ["conv2d_fwd", "conv2d_fwd_bias_relu", "conv2d_bwd_input", "conv2d_bwd_filter", "conv2d_workspace_bytes", "bias_relu_fwd",
            "bias_relu_bwd", "bias_relu_bwd_workspace_bytes", "maxpool_fwd", "maxpool_bwd", "maxpool_bwd_relu_bwd", "apply_sgd",
-           "apply_sgd_multi", "apply_momentum", "apply_adam", "out_len", "nhwc", "window", "TfkError", "abi_version"]
+           "apply_sgd_multi", "apply_momentum", "apply_adam", "softmax_xent", "out_len", "nhwc", "window", "TfkError", "abi_version"]
 
 
 def _dt(t: torch.Tensor) -> int:
@@ -175,21 +175,45 @@ def bias_relu_bwd_workspace_bytes(y) -> int:
 
 
 def bias_relu_bwd(y, dy, dpre=None, dbias=None, ws=None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """dpre = dy * (y > 0) (dpre may be dy), dbias = column sums of dpre (fp32)."""
+    """dpre = dy * (y > 0) (dpre may be dy), dbias = column sums of dpre (fp32).  With y None
+    (a bias-only layer) dpre = dy and dbias = column sums of dy."""
     lib = load()
     if dpre is None:
         dpre = torch.empty_like(dy)
     if dbias is None:
-        dbias = torch.empty(y.shape[3], dtype=torch.float32, device=y.device)
-    need = lib.tfk_bias_relu_bwd_workspace_bytes(nhwc(y), _dt(y))
+        dbias = torch.empty(dy.shape[3], dtype=torch.float32, device=dy.device)
+    view = y if y is not None else dy
+    need = lib.tfk_bias_relu_bwd_workspace_bytes(nhwc(view), _dt(view))
     if ws is None or ws.numel() < need:
-        ws = _ws(need, y.device)
-    d_y, d_dy, d_dp = nhwc(y), nhwc(dy), nhwc(dpre)
+        ws = _ws(need, dy.device)
+    d_y, d_dy, d_dp = nhwc(view), nhwc(dy), nhwc(dpre)
     if (d_y.pixel_stride, d_y.c) != (d_dy.pixel_stride, d_dy.c) or (d_y.pixel_stride, d_y.c) != (d_dp.pixel_stride, d_dp.c):
         raise ValueError("y, dy and dpre must share one view (extents and pixel stride)")
-    check(lib.tfk_bias_relu_bwd(_ptr(y), _ptr(dy), d_y, _ptr(dpre), _ptr(dbias), _dt(y), _ptr(ws), need,
+    check(lib.tfk_bias_relu_bwd(_ptr(y), _ptr(dy), d_y, _ptr(dpre), _ptr(dbias), _dt(dy), _ptr(ws), need,
                                 _stream(stream)))
     return dpre, dbias
+
+
+def softmax_xent(logits, labels, scale, bias=None, loss=None, dlogits=None, stream=None):
+    """Softmax cross-entropy of contiguous logits (rows of the last dimension) + bias against int32
+    labels: returns (per-row loss fp32, dlogits = scale * (softmax - onehot)); dlogits may be logits."""
+    if not logits.is_contiguous():
+        raise ValueError("logits must be contiguous")
+    c = logits.shape[-1]
+    n = logits.numel() // c if c else 0
+    if labels.dtype != torch.int32 or labels.numel() != n:
+        raise ValueError("labels must be int32, one per row")
+    if bias is not None and (bias.dtype != torch.float32 or bias.numel() != c):
+        raise ValueError("bias must be float32 [c]")
+    if loss is None:
+        loss = torch.empty(n, dtype=torch.float32, device=logits.device)
+    if dlogits is None:
+        dlogits = torch.empty_like(logits)
+    if dlogits.dtype != logits.dtype or dlogits.numel() != logits.numel() or not dlogits.is_contiguous():
+        raise ValueError("dlogits must be a contiguous tensor like logits")
+    check(load().tfk_softmax_xent(_ptr(logits), _dt(logits), n, c, _ptr(bias), _ptr(labels), float(scale),
+                                  _ptr(loss), _ptr(dlogits), _stream(stream)))
+    return loss, dlogits
 
 
 # ----------------------------------------------------------------------------- max-pool

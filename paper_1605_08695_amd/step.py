@@ -116,7 +116,13 @@ class Replica:
                 self.act["x"] = xin
             else:
                 self.act[name] = torch.zeros(shape, dtype=dt, device=dev)
-        self.g = torch.from_numpy(inputs.g).to(dt).to(dev)
+        if net.loss == "softmax_xent":
+            # the logits' gradient is written by the cross-entropy kernel every step
+            self.g = torch.zeros(net.tensors[net.output], dtype=dt, device=dev)
+            self.labels = torch.from_numpy(np.asarray(inputs.labels, dtype=np.int32)).to(dev)
+            self.loss_rows = torch.zeros(self.labels.numel(), dtype=torch.float32, device=dev)
+        else:
+            self.g = torch.from_numpy(inputs.g).to(dt).to(dev)
         self.grad: Dict[str, torch.Tensor] = {net.output: self.g}
         for name, shape in net.tensors.items():
             if name == net.output or (name == "x" and not net.input_grad):
@@ -138,7 +144,7 @@ class Replica:
         for op in net.ops:
             if isinstance(op, Pool):
                 w = writers.get(op.src, [])
-                if (len(w) == 1 and isinstance(w[0], Conv) and w[0].dst_c0 == 0
+                if (len(w) == 1 and isinstance(w[0], Conv) and w[0].relu and w[0].dst_c0 == 0
                         and w[0].cout == net.tensors[op.src][3] and len(readers[op.src]) == 1):
                     self.pool_relu[op.name] = w[0]
         # ---- convolutions whose input is the whole ReLU output of another convolution and
@@ -147,7 +153,7 @@ class Replica:
         for op in net.ops:
             if isinstance(op, Conv) and op.src != "x" and op.src != net.output:
                 w = writers.get(op.src, [])
-                if (len(w) == 1 and isinstance(w[0], Conv) and w[0].dst_c0 == 0
+                if (len(w) == 1 and isinstance(w[0], Conv) and w[0].relu and w[0].dst_c0 == 0
                         and w[0].cout == net.tensors[op.src][3] and len(readers[op.src]) == 1):
                     self.bwi_relu[op.name] = w[0]
         self.relu_fused = ({c.name for c in self.pool_relu.values()} |
@@ -181,7 +187,12 @@ class Replica:
         for op in self.net.ops:
             x = self.act[op.src]
             y = self._slice(self.act, op)
-            if isinstance(op, Conv):
+            if isinstance(op, Conv) and not op.relu:
+                # a classifier's logits: the bias is added inside the cross-entropy kernel
+                if trace: trace("conv_fwd", op, stream=stream, x=x, w=self.Wlp[op.name], y=y)
+                ops.conv2d_fwd(x, self.Wlp[op.name], (op.sh, op.sw), op.pads, y=y, ws=self.ws, stream=stream)
+                if trace: trace("conv_fwd:end", op, stream=stream, y=y)
+            elif isinstance(op, Conv):
                 if trace: trace("conv_bias_relu_fwd", op, stream=stream, x=x, w=self.Wlp[op.name],
                                 b=self.b[op.name], y=y)
                 ops.conv2d_fwd_bias_relu(x, self.Wlp[op.name], self.b[op.name], (op.sh, op.sw), op.pads, y=y,
@@ -192,6 +203,23 @@ class Replica:
                 ops.maxpool_fwd(x, (op.kh, op.kw), (op.sh, op.sw), op.pads, y=y, argmax=self.argmax[op.name],
                                 stream=stream)
                 if trace: trace("maxpool_fwd:end", op, stream=stream, y=y, argmax=self.argmax[op.name])
+        if self.net.loss == "softmax_xent":
+            self.loss_fwd_bwd(trace, stream)
+
+    def loss_fwd_bwd(self, trace=None, stream=None):
+        """Mean softmax cross-entropy of the logits (the logits layer's bias added here) and its
+        gradient (softmax - onehot) / N, written as the upstream gradient of the logits."""
+        net = self.net
+        fc = next(op for op in net.ops if isinstance(op, Conv) and op.dst == net.output)
+        logits, bias = self.act[net.output], self.b[fc.name]
+        if trace: trace("softmax_xent", fc, stream=stream, logits=logits, bias=bias, labels=self.labels)
+        ops.softmax_xent(logits, self.labels, 1.0 / logits.shape[0], bias=bias, loss=self.loss_rows,
+                         dlogits=self.g, stream=stream)
+        if trace: trace("softmax_xent:end", fc, stream=stream, loss=self.loss_rows, dlogits=self.g)
+
+    def loss_value(self) -> float:
+        """The last step's batch-mean cross-entropy (host copy; synchronises)."""
+        return float(self.loss_rows.double().mean())
 
     def backward(self, trace=None, stream=None, side=None):
         """Gradients of every variable.  With ``side`` (a second stream), the filter gradient
@@ -207,7 +235,12 @@ class Replica:
             src_grad = op.src != "x" or net.input_grad
             beta = 1.0 if op.src in written else 0.0
             if isinstance(op, Conv):
-                if op.name in self.relu_fused:
+                if not op.relu:
+                    dpre = dy                        # bias only: the gradient passes through
+                    if trace: trace("bias_bwd", op, stream=stream, dy=dy)
+                    ops.bias_relu_bwd(None, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
+                    if trace: trace("bias_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
+                elif op.name in self.relu_fused:
                     dpre = dy                        # written by the fused pool / input-gradient backward
                 else:
                     y = self._slice(self.act, op)

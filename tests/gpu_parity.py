@@ -132,8 +132,10 @@ class ParityTracer:
         self.pending = None
         self.results = []           # (kind, op name, metric, value, bar, ok)
         net, k = rep.net, self.k
-        self.state = {("act", "x"): np.asarray(inputs.x[:k], np.float64),
-                      ("grad", net.output): np.asarray(inputs.g[:k], np.float64)}
+        self.state = {("act", "x"): np.asarray(inputs.x[:k], np.float64)}
+        if inputs.g is not None:
+            self.state[("grad", net.output)] = np.asarray(inputs.g[:k], np.float64)
+        self.labels = None if inputs.labels is None else np.asarray(inputs.labels[:k], np.int32)
         for c in net.convs:
             self.state[("W", c.name)] = np.asarray(inputs.weights[c.name], np.float64)
             self.state[("b", c.name)] = np.asarray(inputs.biases[c.name], np.float64)
@@ -301,7 +303,45 @@ class ParityTracer:
         self._set(out["y"], ref)
         self.state[("argmax", op.name)] = am
 
+    def _force_conv_fwd(self, op, t):
+        return {"x": self._force(t["x"]), "w": self._force(t["w"])}
+
+    def _check_conv_fwd(self, op, u, out):
+        ref = oracle.conv2d_fwd(u["x"], u["w"], (op.sh, op.sw), op.pads)
+        self.record_tensor("conv_fwd", op.name, self._got("conv_fwd", op.name, out["y"]), ref, self.dtype)
+        self._set(out["y"], ref)
+
+    # -------------------------------------------------------------- loss
+    def _force_softmax_xent(self, op, t):
+        lab = t["labels"]
+        lab.copy_(torch.from_numpy(np.tile(self.labels, self.tile)).to(lab.device))
+        return {"logits": self._force(t["logits"]), "bias": self._force(t["bias"]), "n": lab.numel()}
+
+    def _check_softmax_xent(self, op, u, out):
+        z = u["logits"].reshape(self.k, -1)
+        rows, dz = oracle.softmax_xent(z, self.labels, 1.0 / u["n"], bias=u["bias"])
+        loss = out["loss"]
+        if self.tile > 1:
+            first = loss[:self.k]
+            bad = sum(int((loss[r * self.k:(r + 1) * self.k] != first).sum()) for r in range(1, self.tile))
+            self.record("softmax_xent", op.name, "repeat_mismatch", float(bad), 0.0)
+        self.record_tensor("softmax_xent:loss", op.name, f64(loss[:self.k]), rows, torch.float32, torch.float32)
+        got = self._got("softmax_xent", op.name, out["dlogits"]).reshape(self.k, -1)
+        self.record_tensor("softmax_xent", op.name, got, dz, self.dtype, torch.float32)
+        self._set(out["dlogits"], dz.reshape((self.k,) + tuple(out["dlogits"].shape[1:])))
+
     # -------------------------------------------------------------- backward
+    def _force_bias_bwd(self, op, t):
+        return {"dy": self._force(t["dy"])}
+
+    def _check_bias_bwd(self, op, u, out):
+        dpre = self._got("bias_bwd", op.name, out["dpre"])
+        self.record("bias_bwd", op.name, "dpre_mismatch", float(np.sum(dpre != u["dy"])), 0.0)
+        ref_db = u["dy"].sum(axis=(0, 1, 2)) * self.tile
+        self.record_tensor("bias_bwd:db", op.name, f64(out["db"]), ref_db, torch.float32)
+        self._set(out["dpre"], u["dy"])
+        self._set(out["db"], ref_db)
+
     def _force_bias_relu_bwd(self, op, t):
         return {"y": self._force(t["y"]), "dy": self._force(t["dy"])}
 

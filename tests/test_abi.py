@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 6
+    assert lib.tfk_abi_version() == 7
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -228,6 +228,23 @@ def test_momentum_adam_validation(lib):
     assert adam(P, P + 0x1000, P + 0x2001, P + 0x3000, 16) == ALIGN
     assert adam(0, 0, 0, 0, 0) == OK
     assert b"" != lib.tfk_status_string(ARG)
+
+
+def test_softmax_xent_validation(lib):
+    f = ctypes.c_float
+    sm = lambda z, n, c, bias=None, lab=P + 0x10000, loss=P + 0x20000, dz=P + 0x30000, scale=1.0, dt=0: \
+        lib.tfk_softmax_xent(vp(z), dt, n, c, vp(bias) if bias else None, vp(lab), f(scale), vp(loss), vp(dz), None)
+    assert sm(P, -1, 10) == SHAPE
+    assert sm(P, 4, 0) == SHAPE
+    assert sm(P, 4, 10, dt=7) == DTYPE
+    assert sm(P, 4, 10, scale=float("nan")) == ARG
+    assert sm(P, 4, 10, dz=P + 8) == ALIAS                     # partial overlap with the logits
+    assert sm(P, 4, 10, loss=P + 0x10004) == ALIAS             # loss overlaps the labels
+    assert sm(P, 4, 10, bias=P + 0x20000) == ALIAS             # bias overlaps the loss
+    assert sm(P, 4, 10, lab=0) == NULL
+    assert sm(P + 2, 4, 10) == ALIGN
+    assert sm(P, 1 << 30, 1 << 20) == OVERFLOW
+    assert sm(0, 0, 10, lab=0, loss=0, dz=0) == OK             # no rows: nothing to touch
 
 
 def test_empty_batch_conv_fwd_is_noop(lib):

@@ -59,6 +59,10 @@ CONV_CASES = [
     # 288 tiles of 128 x 128 (most CUs with one block): 128 x 96 tiles, forward and input gradient
     ("bj96_tiles_fwd", 36, 32, 32, 64, 128, 3, 3, 1, 1, (1, 1, 1, 1)),
     ("bj96_tiles_bwd", 36, 32, 32, 128, 64, 3, 3, 1, 1, (1, 1, 1, 1)),
+    # fully connected layers as whole-window convolutions: AlexNet's fc6 (6x6x256 -> 4096) and
+    # fc8 (4096 -> 1000 logits), at batch 4
+    ("fc6_6x6_window", 4, 6, 6, 256, 4096, 6, 6, 1, 1, (0, 0, 0, 0)),
+    ("fc8_1x1_c4096_k1000", 4, 1, 1, 4096, 1000, 1, 1, 1, 1, (0, 0, 0, 0)),
 ]
 
 
@@ -530,3 +534,69 @@ def test_adam_and_momentum_steps_from_zero_state():
     gmax = max(float(np.max(np.abs(g))) for g in gs)
     vbound = 5 * 2 * U * (np.abs(ra) + 5 * gmax)
     assert np.all(np.abs(acc.cpu().numpy().astype(np.float64) - ra) <= vbound)
+
+
+# ----------------------------------------------------------------------------- softmax cross-entropy
+SOFTMAX_CASES = [("one_class", 1, 1), ("small", 5, 13), ("alexnet_b128", 128, 1000), ("ragged_rows", 7, 1000),
+                 ("wide_rows", 3, 4097)]
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
+@pytest.mark.parametrize("bias", [False, True], ids=["nobias", "bias"])
+@pytest.mark.parametrize("case", SOFTMAX_CASES, ids=[c[0] for c in SOFTMAX_CASES])
+def test_softmax_xent(case, bias, dtype):
+    name, n, c = case
+    say("softmax_xent", name, bias, dtype)
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    z = _mk((n, c), dtype, rng, 3.0)
+    b = torch.from_numpy(rng.standard_normal(c)).float().to(DEV) if bias else None
+    lab_np = rng.integers(0, c, size=n).astype(np.int32)
+    lab_np[0] = c - 1                              # the edge classes
+    if n > 1:
+        lab_np[1] = 0
+    lab = torch.from_numpy(lab_np).to(DEV)
+    loss, dz = ops.softmax_xent(z, lab, 1.0 / n, bias=b)
+    torch.cuda.synchronize()
+    rows, ref = oracle.softmax_xent(f64(z), lab_np, 1.0 / n, bias=None if b is None else f64(b))
+    assert_close(f64(loss), rows, torch.float32, label="loss rows")
+    assert_close(f64(dz), ref, dtype, torch.float32, label="dlogits")
+    # in place, and shifted by +1000 (the max is taken out: the same loss and gradient)
+    z2 = z.clone()
+    loss2, _ = ops.softmax_xent(z2, lab, 1.0 / n, bias=b, dlogits=z2)
+    torch.cuda.synchronize()
+    assert torch.equal(loss2, loss) and torch.equal(z2, dz)
+    if dtype == torch.float32 and b is None:
+        # (without a bias: with one, the kernel's fp32 sum logit + bias at magnitude 1000 rounds by
+        # up to 2^-14, an error of the inputs' scale that the oracle's fp64 sum does not make)
+        zs = z + 1000.0
+        loss3, dz3 = ops.softmax_xent(zs, lab, 1.0 / n, bias=b)
+        torch.cuda.synchronize()
+        rows3, ref3 = oracle.softmax_xent(f64(zs), lab_np, 1.0 / n, bias=None if b is None else f64(b))
+        assert np.all(np.isfinite(f64(loss3)))
+        # the shifted fp32 logits carry an absolute rounding of up to 2^-14: the bound is the
+        # oracle's on those same rounded logits
+        assert_close(f64(loss3), rows3, torch.float32, label="loss rows +1000")
+        assert_close(f64(dz3), ref3, torch.float32, label="dlogits +1000")
+
+
+def test_softmax_xent_bad_labels_give_nan_rows():
+    rng = np.random.default_rng(77)
+    z = _mk((4, 10), torch.float32, rng)
+    lab = torch.tensor([3, -1, 10, 0], dtype=torch.int32, device=DEV)
+    loss, dz = ops.softmax_xent(z, lab, 0.25)
+    torch.cuda.synchronize()
+    l = loss.cpu().numpy()
+    assert np.isnan(l[1]) and np.isnan(l[2]) and np.all(np.isfinite(l[[0, 3]]))
+    assert bool(torch.isnan(dz[1:3]).all()) and bool(torch.isfinite(dz[[0, 3]]).all())
+
+
+@pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
+def test_bias_only_backward(dtype):
+    """y = NULL: dpre = dy and the bias gradient is the column sums of dy (a logits layer)."""
+    rng = np.random.default_rng(78)
+    dy = _mk((128, 1, 1, 1000), dtype, rng)
+    dy0 = dy.clone()
+    dpre, db = ops.bias_relu_bwd(None, dy, dpre=dy)
+    torch.cuda.synchronize()
+    assert torch.equal(dpre, dy0)
+    assert_close(f64(db), f64(dy0).sum(axis=(0, 1, 2)), torch.float32, dtype, label="db")

@@ -120,6 +120,9 @@ SMALL = [
     ("vgg16_b2_32px", lambda: W.vgg16(batch=2, hw=32)),
     ("googlenet_b2", lambda: W.googlenet(batch=2)),
     ("inception_v3_b1", lambda: W.inception_v3(batch=1)),
+    ("classifier_small_f32", lambda: W.classifier_small(batch=4)),
+    ("classifier_small_bf16", lambda: W.classifier_small(batch=4, dtype="bf16")),
+    ("alexnet_classifier_b2", lambda: W.alexnet(batch=2, classifier=True)),
 ]
 
 
@@ -151,6 +154,36 @@ def test_alexnet_full_size_repeated_images():
     torch.cuda.synchronize()
     bad = _report(tr)
     assert not bad
+
+
+def test_alexnet_classifier_full_size_repeated_images():
+    """AlexNet with its classifier (fc 4096, 4096, 1000 and the softmax cross-entropy) at batch 128,
+    4 distinct images repeated 32 times, every op against the oracle."""
+    net = W.alexnet(batch=128, classifier=True)
+    inp = W.make_inputs(net, seed=0)
+    rep = Replica(net, inp)
+    tr = ParityTracer(rep, inp, distinct=4, label="alexnet_cls_b128")
+    rep.step(trace=tr)
+    torch.cuda.synchronize()
+    bad = _report(tr)
+    assert not bad
+
+
+def test_classifier_step_end_to_end():
+    """fp32 classifier step (conv, pool, fc + ReLU, fc logits, softmax cross-entropy) against the
+    oracle's step, end to end with no forcing: loss, every gradient and the input gradient."""
+    net = W.classifier_small(batch=4)
+    inp = W.make_inputs(net, seed=6)
+    rep = Replica(net, inp)
+    rep.step()
+    torch.cuda.synchronize()
+    ref = onet.step(net, inp.x, inp.weights, inp.biases, None, labels=inp.labels)
+    e = {"loss": abs(rep.loss_value() - ref["loss"]) / abs(ref["loss"]), "dx": err(f64(rep.grad["x"]), ref["grads"]["x"])}
+    for c in net.convs:
+        e["dW_" + c.name] = err(f64(rep.dW[c.name]), ref["dW"][c.name])
+        e["db_" + c.name] = err(f64(rep.db[c.name]), ref["db"][c.name])
+    say("classifier end-to-end:", {k: "%.2e" % v for k, v in e.items()})
+    assert all(v <= 1e-4 for v in e.values()), e
 
 
 @pytest.mark.parametrize("make", [lambda: W.single_layer(), lambda: W.googlenet(batch=4)],
