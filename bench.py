@@ -47,6 +47,9 @@ def parse():
                     help="two streams launched from the host (default), the two-stream step as a HIP graph, "
                          "or one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--classifier-steps", type=int, default=10,
+                    help="also time this many steps of AlexNet with its classifier (fc layers + softmax "
+                         "cross-entropy); 0 skips it")
     ap.add_argument("--cpu-sample", type=int, default=128, help="images of the batch the oracle steps through")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--gemm-reference", action="store_true",
@@ -168,6 +171,43 @@ class EventTrace:
             self.rec.append((kind, op0, s, self._event(stream)))
         else:
             self.open = (event, op, self._event(stream))
+
+
+def measure_classifier(args, torch, W, Replica):
+    """AlexNet with its classifier at the same batch: the two-stream step, and each classifier op
+    alone on one stream (HIP events), as a secondary figure (not the metric's workload)."""
+    net = W.alexnet(batch=args.batch, classifier=True)
+    inp = W.make_inputs(net, seed=args.seed)
+    rep = Replica(net, inp)
+    for _ in range(3):
+        rep.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.classifier_steps):
+        rep.step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.classifier_steps
+    tr = EventTrace(torch)
+    per = {}
+    reps = 3
+    for _ in range(reps):
+        tr.rec.clear()
+        rep.step(trace=tr, concurrent=False)
+        torch.cuda.synchronize()
+        for kind, op, s, e in tr.rec:
+            if op is not None and op.name.startswith("fc") or kind == "softmax_xent":
+                key = "%s/%s" % (kind, op.name)
+                per[key] = per.get(key, 0.0) + s.elapsed_time(e) / reps
+    fc_flop = 0.0
+    for op in net.convs:
+        if op.name.startswith("fc"):
+            f = conv_flops(net, op)
+            fc_flop += 3 * f if op.src != "x" else 2 * f
+    fc_gemm_ms = sum(v for k, v in per.items() if k.split("/")[0].startswith("conv"))
+    return {"workload": net.name, "ms_per_step": round(ms, 4), "images_per_s": round(args.batch / (ms * 1e-3), 1),
+            "params": rep.n_params, "loss_last_step": round(rep.loss_value(), 4),
+            "fc_gemm_tflops": round(fc_flop / (fc_gemm_ms * 1e-3) / 1e12, 1),
+            "per_op_ms": {k: round(v, 4) for k, v in sorted(per.items())}}
 
 
 def gemm_reference(net, torch):
@@ -333,6 +373,8 @@ def main():
                "this_net": dict(n=rep.n_params, **time_updates(torch, ops, rep.n_params)),
                "alexnet_with_classifier": dict(n=61_100_840, **time_updates(torch, ops, 61_100_840))}
 
+    classifier = measure_classifier(args, torch, W, Replica) if args.classifier_steps > 0 else None
+
     # ---------------------------------------------------------------- CPU baseline: the oracle
     cpu = None
     if not args.no_cpu_baseline:
@@ -392,6 +434,7 @@ def main():
                      "flop_per_launch": round(flops[dom] / n_dom)},
         "cpu_baseline": cpu,
         "updates": updates,
+        "classifier": classifier,
     }
     print(json.dumps(out))
     print("per-layer ms:", json.dumps({"%s/%s" % k: round(v, 4) for k, v in sorted(per_layer.items())}),

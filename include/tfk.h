@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 7
+#define TFK_ABI_VERSION 8
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -99,7 +99,10 @@ typedef struct {
  *   ws  : workspace of at least tfk_conv2d_workspace_bytes(0, ...) bytes
  *         (may be NULL when that is 0).
  * Requirements: pad < kernel extent on every side.
- * Image inputs (bf16, 1-4 channels) run as an equivalent 8-channel convolution over the
+ * A window that covers the whole unpadded image once (a fully connected layer over a
+ * densely stored x, output 1 x 1) runs as the 1 x 1 convolution of the flattened image;
+ * with few output tiles (small batch) its reduction is split across blocks into fp32
+ * partial sums in the workspace, added in a fixed order.  Image inputs (bf16, 1-4 channels) run as an equivalent 8-channel convolution over the
  * input padded to 4 (or 8) channels.  When x is already stored that way -- e.g. a
  * 3-channel view with pixel_stride 4 of an RGBx buffer, 16-byte aligned -- it is read in
  * place and not copied; the channels past xd.c then meet zero filter weights and must
@@ -135,6 +138,9 @@ TFK_API tfk_status tfk_conv2d_fwd_bias_relu(const void *x, tfk_nhwc xd, const vo
  *         cannot be recovered from dy, so the caller states it), type dt.
  *   beta: 0 overwrites dx; 1 adds to it (summing the partial gradients of
  *         several paths, Section 4.1).  With beta == 1, dx is read and written.
+ *   ws  : at least tfk_conv2d_workspace_bytes(1, ...) bytes (split-K partial sums
+ *         of fully connected layers at small batch, see tfk_conv2d_fwd; may be NULL
+ *         when that is 0).
  */
 TFK_API tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void *w, tfk_window p,
                                 tfk_dtype dt, void *dx, tfk_nhwc dxd, float beta,

@@ -132,6 +132,20 @@ tfk_status check_conv(tfk_nhwc &xd, int32_t cout, const tfk_window &p, tfk_dtype
 
 int64_t filter_bytes(const ConvShape &s, int64_t es) { return (int64_t)s.KH * s.KW * s.C * s.K * es; }
 
+// A window that covers the whole (unpadded, densely stored) image once is a fully connected layer:
+// x[n][h][w][c] and w[h][w][c][k] flatten to the same (h W + w) C + c order, so the convolution is
+// the 1 x 1 convolution of the flattened image, whose kernels do no per-tap work.  xs is the pixel
+// stride of x (or dx); it becomes the flattened row length.
+static void fold_full_window(ConvShape &s, int64_t &xs) {
+    if (s.OH == 1 && s.OW == 1 && s.KH == s.H && s.KW == s.W && s.pt == 0 && s.pl == 0 && (s.H > 1 || s.W > 1) &&
+        xs == s.C) {
+        s.C = s.H * s.W * s.C;
+        s.H = s.W = s.KH = s.KW = 1;
+        s.sh = s.sw = 1;
+        xs = s.C;
+    }
+}
+
 tfk_status check_ws(void *ws, size_t ws_bytes, size_t need) {
     if (need == 0) return TFK_OK;
     if (!ws) return fail(TFK_ERR_WORKSPACE, "workspace of %zu bytes required, got NULL", need);
@@ -166,15 +180,20 @@ const char *tfk_status_string(tfk_status s) {
 
 // ------------------------------------------------------------------ convolution
 size_t tfk_conv2d_workspace_bytes(int32_t op, tfk_nhwc xd, int32_t cout, tfk_window p, tfk_dtype dt) {
-    if (op != 0 && op != 2 && op != 3) return 0;
+    if (op < 0 || op > 3) return 0;
     if (!valid_dt(dt) || check_view("x", xd) != TFK_OK || check_window(p) != TFK_OK || cout < 1) return 0;
     const int oh = out_len(xd.h, p.kh, p.stride_h, p.pad_top, p.pad_bottom);
     const int ow = out_len(xd.w, p.kw, p.stride_w, p.pad_left, p.pad_right);
     if (oh < 1 || ow < 1 || xd.n == 0) return 0;
     ConvShape s{xd.n, xd.h, xd.w, xd.c, oh, ow, cout, p.kh, p.kw, p.stride_h, p.stride_w, p.pad_top, p.pad_left};
     const int dti = dt == TFK_F32 ? 0 : 1;
-    if (op == 0) return conv_fold_applies(dti, s) ? conv_fold_ws_bytes(0, s) : 0;
-    if (op == 3) return conv_bwd_data_relu_ws_bytes(dti, s, xd.pixel_stride ? xd.pixel_stride : xd.c);
+    // (the fused ReLU backward sums its bias gradient per channel: no flattening there)
+    if (op == 3) return conv_bwd_data_relu_ws_bytes(dti, s, xd.pixel_stride);
+    int64_t xs = xd.pixel_stride;
+    fold_full_window(s, xs);
+    if (op == 0) return std::max(conv_fold_applies(dti, s) ? conv_fold_ws_bytes(0, s) : 0,
+                                 conv_fwd_split_ws_bytes(dti, s));
+    if (op == 1) return conv_bwd_data_ws_bytes(dti, s);
     return conv_bwd_filter_ws_bytes(dti, s);
 }
 
@@ -196,13 +215,17 @@ static tfk_status conv_fwd_impl(const void *x, tfk_nhwc xd, const void *w, int32
     if (overlap(y, yb, x, view_bytes(xd, es)) || overlap(y, yb, w, filter_bytes(s, es)))
         return fail(TFK_ERR_ALIAS, "y overlaps x or w");
     if (bias != nullptr && overlap(y, yb, bias, (int64_t)cout * 4)) return fail(TFK_ERR_ALIAS, "y overlaps bias");
+    const int64_t xbytes = view_bytes(xd, es), wbytes = filter_bytes(s, es);
+    int64_t xs = xd.pixel_stride;
+    fold_full_window(s, xs);
     const int dti = dt == TFK_F32 ? 0 : 1;
-    const size_t need = conv_fold_applies(dti, s) ? conv_fold_ws_bytes(0, s) : 0;
+    const size_t need = std::max(conv_fold_applies(dti, s) ? conv_fold_ws_bytes(0, s) : 0,
+                                 conv_fwd_split_ws_bytes(dti, s));
     TRY(check_ws(ws, ws_bytes, need));
-    if (need && (overlap(ws, (int64_t)need, x, view_bytes(xd, es)) || overlap(ws, (int64_t)need, w, filter_bytes(s, es)) ||
+    if (need && (overlap(ws, (int64_t)need, x, xbytes) || overlap(ws, (int64_t)need, w, wbytes) ||
                  overlap(ws, (int64_t)need, y, yb)))
         return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
-    return hip_status(launch_conv_fwd(dti, x, xd.pixel_stride, w, y, yd.pixel_stride, s, bias, need ? ws : nullptr,
+    return hip_status(launch_conv_fwd(dti, x, xs, w, y, yd.pixel_stride, s, bias, need ? ws : nullptr,
                                       (hipStream_t)stream),
                       what);
 }
@@ -224,8 +247,6 @@ tfk_status tfk_conv2d_fwd_bias_relu(const void *x, tfk_nhwc xd, const void *w, i
 
 tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void *w, tfk_window p, tfk_dtype dt, void *dx,
                                 tfk_nhwc dxd, float beta, void *ws, size_t ws_bytes, void *stream) {
-    (void)ws;
-    (void)ws_bytes;
     ConvShape s;
     TRY(check_conv(dxd, dyd.c, p, dt, dyd, "dx", "dy", s));
     if (!(beta == 0.f || beta == 1.f)) return fail(TFK_ERR_ARG, "beta must be 0 or 1");
@@ -240,8 +261,17 @@ tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void *w, tfk
     const int64_t xb = view_bytes(dxd, es);
     if (overlap(dx, xb, dy, view_bytes(dyd, es)) || overlap(dx, xb, w, filter_bytes(s, es)))
         return fail(TFK_ERR_ALIAS, "dx overlaps dy or w");
-    return hip_status(launch_conv_bwd_data(dt == TFK_F32 ? 0 : 1, dy, dyd.pixel_stride, w, dx, dxd.pixel_stride,
-                                           beta, s, (hipStream_t)stream),
+    const int64_t wbytes = filter_bytes(s, es);
+    int64_t xs = dxd.pixel_stride;
+    fold_full_window(s, xs);
+    const int dti = dt == TFK_F32 ? 0 : 1;
+    const size_t need = conv_bwd_data_ws_bytes(dti, s);
+    TRY(check_ws(ws, ws_bytes, need));
+    if (need && (overlap(ws, (int64_t)need, dy, view_bytes(dyd, es)) || overlap(ws, (int64_t)need, w, wbytes) ||
+                 overlap(ws, (int64_t)need, dx, xb)))
+        return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
+    return hip_status(launch_conv_bwd_data(dti, dy, dyd.pixel_stride, w, dx, xs, beta, s,
+                                           need ? (float *)ws : nullptr, (hipStream_t)stream),
                       "conv2d_bwd_input");
 }
 
@@ -271,7 +301,7 @@ tfk_status tfk_conv2d_bwd_input_relu_bwd(const void *dy, tfk_nhwc dyd, const voi
         overlap(dbias, bb, dpre, xb))
         return fail(TFK_ERR_ALIAS, "dbias overlaps a tensor");
     const int dti = dt == TFK_F32 ? 0 : 1;
-    const int64_t xs = xd.pixel_stride ? xd.pixel_stride : xd.c;
+    const int64_t xs = xd.pixel_stride;      // (not flattened: the bias gradient is per channel)
     const size_t need = conv_bwd_data_relu_ws_bytes(dti, s, xs);
     TRY(check_ws(ws, ws_bytes, need));
     if (overlap(ws, (int64_t)need, dy, yb) || overlap(ws, (int64_t)need, w, wb) || overlap(ws, (int64_t)need, y, xb) ||
@@ -297,15 +327,17 @@ tfk_status tfk_conv2d_bwd_filter(const void *x, tfk_nhwc xd, const void *dy, tfk
     TRY(need_align(x, es, "x"));
     TRY(need_align(dy, es, "dy"));
     const int dti = dt == TFK_F32 ? 0 : 1;
+    const int64_t xb = view_bytes(xd, es), yb = view_bytes(dyd, es);
+    int64_t xs = xd.pixel_stride;
+    fold_full_window(s, xs);
     const size_t need = conv_bwd_filter_ws_bytes(dti, s);
     TRY(check_ws(ws, ws_bytes, need));
-    const int64_t xb = view_bytes(xd, es), yb = view_bytes(dyd, es);
     if (overlap(dw, wb, x, xb) || overlap(dw, wb, dy, yb))
         return fail(TFK_ERR_ALIAS, "dw overlaps x or dy");
     if (need && (overlap(ws, (int64_t)need, x, xb) || overlap(ws, (int64_t)need, dy, yb) ||
                  overlap(ws, (int64_t)need, dw, wb)))
         return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
-    return hip_status(launch_conv_bwd_filter(dti, x, xd.pixel_stride, dy, dyd.pixel_stride, dw, s, ws, st),
+    return hip_status(launch_conv_bwd_filter(dti, x, xs, dy, dyd.pixel_stride, dw, s, ws, st),
                       "conv2d_bwd_filter");
 }
 
@@ -586,7 +618,7 @@ tfk_status tfk_softmax_xent(const void *logits, tfk_dtype dt, int64_t n, int32_t
         for (int j = i + 1; j < 5; ++j)
             if (!(i == 0 && j == 4) && overlap(p[i], b[i], p[j], b[j]))
                 return fail(TFK_ERR_ALIAS, "softmax_xent operands overlap");
-    if ((n + 3) / 4 > INT32_MAX) return fail(TFK_ERR_OVERFLOW, "too many rows");
+    if (n > INT32_MAX) return fail(TFK_ERR_OVERFLOW, "too many rows");
     return hip_status(launch_softmax_xent(dt == TFK_F32 ? 0 : 1, logits, bias, labels, n, c, scale, loss, dlogits,
                                           (hipStream_t)stream),
                       "softmax_xent");

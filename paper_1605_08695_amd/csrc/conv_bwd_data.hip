@@ -13,12 +13,33 @@ static int relu_partial_rows(const ConvShape &s) {
     return z * ((mj + t.bj - 1) / t.bj) * (t.nw / 2);
 }
 
-// relu_y / db_part: the fused ReLU backward of the pipelined kernel (beta 0; false is returned
-// when that kernel does not run, and nothing is launched then).
+// Split-K for 1 x 1 filters at stride 1 with few output tiles (the fully connected layers at
+// small batch): fp32 partials in the workspace, then one epilogue pass (beta, or the fused ReLU
+// backward with partial column sums after the partials).
+static int bwd_data_splits(const ConvShape &s, int *k_split) {
+    *k_split = 0;
+    if (s.KH * s.KW != 1 || s.sh != 1 || s.sw != 1) return 1;
+    return gemm_split_plan(s.C, s.N * s.H * s.W, (int64_t)s.K, k_split);
+}
+
+static size_t split_ws_bytes(int dt, const ConvShape &s, bool relu) {
+    int ks;
+    const int sp = bwd_data_splits(s, &ks);
+    if (dt != 1 || sp <= 1) return 0;
+    const int64_t mj = (int64_t)s.N * s.H * s.W;
+    return (size_t)((sp + (relu ? 1 : 0)) * mj) * s.C * sizeof(float);
+}
+
+size_t conv_bwd_data_ws_bytes(int dt, const ConvShape &s) { return split_ws_bytes(dt, s, false); }
+
+// ws: workspace (split-K partials; with relu_y also the bias-gradient partials).
+// relu_y: the fused ReLU backward (beta 0); *db_parts / *db_at receive the number and place of
+// the bias-gradient partial rows, or 0 when the fused kernels do not apply (nothing is launched
+// then).
 template <typename T>
 static hipError_t conv_bwd_data_t(const void *dy, int64_t dys, const void *w, void *dx, int64_t dxs, float beta,
-                                  const ConvShape &s, hipStream_t st, const void *relu_y = nullptr,
-                                  float *db_part = nullptr, bool *fused = nullptr) {
+                                  const ConvShape &s, hipStream_t st, float *ws, const void *relu_y = nullptr,
+                                  int *db_parts = nullptr, float **db_at = nullptr) {
     constexpr int EPC = Elem<T>::kPerChunk;
     IgArgs a;
     fill_geom(a, s);
@@ -38,11 +59,39 @@ static hipError_t conv_bwd_data_t(const void *dy, int64_t dys, const void *w, vo
         if (vi && vj && s.C % 8 == 0 && dxs % 8 == 0 && aligned16p(dx) &&
             igemm2_fits(a, wb, span_bytes((int64_t)s.N * s.OH * s.OW, dys, s.K))) {
             const int z = s.sh * s.sw;
+            int ks;
+            const int sp = ws != nullptr && aligned16p(ws) ? bwd_data_splits(s, &ks) : 1;
+            if (sp > 1) {
+                a.k_split = ks;
+                a.split_stride = (int64_t)mj * a.NI;
+                a.out = ws;
+                if (!igemm2_launch<DIR_BWD_DATA>(a, mj, sp, igemm2_tiles(a.NI, mj, sp), st))
+                    return hipErrorInvalidValue;
+                const hipError_t e = hipGetLastError();
+                if (e != hipSuccess) return e;
+                SplitEpi ep{};
+                ep.part = ws;
+                ep.splits = sp;
+                ep.rows = mj;
+                ep.ni = a.NI;
+                ep.split_stride = a.split_stride;
+                ep.ostride = dxs;
+                ep.out = dx;
+                ep.beta = beta;
+                ep.relu_y = relu_y;
+                if (relu_y != nullptr) {                 // one partial row per output row
+                    ep.db_part = ws + (int64_t)sp * mj * a.NI;
+                    *db_parts = mj;
+                    *db_at = ep.db_part;
+                }
+                return launch_split_epilogue(ep, st);
+            }
             if (relu_y != nullptr) {
                 a.relu_y = relu_y;
-                a.db_part = db_part;
+                a.db_part = ws;
                 a.db_rows = relu_partial_rows(s);
-                *fused = true;
+                *db_parts = a.db_rows;
+                *db_at = ws;
             }
             if (!igemm2_launch<DIR_BWD_DATA>(a, mj, z, igemm2_tiles(a.NI, mj, z), st)) return hipErrorInvalidValue;
             return hipGetLastError();
@@ -58,27 +107,28 @@ size_t conv_bwd_data_relu_ws_bytes(int dt, const ConvShape &s, int64_t dxs) {
     relu_bwd_plan(dt, (int64_t)s.N * s.H * s.W, s.C, dxs, &G, &ppb);
     const size_t fallback = (size_t)G * s.C * sizeof(float);
     if (dt != 1) return fallback;
-    return std::max(fallback, (size_t)relu_partial_rows(s) * s.C * sizeof(float));
+    return std::max({fallback, (size_t)relu_partial_rows(s) * s.C * sizeof(float), split_ws_bytes(dt, s, true)});
 }
 
 hipError_t launch_conv_bwd_data_relu(int dt, const void *dy, int64_t dys, const void *w, void *dpre, int64_t dxs,
                                      const void *y, float *db, float *ws, const ConvShape &s, hipStream_t st) {
-    bool fused = false;
+    int parts = 0;
+    float *db_at = nullptr;
     if (dt == 1 && ((uintptr_t)y & 7) == 0) {
-        const hipError_t e = conv_bwd_data_t<bf16_t>(dy, dys, w, dpre, dxs, 0.f, s, st, y, ws, &fused);
+        const hipError_t e = conv_bwd_data_t<bf16_t>(dy, dys, w, dpre, dxs, 0.f, s, st, ws, y, &parts, &db_at);
         if (e != hipSuccess) return e;
-        if (fused) return launch_sum_partials(ws, relu_partial_rows(s), s.C, db, st);
+        if (parts > 0) return launch_sum_partials(db_at, parts, s.C, db, st);
     }
     // otherwise the two ops in sequence: the input gradient, then the ReLU backward in place
-    const hipError_t e = launch_conv_bwd_data(dt, dy, dys, w, dpre, dxs, 0.f, s, st);
+    const hipError_t e = launch_conv_bwd_data(dt, dy, dys, w, dpre, dxs, 0.f, s, nullptr, st);
     if (e != hipSuccess) return e;
     return launch_bias_relu_bwd(dt, y, dpre, dpre, (int64_t)s.N * s.H * s.W, s.C, dxs, db, ws, st);
 }
 
 hipError_t launch_conv_bwd_data(int dt, const void *dy, int64_t dys, const void *w, void *dx, int64_t dxs,
-                                float beta, const ConvShape &s, hipStream_t st) {
-    return dt == 0 ? conv_bwd_data_t<float>(dy, dys, w, dx, dxs, beta, s, st)
-                   : conv_bwd_data_t<bf16_t>(dy, dys, w, dx, dxs, beta, s, st);
+                                float beta, const ConvShape &s, float *ws, hipStream_t st) {
+    return dt == 0 ? conv_bwd_data_t<float>(dy, dys, w, dx, dxs, beta, s, st, ws)
+                   : conv_bwd_data_t<bf16_t>(dy, dys, w, dx, dxs, beta, s, st, ws);
 }
 
 }  // namespace tfk

@@ -799,11 +799,63 @@ __global__ __launch_bounds__(256) void opt_kernel(float *__restrict__ var, float
     }
 }
 
+// ------------------------------------------------------------------ split-K epilogue
+// One thread per output row j and group of four channels i (consecutive threads: consecutive
+// groups of one row); the split partials are independent 16-byte loads, added in split order.
+__global__ __launch_bounds__(256) void split_epilogue_kernel(SplitEpi e) {
+    const int groups = e.ni / 4;
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int j = (int)(t / groups);
+    if (j >= e.rows) return;
+    const int i = (int)(t - (int64_t)j * groups) * 4;
+    const float *p = e.part + (int64_t)j * e.ni + i;
+    float4 v = *reinterpret_cast<const float4 *>(p);
+    for (int s = 1; s < e.splits; ++s) {
+        const float4 w = *reinterpret_cast<const float4 *>(p + (int64_t)s * e.split_stride);
+        v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
+    }
+    float r[4] = {v.x, v.y, v.z, v.w};
+    bf16_t *o = reinterpret_cast<bf16_t *>(e.out) + (int64_t)j * e.ostride + i;
+    if (e.bias != nullptr)
+        for (int q = 0; q < 4; ++q) r[q] = fmaxf(r[q] + e.bias[i + q], 0.f);
+    if (e.beta != 0.f) {
+        const uint2 old = *reinterpret_cast<const uint2 *>(o);
+        r[0] += e.beta * bf16_to_f32(old.x & 0xffffu);
+        r[1] += e.beta * bf16_to_f32(old.x >> 16);
+        r[2] += e.beta * bf16_to_f32(old.y & 0xffffu);
+        r[3] += e.beta * bf16_to_f32(old.y >> 16);
+    }
+    if (e.relu_y != nullptr) {
+        const uint2 yv = *reinterpret_cast<const uint2 *>(reinterpret_cast<const bf16_t *>(e.relu_y) +
+                                                          (int64_t)j * e.ostride + i);
+        const float yq[4] = {bf16_to_f32(yv.x & 0xffffu), bf16_to_f32(yv.x >> 16), bf16_to_f32(yv.y & 0xffffu),
+                             bf16_to_f32(yv.y >> 16)};
+        for (int q = 0; q < 4; ++q) r[q] = yq[q] > 0.f ? r[q] : 0.f;
+    }
+    uint2 pk;
+    pk.x = pack_bf16x2(r[0], r[1]);
+    pk.y = pack_bf16x2(r[2], r[3]);
+    *reinterpret_cast<uint2 *>(o) = pk;
+    if (e.db_part != nullptr) {                   // this row's stored values: partial [i][j]
+        e.db_part[(int64_t)(i + 0) * e.rows + j] = bf16_to_f32(pk.x & 0xffffu);
+        e.db_part[(int64_t)(i + 1) * e.rows + j] = bf16_to_f32(pk.x >> 16);
+        e.db_part[(int64_t)(i + 2) * e.rows + j] = bf16_to_f32(pk.y & 0xffffu);
+        e.db_part[(int64_t)(i + 3) * e.rows + j] = bf16_to_f32(pk.y >> 16);
+    }
+}
+
+hipError_t launch_split_epilogue(const SplitEpi &e, hipStream_t st) {
+    const int64_t threads = (int64_t)(e.ni / 4) * e.rows;
+    hipLaunchKernelGGL(split_epilogue_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, e);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ softmax cross-entropy
-// One wave per row of n x c logits (z = logits + bias): the row max, then the sum of exp(z - max),
-// both reduced across the wave by a fixed xor tree, then the loss and the gradient
-// scale * (softmax - onehot).  Each lane reads and writes only its own columns, so dz may be the
-// logits buffer itself.
+// One block of 256 threads per row of n x c logits (z = logits + bias): the row max, then the
+// sum of exp(z - max), each reduced over the block by a fixed tree (xor shuffles inside each
+// wave, then the four wave results in order), then the loss and the gradient
+// scale * (softmax - onehot).  Each thread reads and writes only its own columns, so dz may be
+// the logits buffer itself.
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
@@ -819,27 +871,32 @@ template <typename T>
 __global__ __launch_bounds__(256) void softmax_xent_kernel(const T *z, const float *__restrict__ bias,
                                                            const int32_t *__restrict__ labels, int64_t n, int c,
                                                            float scale, float *__restrict__ loss, T *dz) {
-    const int lane = threadIdx.x & 63;
-    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (row >= n) return;
+    __shared__ float red[2][4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t row = blockIdx.x;
     const T *zr = z + row * c;
     T *dr = dz + row * c;
     const int lab = labels[row];
-    if (lab < 0 || lab >= c) {
-        for (int j = lane; j < c; j += 64) Elem<T>::store(dr + j, __builtin_nanf(""));
-        if (lane == 0) loss[row] = __builtin_nanf("");
+    if (lab < 0 || lab >= c) {                    // (uniform over the block)
+        for (int j = tid; j < c; j += 256) Elem<T>::store(dr + j, __builtin_nanf(""));
+        if (tid == 0) loss[row] = __builtin_nanf("");
         return;
     }
     float m = -INFINITY;
-    for (int j = lane; j < c; j += 64) m = fmaxf(m, Elem<T>::load(zr + j) + (bias ? bias[j] : 0.f));
+    for (int j = tid; j < c; j += 256) m = fmaxf(m, Elem<T>::load(zr + j) + (bias ? bias[j] : 0.f));
     m = wave_max(m);
+    if (lane == 0) red[0][wave] = m;
+    __syncthreads();
+    m = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
     float sum = 0.f;
-    for (int j = lane; j < c; j += 64) sum += expf(Elem<T>::load(zr + j) + (bias ? bias[j] : 0.f) - m);
+    for (int j = tid; j < c; j += 256) sum += expf(Elem<T>::load(zr + j) + (bias ? bias[j] : 0.f) - m);
     sum = wave_sum(sum);
-    const float zl = Elem<T>::load(zr + lab) + (bias ? bias[lab] : 0.f);
-    if (lane == 0) loss[row] = m + logf(sum) - zl;
+    if (lane == 0) red[1][wave] = sum;
+    __syncthreads();
+    sum = ((red[1][0] + red[1][1]) + red[1][2]) + red[1][3];
+    if (tid == 0) loss[row] = m + logf(sum) - (Elem<T>::load(zr + lab) + (bias ? bias[lab] : 0.f));
     const float inv = 1.f / sum;
-    for (int j = lane; j < c; j += 64) {
+    for (int j = tid; j < c; j += 256) {
         const float p = expf(Elem<T>::load(zr + j) + (bias ? bias[j] : 0.f) - m) * inv;
         Elem<T>::store(dr + j, scale * (j == lab ? p - 1.f : p));
     }
@@ -847,13 +904,12 @@ __global__ __launch_bounds__(256) void softmax_xent_kernel(const T *z, const flo
 
 hipError_t launch_softmax_xent(int dt, const void *z, const float *bias, const int32_t *labels, int64_t n, int c,
                                float scale, float *loss, void *dz, hipStream_t st) {
-    const int64_t blocks = (n + 3) / 4;
     if (dt == 0)
-        hipLaunchKernelGGL(softmax_xent_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, (const float *)z, bias,
+        hipLaunchKernelGGL(softmax_xent_kernel<float>, dim3((unsigned)n), dim3(256), 0, st, (const float *)z, bias,
                            labels, n, c, scale, loss, (float *)dz);
     else
-        hipLaunchKernelGGL(softmax_xent_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st, (const bf16_t *)z,
-                           bias, labels, n, c, scale, loss, (bf16_t *)dz);
+        hipLaunchKernelGGL(softmax_xent_kernel<bf16_t>, dim3((unsigned)n), dim3(256), 0, st, (const bf16_t *)z, bias,
+                           labels, n, c, scale, loss, (bf16_t *)dz);
     return hipGetLastError();
 }
 

@@ -193,8 +193,12 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
         k_end = a.KH * a.KW * a.C;
         KHp = a.KH;
         KWp = a.KW;
+        if (a.k_split > 0) {                       // split-K: blockIdx.z picks a reduction range
+            k_beg = bz * a.k_split;
+            k_end = min(k_end, k_beg + a.k_split);
+        }
     } else if constexpr (DIR == DIR_BWD_DATA) {
-        const int z = bz;
+        const int z = a.k_split > 0 ? 0 : bz;      // (split-K runs with one stride phase)
         rh = z / a.sw;
         rw = z - rh * a.sw;
         h0 = ((rh - a.pt) % a.sh + a.sh) % a.sh;
@@ -207,6 +211,10 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
         KWp = rw < a.KW ? (a.KW - rw + a.sw - 1) / a.sw : 0;
         MJ_ext = a.N * Hp * Wp;
         k_end = KHp * KWp * a.K;
+        if (a.k_split > 0) {
+            k_beg = bz * a.k_split;
+            k_end = min(k_end, k_beg + a.k_split);
+        }
     } else {
         MJ_ext = a.KH * a.KW * a.C;
         k_beg = bz * a.k_split;
@@ -549,6 +557,13 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
             const int i = i0 + wi * WI + x * 16 + 4 * lg;
             if (i >= a.NI) continue;
             const f32x4_t v = acc[x][y];
+            if constexpr (DIR != DIR_BWD_FILTER) {
+                if (a.k_split > 0) {                   // split-K: fp32 partial [split][row][NI]
+                    float *o = reinterpret_cast<float *>(a.out) + (int64_t)bz * a.split_stride + (int64_t)j * a.NI + i;
+                    *reinterpret_cast<f32x4_t *>(o) = v;
+                    continue;
+                }
+            }
             if constexpr (DIR == DIR_BWD_FILTER) {
                 float *o = reinterpret_cast<float *>(a.out) + rowoff + i;
                 *reinterpret_cast<f32x4_t *>(o) = v;          // NI % 8 == 0 and rows 16-byte aligned

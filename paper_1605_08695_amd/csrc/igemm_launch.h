@@ -55,7 +55,8 @@ static inline Igemm2Tile igemm2_tiles(int ni, int mj, int zdim) {
         // 128-row tiles that leave most CUs with one block (AlexNet conv4/conv5: 338 blocks)
         // spread better as 96-row tiles, still within one round of two blocks per CU
         const int64_t b128 = (ni / 128) * blocks_j, b96 = (ni / 128) * (int64_t)((mj + 95) / 96) * zdim;
-        if (b128 < 448 && b96 <= 512) return {128, 96, 4, 2};
+        // (not for a single row of tiles: 96-row tiles would leave most of the second row empty)
+        if (b128 < 448 && b96 <= 512 && mj > 128) return {128, 96, 4, 2};
         return {128, 128, 4, 2};
     }
     if (ni % 192 == 0 && (ni / 192) * blocks_j >= 256) return {192, 128, 4, 2};
@@ -95,6 +96,21 @@ static bool igemm2_launch(IgArgs &a, int mj, int zdim, const Igemm2Tile &t, hipS
     case (1 << 12) | (4 << 8) | (4 << 4) | 2: igemm2_go<DIR, 64, 256, 4, 2>(a, grid, st); return true;
     default: return false;
     }
+}
+
+// Split-K for GEMMs with few output tiles (fully connected layers at small batch): the
+// reduction is cut into ranges of whole 64-wide K tiles, one per blockIdx.z, so that about 256
+// blocks run, each range keeping at least 8 K tiles.  Returns the number of ranges (1: no split)
+// and sets k_split to the range length in reduction elements.
+static inline int gemm_split_plan(int ni, int mj, int64_t kred, int *k_split) {
+    const int64_t blocks = (int64_t)((ni + 127) / 128) * ((mj + 127) / 128);
+    const int64_t ktiles = (kred + 63) / 64;
+    const int64_t sp = std::min<int64_t>((256 + blocks - 1) / blocks, ktiles / 8);
+    *k_split = 0;
+    if (blocks >= 128 || sp < 2) return 1;
+    const int64_t per = (ktiles + sp - 1) / sp;
+    *k_split = (int)(per * 64);
+    return (int)((ktiles + per - 1) / per);
 }
 
 // Bytes from the first element of a pixel-major bf16 operand to the end of its last

@@ -43,7 +43,10 @@ struct SgdBatch {
 hipError_t launch_conv_fwd(int dt, const void *x, int64_t xs, const void *w, void *y, int64_t ys,
                            const ConvShape &s, const float *bias, void *ws, hipStream_t st);
 hipError_t launch_conv_bwd_data(int dt, const void *dy, int64_t dys, const void *w, void *dx, int64_t dxs,
-                                float beta, const ConvShape &s, hipStream_t st);
+                                float beta, const ConvShape &s, float *ws, hipStream_t st);
+// Workspace of the split-K forward / input gradient (0: no split for this shape).
+size_t conv_fwd_split_ws_bytes(int dt, const ConvShape &s);
+size_t conv_bwd_data_ws_bytes(int dt, const ConvShape &s);
 // Input gradient fused with the ReLU backward + bias gradient of the layer that produced x:
 // dpre = y > 0 ? bwd_input(dy, w) : +0 (dx's view), db = column sums of dpre; ws: partials.
 hipError_t launch_conv_bwd_data_relu(int dt, const void *dy, int64_t dys, const void *w, void *dpre, int64_t dxs,
@@ -89,6 +92,22 @@ hipError_t launch_maxpool_relu_bwd(int dt, const void *dy, const void *am, bool 
                                    const void *y, void *dpre, float beta, float *db, float *ws, hipStream_t st);
 hipError_t launch_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh, hipStream_t st);
 hipError_t launch_sgd_multi(const SgdBatch &b, float lr, hipStream_t st);
+// Epilogue of a split-K forward or input-gradient GEMM: out[j][i] = f(sum over splits, in split
+// order, of part[s][j][i]) stored as bf16 at out + j * ostride + i, with f adding bias then ReLU
+// (forward, bias set), beta * old out (input gradient), or the ReLU backward mask y > 0 of the
+// producing layer (relu_y set; the stored values also go to db_part[i][j], the rows of the
+// bias gradient's partial sums).
+struct SplitEpi {
+    const float *part;
+    int splits, rows, ni;
+    int64_t split_stride, ostride;
+    void *out;
+    const float *bias;
+    float beta;
+    const void *relu_y;
+    float *db_part;
+};
+hipError_t launch_split_epilogue(const SplitEpi &e, hipStream_t st);
 // Softmax cross-entropy of n x c logits (+ bias) against labels: per-row loss and
 // dz = scale * (softmax - onehot); dz may be z.
 hipError_t launch_softmax_xent(int dt, const void *z, const float *bias, const int32_t *labels, int64_t n, int c,

@@ -113,14 +113,18 @@ def conv2d_fwd_bias_relu(x, w, bias, stride, pads, y=None, ws=None, stream=None)
     return _conv_fwd(x, w, bias, stride, pads, y, ws, stream)
 
 
-def conv2d_bwd_input(dy, w, dx, stride, pads, beta=0.0, stream=None):
+def conv2d_bwd_input(dy, w, dx, stride, pads, beta=0.0, ws=None, stream=None):
     """dx (= or +=) conv2d_fwd^T(dy).  dx gives the forward input's shape (it is written)."""
     lib = load()
     kh, kw, cin, cout = w.shape
     if not (w.dtype == dy.dtype == dx.dtype):
         raise TypeError("dy, w and dx must share one dtype")
-    check(lib.tfk_conv2d_bwd_input(_ptr(dy), nhwc(dy), _ptr(w), window(kh, kw, stride, pads), _dt(dy), _ptr(dx),
-                                   nhwc(dx), float(beta), None, 0, _stream(stream)))
+    win = window(kh, kw, stride, pads)
+    need = lib.tfk_conv2d_workspace_bytes(1, nhwc(dx), cout, win, _dt(dx))
+    if need and (ws is None or ws.numel() < need):
+        ws = _ws(need, dx.device)
+    check(lib.tfk_conv2d_bwd_input(_ptr(dy), nhwc(dy), _ptr(w), win, _dt(dy), _ptr(dx), nhwc(dx), float(beta),
+                                   _ptr(ws) if need else None, need, _stream(stream)))
     return dx
 
 

@@ -162,7 +162,7 @@ class Replica:
         need = 0
         for c in net.convs:
             x = self.act[c.src]
-            for op_kind in (0, 2, 3) if c.name in self.bwi_relu else (0, 2):
+            for op_kind in (0, 1, 2, 3) if c.name in self.bwi_relu else (0, 1, 2):
                 need = max(need, ops.conv2d_workspace_bytes(op_kind, x, c.cout, c.kh, c.kw, (c.sh, c.sw), c.pads))
             need = max(need, ops.bias_relu_bwd_workspace_bytes(self._slice(self.act, c)))
         self.ws = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=dev)
@@ -272,7 +272,7 @@ class Replica:
                     if trace: trace("conv_bwd_input", op, stream=stream, dy=dpre, w=self.Wlp[op.name], dx=dx,
                                     beta=beta)
                     ops.conv2d_bwd_input(dpre, self.Wlp[op.name], dx, (op.sh, op.sw), op.pads, beta=beta,
-                                         stream=stream)
+                                         ws=self.ws, stream=stream)
                     if trace: trace("conv_bwd_input:end", op, stream=stream, dx=dx)
             elif op.name in self.pool_relu:
                 conv = self.pool_relu[op.name]

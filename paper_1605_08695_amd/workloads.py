@@ -192,8 +192,9 @@ def alexnet(batch=128, classifier=False) -> Net:
     """AlexNet-shaped conv stack, bf16: 11x11/4 p2 64, pool 3/2, 5x5 p2 192, pool, 3x3 384, 256, 256, pool.
     With ``classifier``: then fc 4096 + ReLU, fc 4096 + ReLU, fc 1000 logits and the softmax
     cross-entropy of 1000 classes (no dropout)."""
-    b = _Builder("alexnet%s_b%d" % ("_cls" if classifier else "", batch), "bf16", 0.01, False,
-                 (batch, 224, 224, 3))
+    # (the He-initialised classifier on N(0, 1) images diverges at lr 0.01; 1e-4 lowers its loss)
+    b = _Builder("alexnet%s_b%d" % ("_cls" if classifier else "", batch), "bf16", 1e-4 if classifier else 0.01,
+                 False, (batch, 224, 224, 3))
     t = b.conv("x", 64, 11, s=4, pads=(2, 2, 2, 2), name="conv1")
     t = b.pool(t, 3, 2, name="pool1")
     t = b.conv(t, 192, 5, pads=(2, 2, 2, 2), name="conv2")
