@@ -30,6 +30,10 @@ Parity status of each function (pins are in tests/test_oracle_pins.py):
 * softmax_xent      pinned: library cross-entropy and its autograd gradient, uniform-logit
                     closed form, invariance to a per-row shift of 1000 (overflow),
                     zero gradient row sums, NaN rows for out-of-range labels.
+* sampled_softmax   pinned: with every class sampled (the true one removed as an accidental
+                    hit) it is the full softmax cross-entropy of the logits minus log q;
+                    a constant shift of log q changes nothing; finite differences in h,
+                    W and b.
 * step (net.py)     pinned: finite differences of the whole single-layer loss
                     and the exact first-order decrease of a piecewise-linear net.
 """
@@ -90,6 +94,8 @@ def _declare(lib):
     lib.orc_maxpool_bwd.argtypes = [_dp, _ip, _l, _dp, _l, _i]
     lib.orc_apply_sgd.argtypes = [_dp, _dp, _l, ctypes.c_double]
     lib.orc_apply_momentum.argtypes = [_dp, _dp, _dp, _l, ctypes.c_double, ctypes.c_double, ctypes.c_int]
+    lib.orc_sampled_softmax.argtypes = [_dp, _dp, _dp, _ip, _ip, _dp, _dp, _l, _i, _i, _i, ctypes.c_double, _dp,
+                                        _dp, _dp, _dp]
     lib.orc_softmax_xent.argtypes = [_dp, _dp, _ip, _l, _i, ctypes.c_double, _dp, _dp]
     lib.orc_apply_adam.argtypes = [_dp, _dp, _dp, _dp, _l, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                                    ctypes.c_double, ctypes.c_int]
@@ -293,3 +299,22 @@ def softmax_xent(logits, labels, scale=1.0, bias=None):
     lib.orc_softmax_xent(_ptr(z), None if b is None else _ptr(b), lab.ctypes.data_as(_ip), n, c, float(scale),
                          _ptr(loss), _ptr(dz))
     return loss, dz
+
+
+def sampled_softmax(h, W, b, labels, sampled, lq_true, lq_sampled, scale=1.0):
+    """Sampled softmax cross-entropy; returns (loss per row, dh, dW dense, db dense) in fp64."""
+    lib = _load()
+    h, W, b = _f64(h), _f64(W), _f64(b)
+    n, d = h.shape
+    v = W.shape[0]
+    lab = np.ascontiguousarray(labels, dtype=np.int32)
+    smp = np.ascontiguousarray(sampled, dtype=np.int32)
+    lqt, lqs = _f64(lq_true), _f64(lq_sampled)
+    m = smp.size
+    assert W.shape == (v, d) and b.shape == (v,) and lab.shape == (n,) and lqt.shape == (n,) and lqs.shape == (m,)
+    assert np.all((lab >= 0) & (lab < v)) and np.all((smp >= 0) & (smp < v))
+    loss, dh, dW, db = np.zeros(n), np.zeros((n, d)), np.zeros((v, d)), np.zeros(v)
+    lib.orc_sampled_softmax(_ptr(h), _ptr(W), _ptr(b), lab.ctypes.data_as(_ip), smp.ctypes.data_as(_ip),
+                            _ptr(lqt), _ptr(lqs), n, d, v, m, float(scale), _ptr(loss), _ptr(dh), _ptr(dW),
+                            _ptr(db))
+    return loss, dh, dW, db

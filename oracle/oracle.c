@@ -27,6 +27,7 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 #ifdef _OPENMP
 #include <omp.h>
@@ -360,4 +361,57 @@ void orc_softmax_xent(const double *logits, const double *bias, const int32_t *l
             dr[j] = scale * (p - (j == lab ? 1.0 : 0.0));
         }
     }
+}
+
+/* Sampled softmax (Section 4.2, large classifiers; evaluated in Section 6.4; Jean et al. 2015):
+ * the classifier's output h (n x d) meets only the weight rows of each example's true class
+ * and of one shared sample of classes, drawn from a proposal Q by the caller.  For row i the
+ * candidate logits are
+ *   true:     h_i . W[t_i] + b[t_i] - lq_true[i]
+ *   sampled:  h_i . W[s_j] + b[s_j] - lq_sampled[j]    (j < m; lq = log expected count under Q)
+ * and a sampled class equal to t_i (an accidental hit) is left out of row i.  The loss is the
+ * cross-entropy with the true class at position 0:
+ *   loss[i] = log(sum over candidates of exp(logit)) - true logit
+ * Gradients (scale = 1/n for the batch mean), accumulated over every use of a class:
+ *   dh[i] = scale * sum_c (p_c - [c true]) W[c],   dW[c] += scale * (p_c - [c true]) h_i,
+ *   db[c] += scale * (p_c - [c true]).
+ * dW (v x d) and db (v) are dense and overwritten. */
+void orc_sampled_softmax(const double *h, const double *W, const double *b, const int32_t *labels,
+                         const int32_t *sampled, const double *lq_true, const double *lq_sampled, i64 n, int d,
+                         int v, int m, double scale, double *loss, double *dh, double *dW, double *db) {
+    memset(dW, 0, sizeof(double) * (size_t)v * d);
+    memset(db, 0, sizeof(double) * (size_t)v);
+    double *z = (double *)malloc(sizeof(double) * (size_t)(m + 1));
+    for (i64 i = 0; i < n; ++i) {          /* rows in order: the dW, db accumulation order is fixed */
+        const double *hi = h + i * d;
+        const int t = labels[i];
+        double zt = b[t] - lq_true[i];
+        for (int k = 0; k < d; ++k) zt += hi[k] * W[(i64)t * d + k];
+        z[0] = zt;
+        double mx = zt;
+        for (int j = 0; j < m; ++j) {
+            const int c = sampled[j];
+            if (c == t) { z[j + 1] = -INFINITY; continue; }
+            double zz = b[c] - lq_sampled[j];
+            for (int k = 0; k < d; ++k) zz += hi[k] * W[(i64)c * d + k];
+            z[j + 1] = zz;
+            if (zz > mx) mx = zz;
+        }
+        double sum = 0.0;
+        for (int j = 0; j <= m; ++j) sum += exp(z[j] - mx);
+        loss[i] = mx + log(sum) - zt;
+        double *dhi = dh + i * d;
+        for (int k = 0; k < d; ++k) dhi[k] = 0.0;
+        for (int j = 0; j <= m; ++j) {
+            const int c = j == 0 ? t : sampled[j - 1];
+            const double g = scale * (exp(z[j] - mx) / sum - (j == 0 ? 1.0 : 0.0));
+            if (j > 0 && c == t) continue;
+            for (int k = 0; k < d; ++k) {
+                dhi[k] += g * W[(i64)c * d + k];
+                dW[(i64)c * d + k] += g * hi[k];
+            }
+            db[c] += g;
+        }
+    }
+    free(z);
 }

@@ -548,6 +548,53 @@ def check_classifier_step_fd(net, inputs, samples=12, seed=22):
     return worst
 
 
+# ----------------------------------------------------------------------------- sampled softmax
+def _sampled_case(rng, n=6, d=5, v=9):
+    h = rng.standard_normal((n, d))
+    W = rng.standard_normal((v, d))
+    b = rng.standard_normal(v)
+    lab = rng.integers(0, v, size=n).astype(np.int32)
+    lq = rng.standard_normal(v)                    # log expected count of each class
+    return h, W, b, lab, lq
+
+
+def check_sampled_softmax_full_sample(seed=23):
+    """Every class sampled once: with the true class removed from each row as an accidental hit,
+    the candidates are the whole vocabulary, so the loss is the full softmax cross-entropy of the
+    logits h W^T + b - log q, and dh, dW, db follow from its gradient by the chain rule."""
+    rng = np.random.default_rng(seed)
+    h, W, b, lab, lq = _sampled_case(rng)
+    n = h.shape[0]
+    smp = rng.permutation(W.shape[0]).astype(np.int32)
+    loss, dh, dW, db = oracle.sampled_softmax(h, W, b, lab, smp, lq[lab], lq[smp], 1.0 / n)
+    z = h @ W.T + b - lq
+    rows, dz = oracle.softmax_xent(z, lab, 1.0 / n)
+    return max(rel(loss, rows), rel(dh, dz @ W), rel(dW, dz.T @ h), rel(db, dz.sum(axis=0)))
+
+
+def check_sampled_softmax_shift_and_fd(seed=24):
+    """A constant added to every log q changes nothing; central differences of the summed loss in
+    h, W and b (smooth in all of them) match the gradients."""
+    rng = np.random.default_rng(seed)
+    h, W, b, lab, lq = _sampled_case(rng)
+    smp = np.array([1, 4, 7, 2], dtype=np.int32)
+    args = lambda lqx: (lqx[lab], lqx[smp])
+    loss, dh, dW, db = oracle.sampled_softmax(h, W, b, lab, smp, *args(lq), 1.0)
+    l2 = oracle.sampled_softmax(h, W, b, lab, smp, *args(lq + 3.0), 1.0)[0]
+    worst = rel(l2, loss)
+    L = lambda hh, WW, bb: float(np.sum(oracle.sampled_softmax(hh, WW, bb, lab, smp, *args(lq), 1.0)[0]))
+    eps = 1e-6
+    for name, arr, grad in (("h", h, dh), ("W", W, dW), ("b", b, db)):
+        for idx in [tuple(int(rng.integers(0, s)) for s in arr.shape) for _ in range(6)]:
+            ap, am = arr.copy(), arr.copy()
+            ap[idx] += eps
+            am[idx] -= eps
+            f = {"h": lambda a: L(a, W, b), "W": lambda a: L(h, a, b), "b": lambda a: L(h, W, a)}[name]
+            fd = (f(ap) - f(am)) / (2 * eps)
+            worst = max(worst, abs(fd - grad[idx]) / max(1.0, float(np.max(np.abs(grad)))))
+    return worst
+
+
 # ----------------------------------------------------------------------------- whole step
 def check_step_fd(net, inputs, samples=24, seed=14):
     """Finite differences of the whole single-step surrogate loss L(W, b, x) = <g, out>.

@@ -119,6 +119,11 @@ def test_softmax_xent_library_and_closed_forms():
     assert pins.check_softmax_xent_closed_forms() < 1e-12
 
 
+def test_sampled_softmax_full_sample_shift_and_fd():
+    assert pins.check_sampled_softmax_full_sample() < 1e-12
+    assert pins.check_sampled_softmax_shift_and_fd() < 1e-7
+
+
 def test_classifier_step_finite_differences():
     net = W.classifier_small(batch=3)
     inp = W.make_inputs(net, seed=5)
@@ -235,6 +240,12 @@ MUTATIONS = [
      "dr[j] = scale * p;", "check_softmax_xent_vs_torch"),
     ("cross-entropy loss of class 0", "- (zr[lab] + (bias ? bias[lab] : 0.0));", "- (zr[0] + (bias ? bias[0] : 0.0));",
      "check_softmax_xent_vs_torch"),
+    ("sampled softmax adds log q", "double zz = b[c] - lq_sampled[j];", "double zz = b[c] + lq_sampled[j];",
+     "check_sampled_softmax_full_sample"),
+    ("sampled softmax keeps accidental hits", "if (c == t) { z[j + 1] = -INFINITY; continue; }",
+     "if (0) { z[j + 1] = -INFINITY; continue; }", "check_sampled_softmax_full_sample"),
+    ("sampled softmax drops the dW of the true class", "dW[(i64)c * d + k] += g * hi[k];",
+     "if (j > 0) dW[(i64)c * d + k] += g * hi[k];", "check_sampled_softmax_full_sample"),
     ("pool bwd drops beta", "if (!beta) memset(dx, 0, sizeof(double) * (size_t)nx);",
      "memset(dx, 0, sizeof(double) * (size_t)nx);", "check_pool_bwd_beta"),
 ]
