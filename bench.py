@@ -47,6 +47,7 @@ def parse():
                     help="two streams launched from the host (default), the two-stream step as a HIP graph, "
                          "or one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sampled", action="store_true", help="skip the sampled-softmax comparison")
     ap.add_argument("--classifier-steps", type=int, default=10,
                     help="also time this many steps of AlexNet with its classifier (fc layers + softmax "
                          "cross-entropy); 0 skips it")
@@ -208,6 +209,36 @@ def measure_classifier(args, torch, W, Replica):
             "params": rep.n_params, "loss_last_step": round(rep.loss_value(), 4),
             "fc_gemm_tflops": round(fc_flop / (fc_gemm_ms * 1e-3) / 1e12, 1),
             "per_op_ms": {k: round(v, 4) for k, v in sorted(per.items())}}
+
+
+def measure_sampled(args, torch, W):
+    """The language-model classifier of the paper's second workload in miniature: 2560 rows (128
+    sequences x 20 steps) of a 512-wide output, 40000 classes, 512 sampled per batch; one sampled-
+    softmax step against one full-softmax step (HIP events on the current stream)."""
+    from paper_1605_08695_amd.sampled import FullSoftmaxHead, SampledSoftmaxHead
+    n, d, vocab, m = 2560, 512, 40000, 512
+    inp = W.make_sampled_inputs(n, d, vocab, m, seed=args.seed)
+    h = torch.from_numpy(inp.h).to(torch.bfloat16).cuda()
+    sh = SampledSoftmaxHead(inp.W, inp.b, lr=0.1)
+    bt = sh.prepare(inp.labels, inp.sampled, inp.lq_true, inp.lq_sampled)
+    fh = FullSoftmaxHead(inp.W, inp.b, lr=0.1)
+    lab = torch.from_numpy(inp.labels).cuda()
+
+    def timed(fn, reps=10):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+    ms_s = timed(lambda: sh.run(h, bt))
+    ms_f = timed(lambda: fh.run(h, lab))
+    return {"rows": n, "dim": d, "classes": vocab, "sampled": m, "candidates": bt["u"],
+            "sampled_ms": round(ms_s, 4), "full_ms": round(ms_f, 4), "full_over_sampled": round(ms_f / ms_s, 1),
+            "classes_over_candidates": round(vocab / bt["u"], 1)}
 
 
 def gemm_reference(net, torch):
@@ -374,6 +405,7 @@ def main():
                "alexnet_with_classifier": dict(n=61_100_840, **time_updates(torch, ops, 61_100_840))}
 
     classifier = measure_classifier(args, torch, W, Replica) if args.classifier_steps > 0 else None
+    sampled = None if args.no_sampled else measure_sampled(args, torch, W)
 
     # ---------------------------------------------------------------- CPU baseline: the oracle
     cpu = None
@@ -435,6 +467,7 @@ def main():
         "cpu_baseline": cpu,
         "updates": updates,
         "classifier": classifier,
+        "sampled_softmax": sampled,
     }
     print(json.dumps(out))
     print("per-layer ms:", json.dumps({"%s/%s" % k: round(v, 4) for k, v in sorted(per_layer.items())}),

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 8
+#define TFK_ABI_VERSION 9
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -207,7 +207,6 @@ TFK_API tfk_status tfk_bias_relu_fwd(void *y, tfk_nhwc yd, const float *bias, tf
  *   ws          : at least tfk_bias_relu_bwd_workspace_bytes(yd, dt) bytes.
  * y may be NULL: a layer with a bias and no ReLU (a classifier's logits), so
  * dpre = dy and dbias holds the column sums of dy.
- * Requirements: yd.c <= 16384.
  */
 TFK_API tfk_status tfk_bias_relu_bwd(const void *y, const void *dy, tfk_nhwc yd, void *dpre,
                              float *dbias, tfk_dtype dt, void *ws, size_t ws_bytes,
@@ -317,6 +316,55 @@ TFK_API tfk_status tfk_apply_sgd_multi(int32_t count, float *const *vars, const 
 TFK_API tfk_status tfk_softmax_xent(const void *logits, tfk_dtype dt, int64_t n, int32_t c, const float *bias,
                             const int32_t *labels, float scale, float *loss, void *dlogits,
                             void *stream);
+
+/* ---------------------------------------------------------------- sampled softmax
+ * The sampled softmax of Section 4.2 (evaluated in Section 6.4; Jean et al. 2015): a
+ * classifier over many classes multiplies its input h (n x d) only by the weight rows of
+ * each example's true class and of one shared sample of m classes drawn by the caller from
+ * a proposal Q.  The caller lists the distinct candidate classes (the m sampled ones first,
+ * then the true classes not among them: u in all) and, per example, the candidate column of
+ * its true class; the step then runs as
+ *   tfk_gather_rows_t   W[cand] as a d x u_pad filter, b[cand] as u_pad values
+ *   tfk_conv2d_fwd      z = h . W[cand]^T (a 1 x 1 convolution of n 1 x 1 images)
+ *   tfk_sampled_softmax_xent   loss and dz over the candidates
+ *   tfk_bias_relu_bwd (y NULL), tfk_conv2d_bwd_filter, tfk_conv2d_bwd_input
+ *                       db, dW of the candidates (d x u_pad), dh
+ *   tfk_scatter_apply_sgd   W[cand] -= lr dW, b[cand] -= lr db (rows are distinct)
+ *
+ * out_t[k][j] = table[idx[j]][k] for j < u, k < d; 0 for u <= j < u_pad or for an index
+ * outside [0, rows).  table: rows x d row-major, type dt; out_t: d x u_pad, type dt.
+ * Errors: rows < 0, d < 1, u < 0 or u_pad < u (SHAPE); NULL, misaligned or overlapping
+ * buffers (NULL, ALIGN, ALIAS). */
+TFK_API tfk_status tfk_gather_rows_t(const void *table, tfk_dtype dt, int64_t rows, int32_t d, const int32_t *idx,
+                             int32_t u, int32_t u_pad, void *out_t, void *stream);
+
+/* Cross-entropy over candidate logits z (n x u_pad, type dt): column j < m is sampled class
+ * j with log expected count lq_sampled[j]; true_pos[i] is the column of row i's true class,
+ * whose log expected count is lq_true[i].  With bc = bias_c (u_pad values, or NULL):
+ *   true logit     zt = z[i][t] + bc[t] - lq_true[i]              (t = true_pos[i])
+ *   sampled logit  z[i][j] + bc[j] - lq_sampled[j]  for j < m, j != t (j == t: an accidental
+ *                  hit, left out)
+ *   loss[i] = log(sum of exp over the row's logits) - zt
+ *   dz[i][j] = scale * softmax over the row's logits at j, minus scale at the true column;
+ *              0 in every other column (excluded, unsampled, padding).
+ * true_pos outside [0, u) is not checked on the host: the row gets NaN loss and gradients.
+ * Errors: n < 0, not 0 <= m <= u <= u_pad, u < 1 (SHAPE); scale not finite (ARG); NULL,
+ * misaligned, or dz / loss overlapping any operand (NULL, ALIGN, ALIAS). */
+TFK_API tfk_status tfk_sampled_softmax_xent(const void *z, tfk_dtype dt, int64_t n, int32_t u, int32_t u_pad,
+                                    int32_t m, const float *bias_c, const int32_t *true_pos,
+                                    const float *lq_true, const float *lq_sampled, float scale, float *loss,
+                                    void *dz, void *stream);
+
+/* Sparse ApplyGradientDescent of candidate rows (Section 4.2's sparse variable updates):
+ *   var[idx[j]][k] <- fma(-lr, grad_t[k * ld + j], var[idx[j]][k])    j < u, k < d
+ * var: rows x d fp32; var_bf16 (optional) its bf16 shadow, rewritten for the touched rows;
+ * grad_t: d x ld fp32 (the filter-gradient layout of the candidate convolution).  The rows
+ * idx[j] must be distinct (each element then has one writer); an index outside [0, rows)
+ * is skipped.
+ * Errors: rows < 0, d < 1, u < 0 or ld < u (SHAPE); lr not finite (ARG); NULL, misaligned or
+ * overlapping buffers (NULL, ALIGN, ALIAS).  u == 0 is a no-op. */
+TFK_API tfk_status tfk_scatter_apply_sgd(float *var, uint16_t *var_bf16, int64_t rows, int32_t d, const int32_t *idx,
+                                 int32_t u, const float *grad_t, int64_t ld, float lr, void *stream);
 
 /* Momentum, in place (Section 4.1 lists it among the optimizers built from
  * Variable updates: a per-parameter velocity accumulated over the gradients

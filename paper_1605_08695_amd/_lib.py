@@ -20,7 +20,8 @@ EXPORTS = ["tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_maxpool_bwd_relu_b
            "tfk_bias_relu_fwd", "tfk_bias_relu_bwd", "tfk_bias_relu_bwd_workspace_bytes",
            "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps",
            "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd", "tfk_apply_sgd_multi",
-           "tfk_apply_momentum", "tfk_apply_adam", "tfk_softmax_xent", "tfk_status_string", "tfk_last_error", "tfk_abi_version"]
+           "tfk_apply_momentum", "tfk_apply_adam", "tfk_softmax_xent", "tfk_gather_rows_t",
+           "tfk_sampled_softmax_xent", "tfk_scatter_apply_sgd", "tfk_status_string", "tfk_last_error", "tfk_abi_version"]
 
 
 class Nhwc(ctypes.Structure):
@@ -76,11 +77,15 @@ def load(path: str = LIB_PATH):
     lib.tfk_apply_momentum.argtypes = [vp, vp, vp, i64, f32, f32, i32, vp, vp]
     lib.tfk_apply_adam.argtypes = [vp, vp, vp, vp, i64, f32, f32, f32, f32, i64, vp, vp]
     lib.tfk_softmax_xent.argtypes = [vp, st, i64, i32, vp, vp, f32, vp, vp, vp]
+    lib.tfk_gather_rows_t.argtypes = [vp, st, i64, i32, vp, i32, i32, vp, vp]
+    lib.tfk_sampled_softmax_xent.argtypes = [vp, st, i64, i32, i32, i32, vp, vp, vp, vp, f32, vp, vp, vp]
+    lib.tfk_scatter_apply_sgd.argtypes = [vp, vp, i64, i32, vp, i32, vp, i64, f32, vp]
     for name in ("tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_conv2d_bwd_input", "tfk_conv2d_bwd_input_relu_bwd",
                  "tfk_conv2d_bwd_filter", "tfk_bias_relu_fwd",
                  "tfk_bias_relu_bwd", "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_bwd_relu_bwd",
                  "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps", "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd",
-                 "tfk_apply_sgd_multi", "tfk_apply_momentum", "tfk_apply_adam", "tfk_softmax_xent"):
+                 "tfk_apply_sgd_multi", "tfk_apply_momentum", "tfk_apply_adam", "tfk_softmax_xent", "tfk_gather_rows_t",
+                 "tfk_sampled_softmax_xent", "tfk_scatter_apply_sgd"):
         getattr(lib, name).restype = st
     lib.tfk_status_string.argtypes = [st]
     lib.tfk_status_string.restype = ctypes.c_char_p

@@ -376,7 +376,6 @@ tfk_status tfk_bias_relu_bwd(const void *y, const void *dy, tfk_nhwc yd, void *d
     const int64_t es = esize(dt);
     const int64_t vb = view_bytes(yd, es);
     const int64_t bb = (int64_t)yd.c * 4;
-    if (yd.c > 16384) return fail(TFK_ERR_SHAPE, "bias_relu_bwd supports at most 16384 channels");
     if (yd.n == 0) return hip_status(launch_fill_zero(dbias, yd.c, st), "bias_relu_bwd");
     TRY(need_ptr(dy, "dy"));
     TRY(need_ptr(dpre, "dpre"));
@@ -622,6 +621,86 @@ tfk_status tfk_softmax_xent(const void *logits, tfk_dtype dt, int64_t n, int32_t
     return hip_status(launch_softmax_xent(dt == TFK_F32 ? 0 : 1, logits, bias, labels, n, c, scale, loss, dlogits,
                                           (hipStream_t)stream),
                       "softmax_xent");
+}
+
+// ------------------------------------------------------------------ sampled softmax
+tfk_status tfk_gather_rows_t(const void *table, tfk_dtype dt, int64_t rows, int32_t d, const int32_t *idx, int32_t u,
+                             int32_t u_pad, void *out_t, void *stream) {
+    if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
+    if (rows < 0 || d < 1 || u < 0 || u_pad < u) return fail(TFK_ERR_SHAPE, "need rows >= 0, d >= 1, 0 <= u <= u_pad");
+    if ((int64_t)d * u_pad == 0) return ok();
+    if ((int64_t)d * u_pad > ((int64_t)1 << 40) || rows > ((int64_t)1 << 40) / d)
+        return fail(TFK_ERR_OVERFLOW, "sizes too large");
+    const int64_t es = esize(dt);
+    TRY(need_ptr(out_t, "out_t"));
+    if (u > 0) {
+        TRY(need_ptr(table, "table"));
+        TRY(need_ptr(idx, "idx"));
+    }
+    TRY(need_align(table, es, "table"));
+    TRY(need_align(out_t, es, "out_t"));
+    TRY(need_align(idx, 4, "idx"));
+    const int64_t ob = (int64_t)d * u_pad * es;
+    if (overlap(out_t, ob, table, rows * d * es) || overlap(out_t, ob, idx, (int64_t)u * 4))
+        return fail(TFK_ERR_ALIAS, "out_t overlaps table or idx");
+    return hip_status(launch_gather_rows_t(dt == TFK_F32 ? 0 : 1, table, rows, d, idx, u, u_pad, out_t,
+                                           (hipStream_t)stream),
+                      "gather_rows_t");
+}
+
+tfk_status tfk_sampled_softmax_xent(const void *z, tfk_dtype dt, int64_t n, int32_t u, int32_t u_pad, int32_t m,
+                                    const float *bias_c, const int32_t *true_pos, const float *lq_true,
+                                    const float *lq_sampled, float scale, float *loss, void *dz, void *stream) {
+    if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
+    if (n < 0 || m < 0 || u < m || u < 1 || u_pad < u)
+        return fail(TFK_ERR_SHAPE, "need n >= 0 and 0 <= m <= u <= u_pad, u >= 1");
+    if (!isfinite(scale)) return fail(TFK_ERR_ARG, "scale must be finite");
+    if (n == 0) return ok();
+    if (n > INT32_MAX || n > ((int64_t)1 << 40) / u_pad) return fail(TFK_ERR_OVERFLOW, "n * u_pad too large");
+    const int64_t es = esize(dt), zb = n * u_pad * es;
+    TRY(need_ptr(z, "z"));
+    TRY(need_ptr(true_pos, "true_pos"));
+    TRY(need_ptr(lq_true, "lq_true"));
+    if (m > 0) TRY(need_ptr(lq_sampled, "lq_sampled"));
+    TRY(need_ptr(loss, "loss"));
+    TRY(need_ptr(dz, "dz"));
+    TRY(need_align(z, es, "z"));
+    TRY(need_align(dz, es, "dz"));
+    TRY(need_align(bias_c, 4, "bias_c"));
+    TRY(need_align(true_pos, 4, "true_pos"));
+    TRY(need_align(lq_true, 4, "lq_true"));
+    TRY(need_align(lq_sampled, 4, "lq_sampled"));
+    TRY(need_align(loss, 4, "loss"));
+    const void *p[7] = {dz, loss, z, bias_c, true_pos, lq_true, lq_sampled};
+    const int64_t b[7] = {zb, n * 4, zb, (int64_t)u_pad * 4, n * 4, n * 4, (int64_t)m * 4};
+    for (int i = 0; i < 2; ++i)
+        for (int j = i + 1; j < 7; ++j)
+            if (overlap(p[i], b[i], p[j], b[j])) return fail(TFK_ERR_ALIAS, "dz or loss overlaps an operand");
+    return hip_status(launch_sampled_xent(dt == TFK_F32 ? 0 : 1, z, n, u, u_pad, m, bias_c, true_pos, lq_true,
+                                          lq_sampled, scale, loss, dz, (hipStream_t)stream),
+                      "sampled_softmax_xent");
+}
+
+tfk_status tfk_scatter_apply_sgd(float *var, uint16_t *var_bf16, int64_t rows, int32_t d, const int32_t *idx,
+                                 int32_t u, const float *grad_t, int64_t ld, float lr, void *stream) {
+    if (rows < 0 || d < 1 || u < 0 || ld < u) return fail(TFK_ERR_SHAPE, "need rows >= 0, d >= 1, 0 <= u <= ld");
+    if (!isfinite(lr)) return fail(TFK_ERR_ARG, "lr must be finite");
+    if (u == 0) return ok();
+    if ((int64_t)d * ld > ((int64_t)1 << 40) || rows > ((int64_t)1 << 40) / d)
+        return fail(TFK_ERR_OVERFLOW, "sizes too large");
+    TRY(need_ptr(var, "var"));
+    TRY(need_ptr(idx, "idx"));
+    TRY(need_ptr(grad_t, "grad_t"));
+    TRY(need_align(var, 4, "var"));
+    TRY(need_align(var_bf16, 2, "var_bf16"));
+    TRY(need_align(idx, 4, "idx"));
+    TRY(need_align(grad_t, 4, "grad_t"));
+    const int64_t vb = rows * d * 4, gb = (int64_t)d * ld * 4;
+    if (overlap(var, vb, grad_t, gb) || overlap(var, vb, idx, (int64_t)u * 4) || overlap(var, vb, var_bf16, rows * d * 2) ||
+        overlap(var_bf16, rows * d * 2, grad_t, gb) || overlap(var_bf16, rows * d * 2, idx, (int64_t)u * 4))
+        return fail(TFK_ERR_ALIAS, "var or var_bf16 overlaps an operand");
+    return hip_status(launch_scatter_sgd(var, var_bf16, rows, d, idx, u, grad_t, ld, lr, (hipStream_t)stream),
+                      "scatter_apply_sgd");
 }
 
 // ------------------------------------------------------------------ Momentum, Adam

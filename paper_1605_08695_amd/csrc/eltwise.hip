@@ -136,10 +136,16 @@ __global__ __launch_bounds__(256) void relu_bwd_partial_kernel(const T *__restri
             }
             // The stored dpre equals the value summed here: with bf16 storage the
             // masked dy is already a bf16 value, so rounding on store is exact.
+            if (R == 1) {                    // one row group: the partial directly (no LDS)
 #pragma unroll
-            for (int e = 0; e < EPC; ++e) red[row * C + cv * EPC + e] = s[e];
+                for (int e = 0; e < EPC; ++e) partial[(int64_t)(cv * EPC + e) * gridDim.x + blockIdx.x] = s[e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) red[row * C + cv * EPC + e] = s[e];
+            }
         }
     }
+    if (R == 1) return;
     __syncthreads();
     for (int c = t; c < C; c += 256) {
         float acc = 0.f;
@@ -799,6 +805,133 @@ __global__ __launch_bounds__(256) void opt_kernel(float *__restrict__ var, float
     }
 }
 
+// Fixed xor-tree reductions across one wave.
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// ------------------------------------------------------------------ sampled softmax
+// Gather of candidate rows as the columns of a d x u_pad filter: out_t[k][j] = table[idx[j]][k]
+// (zero for j >= u or an index outside [0, rows)).  Thread: one (k, j); consecutive threads
+// write consecutive j.
+template <typename T>
+__global__ __launch_bounds__(256) void gather_rows_t_kernel(const T *__restrict__ table, int64_t rows, int d,
+                                                            const int32_t *__restrict__ idx, int u, int u_pad,
+                                                            T *__restrict__ out_t) {
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= (int64_t)d * u_pad) return;
+    const int k = (int)(t / u_pad), j = (int)(t - (int64_t)k * u_pad);
+    T v = T(0);
+    if (j < u) {
+        const int64_t r = idx[j];
+        if (r >= 0 && r < rows) v = table[r * d + k];
+    }
+    out_t[t] = v;
+}
+
+hipError_t launch_gather_rows_t(int dt, const void *table, int64_t rows, int d, const int32_t *idx, int u,
+                                int u_pad, void *out_t, hipStream_t st) {
+    const int64_t n = (int64_t)d * u_pad;
+    const dim3 g((unsigned)((n + 255) / 256));
+    if (dt == 0)
+        hipLaunchKernelGGL(gather_rows_t_kernel<float>, g, dim3(256), 0, st, (const float *)table, rows, d, idx, u,
+                           u_pad, (float *)out_t);
+    else
+        hipLaunchKernelGGL(gather_rows_t_kernel<uint16_t>, g, dim3(256), 0, st, (const uint16_t *)table, rows, d,
+                           idx, u, u_pad, (uint16_t *)out_t);
+    return hipGetLastError();
+}
+
+// Sampled softmax cross-entropy over candidate logits z (n x u_pad; columns j < m are the shared
+// sample, tp[i] the column of row i's true class): one block per row, the same fixed reduction
+// tree as softmax_xent_kernel.  Column j < m equal to tp[i] is an accidental hit and is left out.
+template <typename T>
+__global__ __launch_bounds__(256) void sampled_xent_kernel(const T *__restrict__ z, int u_pad, int m,
+                                                           const float *__restrict__ bc, const int32_t *__restrict__ tp,
+                                                           const float *__restrict__ lq_true,
+                                                           const float *__restrict__ lq_sampled, float scale,
+                                                           float *__restrict__ loss, T *__restrict__ dz, int u) {
+    __shared__ float red[2][4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t row = blockIdx.x;
+    const T *zr = z + row * u_pad;
+    T *dr = dz + row * u_pad;
+    const int t = tp[row];
+    if (t < 0 || t >= u) {                        // (uniform over the block)
+        for (int j = tid; j < u_pad; j += 256) Elem<T>::store(dr + j, __builtin_nanf(""));
+        if (tid == 0) loss[row] = __builtin_nanf("");
+        return;
+    }
+    const float zt = Elem<T>::load(zr + t) + (bc ? bc[t] : 0.f) - lq_true[row];
+    float mx = zt;
+    for (int j = tid; j < m; j += 256)
+        if (j != t) mx = fmaxf(mx, Elem<T>::load(zr + j) + (bc ? bc[j] : 0.f) - lq_sampled[j]);
+    mx = wave_max(mx);
+    if (lane == 0) red[0][wave] = mx;
+    __syncthreads();
+    mx = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
+    float sum = 0.f;
+    for (int j = tid; j < m; j += 256)
+        if (j != t) sum += expf(Elem<T>::load(zr + j) + (bc ? bc[j] : 0.f) - lq_sampled[j] - mx);
+    sum = wave_sum(sum);
+    if (lane == 0) red[1][wave] = sum;
+    __syncthreads();
+    const float et = expf(zt - mx);
+    sum = (((red[1][0] + red[1][1]) + red[1][2]) + red[1][3]) + et;
+    if (tid == 0) loss[row] = mx + logf(sum) - zt;
+    const float inv = 1.f / sum;
+    for (int j = tid; j < u_pad; j += 256) {
+        float g = 0.f;
+        if (j < m && j != t) g = scale * (expf(Elem<T>::load(zr + j) + (bc ? bc[j] : 0.f) - lq_sampled[j] - mx) * inv);
+        if (j == t) g = scale * (et * inv - 1.f);
+        Elem<T>::store(dr + j, g);
+    }
+}
+
+hipError_t launch_sampled_xent(int dt, const void *z, int64_t n, int u, int u_pad, int m, const float *bc,
+                               const int32_t *tp, const float *lq_true, const float *lq_sampled, float scale,
+                               float *loss, void *dz, hipStream_t st) {
+    if (dt == 0)
+        hipLaunchKernelGGL(sampled_xent_kernel<float>, dim3((unsigned)n), dim3(256), 0, st, (const float *)z, u_pad, m,
+                           bc, tp, lq_true, lq_sampled, scale, loss, (float *)dz, u);
+    else
+        hipLaunchKernelGGL(sampled_xent_kernel<bf16_t>, dim3((unsigned)n), dim3(256), 0, st, (const bf16_t *)z, u_pad,
+                           m, bc, tp, lq_true, lq_sampled, scale, loss, (bf16_t *)dz, u);
+    return hipGetLastError();
+}
+
+// Sparse in-place SGD of candidate rows: var[idx[j]][k] -= lr * grad_t[k][j] (j < u, k < d),
+// the bf16 shadow beside.  The rows idx[j] are distinct (each element has one writer);
+// an index outside [0, rows) is skipped.
+__global__ __launch_bounds__(256) void scatter_sgd_kernel(float *__restrict__ var, uint16_t *__restrict__ sh,
+                                                          int64_t rows, int d, const int32_t *__restrict__ idx, int u,
+                                                          const float *__restrict__ grad_t, int64_t ld, float lr) {
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= (int64_t)d * u) return;
+    const int j = (int)(t / d), k = (int)(t - (int64_t)j * d);
+    const int64_t r = idx[j];
+    if (r < 0 || r >= rows) return;
+    const int64_t o = r * d + k;
+    const float v = fmaf(-lr, grad_t[(int64_t)k * ld + j], var[o]);
+    var[o] = v;
+    if (sh) sh[o] = (uint16_t)f32_to_bf16(v);
+}
+
+hipError_t launch_scatter_sgd(float *var, uint16_t *sh, int64_t rows, int d, const int32_t *idx, int u,
+                              const float *grad_t, int64_t ld, float lr, hipStream_t st) {
+    const int64_t n = (int64_t)d * u;
+    hipLaunchKernelGGL(scatter_sgd_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, var, sh, rows, d, idx,
+                       u, grad_t, ld, lr);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ split-K epilogue
 // One thread per output row j and group of four channels i (consecutive threads: consecutive
 // groups of one row); the split partials are independent 16-byte loads, added in split order.
@@ -856,17 +989,6 @@ hipError_t launch_split_epilogue(const SplitEpi &e, hipStream_t st) {
 // wave, then the four wave results in order), then the loss and the gradient
 // scale * (softmax - onehot).  Each thread reads and writes only its own columns, so dz may be
 // the logits buffer itself.
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-    return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
-}
-
 template <typename T>
 __global__ __launch_bounds__(256) void softmax_xent_kernel(const T *z, const float *__restrict__ bias,
                                                            const int32_t *__restrict__ labels, int64_t n, int c,
@@ -1023,7 +1145,7 @@ static hipError_t relu_bwd_t(const void *y, const void *dy, void *dpre, int64_t 
     const int CV = vec ? C / EPC : C;
     const int CVB = CV < 256 ? CV : 256;
     const int R = 256 / CVB;
-    const size_t smem = (size_t)R * C * sizeof(float);
+    const size_t smem = R == 1 ? 0 : (size_t)R * C * sizeof(float);
     if (vec)
         hipLaunchKernelGGL((relu_bwd_partial_kernel<T, true>), dim3(G), dim3(256), smem, st,
                            (const T *)y, (const T *)dy, (T *)dpre, P, C, ys, ppb, ws);

@@ -108,6 +108,15 @@ struct SplitEpi {
     float *db_part;
 };
 hipError_t launch_split_epilogue(const SplitEpi &e, hipStream_t st);
+// Sampled softmax: candidate-row gather (as the columns of a d x u_pad filter), the
+// candidate cross-entropy, and the sparse SGD of the candidate rows.
+hipError_t launch_gather_rows_t(int dt, const void *table, int64_t rows, int d, const int32_t *idx, int u,
+                                int u_pad, void *out_t, hipStream_t st);
+hipError_t launch_sampled_xent(int dt, const void *z, int64_t n, int u, int u_pad, int m, const float *bc,
+                               const int32_t *tp, const float *lq_true, const float *lq_sampled, float scale,
+                               float *loss, void *dz, hipStream_t st);
+hipError_t launch_scatter_sgd(float *var, uint16_t *sh, int64_t rows, int d, const int32_t *idx, int u,
+                              const float *grad_t, int64_t ld, float lr, hipStream_t st);
 // Softmax cross-entropy of n x c logits (+ bias) against labels: per-row loss and
 // dz = scale * (softmax - onehot); dz may be z.
 hipError_t launch_softmax_xent(int dt, const void *z, const float *bias, const int32_t *labels, int64_t n, int c,

@@ -17,7 +17,8 @@ from ._lib import Nhwc, TfkError, Window, TFK_BF16, TFK_F32, check, load
 
 __all__ = ["conv2d_fwd", "conv2d_fwd_bias_relu", "conv2d_bwd_input", "conv2d_bwd_filter", "conv2d_workspace_bytes", "bias_relu_fwd",
            "bias_relu_bwd", "bias_relu_bwd_workspace_bytes", "maxpool_fwd", "maxpool_bwd", "maxpool_bwd_relu_bwd", "apply_sgd",
-           "apply_sgd_multi", "apply_momentum", "apply_adam", "softmax_xent", "out_len", "nhwc", "window", "TfkError", "abi_version"]
+           "apply_sgd_multi", "apply_momentum", "apply_adam", "softmax_xent",
+           "gather_rows_t", "sampled_softmax_xent", "scatter_apply_sgd", "out_len", "nhwc", "window", "TfkError", "abi_version"]
 
 
 def _dt(t: torch.Tensor) -> int:
@@ -329,3 +330,46 @@ def apply_sgd_multi(vars_: Sequence[torch.Tensor], grads: Sequence[torch.Tensor]
     if shadows is not None:
         sh = VP(*[(t.data_ptr() if t is not None else 0) for t in shadows])
     check(load().tfk_apply_sgd_multi(count, v, g, ns, float(lr), sh, _stream(stream)))
+
+
+# ----------------------------------------------------------------------------- sampled softmax
+def gather_rows_t(table, idx, u_pad, out_t=None, stream=None):
+    """out_t (d x u_pad) = table[idx]^T, zero past len(idx); table (rows x d) contiguous."""
+    rows, d = table.shape
+    u = idx.numel()
+    if idx.dtype != torch.int32 or not table.is_contiguous():
+        raise ValueError("idx must be int32 and table contiguous")
+    if out_t is None:
+        out_t = torch.empty(d, u_pad, dtype=table.dtype, device=table.device)
+    if out_t.dtype != table.dtype or out_t.numel() != d * u_pad or not out_t.is_contiguous():
+        raise ValueError("out_t must be a contiguous d x u_pad tensor of table's type")
+    check(load().tfk_gather_rows_t(_ptr(table), _dt(table), rows, d, _ptr(idx), u, u_pad, _ptr(out_t),
+                                   _stream(stream)))
+    return out_t
+
+
+def sampled_softmax_xent(z, u, m, true_pos, lq_true, lq_sampled, scale, bias_c=None, loss=None, dz=None,
+                         stream=None):
+    """Cross-entropy over candidate logits z (n x u_pad): returns (loss per row, dz)."""
+    n, u_pad = z.shape[0], z.shape[-1]
+    if not z.is_contiguous() or z.numel() != n * u_pad:
+        raise ValueError("z must be contiguous n x u_pad")
+    if loss is None:
+        loss = torch.empty(n, dtype=torch.float32, device=z.device)
+    if dz is None:
+        dz = torch.empty_like(z)
+    check(load().tfk_sampled_softmax_xent(_ptr(z), _dt(z), n, u, u_pad, m, _ptr(bias_c), _ptr(true_pos),
+                                          _ptr(lq_true), _ptr(lq_sampled), float(scale), _ptr(loss), _ptr(dz),
+                                          _stream(stream)))
+    return loss, dz
+
+
+def scatter_apply_sgd(var, idx, grad_t, lr, shadow=None, stream=None):
+    """var[idx[j]] -= lr * grad_t[:, j] (var rows x d fp32; grad_t d x ld fp32); shadow rewritten."""
+    rows, d = var.shape if var.dim() == 2 else (var.shape[0], 1)
+    ld = grad_t.shape[-1]
+    if var.dtype != torch.float32 or grad_t.dtype != torch.float32 or idx.dtype != torch.int32:
+        raise TypeError("var and grad_t are float32, idx int32")
+    check(load().tfk_scatter_apply_sgd(_ptr(var), _ptr(shadow), rows, d, _ptr(idx), idx.numel(), _ptr(grad_t), ld,
+                                       float(lr), _stream(stream)))
+    return var

@@ -440,3 +440,49 @@ def make_inputs(net: Net, seed: int = 0, batch_slice: int | None = None) -> Inpu
 def with_batch(net_fn, batch):
     """The same workload at another batch size (used for bounded CPU samples)."""
     return net_fn(batch=batch)
+
+
+# ----------------------------------------------------------------------------- sampled softmax inputs
+def log_uniform_sample(rng, vocab: int, m: int):
+    """m distinct classes from the log-uniform proposal Q(c) = log((c + 2) / (c + 1)) / log(vocab + 1),
+    drawn (inverse CDF) until m distinct ones appear.  Returns (sampled ids int32, the log of each
+    class's expected count among those draws, as a function of an id array).  These are the
+    random numbers of the method, drawn on the host and handed to both implementations."""
+    out, seen, draws = [], set(), 0
+    while len(out) < m:
+        c = np.minimum((np.exp(rng.random(2 * m) * math.log(vocab + 1.0)) - 1.0).astype(np.int64), vocab - 1)
+        for x in c:
+            draws += 1
+            if x not in seen:
+                seen.add(int(x))
+                out.append(int(x))
+                if len(out) == m:
+                    break
+
+    def log_expected(ids):
+        q = np.log((np.asarray(ids, np.float64) + 2.0) / (np.asarray(ids, np.float64) + 1.0)) / math.log(vocab + 1.0)
+        return np.log(-np.expm1(draws * np.log1p(-q)))
+    return np.asarray(out, np.int32), log_expected
+
+
+@dataclass
+class SampledInputs:
+    h: np.ndarray               # n x d classifier input
+    W: np.ndarray               # vocab x d weights
+    b: np.ndarray               # vocab biases
+    labels: np.ndarray          # n int32
+    sampled: np.ndarray         # m int32, distinct
+    lq_true: np.ndarray         # n: log expected count of each row's true class
+    lq_sampled: np.ndarray      # m
+
+
+def make_sampled_inputs(n: int, d: int, vocab: int, m: int, seed: int = 0) -> SampledInputs:
+    """Seeded sampled-softmax inputs: h ~ N(0, 1), W ~ N(0, 1/d), b ~ N(0, 0.1^2), labels from the
+    same log-uniform law (word frequencies of a language model are Zipfian), then the sample."""
+    rng = np.random.default_rng(seed)
+    h = rng.standard_normal((n, d))
+    W = rng.standard_normal((vocab, d)) / math.sqrt(d)
+    b = rng.standard_normal(vocab) * 0.1
+    labels = np.minimum((np.exp(rng.random(n) * math.log(vocab + 1.0)) - 1.0).astype(np.int64), vocab - 1)
+    sampled, log_expected = log_uniform_sample(rng, vocab, m)
+    return SampledInputs(h, W, b, labels.astype(np.int32), sampled, log_expected(labels), log_expected(sampled))

@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 8
+    assert lib.tfk_abi_version() == 9
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -245,6 +245,34 @@ def test_softmax_xent_validation(lib):
     assert sm(P + 2, 4, 10) == ALIGN
     assert sm(P, 1 << 30, 1 << 20) == OVERFLOW
     assert sm(0, 0, 10, lab=0, loss=0, dz=0) == OK             # no rows: nothing to touch
+
+
+def test_sampled_softmax_validation(lib):
+    f = ctypes.c_float
+    g = lambda table, rows, d, idx, u, u_pad, out, dt=0: lib.tfk_gather_rows_t(vp(table), dt, rows, d, vp(idx), u,
+                                                                              u_pad, vp(out), None)
+    assert g(P, 100, 8, P + 0x10000, 10, 5, P + 0x20000) == SHAPE            # u_pad < u
+    assert g(P, 100, 0, P + 0x10000, 10, 16, P + 0x20000) == SHAPE
+    assert g(P, 100, 8, P + 0x10000, 10, 16, P + 0x100) == ALIAS             # out inside the table
+    assert g(P, 100, 8, 0, 10, 16, P + 0x20000) == NULL
+    assert g(P, 100, 8, P + 0x10000, 10, 16, P + 0x20000, dt=9) == DTYPE
+    sx = lambda n, u, u_pad, m, dz=P + 0x40000, loss=P + 0x50000, tp=P + 0x60000, scale=1.0: \
+        lib.tfk_sampled_softmax_xent(vp(P), 0, n, u, u_pad, m, None, vp(tp), vp(P + 0x70000), vp(P + 0x80000),
+                                     f(scale), vp(loss), vp(dz), None)
+    assert sx(4, 10, 16, 11) == SHAPE                                      # m > u
+    assert sx(4, 10, 8, 5) == SHAPE                                        # u_pad < u
+    assert sx(4, 10, 16, 5, scale=float("inf")) == ARG
+    assert sx(4, 10, 16, 5, dz=P + 0x10) == ALIAS                          # dz overlaps z
+    assert sx(4, 10, 16, 5, loss=P + 0x60000) == ALIAS                     # loss overlaps true_pos
+    assert sx(4, 10, 16, 5, tp=0) == NULL
+    assert sx(0, 10, 16, 5) == OK
+    sc = lambda rows, d, u, ld, var=P, grad=P + 0x100000, lr=0.1: lib.tfk_scatter_apply_sgd(
+        vp(var), None, rows, d, vp(P + 0x200000), u, vp(grad), ld, f(lr), None)
+    assert sc(100, 8, 10, 5) == SHAPE                                      # ld < u
+    assert sc(100, 8, 10, 16, lr=float("nan")) == ARG
+    assert sc(100, 8, 10, 16, grad=P + 0x40) == ALIAS
+    assert sc(100, 8, 10, 16, var=P + 2) == ALIGN
+    assert sc(100, 8, 0, 16, var=0, grad=0) == OK
 
 
 def test_empty_batch_conv_fwd_is_noop(lib):

@@ -591,10 +591,12 @@ def test_softmax_xent_bad_labels_give_nan_rows():
 
 
 @pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
-def test_bias_only_backward(dtype):
-    """y = NULL: dpre = dy and the bias gradient is the column sums of dy (a logits layer)."""
+@pytest.mark.parametrize("shape", [(128, 1, 1, 1000), (64, 1, 1, 40000)], ids=["c1000", "c40000"])
+def test_bias_only_backward(dtype, shape):
+    """y = NULL: dpre = dy and the bias gradient is the column sums of dy (a logits layer; 40000
+    classes: wider than one block's LDS holds)."""
     rng = np.random.default_rng(78)
-    dy = _mk((128, 1, 1, 1000), dtype, rng)
+    dy = _mk(shape, dtype, rng)
     dy0 = dy.clone()
     dpre, db = ops.bias_relu_bwd(None, dy, dpre=dy)
     torch.cuda.synchronize()
