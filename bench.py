@@ -48,6 +48,9 @@ def parse():
                          "or one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sampled", action="store_true", help="skip the sampled-softmax comparison")
+    ap.add_argument("--metric-only", action="store_true",
+                    help="only the metric's workload: no update, classifier or sampled-softmax figures "
+                         "(for profiles of the step's kernels)")
     ap.add_argument("--classifier-steps", type=int, default=10,
                     help="also time this many steps of AlexNet with its classifier (fc layers + softmax "
                          "cross-entropy); 0 skips it")
@@ -400,12 +403,16 @@ def main():
 
     # ---------------------------------------------------------------- in-place updates alone
     # over this network's variables and over 61.1M variables (AlexNet with its classifier)
-    updates = {"bytes_per_variable": UPDATE_BYTES,
-               "this_net": dict(n=rep.n_params, **time_updates(torch, ops, rep.n_params)),
-               "alexnet_with_classifier": dict(n=61_100_840, **time_updates(torch, ops, 61_100_840))}
+    updates = None
+    if not args.metric_only:
+        updates = {"bytes_per_variable": UPDATE_BYTES,
+                   "this_net": dict(n=rep.n_params, **time_updates(torch, ops, rep.n_params)),
+                   "alexnet_with_classifier": dict(n=61_100_840, **time_updates(torch, ops, 61_100_840))}
 
-    classifier = measure_classifier(args, torch, W, Replica) if args.classifier_steps > 0 else None
-    sampled = None if args.no_sampled else measure_sampled(args, torch, W)
+    classifier = None
+    if args.classifier_steps > 0 and not args.metric_only:
+        classifier = measure_classifier(args, torch, W, Replica)
+    sampled = None if args.no_sampled or args.metric_only else measure_sampled(args, torch, W)
 
     # ---------------------------------------------------------------- CPU baseline: the oracle
     cpu = None
