@@ -244,6 +244,51 @@ def measure_sampled(args, torch, W):
             "classes_over_candidates": round(vocab / bt["u"], 1)}
 
 
+def measure_workloads(args, torch, W, Replica):
+    """The other step configurations at their full sizes (two-stream launch): ms per step and the
+    direct-convolution FLOP rate of the whole step (every op's time included)."""
+    out = {}
+    for make in (W.single_layer, W.vgg16, W.googlenet, W.inception_v3):
+        net = make()
+        rep = Replica(net, W.make_inputs(net, seed=args.seed))
+        for _ in range(2):
+            rep.step()
+        torch.cuda.synchronize()
+        steps = 5
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            rep.step()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        # the same step captured once as a HIP graph and replayed: no per-launch host cost
+        st = torch.cuda.Stream()
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            rep.step()
+        torch.cuda.current_stream().wait_stream(st)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            rep.step()
+        g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            g.replay()
+        torch.cuda.synchronize()
+        ms_g = (time.perf_counter() - t0) * 1e3 / steps
+        fl = W.conv_flops(net)
+        best = min(ms, ms_g)
+        out[net.name] = {"batch": net.tensors["x"][0], "dtype": net.dtype, "ms_per_step": round(ms, 3),
+                         "ms_per_step_graph": round(ms_g, 3), "ops": len(net.ops),
+                         "conv_gflop_per_step": round(fl / 1e9, 1),
+                         "step_tflops": round(fl / (best * 1e-3) / 1e12, 1)}
+        del g
+        del rep
+        torch.cuda.empty_cache()
+    return out
+
+
 def gemm_reference(net, torch):
     """Vendor-library bf16 GEMMs with the (M, N, K) of every convolution direction, for reference only."""
     def t(fn, it=20):
@@ -413,6 +458,7 @@ def main():
     if args.classifier_steps > 0 and not args.metric_only:
         classifier = measure_classifier(args, torch, W, Replica)
     sampled = None if args.no_sampled or args.metric_only else measure_sampled(args, torch, W)
+    others = None if args.metric_only else measure_workloads(args, torch, W, Replica)
 
     # ---------------------------------------------------------------- CPU baseline: the oracle
     cpu = None
@@ -475,6 +521,7 @@ def main():
         "updates": updates,
         "classifier": classifier,
         "sampled_softmax": sampled,
+        "other_workloads": others,
     }
     print(json.dumps(out))
     print("per-layer ms:", json.dumps({"%s/%s" % k: round(v, 4) for k, v in sorted(per_layer.items())}),
