@@ -272,3 +272,27 @@ def test_pins_catch_planted_mistakes(label, old, new, check):
         assert err > 1e-3, (label, err)
     finally:
         shutil.rmtree(tmp, ignore_errors=True)
+
+
+def test_log_uniform_sampler_draws_and_expected_counts():
+    """The host-side sampler of the sampled softmax: m distinct in-range classes, and the log
+    expected count 1 - (1 - Q(c))^T against a Monte Carlo estimate of the chance that class c
+    appears among T draws (T the number of draws the sampler made)."""
+    rng = np.random.default_rng(40)
+    vocab, m = 60, 12
+    ids, log_expected = W.log_uniform_sample(rng, vocab, m)
+    assert ids.dtype == np.int32 and ids.size == m and len(set(ids.tolist())) == m
+    assert ids.min() >= 0 and ids.max() < vocab
+    # recover the draw count from class 0's expected count, then simulate T draws
+    q = lambda c: np.log((c + 2.0) / (c + 1.0)) / np.log(vocab + 1.0)
+    T = int(round(np.log1p(-np.exp(log_expected(np.array([0])))[0]) / np.log1p(-q(0))))
+    assert T >= m
+    sim = np.random.default_rng(41)
+    trials = 20000
+    draws = np.minimum((np.exp(sim.random((trials, T)) * np.log(vocab + 1.0)) - 1.0).astype(np.int64), vocab - 1)
+    for c in (0, 3, 17, 59):
+        p_mc = float(np.mean(np.any(draws == c, axis=1)))
+        p = float(np.exp(log_expected(np.array([c]))[0]))
+        assert abs(p_mc - p) < 4 * np.sqrt(p * (1 - p) / trials) + 1e-3, (c, p_mc, p)
+    # the proposal sums to one over the vocabulary
+    assert abs(float(np.sum(q(np.arange(vocab)))) - 1.0) < 1e-12
