@@ -110,7 +110,10 @@ def test_conv_three_directions(case, dtype):
 
 RELU_BWI_CASES = ["ragged_tiles", "3x3s2_valid", "3x3s2_pad_odd", "1x1s2_empty_phase", "5x5_cout192",
                   "alexnet_conv3_shape", "chunks_c192_uneven_pad", "c192_bwd_tiles", "bj96_tiles_bwd",
-                  "one_pixel_out_c64", "odd_channels"]
+                  "one_pixel_out_c64", "odd_channels",
+                  # a fully connected layer at small batch: split-K partials, then the ReLU
+                  # backward and the bias-gradient rows in the epilogue pass
+                  "fc8_1x1_c4096_k1000"]
 
 
 @pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
