@@ -13,13 +13,13 @@ static int relu_partial_rows(const ConvShape &s) {
     return z * ((mj + t.bj - 1) / t.bj) * (t.nw / 2);
 }
 
-// Split-K for 1 x 1 filters at stride 1 with few output tiles (the fully connected layers at
-// small batch): fp32 partials in the workspace, then one epilogue pass (beta, or the fused ReLU
-// backward with partial column sums after the partials).
+// Split-K at stride 1 (one phase) with few output tiles (fully connected layers and small late-
+// stage images at small batch): fp32 partials in the workspace, then one epilogue pass (beta,
+// or the fused ReLU backward with the bias-gradient rows after the partials).
 static int bwd_data_splits(const ConvShape &s, int *k_split) {
     *k_split = 0;
-    if (s.KH * s.KW != 1 || s.sh != 1 || s.sw != 1) return 1;
-    return gemm_split_plan(s.C, s.N * s.H * s.W, (int64_t)s.K, k_split);
+    if (s.sh != 1 || s.sw != 1) return 1;
+    return gemm_split_plan(s.C, s.N * s.H * s.W, (int64_t)s.KH * s.KW * s.K, k_split);
 }
 
 static size_t split_ws_bytes(int dt, const ConvShape &s, bool relu) {

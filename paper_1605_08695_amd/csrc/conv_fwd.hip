@@ -3,12 +3,11 @@
 
 namespace tfk {
 
-// Split-K (fp32 partials in the workspace, then one epilogue pass) for 1 x 1 filters with few
-// output tiles: the fully connected layers, flattened to 1 x 1 convolutions, at small batch.
+// Split-K (fp32 partials in the workspace, then one epilogue pass) for convolutions with few
+// output tiles: the fully connected layers (flattened to 1 x 1 convolutions) and the small
+// images of late stages at small batch.
 static int fwd_splits(const ConvShape &s, int *k_split) {
-    *k_split = 0;
-    if (s.KH * s.KW != 1) return 1;
-    return gemm_split_plan(s.K, s.N * s.OH * s.OW, (int64_t)s.C, k_split);
+    return gemm_split_plan(s.K, s.N * s.OH * s.OW, (int64_t)s.KH * s.KW * s.C, k_split);
 }
 
 size_t conv_fwd_split_ws_bytes(int dt, const ConvShape &s) {

@@ -233,6 +233,13 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
         return;
     }
     const int nk = k_end > k_beg ? (k_end - k_beg + BK - 1) / BK : 0;
+    // K-tile order (see below): with 64 | channels and several taps the tiles are visited
+    // channel-chunk outer, tap inner, and a split-K range [k_beg, k_end) then counts positions
+    // in that order; the tile addresses come from the position, not from k_beg.
+    bool perm = false;
+    if constexpr (DIR == DIR_FWD) perm = a.C % BK == 0 && a.KH * a.KW > 1;
+    if constexpr (DIR == DIR_BWD_DATA) perm = a.K % BK == 0 && KHp * KWp > 1;
+    const int k_addr = perm ? 0 : k_beg;
 
     // ------------------------------------------------------------ copy plan
     // Every copy is one buffer load into LDS with a 32-bit byte offset per lane.  The buffer
@@ -266,7 +273,7 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
             const int pos = (wave * NLI + r) * 64 + lane;
             const int krow = pos / CPR;
             const int co = i0 + ((pos % CPR) ^ kmajor_swz<BI>(krow)) * 8;
-            ivo[r] = (uint32_t)(k_beg + krow) * ldI2 + 2u * (uint32_t)co;
+            ivo[r] = (uint32_t)(k_addr + krow) * ldI2 + 2u * (uint32_t)co;
         }
     } else {
 #pragma unroll
@@ -364,12 +371,16 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     // the same input rows shifted by one tap, which stay in L1/L2.  issue() is called for
     // kt = 0, 1, 2, ... in order, so the (chunk, tap) position advances by one per call; the
     // tap and channel chunk of a tile are then the same for every lane.
-    bool perm = false;
     int perm_CC = 0;
-    if constexpr (DIR == DIR_FWD) perm = a.C % BK == 0 && a.KH * a.KW > 1;
-    if constexpr (DIR == DIR_BWD_DATA) perm = a.K % BK == 0 && KHp * KWp > 1;
     if constexpr (DIR != DIR_BWD_FILTER) perm_CC = (DIR == DIR_FWD ? a.C : a.K) / BK;
     int perm_kh = 0, perm_kw = 0, perm_cc = 0;
+    if (perm && k_beg > 0) {                       // split-K: start at position k_beg / BK
+        const int p0 = k_beg / BK, taps = KHp * KWp;
+        perm_cc = p0 / taps;
+        const int r = p0 - perm_cc * taps;
+        perm_kh = r / KWp;
+        perm_kw = r - perm_kh * KWp;
+    }
 
     // Issue the copies of K-tile kt into LDS stage `st`.
     auto issue = [&](int kt_seq, unsigned char *st) __attribute__((always_inline)) {
