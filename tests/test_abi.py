@@ -332,7 +332,7 @@ def test_fastdiv_host_exhaustive_sample():
 def test_fully_connected_workspace_queries(lib):
     """A whole-window convolution at small batch is flattened and split across blocks: the forward
     and input-gradient queries ask for the split partials (splits x rows x outputs fp32); a large
-    batch, a padded window or a 3x3 filter asks for none."""
+    batch asks for none, and a strided input gradient (several phases) is never split."""
     lib.tfk_conv2d_workspace_bytes.restype = ctypes.c_size_t
     fc6 = Window(6, 6, 1, 1, 0, 0, 0, 0)
     q = lambda op, n, win=fc6, h=6, c=256, cout=4096, dt=BF16: lib.tfk_conv2d_workspace_bytes(
@@ -342,5 +342,7 @@ def test_fully_connected_workspace_queries(lib):
     assert bwi > 0 and bwi % (4 * 4 * 9216) == 0                  # splits x 4 rows x 9216 inputs x 4 B
     assert q(0, 4, dt=F32) == 0 and q(1, 4, dt=F32) == 0          # the split path is the bf16 kernel's
     assert q(0, 4096) == 0 and q(1, 4096) == 0                    # 32 x 32 tiles: no split
-    assert q(1, 4, win=Window(3, 3, 1, 1, 1, 1, 1, 1), h=6) == 0  # 3x3 filter: no flattening, no split
+    s3 = q(1, 4, win=Window(3, 3, 1, 1, 1, 1, 1, 1), h=6)          # 3x3, stride 1: split over 36 K tiles
+    assert s3 > 0 and s3 % (4 * 36 * 256) == 0                    # splits x 144 pixels x 256 x 4 B
+    assert q(1, 4, win=Window(3, 3, 2, 2, 1, 1, 1, 1), h=6) == 0  # stride 2: several phases, no split
     assert q(2, 4) == 0                                           # 4-pixel reduction: no split partials
