@@ -296,3 +296,16 @@ def test_log_uniform_sampler_draws_and_expected_counts():
         assert abs(p_mc - p) < 4 * np.sqrt(p * (1 - p) / trials) + 1e-3, (c, p_mc, p)
     # the proposal sums to one over the vocabulary
     assert abs(float(np.sum(q(np.arange(vocab)))) - 1.0) < 1e-12
+
+
+def test_sampled_softmax_candidate_list():
+    """Host side of the sampled-softmax head: the distinct candidates are the sample (in order)
+    followed by the true classes outside it (first appearance), and each example's column holds
+    its true class."""
+    from paper_1605_08695_amd.sampled import SampledSoftmaxHead
+    sampled = np.array([7, 3, 11], np.int32)
+    labels = np.array([3, 5, 5, 2, 7, 2, 9], np.int32)
+    cand, tp = SampledSoftmaxHead.candidates(labels, sampled)
+    assert cand.tolist() == [7, 3, 11, 5, 2, 9]
+    assert np.array_equal(cand[tp], labels)
+    assert len(set(cand.tolist())) == cand.size
