@@ -147,7 +147,9 @@ TFK_API tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void
                                 void *ws, size_t ws_bytes, void *stream);
 
 /*
- * Conv2DBackpropFilter: the gradient with respect to the filter:
+ * Conv2DBackpropFilter: the gradient with respect to the filter (Section 4.1: the
+ * backpropagation that the differentiation library derives, whose filter gradients are
+ * what the SGD update consumes; Section 6.1 places convolution on the training critical path):
  *   dw[kh,kw,ci,co] = sum_{n,oh,ow} X[n, oh*sh+kh-pt, ow*sw+kw-pl, ci] * dy[n,oh,ow,co]
  *   x   : xd-shaped forward input, type dt.
  *   dy  : dyd-shaped upstream gradient, type dt.
@@ -181,7 +183,8 @@ TFK_API tfk_status tfk_conv2d_bwd_input_relu_bwd(const void *dy, tfk_nhwc dyd, c
                                          tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd,
                                          float *dbias, void *ws, size_t ws_bytes, void *stream);
 
-/* Workspace needed by a convolution: op 0 = forward, 1 = backprop-input,
+/* Workspace needed by a convolution (of the Section 4.1 forward and gradient operations
+ * above): op 0 = forward, 1 = backprop-input,
  * 2 = backprop-filter, 3 = backprop-input fused with the ReLU backward;
  * xd is the forward input, cout the filter's output channels.  Returns 0
  * for invalid arguments (the operation itself then reports the error). */
@@ -198,7 +201,9 @@ TFK_API tfk_status tfk_bias_relu_fwd(void *y, tfk_nhwc yd, const float *bias, tf
                              void *stream);
 
 /*
- * ReLU backward fused with the bias gradient:
+ * ReLU backward fused with the bias gradient (Section 5: the hand-fused kernels of the
+ * ReLU activation and its gradient; the bias gradient is the BiasAdd gradient of
+ * Section 4.1's backpropagation, summed in the same pass):
  *   dpre[p,c] = (y[p,c] > 0) ? dy[p,c] : 0        (mask from the stored y)
  *   dbias[c]  = sum over all pixels p of dpre[p,c]  (fp32, fixed order)
  *   y, dy, dpre : share the view yd (same extents and pixel stride), type dt.
@@ -215,7 +220,8 @@ TFK_API tfk_status tfk_bias_relu_bwd(const void *y, const void *dy, tfk_nhwc yd,
 TFK_API size_t tfk_bias_relu_bwd_workspace_bytes(tfk_nhwc yd, tfk_dtype dt);
 
 /* ---------------------------------------------------------------- max-pool
- * MaxPool forward with argmax.  Each window scans kh (outer) and kw (inner),
+ * MaxPool forward with argmax (Section 6.1: pooling, with convolution, is on the
+ * critical path of the training step).  Each window scans kh (outer) and kw (inner),
  * skipping padded taps; the first maximum in that order wins (a later tap
  * replaces the running maximum only if strictly greater).
  *   x      : xd-shaped input, type dt.
@@ -229,7 +235,8 @@ TFK_API tfk_status tfk_maxpool_fwd(const void *x, tfk_nhwc xd, tfk_window p, tfk
                            void *y, tfk_nhwc yd, int32_t *argmax, void *stream);
 
 /*
- * The same with the selection stored compactly: taps is dense uint8
+ * MaxPool forward (Section 6.1, as tfk_maxpool_fwd) with the selection stored
+ * compactly: taps is dense uint8
  * [yd.n][yd.h][yd.w][yd.c] holding the selected window tap kh * p.kw + kw (the
  * element ((n*H + oh*sh - pt + kh)*W + ow*sw - pl + kw)*C + c of x), a quarter
  * of the int32 argmax's bytes.  Requires p.kh * p.kw <= 256.  The _taps backward
@@ -239,14 +246,16 @@ TFK_API tfk_status tfk_maxpool_fwd_taps(const void *x, tfk_nhwc xd, tfk_window p
                                 void *y, tfk_nhwc yd, uint8_t *taps, void *stream);
 
 /*
- * MaxPool backward: dx[i] = beta*dx[i] + sum over outputs o with argmax[o] == i of dy[o]
+ * MaxPool backward (Section 6.1 pooling on the critical path; Section 4.1
+ * backpropagation, beta = 1 summing the partial gradients of several paths):
+ * dx[i] = beta*dx[i] + sum over outputs o with argmax[o] == i of dy[o]
  * (overlapping windows may route several outputs to one input; all are summed).
  *   dy, argmax : yd-shaped (argmax dense), from tfk_maxpool_fwd.
  *   dx         : xd-shaped, type dt; beta 0 overwrites, 1 accumulates.
  */
 TFK_API tfk_status tfk_maxpool_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p,
                            tfk_dtype dt, void *dx, tfk_nhwc xd, float beta, void *stream);
-/* tfk_maxpool_bwd with the selection from tfk_maxpool_fwd_taps. */
+/* tfk_maxpool_bwd (Section 6.1, Section 4.1) with the selection from tfk_maxpool_fwd_taps. */
 TFK_API tfk_status tfk_maxpool_bwd_taps(const void *dy, const uint8_t *taps, tfk_nhwc yd, tfk_window p,
                                 tfk_dtype dt, void *dx, tfk_nhwc xd, float beta, void *stream);
 
@@ -270,7 +279,8 @@ TFK_API tfk_status tfk_maxpool_bwd_taps(const void *dy, const uint8_t *taps, tfk
 TFK_API tfk_status tfk_maxpool_bwd_relu_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p,
                                     tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd, float beta,
                                     float *dbias, void *ws, size_t ws_bytes, void *stream);
-/* tfk_maxpool_bwd_relu_bwd with the selection from tfk_maxpool_fwd_taps. */
+/* tfk_maxpool_bwd_relu_bwd (Section 5 fused activation gradient, Section 6.1 pooling) with the
+ * selection from tfk_maxpool_fwd_taps. */
 TFK_API tfk_status tfk_maxpool_bwd_relu_bwd_taps(const void *dy, const uint8_t *taps, tfk_nhwc yd, tfk_window p,
                                          tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd, float beta,
                                          float *dbias, void *ws, size_t ws_bytes, void *stream);
@@ -287,8 +297,10 @@ TFK_API tfk_status tfk_maxpool_bwd_relu_bwd_taps(const void *dy, const uint8_t *
 TFK_API tfk_status tfk_apply_sgd(float *var, const float *grad, int64_t n, float lr,
                          uint16_t *var_bf16, void *stream);
 
-/* The same update over `count` independent (var, grad, n, shadow) tuples in one
- * launch per batch of tensors.  shadows may be NULL (no shadows) or hold NULL
+/* ApplyGradientDescent (Section 4.1, W' = W - alpha * dL/dW, as tfk_apply_sgd) over
+ * `count` independent (var, grad, n, shadow) tuples in one launch per batch of tensors:
+ * every variable of a synchronous step is updated from gradients of the same parameter
+ * version (Section 4.4).  shadows may be NULL (no shadows) or hold NULL
  * entries.  The pointer arrays are host memory and are read during the call. */
 TFK_API tfk_status tfk_apply_sgd_multi(int32_t count, float *const *vars, const float *const *grads,
                                const int64_t *ns, float lr, uint16_t *const *shadows,
@@ -338,7 +350,8 @@ TFK_API tfk_status tfk_softmax_xent(const void *logits, tfk_dtype dt, int64_t n,
 TFK_API tfk_status tfk_gather_rows_t(const void *table, tfk_dtype dt, int64_t rows, int32_t d, const int32_t *idx,
                              int32_t u, int32_t u_pad, void *out_t, void *stream);
 
-/* Cross-entropy over candidate logits z (n x u_pad, type dt): column j < m is sampled class
+/* Cross-entropy over candidate logits z (the sampled softmax loss of Section 4.2, as
+ * described above) (n x u_pad, type dt): column j < m is sampled class
  * j with log expected count lq_sampled[j]; true_pos[i] is the column of row i's true class,
  * whose log expected count is lq_true[i].  With bc = bias_c (u_pad values, or NULL):
  *   true logit     zt = z[i][t] + bc[t] - lq_true[i]              (t = true_pos[i])
@@ -396,10 +409,14 @@ TFK_API tfk_status tfk_apply_adam(float *var, float *m, float *v, const float *g
                           float beta1, float beta2, float epsilon, int64_t t, uint16_t *var_bf16,
                           void *stream);
 
-/* ---------------------------------------------------------------- misc */
+/* ---------------------------------------------------------------- misc
+ * Error reporting of the thin C API that the paper's client libraries sit on (Section 5: a C
+ * API separates the user-level code from the core runtime); no tensor arithmetic. */
+/* Name of a status code. */
 TFK_API const char *tfk_status_string(tfk_status s);
 /* Detail of the last non-OK status returned on the calling thread ("" if none). */
 TFK_API const char *tfk_last_error(void);
+/* Version of this interface (incremented when any declaration here changes). */
 TFK_API int32_t tfk_abi_version(void);
 
 #ifdef __cplusplus

@@ -64,12 +64,13 @@ __device__ __forceinline__ f32x4_t fresh_zero4() {
     return f32x4_t{z0, z1, z2, z3};
 }
 
-// One 4-byte direct-to-LDS copy per lane: lane l's word lands at lds_base + 4 l.
+// One 4-byte direct-to-LDS copy per lane: lane l's word lands at lds_base + 4 l.  The s_nop is
+// the wait state that an LDS DMA needs after a scalar write of M0 (as in dma16).
 __device__ __forceinline__ void dma4(const void *src, unsigned char *lds_base) {
     const uint32_t lds_addr = __builtin_amdgcn_readfirstlane(
         (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char *)lds_base);
     uint32_t saved;
-    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dword %1, off\n\ts_mov_b32 m0, %0"
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %1, off\n\ts_mov_b32 m0, %0"
                  : "=&s"(saved)
                  : "v"(src), "s"(lds_addr)
                  : "memory");

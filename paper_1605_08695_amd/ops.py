@@ -68,10 +68,24 @@ def abi_version() -> int:
     return load().tfk_abi_version()
 
 
-def _ws(nbytes: int, device) -> Optional[torch.Tensor]:
+def _empty(stream, *args, **kw) -> torch.Tensor:
+    """torch.empty on the stream the op is enqueued on: the caching allocator then hands the
+    memory, once freed, only to later work on that same stream (a temporary freed on return
+    cannot be reused by another stream while the kernel still runs)."""
+    if stream is None:
+        return torch.empty(*args, **kw)
+    with torch.cuda.stream(stream):
+        return torch.empty(*args, **kw)
+
+
+def _empty_like(stream, t: torch.Tensor) -> torch.Tensor:
+    return _empty(stream, t.shape, dtype=t.dtype, device=t.device)
+
+
+def _ws(nbytes: int, device, stream=None) -> Optional[torch.Tensor]:
     if nbytes == 0:
         return None
-    return torch.empty((nbytes + 15) // 16 * 16, dtype=torch.uint8, device=device)
+    return _empty(stream, (nbytes + 15) // 16 * 16, dtype=torch.uint8, device=device)
 
 
 # ----------------------------------------------------------------------------- convolution
@@ -85,10 +99,10 @@ def _conv_fwd(x, w, bias, stride, pads, y, ws, stream):
     win = window(kh, kw, stride, pads)
     need = lib.tfk_conv2d_workspace_bytes(0, nhwc(x), cout, win, _dt(x))
     if need and (ws is None or ws.numel() < need):
-        ws = _ws(need, x.device)
+        ws = _ws(need, x.device, stream)
     if y is None:
         n, h, ww, _ = x.shape
-        y = torch.empty((n, out_len(h, kh, win.stride_h, pads[0], pads[1]),
+        y = _empty(stream, (n, out_len(h, kh, win.stride_h, pads[0], pads[1]),
                          out_len(ww, kw, win.stride_w, pads[2], pads[3]), cout), dtype=x.dtype, device=x.device)
     if w.dtype != x.dtype or y.dtype != x.dtype:
         raise TypeError("x, w and y must share one dtype")
@@ -123,7 +137,7 @@ def conv2d_bwd_input(dy, w, dx, stride, pads, beta=0.0, ws=None, stream=None):
     win = window(kh, kw, stride, pads)
     need = lib.tfk_conv2d_workspace_bytes(1, nhwc(dx), cout, win, _dt(dx))
     if need and (ws is None or ws.numel() < need):
-        ws = _ws(need, dx.device)
+        ws = _ws(need, dx.device, stream)
     check(lib.tfk_conv2d_bwd_input(_ptr(dy), nhwc(dy), _ptr(w), win, _dt(dy), _ptr(dx), nhwc(dx), float(beta),
                                    _ptr(ws) if need else None, need, _stream(stream)))
     return dx
@@ -140,11 +154,11 @@ def conv2d_bwd_input_relu_bwd(dy, w, y, dpre, stride, pads, dbias=None, ws=None,
     if (d_y.n, d_y.h, d_y.w, d_y.c, d_y.pixel_stride) != (d_p.n, d_p.h, d_p.w, d_p.c, d_p.pixel_stride):
         raise ValueError("y and dpre must share one view (extents and pixel stride)")
     if dbias is None:
-        dbias = torch.empty(cin, dtype=torch.float32, device=y.device)
+        dbias = _empty(stream, cin, dtype=torch.float32, device=y.device)
     win = window(kh, kw, stride, pads)
     need = lib.tfk_conv2d_workspace_bytes(3, d_p, cout, win, _dt(y))
     if need and (ws is None or ws.numel() < need):
-        ws = _ws(need, y.device)
+        ws = _ws(need, y.device, stream)
     check(lib.tfk_conv2d_bwd_input_relu_bwd(_ptr(dy), nhwc(dy), _ptr(w), win, _dt(dy), _ptr(y), _ptr(dpre), d_p,
                                             _ptr(dbias), _ptr(ws) if need else None, need, _stream(stream)))
     return dpre, dbias
@@ -156,13 +170,13 @@ def conv2d_bwd_filter(x, dy, kernel_hw, stride, pads, dw=None, ws=None, stream=N
     kh, kw = kernel_hw
     cout = dy.shape[3]
     if dw is None:
-        dw = torch.empty((kh, kw, x.shape[3], cout), dtype=torch.float32, device=x.device)
+        dw = _empty(stream, (kh, kw, x.shape[3], cout), dtype=torch.float32, device=x.device)
     if dy.dtype != x.dtype or dw.dtype != torch.float32:
         raise TypeError("x and dy share one dtype; dw is float32")
     win = window(kh, kw, stride, pads)
     need = lib.tfk_conv2d_workspace_bytes(2, nhwc(x), cout, win, _dt(x))
     if ws is None or ws.numel() < need:
-        ws = _ws(need, x.device)
+        ws = _ws(need, x.device, stream)
     check(lib.tfk_conv2d_bwd_filter(_ptr(x), nhwc(x), _ptr(dy), nhwc(dy), win, _dt(x), _ptr(dw), _ptr(ws),
                                     need, _stream(stream)))
     return dw
@@ -184,13 +198,13 @@ def bias_relu_bwd(y, dy, dpre=None, dbias=None, ws=None, stream=None) -> Tuple[t
     (a bias-only layer) dpre = dy and dbias = column sums of dy."""
     lib = load()
     if dpre is None:
-        dpre = torch.empty_like(dy)
+        dpre = _empty_like(stream, dy)
     if dbias is None:
-        dbias = torch.empty(dy.shape[3], dtype=torch.float32, device=dy.device)
+        dbias = _empty(stream, dy.shape[3], dtype=torch.float32, device=dy.device)
     view = y if y is not None else dy
     need = lib.tfk_bias_relu_bwd_workspace_bytes(nhwc(view), _dt(view))
     if ws is None or ws.numel() < need:
-        ws = _ws(need, dy.device)
+        ws = _ws(need, dy.device, stream)
     d_y, d_dy, d_dp = nhwc(view), nhwc(dy), nhwc(dpre)
     if (d_y.pixel_stride, d_y.c) != (d_dy.pixel_stride, d_dy.c) or (d_y.pixel_stride, d_y.c) != (d_dp.pixel_stride, d_dp.c):
         raise ValueError("y, dy and dpre must share one view (extents and pixel stride)")
@@ -211,9 +225,9 @@ def softmax_xent(logits, labels, scale, bias=None, loss=None, dlogits=None, stre
     if bias is not None and (bias.dtype != torch.float32 or bias.numel() != c):
         raise ValueError("bias must be float32 [c]")
     if loss is None:
-        loss = torch.empty(n, dtype=torch.float32, device=logits.device)
+        loss = _empty(stream, n, dtype=torch.float32, device=logits.device)
     if dlogits is None:
-        dlogits = torch.empty_like(logits)
+        dlogits = _empty_like(stream, logits)
     if dlogits.dtype != logits.dtype or dlogits.numel() != logits.numel() or not dlogits.is_contiguous():
         raise ValueError("dlogits must be a contiguous tensor like logits")
     check(load().tfk_softmax_xent(_ptr(logits), _dt(logits), n, c, _ptr(bias), _ptr(labels), float(scale),
@@ -232,9 +246,9 @@ def maxpool_fwd(x, kernel_hw, stride, pads, y=None, argmax=None, stream=None, ta
     oh = out_len(h, kh, win.stride_h, pads[0], pads[1])
     ow = out_len(w, kw, win.stride_w, pads[2], pads[3])
     if y is None:
-        y = torch.empty((n, oh, ow, c), dtype=x.dtype, device=x.device)
+        y = _empty(stream, (n, oh, ow, c), dtype=x.dtype, device=x.device)
     if argmax is None:
-        argmax = torch.empty((n, oh, ow, c), dtype=torch.uint8 if taps else torch.int32, device=x.device)
+        argmax = _empty(stream, (n, oh, ow, c), dtype=torch.uint8 if taps else torch.int32, device=x.device)
     fn = _argmax_fn(lib, "tfk_maxpool_fwd", argmax)
     check(fn(_ptr(x), nhwc(x), win, _dt(x), _ptr(y), nhwc(y), _ptr(argmax), _stream(stream)))
     return y, argmax
@@ -264,13 +278,13 @@ def maxpool_bwd_relu_bwd(dy, argmax, y, dpre, kernel_hw, stride, pads, beta=0.0,
     kh, kw = kernel_hw
     fn = _argmax_fn(lib, "tfk_maxpool_bwd_relu_bwd", argmax)
     if dbias is None:
-        dbias = torch.empty(y.shape[3], dtype=torch.float32, device=y.device)
+        dbias = _empty(stream, y.shape[3], dtype=torch.float32, device=y.device)
     d_y, d_p = nhwc(y), nhwc(dpre)
     if (d_y.n, d_y.h, d_y.w, d_y.c, d_y.pixel_stride) != (d_p.n, d_p.h, d_p.w, d_p.c, d_p.pixel_stride):
         raise ValueError("y and dpre must share one view (extents and pixel stride)")
     need = lib.tfk_bias_relu_bwd_workspace_bytes(d_y, _dt(y))
     if ws is None or ws.numel() < need:
-        ws = _ws(need, y.device)
+        ws = _ws(need, y.device, stream)
     check(fn(_ptr(dy), _ptr(argmax), nhwc(dy), window(kh, kw, stride, pads), _dt(dy), _ptr(y), _ptr(dpre), d_y,
              float(beta), _ptr(dbias), _ptr(ws), need, _stream(stream)))
     return dpre, dbias
@@ -340,7 +354,7 @@ def gather_rows_t(table, idx, u_pad, out_t=None, stream=None):
     if idx.dtype != torch.int32 or not table.is_contiguous():
         raise ValueError("idx must be int32 and table contiguous")
     if out_t is None:
-        out_t = torch.empty(d, u_pad, dtype=table.dtype, device=table.device)
+        out_t = _empty(stream, d, u_pad, dtype=table.dtype, device=table.device)
     if out_t.dtype != table.dtype or out_t.numel() != d * u_pad or not out_t.is_contiguous():
         raise ValueError("out_t must be a contiguous d x u_pad tensor of table's type")
     check(load().tfk_gather_rows_t(_ptr(table), _dt(table), rows, d, _ptr(idx), u, u_pad, _ptr(out_t),
@@ -355,9 +369,9 @@ def sampled_softmax_xent(z, u, m, true_pos, lq_true, lq_sampled, scale, bias_c=N
     if not z.is_contiguous() or z.numel() != n * u_pad:
         raise ValueError("z must be contiguous n x u_pad")
     if loss is None:
-        loss = torch.empty(n, dtype=torch.float32, device=z.device)
+        loss = _empty(stream, n, dtype=torch.float32, device=z.device)
     if dz is None:
-        dz = torch.empty_like(z)
+        dz = _empty_like(stream, z)
     check(load().tfk_sampled_softmax_xent(_ptr(z), _dt(z), n, u, u_pad, m, _ptr(bias_c), _ptr(true_pos),
                                           _ptr(lq_true), _ptr(lq_sampled), float(scale), _ptr(loss), _ptr(dz),
                                           _stream(stream)))

@@ -69,9 +69,9 @@ class SampledSoftmaxHead:
         loss, dz = ops.sampled_softmax_xent(z, u, m, bt["true_pos"], bt["lq_true"], bt["lq_sampled"], 1.0 / n,
                                             bias_c=bc, stream=stream)
         _, dbc = ops.bias_relu_bwd(None, dz, dpre=dz, stream=stream)
-        dwc = torch.empty(1, 1, d, u_pad, dtype=torch.float32, device=h.device)
+        dwc = ops._empty(stream, (1, 1, d, u_pad), dtype=torch.float32, device=h.device)
         ops.conv2d_bwd_filter(h4, dz, (1, 1), 1, (0, 0, 0, 0), dw=dwc, stream=stream)
-        dh = torch.empty_like(h4)
+        dh = ops._empty_like(stream, h4)
         ops.conv2d_bwd_input(dz, w4, dh, 1, (0, 0, 0, 0), stream=stream)
         ops.scatter_apply_sgd(self.W, cand, dwc.view(d, u_pad), self.lr, shadow=self.W_lp, stream=stream)
         ops.scatter_apply_sgd(self.b, cand, dbc.view(1, u_pad), self.lr, stream=stream)
@@ -103,9 +103,9 @@ class FullSoftmaxHead:
         z = ops.conv2d_fwd(h4, w4, 1, (0, 0, 0, 0), stream=stream)
         loss, dz = ops.softmax_xent(z, labels, 1.0 / n, bias=self.b, dlogits=z, stream=stream)
         _, db = ops.bias_relu_bwd(None, dz, dpre=dz, stream=stream)
-        dw = torch.empty(1, 1, d, self.vocab, dtype=torch.float32, device=h.device)
+        dw = ops._empty(stream, (1, 1, d, self.vocab), dtype=torch.float32, device=h.device)
         ops.conv2d_bwd_filter(h4, dz, (1, 1), 1, (0, 0, 0, 0), dw=dw, stream=stream)
-        dh = torch.empty_like(h4)
+        dh = ops._empty_like(stream, h4)
         ops.conv2d_bwd_input(dz, w4, dh, 1, (0, 0, 0, 0), stream=stream)
         ops.apply_sgd(self.W.view(-1), dw.view(-1), self.lr, shadow=self.W_lp.view(-1), stream=stream)
         ops.apply_sgd(self.b, db, self.lr, stream=stream)
