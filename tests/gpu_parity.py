@@ -34,6 +34,7 @@ compounding of bf16 storage across layers.
 from __future__ import annotations
 
 import sys
+import time
 
 import numpy as np
 import torch
@@ -130,6 +131,7 @@ class ParityTracer:
         self.label = label
         self.lr = rep.lr
         self.pending = None
+        self._t0 = time.perf_counter()
         self.results = []           # (kind, op name, metric, value, bar, ok)
         net, k = rep.net, self.k
         self.state = {("act", "x"): np.asarray(inputs.x[:k], np.float64)}
@@ -276,6 +278,9 @@ class ParityTracer:
         assert kind == event[:-4] and op0 is op
         getattr(self, "_check_" + kind)(op, used, t)
         self.pending = None
+        now = time.perf_counter()
+        say("    %-28s %-20s checked (%.1f s)" % (kind, op.name if op is not None else "all", now - self._t0))
+        self._t0 = now
 
     # -------------------------------------------------------------- forward
     def _force_conv_bias_relu_fwd(self, op, t):
@@ -442,3 +447,107 @@ class ParityTracer:
         if self.rep.shadow is not None:
             same = torch.equal(self.rep.shadow, out["var"].to(torch.bfloat16))
             self.record("apply_sgd", "shadow", "mismatch", 0.0 if same else 1.0, 0.0)
+
+
+class SampledParityTracer(ParityTracer):
+    """Full-size, all-distinct step check for workloads whose whole-batch oracle step is too slow.
+
+    Every buffer holds distinct images (the seeded inputs, no repetition), and every op's inputs
+    are forced from the harness state before it runs, as in ParityTracer.  The state holds the
+    whole batch:
+
+    * ops whose oracle is cheap at full size (max-pool forward and backward, ReLU backward, bias
+      gradients) are computed by the oracle over the whole batch and checked on every image
+      (argmax and max-pool values bit-exact);
+    * convolution outputs are computed by the oracle only for the images in ``sample`` and
+      checked there element by element; the other images of that output are filled with seeded
+      N(0, rms^2) draws (passed through max(., 0) after a ReLU), so every later op still reads
+      distinct, known values and never a GPU result;
+    * filter gradients are checked at ``n_entries`` seeded HWIO entries, each summed by the oracle
+      over the whole batch; the rest of the filter-gradient state is filled the same way;
+    * an input gradient fused with the ReLU backward is checked on the sampled images and, for
+      its mask, on every image (zero wherever the forced ReLU output is not positive); its bias
+      gradient sums the GPU's own input gradient of the unsampled images, which the oracle does
+      not form, so it is left to the repeated-image full-size test.
+
+    A kernel that reads another image's data (a wrong batch offset or image advance) fails the
+    sampled comparisons, since no two images hold the same values.
+    """
+
+    def __init__(self, rep, inputs, sample, n_entries=256, seed=1234, label=""):
+        super().__init__(rep, inputs, distinct=None, label=label)
+        n = inputs.x.shape[0]
+        self.sample = sorted({int(s) % n for s in sample})
+        self.n_entries = n_entries
+        self.rng = np.random.default_rng(seed)
+        self.skipped = []
+
+    def _gs(self, t):
+        """GPU values of the sampled images of batch tensor t, fp64."""
+        return f64(t[self.sample])
+
+    def _fill(self, shape, ref, relu):
+        """Whole-batch state of a convolution output: seeded draws with the RMS of the oracle's
+        sampled values, the sampled images set to those values."""
+        rms = float(np.sqrt(np.mean(ref * ref))) if ref.size else 1.0
+        full = self.rng.standard_normal(shape, dtype=np.float32).astype(np.float64) * (rms or 1.0)
+        if relu:
+            np.maximum(full, 0.0, out=full)
+        full[self.sample] = ref
+        return full
+
+    def _set_fill(self, t, ref, relu):
+        shape = (self.k,) + tuple(t.shape[1:])
+        self._set(t, self._fill(shape, ref, relu))
+
+    # -------------------------------------------------------------- forward
+    def _check_conv_bias_relu_fwd(self, op, u, out):
+        s = self.sample
+        ref = oracle.bias_relu_fwd(oracle.conv2d_fwd(u["x"][s], u["w"], (op.sh, op.sw), op.pads), u["b"])
+        y = self._gs(out["y"])
+        self.record_tensor("conv_bias_relu_fwd", op.name, y, ref, self.dtype)
+        self.record("conv_bias_relu_fwd", op.name, "negatives", float(np.sum(np.signbit(y))), 0.0)
+        self._set_fill(out["y"], ref, relu=True)
+
+    def _check_conv_fwd(self, op, u, out):
+        s = self.sample
+        ref = oracle.conv2d_fwd(u["x"][s], u["w"], (op.sh, op.sw), op.pads)
+        self.record_tensor("conv_fwd", op.name, self._gs(out["y"]), ref, self.dtype)
+        self._set_fill(out["y"], ref, relu=False)
+
+    # -------------------------------------------------------------- backward
+    def _check_conv_bwd_filter(self, op, u, out):
+        dw = out["dw"]
+        numel = dw.numel()
+        idx = self.rng.choice(numel, size=min(self.n_entries, numel), replace=False)
+        idx = np.unique(np.concatenate([idx, [0, numel - 1]])).astype(np.int64)
+        ref = oracle.conv2d_bwd_filter_at(u["x"], u["dy"], (op.kh, op.kw), (op.sh, op.sw), op.pads, idx)
+        got = dw.reshape(-1)[torch.from_numpy(idx).to(dw.device)].to(torch.float64).cpu().numpy()
+        self.record_tensor("conv_bwd_filter@entries", op.name, got, ref, torch.float32)
+        rms = float(np.sqrt(np.mean(ref * ref))) or 1.0
+        full = self.rng.standard_normal(numel) * rms
+        full[idx] = ref
+        self._set(dw, full.reshape(tuple(dw.shape)))
+
+    def _check_conv_bwd_input(self, op, u, out):
+        s = self.sample
+        dx0 = u["dx"][s] if u["beta"] else None
+        ref = oracle.conv2d_bwd_input(u["dy"][s], u["w"], (len(s),) + u["dx_shape"][1:], (op.sh, op.sw), op.pads,
+                                      dx=dx0, beta=u["beta"])
+        self.record_tensor("conv_bwd_input", op.name, self._gs(out["dx"]), ref, self.dtype)
+        self._set_fill(out["dx"], ref, relu=False)
+
+    def _check_conv_bwd_input_relu_bwd(self, op, u, out):
+        s = self.sample
+        g = oracle.conv2d_bwd_input(u["dy"][s], u["w"], (len(s),) + u["y"].shape[1:], (op.sh, op.sw), op.pads)
+        ref_dpre, _ = oracle.bias_relu_bwd(u["y"][s], g)
+        self.record_tensor("conv_bwd_input_relu_bwd", op.name, self._gs(out["dpre"]), ref_dpre, self.dtype)
+        # the ReLU mask on every image: zero wherever the forced y is not positive
+        masked = out["dpre"][torch.from_numpy(u["y"] <= 0).to(out["dpre"].device)]
+        self.record("conv_bwd_input_relu_bwd", op.name, "masked_nonzero", float((masked != 0).sum()), 0.0)
+        self.skipped.append(("conv_bwd_input_relu_bwd:db", op.name))
+        full = self._fill((self.k,) + u["y"].shape[1:], ref_dpre, relu=False)
+        full[u["y"] <= 0] = 0.0
+        self._set(out["dpre"], full)
+        db_ref = self.rng.standard_normal(out["db"].numel())
+        self._set(out["db"], db_ref)

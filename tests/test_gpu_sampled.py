@@ -96,11 +96,57 @@ def test_scatter_apply_sgd_rows():
     assert torch.equal(sh[torch.from_numpy(touched).to(DEV)], var[torch.from_numpy(touched).to(DEV)].to(torch.bfloat16))
 
 
+U_BF16 = 2.0 ** -8          # unit roundoff of bf16 (round to nearest even, 8-bit significand)
+U_F32 = 2.0 ** -24
+
+
+def _head_error_bounds(h, Wc, bc, lq_true, lq_sampled, true_pos, m, scale):
+    """Per-element bounds of what the head's bf16 storage of the candidate logits and of their
+    gradient allows, given exact (fp64) arithmetic elsewhere and fp32 sums.
+
+    With logits z_i stored in bf16, each moves by at most E_i = u max_j |z_ij| (u = 2^-8), so the
+    softmax p_ij moves by at most p_ij (exp(2 E_i) - 1) and the loss by at most 2 E_i (the
+    log-sum-exp is 1-Lipschitz in the max norm).  The stored gradient dz_ij = scale (p_ij -
+    [j = true]) then errs by at most e_ij = scale p_ij k_i + u (|dz_ij| + scale p_ij k_i), k_i =
+    exp(2 E_i) - 1.  Returns (e, k-independent loss bound, |dz|)."""
+    n, u = h.shape[0], Wc.shape[0]
+    z = h @ Wc.T + bc[None, :]
+    lq = np.broadcast_to(np.concatenate([lq_sampled, np.zeros(u - m)])[None, :], (n, u)).copy()
+    rows = np.arange(n)
+    lq[rows, true_pos] = lq_true
+    z = z - lq
+    keep = np.zeros((n, u), bool)
+    keep[:, :m] = True
+    keep[rows, true_pos] = True          # the true column (an accidental hit is this same column)
+    z = np.where(keep, z, -np.inf)
+    mx = z.max(axis=1, keepdims=True)
+    p = np.exp(z - mx)
+    p /= p.sum(axis=1, keepdims=True)
+    # + the fp32 sums of the candidate GEMM and of the bias and log-count terms
+    gemm = h.shape[1] * U_F32 * np.max(np.abs(h) @ np.abs(Wc).T, axis=1)
+    E = (U_BF16 * np.max(np.where(keep, np.abs(z), 0.0), axis=1) + gemm
+         + 4 * U_F32 * (np.max(np.where(keep, np.abs(z), 0.0), axis=1) + np.max(np.abs(lq), axis=1) + 1))
+    k = np.expm1(2 * E)[:, None]
+    dz = scale * (p - (np.arange(u)[None, :] == true_pos[:, None]))
+    e = scale * p * k + U_BF16 * (np.abs(dz) + scale * p * k)
+    return e, 2 * E, np.abs(dz)
+
+
+def _assert_within(name, a, r, tol):
+    excess = np.abs(a - r) - tol
+    worst = float(np.max(excess / np.maximum(tol, 1e-300))) if a.size else 0.0
+    say("  %-10s max|a-r| %.3e  max tol %.3e  worst (|a-r|-tol)/tol %.3f" % (name, float(np.max(np.abs(a - r))),
+                                                                          float(np.max(tol)), worst))
+    assert np.all(excess <= 0), (name, int(np.sum(excess > 0)))
+
+
 @pytest.mark.parametrize("n,d,vocab,m", [(48, 64, 700, 60), (512, 512, 40000, 512)], ids=["small", "lm"])
 def test_sampled_softmax_head_step(n, d, vocab, m):
     """A whole head step (gather, candidate GEMM, cross-entropy, gradients, sparse update) against
-    the oracle on the same bf16-rounded inputs.  The candidate logits are stored in bf16, so the
-    loss and gradients carry bf16-level error: rel_l2 and err bars of the bf16 path."""
+    the oracle on the same bf16-rounded inputs, element by element.  The head stores the candidate
+    logits and their gradient in bf16, so every element of the loss, dh and the two updates is
+    held to the bound that this storage allows (_head_error_bounds), plus the fp32 rounding of
+    the sums and of the update."""
     say("sampled head step", n, d, vocab, m)
     inp = W.make_sampled_inputs(n, d, vocab, m, seed=5)
     head = SampledSoftmaxHead(inp.W, inp.b, lr=0.1)
@@ -111,13 +157,28 @@ def test_sampled_softmax_head_step(n, d, vocab, m):
     torch.cuda.synchronize()
     lq_t = inp.lq_true.astype(np.float32).astype(np.float64)
     lq_s = inp.lq_sampled.astype(np.float32).astype(np.float64)
-    r_loss, r_dh, r_dW, r_db = oracle.sampled_softmax(f64(h), W0, b0, inp.labels, inp.sampled, lq_t, lq_s, 1.0 / n)
+    scale = 1.0 / n
+    r_loss, r_dh, r_dW, r_db = oracle.sampled_softmax(f64(h), W0, b0, inp.labels, inp.sampled, lq_t, lq_s, scale)
     e = {"loss": err(f64(loss), r_loss), "dh_rel_l2": rel_l2(f64(dh), r_dh),
          "dW_rel_l2": rel_l2(W0 - f64(head.W), head.lr * r_dW), "db_rel_l2": rel_l2(b0 - f64(head.b), head.lr * r_db)}
     say("  ", {k: "%.2e" % v for k, v in e.items()})
     assert e["loss"] <= 2e-2 and all(v <= 2e-2 for k, v in e.items() if k != "loss"), e
+    # element by element, against the bounds of the bf16 storage of the logits and their gradient
+    cand, true_pos = SampledSoftmaxHead.candidates(inp.labels, inp.sampled)
+    hh, Wc, bc = f64(h), W0[cand], b0[cand]
+    lr = head.lr
+    eb, loss_tol, adz = _head_error_bounds(hh, Wc, bc, lq_t, lq_s, true_pos, m, scale)
+    u = cand.size
+    _assert_within("loss", f64(loss), r_loss, loss_tol + 8 * U_F32 * (np.abs(r_loss) + u))
+    dh_err = eb @ np.abs(Wc) + u * U_F32 * (adz @ np.abs(Wc))
+    _assert_within("dh", f64(dh), r_dh, dh_err + U_BF16 * (np.abs(r_dh) + dh_err))
+    # candidate rows of the updated variables: W0 - W1 = lr dW up to the fp32 rounding of W1
+    W1, b1 = f64(head.W)[cand], f64(head.b)[cand]
+    dW_err = eb.T @ np.abs(hh) + n * U_F32 * (adz.T @ np.abs(hh))
+    _assert_within("dW", Wc - W1, lr * r_dW[cand], lr * dW_err + U_F32 * (np.abs(W1) + np.abs(Wc)))
+    db_err = eb.sum(axis=0) + n * U_F32 * adz.sum(axis=0)
+    _assert_within("db", bc - b1, lr * r_db[cand], lr * db_err + U_F32 * (np.abs(b1) + np.abs(bc)))
     # rows outside the candidates are untouched, bit for bit
-    cand, _ = SampledSoftmaxHead.candidates(inp.labels, inp.sampled)
     other = np.ones(vocab, bool)
     other[cand] = False
     assert np.array_equal(f64(head.W)[other], W0[other]) and np.array_equal(f64(head.b)[other], b0[other])
