@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 9
+#define TFK_ABI_VERSION 10
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -162,6 +162,22 @@ TFK_API tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void
 TFK_API tfk_status tfk_conv2d_bwd_filter(const void *x, tfk_nhwc xd, const void *dy, tfk_nhwc dyd,
                                  tfk_window p, tfk_dtype dt, float *dw,
                                  void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * tfk_conv2d_bwd_filter for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same operation and
+ * arguments without the workspace, which is replaced by a scratch array the library keeps in
+ * device memory, 128 MiB per GPU, held from the library's load on that GPU until the process
+ * ends.  The call allocates nothing.
+ *   stream : must belong to the calling thread's current device (else TFK_ERR_HIP).
+ * Errors: as tfk_conv2d_bwd_filter; TFK_ERR_WORKSPACE when the shape needs more scratch than
+ * 128 MiB (tfk_conv2d_workspace_bytes(2, ...) tells how much it needs).
+ * Every call on one GPU uses that GPU's one scratch array: calls that overlap in time on one
+ * GPU (on different streams, or from different threads) race and give wrong results; calls
+ * ordered on one stream do not.  No scratch content needs to start at zero.
+ */
+TFK_API tfk_status tfk_conv2d_bwd_filter_noalloc(const void *x, tfk_nhwc xd, const void *dy, tfk_nhwc dyd,
+                                         tfk_window p, tfk_dtype dt, float *dw, void *stream);
 
 /*
  * Conv2DBackpropInput fused with the ReLU backward and bias gradient of the layer that

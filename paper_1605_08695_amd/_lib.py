@@ -16,7 +16,8 @@ TFK_BF16 = 1
 
 # every symbol include/tfk.h declares
 EXPORTS = ["tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_maxpool_bwd_relu_bwd", "tfk_conv2d_bwd_input",
-           "tfk_conv2d_bwd_input_relu_bwd", "tfk_conv2d_bwd_filter", "tfk_conv2d_workspace_bytes",
+           "tfk_conv2d_bwd_input_relu_bwd", "tfk_conv2d_bwd_filter", "tfk_conv2d_bwd_filter_noalloc",
+           "tfk_conv2d_workspace_bytes",
            "tfk_bias_relu_fwd", "tfk_bias_relu_bwd", "tfk_bias_relu_bwd_workspace_bytes",
            "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps",
            "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd", "tfk_apply_sgd_multi",
@@ -58,6 +59,7 @@ def load(path: str = LIB_PATH):
     lib.tfk_conv2d_fwd_bias_relu.argtypes = [vp, Nhwc, vp, i32, vp, Window, st, vp, Nhwc, vp, sz, vp]
     lib.tfk_conv2d_bwd_input.argtypes = [vp, Nhwc, vp, Window, st, vp, Nhwc, f32, vp, sz, vp]
     lib.tfk_conv2d_bwd_filter.argtypes = [vp, Nhwc, vp, Nhwc, Window, st, vp, vp, sz, vp]
+    lib.tfk_conv2d_bwd_filter_noalloc.argtypes = [vp, Nhwc, vp, Nhwc, Window, st, vp, vp]
     lib.tfk_conv2d_bwd_input_relu_bwd.argtypes = [vp, Nhwc, vp, Window, st, vp, vp, Nhwc, vp, vp, sz, vp]
     lib.tfk_conv2d_workspace_bytes.argtypes = [i32, Nhwc, i32, Window, st]
     lib.tfk_conv2d_workspace_bytes.restype = sz
@@ -81,7 +83,7 @@ def load(path: str = LIB_PATH):
     lib.tfk_sampled_softmax_xent.argtypes = [vp, st, i64, i32, i32, i32, vp, vp, vp, vp, f32, vp, vp, vp]
     lib.tfk_scatter_apply_sgd.argtypes = [vp, vp, i64, i32, vp, i32, vp, i64, f32, vp]
     for name in ("tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_conv2d_bwd_input", "tfk_conv2d_bwd_input_relu_bwd",
-                 "tfk_conv2d_bwd_filter", "tfk_bias_relu_fwd",
+                 "tfk_conv2d_bwd_filter", "tfk_conv2d_bwd_filter_noalloc", "tfk_bias_relu_fwd",
                  "tfk_bias_relu_bwd", "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_bwd_relu_bwd",
                  "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps", "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd",
                  "tfk_apply_sgd_multi", "tfk_apply_momentum", "tfk_apply_adam", "tfk_softmax_xent", "tfk_gather_rows_t",

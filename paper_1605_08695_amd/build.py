@@ -17,7 +17,8 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libtfk.so")
 
-SOURCES = ["api.cpp", "eltwise.hip", "conv_fwd.hip", "conv_bwd_data.hip", "conv_bwd_filter.hip", "conv_fold.hip", "conv_band.hip"]
+SOURCES = ["api.cpp", "eltwise.hip", "conv_fwd.hip", "conv_bwd_data.hip", "conv_bwd_filter.hip", "conv_fold.hip", "conv_band.hip",
+           "noalloc.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

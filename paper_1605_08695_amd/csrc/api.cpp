@@ -341,6 +341,27 @@ tfk_status tfk_conv2d_bwd_filter(const void *x, tfk_nhwc xd, const void *dy, tfk
                       "conv2d_bwd_filter");
 }
 
+tfk_status tfk_conv2d_bwd_filter_noalloc(const void *x, tfk_nhwc xd, const void *dy, tfk_nhwc dyd, tfk_window p,
+                                         tfk_dtype dt, float *dw, void *stream) {
+    ConvShape s;
+    TRY(check_conv(xd, dyd.c, p, dt, dyd, "x", "dy", s));
+    int64_t xs = xd.pixel_stride;
+    fold_full_window(s, xs);
+    const size_t need = conv_bwd_filter_ws_bytes(dt == TFK_F32 ? 0 : 1, s);
+    const size_t have = noalloc_scratch_bytes();
+    if (need > have)
+        return fail(TFK_ERR_WORKSPACE,
+                    "conv2d_bwd_filter_noalloc: this shape needs %zu bytes of scratch, more than the library's "
+                    "fixed %zu bytes; use tfk_conv2d_bwd_filter with a workspace",
+                    need, have);
+    void *scratch = nullptr;
+    if (need) {
+        const hipError_t e = noalloc_scratch(&scratch, (hipStream_t)stream);
+        if (e != hipSuccess) return hip_status(e, "conv2d_bwd_filter_noalloc: device scratch of the stream's GPU");
+    }
+    return tfk_conv2d_bwd_filter(x, xd, dy, dyd, p, dt, dw, scratch, need, stream);
+}
+
 // ------------------------------------------------------------------ bias + ReLU
 tfk_status tfk_bias_relu_fwd(void *y, tfk_nhwc yd, const float *bias, tfk_dtype dt, void *stream) {
     if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);

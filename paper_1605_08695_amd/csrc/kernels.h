@@ -59,6 +59,10 @@ hipError_t launch_conv_bwd_filter(int dt, const void *x, int64_t xs, const void 
 // Split-K plan of bwd-filter: number of splits and reduction elements per split.
 void conv_bwd_filter_plan(int dt, const ConvShape &s, int *splits, int *k_split);
 size_t conv_bwd_filter_ws_bytes(int dt, const ConvShape &s);
+// The library's own device scratch (noalloc.hip): its size, and its address on the current
+// device, which must be the device of `stream`.
+size_t noalloc_scratch_bytes();
+hipError_t noalloc_scratch(void **ptr, hipStream_t stream);
 // bf16 convolutions with C % 8 != 0 run as an equivalent 8-channel convolution (conv_fold.hip).
 bool conv_fold_applies(int dt, const ConvShape &s);
 size_t conv_fold_ws_bytes(int op, const ConvShape &s);

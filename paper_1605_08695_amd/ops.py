@@ -182,6 +182,20 @@ def conv2d_bwd_filter(x, dy, kernel_hw, stride, pads, dw=None, ws=None, stream=N
     return dw
 
 
+def conv2d_bwd_filter_noalloc(x, dy, kernel_hw, stride, pads, dw, stream=None):
+    """conv2d_bwd_filter with the library's own device scratch in place of a workspace: the call
+    allocates nothing (dw must be given).  Calls that overlap in time on one GPU race."""
+    kh, kw = kernel_hw
+    cout = dy.shape[3]
+    if dy.dtype != x.dtype or dw.dtype != torch.float32:
+        raise TypeError("x and dy share one dtype; dw is float32")
+    if tuple(dw.shape) != (kh, kw, x.shape[3], cout) or not dw.is_contiguous():
+        raise ValueError("dw must be a contiguous float32 HWIO tensor")
+    check(load().tfk_conv2d_bwd_filter_noalloc(_ptr(x), nhwc(x), _ptr(dy), nhwc(dy), window(kh, kw, stride, pads),
+                                               _dt(x), _ptr(dw), _stream(stream)))
+    return dw
+
+
 # ----------------------------------------------------------------------------- bias + relu
 def bias_relu_fwd(y, bias, stream=None):
     """In place: y <- max(y + bias, 0)."""

@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 9
+    assert lib.tfk_abi_version() == 10
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -99,6 +99,22 @@ def test_conv_bwd_validation(lib):
     st = lib.tfk_conv2d_bwd_filter(vp(P), xd, vp(P + 0x40000000), Nhwc(64, 56, 56, 64, 0), W, BF16,
                                    vp(0), vp(P + 0xC0000000), need, None)
     assert st == NULL
+
+
+def test_conv_bwd_filter_noalloc_validation(lib):
+    """The filter gradient without a workspace: bad shapes, and a shape that needs more than the
+    library's 128 MiB of device scratch, are refused before any HIP call."""
+    W = Window(3, 3, 1, 1, 1, 1, 1, 1)
+    st = lib.tfk_conv2d_bwd_filter_noalloc(vp(P), Nhwc(2, 8, 8, 16, 0), vp(P + 0x100000), Nhwc(2, 7, 8, 32, 0), W,
+                                           BF16, vp(P + 0x200000), None)
+    assert st == SHAPE                                                 # dy is not the output shape
+    xd, dyd = Nhwc(512, 224, 224, 3, 0), Nhwc(512, 55, 55, 64, 0)
+    W1 = Window(11, 11, 4, 4, 2, 2, 2, 2)
+    need = lib.tfk_conv2d_workspace_bytes(2, xd, 64, W1, BF16)
+    assert need > 128 << 20
+    st = lib.tfk_conv2d_bwd_filter_noalloc(vp(P), xd, vp(P + 0x40000000), dyd, W1, BF16, vp(P + 0x80000000), None)
+    assert st == WORKSPACE
+    assert b"128" in lib.tfk_last_error() or b"134217728" in lib.tfk_last_error()
 
 
 def test_conv_bwd_input_relu_bwd_validation(lib):
