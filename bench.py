@@ -10,8 +10,10 @@ and bias.  All inputs are resident in HBM before timing starts.
 
 Prints one JSON line: ms per step (the timed region is K whole steps between
 two device synchronisations), conv TFLOP/s against the bf16 MFMA peak, the
-roofline entry of the convolution kernels measured with HIP events on the
-stream they run on, and the CPU oracle timed on a bounded batch slice.
+roofline entry of the dominant convolution kernel measured with HIP events on
+the stream it runs on, warm (the step's cache state) and cold (caches flushed
+before every op) per-op figures, and the CPU oracle timed on a bounded batch
+slice, with its host's CPU model and a single-thread one-layer time.
 
 Launch modes: ``streams`` (default) launches every op from the host, the filter
 gradients on a second stream that overlaps the rest of the backward pass;
@@ -157,16 +159,34 @@ def conv_flops(net, op):
 
 
 class EventTrace:
-    """Step-driver hook that brackets every op with HIP events on the stream it runs on."""
+    """Step-driver hook that brackets every op with HIP events on the stream it runs on.
 
-    def __init__(self, torch):
+    Before each start event the stream is given work that keeps the GPU busy while the host
+    enqueues the event, the op and the end event, so the pair measures the op's kernels and no
+    host launch gap: ``pad`` (a spin kernel of a few tens of microseconds, caches untouched:
+    warm figures), or with ``flush`` (a byte buffer larger than the 256 MiB last-level cache)
+    a fill of that buffer, which also evicts the op's inputs from every cache (cold figures)."""
+
+    def __init__(self, torch, pad_cycles=0, flush=None):
         self.torch = torch
+        self.pad_cycles = pad_cycles
+        self.flush = flush
         self.rec = []           # (kind, op, start, end)
+
+    def _stream(self, stream):
+        return stream if stream is not None else self.torch.cuda.current_stream()
 
     def _event(self, stream):
         e = self.torch.cuda.Event(enable_timing=True)
-        e.record(stream if stream is not None else self.torch.cuda.current_stream())
+        e.record(self._stream(stream))
         return e
+
+    def _prefill(self, stream):
+        with self.torch.cuda.stream(self._stream(stream)):
+            if self.flush is not None:
+                self.flush.fill_(1)
+            elif self.pad_cycles:
+                self.torch.cuda._sleep(self.pad_cycles)
 
     def __call__(self, event, op, stream=None, **t):
         if event.endswith(":end"):
@@ -174,7 +194,22 @@ class EventTrace:
             assert kind == event[:-4] and op0 is op
             self.rec.append((kind, op0, s, self._event(stream)))
         else:
+            self._prefill(stream)
             self.open = (event, op, self._event(stream))
+
+
+def sleep_cycles_for(torch, us):
+    """Spin-kernel cycles that take about ``us`` microseconds on this GPU (measured)."""
+    torch.cuda._sleep(1000)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n = 200000
+    e0.record()
+    torch.cuda._sleep(n)
+    e1.record()
+    torch.cuda.synchronize()
+    per_us = n / max(e0.elapsed_time(e1) * 1e3, 1e-3)
+    return max(1000, int(per_us * us))
 
 
 def measure_classifier(args, torch, W, Replica):
@@ -321,6 +356,82 @@ def gemm_reference(net, torch):
     print(json.dumps({"gemm_reference": out}))
 
 
+def cpu_model():
+    """The host CPU's model name (first processor in /proc/cpuinfo)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def per_op_pass(torch, rep, tr, reps):
+    """Average event duration of every op (one-stream step, ``tr`` brackets each op), by kind and
+    by (kind, layer)."""
+    per_kind, per_layer = {}, {}
+    for r in range(reps):
+        tr.rec.clear()
+        rep.step(trace=tr, concurrent=False)
+        torch.cuda.synchronize()
+        for kind, op, s, e in tr.rec:
+            ms = s.elapsed_time(e)
+            if kind == "conv_bias_relu_fwd":
+                kind = "conv_fwd"       # the forward convolution with its bias + ReLU epilogue
+            if kind == "conv_bwd_input_relu_bwd":
+                kind = "conv_bwd_input"  # the input gradient with the producer's ReLU backward epilogue
+            per_kind[kind] = per_kind.get(kind, 0.0) + ms / reps
+            key = (kind, op.name if op is not None else "all")
+            per_layer[key] = per_layer.get(key, 0.0) + ms / reps
+    return per_kind, per_layer
+
+
+def step_figures(net, rep, per_kind, per_layer, D):
+    """Conv FLOP rates and elementwise HBM rates of one per-op pass."""
+    conv_kinds = ("conv_fwd", "conv_bwd_input", "conv_bwd_filter")
+    conv_ms = sum(per_kind.get(k, 0.0) for k in conv_kinds)
+    flops = {k: 0.0 for k in conv_kinds}
+    for op in net.convs:
+        f = conv_flops(net, op)
+        flops["conv_fwd"] += f
+        flops["conv_bwd_filter"] += f
+        if op.src != "x" or net.input_grad:
+            flops["conv_bwd_input"] += f
+    conv_flop = sum(flops.values())
+    ew_kinds = ("bias_relu_fwd", "bias_relu_bwd", "maxpool_fwd", "maxpool_bwd", "maxpool_relu_bwd")
+    ew_bytes = {k: 0.0 for k in ew_kinds}
+    for op in net.ops:
+        # the kinds this op actually ran as (bias + ReLU forward runs in the conv epilogue; a pool
+        # fused with the ReLU backward of its producer replaces that conv's bias_relu_bwd)
+        if hasattr(op, "cout"):
+            kinds = [] if op.name in rep.relu_fused else ["bias_relu_bwd"]
+        else:
+            kinds = ["maxpool_fwd"]
+            if op.name in rep.pool_relu:
+                kinds.append("maxpool_relu_bwd")
+            elif op.src != "x":
+                kinds.append("maxpool_bwd")
+        A = rep.argmax[op.name].element_size() if op.name in rep.argmax else 4
+        for k in kinds:
+            ew_bytes[k] += elementwise_bytes(net, k, op, D, A)
+    sgd_bytes = rep.n_params * 14.0
+    ew_ms = sum(per_kind.get(k, 0.0) for k in ew_kinds) + per_kind.get("apply_sgd", 0.0)
+    ew_total = sum(ew_bytes.values()) + sgd_bytes
+    by_kind = {}
+    for k in ew_kinds:
+        if per_kind.get(k):
+            by_kind[k] = round(ew_bytes[k] / (per_kind[k] * 1e-3) / 1e9, 1)
+    if per_kind.get("apply_sgd"):
+        by_kind["apply_sgd"] = round(sgd_bytes / (per_kind["apply_sgd"] * 1e-3) / 1e9, 1)
+    return {"flops": flops, "conv_flop": conv_flop, "conv_ms": conv_ms,
+            "conv_tflops": conv_flop / (conv_ms * 1e-3) / 1e12,
+            "conv_tflops_by_direction": {k: round(flops[k] / (per_kind[k] * 1e-3) / 1e12, 1) for k in conv_kinds},
+            "ew_ms": ew_ms, "ew_bytes": ew_total, "ew_gbs": ew_total / (ew_ms * 1e-3) / 1e9,
+            "ew_gbs_by_kind": by_kind}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -392,59 +503,24 @@ def main():
 
     # ---------------------------------------------------------------- per-op events
     # Every op launched alone, in order, on one stream and bracketed by HIP events on that
-    # stream: the duration of each kernel by itself (in the two-stream step the filter
-    # gradients share the GPU with the input gradients), from which the roofline is taken.
-    tr = EventTrace(torch)
+    # stream: the duration of each op's kernels by themselves (in the two-stream step the filter
+    # gradients share the GPU with the input gradients), from which the roofline is taken.  Each
+    # op's start event is preceded on its stream by work that keeps the GPU busy while the host
+    # enqueues the op (so no launch gap is counted): a spin kernel for the warm figures (the
+    # step's real cache state), a 512 MiB fill for the cold ones (every cache flushed).
     reps = max(3, min(10, args.steps))
-    per_kind = {}
-    per_layer = {}
-    for r in range(reps):
-        tr.rec.clear()
-        rep.step(trace=tr, concurrent=False)
-        torch.cuda.synchronize()
-        for kind, op, s, e in tr.rec:
-            ms = s.elapsed_time(e)
-            if kind == "conv_bias_relu_fwd":
-                kind = "conv_fwd"       # the forward convolution with its bias + ReLU epilogue
-            if kind == "conv_bwd_input_relu_bwd":
-                kind = "conv_bwd_input"  # the input gradient with the producer's ReLU backward epilogue
-            per_kind.setdefault(kind, 0.0)
-            per_kind[kind] += ms / reps
-            key = (kind, op.name if op is not None else "all")
-            per_layer[key] = per_layer.get(key, 0.0) + ms / reps
+    pad = sleep_cycles_for(torch, 200.0)
+    warm = per_op_pass(torch, rep, EventTrace(torch, pad_cycles=pad), reps)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    cold = per_op_pass(torch, rep, EventTrace(torch, flush=flush), reps)
+    del flush
+    per_kind, per_layer = warm
+    fig_w = step_figures(net, rep, *warm, D)
+    fig_c = step_figures(net, rep, *cold, D)
     conv_kinds = ("conv_fwd", "conv_bwd_input", "conv_bwd_filter")
-    conv_ms = sum(per_kind.get(k, 0.0) for k in conv_kinds)
-    flops = {k: 0.0 for k in conv_kinds}
-    launches = 0
-    for op in net.convs:
-        f = conv_flops(net, op)
-        flops["conv_fwd"] += f
-        flops["conv_bwd_filter"] += f
-        launches += 2
-        if op.src != "x" or net.input_grad:
-            flops["conv_bwd_input"] += f
-            launches += 1
-    conv_flop = sum(flops.values())
-    conv_tflops = conv_flop / (conv_ms * 1e-3) / 1e12
-    ew_kinds = ("bias_relu_fwd", "bias_relu_bwd", "maxpool_fwd", "maxpool_bwd", "maxpool_relu_bwd")
-    ew_bytes = {k: 0.0 for k in ew_kinds}
-    for op in net.ops:
-        # the kinds this op actually ran as (bias + ReLU forward runs in the conv epilogue; a pool
-        # fused with the ReLU backward of its producer replaces that conv's bias_relu_bwd)
-        if hasattr(op, "cout"):
-            kinds = [] if op.name in rep.relu_fused else ["bias_relu_bwd"]
-        else:
-            kinds = ["maxpool_fwd"]
-            if op.name in rep.pool_relu:
-                kinds.append("maxpool_relu_bwd")
-            elif op.src != "x":
-                kinds.append("maxpool_bwd")
-        A = rep.argmax[op.name].element_size() if op.name in rep.argmax else 4
-        for k in kinds:
-            ew_bytes[k] += elementwise_bytes(net, k, op, D, A)
-    sgd_bytes = rep.n_params * 14.0
-    ew_ms = sum(per_kind.get(k, 0.0) for k in ew_kinds) + per_kind.get("apply_sgd", 0.0)
-    ew_gbs = (sum(ew_bytes.values()) + sgd_bytes) / (ew_ms * 1e-3) / 1e9
+    flops, conv_flop = fig_w["flops"], fig_w["conv_flop"]
+    conv_tflops = fig_w["conv_tflops"]
+    ew_gbs = fig_w["ew_gbs"]
 
     # ---------------------------------------------------------------- in-place updates alone
     # over this network's variables and over 61.1M variables (AlexNet with its classifier)
@@ -473,13 +549,41 @@ def main():
         c0 = time.perf_counter()
         onet.step(snet, sinp.x, sinp.weights, sinp.biases, sinp.g)
         c1 = time.perf_counter()
+        # one layer on one thread: AlexNet conv3 forward (3x3, 192 -> 384 channels at 13x13) on 4 images
+        lay = next(op for op in net.convs if op.name == "conv3")
+        nt = oracle.num_threads()
+        xs = np.random.default_rng(1).standard_normal((4,) + net.tensors[lay.src][1:])
+        ws = sinp.weights[lay.name]
+        oracle.set_num_threads(1)
+        try:
+            t0 = time.perf_counter()
+            oracle.conv2d_fwd(xs, ws, (lay.sh, lay.sw), lay.pads)
+            t_one = time.perf_counter() - t0
+        finally:
+            oracle.set_num_threads(nt)
+        f_one = conv_flops(net, lay) * 4 / args.batch
         cpu = {"value": round((c1 - c0) * 1e3 * args.batch / k, 1), "unit": "ms/step",
-               "cores": oracle.num_threads(), "kind": "oracle",
+               "cores": nt, "kind": "oracle", "cpu_model": cpu_model(),
                "sample": "%d of the %d images of one step (fp64 loop nests, %.1f s); oracle cost is linear "
-                         "in batch, scaled x%g" % (k, args.batch, c1 - c0, args.batch / k)}
+                         "in batch, scaled x%g" % (k, args.batch, c1 - c0, args.batch / k),
+               "single_thread_layer": {"layer": "conv3 forward, 4 images", "s": round(t_one, 3),
+                                       "gflops": round(f_one / t_one / 1e9, 3),
+                                       "full_batch_s_scaled": round(t_one * args.batch / 4, 1)}}
 
-    dom = max(conv_kinds, key=lambda k: per_kind.get(k, 0.0))
-    n_dom = sum(1 for op in net.convs if dom != "conv_bwd_input" or op.src != "x" or net.input_grad)
+    # The roofline kernel: the convolution kernel with the most time per step.  The first layer
+    # (3 input channels) runs the band kernels, every other layer of a direction the implicit-GEMM
+    # kernel, so a group is one direction over the layers after the first.
+    groups = {}
+    for (kind, name), ms in per_layer.items():
+        if kind in conv_kinds and name != net.convs[0].name:
+            g = groups.setdefault(kind, [0.0, 0, 0.0])
+            g[0] += ms
+            g[1] += 1
+            g[2] += conv_flops(net, next(op for op in net.convs if op.name == name))
+    dom = max(groups, key=lambda k: groups[k][0])
+    dom_ms, n_dom, dom_flop = groups[dom]
+    cold_ms = sum(v for (kind, name), v in cold[1].items() if kind == dom and name != net.convs[0].name)
+    dom_layers = [op.name for op in net.convs[1:]]
     out = {
         "metric": METRIC,
         "value": round(ms_per_step, 4),
@@ -504,19 +608,30 @@ def main():
         "conv_gflop_per_step": round(conv_flop / 1e9, 2),
         "conv_tflops": round(conv_tflops, 1),
         "conv_pct_bf16_peak": round(100 * conv_tflops / PEAK_BF16_TFLOPS, 2),
-        "conv_tflops_by_direction": {k: round(flops[k] / (per_kind[k] * 1e-3) / 1e12, 1) for k in conv_kinds},
+        "conv_tflops_by_direction": fig_w["conv_tflops_by_direction"],
         "eltwise_gbs": round(ew_gbs, 1),
         "eltwise_pct_hbm_peak": round(100 * ew_gbs / PEAK_HBM_GBS, 2),
+        "eltwise_gbs_by_kind": fig_w["ew_gbs_by_kind"],
+        "cold": {"what": "every op after a 512 MiB fill of a scratch buffer on its stream (caches flushed)",
+                 "conv_tflops": round(fig_c["conv_tflops"], 1),
+                 "conv_pct_bf16_peak": round(100 * fig_c["conv_tflops"] / PEAK_BF16_TFLOPS, 2),
+                 "conv_tflops_by_direction": fig_c["conv_tflops_by_direction"],
+                 "eltwise_gbs": round(fig_c["ew_gbs"], 1),
+                 "eltwise_pct_hbm_peak": round(100 * fig_c["ew_gbs"] / PEAK_HBM_GBS, 2),
+                 "eltwise_gbs_by_kind": fig_c["ew_gbs_by_kind"],
+                 "per_op_ms": {k: round(v, 4) for k, v in sorted(cold[0].items())}},
         "per_op_ms": {k: round(v, 4) for k, v in sorted(per_kind.items())},
-        "roofline": {"kernel": "implicit-GEMM convolution (%s, %d launches/step)" % (dom, n_dom),
+        "roofline": {"kernel": "%s implicit-GEMM kernel of %s (%d launches/step)" % (dom, ",".join(dom_layers), n_dom),
                      "bound": "mfma",
-                     "achieved": round(flops[dom] / (per_kind[dom] * 1e-3) / 1e12, 1),
+                     "achieved": round(dom_flop / (dom_ms * 1e-3) / 1e12, 1),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(flops[dom] / (per_kind[dom] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                     "frac": round(dom_flop / (dom_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
                      "traffic": recorded_traffic(dom),
-                     "avg_launch_us": round(per_kind[dom] * 1e3 / n_dom, 2),
-                     "measured": "HIP events around each launch, every op alone on one stream",
-                     "flop_per_launch": round(flops[dom] / n_dom)},
+                     "avg_launch_us": round(dom_ms * 1e3 / n_dom, 2),
+                     "avg_launch_us_cold": round(cold_ms * 1e3 / n_dom, 2),
+                     "measured": "HIP events around each launch on its stream, every op alone on one stream, "
+                                 "the stream kept busy ahead of the start event",
+                     "flop_per_launch": round(dom_flop / n_dom)},
         "cpu_baseline": cpu,
         "updates": updates,
         "classifier": classifier,
