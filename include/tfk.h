@@ -28,11 +28,12 @@
  *    stream) and returns its status synchronously.  Arguments are validated
  *    before anything is launched: on a non-OK status nothing was enqueued and
  *    no buffer was touched.  tfk_last_error() then holds a message.
- *  - Ownership: the caller owns every buffer.  The library allocates no
- *    device memory and keeps no pointer after the call returns; buffers must
- *    stay valid until the stream has passed the operation.  Operations that
- *    need scratch memory take a caller-provided workspace sized by the
- *    matching *_workspace_bytes query.
+ *  - Ownership: the caller owns every buffer.  No call allocates device
+ *    memory (the library's only memory of its own is the fixed scratch of
+ *    tfk_conv2d_bwd_filter_noalloc) and none keeps a pointer after it returns;
+ *    buffers must stay valid until the stream has passed the operation.
+ *    Operations that need scratch memory take a caller-provided workspace
+ *    sized by the matching *_workspace_bytes query.
  *  - Aliasing: outputs must not overlap inputs except where an argument is
  *    documented as in-place.  A detected overlap returns TFK_ERR_ALIAS.
  *  - An empty batch (n == 0) is valid: nothing is read; reductions over the
