@@ -356,7 +356,8 @@ def gemm_reference(net, torch):
     print(json.dumps({"gemm_reference": out}))
 
 
-CONV_CALLS = {"conv2d_fwd_bias_relu": "conv_fwd", "conv2d_fwd": "conv_fwd", "conv2d_bwd_input": "conv_bwd_input",
+CONV_CALLS = {"conv2d_fwd_bias_relu": "conv_fwd", "conv2d_fwd_bias_relu_maxpool": "conv_fwd", "conv2d_fwd": "conv_fwd",
+              "conv2d_bwd_input": "conv_bwd_input",
               "conv2d_bwd_input_relu_bwd": "conv_bwd_input", "conv2d_bwd_filter": "conv_bwd_filter"}
 
 
@@ -420,8 +421,8 @@ def per_op_pass(torch, rep, tr, reps):
         torch.cuda.synchronize()
         for kind, op, s, e in tr.rec:
             ms = s.elapsed_time(e)
-            if kind == "conv_bias_relu_fwd":
-                kind = "conv_fwd"       # the forward convolution with its bias + ReLU epilogue
+            if kind in ("conv_bias_relu_fwd", "conv_bias_relu_maxpool_fwd"):
+                kind = "conv_fwd"       # the forward convolution with its bias + ReLU (+ max-pool) epilogue
             if kind == "conv_bwd_input_relu_bwd":
                 kind = "conv_bwd_input"  # the input gradient with the producer's ReLU backward epilogue
             per_kind[kind] = per_kind.get(kind, 0.0) + ms / reps
@@ -450,7 +451,7 @@ def step_figures(net, rep, per_kind, per_layer, D):
         if hasattr(op, "cout"):
             kinds = [] if op.name in rep.relu_fused else ["bias_relu_bwd"]
         else:
-            kinds = ["maxpool_fwd"]
+            kinds = [] if op.name in rep.pool_in_conv else ["maxpool_fwd"]
             if op.name in rep.pool_relu:
                 kinds.append("maxpool_relu_bwd")
             elif op.src != "x":

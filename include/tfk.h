@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 10
+#define TFK_ABI_VERSION 11
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -261,6 +261,26 @@ TFK_API tfk_status tfk_maxpool_fwd(const void *x, tfk_nhwc xd, tfk_window p, tfk
  */
 TFK_API tfk_status tfk_maxpool_fwd_taps(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype dt,
                                 void *y, tfk_nhwc yd, uint8_t *taps, void *stream);
+
+/*
+ * Conv2D + BiasAdd + ReLU followed by MaxPool of its output, in one call (Section 5: kernels
+ * hand-fused for performance-critical operations, kernel fusion being the direction the paper
+ * names; Section 6.1: convolution and pooling on the critical path):
+ *   y        = tfk_conv2d_fwd_bias_relu(x, w, bias)          (yd-shaped, written)
+ *   py, taps = tfk_maxpool_fwd_taps(y, pp)                   (pyd-shaped pool of y, uint8 taps)
+ * with the same values, bit for bit, as those two calls.  Where the convolution's output tiles
+ * can be laid out as bands of whole image rows that hold whole pool windows (bf16, a VALID pool,
+ * at most 192 output pixels per band), one kernel computes y, keeps each band in LDS and pools
+ * it there; other shapes run the two kernels.
+ *   x, xd, w, cout, bias, p, dt, y, yd, ws : as tfk_conv2d_fwd_bias_relu (bias required).
+ *   pp   : the pool window over y (kh * kw <= 256).
+ *   py   : pyd-shaped, type dt, overwritten.   taps : dense uint8 [pyd.n][pyd.h][pyd.w][pyd.c].
+ * Errors: as the two calls; py and taps must not overlap x, w, y, bias or each other.
+ */
+TFK_API tfk_status tfk_conv2d_fwd_bias_relu_maxpool(const void *x, tfk_nhwc xd, const void *w, int32_t cout,
+                                            const float *bias, tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
+                                            tfk_window pp, void *py, tfk_nhwc pyd, uint8_t *taps, void *ws,
+                                            size_t ws_bytes, void *stream);
 
 /*
  * MaxPool backward (Section 6.1 pooling on the critical path; Section 4.1

@@ -17,6 +17,7 @@ TFK_BF16 = 1
 # every symbol include/tfk.h declares
 EXPORTS = ["tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_maxpool_bwd_relu_bwd", "tfk_conv2d_bwd_input",
            "tfk_conv2d_bwd_input_relu_bwd", "tfk_conv2d_bwd_filter", "tfk_conv2d_bwd_filter_noalloc",
+           "tfk_conv2d_fwd_bias_relu_maxpool",
            "tfk_conv2d_workspace_bytes",
            "tfk_bias_relu_fwd", "tfk_bias_relu_bwd", "tfk_bias_relu_bwd_workspace_bytes",
            "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps",
@@ -57,6 +58,8 @@ def load(path: str = LIB_PATH):
     st = ctypes.c_int
     lib.tfk_conv2d_fwd.argtypes = [vp, Nhwc, vp, i32, Window, st, vp, Nhwc, vp, sz, vp]
     lib.tfk_conv2d_fwd_bias_relu.argtypes = [vp, Nhwc, vp, i32, vp, Window, st, vp, Nhwc, vp, sz, vp]
+    lib.tfk_conv2d_fwd_bias_relu_maxpool.argtypes = [vp, Nhwc, vp, i32, vp, Window, st, vp, Nhwc, Window, vp, Nhwc,
+                                                     vp, vp, sz, vp]
     lib.tfk_conv2d_bwd_input.argtypes = [vp, Nhwc, vp, Window, st, vp, Nhwc, f32, vp, sz, vp]
     lib.tfk_conv2d_bwd_filter.argtypes = [vp, Nhwc, vp, Nhwc, Window, st, vp, vp, sz, vp]
     lib.tfk_conv2d_bwd_filter_noalloc.argtypes = [vp, Nhwc, vp, Nhwc, Window, st, vp, vp]
@@ -82,7 +85,7 @@ def load(path: str = LIB_PATH):
     lib.tfk_gather_rows_t.argtypes = [vp, st, i64, i32, vp, i32, i32, vp, vp]
     lib.tfk_sampled_softmax_xent.argtypes = [vp, st, i64, i32, i32, i32, vp, vp, vp, vp, f32, vp, vp, vp]
     lib.tfk_scatter_apply_sgd.argtypes = [vp, vp, i64, i32, vp, i32, vp, i64, f32, vp]
-    for name in ("tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_conv2d_bwd_input", "tfk_conv2d_bwd_input_relu_bwd",
+    for name in ("tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_conv2d_fwd_bias_relu_maxpool", "tfk_conv2d_bwd_input", "tfk_conv2d_bwd_input_relu_bwd",
                  "tfk_conv2d_bwd_filter", "tfk_conv2d_bwd_filter_noalloc", "tfk_bias_relu_fwd",
                  "tfk_bias_relu_bwd", "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_bwd_relu_bwd",
                  "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps", "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd",

@@ -197,13 +197,15 @@ size_t tfk_conv2d_workspace_bytes(int32_t op, tfk_nhwc xd, int32_t cout, tfk_win
     return conv_bwd_filter_ws_bytes(dti, s);
 }
 
-// Shared by tfk_conv2d_fwd (bias == nullptr) and tfk_conv2d_fwd_bias_relu.
-static tfk_status conv_fwd_impl(const void *x, tfk_nhwc xd, const void *w, int32_t cout, const float *bias,
-                                tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd, void *ws, size_t ws_bytes,
-                                void *stream, const char *what) {
-    ConvShape s;
+// Validation of the forward convolution (shared by tfk_conv2d_fwd, tfk_conv2d_fwd_bias_relu and the
+// fused max-pool form): fills the shape, x's pixel stride after flattening and the workspace need.
+static tfk_status conv_fwd_check(const void *x, tfk_nhwc &xd, const void *w, int32_t cout, const float *bias,
+                                 tfk_window p, tfk_dtype dt, void *y, tfk_nhwc &yd, void *ws, size_t ws_bytes,
+                                 ConvShape &s, int64_t &xs, size_t &need) {
     TRY(check_conv(xd, cout, p, dt, yd, "x", "y", s));
-    if (xd.n == 0) return ok();
+    xs = xd.pixel_stride;
+    need = 0;
+    if (xd.n == 0) return TFK_OK;
     const int64_t es = esize(dt);
     TRY(need_ptr(x, "x"));
     TRY(need_ptr(w, "w"));
@@ -216,17 +218,27 @@ static tfk_status conv_fwd_impl(const void *x, tfk_nhwc xd, const void *w, int32
         return fail(TFK_ERR_ALIAS, "y overlaps x or w");
     if (bias != nullptr && overlap(y, yb, bias, (int64_t)cout * 4)) return fail(TFK_ERR_ALIAS, "y overlaps bias");
     const int64_t xbytes = view_bytes(xd, es), wbytes = filter_bytes(s, es);
-    int64_t xs = xd.pixel_stride;
     fold_full_window(s, xs);
     const int dti = dt == TFK_F32 ? 0 : 1;
-    const size_t need = std::max(conv_fold_applies(dti, s) ? conv_fold_ws_bytes(0, s) : 0,
-                                 conv_fwd_split_ws_bytes(dti, s));
+    need = std::max(conv_fold_applies(dti, s) ? conv_fold_ws_bytes(0, s) : 0, conv_fwd_split_ws_bytes(dti, s));
     TRY(check_ws(ws, ws_bytes, need));
     if (need && (overlap(ws, (int64_t)need, x, xbytes) || overlap(ws, (int64_t)need, w, wbytes) ||
                  overlap(ws, (int64_t)need, y, yb)))
         return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
-    return hip_status(launch_conv_fwd(dti, x, xs, w, y, yd.pixel_stride, s, bias, need ? ws : nullptr,
-                                      (hipStream_t)stream),
+    return TFK_OK;
+}
+
+// Shared by tfk_conv2d_fwd (bias == nullptr) and tfk_conv2d_fwd_bias_relu.
+static tfk_status conv_fwd_impl(const void *x, tfk_nhwc xd, const void *w, int32_t cout, const float *bias,
+                                tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd, void *ws, size_t ws_bytes,
+                                void *stream, const char *what) {
+    ConvShape s;
+    int64_t xs;
+    size_t need;
+    TRY(conv_fwd_check(x, xd, w, cout, bias, p, dt, y, yd, ws, ws_bytes, s, xs, need));
+    if (xd.n == 0) return ok();
+    return hip_status(launch_conv_fwd(dt == TFK_F32 ? 0 : 1, x, xs, w, y, yd.pixel_stride, s, bias,
+                                      need ? ws : nullptr, (hipStream_t)stream),
                       what);
 }
 
@@ -472,6 +484,49 @@ tfk_status tfk_maxpool_fwd(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype d
 tfk_status tfk_maxpool_fwd_taps(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
                                 uint8_t *taps, void *stream) {
     return maxpool_fwd_impl(x, xd, p, dt, y, yd, taps, true, stream);
+}
+
+tfk_status tfk_conv2d_fwd_bias_relu_maxpool(const void *x, tfk_nhwc xd, const void *w, int32_t cout,
+                                            const float *bias, tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
+                                            tfk_window pp, void *py, tfk_nhwc pyd, uint8_t *taps, void *ws,
+                                            size_t ws_bytes, void *stream) {
+    ConvShape s;
+    int64_t xs;
+    size_t need;
+    TRY(need_ptr(bias, "bias"));
+    TRY(need_align(bias, 4, "bias"));
+    TRY(conv_fwd_check(x, xd, w, cout, bias, p, dt, y, yd, ws, ws_bytes, s, xs, need));
+    tfk_nhwc yin = yd;
+    PoolGeom g;
+    TRY(check_pool(yin, pp, dt, pyd, "y", "py", g));
+    if ((int64_t)pp.kh * pp.kw > 256) return fail(TFK_ERR_SHAPE, "tap argmax needs kh * kw <= 256");
+    if (xd.n == 0) return ok();
+    const int64_t es = esize(dt);
+    TRY(need_ptr(py, "py"));
+    TRY(need_ptr(taps, "taps"));
+    TRY(need_align(py, es, "py"));
+    const int64_t xb = view_bytes(xd, es), wb = filter_bytes(s, es), yb = view_bytes(yd, es);
+    const int64_t pb = view_bytes(pyd, es), tb = (int64_t)pyd.n * pyd.h * pyd.w * pyd.c, bb = (int64_t)cout * 4;
+    if (overlap(y, yb, bias, bb)) return fail(TFK_ERR_ALIAS, "y overlaps bias");
+    if (overlap(py, pb, x, xb) || overlap(py, pb, w, wb) || overlap(py, pb, y, yb) || overlap(py, pb, bias, bb))
+        return fail(TFK_ERR_ALIAS, "py overlaps x, w, y or bias");
+    if (overlap(taps, tb, x, xb) || overlap(taps, tb, w, wb) || overlap(taps, tb, y, yb) || overlap(taps, tb, py, pb) ||
+        overlap(taps, tb, bias, bb))
+        return fail(TFK_ERR_ALIAS, "taps overlap a tensor");
+    if (need && (overlap(ws, (int64_t)need, py, pb) || overlap(ws, (int64_t)need, taps, tb)))
+        return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
+    hipStream_t st = (hipStream_t)stream;
+    const char *what = "conv2d_fwd_bias_relu_maxpool";
+    if (dt == TFK_BF16) {
+        hipError_t e;
+        if (conv_fwd_pool_fused(x, xs, w, y, yd.pixel_stride, s, bias, g, py, pyd.pixel_stride, taps, st, &e))
+            return hip_status(e, what);
+    }
+    // not one kernel for this shape: the convolution, then the max-pool of y
+    const hipError_t e = launch_conv_fwd(dt == TFK_F32 ? 0 : 1, x, xs, w, y, yd.pixel_stride, s, bias,
+                                         need ? ws : nullptr, st);
+    if (e != hipSuccess) return hip_status(e, what);
+    return hip_status(launch_maxpool_fwd(dt == TFK_F32 ? 0 : 1, y, g, py, taps, true, st), what);
 }
 
 static tfk_status maxpool_bwd_impl(const void *dy, const void *argmax, bool taps, tfk_nhwc yd, tfk_window p,

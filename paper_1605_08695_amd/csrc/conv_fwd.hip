@@ -64,6 +64,91 @@ static hipError_t conv_fwd_t(const void *x, int64_t xs, const void *w, void *y, 
     return igemm_launch<T, DIR_FWD>(a, mj, 1, vi, vj, st);
 }
 
+// Row bands of a forward convolution whose J tiles each hold whole windows of a VALID max-pool
+// of its output: q pool rows per band need rows = (q - 1) * psh + pkh output rows of OW
+// pixels (at most bj), consecutive bands start step = q * psh rows apart (sharing the rows
+// their windows overlap on), and enough bands run to cover every pool row and every output row.
+namespace {
+struct BandPlan {
+    int bj, q, rows, step, bands;
+};
+
+bool band_plan(const ConvShape &s, const PoolGeom &g, int bj, BandPlan &b) {
+    int q = 0;
+    while (q < g.OH && (q * g.sh + g.KH) * s.OW <= bj) ++q;
+    if (q < 1) return false;
+    b.bj = bj;
+    b.q = q;
+    b.rows = (q - 1) * g.sh + g.KH;
+    b.step = q * g.sh;
+    const int by_pool = (g.OH + q - 1) / q;
+    const int by_rows = s.OH > b.rows ? (s.OH - b.rows + b.step - 1) / b.step + 1 : 1;
+    b.bands = by_pool > by_rows ? by_pool : by_rows;
+    return true;
+}
+}  // namespace
+
+bool conv_fwd_pool_fused(const void *x, int64_t xs, const void *w, void *y, int64_t ys, const ConvShape &s,
+                         const float *bias, const PoolGeom &g, void *py, int64_t pys, uint8_t *taps,
+                         hipStream_t st, hipError_t *err) {
+    *err = hipSuccess;
+    // the pool reads exactly y (VALID, no padding), and the convolution takes the pipelined
+    // bf16 path without a split
+    if (g.pt != 0 || g.pl != 0 || g.N != s.N || g.H != s.OH || g.W != s.OW || g.C != s.K || g.xs != ys) return false;
+    if (g.KH * g.KW > 256 || g.KH > s.OH || g.KW > s.OW) return false;
+    // (no padding at the bottom or right either: every window lies inside y)
+    if (g.OH != (s.OH - g.KH) / g.sh + 1 || g.OW != (s.OW - g.KW) / g.sw + 1) return false;
+    if (conv_band_fwd_applies(s) || conv_fold_applies(1, s)) return false;
+    if (s.K % 8 != 0 || s.C % 8 != 0 || xs % 8 != 0 || ys % 8 != 0 || pys % 2 != 0) return false;
+    if (!aligned16p(w) || !aligned16p(x) || !aligned16p(y) || ((uintptr_t)py & 3) || ((uintptr_t)taps & 1))
+        return false;
+    int ks;
+    if (fwd_splits(s, &ks) > 1) return false;
+    BandPlan best{}, b{};
+    bool have = false;
+    for (int bj : {128, 192}) {
+        if (band_plan(s, g, bj, b) && (!have || (int64_t)b.bands * b.bj < (int64_t)best.bands * best.bj)) {
+            best = b;
+            have = true;
+        }
+    }
+    if (!have) return false;
+    // Bands cost recomputed rows (windows that overlap across bands) and tile rows past the band's
+    // pixels; fused only when that adds at most 15 % to the output rows (measured on AlexNet:
+    // conv5 + pool5, 13 x 13, one band of 169 of 192 rows: 42.6 -> 41.3 us; conv2 + pool2, 27 x 27,
+    // 5 bands of 189 of 192 rows with a shared row between bands, 32 % more rows: 84 -> 118 us).
+    if ((int64_t)best.bands * best.bj * 100 > (int64_t)s.OH * s.OW * 115) return false;
+    IgArgs a;
+    fill_geom(a, s);
+    a.src_i = w;
+    a.src_j = x;
+    a.out = y;
+    a.xs = xs;
+    a.ys = ys;
+    a.NI = s.K;
+    a.bias = bias;
+    const int64_t wb = (int64_t)s.KH * s.KW * s.C * s.K * 2;
+    if (!igemm2_fits(a, wb, span_bytes((int64_t)s.N * s.H * s.W, xs, s.C))) return false;
+    a.band_rows = best.rows;
+    a.band_step = best.step;
+    a.bands_per_img = best.bands;
+    a.pool_y = py;
+    a.pool_taps = taps;
+    a.pkh = g.KH;
+    a.pkw = g.KW;
+    a.psh = g.sh;
+    a.psw = g.sw;
+    a.pOH = g.OH;
+    a.pOW = g.OW;
+    a.pool_rows = best.q;
+    a.pool_ys = pys;
+    const int bi = 64;       // 64-channel tiles: two blocks per CU (fastest of 64/128/192 on the cases above)
+    const int mj = s.N * best.bands * best.bj;      // one J tile per (image, band)
+    if (!igemm2_launch<DIR_FWD>(a, mj, 1, Igemm2Tile{bi, best.bj, 4, 2}, st)) return false;
+    *err = hipGetLastError();
+    return true;
+}
+
 hipError_t launch_conv_fwd(int dt, const void *x, int64_t xs, const void *w, void *y, int64_t ys,
                            const ConvShape &s, const float *bias, void *ws, hipStream_t st) {
     if (dt == 1 && ws != nullptr && conv_band_fwd_applies(s) && aligned16p(w) && ((uintptr_t)y & 7) == 0 &&

@@ -69,6 +69,18 @@ struct IgArgs {
     const void *relu_y;
     float *db_part;
     int db_rows;
+    // pipelined FWD, row bands (band_rows > 0): J tile tj covers output rows r0 .. r0 + band_rows - 1
+    // (clipped to OH, r0 = (tj % bands_per_img) * band_step) of image tj / bands_per_img, all columns;
+    // consecutive bands may share rows (each computes and stores them, the same values)
+    int band_rows, band_step, bands_per_img;
+    // with row bands, a VALID max-pool of the band's ReLU output (pool_y set): pool rows
+    // q0 .. q0 + pool_rows - 1 of the band (q0 = band * pool_rows) are written to pool_y (pixel
+    // stride pool_ys, same element type) with the selected window tap kh * pkw + kw in pool_taps
+    // (dense uint8 [N][pOH][pOW][K]); the first maximum in (kh, kw) order wins
+    void *pool_y;
+    unsigned char *pool_taps;
+    int pkh, pkw, psh, psw, pOH, pOW, pool_rows;
+    int64_t pool_ys;
 };
 
 template <typename T> struct Mfma;

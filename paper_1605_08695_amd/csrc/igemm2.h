@@ -174,8 +174,7 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    // (the launcher may keep the hardware order: for bwd-filter splits of the AlexNet layers
-    // spreading one split's tiles over all XCDs measured faster than concentrating them)
+    // (the launcher may keep the hardware order)
     const int lin_hw = (int)(blockIdx.x + gridDim.x * blockIdx.z);
     const int lin = a.xcd_order ? xcd_order(lin_hw, (int)(gridDim.x * gridDim.z)) : lin_hw;
     const int bx = lin % (int)gridDim.x;
@@ -183,13 +182,20 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     const int ti = bx % a.tiles_i;
     const int tj = bx / a.tiles_i;
     const int i0 = ti * BI;
-    const int j0 = tj * BJ;
+    // forward row bands: the J tile is rows band_r0 .. of image band_n, indexed locally from 0
+    const bool banded = DIR == DIR_FWD && a.band_rows > 0;
+    int band_n = 0, band_r0 = 0;
+    if (banded) {
+        band_n = tj / a.bands_per_img;
+        band_r0 = (tj - band_n * a.bands_per_img) * a.band_step;
+    }
+    const int j0 = banded ? 0 : tj * BJ;
 
     // ------------------------------------------------------------ direction set-up
     int MJ_ext, k_beg = 0, k_end;
     int rh = 0, rw = 0, h0 = 0, w0 = 0, Hp = 1, Wp = 1, offh = 0, offw = 0, KHp = 1, KWp = 1;
     if constexpr (DIR == DIR_FWD) {
-        MJ_ext = a.N * a.OH * a.OW;
+        MJ_ext = banded ? min(a.band_rows, a.OH - band_r0) * a.OW : a.N * a.OH * a.OW;
         k_end = a.KH * a.KW * a.C;
         KHp = a.KH;
         KWp = a.KW;
@@ -303,7 +309,12 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
             if constexpr (DIR == DIR_FWD) {
                 uint32_t t, owu, n, ohu;
                 a.dOW.divmod((uint32_t)mm, t, owu);
-                a.dOH.divmod(t, n, ohu);
+                if (banded) {
+                    n = (uint32_t)band_n;
+                    ohu = (uint32_t)band_r0 + t;
+                } else {
+                    a.dOH.divmod(t, n, ohu);
+                }
                 const int ow = (int)owu, oh = (int)ohu;
                 y0 = oh * a.sh - a.pt;     // tap kh reads row y0 + kh
                 x0 = ow * a.sw - a.pl;
@@ -542,6 +553,13 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     // of the stored dpre over this wave's rows, in y order, then over the 16 lanes of a column
     // group by a fixed xor tree)
     const bool relu = DIR == DIR_BWD_DATA && a.relu_y != nullptr;
+    // forward with a fused max-pool: the band's bf16 outputs are staged in LDS (channels of the
+    // first half of the tile in lds0, of the second in lds1, [row][channel]) once every wave has
+    // finished reading the operand stages
+    constexpr bool kPoolFits = DIR == DIR_FWD && BJ * BI <= 128 * (BI + BJ) && BI % 4 == 0;
+    const bool pooled = kPoolFits && banded && a.pool_y != nullptr;
+    constexpr int HC = BI / 2;                        // channels per staging half
+    if (pooled) __syncthreads();
     float cs[MI][4];
 #pragma unroll
     for (int x = 0; x < MI; ++x)
@@ -553,7 +571,13 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
         if (j >= MJ_ext) continue;
         int64_t rowoff;
         if constexpr (DIR == DIR_FWD) {
-            rowoff = (int64_t)j * a.ys;
+            if (banded) {
+                uint32_t dr, ow;
+                a.dOW.divmod((uint32_t)j, dr, ow);
+                rowoff = (((int64_t)band_n * a.OH + band_r0 + (int)dr) * a.OW + (int)ow) * a.ys;
+            } else {
+                rowoff = (int64_t)j * a.ys;
+            }
         } else if constexpr (DIR == DIR_BWD_DATA) {
             const int tw = j % Wp;
             const int t = j / Wp;
@@ -611,11 +635,59 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
                 pk.x = pack_bf16x2(r4[0], r4[1]);
                 pk.y = pack_bf16x2(r4[2], r4[3]);
                 *reinterpret_cast<uint2 *>(o) = pk;
+                if constexpr (kPoolFits) {
+                    if (pooled) {
+                        const int il = wi * WI + x * 16 + 4 * lg;     // channel within the tile
+                        const int rl = j;                              // band row (local pixel)
+                        unsigned char *stg = il < HC ? lds0 : lds1;
+                        *reinterpret_cast<uint2 *>(stg + ((int64_t)rl * HC + (il % HC)) * 2) = pk;
+                    }
+                }
                 if (relu) {
                     cs[x][0] += bf16_to_f32(pk.x & 0xffffu);
                     cs[x][1] += bf16_to_f32(pk.x >> 16);
                     cs[x][2] += bf16_to_f32(pk.y & 0xffffu);
                     cs[x][3] += bf16_to_f32(pk.y >> 16);
+                }
+            }
+        }
+    }
+    if constexpr (kPoolFits) {
+        if (pooled) {
+            // pool rows q0 .. q0 + nq - 1 of this band; each thread takes one channel pair of the
+            // tile and every G-th pool position; taps are scanned kh outer, kw inner, and a later
+            // tap replaces the running maximum only when strictly greater
+            __syncthreads();
+            constexpr int CP = BI / 2, G = (NW * 64) / CP > 0 ? (NW * 64) / CP : 1;
+            const int band = tj - band_n * a.bands_per_img;
+            const int q0 = band * a.pool_rows;
+            const int nq = min(a.pool_rows, a.pOH - q0);
+            const int cp = tid % CP, g = tid / CP;
+            const int c = 2 * cp;
+            if (g < G && i0 + c < a.NI && nq > 0) {
+                const unsigned char *stg = c < HC ? lds0 : lds1;
+                const int cl = c % HC;
+                bf16_t *py = reinterpret_cast<bf16_t *>(a.pool_y);
+                for (int p = g; p < nq * a.pOW; p += G) {
+                    const int qq = p / a.pOW, pw = p - qq * a.pOW;
+                    const int q = q0 + qq;
+                    float b0 = 0.f, b1 = 0.f;
+                    int t0 = 0, t1 = 0;
+                    for (int kh = 0; kh < a.pkh; ++kh) {
+                        const int rl = (q * a.psh + kh - band_r0) * a.OW + pw * a.psw;
+                        for (int kw = 0; kw < a.pkw; ++kw) {
+                            const uint32_t v = *reinterpret_cast<const uint32_t *>(
+                                stg + ((int64_t)(rl + kw) * HC + cl) * 2);
+                            const float v0 = bf16_to_f32(v & 0xffffu), v1 = bf16_to_f32(v >> 16);
+                            const int t = kh * a.pkw + kw;
+                            if (t == 0 || v0 > b0) { b0 = v0; t0 = t; }
+                            if (t == 0 || v1 > b1) { b1 = v1; t1 = t; }
+                        }
+                    }
+                    const int64_t opix = ((int64_t)band_n * a.pOH + q) * a.pOW + pw;
+                    *reinterpret_cast<uint32_t *>(py + opix * a.pool_ys + i0 + c) = pack_bf16x2(b0, b1);
+                    *reinterpret_cast<uint16_t *>(a.pool_taps + opix * a.NI + i0 + c) =
+                        (uint16_t)(t0 | (t1 << 8));
                 }
             }
         }

@@ -80,6 +80,16 @@ static bool igemm2_launch(IgArgs &a, int mj, int zdim, const Igemm2Tile &t, hipS
         if constexpr (DIR == DIR_BWD_FILTER) return false;
         else { igemm2_go<DIR, 128, 96, 4, 2>(a, grid, st); return true; }
     }
+    if (t.bj == 192 && t.nw == 4 && t.ns == 2) {
+        // (192-row J tiles: the forward row bands of a fused max-pool)
+        if constexpr (DIR != DIR_FWD) return false;
+        else {
+            if (t.bi == 64) { igemm2_go<DIR, 64, 192, 4, 2>(a, grid, st); return true; }
+            if (t.bi == 128) { igemm2_go<DIR, 128, 192, 4, 2>(a, grid, st); return true; }
+            if (t.bi == 192) { igemm2_go<DIR, 192, 192, 4, 2>(a, grid, st); return true; }
+            return false;
+        }
+    }
     if (t.bi == 192 && t.bj == 128 && t.nw == 4 && t.ns == 2) {
         // (the filter-gradient direction does not fit these tiles in its registers)
         if constexpr (DIR == DIR_BWD_FILTER) return false;
@@ -148,6 +158,11 @@ static inline void fill_geom(IgArgs &a, const ConvShape &s) {
     a.relu_y = nullptr;
     a.db_part = nullptr;
     a.db_rows = 0;
+    a.band_rows = a.band_step = a.bands_per_img = 0;
+    a.pool_y = nullptr;
+    a.pool_taps = nullptr;
+    a.pkh = a.pkw = a.psh = a.psw = a.pOH = a.pOW = a.pool_rows = 0;
+    a.pool_ys = 0;
 }
 
 }  // namespace tfk

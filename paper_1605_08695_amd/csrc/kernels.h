@@ -42,6 +42,13 @@ struct SgdBatch {
 // bias (may be null): fused y = max(conv + bias, +0).
 hipError_t launch_conv_fwd(int dt, const void *x, int64_t xs, const void *w, void *y, int64_t ys,
                            const ConvShape &s, const float *bias, void *ws, hipStream_t st);
+// The forward convolution with bias + ReLU and a VALID max-pool of its output (g: the pool over
+// y) fused in one kernel, when its row bands cover whole pool windows (bf16, the implicit-GEMM
+// path): writes y, the pooled py (pixel stride pys) and the uint8 window taps.  Returns false,
+// launching nothing, when the fused kernel does not apply.
+bool conv_fwd_pool_fused(const void *x, int64_t xs, const void *w, void *y, int64_t ys, const ConvShape &s,
+                         const float *bias, const PoolGeom &g, void *py, int64_t pys, uint8_t *taps,
+                         hipStream_t st, hipError_t *err);
 hipError_t launch_conv_bwd_data(int dt, const void *dy, int64_t dys, const void *w, void *dx, int64_t dxs,
                                 float beta, const ConvShape &s, float *ws, hipStream_t st);
 // Workspace of the split-K forward / input gradient (0: no split for this shape).

@@ -128,6 +128,41 @@ def conv2d_fwd_bias_relu(x, w, bias, stride, pads, y=None, ws=None, stream=None)
     return _conv_fwd(x, w, bias, stride, pads, y, ws, stream)
 
 
+def conv2d_fwd_bias_relu_maxpool(x, w, bias, stride, pads, pool_hw, pool_stride, pool_pads=(0, 0, 0, 0), y=None,
+                                 py=None, taps=None, ws=None, stream=None):
+    """y = max(x (*) w + bias, 0) and its max-pool (py, uint8 window taps) in one call; one kernel
+    where the convolution's row bands hold whole pool windows.  Returns (y, py, taps)."""
+    lib = load()
+    kh, kw, cin, cout = w.shape
+    win = window(kh, kw, stride, pads)
+    need = lib.tfk_conv2d_workspace_bytes(0, nhwc(x), cout, win, _dt(x))
+    if need and (ws is None or ws.numel() < need):
+        ws = _ws(need, x.device, stream)
+    n, h, ww, _ = x.shape
+    oh = out_len(h, kh, win.stride_h, pads[0], pads[1])
+    ow = out_len(ww, kw, win.stride_w, pads[2], pads[3])
+    if y is None:
+        y = _empty(stream, (n, oh, ow, cout), dtype=x.dtype, device=x.device)
+    pkh, pkw = pool_hw
+    pwin = window(pkh, pkw, pool_stride, pool_pads)
+    poh = out_len(oh, pkh, pwin.stride_h, pool_pads[0], pool_pads[1])
+    pow_ = out_len(ow, pkw, pwin.stride_w, pool_pads[2], pool_pads[3])
+    if py is None:
+        py = _empty(stream, (n, poh, pow_, cout), dtype=x.dtype, device=x.device)
+    if taps is None:
+        taps = _empty(stream, (n, poh, pow_, cout), dtype=torch.uint8, device=x.device)
+    if not (w.dtype == y.dtype == py.dtype == x.dtype):
+        raise TypeError("x, w, y and py must share one dtype")
+    if taps.dtype != torch.uint8 or not taps.is_contiguous():
+        raise ValueError("taps must be a dense uint8 tensor")
+    if bias.dtype != torch.float32 or bias.numel() != cout or not bias.is_contiguous():
+        raise ValueError("bias must be a contiguous float32 vector of cout values")
+    check(lib.tfk_conv2d_fwd_bias_relu_maxpool(_ptr(x), nhwc(x), _ptr(w), cout, _ptr(bias), win, _dt(x), _ptr(y),
+                                               nhwc(y), pwin, _ptr(py), nhwc(py), _ptr(taps),
+                                               _ptr(ws) if need else None, need, _stream(stream)))
+    return y, py, taps
+
+
 def conv2d_bwd_input(dy, w, dx, stride, pads, beta=0.0, ws=None, stream=None):
     """dx (= or +=) conv2d_fwd^T(dy).  dx gives the forward input's shape (it is written)."""
     lib = load()

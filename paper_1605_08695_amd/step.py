@@ -158,6 +158,16 @@ class Replica:
                     self.bwi_relu[op.name] = w[0]
         self.relu_fused = ({c.name for c in self.pool_relu.values()} |
                            {c.name for c in self.bwi_relu.values()})
+        # ---- a convolution whose whole ReLU output is pooled by the next op: one forward call
+        # (one kernel where its row bands hold whole pool windows)
+        self.conv_pool = {}                      # conv name -> pool op
+        for k, op in enumerate(net.ops[:-1]):
+            nxt = net.ops[k + 1]
+            if (isinstance(op, Conv) and op.relu and isinstance(nxt, Pool) and nxt.src == op.dst
+                    and op.dst_c0 == 0 and op.cout == net.tensors[op.dst][3] and writers[op.dst] == [op]
+                    and self.argmax[nxt.name].dtype == torch.uint8):
+                self.conv_pool[op.name] = nxt
+        self.pool_in_conv = {p.name for p in self.conv_pool.values()}
         # ---- one workspace big enough for every op
         need = 0
         for c in net.convs:
@@ -192,6 +202,17 @@ class Replica:
                 if trace: trace("conv_fwd", op, stream=stream, x=x, w=self.Wlp[op.name], y=y)
                 ops.conv2d_fwd(x, self.Wlp[op.name], (op.sh, op.sw), op.pads, y=y, ws=self.ws, stream=stream)
                 if trace: trace("conv_fwd:end", op, stream=stream, y=y)
+            elif isinstance(op, Conv) and op.name in self.conv_pool:
+                pool = self.conv_pool[op.name]
+                py, am = self._slice(self.act, pool), self.argmax[pool.name]
+                if trace: trace("conv_bias_relu_maxpool_fwd", op, stream=stream, x=x, w=self.Wlp[op.name],
+                                b=self.b[op.name], y=y, py=py, argmax=am)
+                ops.conv2d_fwd_bias_relu_maxpool(x, self.Wlp[op.name], self.b[op.name], (op.sh, op.sw), op.pads,
+                                                 (pool.kh, pool.kw), (pool.sh, pool.sw), pool.pads, y=y, py=py,
+                                                 taps=am, ws=self.ws, stream=stream)
+                if trace: trace("conv_bias_relu_maxpool_fwd:end", op, stream=stream, y=y, py=py, argmax=am)
+            elif isinstance(op, Pool) and op.name in self.pool_in_conv:
+                continue                         # produced with its convolution
             elif isinstance(op, Conv):
                 if trace: trace("conv_bias_relu_fwd", op, stream=stream, x=x, w=self.Wlp[op.name],
                                 b=self.b[op.name], y=y)

@@ -294,6 +294,47 @@ class ParityTracer:
         self.record("conv_bias_relu_fwd", op.name, "negatives", float(np.sum(np.signbit(y))), 0.0)
         self._set(out["y"], ref)
 
+    def _force_conv_bias_relu_maxpool_fwd(self, op, t):
+        return {"x": self._force(t["x"]), "w": self._force(t["w"]), "b": self._force(t["b"])}
+
+    def _check_conv_bias_relu_maxpool_fwd(self, op, u, out):
+        pool = self.rep.conv_pool[op.name]
+        ref = oracle.bias_relu_fwd(oracle.conv2d_fwd(u["x"], u["w"], (op.sh, op.sw), op.pads), u["b"])
+        y = self._got("conv_bias_relu_maxpool_fwd", op.name, out["y"])
+        self.record_tensor("conv_bias_relu_maxpool_fwd", op.name, y, ref, self.dtype)
+        self.record("conv_bias_relu_maxpool_fwd", op.name, "negatives", float(np.sum(np.signbit(y))), 0.0)
+        self._set(out["y"], ref)
+        yr = self._round(ref, self.dtype).to(torch.float64).numpy()
+        pref, am = oracle.maxpool_fwd(yr, (pool.kh, pool.kw), (pool.sh, pool.sw), pool.pads)
+        py = self._got("conv_bias_relu_maxpool_fwd:py", pool.name, out["py"])
+        got_am = self._dense(out["argmax"][:self.k], yr.shape, pool)
+        if out["argmax"].dtype == torch.uint8:
+            self._got("conv_bias_relu_maxpool_fwd:argmax", pool.name, out["argmax"])
+        self._check_fused_pool(pool, yr, pref, am, py, got_am)
+        self._set(out["py"], pref)
+        self.state[("argmax", pool.name)] = am
+
+    def _check_fused_pool(self, pool, yr, pref, am, py, got_am):
+        """A max-pool fused after its convolution pools the convolution's own output, which is not
+        forced to the oracle's: values are held to the bf16 gate, and the selected tap must be the
+        oracle's wherever the window's two largest oracle values differ by more than the two can
+        move under that gate (2 x (2^-7 |v| + 1e-3 RMS)); near-ties are counted, not gated."""
+        kh, kw, sh, sw = pool.kh, pool.kw, pool.sh, pool.sw
+        n, oh, ow, c = pref.shape
+        pt, pb, pl, pr = pool.pads
+        yp = np.pad(yr, ((0, 0), (pt, pb), (pl, pr), (0, 0)), constant_values=-np.inf) if any(pool.pads) else yr
+        wins = np.stack([yp[:, i:i + sh * (oh - 1) + 1:sh, j:j + sw * (ow - 1) + 1:sw, :]
+                         for i in range(kh) for j in range(kw)])
+        wins.sort(axis=0)
+        top1, top2 = wins[-1], wins[-2] if wins.shape[0] > 1 else wins[-1] - np.inf
+        rms = float(np.sqrt(np.mean(yr * yr))) if yr.size else 0.0
+        tie = (top1 - top2) <= 2 * (2.0 ** -7 * np.abs(top1) + 1e-3 * rms)
+        mism = got_am != am
+        self.record_tensor("fused_maxpool_fwd", pool.name, py, pref, self.dtype)
+        self.record("fused_maxpool_fwd", pool.name, "argmax_mismatch", float(np.sum(mism & ~tie)), 0.0)
+        self.results.append(("fused_maxpool_fwd", pool.name, "near_tie_mismatch(info)", float(np.sum(mism & tie)),
+                             float("inf"), True))
+
     def _force_maxpool_fwd(self, op, t):
         return {"x": self._force(t["x"]), "x_shape": tuple(t["x"].shape)}
 
@@ -508,6 +549,24 @@ class SampledParityTracer(ParityTracer):
         self.record_tensor("conv_bias_relu_fwd", op.name, y, ref, self.dtype)
         self.record("conv_bias_relu_fwd", op.name, "negatives", float(np.sum(np.signbit(y))), 0.0)
         self._set_fill(out["y"], ref, relu=True)
+
+    def _check_conv_bias_relu_maxpool_fwd(self, op, u, out):
+        s = self.sample
+        pool = self.rep.conv_pool[op.name]
+        ref = oracle.bias_relu_fwd(oracle.conv2d_fwd(u["x"][s], u["w"], (op.sh, op.sw), op.pads), u["b"])
+        y = self._gs(out["y"])
+        self.record_tensor("conv_bias_relu_maxpool_fwd", op.name, y, ref, self.dtype)
+        self.record("conv_bias_relu_maxpool_fwd", op.name, "negatives", float(np.sum(np.signbit(y))), 0.0)
+        yr = self._round(ref, self.dtype).to(torch.float64).numpy()
+        pref, am = oracle.maxpool_fwd(yr, (pool.kh, pool.kw), (pool.sh, pool.sw), pool.pads)
+        got_am = self._dense(out["argmax"][s], yr.shape, pool)
+        self._check_fused_pool(pool, yr, pref, am, self._gs(out["py"]), got_am)
+        self._set_fill(out["y"], ref, relu=True)
+        # the whole batch's pool state: the oracle's pool of the (filled) state, as stored
+        full = self._round(self.state[self._lookup(out["y"])[0]], self.dtype).to(torch.float64).numpy()
+        pfull, amfull = oracle.maxpool_fwd(full, (pool.kh, pool.kw), (pool.sh, pool.sw), pool.pads)
+        self._set(out["py"], pfull)
+        self.state[("argmax", pool.name)] = amfull
 
     def _check_conv_fwd(self, op, u, out):
         s = self.sample

@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 10
+    assert lib.tfk_abi_version() == 11
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -99,6 +99,23 @@ def test_conv_bwd_validation(lib):
     st = lib.tfk_conv2d_bwd_filter(vp(P), xd, vp(P + 0x40000000), Nhwc(64, 56, 56, 64, 0), W, BF16,
                                    vp(0), vp(P + 0xC0000000), need, None)
     assert st == NULL
+
+
+def test_conv_bias_relu_maxpool_validation(lib):
+    """The convolution fused with the max-pool of its output: bias is required, the pool must fit
+    y, py and taps must overlap nothing, before any launch."""
+    W = Window(3, 3, 1, 1, 1, 1, 1, 1)
+    PW = Window(3, 3, 2, 2, 0, 0, 0, 0)
+
+    def call(bias=P + 0x300000, py=P + 0x400000, taps=P + 0x500000, pyd=(2, 6, 6, 64, 0), pw=PW):
+        return lib.tfk_conv2d_fwd_bias_relu_maxpool(vp(P), Nhwc(2, 13, 13, 32, 0), vp(P + 0x100000), 64, vp(bias), W,
+                                                    BF16, vp(P + 0x200000), Nhwc(2, 13, 13, 64, 0), pw, vp(py),
+                                                    Nhwc(*pyd), vp(taps), None, 0, None)
+    assert call(bias=0) == NULL
+    assert call(pyd=(2, 7, 6, 64, 0)) == SHAPE                          # not the pool's output shape
+    assert call(py=P + 0x200100) == ALIAS                               # py inside y
+    assert call(taps=P + 0x400010) == ALIAS                             # taps inside py
+    assert call(pw=Window(17, 17, 1, 1, 0, 0, 0, 0), pyd=(2, 1, 1, 64, 0)) == SHAPE   # window past y
 
 
 def test_conv_bwd_filter_noalloc_validation(lib):

@@ -605,3 +605,75 @@ def test_bias_only_backward(dtype, shape):
     torch.cuda.synchronize()
     assert torch.equal(dpre, dy0)
     assert_close(f64(db), f64(dy0).sum(axis=(0, 1, 2)), torch.float32, dtype, label="db")
+
+
+# x shape, cout, conv (k, stride, pads), pool (k, stride, pads), dtype, pool output as a channel slice
+CONV_POOL_CASES = [
+    # one kernel: one band per image (13 x 13 of 192 rows), bands sharing a row (3x3/2 windows, four
+    # 7-row bands of 18 columns), non-overlapping 2x2/2 windows in 4-row bands, a last output row no
+    # window reaches (a band that only writes y), several channel tiles, ragged channel tiles
+    ("alexnet_conv5_pool5", (3, 13, 13, 256), 256, (3, 1, (1, 1, 1, 1)), (3, 2, (0, 0, 0, 0)), torch.bfloat16, False),
+    ("bands_sharing_rows", (2, 25, 18, 32), 64, (3, 1, (1, 1, 1, 1)), (3, 2, (0, 0, 0, 0)), torch.bfloat16, False),
+    ("bands_2x2s2", (2, 32, 32, 32), 128, (3, 1, (1, 1, 1, 1)), (2, 2, (0, 0, 0, 0)), torch.bfloat16, False),
+    ("uncovered_last_row", (2, 33, 32, 32), 64, (3, 1, (1, 1, 1, 1)), (2, 2, (0, 0, 0, 0)), torch.bfloat16, False),
+    ("ragged_channels", (2, 13, 13, 64), 72, (3, 1, (1, 1, 1, 1)), (3, 2, (0, 0, 0, 0)), torch.bfloat16, False),
+    ("pool_into_channel_slice", (2, 13, 13, 64), 128, (3, 1, (1, 1, 1, 1)), (3, 2, (0, 0, 0, 0)), torch.bfloat16,
+     True),
+    # two kernels: too many recomputed rows (AlexNet conv2 + pool2), rows too wide for a band, a
+    # padded pool, fp32
+    ("alexnet_conv2_pool2", (3, 27, 27, 64), 192, (5, 1, (2, 2, 2, 2)), (3, 2, (0, 0, 0, 0)), torch.bfloat16, False),
+    ("wide_rows", (2, 10, 100, 32), 64, (3, 1, (1, 1, 1, 1)), (3, 2, (0, 0, 0, 0)), torch.bfloat16, False),
+    ("same_pool", (2, 14, 14, 32), 64, (3, 1, (1, 1, 1, 1)), (3, 2, (0, 1, 0, 1)), torch.bfloat16, False),
+    ("f32", (2, 13, 13, 32), 64, (3, 1, (1, 1, 1, 1)), (3, 2, (0, 0, 0, 0)), torch.float32, False),
+]
+
+
+@pytest.mark.parametrize("ties", [False, True], ids=["random", "ties"])
+@pytest.mark.parametrize("case", CONV_POOL_CASES, ids=[c[0] for c in CONV_POOL_CASES])
+def test_conv_bias_relu_maxpool(case, ties):
+    """The convolution with bias + ReLU and the max-pool of its output in one call: bit for bit the
+    two calls it replaces (tfk_conv2d_fwd_bias_relu, then tfk_maxpool_fwd_taps), and against the
+    oracle (y within the gate; the pool of the oracle's rounded y, taps equal wherever the window's
+    two largest values are not within the gate of each other).  With ties, a third of the channels
+    get a bias that zeroes them after the ReLU (every window a tie)."""
+    name, xs, cout, (k, st, pads), (pk, ps, ppads), dt, sliced = case
+    say("conv + bias + relu + maxpool", name, "ties" if ties else "")
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    x = torch.from_numpy(np.maximum(rng.standard_normal(xs), 0)).to(dt).to(DEV)
+    w = torch.from_numpy(rng.standard_normal((k, k, xs[3], cout)) * np.sqrt(2.0 / (k * k * xs[3]))).to(dt).to(DEV)
+    b = rng.standard_normal(cout) * 0.1
+    if ties:
+        b[::3] = -1e4
+    bias = torch.from_numpy(b.astype(np.float32)).to(DEV)
+    y, py, taps = ops.conv2d_fwd_bias_relu_maxpool(x, w, bias, st, pads, (pk, pk), ps, ppads)
+    if sliced:
+        big = torch.full(py.shape[:3] + (cout + 48,), -7.0, dtype=dt, device=DEV)
+        pys = big[..., 16:16 + cout]
+        ops.conv2d_fwd_bias_relu_maxpool(x, w, bias, st, pads, (pk, pk), ps, ppads, py=pys, taps=taps)
+        torch.cuda.synchronize()
+        assert torch.equal(pys, py) and bool((big[..., :16] == -7).all()) and bool((big[..., 16 + cout:] == -7).all())
+    y2 = ops.conv2d_fwd_bias_relu(x, w, bias, st, pads)
+    py2, taps2 = ops.maxpool_fwd(y2, (pk, pk), ps, ppads, taps=True)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16) if dt == torch.bfloat16 else y.view(torch.int32),
+                       y2.view(torch.int16) if dt == torch.bfloat16 else y2.view(torch.int32))
+    assert torch.equal(py, py2) and torch.equal(taps, taps2)
+    ref = oracle.bias_relu_fwd(oracle.conv2d_fwd(f64(x), f64(w), st, pads), b.astype(np.float32).astype(np.float64))
+    assert_close(f64(y), ref, dt, label=name + " y")
+    yr = torch.from_numpy(ref).to(dt).to(torch.float64).numpy()
+    pref, am = oracle.maxpool_fwd(yr, (pk, pk), ps, ppads)
+    assert_close(f64(py), pref, dt, label=name + " pool")
+    n, oh, ow, c = pref.shape
+    t = taps.cpu().numpy().astype(np.int64)
+    nn, qq, ww, cc = np.indices(t.shape)
+    h = qq * ps - ppads[0] + t // pk
+    wv = ww * ps - ppads[2] + t % pk
+    dense = ((nn * yr.shape[1] + h) * yr.shape[2] + wv) * c + cc
+    yp = np.pad(yr, ((0, 0), (ppads[0], ppads[1]), (ppads[2], ppads[3]), (0, 0)), constant_values=-np.inf)
+    wins = np.sort(np.stack([yp[:, i:i + ps * (oh - 1) + 1:ps, j:j + ps * (ow - 1) + 1:ps, :]
+                             for i in range(pk) for j in range(pk)]), axis=0)
+    rms = float(np.sqrt(np.mean(yr * yr)))
+    tie = (wins[-1] - wins[-2]) <= 2 * (2.0 ** -7 * np.abs(wins[-1]) + 1e-3 * rms)
+    bad = (dense != am) & ~tie
+    say("  taps: %d differ from the oracle, all at near-ties" % int(np.sum(dense != am)))
+    assert not bad.any()
