@@ -47,6 +47,7 @@ struct BandArgs {
     int N, H, W, C, OH, OW, K, KH, KW, sh, sw, pt, pl;
     int R;                  // output rows per band
     int bands_per_img, bands;
+    int run;                // bands per workgroup: workgroup g takes bands g * run .. g * run + run - 1
     int rows_in;            // staged input rows per band: (R - 1) * sh + KH
     int wst;                // staged pixels per row (even)
     int kwp;                // taps per filter row in the reduction order (forward: KW rounded to 2; bwd-filter: to 4)
@@ -153,8 +154,9 @@ __global__ __launch_bounds__(256, 1) void band_fwd_kernel(const BandArgs a) {
               filt + 1024 * i);
     }
 
-    int b = blockIdx.x;
-    if (b < a.bands) band_dma<X16>(a, b, xb0);
+    int b = blockIdx.x * a.run;
+    const int b_end = min(a.bands, b + a.run);
+    if (b < b_end) band_dma<X16>(a, b, xb0);
     wait_barrier<0>();
 
     // bias of the lane's output channels co0 + 16 x + 4 lg + e, read once (K % 16 == 0: a channel
@@ -183,12 +185,12 @@ __global__ __launch_bounds__(256, 1) void band_fwd_kernel(const BandArgs a) {
 
     const int groups = (a.R * a.OW + 15) >> 4;
     const int passes = (groups + 15) >> 4;
-    for (int it = 0; b < a.bands; b += gridDim.x, ++it) {
+    for (int it = 0; b < b_end; ++b, ++it) {
         const unsigned char *cur = (it & 1) ? xb1 : xb0;
         unsigned char *nxt = (it & 1) ? xb0 : xb1;
-        const int bn = b + (int)gridDim.x;
-        const BandCopier<X16> bc(a, bn < a.bands ? bn : b);
-        const int ncw = bn < a.bands ? bc.count(wave) : 0;     // this wave's copies of the next band
+        const int bn = b + 1;
+        const BandCopier<X16> bc(a, bn < b_end ? bn : b);
+        const int ncw = bn < b_end ? bc.count(wave) : 0;     // this wave's copies of the next band
 
         const int n = b / a.bands_per_img;
         const int oh0 = (b - n * a.bands_per_img) * a.R;
@@ -298,29 +300,202 @@ __global__ __launch_bounds__(256, 1) void band_fwd_kernel(const BandArgs a) {
 }
 
 // ---------------------------------------------------------------------------------- forward, filter in registers
-// For filters of exactly KS reduction steps and bands of at most 32 MJ pixels.  The filter is
-// staged once through LDS (over the band buffers) and then held in registers: wave w takes the
-// band's pixel groups (w & 1) + 2 y (y < MJ) and the channel groups 2 (w >> 1) + {0, 1}, so per
-// step it reads only MJ pixel fragments from LDS for 2 MJ MFMAs (half the LDS traffic per MFMA of
-// band_fwd_kernel, which re-reads the filter every step).  Copies of the next band and the stores
-// of the previous band are issued one per step under the MFMAs, as in band_fwd_kernel.
-template <int KS, int MJ, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void band_fwd_reg_kernel(const BandArgs a) {
-    static_assert(NW == 4 || NW == 8, "waves");
-    constexpr int PS = NW / 2;                  // pixel parts: wave w takes part w % PS, channel half w / PS
-    static_assert(KS % 2 == 0 && KS * 32 * 128 <= 2 * kXBand, "filter staging");
-    __shared__ __attribute__((aligned(1024))) unsigned char xb0[kXBand];
-    __shared__ __attribute__((aligned(1024))) unsigned char xb1[kXBand];
-    unsigned char *filt = xb0;                  // staging of the filter (spans xb0 and xb1)
+// For filters of exactly KS reduction steps and bands of at most 16 UPW pixels (UPW pixel groups
+// of 16), 16-byte pixel pairs and staged rows of at most 256 pixels.  Each of the 4 waves holds
+// the block's whole 64-channel filter slice in registers (staged once through LDS), so one pixel
+// fragment read from LDS feeds up to four MFMAs (one per 16-channel group).  The band's units
+// (pixel group g, channel group x), numbered 4 g + x, are dealt to the waves in equal contiguous
+// runs of UPW: the run of wave w starts S0 = UPW w mod 4 channel groups into its first pixel
+// group, so every wave issues UPW MFMAs per step and reads at most four fragments.  Staged rows
+// have a fixed pitch of 256 pixels (2 KiB), so a band copy is one half of one row and its address
+// is one scalar row offset away from a per-lane base.  Copies of the next band and the stores of
+// the previous band are issued one per step under the MFMAs (the stores a band later, so the
+// barrier that ends a band does not wait for them to drain).
+constexpr int kRegRowBytes = 2048;                 // staged row pitch: 256 pixels of 8 bytes
+constexpr int kRegMaxRows = 23;                    // staged rows per band
+constexpr int kRegBand = kRegMaxRows * kRegRowBytes;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int lg = lane >> 4, ld = lane & 15;
-    const int ph = wave % PS, chh = wave / PS;
+template <int KS, int UPW, int S0>
+__device__ __forceinline__ void band_fwd_reg_body(const BandArgs &a, unsigned char *xb0, unsigned char *xb1,
+                                                  const float *sbias, int wave) {
+    constexpr int NF = (S0 + UPW + 3) / 4;          // pixel fragments per step
+    constexpr int LAST = S0 + UPW - 4 * (NF - 1);    // channel groups of the last fragment
+    static_assert(NF <= 4 && LAST >= 1, "units per wave");
+    const int lane = threadIdx.x & 63, lg = lane >> 4, ld = lane & 15;
     const int co0 = blockIdx.y * 64;
     const int ntaps = a.KH * a.kwp;
+    const int g0 = (UPW * wave) >> 2;               // first pixel group of this wave
 
-    // Filter rows m = (kh * kwp + kw) * 4 + c, k-major with the transposing-read swizzle.
-    for (int i = wave; i < KS * 4; i += NW) {
+    // filter fragments of every step and channel group (the filter is staged over xb0/xb1)
+    U4 fw[KS][4];
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+        const int k = 32 * kk + 8 * lg + (ld >> 2);
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            const int row = 16 * x + 4 * (ld & 3);
+            fw[kk][x] = lds_tr_pair(xb0 + kmajor_off<64>(k, row), xb0 + kmajor_off<64>(k + 4, row));
+        }
+    }
+    wait_barrier<0>();                              // every wave holds its filter: the staging area is free
+
+    // Band copies: wave w copies half (w & 1) of staged rows (w >> 1) + 2 c, c = 0, 1, ...  Its lane
+    // holds pixel pair 64 (w & 1) + lane of a row: image column iw = 2 pc - pl (pairs never
+    // straddle the image edge), zero outside the image.
+    const int pc = 64 * (wave & 1) + lane;
+    const int iw = 2 * pc - a.pl;
+    const bool lane_ok = 2 * pc < a.wst && (unsigned)iw < (unsigned)a.W;
+    const int wrow = wave >> 1;
+    const int64_t row_elems = (int64_t)a.W * 4;
+    const bf16_t *const lane_src = a.x + (int64_t)iw * 4;
+    // first image row of this wave's copies of band bb (ih0) and that row's element offset (base)
+    auto band_rows0 = [&](int bb, int &ih0, int64_t &base) __attribute__((always_inline)) {
+        const int n = bb / a.bands_per_img;
+        ih0 = (bb - n * a.bands_per_img) * a.R * a.sh - a.pt + wrow;
+        base = ((int64_t)n * a.H + ih0) * row_elems;
+    };
+    auto band_copy = [&](int ih0, int64_t base, int c, unsigned char *buf) __attribute__((always_inline)) {
+        const bool ok = lane_ok && (unsigned)(ih0 + 2 * c) < (unsigned)a.H;
+        const bf16_t *src = lane_src + base + 2 * c * row_elems;
+        dma16(ok ? (const void *)src : (const void *)g_zero_chunk,
+              buf + (wrow + 2 * c) * kRegRowBytes + 1024 * (wave & 1));
+    };
+    const int ncw = (a.rows_in - wrow + 1) >> 1;    // this wave's copies of a band
+
+    int b = blockIdx.x * a.run;
+    const int b_end = min(a.bands, b + a.run);
+    if (b < b_end) {
+        int ih0;
+        int64_t base;
+        band_rows0(b, ih0, base);
+        for (int c = 0; c < ncw; ++c) band_copy(ih0, base, c, xb0);
+    }
+    wait_barrier<0>();
+
+    // biases of the lane's channels co0 + 16 x + 4 lg .. + 3 (zero without a bias); with a bias the
+    // outputs are bias + ReLU, rounded once
+    f32x4_t bvec[4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+        const float4 bq = *reinterpret_cast<const float4 *>(sbias + 16 * x + 4 * lg);
+        bvec[x] = f32x4_t{bq.x, bq.y, bq.z, bq.w};
+    }
+    const bool relu = a.bias != nullptr;
+    // unit u of this wave (u < UPW): fragment slot (S0 + u) / 4, channel group (S0 + u) % 4
+    uint2 held[NF][4];
+    int hoff[NF];
+#pragma unroll
+    for (int j = 0; j < NF; ++j) hoff[j] = -1;
+    bf16_t *const out = reinterpret_cast<bf16_t *>(a.out);
+    auto store_one = [&](int u) __attribute__((always_inline)) {
+        const int j = (S0 + u) >> 2, x = (S0 + u) & 3;
+        const int co = co0 + 16 * x + 4 * lg;
+        if (hoff[j] >= 0 && co < a.K) *reinterpret_cast<uint2 *>(out + hoff[j] + co) = held[j][x];
+    };
+
+    for (int it = 0; b < b_end; ++b, ++it) {
+        const unsigned char *cur = (it & 1) ? xb1 : xb0;
+        unsigned char *nxt = (it & 1) ? xb0 : xb1;
+        const int bn = b + 1;
+        const int nc = bn < b_end ? ncw : 0;        // this wave's copies of the next band
+        int nih0 = 0;
+        int64_t nbase = 0;
+        if (bn < b_end) band_rows0(bn, nih0, nbase);
+
+        const int n = b / a.bands_per_img;
+        const int oh0 = (b - n * a.bands_per_img) * a.R;
+        const int pb = min(a.R, a.OH - oh0) * a.OW;             // valid pixels of this band
+        int boff[NF];                                           // pixel-pair index of the window origin
+        int coff[NF];                                           // output offset (elements; fits int32)
+#pragma unroll
+        for (int j = 0; j < NF; ++j) {
+            const int q = (g0 + j) * 16 + ld;
+            uint32_t r, ow;
+            a.dOW.divmod((uint32_t)(q < pb ? q : 0), r, ow);
+            boff[j] = (int)r * a.sh * (kRegRowBytes / 16) + (((int)ow * a.sw) >> 1);
+            coff[j] = q < pb ? ((n * a.OH + oh0 + (int)r) * a.OW + (int)ow) * (int)a.ys : -1;
+        }
+        // Each accumulator starts at its channels' biases (zero without a bias): the first step's
+        // MFMAs take them as the C operand, so no zeroing and no bias add is needed per band.
+        f32x4_t acc[NF][4];
+
+        // Tap pair (kh, kw) = (t / kwp, t % kwp) of t = 8 kk + 2 lg, advanced by 8 taps per step
+        // (kw even: a pair starts at an even pixel).
+        int tkh = (2 * lg) / a.kwp, tkw = (2 * lg) % a.kwp;
+        auto next_tap = [&](int kk) __attribute__((always_inline)) -> int {
+            const int to = 8 * kk + 2 * lg < ntaps ? tkh * (kRegRowBytes / 16) + (tkw >> 1) : 0;   // pairs
+            tkw += 8;
+            if (tkw >= a.kwp) {                     // kwp >= 8: at most one wrap per step
+                tkw -= a.kwp;
+                ++tkh;
+            }
+            return to;
+        };
+        // One fragment per slot: slot j's fragment of step kk + 1 is read right after its MFMAs of
+        // step kk, so it has the other slots' MFMAs to arrive.
+        U4 fj[NF];
+        {
+            const int to = next_tap(0);
+#pragma unroll
+            for (int j = 0; j < NF; ++j) fj[j] = *reinterpret_cast<const U4 *>(cur + ((boff[j] + to) << 4));
+        }
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+            const int to = kk + 1 < KS ? next_tap(kk + 1) : 0;
+            if (kk < nc) band_copy(nih0, nbase, kk, nxt);
+            if (kk < UPW) store_one(kk);
+#pragma unroll
+            for (int j = 0; j < NF; ++j) {
+#pragma unroll
+                for (int x = 0; x < 4; ++x)
+                    if ((j > 0 || x >= S0) && (j < NF - 1 || x < LAST)) {
+                        if (kk == 0) acc[j][x] = bvec[x];
+                        Mfma<bf16_t>::run(acc[j][x], fw[kk][x], fj[j]);
+                    }
+                if (kk + 1 < KS) fj[j] = *reinterpret_cast<const U4 *>(cur + ((boff[j] + to) << 4));
+            }
+        }
+        for (int c = KS; c < nc; ++c) band_copy(nih0, nbase, c, nxt);
+#pragma unroll
+        for (int u = KS; u < UPW; ++u) store_one(u);
+
+        // bias + ReLU, rounded once (lane: channels co .. co + 3 of pixel 16 g + ld)
+#pragma unroll
+        for (int j = 0; j < NF; ++j) {
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                if (!((j > 0 || x >= S0) && (j < NF - 1 || x < LAST))) continue;
+                float v4[4] = {acc[j][x][0], acc[j][x][1], acc[j][x][2], acc[j][x][3]};
+                if (relu) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v4[e] = v4[e] > 0.f ? v4[e] : 0.f;
+                }
+                held[j][x].x = pack_bf16x2(v4[0], v4[1]);
+                held[j][x].y = pack_bf16x2(v4[2], v4[3]);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < NF; ++j) hoff[j] = coff[j];
+        wait_barrier<0>();
+    }
+#pragma unroll
+    for (int u = 0; u < UPW; ++u) store_one(u);
+}
+
+template <int KS, int UPW>
+__global__ __launch_bounds__(256, 1) void band_fwd_reg_kernel(const BandArgs a) {
+    static_assert(KS * 32 * 128 <= 2 * kRegBand, "filter staging");
+    __shared__ __attribute__((aligned(1024))) unsigned char xb[2 * kRegBand];
+    __shared__ __attribute__((aligned(16))) float sbias[64];    // the block's biases (0 past K)
+    unsigned char *const xb0 = xb, *const xb1 = xb + kRegBand;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int co0 = blockIdx.y * 64;
+    if (tid < 64) sbias[tid] = (a.bias != nullptr && co0 + tid < a.K) ? a.bias[co0 + tid] : 0.f;
+    // Filter rows m = (kh * kwp + kw) * 4 + c (zero past the filter), k-major with the
+    // transposing-read swizzle, staged over both band buffers: copy i covers rows 8 i .. 8 i + 7.
+    for (int i = wave; i < KS * 4; i += 4) {
         const int m = 8 * i + (lane >> 3);
         const int ch = (lane & 7) ^ kmajor_swz<64>(m);
         const int c = m & 3;
@@ -330,135 +505,15 @@ __global__ __launch_bounds__(NW * 64, 1) void band_fwd_reg_kernel(const BandArgs
         const bool ok = (int)kh < a.KH && (int)kw < a.KW && c < a.C && co < a.K;
         dma16(ok ? (const void *)(a.w + (((int64_t)kh * a.KW + kw) * a.C + c) * a.K + co)
                  : (const void *)g_zero_chunk,
-              filt + 1024 * i);
+              xb0 + 1024 * i);
     }
     wait_barrier<0>();
-    U4 fw[KS][2];
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-        const int k = 32 * kk + 8 * lg + (ld >> 2);
-#pragma unroll
-        for (int x = 0; x < 2; ++x) {
-            const int row = 16 * (2 * chh + x) + 4 * (ld & 3);
-            fw[kk][x] = lds_tr_pair(filt + kmajor_off<64>(k, row), filt + kmajor_off<64>(k + 4, row));
-        }
-    }
-    wait_barrier<0>();                          // every wave holds its filter: the staging area is free
-
-    int b = blockIdx.x;
-    if (b < a.bands) band_dma<true, NW>(a, b, xb0);
-    wait_barrier<0>();
-
-    float bv[2][4];
-#pragma unroll
-    for (int x = 0; x < 2; ++x) {
-        const int co = co0 + 16 * (2 * chh + x) + 4 * lg;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) bv[x][e] = (a.bias != nullptr && co < a.K) ? a.bias[co + e] : 0.f;
-    }
-    // Outputs of the previous band, stored one per step during the next band: packed bf16 of
-    // acc[x][y] and the output offset of each of the lane's pixels (-1: no pixel).
-    uint2 held[2][MJ];
-    int hoff[MJ];
-#pragma unroll
-    for (int y = 0; y < MJ; ++y) hoff[y] = -1;
-    bf16_t *const out = reinterpret_cast<bf16_t *>(a.out);
-    auto store_one = [&](int x, int y) __attribute__((always_inline)) {
-        const int co = co0 + 16 * (2 * chh + x) + 4 * lg;
-        if (hoff[y] >= 0 && co < a.K) *reinterpret_cast<uint2 *>(out + hoff[y] + co) = held[x][y];
-    };
-
-    for (int it = 0; b < a.bands; b += gridDim.x, ++it) {
-        const unsigned char *cur = (it & 1) ? xb1 : xb0;
-        unsigned char *nxt = (it & 1) ? xb0 : xb1;
-        const int bn = b + (int)gridDim.x;
-        const BandCopier<true> bc(a, bn < a.bands ? bn : b);
-        const int nc = bn < a.bands ? bc.template count<NW>(wave) : 0;   // this wave's copies of the next band
-
-        const int n = b / a.bands_per_img;
-        const int oh0 = (b - n * a.bands_per_img) * a.R;
-        const int pb = min(a.R, a.OH - oh0) * a.OW;             // valid pixels of this band
-        int boff[MJ];                                           // pixel-pair index of the window origin
-        int coff[MJ];                                           // output offset (elements; fits int32)
-#pragma unroll
-        for (int y = 0; y < MJ; ++y) {
-            const int q = (PS * y + ph) * 16 + ld;
-            uint32_t r, ow;
-            a.dOW.divmod((uint32_t)(q < pb ? q : 0), r, ow);
-            boff[y] = ((int)r * a.sh * a.wst + (int)ow * a.sw) >> 1;
-            coff[y] = q < pb ? ((n * a.OH + oh0 + (int)r) * a.OW + (int)ow) * (int)a.ys : -1;
-        }
-        f32x4_t acc[2][MJ];
-#pragma unroll
-        for (int x = 0; x < 2; ++x)
-#pragma unroll
-            for (int y = 0; y < MJ; ++y) acc[x][y] = fresh_zero4();
-
-        // Tap pair (kh, kw) = (t / kwp, t % kwp) of t = 8 kk + 2 lg, advanced by 8 taps per step.
-        int tkh = (2 * lg) / a.kwp, tkw = (2 * lg) % a.kwp;
-        auto next_tap = [&](int kk) __attribute__((always_inline)) -> int {
-            const int to = 8 * kk + 2 * lg < ntaps ? (tkh * a.wst + tkw) >> 1 : 0;     // in pixel pairs
-            tkw += 8;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                if (tkw >= a.kwp) {
-                    tkw -= a.kwp;
-                    ++tkh;
-                }
-            }
-            return to;
-        };
-        auto side = [&](int kk) __attribute__((always_inline)) {
-            if (kk < nc) bc.copy(a, wave + NW * kk, nxt);
-            if (kk < 2 * MJ) store_one(kk / MJ, kk % MJ);
-        };
-        // One fragment per pixel group: the group's fragment of step kk + 1 is read right after its
-        // MFMAs of step kk, so it has the other groups' MFMAs to arrive.
-        U4 fj[MJ];
-        {
-            const int to = next_tap(0);
-#pragma unroll
-            for (int y = 0; y < MJ; ++y) fj[y] = *reinterpret_cast<const U4 *>(cur + ((boff[y] + to) << 4));
-        }
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk) {
-            const int to = kk + 1 < KS ? next_tap(kk + 1) : 0;
-            side(kk);
-#pragma unroll
-            for (int y = 0; y < MJ; ++y) {
-#pragma unroll
-                for (int x = 0; x < 2; ++x) Mfma<bf16_t>::run(acc[x][y], fw[kk][x], fj[y]);
-                if (kk + 1 < KS) fj[y] = *reinterpret_cast<const U4 *>(cur + ((boff[y] + to) << 4));
-            }
-        }
-        for (int c = KS; c < nc; ++c) bc.copy(a, wave + NW * c, nxt);
-
-#pragma unroll
-        for (int i = KS; i < 2 * MJ; ++i) store_one(i / MJ, i % MJ);
-
-        // bias + ReLU, rounded once (lane: channels co .. co + 3 of pixel 16 g + ld)
-#pragma unroll
-        for (int x = 0; x < 2; ++x) {
-#pragma unroll
-            for (int y = 0; y < MJ; ++y) {
-                float v4[4] = {acc[x][y][0], acc[x][y][1], acc[x][y][2], acc[x][y][3]};
-                if (a.bias != nullptr) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float v = v4[e] + bv[x][e];
-                        v4[e] = v > 0.f ? v : 0.f;
-                    }
-                }
-                held[x][y].x = pack_bf16x2(v4[0], v4[1]);
-                held[x][y].y = pack_bf16x2(v4[2], v4[3]);
-            }
-        }
-#pragma unroll
-        for (int y = 0; y < MJ; ++y) hoff[y] = coff[y];
-        wait_barrier<0>();
-    }
-#pragma unroll
-    for (int i = 0; i < 2 * MJ; ++i) store_one(i / MJ, i % MJ);
+    // wave-uniform choice of the run's offset into its first pixel group (UPW even: 0 or 2)
+    static_assert(UPW % 2 == 0, "runs start at channel group 0 or 2");
+    if (((UPW * wave) & 3) == 0)
+        band_fwd_reg_body<KS, UPW, 0>(a, xb0, xb1, sbias, wave);
+    else
+        band_fwd_reg_body<KS, UPW, 2>(a, xb0, xb1, sbias, wave);
 }
 
 // ---------------------------------------------------------------------------------- bwd-filter
@@ -517,18 +572,19 @@ __global__ __launch_bounds__(NW * 64, 1) void band_bwf_kernel(const BandArgs a) 
 #pragma unroll
         for (int y = 0; y < NG; ++y) acc[x][y] = fresh_zero4();
 
-    int b = blockIdx.x;
-    if (b < a.bands) {
+    int b = blockIdx.x * a.run;
+    const int b_end = min(a.bands, b + a.run);
+    if (b < b_end) {
         band_dma<X16, NW>(a, b, xb0);
         dy_dma(b, db0);
     }
     wait_barrier<0>();
 
-    for (int it = 0; b < a.bands; b += gridDim.x, ++it) {
+    for (int it = 0; b < b_end; ++b, ++it) {
         const unsigned char *xc = (it & 1) ? xb1 : xb0;
         const unsigned char *dc = (it & 1) ? db1 : db0;
-        const int bn = b + (int)gridDim.x;
-        if (bn < a.bands) {
+        const int bn = b + 1;
+        if (bn < b_end) {
             band_dma<X16, NW>(a, bn, (it & 1) ? xb0 : xb1);
             dy_dma(bn, (it & 1) ? db0 : db1);
         }
@@ -641,6 +697,12 @@ int band_rows(const ConvShape &s, int wst, int max_pix) {
     return R;
 }
 
+// Consecutive bands of an image share KH - sh input rows; a workgroup takes a run of consecutive
+// bands, so those rows are read again from its L2 instead of from memory.  Runs are as long as
+// one band per CU at most would need: ceil(bands / CUs).
+void set_runs(BandArgs &a) { a.run = (a.bands + kCUs - 1) / kCUs; }
+int band_grid(const BandArgs &a) { return (a.bands + a.run - 1) / a.run; }
+
 bool plan(const ConvShape &s, bool bwf, BandArgs &a) {
     if (s.C > 4 || s.K % 16 != 0) return false;
     const int kwp = bwf ? (s.KW + 3) / 4 * 4 : (s.KW + 1) / 2 * 2;
@@ -664,13 +726,14 @@ bool plan(const ConvShape &s, bool bwf, BandArgs &a) {
     const int64_t bands = (int64_t)s.N * a.bands_per_img;
     if (bands > (1 << 30)) return false;
     a.bands = (int)bands;
+    set_runs(a);
     a.dWst.init((uint32_t)wst);
     a.dOW.init((uint32_t)s.OW);
     a.dKwp.init((uint32_t)kwp);
     return true;
 }
 
-int bwf_splits(const BandArgs &a) { return std::min(a.bands, kCUs); }
+int bwf_splits(const BandArgs &a) { return band_grid(a); }
 
 // 16-byte band copies need pixel pairs that never straddle the image edge.
 bool pairs_aligned(const ConvShape &s) { return s.pl % 2 == 0 && s.W % 2 == 0; }
@@ -719,18 +782,21 @@ hipError_t launch_conv_fwd_band(const bf16_t *x4, const void *w, void *y, int64_
     a.out = y;
     a.bias = bias;
     a.ys = ys;
-    const dim3 grid((unsigned)std::min(a.bands, kCUs), (unsigned)((s.K + 63) / 64));
+    const dim3 grid((unsigned)band_grid(a), (unsigned)((s.K + 63) / 64));
     const bool x16 = pairs_aligned(s);
-    constexpr int kRegKS = 18, kRegMJ = 7, kRegNW = 4;    // AlexNet conv1: 11 x 12 taps x 4 channels
-    if (a.nks == kRegKS && s.sw % 2 == 0 && x16 && (int64_t)s.N * s.OH * s.OW * ys < (int64_t)1 << 31) {
-        const int R = band_rows(s, a.wst, 16 * kRegMJ * (kRegNW / 2));
-        if (R >= 1) {
+    constexpr int kRegKS = 17, kRegUPW = 14;    // AlexNet conv1: 11 x 12 taps x 4 channels, 4 rows of 55
+    const int ks = (s.KH * a.kwp * 4 + 31) / 32;
+    if (ks == kRegKS && s.sw % 2 == 0 && x16 && (int64_t)s.N * s.OH * s.OW * ys < (int64_t)1 << 31) {
+        const int R = band_rows(s, a.wst, 16 * kRegUPW);
+        if (R >= 1 && (R * s.OW + 15) / 16 == kRegUPW && (R - 1) * s.sh + s.KH <= kRegMaxRows &&
+            a.wst <= kRegRowBytes / 8 && a.kwp >= 8) {
             a.R = R;
             a.rows_in = (R - 1) * s.sh + s.KH;
             a.bands_per_img = (s.OH + R - 1) / R;
             a.bands = s.N * a.bands_per_img;
-            const dim3 g2((unsigned)std::min(a.bands, kCUs), (unsigned)((s.K + 63) / 64));
-            hipLaunchKernelGGL((band_fwd_reg_kernel<kRegKS, kRegMJ, kRegNW>), g2, dim3(64 * kRegNW), 0, st, a);
+            set_runs(a);
+            const dim3 g2((unsigned)band_grid(a), (unsigned)((s.K + 63) / 64));
+            hipLaunchKernelGGL((band_fwd_reg_kernel<kRegKS, kRegUPW>), g2, dim3(256), 0, st, a);
             return hipGetLastError();
         }
     }

@@ -224,6 +224,9 @@ BAND_CASES = [
     ("alexnet_conv1_b3", 3, 224, 224, 3, 64, 11, 11, 4, 4, (2, 2, 2, 2)),
     # more bands than workgroups: the double-buffered band loop runs twice on some workgroups
     ("many_bands", 300, 35, 35, 3, 64, 11, 11, 4, 4, (2, 2, 2, 2)),
+    # AlexNet conv1 with 280 bands: the register-filter forward kernel runs its band loop twice on
+    # some workgroups (and once on the others)
+    ("alexnet_conv1_b20", 20, 224, 224, 3, 64, 11, 11, 4, 4, (2, 2, 2, 2)),
     # two output-channel blocks; a partly empty channel block
     ("cin3_k128_5x5s2", 4, 30, 30, 3, 128, 5, 5, 2, 2, (2, 2, 2, 2)),
     ("cin3_k48_5x5s2", 3, 27, 29, 3, 48, 5, 5, 2, 2, (1, 2, 2, 1)),
