@@ -154,13 +154,13 @@ __global__ __launch_bounds__(256) void relu_bwd_partial_kernel(const T *__restri
     }
 }
 
-// Pass 2: one block per channel sums its G partials (stored channel-major, so
-// the reads are contiguous): thread t takes b = t, t + 256, ... in order, then
-// a fixed-shape tree combines the 256 running sums.  The loads of 16 consecutive
-// b of one thread are issued together before they are added (same order).
+// Pass 2: one block per channel sums its G partials (stored channel-major, so the reads are
+// contiguous): thread t takes b = t, t + 256, ... in order (the loads of 16 consecutive b of one
+// thread are issued together before they are added, in the same order), then a fixed xor tree
+// combines the 64 lanes of each wave and thread 0 adds the four wave sums in wave order.
 __global__ __launch_bounds__(256) void sum_partials_kernel(const float *__restrict__ partial, int G, int C,
                                                            float *__restrict__ out) {
-    __shared__ float red[256];
+    __shared__ float wsum[4];
     const int c = blockIdx.x;
     const float *row = partial + (int64_t)c * G;
     float acc = 0.f;
@@ -176,13 +176,11 @@ __global__ __launch_bounds__(256) void sum_partials_kernel(const float *__restri
         for (int u = 0; u < U; ++u)
             if (b0 + u * 256 < G) acc += v[u];
     }
-    red[threadIdx.x] = acc;
+#pragma unroll
+    for (int m = 32; m > 0; m >>= 1) acc += __shfl_xor(acc, m, 64);
+    if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = acc;
     __syncthreads();
-    for (int s = 128; s > 0; s >>= 1) {
-        if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) out[c] = red[0];
+    if (threadIdx.x == 0) out[c] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
 }
 
 // ------------------------------------------------------------------ pixel decomposition
@@ -585,7 +583,9 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *
 // form reloads them for every pixel) and each window's gradient is routed to the pixel its
 // argmax names, windows in ascending order (the same sums, in the same order, as the gather).
 // Bias-gradient partials as in maxpool_relu_bwd_partial_kernel, over cells instead of pixels.
-template <typename T, typename A>
+// PK > 0: the windows are PK x PK (a compile-time size, so the window/pixel pairs that can never
+// match are dropped: 9 of 16 remain for 3 x 3); PK = 0: the size comes from g.
+template <typename T, typename A, int PK>
 __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__restrict__ dy,
                                                                     const A *__restrict__ argmax, PoolGeom g,
                                                                     const T *__restrict__ y, T *dpre, float beta,
@@ -650,7 +650,9 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
                     for (int m = 0; m < 4; ++m) {
                         // pixel m is tap (2 (1 - k/2) + m/2, 2 (1 - k%2) + m%2) of window k
                         const int th = 2 * (1 - (k >> 1)) + (m >> 1), tw = 2 * (1 - (k & 1)) + (m & 1);
-                        const int32_t self = sizeof(A) == 1 ? (th < g.KH && tw < g.KW ? th * g.KW + tw : -1)
+                        const int KH = PK > 0 ? PK : g.KH, KW = PK > 0 ? PK : g.KW;
+                        if (PK > 0 && sizeof(A) == 1 && (th >= KH || tw >= KW)) continue;
+                        const int32_t self = sizeof(A) == 1 ? (th < KH && tw < KW ? th * KW + tw : -1)
                                                             : (int32_t)(pix[m] * g.C + cv * EPC);
 #pragma unroll
                         for (int e = 0; e < EPC; ++e)
@@ -1186,9 +1188,16 @@ static hipError_t maxpool_relu_bwd_t(const void *dy, const A *am, const PoolGeom
         const int64_t gc = std::max<int64_t>(1, std::min<int64_t>(G, (ncell + 2 * R - 1) / (2 * R)));
         const int Gc = (int)gc;
         const int64_t cpb = (ncell + gc - 1) / gc;
-        hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am, g,
-                           (const T *)y, (T *)dpre, beta, cpb, CH, CW, FastDiv((uint32_t)CW), FastDiv((uint32_t)CH),
-                           ws);
+        const FastDiv dCW((uint32_t)CW), dCH((uint32_t)CH);
+        if (g.KH == 3 && g.KW == 3)
+            hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A, 3>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am,
+                               g, (const T *)y, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
+        else if (g.KH == 2 && g.KW == 2)
+            hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A, 2>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am,
+                               g, (const T *)y, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
+        else
+            hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A, 0>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am,
+                               g, (const T *)y, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
         hipLaunchKernelGGL(sum_partials_kernel, dim3(g.C), dim3(256), 0, st, ws, Gc, g.C, db);
         return hipGetLastError();
     }
