@@ -6,7 +6,7 @@ accumulation, conv 11x11/4 64 -> pool 3/2 -> 5x5 192 -> pool -> 3x3 384 ->
 N(0,1) upstream gradient of the last pool, plain SGD (lr 0.01) of every filter
 and bias.  All inputs are resident in HBM before timing starts.
 
-    python bench.py [--steps K] [--warmup W] [--launch streams|graph|serial] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--launch program|streams|graph|serial] [--no-cpu-baseline]
 
 Prints one JSON line: ms per step (the timed region is K whole steps between
 two device synchronisations), conv TFLOP/s against the bf16 MFMA peak, the
@@ -45,9 +45,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--batch", type=int, default=128)
-    ap.add_argument("--launch", choices=("streams", "graph", "serial"), default="streams",
-                    help="two streams launched from the host (default), the two-stream step as a HIP graph, "
-                         "or one stream")
+    ap.add_argument("--launch", choices=("program", "streams", "graph", "serial"), default="program",
+                    help="the two-stream step recorded once and issued again from C++ (default), two streams "
+                         "launched from Python, the two-stream step as a HIP graph, or one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sampled", action="store_true", help="skip the sampled-softmax comparison")
     ap.add_argument("--metric-only", action="store_true",
@@ -312,10 +312,20 @@ def measure_workloads(args, torch, W, Replica):
             g.replay()
         torch.cuda.synchronize()
         ms_g = (time.perf_counter() - t0) * 1e3 / steps
+        # the step recorded once into a program and issued again from C++
+        prog = rep.record_step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            rep.run_program(prog)
+        torch.cuda.synchronize()
+        ms_p = (time.perf_counter() - t0) * 1e3 / steps
+        prog.close()
         fl = W.conv_flops(net)
-        best = min(ms, ms_g)
+        best = min(ms, ms_g, ms_p)
         out[net.name] = {"batch": net.tensors["x"][0], "dtype": net.dtype, "ms_per_step": round(ms, 3),
-                         "ms_per_step_graph": round(ms_g, 3), "ops": len(net.ops),
+                         "ms_per_step_graph": round(ms_g, 3), "ms_per_step_program": round(ms_p, 3),
+                         "ops": len(net.ops),
                          "conv_gflop_per_step": round(fl / 1e9, 1),
                          "step_tflops": round(fl / (best * 1e-3) / 1e12, 1)}
         del g
@@ -529,6 +539,9 @@ def main():
         with torch.cuda.graph(graph):
             rep.step()
         run = graph.replay
+    elif args.launch == "program":
+        prog = rep.record_step()           # the recording run is the first warm-up step
+        run = lambda: rep.run_program(prog)
     else:
         concurrent = args.launch == "streams"
         run = lambda: rep.step(concurrent=concurrent)
@@ -549,6 +562,26 @@ def main():
     step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
     print("bench: timed %d steps, %.3f ms/step (median %.3f)" % (args.steps, ms_per_step, np.median(step_ms)),
           file=sys.stderr, flush=True)
+
+    # ---------------------------------------------------------------- host enqueue time
+    # Wall time of the host call that enqueues one step, with the GPU kept busy by a spin kernel
+    # queued first (so the call never waits for the device): Python launches on two streams or
+    # one, and the recorded program issued from C++.
+    def host_ms(fn, reps=5):
+        out = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            torch.cuda._sleep(20_000_000)
+            h0 = time.perf_counter()
+            fn()
+            out.append((time.perf_counter() - h0) * 1e3)
+        torch.cuda.synchronize()
+        return round(float(np.median(out)), 4)
+    hprog = prog if args.launch == "program" else rep.record_step()
+    host_enqueue = {"streams": host_ms(lambda: rep.step(concurrent=True)),
+                    "serial": host_ms(lambda: rep.step(concurrent=False)),
+                    "program": host_ms(lambda: rep.run_program(hprog))}
+    print("bench: host enqueue ms per step %s" % host_enqueue, file=sys.stderr, flush=True)
 
     # ---------------------------------------------------------------- per-op events
     # Every op launched alone, in order, on one stream and bracketed by HIP events on that
@@ -663,7 +696,9 @@ def main():
         "config": {"workload": "alexnet_b%d" % args.batch, "global_batch": args.batch, "image": [224, 224, 3],
                    "layers": "conv11x11/4-64,pool3/2,conv5x5-192,pool3/2,conv3x3-384,conv3x3-256,conv3x3-256,pool3/2",
                    "launch": {"streams": "host launches, two streams", "graph": "hip_graph, two streams",
+                              "program": "recorded program issued from C++, two streams",
                               "serial": "host launches, one stream"}[args.launch]},
+        "host_enqueue_ms": host_enqueue,
         "step_ms_median": round(float(np.median(step_ms)), 4),
         "step_ms_p10": round(float(np.percentile(step_ms, 10)), 4),
         "step_ms_p90": round(float(np.percentile(step_ms, 90)), 4),

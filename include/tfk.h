@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 11
+#define TFK_ABI_VERSION 12
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -445,6 +445,46 @@ TFK_API tfk_status tfk_apply_momentum(float *var, float *accum, const float *gra
 TFK_API tfk_status tfk_apply_adam(float *var, float *m, float *v, const float *grad, int64_t n, float lr,
                           float beta1, float beta2, float epsilon, int64_t t, uint16_t *var_bf16,
                           void *stream);
+
+/* ---------------------------------------------------------------- streams and programs
+ * The dataflow executor runs independent kernels of a step on several GPU streams (Section 5);
+ * a step's subgraph is pruned and placed once, cached, and run again for every later step from
+ * one small request (Sections 3.2 and 3.3).  Here a step is a sequence of calls to this library;
+ * a program records that sequence once and issues it again from C++.
+ *
+ * tfk_stream_wait: work enqueued on `waiter` after this call starts only after everything
+ * enqueued on `producer` before it has completed (an event recorded on producer, waited on by
+ * waiter; no host synchronisation).  waiter == producer is a no-op.  NULL is the default stream.
+ * Errors: HIP (event creation, record or wait failed). */
+TFK_API tfk_status tfk_stream_wait(void *waiter, void *producer);
+
+/* Opaque recorded call sequence. */
+typedef struct tfk_program tfk_program;
+
+/* Creates an empty program in *prog (owned by the caller; release with tfk_program_destroy).
+ * Errors: NULL (prog is NULL); ARG (out of host memory). */
+TFK_API tfk_status tfk_program_create(tfk_program **prog);
+/* Releases a program and the events its recorded stream joins own (work already enqueued is
+ * not affected).  Stops its recording if it is recording on the calling thread.  NULL: no-op. */
+TFK_API void tfk_program_destroy(tfk_program *prog);
+/* Starts recording on the calling thread (previous contents are dropped).  Until
+ * tfk_program_end, every tfk_* call on this thread that enqueues work (convolutions, bias/ReLU,
+ * pooling, updates, losses, sampled-softmax ops, tfk_stream_wait) runs as usual and, when it
+ * returns TFK_OK, is appended to the program with its arguments by value: the same pointers,
+ * shapes, scalars and streams.  Calls that fail are not appended.  Queries
+ * (*_workspace_bytes) are never recorded.  Errors: NULL; ARG (this thread already records). */
+TFK_API tfk_status tfk_program_begin(tfk_program *prog);
+/* Stops recording.  Errors: NULL; ARG (prog is not recording on this thread). */
+TFK_API tfk_status tfk_program_end(tfk_program *prog);
+/* Number of recorded calls (0 for NULL). */
+TFK_API int64_t tfk_program_length(const tfk_program *prog);
+/* Issues the recorded calls again, in order, each validated as when it was recorded.  Every
+ * buffer a recorded call names must still be allocated, and each call's results depend only
+ * on what its buffers hold when it runs: scalars are replayed as recorded (a recorded
+ * tfk_apply_adam replays its step count t unchanged).  Stops at the first call that fails
+ * and returns its status.  Errors: NULL; ARG (a program is recording on this thread); any
+ * status a recorded call returns. */
+TFK_API tfk_status tfk_program_run(tfk_program *prog);
 
 /* ---------------------------------------------------------------- misc
  * Error reporting of the thin C API that the paper's client libraries sit on (Section 5: a C

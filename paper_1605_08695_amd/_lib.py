@@ -23,7 +23,9 @@ EXPORTS = ["tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_maxpool_bwd_relu_b
            "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps",
            "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd", "tfk_apply_sgd_multi",
            "tfk_apply_momentum", "tfk_apply_adam", "tfk_softmax_xent", "tfk_gather_rows_t",
-           "tfk_sampled_softmax_xent", "tfk_scatter_apply_sgd", "tfk_status_string", "tfk_last_error", "tfk_abi_version"]
+           "tfk_sampled_softmax_xent", "tfk_scatter_apply_sgd", "tfk_stream_wait", "tfk_program_create",
+           "tfk_program_destroy", "tfk_program_begin", "tfk_program_end", "tfk_program_length", "tfk_program_run",
+           "tfk_status_string", "tfk_last_error", "tfk_abi_version"]
 
 
 class Nhwc(ctypes.Structure):
@@ -91,6 +93,16 @@ def load(path: str = LIB_PATH):
                  "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps", "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd",
                  "tfk_apply_sgd_multi", "tfk_apply_momentum", "tfk_apply_adam", "tfk_softmax_xent", "tfk_gather_rows_t",
                  "tfk_sampled_softmax_xent", "tfk_scatter_apply_sgd"):
+        getattr(lib, name).restype = st
+    lib.tfk_stream_wait.argtypes = [vp, vp]
+    lib.tfk_program_create.argtypes = [ctypes.POINTER(vp)]
+    lib.tfk_program_destroy.argtypes = [vp]
+    lib.tfk_program_destroy.restype = None
+    for name in ("tfk_program_begin", "tfk_program_end", "tfk_program_run"):
+        getattr(lib, name).argtypes = [vp]
+    lib.tfk_program_length.argtypes = [vp]
+    lib.tfk_program_length.restype = i64
+    for name in ("tfk_stream_wait", "tfk_program_create", "tfk_program_begin", "tfk_program_end", "tfk_program_run"):
         getattr(lib, name).restype = st
     lib.tfk_status_string.argtypes = [st]
     lib.tfk_status_string.restype = ctypes.c_char_p

@@ -10,7 +10,10 @@
 #include <string.h>
 
 #include <algorithm>
+#include <functional>
+#include <memory>
 #include <string>
+#include <vector>
 
 #include "../../include/tfk.h"
 #include "kernels.h"
@@ -156,6 +159,53 @@ tfk_status check_ws(void *ws, size_t ws_bytes, size_t need) {
 
 }  // namespace
 
+// A recorded sequence of library calls (arguments by value) that tfk_program_run issues again in
+// the same order: one step's kernels, workspaces and stream joins, enqueued from C++ with no
+// per-call marshalling by the caller.
+struct tfk_program {
+    std::vector<std::function<tfk_status()>> calls;
+};
+
+namespace {
+
+// The program recording on this thread, if any.
+thread_local tfk_program *g_rec = nullptr;
+
+// While a program records on this thread, a call runs with recording paused (so that it is not
+// appended twice) and, when it succeeds, is appended with its arguments by value.
+#define RECORDED(fn, ...)                                                                        \
+    do {                                                                                         \
+        if (g_rec != nullptr) {                                                                  \
+            tfk_program *const rec_ = g_rec;                                                     \
+            g_rec = nullptr;                                                                     \
+            const tfk_status s_ = fn(__VA_ARGS__);                                               \
+            g_rec = rec_;                                                                        \
+            if (s_ != TFK_OK) return s_;                                                         \
+            try {                                                                                \
+                rec_->calls.emplace_back([=]() { return fn(__VA_ARGS__); });                     \
+            } catch (...) {                                                                      \
+                return fail(TFK_ERR_ARG, "%s: out of host memory while recording", #fn);         \
+            }                                                                                    \
+            return s_;                                                                           \
+        }                                                                                        \
+    } while (0)
+
+// An event owned by a recorded stream join (released with its program).
+struct OwnedEvent {
+    hipEvent_t e = nullptr;
+    ~OwnedEvent() {
+        if (e != nullptr) (void)hipEventDestroy(e);
+    }
+};
+
+tfk_status join(hipEvent_t e, hipStream_t waiter, hipStream_t producer) {
+    hipError_t r = hipEventRecord(e, producer);
+    if (r == hipSuccess) r = hipStreamWaitEvent(waiter, e, 0);
+    return hip_status(r, "stream_wait");
+}
+
+}  // namespace
+
 extern "C" {
 
 int32_t tfk_abi_version(void) { return TFK_ABI_VERSION; }
@@ -244,12 +294,14 @@ static tfk_status conv_fwd_impl(const void *x, tfk_nhwc xd, const void *w, int32
 
 tfk_status tfk_conv2d_fwd(const void *x, tfk_nhwc xd, const void *w, int32_t cout, tfk_window p, tfk_dtype dt,
                           void *y, tfk_nhwc yd, void *ws, size_t ws_bytes, void *stream) {
+    RECORDED(tfk_conv2d_fwd, x, xd, w, cout, p, dt, y, yd, ws, ws_bytes, stream);
     return conv_fwd_impl(x, xd, w, cout, nullptr, p, dt, y, yd, ws, ws_bytes, stream, "conv2d_fwd");
 }
 
 tfk_status tfk_conv2d_fwd_bias_relu(const void *x, tfk_nhwc xd, const void *w, int32_t cout, const float *bias,
                                     tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd, void *ws, size_t ws_bytes,
                                     void *stream) {
+    RECORDED(tfk_conv2d_fwd_bias_relu, x, xd, w, cout, bias, p, dt, y, yd, ws, ws_bytes, stream);
     if (xd.n > 0 && cout > 0) {
         TRY(need_ptr(bias, "bias"));
         TRY(need_align(bias, 4, "bias"));
@@ -259,6 +311,7 @@ tfk_status tfk_conv2d_fwd_bias_relu(const void *x, tfk_nhwc xd, const void *w, i
 
 tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void *w, tfk_window p, tfk_dtype dt, void *dx,
                                 tfk_nhwc dxd, float beta, void *ws, size_t ws_bytes, void *stream) {
+    RECORDED(tfk_conv2d_bwd_input, dy, dyd, w, p, dt, dx, dxd, beta, ws, ws_bytes, stream);
     ConvShape s;
     TRY(check_conv(dxd, dyd.c, p, dt, dyd, "dx", "dy", s));
     if (!(beta == 0.f || beta == 1.f)) return fail(TFK_ERR_ARG, "beta must be 0 or 1");
@@ -290,6 +343,7 @@ tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void *w, tfk
 tfk_status tfk_conv2d_bwd_input_relu_bwd(const void *dy, tfk_nhwc dyd, const void *w, tfk_window p, tfk_dtype dt,
                                          const void *y, void *dpre, tfk_nhwc xd, float *dbias, void *ws,
                                          size_t ws_bytes, void *stream) {
+    RECORDED(tfk_conv2d_bwd_input_relu_bwd, dy, dyd, w, p, dt, y, dpre, xd, dbias, ws, ws_bytes, stream);
     ConvShape s;
     TRY(check_conv(xd, dyd.c, p, dt, dyd, "dpre", "dy", s));
     if (xd.c > 16384) return fail(TFK_ERR_SHAPE, "conv2d_bwd_input_relu_bwd supports at most 16384 channels");
@@ -326,6 +380,7 @@ tfk_status tfk_conv2d_bwd_input_relu_bwd(const void *dy, tfk_nhwc dyd, const voi
 
 tfk_status tfk_conv2d_bwd_filter(const void *x, tfk_nhwc xd, const void *dy, tfk_nhwc dyd, tfk_window p,
                                  tfk_dtype dt, float *dw, void *ws, size_t ws_bytes, void *stream) {
+    RECORDED(tfk_conv2d_bwd_filter, x, xd, dy, dyd, p, dt, dw, ws, ws_bytes, stream);
     ConvShape s;
     TRY(check_conv(xd, dyd.c, p, dt, dyd, "x", "dy", s));
     TRY(need_ptr(dw, "dw"));
@@ -355,6 +410,7 @@ tfk_status tfk_conv2d_bwd_filter(const void *x, tfk_nhwc xd, const void *dy, tfk
 
 tfk_status tfk_conv2d_bwd_filter_noalloc(const void *x, tfk_nhwc xd, const void *dy, tfk_nhwc dyd, tfk_window p,
                                          tfk_dtype dt, float *dw, void *stream) {
+    RECORDED(tfk_conv2d_bwd_filter_noalloc, x, xd, dy, dyd, p, dt, dw, stream);
     ConvShape s;
     TRY(check_conv(xd, dyd.c, p, dt, dyd, "x", "dy", s));
     int64_t xs = xd.pixel_stride;
@@ -376,6 +432,7 @@ tfk_status tfk_conv2d_bwd_filter_noalloc(const void *x, tfk_nhwc xd, const void 
 
 // ------------------------------------------------------------------ bias + ReLU
 tfk_status tfk_bias_relu_fwd(void *y, tfk_nhwc yd, const float *bias, tfk_dtype dt, void *stream) {
+    RECORDED(tfk_bias_relu_fwd, y, yd, bias, dt, stream);
     if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
     TRY(check_view("y", yd));
     if (yd.n == 0) return ok();
@@ -401,6 +458,7 @@ size_t tfk_bias_relu_bwd_workspace_bytes(tfk_nhwc yd, tfk_dtype dt) {
 
 tfk_status tfk_bias_relu_bwd(const void *y, const void *dy, tfk_nhwc yd, void *dpre, float *dbias, tfk_dtype dt,
                              void *ws, size_t ws_bytes, void *stream) {
+    RECORDED(tfk_bias_relu_bwd, y, dy, yd, dpre, dbias, dt, ws, ws_bytes, stream);
     if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
     TRY(check_view("y", yd));
     TRY(need_ptr(dbias, "dbias"));
@@ -478,11 +536,13 @@ static tfk_status maxpool_fwd_impl(const void *x, tfk_nhwc xd, tfk_window p, tfk
 
 tfk_status tfk_maxpool_fwd(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
                            int32_t *argmax, void *stream) {
+    RECORDED(tfk_maxpool_fwd, x, xd, p, dt, y, yd, argmax, stream);
     return maxpool_fwd_impl(x, xd, p, dt, y, yd, argmax, false, stream);
 }
 
 tfk_status tfk_maxpool_fwd_taps(const void *x, tfk_nhwc xd, tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
                                 uint8_t *taps, void *stream) {
+    RECORDED(tfk_maxpool_fwd_taps, x, xd, p, dt, y, yd, taps, stream);
     return maxpool_fwd_impl(x, xd, p, dt, y, yd, taps, true, stream);
 }
 
@@ -490,6 +550,7 @@ tfk_status tfk_conv2d_fwd_bias_relu_maxpool(const void *x, tfk_nhwc xd, const vo
                                             const float *bias, tfk_window p, tfk_dtype dt, void *y, tfk_nhwc yd,
                                             tfk_window pp, void *py, tfk_nhwc pyd, uint8_t *taps, void *ws,
                                             size_t ws_bytes, void *stream) {
+    RECORDED(tfk_conv2d_fwd_bias_relu_maxpool, x, xd, w, cout, bias, p, dt, y, yd, pp, py, pyd, taps, ws, ws_bytes, stream);
     ConvShape s;
     int64_t xs;
     size_t need;
@@ -552,11 +613,13 @@ static tfk_status maxpool_bwd_impl(const void *dy, const void *argmax, bool taps
 
 tfk_status tfk_maxpool_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
                            void *dx, tfk_nhwc xd, float beta, void *stream) {
+    RECORDED(tfk_maxpool_bwd, dy, argmax, yd, p, dt, dx, xd, beta, stream);
     return maxpool_bwd_impl(dy, argmax, false, yd, p, dt, dx, xd, beta, stream);
 }
 
 tfk_status tfk_maxpool_bwd_taps(const void *dy, const uint8_t *taps, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
                                 void *dx, tfk_nhwc xd, float beta, void *stream) {
+    RECORDED(tfk_maxpool_bwd_taps, dy, taps, yd, p, dt, dx, xd, beta, stream);
     return maxpool_bwd_impl(dy, taps, true, yd, p, dt, dx, xd, beta, stream);
 }
 
@@ -602,12 +665,14 @@ static tfk_status maxpool_relu_bwd_impl(const void *dy, const void *argmax, bool
 tfk_status tfk_maxpool_bwd_relu_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
                                     const void *y, void *dpre, tfk_nhwc xd, float beta, float *dbias, void *ws,
                                     size_t ws_bytes, void *stream) {
+    RECORDED(tfk_maxpool_bwd_relu_bwd, dy, argmax, yd, p, dt, y, dpre, xd, beta, dbias, ws, ws_bytes, stream);
     return maxpool_relu_bwd_impl(dy, argmax, false, yd, p, dt, y, dpre, xd, beta, dbias, ws, ws_bytes, stream);
 }
 
 tfk_status tfk_maxpool_bwd_relu_bwd_taps(const void *dy, const uint8_t *taps, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
                                          const void *y, void *dpre, tfk_nhwc xd, float beta, float *dbias, void *ws,
                                          size_t ws_bytes, void *stream) {
+    RECORDED(tfk_maxpool_bwd_relu_bwd_taps, dy, taps, yd, p, dt, y, dpre, xd, beta, dbias, ws, ws_bytes, stream);
     return maxpool_relu_bwd_impl(dy, taps, true, yd, p, dt, y, dpre, xd, beta, dbias, ws, ws_bytes, stream);
 }
 
@@ -628,6 +693,7 @@ static tfk_status check_sgd(float *var, const float *grad, int64_t n, float lr, 
 }
 
 tfk_status tfk_apply_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *var_bf16, void *stream) {
+    RECORDED(tfk_apply_sgd, var, grad, n, lr, var_bf16, stream);
     TRY(check_sgd(var, grad, n, lr, var_bf16));
     if (n == 0) return ok();
     return hip_status(launch_sgd(var, grad, n, lr, var_bf16, (hipStream_t)stream), "apply_sgd");
@@ -635,6 +701,28 @@ tfk_status tfk_apply_sgd(float *var, const float *grad, int64_t n, float lr, uin
 
 tfk_status tfk_apply_sgd_multi(int32_t count, float *const *vars, const float *const *grads, const int64_t *ns,
                                float lr, uint16_t *const *shadows, void *stream) {
+    if (g_rec != nullptr && count > 0 && vars != nullptr && grads != nullptr && ns != nullptr) {
+        // the pointer arrays belong to the caller: the recorded call keeps copies of them
+        tfk_program *const rec_ = g_rec;
+        g_rec = nullptr;
+        const tfk_status s_ = tfk_apply_sgd_multi(count, vars, grads, ns, lr, shadows, stream);
+        g_rec = rec_;
+        if (s_ != TFK_OK) return s_;
+        try {
+            std::vector<float *> v(vars, vars + count);
+            std::vector<const float *> g(grads, grads + count);
+            std::vector<int64_t> n(ns, ns + count);
+            std::vector<uint16_t *> sh;
+            if (shadows != nullptr) sh.assign(shadows, shadows + count);
+            rec_->calls.emplace_back([=]() {
+                return tfk_apply_sgd_multi(count, v.data(), g.data(), n.data(), lr,
+                                           sh.empty() ? nullptr : sh.data(), stream);
+            });
+        } catch (...) {
+            return fail(TFK_ERR_ARG, "tfk_apply_sgd_multi: out of host memory while recording");
+        }
+        return s_;
+    }
     if (count < 0) return fail(TFK_ERR_ARG, "count must be >= 0");
     if (count == 0) return ok();
     TRY(need_ptr(vars, "vars"));
@@ -670,6 +758,7 @@ tfk_status tfk_apply_sgd_multi(int32_t count, float *const *vars, const float *c
 // ------------------------------------------------------------------ softmax cross-entropy
 tfk_status tfk_softmax_xent(const void *logits, tfk_dtype dt, int64_t n, int32_t c, const float *bias,
                             const int32_t *labels, float scale, float *loss, void *dlogits, void *stream) {
+    RECORDED(tfk_softmax_xent, logits, dt, n, c, bias, labels, scale, loss, dlogits, stream);
     if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
     if (n < 0 || c < 1) return fail(TFK_ERR_SHAPE, "need n >= 0 and c >= 1 (n=%lld, c=%d)", (long long)n, c);
     if (!isfinite(scale)) return fail(TFK_ERR_ARG, "scale must be finite");
@@ -702,6 +791,7 @@ tfk_status tfk_softmax_xent(const void *logits, tfk_dtype dt, int64_t n, int32_t
 // ------------------------------------------------------------------ sampled softmax
 tfk_status tfk_gather_rows_t(const void *table, tfk_dtype dt, int64_t rows, int32_t d, const int32_t *idx, int32_t u,
                              int32_t u_pad, void *out_t, void *stream) {
+    RECORDED(tfk_gather_rows_t, table, dt, rows, d, idx, u, u_pad, out_t, stream);
     if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
     if (rows < 0 || d < 1 || u < 0 || u_pad < u) return fail(TFK_ERR_SHAPE, "need rows >= 0, d >= 1, 0 <= u <= u_pad");
     if ((int64_t)d * u_pad == 0) return ok();
@@ -727,6 +817,7 @@ tfk_status tfk_gather_rows_t(const void *table, tfk_dtype dt, int64_t rows, int3
 tfk_status tfk_sampled_softmax_xent(const void *z, tfk_dtype dt, int64_t n, int32_t u, int32_t u_pad, int32_t m,
                                     const float *bias_c, const int32_t *true_pos, const float *lq_true,
                                     const float *lq_sampled, float scale, float *loss, void *dz, void *stream) {
+    RECORDED(tfk_sampled_softmax_xent, z, dt, n, u, u_pad, m, bias_c, true_pos, lq_true, lq_sampled, scale, loss, dz, stream);
     if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
     if (n < 0 || m < 0 || u < m || u < 1 || u_pad < u)
         return fail(TFK_ERR_SHAPE, "need n >= 0 and 0 <= m <= u <= u_pad, u >= 1");
@@ -759,6 +850,7 @@ tfk_status tfk_sampled_softmax_xent(const void *z, tfk_dtype dt, int64_t n, int3
 
 tfk_status tfk_scatter_apply_sgd(float *var, uint16_t *var_bf16, int64_t rows, int32_t d, const int32_t *idx,
                                  int32_t u, const float *grad_t, int64_t ld, float lr, void *stream) {
+    RECORDED(tfk_scatter_apply_sgd, var, var_bf16, rows, d, idx, u, grad_t, ld, lr, stream);
     if (rows < 0 || d < 1 || u < 0 || ld < u) return fail(TFK_ERR_SHAPE, "need rows >= 0, d >= 1, 0 <= u <= ld");
     if (!isfinite(lr)) return fail(TFK_ERR_ARG, "lr must be finite");
     if (u == 0) return ok();
@@ -806,6 +898,7 @@ static tfk_status check_slots(float *var, const float *grad, const float *s1, co
 
 tfk_status tfk_apply_momentum(float *var, float *accum, const float *grad, int64_t n, float lr, float momentum,
                               int32_t nesterov, uint16_t *var_bf16, void *stream) {
+    RECORDED(tfk_apply_momentum, var, accum, grad, n, lr, momentum, nesterov, var_bf16, stream);
     if (!isfinite(lr)) return fail(TFK_ERR_ARG, "lr must be finite");
     if (!isfinite(momentum)) return fail(TFK_ERR_ARG, "momentum must be finite");
     if (nesterov != 0 && nesterov != 1) return fail(TFK_ERR_ARG, "nesterov must be 0 or 1");
@@ -820,6 +913,7 @@ tfk_status tfk_apply_momentum(float *var, float *accum, const float *grad, int64
 
 tfk_status tfk_apply_adam(float *var, float *m, float *v, const float *grad, int64_t n, float lr, float beta1,
                           float beta2, float epsilon, int64_t t, uint16_t *var_bf16, void *stream) {
+    RECORDED(tfk_apply_adam, var, m, v, grad, n, lr, beta1, beta2, epsilon, t, var_bf16, stream);
     if (!isfinite(lr)) return fail(TFK_ERR_ARG, "lr must be finite");
     if (!(beta1 >= 0.f && beta1 < 1.f)) return fail(TFK_ERR_ARG, "beta1 must be in [0, 1)");
     if (!(beta2 >= 0.f && beta2 < 1.f)) return fail(TFK_ERR_ARG, "beta2 must be in [0, 1)");
@@ -838,6 +932,73 @@ tfk_status tfk_apply_adam(float *var, float *m, float *v, const float *grad, int
     p.eps = epsilon;
     if (!isfinite(p.lr) || !isfinite(p.rc2)) return fail(TFK_ERR_OVERFLOW, "bias-corrected step overflows fp32");
     return hip_status(launch_opt(2, var, m, v, grad, n, p, var_bf16, (hipStream_t)stream), "apply_adam");
+}
+
+// ------------------------------------------------------------------ streams and programs
+tfk_status tfk_stream_wait(void *waiter, void *producer) {
+    if (waiter == producer) return ok();
+    if (g_rec != nullptr) {
+        auto ev = std::make_shared<OwnedEvent>();
+        hipError_t r = hipEventCreateWithFlags(&ev->e, hipEventDisableTiming);
+        if (r != hipSuccess) {
+            ev->e = nullptr;
+            return hip_status(r, "stream_wait");
+        }
+        TRY(join(ev->e, (hipStream_t)waiter, (hipStream_t)producer));
+        try {
+            g_rec->calls.emplace_back([=]() { return join(ev->e, (hipStream_t)waiter, (hipStream_t)producer); });
+        } catch (...) {
+            return fail(TFK_ERR_ARG, "tfk_stream_wait: out of host memory while recording");
+        }
+        return ok();
+    }
+    hipEvent_t e;
+    hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+    if (r != hipSuccess) return hip_status(r, "stream_wait");
+    const tfk_status s = join(e, (hipStream_t)waiter, (hipStream_t)producer);
+    (void)hipEventDestroy(e);      // released once the recorded work completes
+    return s;
+}
+
+tfk_status tfk_program_create(tfk_program **prog) {
+    TRY(need_ptr(prog, "prog"));
+    try {
+        *prog = new tfk_program();
+    } catch (...) {
+        *prog = nullptr;
+        return fail(TFK_ERR_ARG, "out of host memory");
+    }
+    return ok();
+}
+
+void tfk_program_destroy(tfk_program *prog) {
+    if (prog == nullptr) return;
+    if (g_rec == prog) g_rec = nullptr;
+    delete prog;
+}
+
+tfk_status tfk_program_begin(tfk_program *prog) {
+    TRY(need_ptr(prog, "prog"));
+    if (g_rec != nullptr) return fail(TFK_ERR_ARG, "a program is already recording on this thread");
+    prog->calls.clear();
+    g_rec = prog;
+    return ok();
+}
+
+tfk_status tfk_program_end(tfk_program *prog) {
+    TRY(need_ptr(prog, "prog"));
+    if (g_rec != prog) return fail(TFK_ERR_ARG, "this program is not recording on this thread");
+    g_rec = nullptr;
+    return ok();
+}
+
+int64_t tfk_program_length(const tfk_program *prog) { return prog == nullptr ? 0 : (int64_t)prog->calls.size(); }
+
+tfk_status tfk_program_run(tfk_program *prog) {
+    TRY(need_ptr(prog, "prog"));
+    if (g_rec != nullptr) return fail(TFK_ERR_ARG, "cannot run a program while one is recording on this thread");
+    for (const auto &call : prog->calls) TRY(call());
+    return ok();
 }
 
 }  // extern "C"

@@ -18,7 +18,8 @@ from ._lib import Nhwc, TfkError, Window, TFK_BF16, TFK_F32, check, load
 __all__ = ["conv2d_fwd", "conv2d_fwd_bias_relu", "conv2d_bwd_input", "conv2d_bwd_filter", "conv2d_workspace_bytes", "bias_relu_fwd",
            "bias_relu_bwd", "bias_relu_bwd_workspace_bytes", "maxpool_fwd", "maxpool_bwd", "maxpool_bwd_relu_bwd", "apply_sgd",
            "apply_sgd_multi", "apply_momentum", "apply_adam", "softmax_xent",
-           "gather_rows_t", "sampled_softmax_xent", "scatter_apply_sgd", "out_len", "nhwc", "window", "TfkError", "abi_version"]
+           "gather_rows_t", "sampled_softmax_xent", "scatter_apply_sgd", "stream_wait", "Program", "out_len", "nhwc",
+           "window", "TfkError", "abi_version"]
 
 
 def _dt(t: torch.Tensor) -> int:
@@ -436,3 +437,55 @@ def scatter_apply_sgd(var, idx, grad_t, lr, shadow=None, stream=None):
     check(load().tfk_scatter_apply_sgd(_ptr(var), _ptr(shadow), rows, d, _ptr(idx), idx.numel(), _ptr(grad_t), ld,
                                        float(lr), _stream(stream)))
     return var
+
+
+# ----------------------------------------------------------------------------- streams and programs
+def stream_wait(waiter, producer):
+    """Work enqueued on ``waiter`` afterwards waits for everything enqueued on ``producer`` so far
+    (an event join inside the library; recorded into a program like the ops)."""
+    check(load().tfk_stream_wait(ctypes.c_void_p(waiter.cuda_stream), ctypes.c_void_p(producer.cuda_stream)))
+
+
+class Program:
+    """A recorded sequence of library calls, issued again from C++ by ``run()``.
+
+    ``with prog.recording(): ...`` runs the calls made inside the block as usual and records
+    each one that succeeds (same pointers, shapes, scalars and streams); ``run()`` enqueues them
+    again in order.  Buffers the calls name must stay allocated while the program is used."""
+
+    def __init__(self):
+        self._lib = load()
+        h = ctypes.c_void_p()
+        check(self._lib.tfk_program_create(ctypes.byref(h)))
+        self._h = h
+
+    def recording(self):
+        prog = self
+
+        class _Rec:
+            def __enter__(self):
+                check(prog._lib.tfk_program_begin(prog._h))
+                return prog
+
+            def __exit__(self, *exc):
+                check(prog._lib.tfk_program_end(prog._h))
+                return False
+
+        return _Rec()
+
+    def __len__(self) -> int:
+        return int(self._lib.tfk_program_length(self._h))
+
+    def run(self):
+        check(self._lib.tfk_program_run(self._h))
+
+    def close(self):
+        if self._h is not None and self._h.value:
+            self._lib.tfk_program_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -274,7 +274,7 @@ class Replica:
                 # on the main stream, where it is next on the critical path
                 on_side = side is not None and src_grad
                 if on_side:
-                    side.wait_stream(cur)
+                    ops.stream_wait(side, cur)
                 fs = side if on_side else stream
                 if trace: trace("conv_bwd_filter", op, stream=fs, x=x, dy=dpre)
                 ops.conv2d_bwd_filter(x, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, dw=self.dW[op.name],
@@ -314,7 +314,7 @@ class Replica:
             if src_grad:
                 written.add(op.src)
         if side is not None:
-            cur.wait_stream(side)
+            ops.stream_wait(cur, side)
 
     def update(self, trace=None, stream=None):
         a = self.opt_args
@@ -342,6 +342,31 @@ class Replica:
         self.forward(trace, stream)
         self.backward(trace, stream, side=self.side if concurrent else None)
         self.update(trace, stream)
+
+    def record_step(self, stream=None, concurrent=True) -> "ops.Program":
+        """Runs one step (as ``step``) while recording its library calls into a program, which
+        ``run_program`` issues again for every later step from C++ (the cached step subgraph of
+        Sections 3.2 and 3.3).  The update is recorded too, except Adam's, whose bias correction
+        depends on the step count: ``run_program`` then runs it after the recorded calls."""
+        prog = ops.Program()
+        prog.with_update = self.optimizer != "adam"
+        with prog.recording():
+            self.forward(None, stream)
+            self.backward(None, stream, side=self.side if concurrent else None)
+            if prog.with_update:
+                self.update(None, stream)
+        if not prog.with_update:
+            self.update(None, stream)
+        return prog
+
+    def run_program(self, prog, stream=None):
+        """One training step from a program made by ``record_step`` (on the streams it was
+        recorded on; ``stream`` only places an update that was not recorded)."""
+        prog.run()
+        if prog.with_update:
+            self.t += 1
+        else:
+            self.update(None, stream)
 
     # ------------------------------------------------------------------ state
     def snapshot(self):

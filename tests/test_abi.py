@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 11
+    assert lib.tfk_abi_version() == 12
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -379,3 +379,38 @@ def test_fully_connected_workspace_queries(lib):
     assert s3 > 0 and s3 % (4 * 36 * 256) == 0                    # splits x 144 pixels x 256 x 4 B
     assert q(1, 4, win=Window(3, 3, 2, 2, 1, 1, 1, 1), h=6) == 0  # stride 2: several phases, no split
     assert q(2, 4) == 0                                           # 4-pixel reduction: no split partials
+
+
+def test_program_records_successful_calls_only(lib):
+    # Recording on the calling thread: calls that pass validation are appended (here no-ops with an
+    # empty batch, which enqueue nothing), failing calls are not; a run re-issues the recorded ones.
+    prog = ops.Program()
+    with prog.recording():
+        assert conv_fwd(lib, x=0, w=0, y=0, xd=(0, 8, 8, 16, 0), yd=(0, 8, 8, 32, 0)) == OK
+        assert conv_fwd(lib, x=0) == NULL                         # rejected: not recorded
+        assert lib.tfk_apply_sgd(None, None, 0, ctypes.c_float(0.1), None, None) == OK
+    assert len(prog) == 2
+    prog.run()
+    assert len(prog) == 2
+    with prog.recording():                                       # recording again starts empty
+        pass
+    assert len(prog) == 0
+    prog.close()
+
+
+def test_program_state_errors(lib):
+    a, b = ops.Program(), ops.Program()
+    assert lib.tfk_program_begin(a._h) == OK
+    assert lib.tfk_program_begin(b._h) == ARG                    # one recording per thread
+    assert lib.tfk_program_run(b._h) == ARG                      # no runs while recording
+    assert lib.tfk_program_end(b._h) == ARG                      # b is not the one recording
+    assert lib.tfk_program_end(a._h) == OK
+    assert lib.tfk_program_end(a._h) == ARG
+    assert lib.tfk_program_begin(None) == NULL
+    assert lib.tfk_program_length(None) == 0
+    assert lib.tfk_program_begin(a._h) == OK
+    a.close()                                                    # destroying stops its recording
+    assert lib.tfk_program_begin(b._h) == OK
+    assert lib.tfk_program_end(b._h) == OK
+    assert lib.tfk_stream_wait(None, None) == OK                 # same stream: no-op
+    b.close()

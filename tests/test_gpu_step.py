@@ -322,3 +322,35 @@ def test_graph_capture_replays_match_eager():
         assert bitwise_equal(eager.params, graphed.params), r
         assert bitwise_equal(eager.grads, graphed.grads), r
         _ = torch.ones(1024, device="cuda").sum().item()      # unrelated eager work between replays
+
+
+@pytest.mark.parametrize("make,opt", [(lambda: W.alexnet(batch=8), "sgd"), (lambda: W.googlenet(batch=4), "sgd"),
+                                      (lambda: W.alexnet(batch=8), "momentum"), (lambda: W.alexnet(batch=8), "adam")],
+                         ids=["alexnet_b8_sgd", "googlenet_b4_sgd", "alexnet_b8_momentum", "alexnet_b8_adam"])
+def test_program_replays_match_eager(make, opt):
+    """The step recorded once into a native program (its library calls, stream joins included)
+    and issued again from C++: every replay, with eager steps and synchronisations in between,
+    must equal the eager two-stream step from the same state (the Adam update, whose step count
+    changes, runs eagerly after the recorded calls)."""
+    net = make()
+    net.lr = 1e-6
+    inp = W.make_inputs(net, seed=4)
+    eager, prog_rep = Replica(net, inp, optimizer=opt), Replica(net, inp, optimizer=opt)
+    eager.step()
+    prog = prog_rep.record_step()
+    torch.cuda.synchronize()
+    say("program", net.name, opt, "recorded calls:", len(prog))
+    assert len(prog) > len(net.ops)
+    assert bitwise_equal(eager.params, prog_rep.params)
+    for r in range(3):
+        eager.step()
+        prog_rep.run_program(prog)
+        torch.cuda.synchronize()
+        assert eager.t == prog_rep.t, r
+        assert bool(torch.isfinite(prog_rep.params).all()), r
+        assert bitwise_equal(eager.grads, prog_rep.grads), r
+        assert bitwise_equal(eager.params, prog_rep.params), r
+        for a, b in zip(eager.slots, prog_rep.slots):
+            assert bitwise_equal(a, b), r
+        _ = torch.ones(1024, device="cuda").sum().item()      # unrelated eager work between replays
+    prog.close()
