@@ -66,13 +66,26 @@ class Replica:
         dev, dt = self.device, self.dtype
 
         # ---- variables
+        # Filters first; then the biases, those of the convolutions that write one tensor side
+        # by side in channel order (a concat's branches), so that a group of them has one
+        # contiguous bias-gradient slice (see relu_groups below).
         off = 0
         self._layout = {}
+        wofs = {}
         for c in net.convs:
             cin = net.tensors[c.src][3]
             wn = c.kh * c.kw * cin * c.cout
-            self._layout[c.name] = (off, (c.kh, c.kw, cin, c.cout), off + _align(wn), c.cout)
-            off += _align(wn) + _align(c.cout)
+            wofs[c.name] = (off, (c.kh, c.kw, cin, c.cout))
+            off += _align(wn)
+        by_dst = {}
+        for c in net.convs:
+            by_dst.setdefault(c.dst, []).append(c)
+        for dst, cs in by_dst.items():
+            off = _align(off)
+            for c in sorted(cs, key=lambda c: c.dst_c0):
+                self._layout[c.name] = wofs[c.name] + (off, c.cout)
+                off += c.cout
+        off = _align(off)
         self.n_params = off
         self.params = torch.zeros(off, dtype=torch.float32, device=dev)
         self.grads = torch.zeros(off, dtype=torch.float32, device=dev)
@@ -158,6 +171,31 @@ class Replica:
                     self.bwi_relu[op.name] = w[0]
         self.relu_fused = ({c.name for c in self.pool_relu.values()} |
                            {c.name for c in self.bwi_relu.values()})
+        # ---- convolutions writing adjacent channel ranges of one tensor (a concat's branches,
+        # each with its own ReLU and bias) whose readers all come after the last of them: their
+        # ReLU backward runs once over the whole range, with one bias-gradient reduction into
+        # their adjacent bias-gradient slices
+        pos = {op.name: k for k, op in enumerate(net.ops)}
+        self.relu_groups = {}                    # conv name -> (first channel, width, [convs])
+        for dst, cs in by_dst.items():
+            cand = sorted((c for c in cs if c.relu and c.name not in self.relu_fused and dst != net.output),
+                          key=lambda c: c.dst_c0)
+            runs, cur = [], []
+            for c in cand:
+                if cur and c.dst_c0 == cur[-1].dst_c0 + cur[-1].cout:
+                    cur.append(c)
+                else:
+                    if len(cur) > 1:
+                        runs.append(cur)
+                    cur = [c]
+            if len(cur) > 1:
+                runs.append(cur)
+            for run in runs:
+                last = max(pos[c.name] for c in run)
+                if all(pos[r.name] > last for r in readers.get(dst, [])):
+                    g = (run[0].dst_c0, sum(c.cout for c in run), run)
+                    for c in run:
+                        self.relu_groups[c.name] = g
         # ---- a convolution whose whole ReLU output is pooled by the next op: one forward call
         # (one kernel where its row bands hold whole pool windows)
         self.conv_pool = {}                      # conv name -> pool op
@@ -175,6 +213,8 @@ class Replica:
             for op_kind in (0, 1, 2, 3) if c.name in self.bwi_relu else (0, 1, 2):
                 need = max(need, ops.conv2d_workspace_bytes(op_kind, x, c.cout, c.kh, c.kw, (c.sh, c.sw), c.pads))
             need = max(need, ops.bias_relu_bwd_workspace_bytes(self._slice(self.act, c)))
+        for c0, width, run in {id(g[2]): g for g in self.relu_groups.values()}.values():
+            need = max(need, ops.bias_relu_bwd_workspace_bytes(self.act[run[0].dst][..., c0:c0 + width]))
         self.ws = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=dev)
         # ---- filter gradients run on a second stream, with a workspace of their own
         need = 0
@@ -250,6 +290,7 @@ class Replica:
         independent kernels on several GPU streams, Section 5)."""
         net = self.net
         written = set()
+        grouped = set()                          # ReLU groups whose backward has run
         cur = stream if stream is not None else torch.cuda.current_stream()
         for op in reversed(net.ops):
             dy = self._slice(self.grad, op)
@@ -263,6 +304,16 @@ class Replica:
                     if trace: trace("bias_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
                 elif op.name in self.relu_fused:
                     dpre = dy                        # written by the fused pool / input-gradient backward
+                elif op.name in self.relu_groups:
+                    dpre = dy
+                    c0, width, run = self.relu_groups[op.name]
+                    if id(run) not in grouped:       # the group's last convolution in forward order
+                        grouped.add(id(run))
+                        yg, dyg = self.act[op.dst][..., c0:c0 + width], self.grad[op.dst][..., c0:c0 + width]
+                        dbg = self.grads[self._layout[run[0].name][2]:self._layout[run[0].name][2] + width]
+                        if trace: trace("bias_relu_bwd", op, stream=stream, y=yg, dy=dyg)
+                        ops.bias_relu_bwd(yg, dyg, dpre=dyg, dbias=dbg, ws=self.ws, stream=stream)
+                        if trace: trace("bias_relu_bwd:end", op, stream=stream, dpre=dyg, db=dbg)
                 else:
                     y = self._slice(self.act, op)
                     dpre = self._slice({op.dst: self.dpre_out}, op) if op.dst == net.output else dy

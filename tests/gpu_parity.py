@@ -174,7 +174,27 @@ class ParityTracer:
         v = self.state[key]
         return v if c0 is None else v[..., c0:c0 + t.shape[3]]
 
+    def _spans(self, t):
+        """The whole variables a 1-D slice covers exactly, side by side (the bias gradients of a
+        group of concat branches): [(key, first element of t, length)], or None."""
+        if t.dim() != 1:
+            return None
+        p, es, n = t.data_ptr(), t.element_size(), t.numel()
+        parts = sorted(((b.data_ptr() - p) // es, key, b.numel()) for key, b in self.whole
+                       if b.dtype == t.dtype and b.dim() == 1 and p <= b.data_ptr() < p + n * es)
+        at = 0
+        for off, _, m in parts:
+            if off != at:
+                return None
+            at += m
+        return [(key, off, m) for off, key, m in parts] if at == n and len(parts) > 1 else None
+
     def _set(self, t, v):
+        spans = self._spans(t)
+        if spans is not None:
+            for key, off, m in spans:
+                self.state[key] = np.array(v[off:off + m], np.float64)
+            return
         key, c0, shape = self._lookup(t)
         if c0 is None:
             self.state[key] = np.array(v, np.float64)
