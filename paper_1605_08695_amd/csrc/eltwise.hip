@@ -7,6 +7,8 @@
 // one element per thread otherwise.  Reductions are two-pass with a fixed
 // order, so results do not depend on scheduling.
 #include "common.h"
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace tfk {
@@ -110,23 +112,47 @@ __global__ __launch_bounds__(256) void relu_bwd_partial_kernel(const T *__restri
 #pragma unroll
         for (int e = 0; e < EPC; ++e) s[e] = 0.f;
         if (active) {
-            for (int64_t p = p0 + row; p < p1; p += R) {
+            if constexpr (VEC) {
+                // Four pixels per iteration, all loads issued before the first store (dpre may be
+                // dy itself, so the compiler cannot move a later pixel's loads above a store); the
+                // pixels are still summed in ascending order.
+                constexpr int U = 4;
+                for (int64_t p = p0 + row; p < p1; p += (int64_t)R * U) {
+                    U4 ly[U], ld[U];
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        const int64_t pp = p + (int64_t)u * R;
+                        if (pp < p1) {
+                            const int64_t off = pp * ys + (int64_t)cv * EPC;
+                            if (y != nullptr) ly[u] = *reinterpret_cast<const U4 *>(y + off);
+                            ld[u] = *reinterpret_cast<const U4 *>(dy + off);
+                        }
+                    }
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        const int64_t pp = p + (int64_t)u * R;
+                        if (pp >= p1) break;
+                        const int64_t off = pp * ys + (int64_t)cv * EPC;
+                        float fy[EPC], fd[EPC];
+                        if (y != nullptr) {
+                            chunk_to_f32<T>(ly[u], fy);
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < EPC; ++e) fy[e] = 1.f;
+                        }
+                        chunk_to_f32<T>(ld[u], fd);
+#pragma unroll
+                        for (int e = 0; e < EPC; ++e) {
+                            fd[e] = fy[e] > 0.f ? fd[e] : 0.f;
+                            s[e] += fd[e];
+                        }
+                        *reinterpret_cast<U4 *>(dpre + off) = f32_to_chunk<T>(fd);
+                    }
+                }
+            }
+            for (int64_t p = p0 + row; !VEC && p < p1; p += R) {
                 const int64_t off = p * ys + (int64_t)cv * EPC;
                 if constexpr (VEC) {
-                    float fy[EPC], fd[EPC];
-                    if (y != nullptr) {
-                        chunk_to_f32<T>(*reinterpret_cast<const U4 *>(y + off), fy);
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < EPC; ++e) fy[e] = 1.f;
-                    }
-                    chunk_to_f32<T>(*reinterpret_cast<const U4 *>(dy + off), fd);
-#pragma unroll
-                    for (int e = 0; e < EPC; ++e) {
-                        fd[e] = fy[e] > 0.f ? fd[e] : 0.f;
-                        s[e] += fd[e];
-                    }
-                    *reinterpret_cast<U4 *>(dpre + off) = f32_to_chunk<T>(fd);
                 } else {
                     const float fy = y != nullptr ? Elem<T>::load(y + off) : 1.f;
                     const float fd = fy > 0.f ? Elem<T>::load(dy + off) : 0.f;
@@ -405,10 +431,12 @@ __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const A *_
         else return self + e;
     };
     if constexpr (VEC) {
-        if (g.KH <= 2 * g.sh && g.KW <= 2 * g.sw) {
-            // At most 2 x 2 windows contain the element: issue every argmax and dy load of
-            // all four candidates first (clamped to a valid window, masked afterwards), so
-            // the gather costs one memory round trip instead of one or two per window.
+        // At most NC x NC windows contain the element (NC = 2: windows no larger than twice the
+        // stride; NC = 3: three times, e.g. 3 x 3 windows at stride 1): issue every argmax and dy
+        // load of all the candidates first (clamped to a valid window, masked afterwards), so the
+        // gather costs one memory round trip instead of one or two per window.
+        auto candidates = [&](auto NC_) __attribute__((always_inline)) {
+            constexpr int NC = decltype(NC_)::value;
             const int hp = h + g.pt, wp = w + g.pl;
             const int oh_lo = hp - g.KH + 1 <= 0 ? 0 : (hp - g.KH + 1 + g.sh - 1) / g.sh;
             const int oh_hi = min(g.OH - 1, hp / g.sh);
@@ -416,12 +444,12 @@ __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const A *_
             const int ow_hi = min(g.OW - 1, wp / g.sw);
             // (an element no window reaches has oh_lo > oh_hi; its loads go to the last window)
             const int ohc = min(oh_lo, g.OH - 1), owc = min(ow_lo, g.OW - 1);
-            int32_t ai[4][EPC];
-            U4 dv[4];
-            bool valid[4];
+            int32_t ai[NC * NC][EPC];
+            U4 dv[NC * NC];
+            bool valid[NC * NC];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int oh = oh_lo + (q >> 1), ow = ow_lo + (q & 1);
+            for (int q = 0; q < NC * NC; ++q) {
+                const int oh = oh_lo + q / NC, ow = ow_lo + q % NC;
                 valid[q] = oh <= oh_hi && ow <= ow_hi;
                 const int64_t opix = ((int64_t)n * g.OH + (valid[q] ? oh : ohc)) * g.OW + (valid[q] ? ow : owc);
                 arg_load<A, EPC>(argmax + opix * g.C + cv * EPC, ai[q]);
@@ -430,14 +458,21 @@ __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const A *_
 #pragma unroll
             for (int e = 0; e < EPC; ++e) s[e] = 0.f;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {             // windows in ascending output order
+            for (int q = 0; q < NC * NC; ++q) {       // windows in ascending output order
                 float v[EPC];
                 chunk_to_f32<T>(dv[q], v);
-                const int oh = oh_lo + (q >> 1), ow = ow_lo + (q & 1);
+                const int oh = oh_lo + q / NC, ow = ow_lo + q % NC;
 #pragma unroll
                 for (int e = 0; e < EPC; ++e)
                     if (valid[q] && ai[q][e] == want(oh, ow, e)) s[e] += v[e];
             }
+        };
+        if (g.KH <= 2 * g.sh && g.KW <= 2 * g.sw) {
+            candidates(std::integral_constant<int, 2>{});
+            return;
+        }
+        if (g.KH <= 3 * g.sh && g.KW <= 3 * g.sw) {
+            candidates(std::integral_constant<int, 3>{});
             return;
         }
     }
@@ -1136,6 +1171,25 @@ void relu_bwd_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *ppb) {
     *ppb = (P + g - 1) / g;
 }
 
+// Partial-sum grid of the standalone ReLU backward (shared with its workspace query): its pixel
+// loop batches the loads of four pixels, so a thread takes about 16 channel chunks, and never
+// fewer than 4 pixel rows (each block scatters C channel-major partials, which for wide tensors
+// cost more than a longer loop).
+void relu_bwd_only_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *ppb) {
+    const int EPC = dt == 0 ? 4 : 8;
+    const bool vec = C % EPC == 0 && ys % EPC == 0;
+    const int CV = vec ? C / EPC : C;
+    const int CVB = CV < 256 ? CV : 256;
+    const int R = 256 / CVB;
+    const int64_t rows = (P + R - 1) / R;
+    int64_t g = std::min((rows + 3) / 4, (P * CV + 256 * 16 - 1) / (256 * 16));
+    const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(4096, (1 << 22) / std::max(C, 1)));
+    if (g > cap) g = cap;
+    if (g < 1) g = 1;
+    *G = (int)g;
+    *ppb = (P + g - 1) / g;
+}
+
 template <typename T>
 static hipError_t relu_bwd_t(const void *y, const void *dy, void *dpre, int64_t P, int C, int64_t ys,
                              float *db, float *ws, hipStream_t st) {
@@ -1143,7 +1197,7 @@ static hipError_t relu_bwd_t(const void *y, const void *dy, void *dpre, int64_t 
     const bool vec = C % EPC == 0 && ys % EPC == 0 && aligned16(y) && aligned16(dy) && aligned16(dpre);
     int G;
     int64_t ppb;
-    relu_bwd_plan(sizeof(T) == 4 ? 0 : 1, P, C, ys, &G, &ppb);
+    relu_bwd_only_plan(sizeof(T) == 4 ? 0 : 1, P, C, ys, &G, &ppb);
     const int CV = vec ? C / EPC : C;
     const int CVB = CV < 256 ? CV : 256;
     const int R = 256 / CVB;

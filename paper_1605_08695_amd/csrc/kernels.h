@@ -91,6 +91,7 @@ hipError_t launch_conv_bwd_filter_band(const uint16_t *x4, const void *dy, int64
 
 hipError_t launch_bias_relu_fwd(int dt, void *y, int64_t P, int C, int64_t ys, const float *bias, hipStream_t st);
 void relu_bwd_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *ppb);
+void relu_bwd_only_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *ppb);
 hipError_t launch_bias_relu_bwd(int dt, const void *y, const void *dy, void *dpre, int64_t P, int C,
                                 int64_t ys, float *db, float *ws, hipStream_t st);
 // am: int32 dense-index argmax, or with taps the uint8 window tap kh * KW + kw.

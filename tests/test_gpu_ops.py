@@ -321,6 +321,10 @@ POOL_CASES = [
     ("alexnet_pool1", (2, 55, 55, 64), 3, 2, (0, 0, 0, 0)),
     ("same_3s2", (2, 28, 28, 192), 3, 2, (0, 1, 0, 1)),
     ("branch_3s1", (2, 6, 5, 8), 3, 1, (1, 1, 1, 1)),
+    # stride-1 3x3 pools: the backward gather loads its nine candidate windows at once; SAME and
+    # VALID padding
+    ("inception_3s1", (2, 14, 15, 48), 3, 1, (1, 1, 1, 1)),
+    ("valid_3s1", (3, 9, 7, 16), 3, 1, (0, 0, 0, 0)),
     ("odd_c", (2, 8, 8, 5), 2, 2, (0, 0, 0, 0)),
     ("vgg_2s2", (2, 14, 14, 128), 2, 2, (0, 0, 0, 0)),
     # trailing rows/columns that no window reaches (gradient 0 there)
