@@ -4,12 +4,20 @@
 
 namespace tfk {
 
+// Tile of the pipelined input-gradient kernel: at most 32 input channels take 32-channel tiles
+// (the filter operand is stored [row][k], so any multiple of 32 rows lays out; a 64-channel
+// tile would leave half of its MFMA rows empty), otherwise the shared rules.
+static Igemm2Tile bwd_data_tiles(int ni, int mj, int zdim) {
+    if (ni <= 32) return {32, 128, 4, 2};
+    return igemm2_tiles(ni, mj, zdim);
+}
+
 // Rows of bias-gradient partials of the fused ReLU-backward epilogue: one per block and wave
 // column of the pipelined kernel's grid.
 static int relu_partial_rows(const ConvShape &s) {
     const int mj = s.N * ((s.H + s.sh - 1) / s.sh) * ((s.W + s.sw - 1) / s.sw);
     const int z = s.sh * s.sw;
-    const Igemm2Tile t = igemm2_tiles(s.C, mj, z);
+    const Igemm2Tile t = bwd_data_tiles(s.C, mj, z);
     return z * ((mj + t.bj - 1) / t.bj) * (t.nw / 2);
 }
 
@@ -65,7 +73,7 @@ static hipError_t conv_bwd_data_t(const void *dy, int64_t dys, const void *w, vo
                 a.k_split = ks;
                 a.split_stride = (int64_t)mj * a.NI;
                 a.out = ws;
-                if (!igemm2_launch<DIR_BWD_DATA>(a, mj, sp, igemm2_tiles(a.NI, mj, sp), st))
+                if (!igemm2_launch<DIR_BWD_DATA>(a, mj, sp, bwd_data_tiles(a.NI, mj, sp), st))
                     return hipErrorInvalidValue;
                 const hipError_t e = hipGetLastError();
                 if (e != hipSuccess) return e;
@@ -93,7 +101,7 @@ static hipError_t conv_bwd_data_t(const void *dy, int64_t dys, const void *w, vo
                 *db_parts = a.db_rows;
                 *db_at = ws;
             }
-            if (!igemm2_launch<DIR_BWD_DATA>(a, mj, z, igemm2_tiles(a.NI, mj, z), st)) return hipErrorInvalidValue;
+            if (!igemm2_launch<DIR_BWD_DATA>(a, mj, z, bwd_data_tiles(a.NI, mj, z), st)) return hipErrorInvalidValue;
             return hipGetLastError();
         }
     }

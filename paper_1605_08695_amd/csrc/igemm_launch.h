@@ -75,6 +75,11 @@ static bool igemm2_launch(IgArgs &a, int mj, int zdim, const Igemm2Tile &t, hipS
     const int tiles_j = (mj + t.bj - 1) / t.bj;
     const dim3 grid((unsigned)(a.tiles_i * tiles_j), 1, (unsigned)zdim);
     const int key = ((t.bi / 64) << 12) | ((t.bj / 64) << 8) | (t.nw << 4) | t.ns;
+    if (t.bi == 32 && t.bj == 128 && t.nw == 4 && t.ns == 2) {
+        // (32-row I tiles: only the input gradient's [row][k] filter operand lays them out)
+        if constexpr (DIR != DIR_BWD_DATA) return false;
+        else { igemm2_go<DIR, 32, 128, 4, 2>(a, grid, st); return true; }
+    }
     if (t.bi == 128 && t.bj == 96 && t.nw == 4 && t.ns == 2) {
         // (96-row k-major tiles are not laid out: forward and bwd-input only)
         if constexpr (DIR == DIR_BWD_FILTER) return false;

@@ -63,6 +63,10 @@ CONV_CASES = [
     # fc8 (4096 -> 1000 logits), at batch 4
     ("fc6_6x6_window", 4, 6, 6, 256, 4096, 6, 6, 1, 1, (0, 0, 0, 0)),
     ("fc8_1x1_c4096_k1000", 4, 1, 1, 4096, 1000, 1, 1, 1, 1, (0, 0, 0, 0)),
+    # at most 32 input channels: 32-channel input-gradient tiles (a GoogLeNet 5x5 branch; a
+    # split reduction over few pixels)
+    ("5x5_c32_k96", 4, 14, 14, 32, 96, 5, 5, 1, 1, (2, 2, 2, 2)),
+    ("narrow_split_c24_k1024", 2, 4, 4, 24, 1024, 1, 1, 1, 1, (0, 0, 0, 0)),
 ]
 
 
@@ -110,7 +114,7 @@ def test_conv_three_directions(case, dtype):
 
 RELU_BWI_CASES = ["ragged_tiles", "3x3s2_valid", "3x3s2_pad_odd", "1x1s2_empty_phase", "5x5_cout192",
                   "alexnet_conv3_shape", "chunks_c192_uneven_pad", "c192_bwd_tiles", "bj96_tiles_bwd",
-                  "one_pixel_out_c64", "odd_channels",
+                  "one_pixel_out_c64", "odd_channels", "5x5_c32_k96", "narrow_split_c24_k1024",
                   # a fully connected layer at small batch: split-K partials, then the ReLU
                   # backward and the bias-gradient rows in the epilogue pass
                   "fc8_1x1_c4096_k1000"]
