@@ -4,13 +4,7 @@
 
 namespace tfk {
 
-// Tile of the pipelined input-gradient kernel: at most 32 input channels take 32-channel tiles
-// (the filter operand is stored [row][k], so any multiple of 32 rows lays out; a 64-channel
-// tile would leave half of its MFMA rows empty), otherwise the shared rules.
-static Igemm2Tile bwd_data_tiles(int ni, int mj, int zdim) {
-    if (ni <= 32) return {32, 128, 4, 2};
-    return igemm2_tiles(ni, mj, zdim);
-}
+static Igemm2Tile bwd_data_tiles(int ni, int mj, int zdim) { return igemm2_tiles_narrow(ni, mj, zdim); }
 
 // Rows of bias-gradient partials of the fused ReLU-backward epilogue: one per block and wave
 // column of the pipelined kernel's grid.

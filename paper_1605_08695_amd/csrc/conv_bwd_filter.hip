@@ -17,14 +17,15 @@ struct BwfPlan {
 // one full round of two blocks per CU (512 blocks): a last round with only a few blocks
 // costs a whole block time, and more splits only add partial-sum traffic (AlexNet conv2-5:
 // 357 us with four-block rounds, 297 us with this rule).  64-channel layers take 64 x 128
-// tiles.  (192-channel tiles, which pay in the forward pass, need more registers here than
-// two waves per SIMD have and spill.)
+// tiles, layers of at most 32 output channels 32 x 128.  (192-channel tiles, which pay in the
+// forward pass, need more registers here than two waves per SIMD have and spill.)
 BwfPlan bwf_plan(int dt, const ConvShape &s, bool v2) {
     BwfPlan p;
     const int bk = dt == 0 ? 32 : 64;
     const int m = s.KH * s.KW * s.C;
     if (v2) {
-        p.t = s.K > 64 ? Igemm2Tile{128, 128, 4, 2} : Igemm2Tile{64, 128, 4, 2};
+        p.t = s.K > 64 ? Igemm2Tile{128, 128, 4, 2}
+                       : (s.K > 32 ? Igemm2Tile{64, 128, 4, 2} : Igemm2Tile{32, 128, 4, 2});
         p.bi = p.t.bi;
         p.bj = p.t.bj;
     } else {

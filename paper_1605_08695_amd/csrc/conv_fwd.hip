@@ -43,7 +43,7 @@ static hipError_t conv_fwd_t(const void *x, int64_t xs, const void *w, void *y, 
                 a.k_split = ks;
                 a.split_stride = (int64_t)mj * a.NI;
                 a.out = ws;
-                if (!igemm2_launch<DIR_FWD>(a, mj, sp, igemm2_tiles(a.NI, mj, sp), st)) return hipErrorInvalidValue;
+                if (!igemm2_launch<DIR_FWD>(a, mj, sp, igemm2_tiles_narrow(a.NI, mj, sp), st)) return hipErrorInvalidValue;
                 const hipError_t e = hipGetLastError();
                 if (e != hipSuccess) return e;
                 SplitEpi ep{};
@@ -57,7 +57,7 @@ static hipError_t conv_fwd_t(const void *x, int64_t xs, const void *w, void *y, 
                 ep.bias = bias;
                 return launch_split_epilogue(ep, st);
             }
-            if (!igemm2_launch<DIR_FWD>(a, mj, 1, igemm2_tiles(a.NI, mj, 1), st)) return hipErrorInvalidValue;
+            if (!igemm2_launch<DIR_FWD>(a, mj, 1, igemm2_tiles_narrow(a.NI, mj, 1), st)) return hipErrorInvalidValue;
             return hipGetLastError();
         }
     }

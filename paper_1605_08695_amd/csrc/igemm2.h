@@ -122,11 +122,13 @@ __device__ __forceinline__ U4 lds_tr_pair(const unsigned char *p0, const unsigne
 // group to the free chunk pairs instead).  192-row k-rows are 384 bytes, so consecutive
 // k-rows start alternately at bank 0 and bank 32: bit 1 of k moves k-rows 2 and 3 of a
 // group by one chunk pair and bit 3 of k the second group by two, which keeps every chunk
-// inside its aligned group of eight.
+// inside its aligned group of eight.  32-row k-rows are 64 bytes: the 4 k-rows of a group already
+// cover every bank once, and bit 3 of k moves the second group to the other chunk pair.
 template <int R>
 __device__ __forceinline__ int kmajor_swz(int k) {
-    static_assert(R == 64 || R == 128 || R == 192 || R == 256, "k-major tile rows");
-    if constexpr (R == 64) return ((k & 3) ^ ((k >> 3) & 1)) << 1;
+    static_assert(R == 32 || R == 64 || R == 128 || R == 192 || R == 256, "k-major tile rows");
+    if constexpr (R == 32) return ((k >> 3) & 1) << 1;
+    else if constexpr (R == 64) return ((k & 3) ^ ((k >> 3) & 1)) << 1;
     else if constexpr (R != 192) return ((k & 3) << 1) ^ (((k >> 3) & 1) << 3);
     else return (((k >> 1) & 1) << 1) | (((k >> 3) & 1) << 2);
 }

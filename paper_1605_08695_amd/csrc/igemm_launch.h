@@ -63,6 +63,13 @@ static inline Igemm2Tile igemm2_tiles(int ni, int mj, int zdim) {
     return {64, 128, 4, 2};
 }
 
+// At most 32 output rows (channels) on the I side: 32-row tiles, which keep every MFMA row in use
+// (a 64-row tile would compute half or more of its rows for nothing).
+static inline Igemm2Tile igemm2_tiles_narrow(int ni, int mj, int zdim) {
+    if (ni <= 32) return {32, 128, 4, 2};
+    return igemm2_tiles(ni, mj, zdim);
+}
+
 template <int DIR, int BI, int BJ, int NW, int NS>
 static void igemm2_go(const IgArgs &a, dim3 grid, hipStream_t st) {
     hipLaunchKernelGGL((igemm2_kernel<DIR, BI, BJ, NW, NS>), grid, dim3(NW * 64), 0, st, a);
@@ -76,9 +83,8 @@ static bool igemm2_launch(IgArgs &a, int mj, int zdim, const Igemm2Tile &t, hipS
     const dim3 grid((unsigned)(a.tiles_i * tiles_j), 1, (unsigned)zdim);
     const int key = ((t.bi / 64) << 12) | ((t.bj / 64) << 8) | (t.nw << 4) | t.ns;
     if (t.bi == 32 && t.bj == 128 && t.nw == 4 && t.ns == 2) {
-        // (32-row I tiles: only the input gradient's [row][k] filter operand lays them out)
-        if constexpr (DIR != DIR_BWD_DATA) return false;
-        else { igemm2_go<DIR, 32, 128, 4, 2>(a, grid, st); return true; }
+        igemm2_go<DIR, 32, 128, 4, 2>(a, grid, st);
+        return true;
     }
     if (t.bi == 128 && t.bj == 96 && t.nw == 4 && t.ns == 2) {
         // (96-row k-major tiles are not laid out: forward and bwd-input only)
