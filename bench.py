@@ -23,6 +23,7 @@ launches every op in order on one stream.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -122,6 +123,44 @@ def recorded_traffic(kind):
 UPDATE_BYTES = {"sgd": 4 + 4 + 4 + 2, "momentum": 12 + 8 + 2, "adam": 16 + 12 + 2}
 
 
+class HipEvent:
+    """A timing event recorded without the system-scope fence (hipEventDisableSystemFence, the flag
+    HIP gives events that only time work).  An ordinary event's fence writes back and invalidates
+    the caches when it is reached, which also slows the work enqueued after it.  Same interface as
+    torch.cuda.Event for what is used here: record(stream) and elapsed_time(end) in ms."""
+    _hip = None
+
+    def __init__(self):
+        if HipEvent._hip is None:
+            # the HIP runtime torch has loaded (the library's kernels run on the same one)
+            path = next(l.split()[-1] for l in open("/proc/self/maps") if "libamdhip64" in l)
+            h = ctypes.CDLL(path)
+            h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            HipEvent._hip = h
+        self.e = ctypes.c_void_p()
+        if HipEvent._hip.hipEventCreateWithFlags(ctypes.byref(self.e), 0x20000000) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
+
+    def record(self, stream=None):
+        import torch
+        st = stream if stream is not None else torch.cuda.current_stream()
+        if HipEvent._hip.hipEventRecord(self.e, ctypes.c_void_p(st.cuda_stream)) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_time(self, end):
+        ms = ctypes.c_float()
+        if HipEvent._hip.hipEventElapsedTime(ctypes.byref(ms), self.e, end.e) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def __del__(self):
+        if self.e.value and HipEvent._hip is not None:
+            HipEvent._hip.hipEventDestroy(self.e)
+
+
 def time_updates(torch, ops, n, reps=20):
     """Average launch time of each update over n fp32 variables (HIP events on the current stream)."""
     dev = "cuda"
@@ -139,7 +178,7 @@ def time_updates(torch, ops, n, reps=20):
     for name, fn in calls.items():
         for t in range(1, 4):
             fn(t)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0, e1 = HipEvent(), HipEvent()
         e0.record()
         for t in range(4, 4 + reps):
             fn(t)
@@ -177,7 +216,7 @@ class EventTrace:
         return stream if stream is not None else self.torch.cuda.current_stream()
 
     def _event(self, stream):
-        e = self.torch.cuda.Event(enable_timing=True)
+        e = HipEvent()
         e.record(self._stream(stream))
         return e
 
@@ -202,7 +241,7 @@ def sleep_cycles_for(torch, us):
     """Spin-kernel cycles that take about ``us`` microseconds on this GPU (measured)."""
     torch.cuda._sleep(1000)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0, e1 = HipEvent(), HipEvent()
     n = 200000
     e0.record()
     torch.cuda._sleep(n)
@@ -265,7 +304,7 @@ def measure_sampled(args, torch, W):
     def timed(fn, reps=10):
         for _ in range(3):
             fn()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0, e1 = HipEvent(), HipEvent()
         e0.record()
         for _ in range(reps):
             fn()
@@ -340,7 +379,7 @@ def gemm_reference(net, torch):
         for _ in range(3):
             fn()
         torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a, b = HipEvent(), HipEvent()
         a.record()
         for _ in range(it):
             fn()
@@ -405,7 +444,7 @@ def time_back_to_back(torch, calls, pad, reps=20):
         fn(*a, **k)
         torch.cuda.synchronize()
         torch.cuda._sleep(pad)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0, e1 = HipEvent(), HipEvent()
         e0.record()
         for _ in range(reps):
             fn(*a, **k)
@@ -548,17 +587,22 @@ def main():
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
-    step_ms = []
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
+    # The K timed steps run back to back with nothing between them; a timing event records with a
+    # system-scope fence (a cache write-back and invalidation that also slows the work after it),
+    # so the per-step distribution (median, p10, p90) comes from K more steps, each bracketed by
+    # events, after the timed region.
     t0 = time.perf_counter()
+    for i in range(args.steps):
+        run()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    ev = [HipEvent() for _ in range(args.steps + 1)]
     ev[0].record()
     for i in range(args.steps):
         run()
         ev[i + 1].record()
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
     step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
     print("bench: timed %d steps, %.3f ms/step (median %.3f)" % (args.steps, ms_per_step, np.median(step_ms)),
           file=sys.stderr, flush=True)
