@@ -69,6 +69,8 @@ static hipError_t conv_fwd_t(const void *x, int64_t xs, const void *w, void *y, 
 // pixels (at most bj), consecutive bands start step = q * psh rows apart (sharing the rows
 // their windows overlap on), and enough bands run to cover every pool row and every output row.
 namespace {
+constexpr int64_t kFusedPoolCUs = 256;  // MI355X compute units
+
 struct BandPlan {
     int bj, q, rows, step, bands;
 };
@@ -118,6 +120,17 @@ bool conv_fwd_pool_fused(const void *x, int64_t xs, const void *w, void *y, int6
     // conv5 + pool5, 13 x 13, one band of 169 of 192 rows: 42.6 -> 41.3 us; conv2 + pool2, 27 x 27,
     // 5 bands of 189 of 192 rows with a shared row between bands, 32 % more rows: 84 -> 118 us).
     if ((int64_t)best.bands * best.bj * 100 > (int64_t)s.OH * s.OW * 115) return false;
+    // and only when the unfused convolution runs as one round of two blocks per CU, whose last
+    // blocks set its time and absorb the extra rows: over several rounds they add their share to
+    // every round and cost more than the separate pool pass (VGG-16 b64, conv7 + pool3, 56 x 56 x
+    // 256, and conv10 + pool4, 28 x 28 x 512, each 14 % more rows: 298 -> 364 and 287 -> 341 us
+    // fused with 64-channel tiles, 322 and 292 us with 128-channel tiles)
+    {
+        const int mj_plain = s.N * s.OH * s.OW;
+        const Igemm2Tile pt = igemm2_tiles_narrow(s.K, mj_plain, 1);
+        const int64_t blocks = (int64_t)((s.K + pt.bi - 1) / pt.bi) * ((mj_plain + pt.bj - 1) / pt.bj);
+        if (blocks > 2 * kFusedPoolCUs) return false;
+    }
     IgArgs a;
     fill_geom(a, s);
     a.src_i = w;

@@ -630,9 +630,10 @@ CONV_POOL_CASES = [
     ("ragged_channels", (2, 13, 13, 64), 72, (3, 1, (1, 1, 1, 1)), (3, 2, (0, 0, 0, 0)), torch.bfloat16, False),
     ("pool_into_channel_slice", (2, 13, 13, 64), 128, (3, 1, (1, 1, 1, 1)), (3, 2, (0, 0, 0, 0)), torch.bfloat16,
      True),
-    # two kernels: too many recomputed rows (AlexNet conv2 + pool2), rows too wide for a band, a
-    # padded pool, fp32
+    # two kernels: too many recomputed rows (AlexNet conv2 + pool2), a grid of several rounds of
+    # blocks (588 128 x 128 tiles), rows too wide for a band, a padded pool, fp32
     ("alexnet_conv2_pool2", (3, 27, 27, 64), 192, (5, 1, (2, 2, 2, 2)), (3, 2, (0, 0, 0, 0)), torch.bfloat16, False),
+    ("several_rounds", (24, 56, 56, 16), 128, (3, 1, (1, 1, 1, 1)), (2, 2, (0, 0, 0, 0)), torch.bfloat16, False),
     ("wide_rows", (2, 10, 100, 32), 64, (3, 1, (1, 1, 1, 1)), (3, 2, (0, 0, 0, 0)), torch.bfloat16, False),
     ("same_pool", (2, 14, 14, 32), 64, (3, 1, (1, 1, 1, 1)), (3, 2, (0, 1, 0, 1)), torch.bfloat16, False),
     ("f32", (2, 13, 13, 32), 64, (3, 1, (1, 1, 1, 1)), (3, 2, (0, 0, 0, 0)), torch.float32, False),
