@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 12
+#define TFK_ABI_VERSION 13
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -305,22 +305,36 @@ TFK_API tfk_status tfk_maxpool_bwd_taps(const void *dy, const uint8_t *taps, tfk
  *   dbias[c] = sum over the pixels of dpre[., c]  (of the stored values; fp32)
  * It equals tfk_maxpool_bwd(dy, argmax, ..., dx = dpre, beta) followed by
  * tfk_bias_relu_bwd(y, dpre, ...), with the pool gradient rounded once instead of twice.
+ * When beta = 0 the mask can come from the pool's output instead of y: an element receives
+ * gradient only from windows whose argmax it is, and each such window's output is exactly the
+ * element's value, so routing +0 from windows whose output is not positive gives the same
+ * dpre, bit for bit, without reading y (a quarter of the bytes for a 2x2- or 3x3-stride-2 pool).
  *   dy, argmax, yd, p : the max-pool's output gradient, its tfk_maxpool_fwd argmax and window.
- *   y     : xd-shaped pool input (the ReLU output), element type dt; read only.
+ *   y     : xd-shaped pool input (the ReLU output), element type dt; read only.  Not read, and
+ *           may be NULL, when py is used.
+ *   py, py_stride : NULL, or the pool's output that argmax was selected with (yd-shaped, pixel
+ *           stride py_stride >= yd.c elements, element type dt; read only).  Used when beta = 0;
+ *           ignored when beta = 1 (the stored gradient then needs y's mask at every element).
  *   dpre  : xd-shaped, written (read first when beta = 1, which adds the gradient the other
- *           consumers of y already stored there); must not overlap y, dy or argmax.
+ *           consumers of y already stored there); must not overlap y, py, dy or argmax.
  *   dbias : xd.c fp32 values, overwritten.
  *   ws    : at least tfk_bias_relu_bwd_workspace_bytes(xd, dt) bytes.
  * Requirements: beta is 0 or 1; xd.c <= 16384.  xd.n == 0 sets dbias to 0.
+ * Errors: NULL (dy, argmax, dpre, dbias, or y where it is read), SHAPE (pool geometry,
+ * xd.c > 16384, py_stride < yd.c), ARG (beta), ALIGN (element alignment), ALIAS (the overlaps
+ * above), WORKSPACE (ws too small).
  */
 TFK_API tfk_status tfk_maxpool_bwd_relu_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p,
-                                    tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd, float beta,
-                                    float *dbias, void *ws, size_t ws_bytes, void *stream);
+                                    tfk_dtype dt, const void *y, const void *py, int64_t py_stride,
+                                    void *dpre, tfk_nhwc xd, float beta, float *dbias, void *ws,
+                                    size_t ws_bytes, void *stream);
 /* tfk_maxpool_bwd_relu_bwd (Section 5 fused activation gradient, Section 6.1 pooling) with the
- * selection from tfk_maxpool_fwd_taps. */
+ * selection from tfk_maxpool_fwd_taps (py: the output of that call, or of
+ * tfk_conv2d_fwd_bias_relu_maxpool). */
 TFK_API tfk_status tfk_maxpool_bwd_relu_bwd_taps(const void *dy, const uint8_t *taps, tfk_nhwc yd, tfk_window p,
-                                         tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd, float beta,
-                                         float *dbias, void *ws, size_t ws_bytes, void *stream);
+                                         tfk_dtype dt, const void *y, const void *py, int64_t py_stride,
+                                         void *dpre, tfk_nhwc xd, float beta, float *dbias, void *ws,
+                                         size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------- update
  * ApplyGradientDescent, in place (Section 4.1: W' = W - alpha * dL/dW written

@@ -74,7 +74,7 @@ def load(path: str = LIB_PATH):
     lib.tfk_bias_relu_bwd_workspace_bytes.restype = sz
     lib.tfk_maxpool_fwd.argtypes = [vp, Nhwc, Window, st, vp, Nhwc, vp, vp]
     lib.tfk_maxpool_bwd.argtypes = [vp, vp, Nhwc, Window, st, vp, Nhwc, f32, vp]
-    lib.tfk_maxpool_bwd_relu_bwd.argtypes = [vp, vp, Nhwc, Window, st, vp, vp, Nhwc, f32, vp, vp, sz, vp]
+    lib.tfk_maxpool_bwd_relu_bwd.argtypes = [vp, vp, Nhwc, Window, st, vp, vp, i64, vp, Nhwc, f32, vp, vp, sz, vp]
     lib.tfk_maxpool_fwd_taps.argtypes = lib.tfk_maxpool_fwd.argtypes
     lib.tfk_maxpool_bwd_taps.argtypes = lib.tfk_maxpool_bwd.argtypes
     lib.tfk_maxpool_bwd_relu_bwd_taps.argtypes = lib.tfk_maxpool_bwd_relu_bwd.argtypes

@@ -629,8 +629,9 @@ tfk_status tfk_maxpool_bwd_taps(const void *dy, const uint8_t *taps, tfk_nhwc yd
 }
 
 static tfk_status maxpool_relu_bwd_impl(const void *dy, const void *argmax, bool taps, tfk_nhwc yd, tfk_window p,
-                                        tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd, float beta,
-                                        float *dbias, void *ws, size_t ws_bytes, void *stream) {
+                                        tfk_dtype dt, const void *y, const void *py, int64_t py_stride, void *dpre,
+                                        tfk_nhwc xd, float beta, float *dbias, void *ws, size_t ws_bytes,
+                                        void *stream) {
     PoolGeom g;
     TRY(check_pool(xd, p, dt, yd, "y", "dy", g));
     if (!(beta == 0.f || beta == 1.f)) return fail(TFK_ERR_ARG, "beta must be 0 or 1");
@@ -643,42 +644,54 @@ static tfk_status maxpool_relu_bwd_impl(const void *dy, const void *argmax, bool
     const int64_t es = esize(dt);
     TRY(need_ptr(dy, "dy"));
     TRY(need_ptr(argmax, "argmax"));
-    TRY(need_ptr(y, "y"));
+    // the pool's output replaces y as the mask when the gradient is not accumulated
+    if (beta != 0.f) py = nullptr;
+    if (py == nullptr) TRY(need_ptr(y, "y"));
+    else y = nullptr;
     TRY(need_ptr(dpre, "dpre"));
     TRY(need_align(dy, es, "dy"));
     TRY(need_align(y, es, "y"));
+    TRY(need_align(py, es, "py"));
     TRY(need_align(dpre, es, "dpre"));
     TRY(need_align(argmax, taps ? 1 : 4, "argmax"));
-    const int64_t xb = view_bytes(xd, es), yb = view_bytes(yd, es);
+    tfk_nhwc pyd = yd;
+    pyd.pixel_stride = py_stride;
+    if (py != nullptr && py_stride < yd.c) return fail(TFK_ERR_SHAPE, "py_stride is below the channel count");
+    const int64_t xb = view_bytes(xd, es), yb = view_bytes(yd, es), pb = py ? view_bytes(pyd, es) : 0;
     const int64_t ab = (int64_t)yd.n * yd.h * yd.w * yd.c * (taps ? 1 : 4), bb = (int64_t)xd.c * 4;
-    if (overlap(dpre, xb, y, xb) || overlap(dpre, xb, dy, yb) || overlap(dpre, xb, argmax, ab))
-        return fail(TFK_ERR_ALIAS, "dpre overlaps y, dy or argmax");
+    if (overlap(dpre, xb, y, xb) || overlap(dpre, xb, dy, yb) || overlap(dpre, xb, argmax, ab) ||
+        overlap(dpre, xb, py, pb))
+        return fail(TFK_ERR_ALIAS, "dpre overlaps y, py, dy or argmax");
     if (overlap(dbias, bb, y, xb) || overlap(dbias, bb, dy, yb) || overlap(dbias, bb, dpre, xb) ||
-        overlap(dbias, bb, argmax, ab))
+        overlap(dbias, bb, argmax, ab) || overlap(dbias, bb, py, pb))
         return fail(TFK_ERR_ALIAS, "dbias overlaps a tensor");
     const size_t need = tfk_bias_relu_bwd_workspace_bytes(xd, dt);
     TRY(check_ws(ws, ws_bytes, need));
     if (overlap(ws, (int64_t)need, y, xb) || overlap(ws, (int64_t)need, dy, yb) ||
         overlap(ws, (int64_t)need, dpre, xb) || overlap(ws, (int64_t)need, dbias, bb) ||
-        overlap(ws, (int64_t)need, argmax, ab))
+        overlap(ws, (int64_t)need, argmax, ab) || overlap(ws, (int64_t)need, py, pb))
         return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
-    return hip_status(launch_maxpool_relu_bwd(dt == TFK_F32 ? 0 : 1, dy, argmax, taps, g, y, dpre, beta, dbias,
-                                              (float *)ws, st),
+    return hip_status(launch_maxpool_relu_bwd(dt == TFK_F32 ? 0 : 1, dy, argmax, taps, g, y, py, py_stride, dpre,
+                                              beta, dbias, (float *)ws, st),
                       "maxpool_bwd_relu_bwd");
 }
 
 tfk_status tfk_maxpool_bwd_relu_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
-                                    const void *y, void *dpre, tfk_nhwc xd, float beta, float *dbias, void *ws,
-                                    size_t ws_bytes, void *stream) {
-    RECORDED(tfk_maxpool_bwd_relu_bwd, dy, argmax, yd, p, dt, y, dpre, xd, beta, dbias, ws, ws_bytes, stream);
-    return maxpool_relu_bwd_impl(dy, argmax, false, yd, p, dt, y, dpre, xd, beta, dbias, ws, ws_bytes, stream);
+                                    const void *y, const void *py, int64_t py_stride, void *dpre, tfk_nhwc xd,
+                                    float beta, float *dbias, void *ws, size_t ws_bytes, void *stream) {
+    RECORDED(tfk_maxpool_bwd_relu_bwd, dy, argmax, yd, p, dt, y, py, py_stride, dpre, xd, beta, dbias, ws, ws_bytes,
+             stream);
+    return maxpool_relu_bwd_impl(dy, argmax, false, yd, p, dt, y, py, py_stride, dpre, xd, beta, dbias, ws, ws_bytes,
+                                 stream);
 }
 
 tfk_status tfk_maxpool_bwd_relu_bwd_taps(const void *dy, const uint8_t *taps, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
-                                         const void *y, void *dpre, tfk_nhwc xd, float beta, float *dbias, void *ws,
-                                         size_t ws_bytes, void *stream) {
-    RECORDED(tfk_maxpool_bwd_relu_bwd_taps, dy, taps, yd, p, dt, y, dpre, xd, beta, dbias, ws, ws_bytes, stream);
-    return maxpool_relu_bwd_impl(dy, taps, true, yd, p, dt, y, dpre, xd, beta, dbias, ws, ws_bytes, stream);
+                                         const void *y, const void *py, int64_t py_stride, void *dpre, tfk_nhwc xd,
+                                         float beta, float *dbias, void *ws, size_t ws_bytes, void *stream) {
+    RECORDED(tfk_maxpool_bwd_relu_bwd_taps, dy, taps, yd, p, dt, y, py, py_stride, dpre, xd, beta, dbias, ws,
+             ws_bytes, stream);
+    return maxpool_relu_bwd_impl(dy, taps, true, yd, p, dt, y, py, py_stride, dpre, xd, beta, dbias, ws, ws_bytes,
+                                 stream);
 }
 
 // ------------------------------------------------------------------ SGD

@@ -36,6 +36,16 @@ __device__ __forceinline__ void chunk_to_f32(const U4 &v, float *f) {
     }
 }
 
+// v[e] <- +0 where element e of the chunk m is not positive (the ReLU gradient mask)
+template <typename T>
+__device__ __forceinline__ void relu_mask(const U4 &m, float *v) {
+    constexpr int EPC = Elem<T>::kPerChunk;
+    float f[EPC];
+    chunk_to_f32<T>(m, f);
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) v[e] = f[e] > 0.f ? v[e] : 0.f;
+}
+
 template <typename T>
 __device__ __forceinline__ U4 f32_to_chunk(const float *f) {
     U4 v;
@@ -419,10 +429,13 @@ __global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restric
 // pix * C + cv * EPC + e, pixel pix = (n, h, w) of the pool input.
 // (A: argmax format.  Element e of the chunk matches window (oh, ow) when the window's stored
 // value is self + e (dense index) or this pixel's tap in that window (tap index).)
+// py (optional, pixel stride pys): the pool's output; a window whose output element is not
+// positive routes +0 instead of its dy (the ReLU mask of the element its argmax names, whose
+// value the window's output is).
 template <typename T, bool VEC, typename A>
 __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const A *__restrict__ argmax,
                                             const PoolGeom &g, int n, int h, int w, int64_t pix, int cv,
-                                            float *s) {
+                                            float *s, const T *__restrict__ py = nullptr, int64_t pys = 0) {
     constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
     constexpr bool TAP = sizeof(A) == 1;
     const int32_t self = (int32_t)(pix * g.C + cv * EPC);
@@ -445,7 +458,7 @@ __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const A *_
             // (an element no window reaches has oh_lo > oh_hi; its loads go to the last window)
             const int ohc = min(oh_lo, g.OH - 1), owc = min(ow_lo, g.OW - 1);
             int32_t ai[NC * NC][EPC];
-            U4 dv[NC * NC];
+            U4 dv[NC * NC], pv[NC * NC];
             bool valid[NC * NC];
 #pragma unroll
             for (int q = 0; q < NC * NC; ++q) {
@@ -454,6 +467,7 @@ __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const A *_
                 const int64_t opix = ((int64_t)n * g.OH + (valid[q] ? oh : ohc)) * g.OW + (valid[q] ? ow : owc);
                 arg_load<A, EPC>(argmax + opix * g.C + cv * EPC, ai[q]);
                 dv[q] = *reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC);
+                if (py) pv[q] = *reinterpret_cast<const U4 *>(py + opix * pys + cv * EPC);
             }
 #pragma unroll
             for (int e = 0; e < EPC; ++e) s[e] = 0.f;
@@ -461,6 +475,7 @@ __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const A *_
             for (int q = 0; q < NC * NC; ++q) {       // windows in ascending output order
                 float v[EPC];
                 chunk_to_f32<T>(dv[q], v);
+                if (py) relu_mask<T>(pv[q], v);
                 const int oh = oh_lo + q / NC, ow = ow_lo + q % NC;
 #pragma unroll
                 for (int e = 0; e < EPC; ++e)
@@ -496,12 +511,14 @@ __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const A *_
                 if (any) {
                     float v[EPC];
                     chunk_to_f32<T>(*reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC), v);
+                    if (py) relu_mask<T>(*reinterpret_cast<const U4 *>(py + opix * pys + cv * EPC), v);
 #pragma unroll
                     for (int e = 0; e < EPC; ++e)
                         if (ai[e] == want(oh, ow, e)) s[e] += v[e];
                 }
             } else {
-                if ((int32_t)argmax[opix * g.C + cv] == want(oh, ow, 0)) s[0] += Elem<T>::load(dy + opix * g.ys + cv);
+                if ((int32_t)argmax[opix * g.C + cv] == want(oh, ow, 0))
+                    s[0] += py && !(Elem<T>::load(py + opix * pys + cv) > 0.f) ? 0.f : Elem<T>::load(dy + opix * g.ys + cv);
             }
         }
     }
@@ -544,10 +561,14 @@ __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T *__restrict__ 
 // relu_bwd_partial_kernel: block b owns pixels [b ppb, (b+1) ppb), thread t channel chunk
 // t % CVB (+ CVB ...) and pixel rows t / CVB (+ R ...); db sums the stored (rounded) dpre,
 // the tensor the filter gradient is formed from.
+// With py (the pool's output, pixel stride pys; beta = 0 only) the mask is taken per window
+// from it instead of per element from y, which is not read: an element receives gradient only
+// from windows whose argmax it is, and each such window's output is the element's value.
 template <typename T, bool VEC, typename A>
 __global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *__restrict__ dy,
                                                                        const A *__restrict__ argmax,
-                                                                       PoolGeom g, const T *__restrict__ y, T *dpre,
+                                                                       PoolGeom g, const T *__restrict__ y,
+                                                                       const T *__restrict__ py, int64_t pys, T *dpre,
                                                                        float beta, int64_t ppb, FastDiv dW, FastDiv dH,
                                                                        float *__restrict__ partial) {
     constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
@@ -573,19 +594,16 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *
                 dW.divmod((uint32_t)p, q, w);
                 dH.divmod(q, n, h);
                 float s[EPC];
-                pool_gather<T, VEC, A>(dy, argmax, g, (int)n, (int)h, (int)w, p, cv, s);
+                pool_gather<T, VEC, A>(dy, argmax, g, (int)n, (int)h, (int)w, p, cv, s, py, pys);
                 const int64_t off = p * g.xs + (int64_t)cv * EPC;
                 if constexpr (VEC) {
-                    float fy[EPC];
-                    chunk_to_f32<T>(*reinterpret_cast<const U4 *>(y + off), fy);
                     if (beta != 0.f) {
                         float o[EPC];
                         chunk_to_f32<T>(*reinterpret_cast<const U4 *>(dpre + off), o);
 #pragma unroll
                         for (int e = 0; e < EPC; ++e) s[e] += beta * o[e];
                     }
-#pragma unroll
-                    for (int e = 0; e < EPC; ++e) s[e] = fy[e] > 0.f ? s[e] : 0.f;
+                    if (!py) relu_mask<T>(*reinterpret_cast<const U4 *>(y + off), s);
                     const U4 packed = f32_to_chunk<T>(s);
                     *reinterpret_cast<U4 *>(dpre + off) = packed;
                     float st[EPC];
@@ -594,7 +612,7 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *
                     for (int e = 0; e < EPC; ++e) acc[e] += st[e];
                 } else {
                     if (beta != 0.f) s[0] += beta * Elem<T>::load(dpre + off);
-                    const float v = Elem<T>::load(y + off) > 0.f ? s[0] : 0.f;
+                    const float v = py || Elem<T>::load(y + off) > 0.f ? s[0] : 0.f;
                     Elem<T>::store(dpre + off, v);
                     acc[0] += Elem<T>::load(dpre + off);
                 }
@@ -620,10 +638,14 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *
 // Bias-gradient partials as in maxpool_relu_bwd_partial_kernel, over cells instead of pixels.
 // PK > 0: the windows are PK x PK (a compile-time size, so the window/pixel pairs that can never
 // match are dropped: 9 of 16 remain for 3 x 3); PK = 0: the size comes from g.
+// py: as in maxpool_relu_bwd_partial_kernel (the four windows' outputs replace the four pixels'
+// y as the mask).
 template <typename T, typename A, int PK>
 __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__restrict__ dy,
                                                                     const A *__restrict__ argmax, PoolGeom g,
-                                                                    const T *__restrict__ y, T *dpre, float beta,
+                                                                    const T *__restrict__ y,
+                                                                    const T *__restrict__ py, int64_t pys,
+                                                                    T *dpre, float beta,
                                                                     int64_t cpb, int CH, int CW, FastDiv dCW,
                                                                     FastDiv dCH, float *__restrict__ partial) {
     constexpr int EPC = Elem<T>::kPerChunk;
@@ -650,7 +672,7 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
                 dCH.divmod(q, n, ch);
                 // the (up to) four windows, in ascending output order
                 int32_t ai[4][EPC];
-                U4 dv[4];
+                U4 dv[4], pv[4];
                 bool wok[4];
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
@@ -659,6 +681,7 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
                     const int64_t opix = ((int64_t)n * g.OH + (wok[k] ? oh : 0)) * g.OW + (wok[k] ? ow : 0);
                     arg_load<A, EPC>(argmax + opix * g.C + cv * EPC, ai[k]);
                     dv[k] = *reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC);
+                    if (py) pv[k] = *reinterpret_cast<const U4 *>(py + opix * pys + cv * EPC);
                 }
                 // the four pixels of the cell
                 int64_t pix[4];
@@ -669,7 +692,7 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
                     const int h = 2 * (int)ch - g.pt + (m >> 1), w = 2 * (int)cw - g.pl + (m & 1);
                     pok[m] = (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
                     pix[m] = ((int64_t)n * g.H + (pok[m] ? h : 0)) * g.W + (pok[m] ? w : 0);
-                    yv[m] = *reinterpret_cast<const U4 *>(y + pix[m] * g.xs + cv * EPC);
+                    if (!py) yv[m] = *reinterpret_cast<const U4 *>(y + pix[m] * g.xs + cv * EPC);
                     if (beta != 0.f) ov[m] = *reinterpret_cast<const U4 *>(dpre + pix[m] * g.xs + cv * EPC);
                 }
                 float s[4][EPC];
@@ -681,6 +704,7 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
                 for (int k = 0; k < 4; ++k) {
                     float v[EPC];
                     chunk_to_f32<T>(dv[k], v);
+                    if (py) relu_mask<T>(pv[k], v);
 #pragma unroll
                     for (int m = 0; m < 4; ++m) {
                         // pixel m is tap (2 (1 - k/2) + m/2, 2 (1 - k%2) + m%2) of window k
@@ -697,16 +721,13 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
 #pragma unroll
                 for (int m = 0; m < 4; ++m) {
                     if (!pok[m]) continue;
-                    float fy[EPC];
-                    chunk_to_f32<T>(yv[m], fy);
                     if (beta != 0.f) {
                         float o[EPC];
                         chunk_to_f32<T>(ov[m], o);
 #pragma unroll
                         for (int e = 0; e < EPC; ++e) s[m][e] += beta * o[e];
                     }
-#pragma unroll
-                    for (int e = 0; e < EPC; ++e) s[m][e] = fy[e] > 0.f ? s[m][e] : 0.f;
+                    if (!py) relu_mask<T>(yv[m], s[m]);
                     const U4 packed = f32_to_chunk<T>(s[m]);
                     *reinterpret_cast<U4 *>(dpre + pix[m] * g.xs + cv * EPC) = packed;
                     float st[EPC];
@@ -1219,11 +1240,12 @@ hipError_t launch_bias_relu_bwd(int dt, const void *y, const void *dy, void *dpr
 }
 
 template <typename T, typename A>
-static hipError_t maxpool_relu_bwd_t(const void *dy, const A *am, const PoolGeom &g, const void *y, void *dpre,
-                                     float beta, float *db, float *ws, hipStream_t st) {
+static hipError_t maxpool_relu_bwd_t(const void *dy, const A *am, const PoolGeom &g, const void *y,
+                                     const void *py, int64_t pys, void *dpre, float beta, float *db, float *ws,
+                                     hipStream_t st) {
     constexpr int EPC = Elem<T>::kPerChunk;
     const bool vec = g.C % EPC == 0 && g.xs % EPC == 0 && g.ys % EPC == 0 && aligned16(dy) && aligned16(am) &&
-                     aligned16(y) && aligned16(dpre);
+                     (py ? pys % EPC == 0 && aligned16(py) : aligned16(y)) && aligned16(dpre);
     const int64_t P = (int64_t)g.N * g.H * g.W;
     int G;
     int64_t ppb;
@@ -1245,33 +1267,34 @@ static hipError_t maxpool_relu_bwd_t(const void *dy, const A *am, const PoolGeom
         const FastDiv dCW((uint32_t)CW), dCH((uint32_t)CH);
         if (g.KH == 3 && g.KW == 3)
             hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A, 3>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am,
-                               g, (const T *)y, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
+                               g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
         else if (g.KH == 2 && g.KW == 2)
             hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A, 2>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am,
-                               g, (const T *)y, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
+                               g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
         else
             hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A, 0>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am,
-                               g, (const T *)y, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
+                               g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
         hipLaunchKernelGGL(sum_partials_kernel, dim3(g.C), dim3(256), 0, st, ws, Gc, g.C, db);
         return hipGetLastError();
     }
     if (vec)
         hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, true, A>), dim3(G), dim3(256), smem, st, (const T *)dy, am,
-                           g, (const T *)y, (T *)dpre, beta, ppb, dW, dH, ws);
+                           g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, ppb, dW, dH, ws);
     else
         hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, false, A>), dim3(G), dim3(256), smem, st, (const T *)dy,
-                           am, g, (const T *)y, (T *)dpre, beta, ppb, dW, dH, ws);
+                           am, g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, ppb, dW, dH, ws);
     hipLaunchKernelGGL(sum_partials_kernel, dim3(g.C), dim3(256), 0, st, ws, G, g.C, db);
     return hipGetLastError();
 }
 
 hipError_t launch_maxpool_relu_bwd(int dt, const void *dy, const void *am, bool taps, const PoolGeom &g,
-                                   const void *y, void *dpre, float beta, float *db, float *ws, hipStream_t st) {
+                                   const void *y, const void *py, int64_t pys, void *dpre, float beta, float *db,
+                                   float *ws, hipStream_t st) {
     if (taps)
-        return dt == 0 ? maxpool_relu_bwd_t<float>(dy, (const uint8_t *)am, g, y, dpre, beta, db, ws, st)
-                       : maxpool_relu_bwd_t<bf16_t>(dy, (const uint8_t *)am, g, y, dpre, beta, db, ws, st);
-    return dt == 0 ? maxpool_relu_bwd_t<float>(dy, (const int32_t *)am, g, y, dpre, beta, db, ws, st)
-                   : maxpool_relu_bwd_t<bf16_t>(dy, (const int32_t *)am, g, y, dpre, beta, db, ws, st);
+        return dt == 0 ? maxpool_relu_bwd_t<float>(dy, (const uint8_t *)am, g, y, py, pys, dpre, beta, db, ws, st)
+                       : maxpool_relu_bwd_t<bf16_t>(dy, (const uint8_t *)am, g, y, py, pys, dpre, beta, db, ws, st);
+    return dt == 0 ? maxpool_relu_bwd_t<float>(dy, (const int32_t *)am, g, y, py, pys, dpre, beta, db, ws, st)
+                   : maxpool_relu_bwd_t<bf16_t>(dy, (const int32_t *)am, g, y, py, pys, dpre, beta, db, ws, st);
 }
 
 template <typename T, typename A>

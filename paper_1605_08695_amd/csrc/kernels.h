@@ -99,9 +99,11 @@ hipError_t launch_maxpool_fwd(int dt, const void *x, const PoolGeom &g, void *y,
 hipError_t launch_maxpool_bwd(int dt, const void *dy, const void *am, bool taps, const PoolGeom &g, float beta,
                               void *dx, hipStream_t st);
 // Fused max-pool backward + ReLU backward + bias gradient over the pool input y (pixel stride g.xs);
-// ws holds the bias-gradient partials of relu_bwd_plan.
+// ws holds the bias-gradient partials of relu_bwd_plan.  py (beta = 0 only; else NULL): the pool's
+// output (pixel stride pys), whose windows give the ReLU mask in place of y, which is then not read.
 hipError_t launch_maxpool_relu_bwd(int dt, const void *dy, const void *am, bool taps, const PoolGeom &g,
-                                   const void *y, void *dpre, float beta, float *db, float *ws, hipStream_t st);
+                                   const void *y, const void *py, int64_t pys, void *dpre, float beta, float *db,
+                                   float *ws, hipStream_t st);
 hipError_t launch_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh, hipStream_t st);
 hipError_t launch_sgd_multi(const SgdBatch &b, float lr, hipStream_t st);
 // Epilogue of a split-K forward or input-gradient GEMM: out[j][i] = f(sum over splits, in split

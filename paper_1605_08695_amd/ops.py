@@ -319,23 +319,34 @@ def maxpool_bwd(dy, argmax, dx, kernel_hw, stride, pads, beta=0.0, stream=None):
     return dx
 
 
-def maxpool_bwd_relu_bwd(dy, argmax, y, dpre, kernel_hw, stride, pads, beta=0.0, dbias=None, ws=None, stream=None):
+def maxpool_bwd_relu_bwd(dy, argmax, y, dpre, kernel_hw, stride, pads, beta=0.0, dbias=None, ws=None, stream=None,
+                         py=None):
     """dpre = (y > 0) * (beta * dpre + max-pool gradient of dy), dbias = column sums of dpre (fp32).
 
-    y is the pool input (the ReLU output); dpre has its shape and view.
+    y is the pool input (the ReLU output); dpre has its shape and view.  py (optional) is the
+    pool's output: with beta = 0 the mask is taken from it per window and y is not read (y may
+    then be None).
     """
     lib = load()
     kh, kw = kernel_hw
     fn = _argmax_fn(lib, "tfk_maxpool_bwd_relu_bwd", argmax)
+    d_p = nhwc(dpre)
+    if y is not None:
+        d_y = nhwc(y)
+        if (d_y.n, d_y.h, d_y.w, d_y.c, d_y.pixel_stride) != (d_p.n, d_p.h, d_p.w, d_p.c, d_p.pixel_stride):
+            raise ValueError("y and dpre must share one view (extents and pixel stride)")
+    pys = 0
+    if py is not None:
+        if tuple(py.shape) != tuple(dy.shape) or py.dtype != dy.dtype:
+            raise ValueError("py must have dy's shape and element type")
+        pys = nhwc(py).pixel_stride
     if dbias is None:
-        dbias = _empty(stream, y.shape[3], dtype=torch.float32, device=y.device)
-    d_y, d_p = nhwc(y), nhwc(dpre)
-    if (d_y.n, d_y.h, d_y.w, d_y.c, d_y.pixel_stride) != (d_p.n, d_p.h, d_p.w, d_p.c, d_p.pixel_stride):
-        raise ValueError("y and dpre must share one view (extents and pixel stride)")
-    need = lib.tfk_bias_relu_bwd_workspace_bytes(d_y, _dt(y))
+        dbias = _empty(stream, dpre.shape[3], dtype=torch.float32, device=dpre.device)
+    need = lib.tfk_bias_relu_bwd_workspace_bytes(d_p, _dt(dpre))
     if ws is None or ws.numel() < need:
-        ws = _ws(need, y.device, stream)
-    check(fn(_ptr(dy), _ptr(argmax), nhwc(dy), window(kh, kw, stride, pads), _dt(dy), _ptr(y), _ptr(dpre), d_y,
+        ws = _ws(need, dpre.device, stream)
+    check(fn(_ptr(dy), _ptr(argmax), nhwc(dy), window(kh, kw, stride, pads), _dt(dy),
+             _ptr(y), _ptr(py), pys, _ptr(dpre), d_p,
              float(beta), _ptr(dbias), _ptr(ws), need, _stream(stream)))
     return dpre, dbias
 

@@ -349,10 +349,12 @@ class Replica:
             elif op.name in self.pool_relu:
                 conv = self.pool_relu[op.name]
                 y, dpre, am = self.act[op.src], self.grad[op.src], self.argmax[op.name]
-                if trace: trace("maxpool_relu_bwd", op, stream=stream, dy=dy, argmax=am, y=y, dpre=dpre,
+                py = self._slice(self.act, op)
+                if trace: trace("maxpool_relu_bwd", op, stream=stream, dy=dy, argmax=am, y=y, py=py, dpre=dpre,
                                 beta=beta)
+                # (the pool's output gives the ReLU mask where the gradient is not accumulated)
                 ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
-                                         dbias=self.db[conv.name], ws=self.ws, stream=stream)
+                                         dbias=self.db[conv.name], ws=self.ws, stream=stream, py=py)
                 if trace: trace("maxpool_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[conv.name])
             else:
                 if src_grad:

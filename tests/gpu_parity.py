@@ -470,6 +470,10 @@ class ParityTracer:
         y_shape = tuple(t["y"].shape)
         u = {"dy": self._force(t["dy"]), "am": self._force_argmax(t["argmax"], op, y_shape), "y": self._force(t["y"]),
              "beta": t["beta"]}
+        # the pool's output, which may stand in for y as the mask: the state the forward check left,
+        # the oracle's pool of the state of y (the check below still takes the mask from y)
+        if t.get("py") is not None:
+            self._force(t["py"])
         u["dpre"] = self._force(t["dpre"]) if t["beta"] else None
         return u
 

@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 12
+    assert lib.tfk_abi_version() == 13
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -187,15 +187,22 @@ def test_maxpool_relu_bwd_validation(lib):
     W = Window(3, 3, 2, 2, 0, 0, 0, 0)
     yd, xd = Nhwc(2, 3, 3, 8, 0), Nhwc(2, 7, 7, 8, 0)
     def fused(dy=P, am=P + 0x100000, y=P + 0x200000, dpre=P + 0x300000, beta=0.0, db=P + 0x400000, ws=P + 0x500000,
-              ws_bytes=1 << 20, x=xd):
-        return lib.tfk_maxpool_bwd_relu_bwd(vp(dy), vp(am), yd, W, BF16, vp(y), vp(dpre), x, ctypes.c_float(beta),
-                                            vp(db), vp(ws), ws_bytes, None)
+              ws_bytes=1 << 20, x=xd, py=0, pys=0):
+        return lib.tfk_maxpool_bwd_relu_bwd(vp(dy), vp(am), yd, W, BF16, vp(y), vp(py), pys, vp(dpre), x,
+                                            ctypes.c_float(beta), vp(db), vp(ws), ws_bytes, None)
     assert fused(db=0) == NULL
     assert fused(beta=0.5) == ARG
     assert fused(dpre=P + 0x200010) == ALIAS                           # dpre overlaps y
     assert fused(x=Nhwc(2, 9, 9, 8, 0)) == SHAPE                        # 9 -> 4 with a 3x3/2 window, not 3
     assert fused(ws_bytes=0) == WORKSPACE
     assert fused(ws=P + 0x300000) == ALIAS                              # workspace inside dpre
+    # the pool's output as the mask: y may then be NULL (beta = 0), not when beta = 1 (py ignored)
+    assert fused(y=0) == NULL
+    assert fused(y=0, py=P + 0x600000, pys=8, beta=1.0) == NULL
+    assert fused(y=0, py=P + 0x600000, pys=4) == SHAPE                 # pixel stride below the channels
+    assert fused(y=0, py=P + 0x300010, pys=8) == ALIAS                 # py inside dpre
+    assert fused(y=0, py=P + 0x600001, pys=8) == ALIGN
+    assert fused(y=0, py=P + 0x600000, pys=8, ws=P + 0x600000) == ALIAS  # workspace over py
 
 
 def test_maxpool_taps_validation(lib):
@@ -212,7 +219,7 @@ def test_maxpool_taps_validation(lib):
                                     None) == NULL
     assert lib.tfk_maxpool_bwd_taps(vp(P), vp(P + 0x100000), yd, big, BF16, vp(P + 0x200000), xd,
                                     ctypes.c_float(0.0), None) == SHAPE
-    assert lib.tfk_maxpool_bwd_relu_bwd_taps(vp(P), vp(P + 0x100000), yd, W, BF16, vp(P + 0x200000),
+    assert lib.tfk_maxpool_bwd_relu_bwd_taps(vp(P), vp(P + 0x100000), yd, W, BF16, vp(P + 0x200000), vp(0), 0,
                                              vp(P + 0x200010), xd, ctypes.c_float(0.0), vp(P + 0x400000),
                                              vp(P + 0x500000), 1 << 20, None) == ALIAS   # dpre overlaps y
 

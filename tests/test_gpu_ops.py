@@ -372,7 +372,8 @@ def test_maxpool(case, dtype, ties):
 @pytest.mark.parametrize("case", POOL_CASES, ids=[c[0] for c in POOL_CASES])
 def test_maxpool_relu_bwd_fused(case, dtype, taps):
     """Fused max-pool backward + ReLU backward + bias gradient against the oracle's two ops,
-    with the selection stored as dense indices or as uint8 window taps."""
+    with the selection stored as dense indices or as uint8 window taps.  With the pool's output
+    as the mask (beta = 0: y is not read, NULL; beta = 1: ignored) the result is the same bits."""
     name, shape, k, s, pads = case
     rng = np.random.default_rng(29)
     # the pool input is a ReLU output: exact zeros (masked, and ties inside windows)
@@ -383,9 +384,13 @@ def test_maxpool_relu_bwd_fused(case, dtype, taps):
     ref_am = oracle.maxpool_fwd(f64(y), (k, k), s, pads)[1]
     for beta in (0.0, 1.0):
         dpre = _mk(shape, dtype, rng)
+        dpre_p = dpre.clone()
         old = f64(dpre)
         _, db = ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (k, k), s, pads, beta=beta)
+        _, db_p = ops.maxpool_bwd_relu_bwd(dy, am, None if beta == 0 else y, dpre_p, (k, k), s, pads, beta=beta,
+                                           py=out)
         torch.cuda.synchronize()
+        assert torch.equal(dpre_p, dpre) and torch.equal(db_p, db), "mask from the pool output"
         g = oracle.maxpool_bwd(f64(dy), ref_am, shape, dx=old, beta=beta)
         ref_dpre, ref_db = oracle.bias_relu_bwd(f64(y), g)
         assert_close(f64(dpre), ref_dpre, dtype, label="fused dpre beta=%g" % beta)
@@ -412,6 +417,16 @@ def test_maxpool_slice_views(dtype):
     ops.maxpool_bwd(dy, am, dx, (3, 3), 2, (0, 0, 0, 0))
     torch.cuda.synchronize()
     assert_close(f64(dx), oracle.maxpool_bwd(f64(dy), ref_am, x.shape), dtype, label="maxpool_bwd slice")
+    # the fused ReLU backward with the mask from the pool output held in the concat slice
+    xr = torch.relu(x)
+    _, am_r = ops.maxpool_fwd(xr, (3, 3), 2, (0, 0, 0, 0), y=y)
+    d1, d2 = torch.empty_like(x), torch.empty_like(x)
+    _, db1 = ops.maxpool_bwd_relu_bwd(dy, am_r, xr, d1, (3, 3), 2, (0, 0, 0, 0))
+    _, db2 = ops.maxpool_bwd_relu_bwd(dy, am_r, None, d2, (3, 3), 2, (0, 0, 0, 0), py=y)
+    torch.cuda.synchronize()
+    assert torch.equal(d1, d2) and torch.equal(db1, db2)
+    g = oracle.maxpool_bwd(f64(dy), oracle.maxpool_fwd(f64(xr), (3, 3), 2, (0, 0, 0, 0))[1], x.shape)
+    assert_close(f64(d2), oracle.bias_relu_bwd(f64(xr), g)[0], dtype, label="maxpool_relu_bwd slice py")
 
 
 # ----------------------------------------------------------------------------- sgd
