@@ -59,7 +59,17 @@ static inline Igemm2Tile igemm2_tiles(int ni, int mj, int zdim) {
         if (b128 < 448 && b96 <= 512 && mj > 128) return {128, 96, 4, 2};
         return {128, 128, 4, 2};
     }
-    if (ni % 192 == 0 && (ni / 192) * blocks_j >= 256) return {192, 128, 4, 2};
+    if (ni % 192 == 0 && (ni / 192) * blocks_j >= 256) {
+        // 96-row J tiles when they fill the last round of two blocks per CU better: the same
+        // operand reuse per byte (192 x 96 tiles read 64 flop per copied byte, 96 x 48 wave
+        // tiles 32 per LDS byte, as 128 x 128 tiles do) in more, smaller blocks (AlexNet conv2
+        // forward, 93312 pixels: 729 blocks of 128 rows fill 71 % of two rounds, 972 of 96
+        // rows 95 %; 73.4 -> 71.9 us back to back)
+        const int64_t b128 = (ni / 192) * blocks_j, b96 = (ni / 192) * (int64_t)((mj + 95) / 96) * zdim;
+        auto fill = [](int64_t b) { return (double)b / (double)(((b + 511) / 512) * 512); };
+        if (zdim == 1 && fill(b96) > fill(b128) + 0.05) return {192, 96, 4, 2};
+        return {192, 128, 4, 2};
+    }
     return {64, 128, 4, 2};
 }
 
@@ -100,6 +110,10 @@ static bool igemm2_launch(IgArgs &a, int mj, int zdim, const Igemm2Tile &t, hipS
             if (t.bi == 192) { igemm2_go<DIR, 192, 192, 4, 2>(a, grid, st); return true; }
             return false;
         }
+    }
+    if (t.bi == 192 && t.bj == 96 && t.nw == 4 && t.ns == 2) {
+        if constexpr (DIR == DIR_BWD_FILTER) return false;
+        else { igemm2_go<DIR, 192, 96, 4, 2>(a, grid, st); return true; }
     }
     if (t.bi == 192 && t.bj == 128 && t.nw == 4 && t.ns == 2) {
         // (the filter-gradient direction does not fit these tiles in its registers)

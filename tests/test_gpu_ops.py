@@ -52,10 +52,14 @@ CONV_CASES = [
     ("chunks_c192_uneven_pad", 3, 11, 9, 192, 128, 3, 3, 1, 1, (1, 1, 0, 2)),
     ("5x5_c128_k192", 2, 14, 14, 128, 192, 5, 5, 1, 1, (2, 2, 2, 2)),
     # enough output pixels (256 tiles of 128) for the 192-channel tiles of the forward pass
-    # and the filter gradient
+    # (192 x 96: 342 blocks fill the last round better than 256 of 128 rows) and the filter
+    # gradient
     ("k192_tiles", 32, 32, 32, 64, 192, 3, 3, 1, 1, (1, 1, 1, 1)),
     # ... and of the input gradient (192 input channels)
     ("c192_bwd_tiles", 32, 32, 32, 192, 64, 3, 3, 1, 1, (1, 1, 1, 1)),
+    # 192 x 128 tiles: three 192-channel tiles x 170 of 128 pixels fill two rounds of blocks
+    ("k576_tiles_192x128", 85, 16, 16, 16, 576, 3, 3, 1, 1, (1, 1, 1, 1)),
+    ("c576_bwd_tiles_192x128", 85, 16, 16, 576, 16, 3, 3, 1, 1, (1, 1, 1, 1)),
     # 288 tiles of 128 x 128 (most CUs with one block): 128 x 96 tiles, forward and input gradient
     ("bj96_tiles_fwd", 36, 32, 32, 64, 128, 3, 3, 1, 1, (1, 1, 1, 1)),
     ("bj96_tiles_bwd", 36, 32, 32, 128, 64, 3, 3, 1, 1, (1, 1, 1, 1)),
