@@ -1451,6 +1451,45 @@ __global__ __launch_bounds__(256) void sum_splits_grouped_kernel(const float *__
     }
 }
 
+// The two fixed levels of sum_split_groups_kernel + sum_groups_kernel in one pass (the same
+// sums in the same order): GP threads per output (GP a power of two >= the number of groups,
+// at most 64), thread g adding group g's splits in split order, then the group sums added in
+// group order through LDS.  A block covers 256 / GP consecutive outputs.
+template <int VEC, int GP>
+__global__ __launch_bounds__(256) void sum_split_groups_one_pass_kernel(const float *__restrict__ part, int splits,
+                                                                        int64_t mn, float *__restrict__ out) {
+    typedef typename FVec<VEC>::T V;
+    constexpr int COLS = 256 / GP;
+    __shared__ V red[GP][COLS];
+    const int64_t mv = mn / VEC;
+    const int groups = (splits + kSplitGroup - 1) / kSplitGroup;
+    const int c = threadIdx.x % COLS, g = threadIdx.x / COLS;
+    const int s0 = g * kSplitGroup, n = min(kSplitGroup, splits - s0);
+    for (int64_t base = (int64_t)blockIdx.x * COLS; base < mv; base += (int64_t)gridDim.x * COLS) {
+        const int64_t i = base + c;
+        V acc = V{};
+        if (i < mv && g < groups) {
+            const V *src = reinterpret_cast<const V *>(part) + (int64_t)s0 * mv + i;
+            V v[kSplitGroup];
+#pragma unroll
+            for (int q = 0; q < kSplitGroup; ++q)
+                if (q < n) v[q] = src[(int64_t)q * mv];
+            acc = v[0];
+#pragma unroll
+            for (int q = 1; q < kSplitGroup; ++q)
+                if (q < n) acc += v[q];
+        }
+        red[g][c] = acc;
+        __syncthreads();
+        if (g == 0 && i < mv) {
+            V t = red[0][c];
+            for (int q = 1; q < groups; ++q) t += red[q][c];
+            reinterpret_cast<V *>(out)[i] = t;
+        }
+        __syncthreads();
+    }
+}
+
 template <int VEC>
 static hipError_t sum_splits_t(float *part, int splits, int64_t mn, float *out, hipStream_t st) {
     const int groups = (splits + kSplitGroup - 1) / kSplitGroup;
@@ -1474,6 +1513,23 @@ static hipError_t sum_splits_t(float *part, int splits, int64_t mn, float *out, 
         hipLaunchKernelGGL((sum_splits_grouped_kernel<VEC, 16>), dim3(grid_for(mv, 16, 16384)), dim3(256), 0, st,
                            part, splits, mn, out);
         return hipGetLastError();
+    }
+    // one pass for at most 64 groups (1024 splits); the same sums in the same order as the two
+    // kernels below
+    if (groups <= 64) {
+        int gp = 1;
+        while (gp < groups) gp *= 2;
+        switch (gp) {
+#define TFK_ONE_PASS(G_)                                                                                          \
+    case G_:                                                                                                      \
+        hipLaunchKernelGGL((sum_split_groups_one_pass_kernel<VEC, G_>), dim3(grid_for(mv, 256 / G_, 16384)),      \
+                           dim3(256), 0, st, (const float *)part, splits, mn, out);                               \
+        return hipGetLastError();
+            TFK_ONE_PASS(1) TFK_ONE_PASS(2) TFK_ONE_PASS(4) TFK_ONE_PASS(8) TFK_ONE_PASS(16) TFK_ONE_PASS(32)
+            TFK_ONE_PASS(64)
+#undef TFK_ONE_PASS
+        default: break;
+        }
     }
     hipLaunchKernelGGL(sum_split_groups_kernel<VEC>, dim3(grid_for(mv * groups, 256, 16384)), dim3(256), 0, st, part,
                        splits, mn, groups);
