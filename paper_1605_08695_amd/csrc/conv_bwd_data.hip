@@ -4,7 +4,13 @@
 
 namespace tfk {
 
-static Igemm2Tile bwd_data_tiles(int ni, int mj, int zdim) { return igemm2_tiles_narrow(ni, mj, zdim); }
+// 33-64 input channels over many pixels at stride 1: 64 x 192 tiles, which copy 48 flop per byte
+// against 64 x 128's 43 and still give about a round of two blocks per CU (AlexNet conv2, 93312
+// pixels: 486 blocks; 74.8 -> 71.3 us back to back)
+static Igemm2Tile bwd_data_tiles(int ni, int mj, int zdim) {
+    if (ni > 32 && ni <= 64 && zdim == 1 && (mj + 191) / 192 >= 384) return {64, 192, 4, 2};
+    return igemm2_tiles_narrow(ni, mj, zdim);
+}
 
 // Rows of bias-gradient partials of the fused ReLU-backward epilogue: one per block and wave
 // column of the pipelined kernel's grid.

@@ -63,6 +63,8 @@ CONV_CASES = [
     # 288 tiles of 128 x 128 (most CUs with one block): 128 x 96 tiles, forward and input gradient
     ("bj96_tiles_fwd", 36, 32, 32, 64, 128, 3, 3, 1, 1, (1, 1, 1, 1)),
     ("bj96_tiles_bwd", 36, 32, 32, 128, 64, 3, 3, 1, 1, (1, 1, 1, 1)),
+    # 64 input channels over 75264 pixels: 64 x 192 input-gradient tiles (392 blocks)
+    ("c64_bwd_tiles_64x192", 96, 28, 28, 64, 32, 3, 3, 1, 1, (1, 1, 1, 1)),
     # fully connected layers as whole-window convolutions: AlexNet's fc6 (6x6x256 -> 4096) and
     # fc8 (4096 -> 1000 logits), at batch 4
     ("fc6_6x6_window", 4, 6, 6, 256, 4096, 6, 6, 1, 1, (0, 0, 0, 0)),
@@ -118,6 +120,7 @@ def test_conv_three_directions(case, dtype):
 
 RELU_BWI_CASES = ["ragged_tiles", "3x3s2_valid", "3x3s2_pad_odd", "1x1s2_empty_phase", "5x5_cout192",
                   "alexnet_conv3_shape", "chunks_c192_uneven_pad", "c192_bwd_tiles", "bj96_tiles_bwd",
+                  "c64_bwd_tiles_64x192",
                   "one_pixel_out_c64", "odd_channels", "5x5_c32_k96", "narrow_split_c24_k1024",
                   # a fully connected layer at small batch: split-K partials, then the ReLU
                   # backward and the bias-gradient rows in the epilogue pass
