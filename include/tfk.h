@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 13
+#define TFK_ABI_VERSION 14
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -192,7 +192,7 @@ TFK_API tfk_status tfk_conv2d_bwd_filter_noalloc(const void *x, tfk_nhwc xd, con
  *   dy, dyd, w, p, dt : as tfk_conv2d_bwd_input.
  *   y     : xd-shaped (the same view as dpre), the forward ReLU output; read only.
  *   dpre  : xd-shaped, overwritten; must not overlap dy, w, y or dbias.
- *   dbias : xd.c fp32 values, overwritten.
+ *   dbias : xd.c fp32 values, overwritten; or NULL: deferred (see tfk_bias_grad_finish).
  *   ws    : at least tfk_conv2d_workspace_bytes(3, xd, dyd.c, p, dt) bytes.
  * Requirements: xd.c <= 16384.  xd.n == 0 sets dbias to 0.
  */
@@ -225,7 +225,7 @@ TFK_API tfk_status tfk_bias_relu_fwd(void *y, tfk_nhwc yd, const float *bias, tf
  *   dbias[c]  = sum over all pixels p of dpre[p,c]  (fp32, fixed order)
  *   y, dy, dpre : share the view yd (same extents and pixel stride), type dt.
  *                 dpre may equal dy (in place); any other overlap is an error.
- *   dbias       : fp32 [yd.c], overwritten.
+ *   dbias       : fp32 [yd.c], overwritten; or NULL: deferred (see tfk_bias_grad_finish).
  *   ws          : at least tfk_bias_relu_bwd_workspace_bytes(yd, dt) bytes.
  * y may be NULL: a layer with a bias and no ReLU (a classifier's logits), so
  * dpre = dy and dbias holds the column sums of dy.
@@ -235,6 +235,33 @@ TFK_API tfk_status tfk_bias_relu_bwd(const void *y, const void *dy, tfk_nhwc yd,
                              void *stream);
 
 TFK_API size_t tfk_bias_relu_bwd_workspace_bytes(tfk_nhwc yd, tfk_dtype dt);
+
+/*
+ * Deferred bias gradients.  Every call that forms a bias gradient from per-block partial sums
+ * (tfk_bias_relu_bwd, tfk_conv2d_bwd_input_relu_bwd, tfk_maxpool_bwd_relu_bwd[_taps]) sums
+ * them per channel in a second short launch.  Given dbias = NULL it launches only the first:
+ * the partials stay in its workspace (channel c's `rows` values at part[c * rows ...]), and
+ * tfk_bias_grad_finish later sums the partials that several such calls left, all in one
+ * launch, each channel in the same fixed order as the call itself would have summed it (the
+ * same bits).  A step issues its bias gradients this way and finishes them together before
+ * its update (Section 4.1: every gradient of the step is formed before the update; Section 5:
+ * fewer, larger launches).  The caller keeps each deferred call's workspace untouched until
+ * the finish has run on the same stream (or after it on another).
+ *
+ * tfk_last_bias_partials: where the last call on this thread that was given dbias = NULL left
+ * its partials (*part inside that call's workspace, *rows per channel; 0 rows: an empty
+ * tensor, whose bias gradient is 0).  Errors: NULL (part or rows), ARG (no such call yet).
+ */
+TFK_API tfk_status tfk_last_bias_partials(const float **part, int32_t *rows);
+/*
+ * tfk_bias_grad_finish: for i < count, dbias[i][c] = the fixed-order sum of the rows[i]
+ * partials of channel c at parts[i] (c < channels[i]).  The arrays are the caller's (read
+ * during the call only).  count 0 is a no-op.  Errors: ARG (count < 0), NULL (an array,
+ * dbias[i], or parts[i] with rows[i] > 0), SHAPE (rows[i] < 0, channels[i] outside 1..16384),
+ * ALIGN (4 bytes), ALIAS (a dbias[i] overlapping partials or another dbias).
+ */
+TFK_API tfk_status tfk_bias_grad_finish(int32_t count, const float *const *parts, const int32_t *rows,
+                                const int32_t *channels, float *const *dbias, void *stream);
 
 /* ---------------------------------------------------------------- max-pool
  * MaxPool forward with argmax (Section 6.1: pooling, with convolution, is on the
@@ -317,10 +344,10 @@ TFK_API tfk_status tfk_maxpool_bwd_taps(const void *dy, const uint8_t *taps, tfk
  *           ignored when beta = 1 (the stored gradient then needs y's mask at every element).
  *   dpre  : xd-shaped, written (read first when beta = 1, which adds the gradient the other
  *           consumers of y already stored there); must not overlap y, py, dy or argmax.
- *   dbias : xd.c fp32 values, overwritten.
+ *   dbias : xd.c fp32 values, overwritten; or NULL: deferred (see tfk_bias_grad_finish).
  *   ws    : at least tfk_bias_relu_bwd_workspace_bytes(xd, dt) bytes.
  * Requirements: beta is 0 or 1; xd.c <= 16384.  xd.n == 0 sets dbias to 0.
- * Errors: NULL (dy, argmax, dpre, dbias, or y where it is read), SHAPE (pool geometry,
+ * Errors: NULL (dy, argmax, dpre, or y where it is read), SHAPE (pool geometry,
  * xd.c > 16384, py_stride < yd.c), ARG (beta), ALIGN (element alignment), ALIAS (the overlaps
  * above), WORKSPACE (ws too small).
  */

@@ -20,6 +20,7 @@ EXPORTS = ["tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_maxpool_bwd_relu_b
            "tfk_conv2d_fwd_bias_relu_maxpool",
            "tfk_conv2d_workspace_bytes",
            "tfk_bias_relu_fwd", "tfk_bias_relu_bwd", "tfk_bias_relu_bwd_workspace_bytes",
+           "tfk_last_bias_partials", "tfk_bias_grad_finish",
            "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps",
            "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd", "tfk_apply_sgd_multi",
            "tfk_apply_momentum", "tfk_apply_adam", "tfk_softmax_xent", "tfk_gather_rows_t",
@@ -93,6 +94,11 @@ def load(path: str = LIB_PATH):
                  "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps", "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd",
                  "tfk_apply_sgd_multi", "tfk_apply_momentum", "tfk_apply_adam", "tfk_softmax_xent", "tfk_gather_rows_t",
                  "tfk_sampled_softmax_xent", "tfk_scatter_apply_sgd"):
+        getattr(lib, name).restype = st
+    lib.tfk_last_bias_partials.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(i32)]
+    lib.tfk_bias_grad_finish.argtypes = [i32, ctypes.POINTER(vp), ctypes.POINTER(i32), ctypes.POINTER(i32),
+                                         ctypes.POINTER(vp), vp]
+    for name in ("tfk_last_bias_partials", "tfk_bias_grad_finish"):
         getattr(lib, name).restype = st
     lib.tfk_stream_wait.argtypes = [vp, vp]
     lib.tfk_program_create.argtypes = [ctypes.POINTER(vp)]

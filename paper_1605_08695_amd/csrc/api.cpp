@@ -190,6 +190,20 @@ thread_local tfk_program *g_rec = nullptr;
         }                                                                                        \
     } while (0)
 
+// Where the last call on this thread that was given dbias = NULL left its bias-gradient partials.
+struct LastPartials {
+    const float *part = nullptr;
+    int32_t rows = 0;
+    bool valid = false;
+};
+thread_local LastPartials g_partials;
+
+static void note_partials(const float *part, int rows) {
+    g_partials.part = part;
+    g_partials.rows = rows;
+    g_partials.valid = true;
+}
+
 // An event owned by a recorded stream join (released with its program).
 struct OwnedEvent {
     hipEvent_t e = nullptr;
@@ -352,10 +366,15 @@ tfk_status tfk_conv2d_bwd_input_relu_bwd(const void *dy, tfk_nhwc dyd, const voi
     ConvShape s;
     TRY(check_conv(xd, dyd.c, p, dt, dyd, "dpre", "dy", s));
     if (xd.c > 16384) return fail(TFK_ERR_SHAPE, "conv2d_bwd_input_relu_bwd supports at most 16384 channels");
-    TRY(need_ptr(dbias, "dbias"));
     TRY(need_align(dbias, 4, "dbias"));
     hipStream_t st = (hipStream_t)stream;
-    if (xd.n == 0) return hip_status(launch_fill_zero(dbias, xd.c, st), "conv2d_bwd_input_relu_bwd");
+    if (xd.n == 0) {
+        if (dbias == nullptr) {
+            note_partials((const float *)ws, 0);
+            return ok();
+        }
+        return hip_status(launch_fill_zero(dbias, xd.c, st), "conv2d_bwd_input_relu_bwd");
+    }
     const int64_t es = esize(dt);
     TRY(need_ptr(dy, "dy"));
     TRY(need_ptr(w, "w"));
@@ -378,9 +397,12 @@ tfk_status tfk_conv2d_bwd_input_relu_bwd(const void *dy, tfk_nhwc dyd, const voi
     if (overlap(ws, (int64_t)need, dy, yb) || overlap(ws, (int64_t)need, w, wb) || overlap(ws, (int64_t)need, y, xb) ||
         overlap(ws, (int64_t)need, dpre, xb) || overlap(ws, (int64_t)need, dbias, bb))
         return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
-    return hip_status(launch_conv_bwd_data_relu(dti, dy, dyd.pixel_stride ? dyd.pixel_stride : dyd.c, w, dpre, xs, y,
-                                                dbias, (float *)ws, s, st),
-                      "conv2d_bwd_input_relu_bwd");
+    BiasPartials bp{nullptr, 0};
+    TRY(hip_status(launch_conv_bwd_data_relu(dti, dy, dyd.pixel_stride ? dyd.pixel_stride : dyd.c, w, dpre, xs, y,
+                                             dbias, (float *)ws, s, st, dbias ? nullptr : &bp),
+                   "conv2d_bwd_input_relu_bwd"));
+    if (dbias == nullptr) note_partials(bp.part, bp.rows);
+    return ok();
 }
 
 tfk_status tfk_conv2d_bwd_filter(const void *x, tfk_nhwc xd, const void *dy, tfk_nhwc dyd, tfk_window p,
@@ -466,13 +488,18 @@ tfk_status tfk_bias_relu_bwd(const void *y, const void *dy, tfk_nhwc yd, void *d
     RECORDED(tfk_bias_relu_bwd, y, dy, yd, dpre, dbias, dt, ws, ws_bytes, stream);
     if (!valid_dt(dt)) return fail(TFK_ERR_DTYPE, "unknown dtype %d", (int)dt);
     TRY(check_view("y", yd));
-    TRY(need_ptr(dbias, "dbias"));
     TRY(need_align(dbias, 4, "dbias"));
     hipStream_t st = (hipStream_t)stream;
     const int64_t es = esize(dt);
     const int64_t vb = view_bytes(yd, es);
     const int64_t bb = (int64_t)yd.c * 4;
-    if (yd.n == 0) return hip_status(launch_fill_zero(dbias, yd.c, st), "bias_relu_bwd");
+    if (yd.n == 0) {
+        if (dbias == nullptr) {
+            note_partials((const float *)ws, 0);
+            return ok();
+        }
+        return hip_status(launch_fill_zero(dbias, yd.c, st), "bias_relu_bwd");
+    }
     TRY(need_ptr(dy, "dy"));
     TRY(need_ptr(dpre, "dpre"));
     TRY(need_align(y, es, "y"));
@@ -488,9 +515,12 @@ tfk_status tfk_bias_relu_bwd(const void *y, const void *dy, tfk_nhwc yd, void *d
         overlap(ws, (int64_t)need, dpre, vb) || overlap(ws, (int64_t)need, dbias, bb))
         return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
     const int64_t P = (int64_t)yd.n * yd.h * yd.w;
-    return hip_status(launch_bias_relu_bwd(dt == TFK_F32 ? 0 : 1, y, dy, dpre, P, yd.c, yd.pixel_stride, dbias,
-                                           (float *)ws, st),
-                      "bias_relu_bwd");
+    BiasPartials bp{nullptr, 0};
+    TRY(hip_status(launch_bias_relu_bwd(dt == TFK_F32 ? 0 : 1, y, dy, dpre, P, yd.c, yd.pixel_stride, dbias,
+                                        (float *)ws, st, dbias ? nullptr : &bp),
+                   "bias_relu_bwd"));
+    if (dbias == nullptr) note_partials(bp.part, bp.rows);
+    return ok();
 }
 
 // ------------------------------------------------------------------ max-pool
@@ -637,10 +667,15 @@ static tfk_status maxpool_relu_bwd_impl(const void *dy, const void *argmax, bool
     if (!(beta == 0.f || beta == 1.f)) return fail(TFK_ERR_ARG, "beta must be 0 or 1");
     if (xd.c > 16384) return fail(TFK_ERR_SHAPE, "maxpool_bwd_relu_bwd supports at most 16384 channels");
     if (taps && (int64_t)p.kh * p.kw > 256) return fail(TFK_ERR_SHAPE, "tap argmax needs kh * kw <= 256");
-    TRY(need_ptr(dbias, "dbias"));
     TRY(need_align(dbias, 4, "dbias"));
     hipStream_t st = (hipStream_t)stream;
-    if (xd.n == 0) return hip_status(launch_fill_zero(dbias, xd.c, st), "maxpool_bwd_relu_bwd");
+    if (xd.n == 0) {
+        if (dbias == nullptr) {
+            note_partials((const float *)ws, 0);
+            return ok();
+        }
+        return hip_status(launch_fill_zero(dbias, xd.c, st), "maxpool_bwd_relu_bwd");
+    }
     const int64_t es = esize(dt);
     TRY(need_ptr(dy, "dy"));
     TRY(need_ptr(argmax, "argmax"));
@@ -671,9 +706,12 @@ static tfk_status maxpool_relu_bwd_impl(const void *dy, const void *argmax, bool
         overlap(ws, (int64_t)need, dpre, xb) || overlap(ws, (int64_t)need, dbias, bb) ||
         overlap(ws, (int64_t)need, argmax, ab) || overlap(ws, (int64_t)need, py, pb))
         return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
-    return hip_status(launch_maxpool_relu_bwd(dt == TFK_F32 ? 0 : 1, dy, argmax, taps, g, y, py, py_stride, dpre,
-                                              beta, dbias, (float *)ws, st),
-                      "maxpool_bwd_relu_bwd");
+    BiasPartials bp{nullptr, 0};
+    TRY(hip_status(launch_maxpool_relu_bwd(dt == TFK_F32 ? 0 : 1, dy, argmax, taps, g, y, py, py_stride, dpre, beta,
+                                           dbias, (float *)ws, st, dbias ? nullptr : &bp),
+                   "maxpool_bwd_relu_bwd"));
+    if (dbias == nullptr) note_partials(bp.part, bp.rows);
+    return ok();
 }
 
 tfk_status tfk_maxpool_bwd_relu_bwd(const void *dy, const int32_t *argmax, tfk_nhwc yd, tfk_window p, tfk_dtype dt,
@@ -692,6 +730,67 @@ tfk_status tfk_maxpool_bwd_relu_bwd_taps(const void *dy, const uint8_t *taps, tf
              ws_bytes, stream);
     return maxpool_relu_bwd_impl(dy, taps, true, yd, p, dt, y, py, py_stride, dpre, xd, beta, dbias, ws, ws_bytes,
                                  stream);
+}
+
+// ------------------------------------------------------------------ deferred bias gradients
+tfk_status tfk_last_bias_partials(const float **part, int32_t *rows) {
+    TRY(need_ptr(part, "part"));
+    TRY(need_ptr(rows, "rows"));
+    if (!g_partials.valid) return fail(TFK_ERR_ARG, "no call on this thread has left bias-gradient partials");
+    *part = g_partials.part;
+    *rows = g_partials.rows;
+    return ok();
+}
+
+tfk_status tfk_bias_grad_finish(int32_t count, const float *const *parts, const int32_t *rows,
+                                const int32_t *channels, float *const *dbias, void *stream) {
+    if (g_rec != nullptr && count > 0 && parts != nullptr && rows != nullptr && channels != nullptr &&
+        dbias != nullptr) {
+        // the arrays belong to the caller: the recorded call keeps copies of them
+        tfk_program *const rec_ = g_rec;
+        g_rec = nullptr;
+        const tfk_status s_ = tfk_bias_grad_finish(count, parts, rows, channels, dbias, stream);
+        g_rec = rec_;
+        if (s_ != TFK_OK) return s_;
+        try {
+            std::vector<const float *> p(parts, parts + count);
+            std::vector<int32_t> r(rows, rows + count), c(channels, channels + count);
+            std::vector<float *> d(dbias, dbias + count);
+            rec_->calls.emplace_back(
+                [=]() { return tfk_bias_grad_finish(count, p.data(), r.data(), c.data(), d.data(), stream); });
+        } catch (...) {
+            return fail(TFK_ERR_ARG, "tfk_bias_grad_finish: out of host memory while recording");
+        }
+        return s_;
+    }
+    if (count < 0) return fail(TFK_ERR_ARG, "count must be >= 0");
+    if (count == 0) return ok();
+    TRY(need_ptr(parts, "parts"));
+    TRY(need_ptr(rows, "rows"));
+    TRY(need_ptr(channels, "channels"));
+    TRY(need_ptr(dbias, "dbias"));
+    std::vector<int> r(count), c(count);
+    for (int i = 0; i < count; ++i) {
+        if (rows[i] < 0 || channels[i] < 1 || channels[i] > 16384)
+            return fail(TFK_ERR_SHAPE, "tensor %d: rows must be >= 0 and channels in 1..16384", i);
+        if (rows[i] > 0) {
+            TRY(need_ptr(parts[i], "parts[i]"));
+            TRY(need_align(parts[i], 4, "parts[i]"));
+        }
+        TRY(need_ptr(dbias[i], "dbias[i]"));
+        TRY(need_align(dbias[i], 4, "dbias[i]"));
+        const int64_t bb = (int64_t)channels[i] * 4;
+        for (int j = 0; j < count; ++j) {
+            if (overlap(dbias[i], bb, parts[j], (int64_t)rows[j] * channels[j] * 4))
+                return fail(TFK_ERR_ALIAS, "dbias[%d] overlaps the partials of tensor %d", i, j);
+            if (j != i && overlap(dbias[i], bb, dbias[j], (int64_t)channels[j] * 4))
+                return fail(TFK_ERR_ALIAS, "dbias[%d] overlaps dbias[%d]", i, j);
+        }
+        r[i] = rows[i];
+        c[i] = channels[i];
+    }
+    return hip_status(launch_sum_partials_multi(count, parts, r.data(), c.data(), dbias, (hipStream_t)stream),
+                      "bias_grad_finish");
 }
 
 // ------------------------------------------------------------------ SGD

@@ -119,18 +119,26 @@ size_t conv_bwd_data_relu_ws_bytes(int dt, const ConvShape &s, int64_t dxs) {
 }
 
 hipError_t launch_conv_bwd_data_relu(int dt, const void *dy, int64_t dys, const void *w, void *dpre, int64_t dxs,
-                                     const void *y, float *db, float *ws, const ConvShape &s, hipStream_t st) {
+                                     const void *y, float *db, float *ws, const ConvShape &s, hipStream_t st,
+                                     BiasPartials *defer) {
     int parts = 0;
     float *db_at = nullptr;
     if (dt == 1 && ((uintptr_t)y & 7) == 0) {
         const hipError_t e = conv_bwd_data_t<bf16_t>(dy, dys, w, dpre, dxs, 0.f, s, st, ws, y, &parts, &db_at);
         if (e != hipSuccess) return e;
-        if (parts > 0) return launch_sum_partials(db_at, parts, s.C, db, st);
+        if (parts > 0) {
+            if (defer != nullptr) {
+                defer->part = db_at;
+                defer->rows = parts;
+                return hipSuccess;
+            }
+            return launch_sum_partials(db_at, parts, s.C, db, st);
+        }
     }
     // otherwise the two ops in sequence: the input gradient, then the ReLU backward in place
     const hipError_t e = launch_conv_bwd_data(dt, dy, dys, w, dpre, dxs, 0.f, s, nullptr, st);
     if (e != hipSuccess) return e;
-    return launch_bias_relu_bwd(dt, y, dpre, dpre, (int64_t)s.N * s.H * s.W, s.C, dxs, db, ws, st);
+    return launch_bias_relu_bwd(dt, y, dpre, dpre, (int64_t)s.N * s.H * s.W, s.C, dxs, db, ws, st, defer);
 }
 
 hipError_t launch_conv_bwd_data(int dt, const void *dy, int64_t dys, const void *w, void *dx, int64_t dxs,

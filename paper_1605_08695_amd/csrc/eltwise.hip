@@ -194,11 +194,9 @@ __global__ __launch_bounds__(256) void relu_bwd_partial_kernel(const T *__restri
 // contiguous): thread t takes b = t, t + 256, ... in order (the loads of 16 consecutive b of one
 // thread are issued together before they are added, in the same order), then a fixed xor tree
 // combines the 64 lanes of each wave and thread 0 adds the four wave sums in wave order.
-__global__ __launch_bounds__(256) void sum_partials_kernel(const float *__restrict__ partial, int G, int C,
-                                                           float *__restrict__ out) {
-    __shared__ float wsum[4];
-    const int c = blockIdx.x;
-    const float *row = partial + (int64_t)c * G;
+// One channel's G partials, summed by a block of 256 threads in a fixed order (strided runs per
+// thread, a wave shuffle tree, the four wave sums in order); the result is valid in thread 0.
+__device__ __forceinline__ float sum_partial_row(const float *__restrict__ row, int G, float *wsum) {
     float acc = 0.f;
     constexpr int U = 16;
     for (int b0 = threadIdx.x; b0 < G; b0 += 256 * U) {
@@ -216,7 +214,27 @@ __global__ __launch_bounds__(256) void sum_partials_kernel(const float *__restri
     for (int m = 32; m > 0; m >>= 1) acc += __shfl_xor(acc, m, 64);
     if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = acc;
     __syncthreads();
-    if (threadIdx.x == 0) out[c] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+    return ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+}
+
+__global__ __launch_bounds__(256) void sum_partials_kernel(const float *__restrict__ partial, int G, int C,
+                                                           float *__restrict__ out) {
+    __shared__ float wsum[4];
+    const int c = blockIdx.x;
+    const float t = sum_partial_row(partial + (int64_t)c * G, G, wsum);
+    if (threadIdx.x == 0) out[c] = t;
+}
+
+// Several tensors' partials in one launch: block b is channel b - chan0[i] of job i
+// (chan0[i] <= b < chan0[i + 1]), summed as sum_partials_kernel sums it.
+__global__ __launch_bounds__(256) void sum_partials_multi_kernel(const PartialsBatch jobs) {
+    __shared__ float wsum[4];
+    const int b = blockIdx.x;
+    int i = 0;
+    while (i + 1 < jobs.count && b >= jobs.chan0[i + 1]) ++i;
+    const int c = b - jobs.chan0[i];
+    const float t = sum_partial_row(jobs.part[i] + (int64_t)c * jobs.rows[i], jobs.rows[i], wsum);
+    if (threadIdx.x == 0) jobs.out[i][c] = t;
 }
 
 // ------------------------------------------------------------------ pixel decomposition
@@ -1211,9 +1229,21 @@ void relu_bwd_only_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *p
     *ppb = (P + g - 1) / g;
 }
 
+// The per-channel sum of G partial rows at ws into db, or, with defer, their place left for a
+// later batched sum.
+static hipError_t finish_partials(const float *ws, int G, int C, float *db, hipStream_t st, BiasPartials *defer) {
+    if (defer != nullptr) {
+        defer->part = ws;
+        defer->rows = G;
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL(sum_partials_kernel, dim3(C), dim3(256), 0, st, ws, G, C, db);
+    return hipGetLastError();
+}
+
 template <typename T>
 static hipError_t relu_bwd_t(const void *y, const void *dy, void *dpre, int64_t P, int C, int64_t ys,
-                             float *db, float *ws, hipStream_t st) {
+                             float *db, float *ws, hipStream_t st, BiasPartials *defer) {
     constexpr int EPC = Elem<T>::kPerChunk;
     const bool vec = C % EPC == 0 && ys % EPC == 0 && aligned16(y) && aligned16(dy) && aligned16(dpre);
     int G;
@@ -1229,20 +1259,19 @@ static hipError_t relu_bwd_t(const void *y, const void *dy, void *dpre, int64_t 
     else
         hipLaunchKernelGGL((relu_bwd_partial_kernel<T, false>), dim3(G), dim3(256), smem, st,
                            (const T *)y, (const T *)dy, (T *)dpre, P, C, ys, ppb, ws);
-    hipLaunchKernelGGL(sum_partials_kernel, dim3(C), dim3(256), 0, st, ws, G, C, db);
-    return hipGetLastError();
+    return finish_partials(ws, G, C, db, st, defer);
 }
 
 hipError_t launch_bias_relu_bwd(int dt, const void *y, const void *dy, void *dpre, int64_t P, int C,
-                                int64_t ys, float *db, float *ws, hipStream_t st) {
-    return dt == 0 ? relu_bwd_t<float>(y, dy, dpre, P, C, ys, db, ws, st)
-                   : relu_bwd_t<bf16_t>(y, dy, dpre, P, C, ys, db, ws, st);
+                                int64_t ys, float *db, float *ws, hipStream_t st, BiasPartials *defer) {
+    return dt == 0 ? relu_bwd_t<float>(y, dy, dpre, P, C, ys, db, ws, st, defer)
+                   : relu_bwd_t<bf16_t>(y, dy, dpre, P, C, ys, db, ws, st, defer);
 }
 
 template <typename T, typename A>
 static hipError_t maxpool_relu_bwd_t(const void *dy, const A *am, const PoolGeom &g, const void *y,
                                      const void *py, int64_t pys, void *dpre, float beta, float *db, float *ws,
-                                     hipStream_t st) {
+                                     hipStream_t st, BiasPartials *defer) {
     constexpr int EPC = Elem<T>::kPerChunk;
     const bool vec = g.C % EPC == 0 && g.xs % EPC == 0 && g.ys % EPC == 0 && aligned16(dy) && aligned16(am) &&
                      (py ? pys % EPC == 0 && aligned16(py) : aligned16(y)) && aligned16(dpre);
@@ -1274,8 +1303,9 @@ static hipError_t maxpool_relu_bwd_t(const void *dy, const A *am, const PoolGeom
         else
             hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A, 0>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am,
                                g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
-        hipLaunchKernelGGL(sum_partials_kernel, dim3(g.C), dim3(256), 0, st, ws, Gc, g.C, db);
-        return hipGetLastError();
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        return finish_partials(ws, Gc, g.C, db, st, defer);
     }
     if (vec)
         hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, true, A>), dim3(G), dim3(256), smem, st, (const T *)dy, am,
@@ -1283,18 +1313,22 @@ static hipError_t maxpool_relu_bwd_t(const void *dy, const A *am, const PoolGeom
     else
         hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, false, A>), dim3(G), dim3(256), smem, st, (const T *)dy,
                            am, g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, ppb, dW, dH, ws);
-    hipLaunchKernelGGL(sum_partials_kernel, dim3(g.C), dim3(256), 0, st, ws, G, g.C, db);
-    return hipGetLastError();
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return finish_partials(ws, G, g.C, db, st, defer);
 }
 
 hipError_t launch_maxpool_relu_bwd(int dt, const void *dy, const void *am, bool taps, const PoolGeom &g,
                                    const void *y, const void *py, int64_t pys, void *dpre, float beta, float *db,
-                                   float *ws, hipStream_t st) {
+                                   float *ws, hipStream_t st, BiasPartials *defer) {
     if (taps)
-        return dt == 0 ? maxpool_relu_bwd_t<float>(dy, (const uint8_t *)am, g, y, py, pys, dpre, beta, db, ws, st)
-                       : maxpool_relu_bwd_t<bf16_t>(dy, (const uint8_t *)am, g, y, py, pys, dpre, beta, db, ws, st);
-    return dt == 0 ? maxpool_relu_bwd_t<float>(dy, (const int32_t *)am, g, y, py, pys, dpre, beta, db, ws, st)
-                   : maxpool_relu_bwd_t<bf16_t>(dy, (const int32_t *)am, g, y, py, pys, dpre, beta, db, ws, st);
+        return dt == 0 ? maxpool_relu_bwd_t<float>(dy, (const uint8_t *)am, g, y, py, pys, dpre, beta, db, ws, st,
+                                                   defer)
+                       : maxpool_relu_bwd_t<bf16_t>(dy, (const uint8_t *)am, g, y, py, pys, dpre, beta, db, ws, st,
+                                                    defer);
+    return dt == 0 ? maxpool_relu_bwd_t<float>(dy, (const int32_t *)am, g, y, py, pys, dpre, beta, db, ws, st, defer)
+                   : maxpool_relu_bwd_t<bf16_t>(dy, (const int32_t *)am, g, y, py, pys, dpre, beta, db, ws, st,
+                                                defer);
 }
 
 template <typename T, typename A>
@@ -1547,6 +1581,28 @@ hipError_t launch_sum_splits(float *part, int splits, int64_t mn, float *out, hi
 hipError_t launch_sum_partials(const float *partial, int G, int C, float *out, hipStream_t st) {
     hipLaunchKernelGGL(sum_partials_kernel, dim3(C), dim3(256), 0, st, partial, G, C, out);
     return hipGetLastError();
+}
+
+hipError_t launch_sum_partials_multi(int count, const float *const *part, const int *rows, const int *channels,
+                                     float *const *out, hipStream_t st) {
+    for (int i0 = 0; i0 < count; i0 += kPartialsBatch) {
+        PartialsBatch b{};
+        b.count = std::min(kPartialsBatch, count - i0);
+        int total = 0;
+        for (int i = 0; i < b.count; ++i) {
+            b.chan0[i] = total;
+            b.part[i] = part[i0 + i];
+            b.rows[i] = rows[i0 + i];
+            b.out[i] = out[i0 + i];
+            total += channels[i0 + i];
+        }
+        b.chan0[b.count] = total;
+        if (total == 0) continue;
+        hipLaunchKernelGGL(sum_partials_multi_kernel, dim3(total), dim3(256), 0, st, b);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_fill_zero(float *out, int64_t n, hipStream_t st) {

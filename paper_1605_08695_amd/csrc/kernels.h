@@ -54,13 +54,33 @@ hipError_t launch_conv_bwd_data(int dt, const void *dy, int64_t dys, const void 
 // Workspace of the split-K forward / input gradient (0: no split for this shape).
 size_t conv_fwd_split_ws_bytes(int dt, const ConvShape &s);
 size_t conv_bwd_data_ws_bytes(int dt, const ConvShape &s);
+// Where a bias-gradient producer given a BiasPartials* left its per-channel partial sums instead of
+// reducing them: channel c's rows values at part[c * rows .. c * rows + rows - 1] (inside its ws).
+struct BiasPartials {
+    const float *part;
+    int rows;
+};
 // Input gradient fused with the ReLU backward + bias gradient of the layer that produced x:
 // dpre = y > 0 ? bwd_input(dy, w) : +0 (dx's view), db = column sums of dpre; ws: partials.
+// defer: if not NULL, db is not written and the partials are left where *defer says.
 hipError_t launch_conv_bwd_data_relu(int dt, const void *dy, int64_t dys, const void *w, void *dpre, int64_t dxs,
-                                     const void *y, float *db, float *ws, const ConvShape &s, hipStream_t st);
+                                     const void *y, float *db, float *ws, const ConvShape &s, hipStream_t st,
+                                     BiasPartials *defer = nullptr);
 size_t conv_bwd_data_relu_ws_bytes(int dt, const ConvShape &s, int64_t dxs);
 // Per-channel sums of partial[c][G] (G values per channel, summed in order) into out[C].
 hipError_t launch_sum_partials(const float *partial, int G, int C, float *out, hipStream_t st);
+// The same sums for several tensors in one launch per kPartialsBatch of them (job i: channels[i]
+// channels of rows[i] partials at part[i], into out[i]), each channel summed in the same order.
+constexpr int kPartialsBatch = 32;
+struct PartialsBatch {
+    int count;
+    int chan0[kPartialsBatch + 1];                 // first block of each job; chan0[count] = total
+    const float *part[kPartialsBatch];
+    int rows[kPartialsBatch];
+    float *out[kPartialsBatch];
+};
+hipError_t launch_sum_partials_multi(int count, const float *const *part, const int *rows, const int *channels,
+                                     float *const *out, hipStream_t st);
 hipError_t launch_conv_bwd_filter(int dt, const void *x, int64_t xs, const void *dy, int64_t dys, float *dw,
                                   const ConvShape &s, void *ws, hipStream_t st);
 // Split-K plan of bwd-filter: number of splits and reduction elements per split.
@@ -93,7 +113,7 @@ hipError_t launch_bias_relu_fwd(int dt, void *y, int64_t P, int C, int64_t ys, c
 void relu_bwd_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *ppb);
 void relu_bwd_only_plan(int dt, int64_t P, int C, int64_t ys, int *G, int64_t *ppb);
 hipError_t launch_bias_relu_bwd(int dt, const void *y, const void *dy, void *dpre, int64_t P, int C,
-                                int64_t ys, float *db, float *ws, hipStream_t st);
+                                int64_t ys, float *db, float *ws, hipStream_t st, BiasPartials *defer = nullptr);
 // am: int32 dense-index argmax, or with taps the uint8 window tap kh * KW + kw.
 hipError_t launch_maxpool_fwd(int dt, const void *x, const PoolGeom &g, void *y, void *am, bool taps, hipStream_t st);
 hipError_t launch_maxpool_bwd(int dt, const void *dy, const void *am, bool taps, const PoolGeom &g, float beta,
@@ -103,7 +123,7 @@ hipError_t launch_maxpool_bwd(int dt, const void *dy, const void *am, bool taps,
 // output (pixel stride pys), whose windows give the ReLU mask in place of y, which is then not read.
 hipError_t launch_maxpool_relu_bwd(int dt, const void *dy, const void *am, bool taps, const PoolGeom &g,
                                    const void *y, const void *py, int64_t pys, void *dpre, float beta, float *db,
-                                   float *ws, hipStream_t st);
+                                   float *ws, hipStream_t st, BiasPartials *defer = nullptr);
 hipError_t launch_sgd(float *var, const float *grad, int64_t n, float lr, uint16_t *sh, hipStream_t st);
 hipError_t launch_sgd_multi(const SgdBatch &b, float lr, hipStream_t st);
 // Epilogue of a split-K forward or input-gradient GEMM: out[j][i] = f(sum over splits, in split

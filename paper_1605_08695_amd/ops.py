@@ -9,7 +9,7 @@ current stream) and raises TfkError on a non-OK status.  There is no CPU path.
 from __future__ import annotations
 
 import ctypes
-from typing import Optional, Sequence, Tuple
+from typing import NamedTuple, Optional, Sequence, Tuple
 
 import torch
 
@@ -19,7 +19,7 @@ __all__ = ["conv2d_fwd", "conv2d_fwd_bias_relu", "conv2d_bwd_input", "conv2d_bwd
            "bias_relu_bwd", "bias_relu_bwd_workspace_bytes", "maxpool_fwd", "maxpool_bwd", "maxpool_bwd_relu_bwd", "apply_sgd",
            "apply_sgd_multi", "apply_momentum", "apply_adam", "softmax_xent",
            "gather_rows_t", "sampled_softmax_xent", "scatter_apply_sgd", "stream_wait", "Program", "out_len", "nhwc",
-           "window", "TfkError", "abi_version"]
+           "window", "TfkError", "abi_version", "DeferredBias", "bias_grad_finish"]
 
 
 def _dt(t: torch.Tensor) -> int:
@@ -179,9 +179,10 @@ def conv2d_bwd_input(dy, w, dx, stride, pads, beta=0.0, ws=None, stream=None):
     return dx
 
 
-def conv2d_bwd_input_relu_bwd(dy, w, y, dpre, stride, pads, dbias=None, ws=None, stream=None):
+def conv2d_bwd_input_relu_bwd(dy, w, y, dpre, stride, pads, dbias=None, ws=None, stream=None, defer=False):
     """dpre = (y > 0) * conv2d_fwd^T(dy), dbias = column sums of dpre (fp32): the input gradient
-    fused with the ReLU backward of the layer that produced the input (y, dpre: its view)."""
+    fused with the ReLU backward of the layer that produced the input (y, dpre: its view).
+    defer=True: returns (dpre, DeferredBias) instead, the partials left in ws (see bias_grad_finish)."""
     lib = load()
     kh, kw, cin, cout = w.shape
     if not (w.dtype == dy.dtype == y.dtype == dpre.dtype):
@@ -189,15 +190,18 @@ def conv2d_bwd_input_relu_bwd(dy, w, y, dpre, stride, pads, dbias=None, ws=None,
     d_y, d_p = nhwc(y), nhwc(dpre)
     if (d_y.n, d_y.h, d_y.w, d_y.c, d_y.pixel_stride) != (d_p.n, d_p.h, d_p.w, d_p.c, d_p.pixel_stride):
         raise ValueError("y and dpre must share one view (extents and pixel stride)")
-    if dbias is None:
-        dbias = _empty(stream, cin, dtype=torch.float32, device=y.device)
     win = window(kh, kw, stride, pads)
     need = lib.tfk_conv2d_workspace_bytes(3, d_p, cout, win, _dt(y))
+    if defer:
+        _need_ws(ws, need)
+        dbias = None
+    elif dbias is None:
+        dbias = _empty(stream, cin, dtype=torch.float32, device=y.device)
     if need and (ws is None or ws.numel() < need):
         ws = _ws(need, y.device, stream)
     check(lib.tfk_conv2d_bwd_input_relu_bwd(_ptr(dy), nhwc(dy), _ptr(w), win, _dt(dy), _ptr(y), _ptr(dpre), d_p,
                                             _ptr(dbias), _ptr(ws) if need else None, need, _stream(stream)))
-    return dpre, dbias
+    return dpre, (_deferred(lib, cin) if defer else dbias)
 
 
 def conv2d_bwd_filter(x, dy, kernel_hw, stride, pads, dw=None, ws=None, stream=None):
@@ -243,16 +247,20 @@ def bias_relu_bwd_workspace_bytes(y) -> int:
     return load().tfk_bias_relu_bwd_workspace_bytes(nhwc(y), _dt(y))
 
 
-def bias_relu_bwd(y, dy, dpre=None, dbias=None, ws=None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+def bias_relu_bwd(y, dy, dpre=None, dbias=None, ws=None, stream=None, defer=False):
     """dpre = dy * (y > 0) (dpre may be dy), dbias = column sums of dpre (fp32).  With y None
-    (a bias-only layer) dpre = dy and dbias = column sums of dy."""
+    (a bias-only layer) dpre = dy and dbias = column sums of dy.  defer=True: returns
+    (dpre, DeferredBias) instead, the partials left in ws (see bias_grad_finish)."""
     lib = load()
     if dpre is None:
         dpre = _empty_like(stream, dy)
-    if dbias is None:
-        dbias = _empty(stream, dy.shape[3], dtype=torch.float32, device=dy.device)
     view = y if y is not None else dy
     need = lib.tfk_bias_relu_bwd_workspace_bytes(nhwc(view), _dt(view))
+    if defer:
+        _need_ws(ws, need)
+        dbias = None
+    elif dbias is None:
+        dbias = _empty(stream, dy.shape[3], dtype=torch.float32, device=dy.device)
     if ws is None or ws.numel() < need:
         ws = _ws(need, dy.device, stream)
     d_y, d_dy, d_dp = nhwc(view), nhwc(dy), nhwc(dpre)
@@ -260,7 +268,7 @@ def bias_relu_bwd(y, dy, dpre=None, dbias=None, ws=None, stream=None) -> Tuple[t
         raise ValueError("y, dy and dpre must share one view (extents and pixel stride)")
     check(lib.tfk_bias_relu_bwd(_ptr(y), _ptr(dy), d_y, _ptr(dpre), _ptr(dbias), _dt(dy), _ptr(ws), need,
                                 _stream(stream)))
-    return dpre, dbias
+    return dpre, (_deferred(lib, dy.shape[3]) if defer else dbias)
 
 
 def softmax_xent(logits, labels, scale, bias=None, loss=None, dlogits=None, stream=None):
@@ -320,12 +328,13 @@ def maxpool_bwd(dy, argmax, dx, kernel_hw, stride, pads, beta=0.0, stream=None):
 
 
 def maxpool_bwd_relu_bwd(dy, argmax, y, dpre, kernel_hw, stride, pads, beta=0.0, dbias=None, ws=None, stream=None,
-                         py=None):
+                         py=None, defer=False):
     """dpre = (y > 0) * (beta * dpre + max-pool gradient of dy), dbias = column sums of dpre (fp32).
 
     y is the pool input (the ReLU output); dpre has its shape and view.  py (optional) is the
     pool's output: with beta = 0 the mask is taken from it per window and y is not read (y may
-    then be None).
+    then be None).  defer=True: returns (dpre, DeferredBias) instead, the partials left in ws
+    (see bias_grad_finish).
     """
     lib = load()
     kh, kw = kernel_hw
@@ -340,15 +349,53 @@ def maxpool_bwd_relu_bwd(dy, argmax, y, dpre, kernel_hw, stride, pads, beta=0.0,
         if tuple(py.shape) != tuple(dy.shape) or py.dtype != dy.dtype:
             raise ValueError("py must have dy's shape and element type")
         pys = nhwc(py).pixel_stride
-    if dbias is None:
-        dbias = _empty(stream, dpre.shape[3], dtype=torch.float32, device=dpre.device)
     need = lib.tfk_bias_relu_bwd_workspace_bytes(d_p, _dt(dpre))
+    if defer:
+        _need_ws(ws, need)
+        dbias = None
+    elif dbias is None:
+        dbias = _empty(stream, dpre.shape[3], dtype=torch.float32, device=dpre.device)
     if ws is None or ws.numel() < need:
         ws = _ws(need, dpre.device, stream)
     check(fn(_ptr(dy), _ptr(argmax), nhwc(dy), window(kh, kw, stride, pads), _dt(dy),
              _ptr(y), _ptr(py), pys, _ptr(dpre), d_p,
              float(beta), _ptr(dbias), _ptr(ws), need, _stream(stream)))
-    return dpre, dbias
+    return dpre, (_deferred(lib, dpre.shape[3]) if defer else dbias)
+
+
+# ----------------------------------------------------------------------------- deferred bias gradients
+class DeferredBias(NamedTuple):
+    """Where a call made with defer=True left its bias-gradient partials: inside the workspace it
+    was given, which must stay untouched until bias_grad_finish has run."""
+    part: int          # device address
+    rows: int          # partials per channel
+    channels: int
+
+
+def _need_ws(ws, need):
+    if ws is None or ws.numel() < need:
+        raise ValueError("defer=True needs a caller workspace of at least %d bytes (the partials stay in it)" % need)
+
+
+def _deferred(lib, channels) -> DeferredBias:
+    part, rows = ctypes.c_void_p(), ctypes.c_int32()
+    check(lib.tfk_last_bias_partials(ctypes.byref(part), ctypes.byref(rows)))
+    return DeferredBias(part.value or 0, rows.value, int(channels))
+
+
+def bias_grad_finish(jobs, stream=None):
+    """For every (DeferredBias, dbias) in jobs: dbias = the fixed-order per-channel sums of the
+    partials its deferred call left (the same bits as the call given dbias), in one launch."""
+    lib = load()
+    n = len(jobs)
+    for d, db in jobs:
+        if db.dtype != torch.float32 or not db.is_contiguous() or db.numel() != d.channels:
+            raise ValueError("dbias must be contiguous float32 with one value per channel")
+    parts = (ctypes.c_void_p * max(n, 1))(*[d.part for d, _ in jobs])
+    rows = (ctypes.c_int32 * max(n, 1))(*[d.rows for d, _ in jobs])
+    chans = (ctypes.c_int32 * max(n, 1))(*[d.channels for d, _ in jobs])
+    dbs = (ctypes.c_void_p * max(n, 1))(*[db.data_ptr() for _, db in jobs])
+    check(lib.tfk_bias_grad_finish(n, parts, rows, chans, dbs, _stream(stream)))
 
 
 # ----------------------------------------------------------------------------- update

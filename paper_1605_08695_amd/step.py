@@ -223,8 +223,21 @@ class Replica:
                                                         c.pads))
         self.ws_side = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=dev)
         self.side = torch.cuda.Stream(device=dev)
+        # ---- bias gradients of an untraced step: each ReLU/bias backward leaves its per-block
+        # partials in a workspace of its own, and one launch sums them all before the update
+        self.defer_bias = True
+        self.bias_ws: Dict[object, torch.Tensor] = {}
 
     # ------------------------------------------------------------------ helpers
+    def _bias_ws(self, key, need: int) -> torch.Tensor:
+        """The workspace of one deferred bias gradient, made at its first use and kept (a recorded
+        program finds its partials where its calls left them)."""
+        t = self.bias_ws.get(key)
+        if t is None or t.numel() < need:
+            t = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=self.params.device)
+            self.bias_ws[key] = t
+        return t
+
     def _width(self, op) -> int:
         return op.cout if isinstance(op, Conv) else self.net.tensors[op.src][3]
 
@@ -292,6 +305,9 @@ class Replica:
         written = set()
         grouped = set()                          # ReLU groups whose backward has run
         cur = stream if stream is not None else torch.cuda.current_stream()
+        # (traced steps form each bias gradient at once, so that the tracer can check it)
+        defer = trace is None and self.defer_bias
+        jobs = []                                # deferred bias gradients: (partials, dbias)
         for op in reversed(net.ops):
             dy = self._slice(self.grad, op)
             src_grad = op.src != "x" or net.input_grad
@@ -300,7 +316,12 @@ class Replica:
                 if not op.relu:
                     dpre = dy                        # bias only: the gradient passes through
                     if trace: trace("bias_bwd", op, stream=stream, dy=dy)
-                    ops.bias_relu_bwd(None, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
+                    if defer:
+                        ws = self._bias_ws(("bias", op.name), ops.bias_relu_bwd_workspace_bytes(dy))
+                        jobs.append((ops.bias_relu_bwd(None, dy, dpre=dpre, ws=ws, stream=stream, defer=True)[1],
+                                     self.db[op.name]))
+                    else:
+                        ops.bias_relu_bwd(None, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
                     if trace: trace("bias_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
                 elif op.name in self.relu_fused:
                     dpre = dy                        # written by the fused pool / input-gradient backward
@@ -312,13 +333,23 @@ class Replica:
                         yg, dyg = self.act[op.dst][..., c0:c0 + width], self.grad[op.dst][..., c0:c0 + width]
                         dbg = self.grads[self._layout[run[0].name][2]:self._layout[run[0].name][2] + width]
                         if trace: trace("bias_relu_bwd", op, stream=stream, y=yg, dy=dyg)
-                        ops.bias_relu_bwd(yg, dyg, dpre=dyg, dbias=dbg, ws=self.ws, stream=stream)
+                        if defer:
+                            ws = self._bias_ws(("group", op.dst, c0), ops.bias_relu_bwd_workspace_bytes(yg))
+                            jobs.append((ops.bias_relu_bwd(yg, dyg, dpre=dyg, ws=ws, stream=stream, defer=True)[1],
+                                         dbg))
+                        else:
+                            ops.bias_relu_bwd(yg, dyg, dpre=dyg, dbias=dbg, ws=self.ws, stream=stream)
                         if trace: trace("bias_relu_bwd:end", op, stream=stream, dpre=dyg, db=dbg)
                 else:
                     y = self._slice(self.act, op)
                     dpre = self._slice({op.dst: self.dpre_out}, op) if op.dst == net.output else dy
                     if trace: trace("bias_relu_bwd", op, stream=stream, y=y, dy=dy)
-                    ops.bias_relu_bwd(y, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
+                    if defer:
+                        ws = self._bias_ws(("relu", op.name), ops.bias_relu_bwd_workspace_bytes(y))
+                        jobs.append((ops.bias_relu_bwd(y, dy, dpre=dpre, ws=ws, stream=stream, defer=True)[1],
+                                     self.db[op.name]))
+                    else:
+                        ops.bias_relu_bwd(y, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
                     if trace: trace("bias_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
                 x = self.act[op.src]
                 # a filter gradient with no input gradient beside it (the first layer) stays
@@ -336,8 +367,15 @@ class Replica:
                     dx, y = self.grad[op.src], self.act[op.src]
                     if trace: trace("conv_bwd_input_relu_bwd", op, stream=stream, dy=dpre, w=self.Wlp[op.name],
                                     y=y)
-                    ops.conv2d_bwd_input_relu_bwd(dpre, self.Wlp[op.name], y, dx, (op.sh, op.sw), op.pads,
-                                                  dbias=self.db[prod.name], ws=self.ws, stream=stream)
+                    if defer:
+                        ws = self._bias_ws(("bwi", op.name), ops.conv2d_workspace_bytes(
+                            3, y, op.cout, op.kh, op.kw, (op.sh, op.sw), op.pads))
+                        jobs.append((ops.conv2d_bwd_input_relu_bwd(dpre, self.Wlp[op.name], y, dx, (op.sh, op.sw),
+                                                                   op.pads, ws=ws, stream=stream, defer=True)[1],
+                                     self.db[prod.name]))
+                    else:
+                        ops.conv2d_bwd_input_relu_bwd(dpre, self.Wlp[op.name], y, dx, (op.sh, op.sw), op.pads,
+                                                      dbias=self.db[prod.name], ws=self.ws, stream=stream)
                     if trace: trace("conv_bwd_input_relu_bwd:end", op, stream=stream, dpre=dx, db=self.db[prod.name])
                 elif src_grad:
                     dx = self.grad[op.src]
@@ -353,8 +391,14 @@ class Replica:
                 if trace: trace("maxpool_relu_bwd", op, stream=stream, dy=dy, argmax=am, y=y, py=py, dpre=dpre,
                                 beta=beta)
                 # (the pool's output gives the ReLU mask where the gradient is not accumulated)
-                ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
-                                         dbias=self.db[conv.name], ws=self.ws, stream=stream, py=py)
+                if defer:
+                    ws = self._bias_ws(("pool", op.name), ops.bias_relu_bwd_workspace_bytes(dpre))
+                    jobs.append((ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads,
+                                                          beta=beta, ws=ws, stream=stream, py=py, defer=True)[1],
+                                 self.db[conv.name]))
+                else:
+                    ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
+                                             dbias=self.db[conv.name], ws=self.ws, stream=stream, py=py)
                 if trace: trace("maxpool_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[conv.name])
             else:
                 if src_grad:
@@ -366,6 +410,8 @@ class Replica:
                     if trace: trace("maxpool_bwd:end", op, stream=stream, dx=dx)
             if src_grad:
                 written.add(op.src)
+        if jobs:
+            ops.bias_grad_finish(jobs, stream=stream)
         if side is not None:
             ops.stream_wait(cur, side)
 

@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 13
+    assert lib.tfk_abi_version() == 14
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -147,8 +147,9 @@ def test_conv_bwd_input_relu_bwd_validation(lib):
               ws=P + 0x50000000, ws_bytes=need):
         return lib.tfk_conv2d_bwd_input_relu_bwd(vp(dy), dyd, vp(w), W, BF16, vp(y), vp(dpre), xd, vp(db), vp(ws),
                                                  ws_bytes, None)
-    assert fused(db=0) == NULL
+    assert fused(dy=0) == NULL
     assert fused(y=0) == NULL
+    assert fused(db=0, ws_bytes=need - 1) == WORKSPACE                  # deferred: the same checks
     assert fused(dpre=P + 0x20000010) == ALIAS                         # dpre overlaps y
     assert fused(db=P + 0x30000000) == ALIAS                           # dbias inside dpre
     assert fused(ws_bytes=need - 1) == WORKSPACE
@@ -190,7 +191,8 @@ def test_maxpool_relu_bwd_validation(lib):
               ws_bytes=1 << 20, x=xd, py=0, pys=0):
         return lib.tfk_maxpool_bwd_relu_bwd(vp(dy), vp(am), yd, W, BF16, vp(y), vp(py), pys, vp(dpre), x,
                                             ctypes.c_float(beta), vp(db), vp(ws), ws_bytes, None)
-    assert fused(db=0) == NULL
+    assert fused(dy=0) == NULL
+    assert fused(db=0, dpre=P + 0x200010) == ALIAS                     # deferred: the same checks
     assert fused(beta=0.5) == ARG
     assert fused(dpre=P + 0x200010) == ALIAS                           # dpre overlaps y
     assert fused(x=Nhwc(2, 9, 9, 8, 0)) == SHAPE                        # 9 -> 4 with a 3x3/2 window, not 3
@@ -421,3 +423,39 @@ def test_program_state_errors(lib):
     assert lib.tfk_program_end(b._h) == OK
     assert lib.tfk_stream_wait(None, None) == OK                 # same stream: no-op
     b.close()
+
+
+def test_deferred_bias_validation(lib):
+    """Deferred bias gradients: where a call given dbias = NULL left its partials (thread-local),
+    and the argument checks of the batched finish (nothing is launched in this test)."""
+    import threading
+    part, rows = ctypes.c_void_p(), ctypes.c_int32()
+    assert lib.tfk_last_bias_partials(None, ctypes.byref(rows)) == NULL
+    got = []
+    t = threading.Thread(target=lambda: got.append(lib.tfk_last_bias_partials(ctypes.byref(part),
+                                                                              ctypes.byref(rows))))
+    t.start()
+    t.join()
+    assert got == [ARG]                                 # no deferred call on that thread yet
+    # an empty tensor: deferred without a launch, 0 partial rows left at the workspace
+    yd = Nhwc(0, 4, 4, 8, 0)
+    assert lib.tfk_bias_relu_bwd(vp(P), vp(P + 0x1000), yd, vp(P + 0x1000), vp(0), BF16, vp(P + 0x2000), 0,
+                                 None) == OK
+    assert lib.tfk_last_bias_partials(ctypes.byref(part), ctypes.byref(rows)) == OK
+    assert rows.value == 0 and part.value == P + 0x2000
+    Arr = lambda T, *v: (T * len(v))(*v)
+    def finish(n=1, parts=(P,), rws=(4,), chans=(8,), dbs=(P + 0x10000,)):
+        return lib.tfk_bias_grad_finish(n, Arr(ctypes.c_void_p, *parts) if parts is not None else None,
+                                        Arr(ctypes.c_int32, *rws), Arr(ctypes.c_int32, *chans),
+                                        Arr(ctypes.c_void_p, *dbs), None)
+    assert finish(n=-1) == ARG
+    assert lib.tfk_bias_grad_finish(0, None, None, None, None, None) == OK
+    assert finish(parts=None) == NULL
+    assert finish(parts=(0,)) == NULL                   # rows > 0 need partials
+    assert finish(rws=(-1,)) == SHAPE
+    assert finish(chans=(0,)) == SHAPE
+    assert finish(chans=(16385,)) == SHAPE
+    assert finish(dbs=(0,)) == NULL
+    assert finish(dbs=(P + 0x10002,)) == ALIGN
+    assert finish(dbs=(P + 16,)) == ALIAS               # dbias inside the partials (4 x 8 floats)
+    assert finish(n=2, parts=(P, P + 0x1000), rws=(4, 4), chans=(8, 8), dbs=(P + 0x10000, P + 0x10010)) == ALIAS

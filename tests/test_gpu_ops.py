@@ -711,3 +711,69 @@ def test_conv_bias_relu_maxpool(case, ties):
     bad = (dense != am) & ~tie
     say("  taps: %d differ from the oracle, all at near-ties" % int(np.sum(dense != am)))
     assert not bad.any()
+
+
+# ----------------------------------------------------------------------------- deferred bias gradients
+def test_deferred_bias_gradients_bitwise():
+    """Every bias-gradient producer called with defer=True leaves its partials in its own
+    workspace; one bias_grad_finish over all of them (more than one launch batch of 32, an empty
+    tensor among them) must give the bits the immediate calls give, and the same dpre."""
+    rng = np.random.default_rng(41)
+    bf = torch.bfloat16
+    jobs, want, keep = [], [], []
+
+    def ws_for(need):
+        # (each workspace holds its call's partials until the finish: kept alive here)
+        keep.append(torch.zeros(max(16, need), dtype=torch.uint8, device=DEV))
+        return keep[-1]
+
+    for rep in range(9):
+        # ReLU backward, a channel slice of a wider tensor, and bias only
+        buf = torch.from_numpy(np.maximum(rng.standard_normal((4, 13, 13, 96)), 0)).to(bf).to(DEV)
+        y = buf[..., 16:80]
+        dy = _mk(buf.shape, bf, rng)[..., 16:80]
+        d1 = torch.empty_like(buf)[..., 16:80]
+        d2 = torch.empty_like(buf)[..., 16:80]
+        _, db1 = ops.bias_relu_bwd(y, dy, dpre=d1)
+        _, part = ops.bias_relu_bwd(y, dy, dpre=d2, ws=ws_for(ops.bias_relu_bwd_workspace_bytes(y)), defer=True)
+        assert torch.equal(d1, d2)
+        jobs.append((part, torch.empty(64, device=DEV))); want.append(db1)
+        g = _mk((3, 5, 7, 24), bf, rng)
+        _, db1 = ops.bias_relu_bwd(None, g, dpre=g.clone())
+        _, part = ops.bias_relu_bwd(None, g, dpre=g.clone(), ws=ws_for(ops.bias_relu_bwd_workspace_bytes(g)),
+                                    defer=True)
+        jobs.append((part, torch.empty(24, device=DEV))); want.append(db1)
+        # pool + ReLU backward (tap and index selections)
+        x = torch.from_numpy(np.maximum(rng.standard_normal((2, 27, 27, 64)), 0)).to(bf).to(DEV)
+        for taps in (True, False):
+            out, am = ops.maxpool_fwd(x, (3, 3), 2, (0, 0, 0, 0), taps=taps)
+            dyp = _mk(out.shape, bf, rng)
+            p1, p2 = torch.empty_like(x), torch.empty_like(x)
+            _, db1 = ops.maxpool_bwd_relu_bwd(dyp, am, x, p1, (3, 3), 2, (0, 0, 0, 0))
+            _, part = ops.maxpool_bwd_relu_bwd(dyp, am, x, p2, (3, 3), 2, (0, 0, 0, 0),
+                                               ws=ws_for(ops.bias_relu_bwd_workspace_bytes(p2)), defer=True)
+            assert torch.equal(p1, p2)
+            jobs.append((part, torch.empty(64, device=DEV))); want.append(db1)
+        # input gradient fused with the ReLU backward: the pipelined kernel and the split path
+        for (n, h, cin, cout, k) in ((4, 13, 192, 384, 3), (2, 4, 24, 1024, 1)):
+            yv = torch.from_numpy(np.maximum(rng.standard_normal((n, h, h, cin)), 0)).to(bf).to(DEV)
+            w = (torch.from_numpy(rng.standard_normal((k, k, cin, cout)) * 0.05)).to(bf).to(DEV)
+            dyc = _mk((n, h, h, cout), bf, rng)
+            p1, p2 = torch.empty_like(yv), torch.empty_like(yv)
+            pd = k // 2
+            _, db1 = ops.conv2d_bwd_input_relu_bwd(dyc, w, yv, p1, (1, 1), (pd, pd, pd, pd))
+            need = ops.conv2d_workspace_bytes(3, yv, cout, k, k, (1, 1), (pd, pd, pd, pd))
+            _, part = ops.conv2d_bwd_input_relu_bwd(dyc, w, yv, p2, (1, 1), (pd, pd, pd, pd), ws=ws_for(need),
+                                                    defer=True)
+            assert torch.equal(p1, p2)
+            jobs.append((part, torch.empty(cin, device=DEV))); want.append(db1)
+    # an empty tensor: no partials, bias gradient 0
+    e = torch.zeros((0, 4, 4, 8), dtype=bf, device=DEV)
+    _, part = ops.bias_relu_bwd(e, e, dpre=e, ws=ws_for(16), defer=True)
+    assert part.rows == 0
+    jobs.append((part, torch.full((8,), 7.0, device=DEV))); want.append(torch.zeros(8, device=DEV))
+    assert len(jobs) > 32
+    ops.bias_grad_finish(jobs)
+    torch.cuda.synchronize()
+    for i, ((_, got), ref) in enumerate(zip(jobs, want)):
+        assert torch.equal(got.view(torch.int32), ref.view(torch.int32)), i

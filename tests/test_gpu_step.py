@@ -354,3 +354,25 @@ def test_program_replays_match_eager(make, opt):
             assert bitwise_equal(a, b), r
         _ = torch.ones(1024, device="cuda").sum().item()      # unrelated eager work between replays
     prog.close()
+
+
+@pytest.mark.parametrize("make", [lambda: W.alexnet(batch=8), lambda: W.googlenet(batch=4),
+                                  lambda: W.alexnet(batch=4, classifier=True)],
+                         ids=["alexnet_b8", "googlenet_b4", "alexnet_cls_b4"])
+def test_deferred_bias_gradients_match_immediate(make):
+    """The untraced step leaves every main-stream bias gradient's partials in a workspace of its
+    own and sums them all in one launch before the update; it must equal, bit for bit, the step
+    that sums each one as it is formed (the same per-channel order), over two steps."""
+    net = make()
+    net.lr = 1e-6
+    inp = W.make_inputs(net, seed=8)
+    a, b = Replica(net, inp), Replica(net, inp)
+    b.defer_bias = False
+    for r in range(2):
+        a.step()
+        b.step()
+        torch.cuda.synchronize()
+        assert len(a.bias_ws) > 0 and len(b.bias_ws) == 0
+        assert bitwise_equal(a.grads, b.grads), r
+        assert bitwise_equal(a.params, b.params), r
+    say("deferred bias gradients", net.name, "workspaces:", len(a.bias_ws))
