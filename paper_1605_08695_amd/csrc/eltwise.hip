@@ -279,6 +279,18 @@ __device__ __forceinline__ void decode(const Decode &d, int64_t t, int &cv, int6
     }
 }
 
+// Index arithmetic of the pool kernels: 64-bit, or (O32: pixel counts, strides and channel
+// counts below 2^24 and element offsets below 2^29, checked by the host with pool_o32) 32-bit with
+// full-rate 24-bit multiplies in place of quarter-rate 64-bit ones.
+template <bool O32>
+struct PoolIx {
+    typedef typename std::conditional<O32, uint32_t, int64_t>::type I;
+    static __device__ __forceinline__ I mul(I a, I b) {
+        if constexpr (O32) return __umul24(a, b);
+        else return a * b;
+    }
+};
+
 // ------------------------------------------------------------------ argmax formats
 // A max-pool records, per output element, which input element its window selected: as the
 // dense NHWC index of that element (int32_t) or as the window tap kh * KW + kw (uint8_t, a
@@ -390,11 +402,13 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T *__restrict__ 
 // Fixed small windows (3x3, 2x2) on the 16-byte path: the window loop is unrolled and all of a
 // thread's loads are issued before the first comparison, so their latencies overlap (the
 // run-time loop above waits for each tap in turn).  Same scan order and tie rule.
-template <typename T, int KH, int KW, typename A>
+template <typename T, int KH, int KW, typename A, bool O32>
 __global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restrict__ x, PoolGeom g,
                                                               T *__restrict__ y, A *__restrict__ argmax,
                                                               Decode dec) {
     constexpr int EPC = Elem<T>::kPerChunk;
+    typedef PoolIx<O32> M;
+    typedef typename M::I I;
     const int CV = g.C / EPC;
     const int64_t total = (int64_t)g.N * g.OH * g.OW * CV;
     for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
@@ -404,7 +418,7 @@ __global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restric
         decode(dec, t, cv, pix, ow, oh, n);
         U4 v[KH * KW];
         bool ok[KH * KW];
-        int64_t pidx[KH * KW];
+        I pidx[KH * KW];
 #pragma unroll
         for (int kh = 0; kh < KH; ++kh) {
 #pragma unroll
@@ -412,8 +426,8 @@ __global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restric
                 const int q = kh * KW + kw;
                 const int ih = oh * g.sh + kh - g.pt, iw = ow * g.sw + kw - g.pl;
                 ok[q] = (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
-                pidx[q] = ((int64_t)n * g.H + (ok[q] ? ih : 0)) * g.W + (ok[q] ? iw : 0);
-                v[q] = *reinterpret_cast<const U4 *>(x + pidx[q] * g.xs + cv * EPC);
+                pidx[q] = M::mul(M::mul((I)n, (I)g.H) + (I)(ok[q] ? ih : 0), (I)g.W) + (I)(ok[q] ? iw : 0);
+                v[q] = *reinterpret_cast<const U4 *>(x + (M::mul(pidx[q], (I)g.xs) + (I)(cv * EPC)));
             }
         }
         float best[EPC];
@@ -424,7 +438,7 @@ __global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restric
             if (!ok[q]) continue;
             float f[EPC];
             chunk_to_f32<T>(v[q], f);
-            const int32_t dense = (int32_t)(pidx[q] * g.C + cv * EPC);
+            const int32_t dense = (int32_t)(M::mul(pidx[q], (I)g.C) + (I)(cv * EPC));
 #pragma unroll
             for (int e = 0; e < EPC; ++e) {
                 if (!have || f[e] > best[e]) {
@@ -434,9 +448,9 @@ __global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restric
             }
             have = true;
         }
-        const int64_t opix = ((int64_t)n * g.OH + oh) * g.OW + ow;
-        *reinterpret_cast<U4 *>(y + opix * g.ys + cv * EPC) = f32_to_chunk<T>(best);
-        arg_store<A, EPC>(argmax + opix * g.C + cv * EPC, bi);
+        const I opix = M::mul(M::mul((I)n, (I)g.OH) + (I)oh, (I)g.OW) + (I)ow;
+        *reinterpret_cast<U4 *>(y + (M::mul(opix, (I)g.ys) + (I)(cv * EPC))) = f32_to_chunk<T>(best);
+        arg_store<A, EPC>(argmax + (M::mul(opix, (I)g.C) + (I)(cv * EPC)), bi);
     }
 }
 
@@ -450,13 +464,16 @@ __global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restric
 // py (optional, pixel stride pys): the pool's output; a window whose output element is not
 // positive routes +0 instead of its dy (the ReLU mask of the element its argmax names, whose
 // value the window's output is).
-template <typename T, bool VEC, typename A>
+template <typename T, bool VEC, typename A, bool O32 = false>
 __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const A *__restrict__ argmax,
                                             const PoolGeom &g, int n, int h, int w, int64_t pix, int cv,
                                             float *s, const T *__restrict__ py = nullptr, int64_t pys = 0) {
     constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
     constexpr bool TAP = sizeof(A) == 1;
-    const int32_t self = (int32_t)(pix * g.C + cv * EPC);
+    typedef PoolIx<O32> M;
+    typedef typename M::I I;
+    const int32_t self = (int32_t)(M::mul((I)pix, (I)g.C) + (I)(cv * EPC));
+    const I nrow = M::mul((I)n, (I)g.OH);
     auto want = [&](int oh, int ow, int e) __attribute__((always_inline)) -> int32_t {
         if constexpr (TAP) return (h + g.pt - oh * g.sh) * g.KW + (w + g.pl - ow * g.sw);
         else return self + e;
@@ -482,10 +499,10 @@ __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const A *_
             for (int q = 0; q < NC * NC; ++q) {
                 const int oh = oh_lo + q / NC, ow = ow_lo + q % NC;
                 valid[q] = oh <= oh_hi && ow <= ow_hi;
-                const int64_t opix = ((int64_t)n * g.OH + (valid[q] ? oh : ohc)) * g.OW + (valid[q] ? ow : owc);
-                arg_load<A, EPC>(argmax + opix * g.C + cv * EPC, ai[q]);
-                dv[q] = *reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC);
-                if (py) pv[q] = *reinterpret_cast<const U4 *>(py + opix * pys + cv * EPC);
+                const I opix = M::mul(nrow + (I)(valid[q] ? oh : ohc), (I)g.OW) + (I)(valid[q] ? ow : owc);
+                arg_load<A, EPC>(argmax + (M::mul(opix, (I)g.C) + (I)(cv * EPC)), ai[q]);
+                dv[q] = *reinterpret_cast<const U4 *>(dy + (M::mul(opix, (I)g.ys) + (I)(cv * EPC)));
+                if (py) pv[q] = *reinterpret_cast<const U4 *>(py + (M::mul(opix, (I)pys) + (I)(cv * EPC)));
             }
 #pragma unroll
             for (int e = 0; e < EPC; ++e) s[e] = 0.f;
@@ -542,11 +559,13 @@ __device__ __forceinline__ void pool_gather(const T *__restrict__ dy, const A *_
     }
 }
 
-template <typename T, bool VEC, typename A>
+template <typename T, bool VEC, typename A, bool O32>
 __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T *__restrict__ dy,
                                                           const A *__restrict__ argmax, PoolGeom g,
                                                           float beta, T *dx, Decode dec) {
     constexpr int EPC = VEC ? Elem<T>::kPerChunk : 1;
+    typedef PoolIx<O32> M;
+    typedef typename M::I I;
     const int CV = g.C / EPC;
     const int64_t total = (int64_t)g.N * g.H * g.W * CV;
     for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
@@ -555,8 +574,8 @@ __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T *__restrict__ 
         int64_t pix;
         decode(dec, t, cv, pix, w, h, n);
         float s[EPC];
-        pool_gather<T, VEC, A>(dy, argmax, g, n, h, w, pix, cv, s);
-        T *out = dx + pix * g.xs + cv * EPC;
+        pool_gather<T, VEC, A, O32>(dy, argmax, g, n, h, w, pix, cv, s);
+        T *out = dx + (M::mul((I)pix, (I)g.xs) + (I)(cv * EPC));
         if constexpr (VEC) {
             if (beta != 0.f) {
                 float o[EPC];
@@ -582,7 +601,7 @@ __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T *__restrict__ 
 // With py (the pool's output, pixel stride pys; beta = 0 only) the mask is taken per window
 // from it instead of per element from y, which is not read: an element receives gradient only
 // from windows whose argmax it is, and each such window's output is the element's value.
-template <typename T, bool VEC, typename A>
+template <typename T, bool VEC, typename A, bool O32>
 __global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *__restrict__ dy,
                                                                        const A *__restrict__ argmax,
                                                                        PoolGeom g, const T *__restrict__ y,
@@ -612,8 +631,9 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *
                 dW.divmod((uint32_t)p, q, w);
                 dH.divmod(q, n, h);
                 float s[EPC];
-                pool_gather<T, VEC, A>(dy, argmax, g, (int)n, (int)h, (int)w, p, cv, s, py, pys);
-                const int64_t off = p * g.xs + (int64_t)cv * EPC;
+                pool_gather<T, VEC, A, O32>(dy, argmax, g, (int)n, (int)h, (int)w, p, cv, s, py, pys);
+                typedef PoolIx<O32> M;
+                const typename M::I off = M::mul((typename M::I)p, (typename M::I)g.xs) + (typename M::I)(cv * EPC);
                 if constexpr (VEC) {
                     if (beta != 0.f) {
                         float o[EPC];
@@ -658,7 +678,9 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_partial_kernel(const T *
 // match are dropped: 9 of 16 remain for 3 x 3); PK = 0: the size comes from g.
 // py: as in maxpool_relu_bwd_partial_kernel (the four windows' outputs replace the four pixels'
 // y as the mask).
-template <typename T, typename A, int PK>
+// O32: pixel indices below 2^24 and element offsets below 2^29 (checked by the host), so the index
+// arithmetic runs in 32 bits with full-rate 24-bit multiplies instead of quarter-rate 64-bit ones.
+template <typename T, typename A, int PK, bool O32>
 __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__restrict__ dy,
                                                                     const A *__restrict__ argmax, PoolGeom g,
                                                                     const T *__restrict__ y,
@@ -679,6 +701,11 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
     const int64_t c0 = (int64_t)blockIdx.x * cpb;
     const int64_t c1 = min(ncell, c0 + cpb);
     const bool active = row < R;
+    using Ix = typename std::conditional<O32, uint32_t, int64_t>::type;
+    auto mul = [](Ix a, Ix b) __attribute__((always_inline)) -> Ix {
+        if constexpr (O32) return __umul24(a, b);
+        else return a * b;
+    };
     for (int cv = lane_cv; cv < CV; cv += CVB) {
         float acc[EPC];
 #pragma unroll
@@ -696,22 +723,23 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
                 for (int k = 0; k < 4; ++k) {
                     const int oh = (int)ch - 1 + (k >> 1), ow = (int)cw - 1 + (k & 1);
                     wok[k] = (unsigned)oh < (unsigned)g.OH && (unsigned)ow < (unsigned)g.OW;
-                    const int64_t opix = ((int64_t)n * g.OH + (wok[k] ? oh : 0)) * g.OW + (wok[k] ? ow : 0);
-                    arg_load<A, EPC>(argmax + opix * g.C + cv * EPC, ai[k]);
-                    dv[k] = *reinterpret_cast<const U4 *>(dy + opix * g.ys + cv * EPC);
-                    if (py) pv[k] = *reinterpret_cast<const U4 *>(py + opix * pys + cv * EPC);
+                    const Ix opix = mul(mul((Ix)n, (Ix)g.OH) + (Ix)(wok[k] ? oh : 0), (Ix)g.OW) + (Ix)(wok[k] ? ow : 0);
+                    arg_load<A, EPC>(argmax + (mul(opix, (Ix)g.C) + (Ix)(cv * EPC)), ai[k]);
+                    dv[k] = *reinterpret_cast<const U4 *>(dy + (mul(opix, (Ix)g.ys) + (Ix)(cv * EPC)));
+                    if (py) pv[k] = *reinterpret_cast<const U4 *>(py + (mul(opix, (Ix)pys) + (Ix)(cv * EPC)));
                 }
                 // the four pixels of the cell
-                int64_t pix[4];
+                Ix pix[4], poff[4];
                 bool pok[4];
                 U4 yv[4], ov[4];
 #pragma unroll
                 for (int m = 0; m < 4; ++m) {
                     const int h = 2 * (int)ch - g.pt + (m >> 1), w = 2 * (int)cw - g.pl + (m & 1);
                     pok[m] = (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
-                    pix[m] = ((int64_t)n * g.H + (pok[m] ? h : 0)) * g.W + (pok[m] ? w : 0);
-                    if (!py) yv[m] = *reinterpret_cast<const U4 *>(y + pix[m] * g.xs + cv * EPC);
-                    if (beta != 0.f) ov[m] = *reinterpret_cast<const U4 *>(dpre + pix[m] * g.xs + cv * EPC);
+                    pix[m] = mul(mul((Ix)n, (Ix)g.H) + (Ix)(pok[m] ? h : 0), (Ix)g.W) + (Ix)(pok[m] ? w : 0);
+                    poff[m] = mul(pix[m], (Ix)g.xs) + (Ix)(cv * EPC);
+                    if (!py) yv[m] = *reinterpret_cast<const U4 *>(y + poff[m]);
+                    if (beta != 0.f) ov[m] = *reinterpret_cast<const U4 *>(dpre + poff[m]);
                 }
                 float s[4][EPC];
 #pragma unroll
@@ -730,7 +758,7 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
                         const int KH = PK > 0 ? PK : g.KH, KW = PK > 0 ? PK : g.KW;
                         if (PK > 0 && sizeof(A) == 1 && (th >= KH || tw >= KW)) continue;
                         const int32_t self = sizeof(A) == 1 ? (th < KH && tw < KW ? th * KW + tw : -1)
-                                                            : (int32_t)(pix[m] * g.C + cv * EPC);
+                                                            : (int32_t)(mul(pix[m], (Ix)g.C) + (Ix)(cv * EPC));
 #pragma unroll
                         for (int e = 0; e < EPC; ++e)
                             if (wok[k] && ai[k][e] == self + (sizeof(A) == 1 ? 0 : e)) s[m][e] += v[e];
@@ -747,7 +775,7 @@ __global__ __launch_bounds__(256) void maxpool_relu_bwd_cell_kernel(const T *__r
                     }
                     if (!py) relu_mask<T>(yv[m], s[m]);
                     const U4 packed = f32_to_chunk<T>(s[m]);
-                    *reinterpret_cast<U4 *>(dpre + pix[m] * g.xs + cv * EPC) = packed;
+                    *reinterpret_cast<U4 *>(dpre + poff[m]) = packed;
                     float st[EPC];
                     chunk_to_f32<T>(packed, st);
 #pragma unroll
@@ -1268,6 +1296,15 @@ hipError_t launch_bias_relu_bwd(int dt, const void *y, const void *dy, void *dpr
                    : relu_bwd_t<bf16_t>(y, dy, dpre, P, C, ys, db, ws, st, defer);
 }
 
+// 32-bit index arithmetic for a pool: pixel counts below 2^24 (24-bit multiplies), strides and
+// channel counts below 2^24, and every element offset below 2^29 (byte offsets below 2^31 for fp32).
+static bool pool_o32(const PoolGeom &g, int64_t pys) {
+    constexpr int64_t k24 = 1 << 24, k29 = 1ll << 29;
+    const int64_t P = (int64_t)g.N * g.H * g.W, Q = (int64_t)g.N * g.OH * g.OW;
+    return P < k24 && Q < k24 && g.C < k24 && g.xs < k24 && g.ys < k24 && pys < k24 && P * g.xs < k29 &&
+           Q * g.ys < k29 && Q * g.C < k29 && Q * pys < k29 && P * g.C < k29;
+}
+
 template <typename T, typename A>
 static hipError_t maxpool_relu_bwd_t(const void *dy, const A *am, const PoolGeom &g, const void *y,
                                      const void *py, int64_t pys, void *dpre, float beta, float *db, float *ws,
@@ -1294,25 +1331,35 @@ static hipError_t maxpool_relu_bwd_t(const void *dy, const A *am, const PoolGeom
         const int Gc = (int)gc;
         const int64_t cpb = (ncell + gc - 1) / gc;
         const FastDiv dCW((uint32_t)CW), dCH((uint32_t)CH);
-        if (g.KH == 3 && g.KW == 3)
-            hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A, 3>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am,
-                               g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
-        else if (g.KH == 2 && g.KW == 2)
-            hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A, 2>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am,
-                               g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
-        else
-            hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A, 0>), dim3(Gc), dim3(256), smem, st, (const T *)dy, am,
-                               g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, cpb, CH, CW, dCW, dCH, ws);
+        const bool o32 = pool_o32(g, py ? pys : 0);
+        auto go = [&](auto PK_, auto O_) {
+            constexpr int PK = decltype(PK_)::value;
+            constexpr bool O = decltype(O_)::value;
+            hipLaunchKernelGGL((maxpool_relu_bwd_cell_kernel<T, A, PK, O>), dim3(Gc), dim3(256), smem, st,
+                               (const T *)dy, am, g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, cpb, CH, CW,
+                               dCW, dCH, ws);
+        };
+        using I3 = std::integral_constant<int, 3>;
+        using I2 = std::integral_constant<int, 2>;
+        using I0 = std::integral_constant<int, 0>;
+        using BT = std::true_type;
+        using BF = std::false_type;
+        if (g.KH == 3 && g.KW == 3) o32 ? go(I3{}, BT{}) : go(I3{}, BF{});
+        else if (g.KH == 2 && g.KW == 2) o32 ? go(I2{}, BT{}) : go(I2{}, BF{});
+        else o32 ? go(I0{}, BT{}) : go(I0{}, BF{});
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         return finish_partials(ws, Gc, g.C, db, st, defer);
     }
-    if (vec)
-        hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, true, A>), dim3(G), dim3(256), smem, st, (const T *)dy, am,
-                           g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, ppb, dW, dH, ws);
+    if (vec && pool_o32(g, py ? pys : 0))
+        hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, true, A, true>), dim3(G), dim3(256), smem, st,
+                           (const T *)dy, am, g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, ppb, dW, dH, ws);
+    else if (vec)
+        hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, true, A, false>), dim3(G), dim3(256), smem, st,
+                           (const T *)dy, am, g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, ppb, dW, dH, ws);
     else
-        hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, false, A>), dim3(G), dim3(256), smem, st, (const T *)dy,
-                           am, g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, ppb, dW, dH, ws);
+        hipLaunchKernelGGL((maxpool_relu_bwd_partial_kernel<T, false, A, false>), dim3(G), dim3(256), smem, st,
+                           (const T *)dy, am, g, (const T *)y, (const T *)py, pys, (T *)dpre, beta, ppb, dW, dH, ws);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return finish_partials(ws, G, g.C, db, st, defer);
@@ -1340,12 +1387,19 @@ static hipError_t maxpool_fwd_t(const void *x, const PoolGeom &g, void *y, A *am
     const int64_t work = (int64_t)g.N * g.OH * g.OW * cv;
     const int grid = grid_for(work, 256, 16384);
     const Decode dec = make_decode(cv, g.OW, g.OH, work);
-    if (vec && g.KH == 3 && g.KW == 3)
-        hipLaunchKernelGGL((maxpool_fwd_win_kernel<T, 3, 3, A>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y,
-                           am, dec);
+    const bool o32 = pool_o32(g, 0);
+    if (vec && g.KH == 3 && g.KW == 3 && o32)
+        hipLaunchKernelGGL((maxpool_fwd_win_kernel<T, 3, 3, A, true>), dim3(grid), dim3(256), 0, st, (const T *)x, g,
+                           (T *)y, am, dec);
+    else if (vec && g.KH == 3 && g.KW == 3)
+        hipLaunchKernelGGL((maxpool_fwd_win_kernel<T, 3, 3, A, false>), dim3(grid), dim3(256), 0, st, (const T *)x, g,
+                           (T *)y, am, dec);
+    else if (vec && g.KH == 2 && g.KW == 2 && o32)
+        hipLaunchKernelGGL((maxpool_fwd_win_kernel<T, 2, 2, A, true>), dim3(grid), dim3(256), 0, st, (const T *)x, g,
+                           (T *)y, am, dec);
     else if (vec && g.KH == 2 && g.KW == 2)
-        hipLaunchKernelGGL((maxpool_fwd_win_kernel<T, 2, 2, A>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y,
-                           am, dec);
+        hipLaunchKernelGGL((maxpool_fwd_win_kernel<T, 2, 2, A, false>), dim3(grid), dim3(256), 0, st, (const T *)x, g,
+                           (T *)y, am, dec);
     else if (vec)
         hipLaunchKernelGGL((maxpool_fwd_kernel<T, true, A>), dim3(grid), dim3(256), 0, st, (const T *)x, g, (T *)y, am,
                            dec);
@@ -1372,12 +1426,15 @@ static hipError_t maxpool_bwd_t(const void *dy, const A *am, const PoolGeom &g, 
     const int64_t work = (int64_t)g.N * g.H * g.W * cv;
     const int grid = grid_for(work, 256, 16384);
     const Decode dec = make_decode(cv, g.W, g.H, work);
-    if (vec)
-        hipLaunchKernelGGL((maxpool_bwd_kernel<T, true, A>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g, beta,
-                           (T *)dx, dec);
+    if (vec && pool_o32(g, 0))
+        hipLaunchKernelGGL((maxpool_bwd_kernel<T, true, A, true>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g,
+                           beta, (T *)dx, dec);
+    else if (vec)
+        hipLaunchKernelGGL((maxpool_bwd_kernel<T, true, A, false>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g,
+                           beta, (T *)dx, dec);
     else
-        hipLaunchKernelGGL((maxpool_bwd_kernel<T, false, A>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g, beta,
-                           (T *)dx, dec);
+        hipLaunchKernelGGL((maxpool_bwd_kernel<T, false, A, false>), dim3(grid), dim3(256), 0, st, (const T *)dy, am, g,
+                           beta, (T *)dx, dec);
     return hipGetLastError();
 }
 
