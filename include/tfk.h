@@ -35,7 +35,10 @@
  *    Operations that need scratch memory take a caller-provided workspace
  *    sized by the matching *_workspace_bytes query.
  *  - Aliasing: outputs must not overlap inputs except where an argument is
- *    documented as in-place.  A detected overlap returns TFK_ERR_ALIAS.
+ *    documented as in-place.  A detected overlap returns TFK_ERR_ALIAS.  Two
+ *    NHWC views with one pixel stride overlap only if they share an element:
+ *    channel slices of one buffer that lie side by side within every pixel
+ *    (say a concat's branches, one read while another is written) do not.
  *  - An empty batch (n == 0) is valid: nothing is read; reductions over the
  *    batch (filter and bias gradients) are written as zeros.  Pointers of
  *    empty tensors may be NULL.

@@ -94,6 +94,19 @@ bool overlap(const void *a, int64_t abytes, const void *b, int64_t bbytes) {
 
 bool aligned(const void *p, int64_t a) { return ((uintptr_t)p % (uintptr_t)a) == 0; }
 
+// Whether two NHWC views may share an element.  Besides disjoint byte ranges, two views with one
+// pixel stride whose channels lie side by side within every pixel (channel slices of one buffer,
+// e.g. a concat's branches) share none: b's channels start d bytes into a's pixel period, with
+// a's channels before d and b's ending within the period.
+bool nhwc_overlap(const void *a, const tfk_nhwc &ad, const void *b, const tfk_nhwc &bd, int64_t es) {
+    if (!overlap(a, view_bytes(ad, es), b, view_bytes(bd, es))) return false;
+    if (ad.pixel_stride != bd.pixel_stride || ad.pixel_stride <= 0) return true;
+    const int64_t S = ad.pixel_stride * es;
+    int64_t d = ((int64_t)(intptr_t)b - (int64_t)(intptr_t)a) % S;
+    if (d < 0) d += S;
+    return !(d >= (int64_t)ad.c * es && d + (int64_t)bd.c * es <= S);
+}
+
 tfk_status need_ptr(const void *p, const char *name) {
     if (!p) return fail(TFK_ERR_NULL, "%s is NULL", name);
     return TFK_OK;
@@ -283,7 +296,7 @@ static tfk_status conv_fwd_check(const void *x, tfk_nhwc &xd, const void *w, int
     TRY(need_align(w, es, "w"));
     TRY(need_align(y, es, "y"));
     const int64_t yb = view_bytes(yd, es);
-    if (overlap(y, yb, x, view_bytes(xd, es)) || overlap(y, yb, w, filter_bytes(s, es)))
+    if (nhwc_overlap(y, yd, x, xd, es) || overlap(y, yb, w, filter_bytes(s, es)))
         return fail(TFK_ERR_ALIAS, "y overlaps x or w");
     if (bias != nullptr && overlap(y, yb, bias, (int64_t)cout * 4)) return fail(TFK_ERR_ALIAS, "y overlaps bias");
     const int64_t xbytes = view_bytes(xd, es), wbytes = filter_bytes(s, es);
@@ -343,7 +356,7 @@ tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void *w, tfk
     TRY(need_align(w, es, "w"));
     TRY(need_align(dx, es, "dx"));
     const int64_t xb = view_bytes(dxd, es);
-    if (overlap(dx, xb, dy, view_bytes(dyd, es)) || overlap(dx, xb, w, filter_bytes(s, es)))
+    if (nhwc_overlap(dx, dxd, dy, dyd, es) || overlap(dx, xb, w, filter_bytes(s, es)))
         return fail(TFK_ERR_ALIAS, "dx overlaps dy or w");
     const int64_t wbytes = filter_bytes(s, es);
     int64_t xs = dxd.pixel_stride;
@@ -385,7 +398,7 @@ tfk_status tfk_conv2d_bwd_input_relu_bwd(const void *dy, tfk_nhwc dyd, const voi
     TRY(need_align(y, es, "y"));
     TRY(need_align(dpre, es, "dpre"));
     const int64_t xb = view_bytes(xd, es), yb = view_bytes(dyd, es), wb = filter_bytes(s, es), bb = (int64_t)xd.c * 4;
-    if (overlap(dpre, xb, dy, yb) || overlap(dpre, xb, w, wb) || overlap(dpre, xb, y, xb))
+    if (nhwc_overlap(dpre, xd, dy, dyd, es) || overlap(dpre, xb, w, wb) || nhwc_overlap(dpre, xd, y, xd, es))
         return fail(TFK_ERR_ALIAS, "dpre overlaps dy, w or y");
     if (overlap(dbias, bb, dy, yb) || overlap(dbias, bb, w, wb) || overlap(dbias, bb, y, xb) ||
         overlap(dbias, bb, dpre, xb))

@@ -45,15 +45,65 @@ def _align(n: int) -> int:
     return (n + _ALIGN - 1) // _ALIGN * _ALIGN
 
 
+def _merge_groups(net: Net):
+    """1x1 convolutions (stride 1, ReLU) that read one tensor, at least two of them, each writing
+    either a tensor of its own or the first channels of a concat tensor (at most one per group).
+    Their outputs are laid out side by side in one buffer -- the own tensors first, then the concat
+    whose first channels that one writes -- so that one convolution with their filters side by side
+    (a wider 1x1) computes them all: one pass over the input per direction instead of one per
+    member (an inception module's branch reductions)."""
+    if net.dtype != "bf16":
+        return []
+    writers = {}
+    for op in net.ops:
+        writers.setdefault(op.dst, []).append(op)
+    pos = {op.name: k for k, op in enumerate(net.ops)}
+    cand = {}
+    for c in net.convs:
+        if not (c.kh == c.kw == 1 and c.sh == c.sw == 1 and tuple(c.pads) == (0, 0, 0, 0) and c.relu):
+            continue
+        if c.dst in ("x", net.output):
+            continue
+        k = pos[c.name]
+        nxt = net.ops[k + 1] if k + 1 < len(net.ops) else None
+        if isinstance(nxt, Pool) and nxt.src == c.dst:
+            continue                                  # (its forward runs with that pool)
+        cand.setdefault(c.src, []).append(c)
+    groups, used = [], set()
+    for src, cs in cand.items():
+        own = [c for c in cs if c.dst_c0 == 0 and c.cout == net.tensors[c.dst][3] and writers[c.dst] == [c]
+               and c.dst not in used]
+        cat = [c for c in cs if c not in own and c.dst_c0 == 0 and c.dst not in used]
+        members = own + cat[:1]
+        if len(members) < 2:
+            continue
+        offs, w = {}, 0
+        for c in own:
+            offs[c.dst] = w
+            w += c.cout
+        catt = cat[0].dst if cat else None
+        if catt is not None:
+            offs[catt] = w
+            w += net.tensors[catt][3]
+        used.update(offs)
+        first = min(members, key=lambda c: pos[c.name])
+        mconv = Conv(name="merged_" + first.name, src=src, dst="merged_" + first.name, dst_c0=0,
+                     cout=sum(c.cout for c in members), kh=1, kw=1, sh=1, sw=1, pads=(0, 0, 0, 0))
+        groups.append({"op": mconv, "members": members, "offs": offs, "width": w, "cat": catt,
+                       "at": pos[first.name]})
+    return groups
+
+
 class Replica:
     """Device state of one replica of ``net`` and its training step."""
 
     def __init__(self, net: Net, inputs: Inputs, device: str = "cuda", optimizer: str = "sgd",
                  momentum: float = 0.9, nesterov: bool = False, beta1: float = 0.9, beta2: float = 0.999,
-                 epsilon: float = 1e-8):
+                 epsilon: float = 1e-8, merge: bool = True):
         """``optimizer`` picks the in-place variable update that ends the step: "sgd"
         (ApplyGradientDescent), "momentum" (velocity slot, optional look-ahead form) or "adam"
-        (two moment slots, bias-corrected by the step count)."""
+        (two moment slots, bias-corrected by the step count).  ``merge``: run each group of 1x1
+        convolutions that read one tensor as one wider convolution (see _merge_groups)."""
         if optimizer not in ("sgd", "momentum", "adam"):
             raise ValueError("optimizer is 'sgd', 'momentum' or 'adam'")
         self.net = net
@@ -65,25 +115,46 @@ class Replica:
         self.lr = float(np.float32(net.lr))
         dev, dt = self.device, self.dtype
 
+        # ---- 1x1 convolutions merged into one (their outputs side by side in one buffer)
+        self.merges = _merge_groups(net) if merge else []
+        member_of = {c.name: g for g in self.merges for c in g["members"]}
+        store = {}                                   # tensor -> (storage name, first channel)
+        for g in self.merges:
+            for t, o in g["offs"].items():
+                store[t] = (g["op"].name, o)
+
         # ---- variables
-        # Filters first; then the biases, those of the convolutions that write one tensor side
-        # by side in channel order (a concat's branches), so that a group of them has one
-        # contiguous bias-gradient slice (see relu_groups below).
+        # Filters first (a merged group's filters side by side as one HWIO block); then the
+        # biases, in the channel order of the buffers the convolutions write (a concat's
+        # branches, a merged group's members), so that a group of them has one contiguous
+        # bias(-gradient) slice (see relu_groups and merges).
         off = 0
         self._layout = {}
-        wofs = {}
+        self._wslot = {}                             # name -> (block offset, block shape, first channel)
         for c in net.convs:
+            g = member_of.get(c.name)
+            if g is not None and g["op"].name in self._wslot:
+                continue
             cin = net.tensors[c.src][3]
-            wn = c.kh * c.kw * cin * c.cout
-            wofs[c.name] = (off, (c.kh, c.kw, cin, c.cout))
-            off += _align(wn)
-        by_dst = {}
+            cout = g["op"].cout if g is not None else c.cout
+            key = g["op"].name if g is not None else c.name
+            self._wslot[key] = (off, (c.kh, c.kw, cin, cout), 0)
+            off += _align(c.kh * c.kw * cin * cout)
+        for g in self.merges:
+            bo, shp, _ = self._wslot[g["op"].name]
+            a = 0
+            for c in g["members"]:
+                self._wslot[c.name] = (bo, shp, a)
+                a += c.cout
+        by_store = {}
         for c in net.convs:
-            by_dst.setdefault(c.dst, []).append(c)
-        for dst, cs in by_dst.items():
+            st, base = store.get(c.dst, (c.dst, 0))
+            by_store.setdefault(st, []).append((base + c.dst_c0, c))
+        for st, cs in by_store.items():
             off = _align(off)
-            for c in sorted(cs, key=lambda c: c.dst_c0):
-                self._layout[c.name] = wofs[c.name] + (off, c.cout)
+            for _, c in sorted(cs, key=lambda e: e[0]):
+                wo, wshape, a = self._wslot[c.name]
+                self._layout[c.name] = (wo, wshape, off, c.cout)
                 off += c.cout
         off = _align(off)
         self.n_params = off
@@ -95,8 +166,8 @@ class Replica:
         self.slots = [torch.zeros(off, dtype=torch.float32, device=dev) for _ in range(n_slots)]
         host = np.zeros(off, dtype=np.float32)
         for c in net.convs:
+            self.place_filter(host, c.name, inputs.weights[c.name])
             wo, wshape, bo, bn = self._layout[c.name]
-            host[wo:wo + int(np.prod(wshape))] = inputs.weights[c.name].astype(np.float32).ravel()
             host[bo:bo + bn] = inputs.biases[c.name].astype(np.float32)
         p = torch.from_numpy(host)
         if dt == torch.bfloat16:
@@ -105,15 +176,32 @@ class Replica:
         if self.shadow is not None:
             self.shadow.copy_(self.params.to(torch.bfloat16))
         self.W, self.b, self.dW, self.db, self.Wlp = {}, {}, {}, {}, {}
+        blocks = {}
+        for key, (wo, wshape, a) in self._wslot.items():
+            if a == 0 and key not in member_of:
+                wn = int(np.prod(wshape))
+                blocks[key] = (self.params[wo:wo + wn].view(wshape), self.grads[wo:wo + wn].view(wshape),
+                               self.shadow[wo:wo + wn].view(wshape) if self.shadow is not None else None)
         for c in net.convs:
-            wo, wshape, bo, bn = self._layout[c.name]
-            wn = int(np.prod(wshape))
-            self.W[c.name] = self.params[wo:wo + wn].view(wshape)
-            self.dW[c.name] = self.grads[wo:wo + wn].view(wshape)
+            g = member_of.get(c.name)
+            wo, wshape, a = self._wslot[c.name]
+            W, dW, Wlp = blocks[g["op"].name if g is not None else c.name]
+            sl = (Ellipsis, slice(a, a + c.cout))
+            self.W[c.name], self.dW[c.name] = W[sl], dW[sl]
+            self.Wlp[c.name] = Wlp[sl] if Wlp is not None else self.W[c.name]
+            _, _, bo, bn = self._layout[c.name]
             self.b[c.name] = self.params[bo:bo + bn]
             self.db[c.name] = self.grads[bo:bo + bn]
-            self.Wlp[c.name] = (self.shadow[wo:wo + wn].view(wshape) if self.shadow is not None
-                                else self.W[c.name])
+        # the merged convolutions' dense filters and contiguous biases
+        self.mW, self.mWlp, self.mdW, self.mb, self.mdb = {}, {}, {}, {}, {}
+        for g in self.merges:
+            name = g["op"].name
+            W, dW, Wlp = blocks[name]
+            self.mW[name], self.mdW[name] = W, dW
+            self.mWlp[name] = Wlp if Wlp is not None else W
+            bo = self._layout[g["members"][0].name][2]
+            self.mb[name] = self.params[bo:bo + g["op"].cout]
+            self.mdb[name] = self.grads[bo:bo + g["op"].cout]
 
         # ---- activations, gradients, argmax
         self.act: Dict[str, torch.Tensor] = {}
@@ -141,6 +229,29 @@ class Replica:
             if name == net.output or (name == "x" and not net.input_grad):
                 continue
             self.grad[name] = torch.zeros(shape, dtype=dt, device=dev)
+        # merged groups: one buffer each for the activations and one for the gradients, the
+        # members' tensors (and the concat) channel slices of it
+        self.m_act, self.m_grad = {}, {}
+        for g in self.merges:
+            shape = net.tensors[g["members"][0].dst][:3] + (g["width"],)
+            A = torch.zeros(shape, dtype=dt, device=dev)
+            G = torch.zeros(shape, dtype=dt, device=dev)
+            for t, o in g["offs"].items():
+                w = net.tensors[t][3]
+                self.act[t] = A[..., o:o + w]
+                self.grad[t] = G[..., o:o + w]
+            self.m_act[g["op"].name] = A[..., :g["op"].cout]
+            self.m_grad[g["op"].name] = G[..., :g["op"].cout]
+        # the ops the step runs: each merged group's members replaced by its convolution, at the
+        # place of its first member
+        merged_at = {g["at"]: g["op"] for g in self.merges}
+        self.ops = []
+        for k, op in enumerate(net.ops):
+            if k in merged_at:
+                self.ops.append(merged_at[k])
+            if op.name not in member_of:
+                self.ops.append(op)
+        self.merged = {g["op"].name: g for g in self.merges}
         # ReLU-backward of the ops that write the output tensor must not overwrite the seed g
         self.dpre_out = torch.zeros(net.tensors[net.output], dtype=dt, device=dev)
         # each max-pool's selection as uint8 window taps (windows of at most 256 taps)
@@ -176,6 +287,9 @@ class Replica:
         # ReLU backward runs once over the whole range, with one bias-gradient reduction into
         # their adjacent bias-gradient slices
         pos = {op.name: k for k, op in enumerate(net.ops)}
+        by_dst = {}
+        for c in net.convs:
+            by_dst.setdefault(c.dst, []).append(c)
         self.relu_groups = {}                    # conv name -> (first channel, width, [convs])
         for dst, cs in by_dst.items():
             cand = sorted((c for c in cs if c.relu and c.name not in self.relu_fused and dst != net.output),
@@ -215,10 +329,14 @@ class Replica:
             need = max(need, ops.bias_relu_bwd_workspace_bytes(self._slice(self.act, c)))
         for c0, width, run in {id(g[2]): g for g in self.relu_groups.values()}.values():
             need = max(need, ops.bias_relu_bwd_workspace_bytes(self.act[run[0].dst][..., c0:c0 + width]))
+        for g in self.merges:
+            m = g["op"]
+            for op_kind in (0, 1):
+                need = max(need, ops.conv2d_workspace_bytes(op_kind, self.act[m.src], m.cout, 1, 1, (1, 1), m.pads))
         self.ws = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=dev)
         # ---- filter gradients run on a second stream, with a workspace of their own
         need = 0
-        for c in net.convs:
+        for c in list(net.convs) + [g["op"] for g in self.merges]:
             need = max(need, ops.conv2d_workspace_bytes(2, self.act[c.src], c.cout, c.kh, c.kw, (c.sh, c.sw),
                                                         c.pads))
         self.ws_side = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=dev)
@@ -229,6 +347,13 @@ class Replica:
         self.bias_ws: Dict[object, torch.Tensor] = {}
 
     # ------------------------------------------------------------------ helpers
+    def place_filter(self, flat, name: str, w) -> None:
+        """Writes filter ``w`` (HWIO) of convolution ``name`` where the flat variable layout keeps
+        it: its own block, or its channels of its merged group's block."""
+        wo, (kh, kw, cin, cout), a = self._wslot[name]
+        blk = flat[wo:wo + kh * kw * cin * cout].reshape(kh, kw, cin, cout)
+        blk[..., a:a + w.shape[3]] = w
+
     def _bias_ws(self, key, need: int) -> torch.Tensor:
         """The workspace of one deferred bias gradient, made at its first use and kept (a recorded
         program finds its partials where its calls left them)."""
@@ -247,8 +372,14 @@ class Replica:
 
     # ------------------------------------------------------------------ the step
     def forward(self, trace=None, stream=None):
-        for op in self.net.ops:
+        for op in self.ops:
             x = self.act[op.src]
+            if op.name in self.merged:
+                y, w, b = self.m_act[op.name], self.mWlp[op.name], self.mb[op.name]
+                if trace: trace("conv_bias_relu_fwd", op, stream=stream, x=x, w=w, b=b, y=y)
+                ops.conv2d_fwd_bias_relu(x, w, b, (1, 1), op.pads, y=y, ws=self.ws, stream=stream)
+                if trace: trace("conv_bias_relu_fwd:end", op, stream=stream, y=y)
+                continue
             y = self._slice(self.act, op)
             if isinstance(op, Conv) and not op.relu:
                 # a classifier's logits: the bias is added inside the cross-entropy kernel
@@ -295,6 +426,51 @@ class Replica:
         """The last step's batch-mean cross-entropy (host copy; synchronises)."""
         return float(self.loss_rows.double().mean())
 
+    def _relu_backward(self, op, dy, trace, stream, defer, jobs, grouped):
+        """The ReLU (or bias-only) backward of convolution ``op``'s output gradient ``dy``, unless a
+        fused kernel forms it (a pool's or a consumer's input gradient); returns the gradient
+        before the ReLU, the one its filter and input gradients read."""
+        net = self.net
+        if not op.relu:
+            dpre = dy                        # bias only: the gradient passes through
+            if trace: trace("bias_bwd", op, stream=stream, dy=dy)
+            if defer:
+                ws = self._bias_ws(("bias", op.name), ops.bias_relu_bwd_workspace_bytes(dy))
+                jobs.append((ops.bias_relu_bwd(None, dy, dpre=dpre, ws=ws, stream=stream, defer=True)[1],
+                             self.db[op.name]))
+            else:
+                ops.bias_relu_bwd(None, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
+            if trace: trace("bias_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
+        elif op.name in self.relu_fused:
+            dpre = dy                        # written by the fused pool / input-gradient backward
+        elif op.name in self.relu_groups:
+            dpre = dy
+            c0, width, run = self.relu_groups[op.name]
+            if id(run) not in grouped:       # the group's last convolution in forward order
+                grouped.add(id(run))
+                yg, dyg = self.act[op.dst][..., c0:c0 + width], self.grad[op.dst][..., c0:c0 + width]
+                dbg = self.grads[self._layout[run[0].name][2]:self._layout[run[0].name][2] + width]
+                if trace: trace("bias_relu_bwd", op, stream=stream, y=yg, dy=dyg)
+                if defer:
+                    ws = self._bias_ws(("group", op.dst, c0), ops.bias_relu_bwd_workspace_bytes(yg))
+                    jobs.append((ops.bias_relu_bwd(yg, dyg, dpre=dyg, ws=ws, stream=stream, defer=True)[1],
+                                 dbg))
+                else:
+                    ops.bias_relu_bwd(yg, dyg, dpre=dyg, dbias=dbg, ws=self.ws, stream=stream)
+                if trace: trace("bias_relu_bwd:end", op, stream=stream, dpre=dyg, db=dbg)
+        else:
+            y = self._slice(self.act, op)
+            dpre = self._slice({op.dst: self.dpre_out}, op) if op.dst == net.output else dy
+            if trace: trace("bias_relu_bwd", op, stream=stream, y=y, dy=dy)
+            if defer:
+                ws = self._bias_ws(("relu", op.name), ops.bias_relu_bwd_workspace_bytes(y))
+                jobs.append((ops.bias_relu_bwd(y, dy, dpre=dpre, ws=ws, stream=stream, defer=True)[1],
+                             self.db[op.name]))
+            else:
+                ops.bias_relu_bwd(y, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
+            if trace: trace("bias_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
+        return dpre
+
     def backward(self, trace=None, stream=None, side=None):
         """Gradients of every variable.  With ``side`` (a second stream), the filter gradient
         of each convolution that also has an input gradient runs there, concurrently with that
@@ -308,49 +484,34 @@ class Replica:
         # (traced steps form each bias gradient at once, so that the tracer can check it)
         defer = trace is None and self.defer_bias
         jobs = []                                # deferred bias gradients: (partials, dbias)
-        for op in reversed(net.ops):
-            dy = self._slice(self.grad, op)
+        for op in reversed(self.ops):
+            dy = self._slice(self.grad, op) if op.name not in self.merged else None
             src_grad = op.src != "x" or net.input_grad
             beta = 1.0 if op.src in written else 0.0
+            if op.name in self.merged:
+                # each member's ReLU backward (most are fused into other kernels), then the merged
+                # filter and input gradients over the members' adjacent gradient channels
+                for m in self.merged[op.name]["members"]:
+                    self._relu_backward(m, self._slice(self.grad, m), trace, stream, defer, jobs, grouped)
+                dpre, x = self.m_grad[op.name], self.act[op.src]
+                on_side = side is not None and src_grad
+                if on_side:
+                    ops.stream_wait(side, cur)
+                fs = side if on_side else stream
+                dw = self.mdW[op.name]
+                if trace: trace("conv_bwd_filter", op, stream=fs, x=x, dy=dpre)
+                ops.conv2d_bwd_filter(x, dpre, (1, 1), (1, 1), op.pads, dw=dw,
+                                      ws=self.ws_side if on_side else self.ws, stream=fs)
+                if trace: trace("conv_bwd_filter:end", op, stream=fs, dw=dw)
+                if src_grad:
+                    dx, w = self.grad[op.src], self.mWlp[op.name]
+                    if trace: trace("conv_bwd_input", op, stream=stream, dy=dpre, w=w, dx=dx, beta=beta)
+                    ops.conv2d_bwd_input(dpre, w, dx, (1, 1), op.pads, beta=beta, ws=self.ws, stream=stream)
+                    if trace: trace("conv_bwd_input:end", op, stream=stream, dx=dx)
+                    written.add(op.src)
+                continue
             if isinstance(op, Conv):
-                if not op.relu:
-                    dpre = dy                        # bias only: the gradient passes through
-                    if trace: trace("bias_bwd", op, stream=stream, dy=dy)
-                    if defer:
-                        ws = self._bias_ws(("bias", op.name), ops.bias_relu_bwd_workspace_bytes(dy))
-                        jobs.append((ops.bias_relu_bwd(None, dy, dpre=dpre, ws=ws, stream=stream, defer=True)[1],
-                                     self.db[op.name]))
-                    else:
-                        ops.bias_relu_bwd(None, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
-                    if trace: trace("bias_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
-                elif op.name in self.relu_fused:
-                    dpre = dy                        # written by the fused pool / input-gradient backward
-                elif op.name in self.relu_groups:
-                    dpre = dy
-                    c0, width, run = self.relu_groups[op.name]
-                    if id(run) not in grouped:       # the group's last convolution in forward order
-                        grouped.add(id(run))
-                        yg, dyg = self.act[op.dst][..., c0:c0 + width], self.grad[op.dst][..., c0:c0 + width]
-                        dbg = self.grads[self._layout[run[0].name][2]:self._layout[run[0].name][2] + width]
-                        if trace: trace("bias_relu_bwd", op, stream=stream, y=yg, dy=dyg)
-                        if defer:
-                            ws = self._bias_ws(("group", op.dst, c0), ops.bias_relu_bwd_workspace_bytes(yg))
-                            jobs.append((ops.bias_relu_bwd(yg, dyg, dpre=dyg, ws=ws, stream=stream, defer=True)[1],
-                                         dbg))
-                        else:
-                            ops.bias_relu_bwd(yg, dyg, dpre=dyg, dbias=dbg, ws=self.ws, stream=stream)
-                        if trace: trace("bias_relu_bwd:end", op, stream=stream, dpre=dyg, db=dbg)
-                else:
-                    y = self._slice(self.act, op)
-                    dpre = self._slice({op.dst: self.dpre_out}, op) if op.dst == net.output else dy
-                    if trace: trace("bias_relu_bwd", op, stream=stream, y=y, dy=dy)
-                    if defer:
-                        ws = self._bias_ws(("relu", op.name), ops.bias_relu_bwd_workspace_bytes(y))
-                        jobs.append((ops.bias_relu_bwd(y, dy, dpre=dpre, ws=ws, stream=stream, defer=True)[1],
-                                     self.db[op.name]))
-                    else:
-                        ops.bias_relu_bwd(y, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
-                    if trace: trace("bias_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
+                dpre = self._relu_backward(op, dy, trace, stream, defer, jobs, grouped)
                 x = self.act[op.src]
                 # a filter gradient with no input gradient beside it (the first layer) stays
                 # on the main stream, where it is next on the critical path

@@ -141,6 +141,15 @@ class ParityTracer:
         for c in net.convs:
             self.state[("W", c.name)] = np.asarray(inputs.weights[c.name], np.float64)
             self.state[("b", c.name)] = np.asarray(inputs.biases[c.name], np.float64)
+        # merged 1x1 groups: their filters side by side, as the replica holds them
+        self.member_of = {}
+        for g in getattr(rep, "merges", []):
+            name = g["op"].name
+            self.state[("W", name)] = np.concatenate([self.state[("W", m.name)] for m in g["members"]], axis=3)
+            a = 0
+            for m in g["members"]:
+                self.member_of[m.name] = (name, a)
+                a += m.cout
         # every buffer an op reads or writes, under the oracle state key that mirrors it;
         # NHWC batch buffers may be viewed as channel slices, the variables only whole
         self.batched = [(("act", nm), t) for nm, t in rep.act.items()]
@@ -150,6 +159,8 @@ class ParityTracer:
         self.whole += [(("b", nm), t) for nm, t in rep.b.items()]
         self.whole += [(("dW", nm), t) for nm, t in rep.dW.items()]
         self.whole += [(("db", nm), t) for nm, t in rep.db.items()]
+        self.whole += [(("W", nm), t) for nm, t in getattr(rep, "mWlp", {}).items()]
+        self.whole += [(("dW", nm), t) for nm, t in getattr(rep, "mdW", {}).items()]
 
     # -------------------------------------------------------------- buffers
     def _lookup(self, t):
@@ -169,7 +180,38 @@ class ParityTracer:
                 return key, c0, tuple(b.shape)
         raise KeyError("tensor at %#x %s is none of the replica's buffers" % (p, tuple(t.shape)))
 
+    def _chan_spans(self, t):
+        """A 4-D view whose channels are several batch buffers side by side in one allocation (a
+        merged group's outputs or gradients): [(key, first channel in the buffer, first channel
+        in t, width)] covering t's channels in order, or None."""
+        if t.dim() != 4:
+            return None
+        es, p, width = t.element_size(), t.data_ptr(), t.shape[3]
+        parts = []
+        for key, b in self.batched:
+            if (b.dtype != t.dtype or b.dim() != 4 or tuple(b.shape[:3]) != tuple(t.shape[:3])
+                    or b.stride() != t.stride()):
+                continue
+            d = (b.data_ptr() - p) // es                 # b's channel 0 in t's channel numbering
+            if (b.data_ptr() - p) % es or d >= width or d + b.shape[3] <= 0:
+                continue
+            lo, hi = max(0, d), min(width, d + b.shape[3])
+            parts.append((lo, key, lo - d, hi - lo))
+        parts.sort(key=lambda e: e[0])
+        at = 0
+        for lo, _, _, w in parts:
+            if lo != at:
+                return None
+            at += w
+        return [(key, bc0, lo, w) for lo, key, bc0, w in parts] if at == width and len(parts) > 1 else None
+
     def _get(self, t):
+        spans = self._chan_spans(t)
+        if spans is not None:
+            return np.concatenate([self.state[key][..., bc0:bc0 + w] for key, bc0, _, w in spans], axis=3)
+        vspans = self._spans(t)
+        if vspans is not None:                           # (a merged group's biases side by side)
+            return np.concatenate([np.asarray(self.state[key], np.float64).reshape(-1) for key, _, _ in vspans])
         key, c0, _ = self._lookup(t)
         v = self.state[key]
         return v if c0 is None else v[..., c0:c0 + t.shape[3]]
@@ -195,6 +237,14 @@ class ParityTracer:
             for key, off, m in spans:
                 self.state[key] = np.array(v[off:off + m], np.float64)
             return
+        cspans = self._chan_spans(t)
+        if cspans is not None:
+            for key, bc0, tc0, w in cspans:
+                if key not in self.state:
+                    shape = next(tuple(b.shape) for k, b in self.batched if k == key)
+                    self.state[key] = np.zeros((self.k,) + shape[1:])
+                self.state[key][..., bc0:bc0 + w] = v[..., tc0:tc0 + w]
+            return
         key, c0, shape = self._lookup(t)
         if c0 is None:
             self.state[key] = np.array(v, np.float64)
@@ -216,7 +266,13 @@ class ParityTracer:
         """Overwrite t with the oracle's value of its buffer rounded to t's type; returns the
         rounded value (k images for a batch tensor) in fp64."""
         r = self._round(self._get(t), t.dtype)
-        self._write(t, r, self._lookup(t)[1] is not None)
+        if self._chan_spans(t) is not None:
+            batched = True
+        elif self._spans(t) is not None:
+            batched = False
+        else:
+            batched = self._lookup(t)[1] is not None
+        self._write(t, r, batched)
         return r.to(torch.float64).numpy()
 
     def _force_argmax(self, t, op, x_shape):
@@ -494,8 +550,15 @@ class ParityTracer:
         flat = np.zeros(rep.n_params, np.float64)
         for c in rep.net.convs:
             wo, wshape, bo, bn = rep._layout[c.name]
-            wv = self._round(self.state[(kind_w, c.name)], wdtype).to(torch.float32)
-            flat[wo:wo + int(np.prod(wshape))] = wv.to(torch.float64).numpy().ravel()
+            key = (kind_w, c.name)
+            if key not in self.state and c.name in self.member_of:
+                # (a merged group's member: its channels of the group's filter gradient)
+                name, a = self.member_of[c.name]
+                w = self.state[(kind_w, name)][..., a:a + c.cout]
+            else:
+                w = self.state[key]
+            wv = self._round(w, wdtype).to(torch.float32).to(torch.float64).numpy()
+            rep.place_filter(flat, c.name, wv)
             flat[bo:bo + bn] = self._round(self.state[(kind_b, c.name)], torch.float32).to(torch.float64).numpy()
         return flat
 

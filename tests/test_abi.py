@@ -459,3 +459,17 @@ def test_deferred_bias_validation(lib):
     assert finish(dbs=(P + 0x10002,)) == ALIGN
     assert finish(dbs=(P + 16,)) == ALIAS               # dbias inside the partials (4 x 8 floats)
     assert finish(n=2, parts=(P, P + 0x1000), rws=(4, 4), chans=(8, 8), dbs=(P + 0x10000, P + 0x10010)) == ALIAS
+
+
+def test_channel_slices_alias(lib):
+    """Two channel slices of one pixel-strided buffer overlap only where their channels do: the
+    check rejects sharing channels (nothing launched here)."""
+    W = Window(3, 3, 1, 1, 1, 1, 1, 1)
+    # x = channels 8..23 and y = channels 0..15 of one 4 x 4 image of 64-channel pixels
+    xd, yd = Nhwc(1, 4, 4, 16, 64), Nhwc(1, 4, 4, 16, 64)
+    st = lib.tfk_conv2d_fwd(vp(P + 16), xd, vp(P + 0x100000), 16, W, BF16, vp(P), yd, None, 0, None)
+    assert st == ALIAS
+    # dpre = channels 0..15 and dy = channels 12..27: the fused input gradient rejects them too
+    st = lib.tfk_conv2d_bwd_input(vp(P + 24), yd, vp(P + 0x100000), W, BF16, vp(P), xd, ctypes.c_float(0.0),
+                                  None, 0, None)
+    assert st == ALIAS
