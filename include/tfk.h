@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 14
+#define TFK_ABI_VERSION 15
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -184,23 +184,25 @@ TFK_API tfk_status tfk_conv2d_bwd_filter_noalloc(const void *x, tfk_nhwc xd, con
                                          tfk_window p, tfk_dtype dt, float *dw, void *stream);
 
 /*
- * Conv2DBackpropInput fused with the ReLU backward and bias gradient of the layer that
- * produced x (the hand-fused activation-gradient kernels of Section 5), for an x that is the
- * output y of BiasAdd + ReLU and feeds only this convolution:
- *   g        = the input gradient of tfk_conv2d_bwd_input (beta 0)
- *   dpre[i]  = y[i] > 0 ? g[i] : +0          (xd-shaped, rounded to dt once when stored)
+ * Conv2DBackpropInput fused with the ReLU backward and bias gradient of the layers that
+ * produced x (the hand-fused activation-gradient kernels of Section 5), for an x whose
+ * channels are all outputs y of BiasAdd + ReLU, when this convolution is the last of x's
+ * readers to add its gradient (beta = 1 adds it to what the others stored in dpre; Section
+ * 4.1's sum of the gradients of several paths):
+ *   g        = the input gradient of tfk_conv2d_bwd_input
+ *   dpre[i]  = y[i] > 0 ? beta * dpre[i] + g[i] : +0   (xd-shaped, rounded to dt once when stored)
  *   dbias[c] = sum over the pixels of dpre[., c]   (fp32, of the stored values)
- * It equals tfk_conv2d_bwd_input(..., dx = dpre, beta = 0) followed by tfk_bias_relu_bwd(y,
+ * It equals tfk_conv2d_bwd_input(..., dx = dpre, beta) followed by tfk_bias_relu_bwd(y,
  * dpre, ...) up to the order of the fp32 bias-gradient sums, without forming g in memory.
  *   dy, dyd, w, p, dt : as tfk_conv2d_bwd_input.
  *   y     : xd-shaped (the same view as dpre), the forward ReLU output; read only.
  *   dpre  : xd-shaped, overwritten; must not overlap dy, w, y or dbias.
  *   dbias : xd.c fp32 values, overwritten; or NULL: deferred (see tfk_bias_grad_finish).
  *   ws    : at least tfk_conv2d_workspace_bytes(3, xd, dyd.c, p, dt) bytes.
- * Requirements: xd.c <= 16384.  xd.n == 0 sets dbias to 0.
+ * Requirements: beta is 0 or 1 (else ARG); xd.c <= 16384.  xd.n == 0 sets dbias to 0.
  */
 TFK_API tfk_status tfk_conv2d_bwd_input_relu_bwd(const void *dy, tfk_nhwc dyd, const void *w, tfk_window p,
-                                         tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd,
+                                         tfk_dtype dt, const void *y, void *dpre, tfk_nhwc xd, float beta,
                                          float *dbias, void *ws, size_t ws_bytes, void *stream);
 
 /* Workspace needed by a convolution (of the Section 4.1 forward and gradient operations

@@ -66,7 +66,7 @@ def load(path: str = LIB_PATH):
     lib.tfk_conv2d_bwd_input.argtypes = [vp, Nhwc, vp, Window, st, vp, Nhwc, f32, vp, sz, vp]
     lib.tfk_conv2d_bwd_filter.argtypes = [vp, Nhwc, vp, Nhwc, Window, st, vp, vp, sz, vp]
     lib.tfk_conv2d_bwd_filter_noalloc.argtypes = [vp, Nhwc, vp, Nhwc, Window, st, vp, vp]
-    lib.tfk_conv2d_bwd_input_relu_bwd.argtypes = [vp, Nhwc, vp, Window, st, vp, vp, Nhwc, vp, vp, sz, vp]
+    lib.tfk_conv2d_bwd_input_relu_bwd.argtypes = [vp, Nhwc, vp, Window, st, vp, vp, Nhwc, f32, vp, vp, sz, vp]
     lib.tfk_conv2d_workspace_bytes.argtypes = [i32, Nhwc, i32, Window, st]
     lib.tfk_conv2d_workspace_bytes.restype = sz
     lib.tfk_bias_relu_fwd.argtypes = [vp, Nhwc, vp, st, vp]

@@ -373,11 +373,12 @@ tfk_status tfk_conv2d_bwd_input(const void *dy, tfk_nhwc dyd, const void *w, tfk
 }
 
 tfk_status tfk_conv2d_bwd_input_relu_bwd(const void *dy, tfk_nhwc dyd, const void *w, tfk_window p, tfk_dtype dt,
-                                         const void *y, void *dpre, tfk_nhwc xd, float *dbias, void *ws,
-                                         size_t ws_bytes, void *stream) {
-    RECORDED(tfk_conv2d_bwd_input_relu_bwd, dy, dyd, w, p, dt, y, dpre, xd, dbias, ws, ws_bytes, stream);
+                                         const void *y, void *dpre, tfk_nhwc xd, float beta, float *dbias,
+                                         void *ws, size_t ws_bytes, void *stream) {
+    RECORDED(tfk_conv2d_bwd_input_relu_bwd, dy, dyd, w, p, dt, y, dpre, xd, beta, dbias, ws, ws_bytes, stream);
     ConvShape s;
     TRY(check_conv(xd, dyd.c, p, dt, dyd, "dpre", "dy", s));
+    if (!(beta == 0.f || beta == 1.f)) return fail(TFK_ERR_ARG, "beta must be 0 or 1");
     if (xd.c > 16384) return fail(TFK_ERR_SHAPE, "conv2d_bwd_input_relu_bwd supports at most 16384 channels");
     TRY(need_align(dbias, 4, "dbias"));
     hipStream_t st = (hipStream_t)stream;
@@ -412,7 +413,7 @@ tfk_status tfk_conv2d_bwd_input_relu_bwd(const void *dy, tfk_nhwc dyd, const voi
         return fail(TFK_ERR_ALIAS, "workspace overlaps an operand");
     BiasPartials bp{nullptr, 0};
     TRY(hip_status(launch_conv_bwd_data_relu(dti, dy, dyd.pixel_stride ? dyd.pixel_stride : dyd.c, w, dpre, xs, y,
-                                             dbias, (float *)ws, s, st, dbias ? nullptr : &bp),
+                                             beta, dbias, (float *)ws, s, st, dbias ? nullptr : &bp),
                    "conv2d_bwd_input_relu_bwd"));
     if (dbias == nullptr) note_partials(bp.part, bp.rows);
     return ok();

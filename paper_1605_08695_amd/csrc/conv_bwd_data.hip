@@ -41,7 +41,7 @@ static size_t split_ws_bytes(int dt, const ConvShape &s, bool relu) {
 size_t conv_bwd_data_ws_bytes(int dt, const ConvShape &s) { return split_ws_bytes(dt, s, false); }
 
 // ws: workspace (split-K partials; with relu_y also the bias-gradient partials).
-// relu_y: the fused ReLU backward (beta 0); *db_parts / *db_at receive the number and place of
+// relu_y: the fused ReLU backward (of beta dx + the gradient); *db_parts / *db_at receive the number and place of
 // the bias-gradient partial rows, or 0 when the fused kernels do not apply (nothing is launched
 // then).
 template <typename T>
@@ -119,12 +119,12 @@ size_t conv_bwd_data_relu_ws_bytes(int dt, const ConvShape &s, int64_t dxs) {
 }
 
 hipError_t launch_conv_bwd_data_relu(int dt, const void *dy, int64_t dys, const void *w, void *dpre, int64_t dxs,
-                                     const void *y, float *db, float *ws, const ConvShape &s, hipStream_t st,
-                                     BiasPartials *defer) {
+                                     const void *y, float beta, float *db, float *ws, const ConvShape &s,
+                                     hipStream_t st, BiasPartials *defer) {
     int parts = 0;
     float *db_at = nullptr;
     if (dt == 1 && ((uintptr_t)y & 7) == 0) {
-        const hipError_t e = conv_bwd_data_t<bf16_t>(dy, dys, w, dpre, dxs, 0.f, s, st, ws, y, &parts, &db_at);
+        const hipError_t e = conv_bwd_data_t<bf16_t>(dy, dys, w, dpre, dxs, beta, s, st, ws, y, &parts, &db_at);
         if (e != hipSuccess) return e;
         if (parts > 0) {
             if (defer != nullptr) {
@@ -136,7 +136,7 @@ hipError_t launch_conv_bwd_data_relu(int dt, const void *dy, int64_t dys, const 
         }
     }
     // otherwise the two ops in sequence: the input gradient, then the ReLU backward in place
-    const hipError_t e = launch_conv_bwd_data(dt, dy, dys, w, dpre, dxs, 0.f, s, nullptr, st);
+    const hipError_t e = launch_conv_bwd_data(dt, dy, dys, w, dpre, dxs, beta, s, nullptr, st);
     if (e != hipSuccess) return e;
     return launch_bias_relu_bwd(dt, y, dpre, dpre, (int64_t)s.N * s.H * s.W, s.C, dxs, db, ws, st, defer);
 }

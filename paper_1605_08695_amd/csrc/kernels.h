@@ -64,8 +64,8 @@ struct BiasPartials {
 // dpre = y > 0 ? bwd_input(dy, w) : +0 (dx's view), db = column sums of dpre; ws: partials.
 // defer: if not NULL, db is not written and the partials are left where *defer says.
 hipError_t launch_conv_bwd_data_relu(int dt, const void *dy, int64_t dys, const void *w, void *dpre, int64_t dxs,
-                                     const void *y, float *db, float *ws, const ConvShape &s, hipStream_t st,
-                                     BiasPartials *defer = nullptr);
+                                     const void *y, float beta, float *db, float *ws, const ConvShape &s,
+                                     hipStream_t st, BiasPartials *defer = nullptr);
 size_t conv_bwd_data_relu_ws_bytes(int dt, const ConvShape &s, int64_t dxs);
 // Per-channel sums of partial[c][G] (G values per channel, summed in order) into out[C].
 hipError_t launch_sum_partials(const float *partial, int G, int C, float *out, hipStream_t st);

@@ -179,9 +179,11 @@ def conv2d_bwd_input(dy, w, dx, stride, pads, beta=0.0, ws=None, stream=None):
     return dx
 
 
-def conv2d_bwd_input_relu_bwd(dy, w, y, dpre, stride, pads, dbias=None, ws=None, stream=None, defer=False):
-    """dpre = (y > 0) * conv2d_fwd^T(dy), dbias = column sums of dpre (fp32): the input gradient
-    fused with the ReLU backward of the layer that produced the input (y, dpre: its view).
+def conv2d_bwd_input_relu_bwd(dy, w, y, dpre, stride, pads, dbias=None, ws=None, stream=None, defer=False,
+                              beta=0.0):
+    """dpre = (y > 0) * (beta * dpre + conv2d_fwd^T(dy)), dbias = column sums of dpre (fp32): the
+    input gradient fused with the ReLU backward of the layers that produced the input (y, dpre: its
+    view); beta = 1 adds it to the gradient the input's other readers stored in dpre.
     defer=True: returns (dpre, DeferredBias) instead, the partials left in ws (see bias_grad_finish)."""
     lib = load()
     kh, kw, cin, cout = w.shape
@@ -200,7 +202,8 @@ def conv2d_bwd_input_relu_bwd(dy, w, y, dpre, stride, pads, dbias=None, ws=None,
     if need and (ws is None or ws.numel() < need):
         ws = _ws(need, y.device, stream)
     check(lib.tfk_conv2d_bwd_input_relu_bwd(_ptr(dy), nhwc(dy), _ptr(w), win, _dt(dy), _ptr(y), _ptr(dpre), d_p,
-                                            _ptr(dbias), _ptr(ws) if need else None, need, _stream(stream)))
+                                            float(beta), _ptr(dbias), _ptr(ws) if need else None, need,
+                                            _stream(stream)))
     return dpre, (_deferred(lib, cin) if defer else dbias)
 
 

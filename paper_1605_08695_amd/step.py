@@ -310,6 +310,21 @@ class Replica:
                     g = (run[0].dst_c0, sum(c.cout for c in run), run)
                     for c in run:
                         self.relu_groups[c.name] = g
+        # ---- a ReLU group over a whole tensor (a concat's branches) is applied by the last of the
+        # tensor's readers to write its gradient (the first in forward order): a convolution's
+        # input gradient, or a max-pool's, adds its part to what the others stored and masks and
+        # sums the bias gradient in the same pass (no separate ReLU-backward pass over the concat)
+        self.relu_last = {}                      # reader op name -> (tensor, group)
+        for t, g in {run[0].dst: (c0, width, run) for c0, width, run in self.relu_groups.values()}.items():
+            c0, width, run = g
+            if c0 != 0 or width != net.tensors[t][3] or t in ("x", net.output):
+                continue
+            first = next((op for op in self.ops if op.src == t), None)
+            if first is None or (isinstance(first, Conv) and first.name in self.bwi_relu):
+                continue
+            if isinstance(first, Pool) and first.name in self.pool_relu:
+                continue
+            self.relu_last[first.name] = (t, g)
         # ---- a convolution whose whole ReLU output is pooled by the next op: one forward call
         # (one kernel where its row bands hold whole pool windows)
         self.conv_pool = {}                      # conv name -> pool op
@@ -471,6 +486,25 @@ class Replica:
             if trace: trace("bias_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
         return dpre
 
+    def _input_grad_relu_last(self, op, dpre, w, beta, trace, stream, defer, jobs, grouped):
+        """The input gradient of convolution ``op`` as the last of its input's readers, fused with
+        the ReLU backward of the group of convolutions that produced the whole input."""
+        t, (c0, width, run) = self.relu_last[op.name]
+        y, dx = self.act[t], self.grad[t]
+        bo = self._layout[run[0].name][2]
+        dbg = self.grads[bo:bo + width]
+        grouped.add(id(run))
+        if trace: trace("conv_bwd_input_relu_bwd", op, stream=stream, dy=dpre, w=w, y=y, dpre=dx, beta=beta)
+        if defer:
+            ws = self._bias_ws(("last", op.name), ops.conv2d_workspace_bytes(
+                3, y, op.cout, op.kh, op.kw, (op.sh, op.sw), op.pads))
+            jobs.append((ops.conv2d_bwd_input_relu_bwd(dpre, w, y, dx, (op.sh, op.sw), op.pads, ws=ws, stream=stream,
+                                                       defer=True, beta=beta)[1], dbg))
+        else:
+            ops.conv2d_bwd_input_relu_bwd(dpre, w, y, dx, (op.sh, op.sw), op.pads, dbias=dbg, ws=self.ws,
+                                          stream=stream, beta=beta)
+        if trace: trace("conv_bwd_input_relu_bwd:end", op, stream=stream, dpre=dx, db=dbg)
+
     def backward(self, trace=None, stream=None, side=None):
         """Gradients of every variable.  With ``side`` (a second stream), the filter gradient
         of each convolution that also has an input gradient runs there, concurrently with that
@@ -503,7 +537,11 @@ class Replica:
                 ops.conv2d_bwd_filter(x, dpre, (1, 1), (1, 1), op.pads, dw=dw,
                                       ws=self.ws_side if on_side else self.ws, stream=fs)
                 if trace: trace("conv_bwd_filter:end", op, stream=fs, dw=dw)
-                if src_grad:
+                if src_grad and op.name in self.relu_last:
+                    self._input_grad_relu_last(op, dpre, self.mWlp[op.name], beta, trace, stream, defer, jobs,
+                                               grouped)
+                    written.add(op.src)
+                elif src_grad:
                     dx, w = self.grad[op.src], self.mWlp[op.name]
                     if trace: trace("conv_bwd_input", op, stream=stream, dy=dpre, w=w, dx=dx, beta=beta)
                     ops.conv2d_bwd_input(dpre, w, dx, (1, 1), op.pads, beta=beta, ws=self.ws, stream=stream)
@@ -538,6 +576,9 @@ class Replica:
                         ops.conv2d_bwd_input_relu_bwd(dpre, self.Wlp[op.name], y, dx, (op.sh, op.sw), op.pads,
                                                       dbias=self.db[prod.name], ws=self.ws, stream=stream)
                     if trace: trace("conv_bwd_input_relu_bwd:end", op, stream=stream, dpre=dx, db=self.db[prod.name])
+                elif src_grad and op.name in self.relu_last:
+                    self._input_grad_relu_last(op, dpre, self.Wlp[op.name], beta, trace, stream, defer, jobs,
+                                               grouped)
                 elif src_grad:
                     dx = self.grad[op.src]
                     if trace: trace("conv_bwd_input", op, stream=stream, dy=dpre, w=self.Wlp[op.name], dx=dx,
@@ -561,6 +602,25 @@ class Replica:
                     ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
                                              dbias=self.db[conv.name], ws=self.ws, stream=stream, py=py)
                 if trace: trace("maxpool_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[conv.name])
+            elif src_grad and op.name in self.relu_last:
+                # the last reader of a concat: its pool gradient added, then the concat's ReLU backward
+                t, (c0, width, run) = self.relu_last[op.name]
+                y, dpre, am = self.act[t], self.grad[t], self.argmax[op.name]
+                bo = self._layout[run[0].name][2]
+                dbg = self.grads[bo:bo + width]
+                grouped.add(id(run))
+                py = self._slice(self.act, op)
+                if trace: trace("maxpool_relu_bwd", op, stream=stream, dy=dy, argmax=am, y=y, py=py, dpre=dpre,
+                                beta=beta)
+                if defer:
+                    ws = self._bias_ws(("last", op.name), ops.bias_relu_bwd_workspace_bytes(dpre))
+                    jobs.append((ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads,
+                                                          beta=beta, ws=ws, stream=stream, py=py, defer=True)[1],
+                                 dbg))
+                else:
+                    ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
+                                             dbias=dbg, ws=self.ws, stream=stream, py=py)
+                if trace: trace("maxpool_relu_bwd:end", op, stream=stream, dpre=dpre, db=dbg)
             else:
                 if src_grad:
                     dx = self.grad[op.src]

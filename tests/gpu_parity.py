@@ -497,11 +497,16 @@ class ParityTracer:
         self._set(out["dx"], ref)
 
     def _force_conv_bwd_input_relu_bwd(self, op, t):
-        return {"dy": self._force(t["dy"]), "w": self._force(t["w"]), "y": self._force(t["y"])}
+        u = {"dy": self._force(t["dy"]), "w": self._force(t["w"]), "y": self._force(t["y"]),
+             "beta": t.get("beta", 0.0)}
+        u["dpre"] = self._force(t["dpre"]) if u["beta"] else None
+        return u
 
     def _check_conv_bwd_input_relu_bwd(self, op, u, out):
-        # the input gradient of op fused with the ReLU backward of the layer that produced its input
-        g = oracle.conv2d_bwd_input(u["dy"], u["w"], u["y"].shape, (op.sh, op.sw), op.pads)
+        # the input gradient of op (added to what the input's other readers stored, beta = 1) fused
+        # with the ReLU backward of the layers that produced its input
+        g = oracle.conv2d_bwd_input(u["dy"], u["w"], u["y"].shape, (op.sh, op.sw), op.pads, dx=u["dpre"],
+                                    beta=u["beta"])
         ref_dpre, ref_db = oracle.bias_relu_bwd(u["y"], g)
         got = self._got("conv_bwd_input_relu_bwd", op.name, out["dpre"])
         self.record_tensor("conv_bwd_input_relu_bwd", op.name, got, ref_dpre, self.dtype)
@@ -685,7 +690,8 @@ class SampledParityTracer(ParityTracer):
 
     def _check_conv_bwd_input_relu_bwd(self, op, u, out):
         s = self.sample
-        g = oracle.conv2d_bwd_input(u["dy"][s], u["w"], (len(s),) + u["y"].shape[1:], (op.sh, op.sw), op.pads)
+        g = oracle.conv2d_bwd_input(u["dy"][s], u["w"], (len(s),) + u["y"].shape[1:], (op.sh, op.sw), op.pads,
+                                    dx=u["dpre"][s] if u["beta"] else None, beta=u["beta"])
         ref_dpre, _ = oracle.bias_relu_bwd(u["y"][s], g)
         self.record_tensor("conv_bwd_input_relu_bwd", op.name, self._gs(out["dpre"]), ref_dpre, self.dtype)
         # the ReLU mask on every image: zero wherever the forced y is not positive

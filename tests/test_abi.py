@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 14
+    assert lib.tfk_abi_version() == 15
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -144,11 +144,12 @@ def test_conv_bwd_input_relu_bwd_validation(lib):
     assert need >= 384 * 4 * ((128 * 13 * 13 + 127) // 128)
     assert lib.tfk_conv2d_workspace_bytes(1, xd, 256, W, BF16) == 0
     def fused(dy=P, w=P + 0x10000000, y=P + 0x20000000, dpre=P + 0x30000000, db=P + 0x40000000,
-              ws=P + 0x50000000, ws_bytes=need):
-        return lib.tfk_conv2d_bwd_input_relu_bwd(vp(dy), dyd, vp(w), W, BF16, vp(y), vp(dpre), xd, vp(db), vp(ws),
-                                                 ws_bytes, None)
+              ws=P + 0x50000000, ws_bytes=need, beta=0.0):
+        return lib.tfk_conv2d_bwd_input_relu_bwd(vp(dy), dyd, vp(w), W, BF16, vp(y), vp(dpre), xd,
+                                                 ctypes.c_float(beta), vp(db), vp(ws), ws_bytes, None)
     assert fused(dy=0) == NULL
     assert fused(y=0) == NULL
+    assert fused(beta=0.5) == ARG
     assert fused(db=0, ws_bytes=need - 1) == WORKSPACE                  # deferred: the same checks
     assert fused(dpre=P + 0x20000010) == ALIAS                         # dpre overlaps y
     assert fused(db=P + 0x30000000) == ALIAS                           # dbias inside dpre

@@ -157,6 +157,19 @@ def test_conv_bwd_input_relu_bwd_fused(name, dtype):
     dp2, _ = ops.bias_relu_bwd(y, dx)
     torch.cuda.synchronize()
     assert torch.equal(dpre, dp2)
+    # beta = 1: added to the gradient the input's other readers stored, then masked
+    old = _mk(y.shape, dtype, rng)
+    dp3 = old.clone()
+    _, db3 = ops.conv2d_bwd_input_relu_bwd(dy, w, y, dp3, (sh, sw), pads, beta=1.0)
+    dx4 = old.clone()
+    ops.conv2d_bwd_input(dy, w, dx4, (sh, sw), pads, beta=1.0)
+    dp4, _ = ops.bias_relu_bwd(y, dx4)
+    torch.cuda.synchronize()
+    g1 = oracle.conv2d_bwd_input(f64(dy), f64(w), y.shape, (sh, sw), pads, dx=f64(old), beta=1.0)
+    ref_dpre1, ref_db1 = oracle.bias_relu_bwd(f64(y), g1)
+    assert_close(f64(dp3), ref_dpre1, dtype, label="fused dpre beta=1")
+    assert_close(f64(db3), ref_db1, torch.float32, dtype, label="fused db beta=1")
+    assert torch.equal(dp3, dp4)
 
 
 @pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
