@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define TFK_ABI_VERSION 15
+#define TFK_ABI_VERSION 16
 
 #if defined(__GNUC__)
 #define TFK_API __attribute__((visibility("default")))
@@ -504,6 +504,23 @@ TFK_API tfk_status tfk_apply_adam(float *var, float *m, float *v, const float *g
  * Errors: HIP (event creation, record or wait failed). */
 TFK_API tfk_status tfk_stream_wait(void *waiter, void *producer);
 
+/* A caller-owned point on a stream: tfk_mark_record places it after everything enqueued on
+ * `stream` so far, and work enqueued on `waiter` after tfk_stream_wait_mark starts only once
+ * that point (the mark's latest record before the wait call) has been reached.  Unlike
+ * tfk_stream_wait, the producer may enqueue more work between the two calls without the waiter
+ * waiting for it: the independent branches of a step run on several streams that each wait only
+ * for the kernels producing their inputs (the executor's per-edge dependencies, Section 3.1;
+ * several GPU streams, Section 5).  Both calls are recorded into a program like the ops (the
+ * mark by pointer: it must outlive the program's use).  tfk_mark_create errors: NULL; ARG (out
+ * of host memory); HIP (event creation).  tfk_mark_record / tfk_stream_wait_mark errors: NULL
+ * (mark is NULL); HIP.  tfk_mark_destroy(NULL) is a no-op; a mark that work still waits for may
+ * be destroyed (the runtime keeps the event until it completes). */
+typedef struct tfk_mark tfk_mark;
+TFK_API tfk_status tfk_mark_create(tfk_mark **mark);
+TFK_API void tfk_mark_destroy(tfk_mark *mark);
+TFK_API tfk_status tfk_mark_record(tfk_mark *mark, void *stream);
+TFK_API tfk_status tfk_stream_wait_mark(void *waiter, tfk_mark *mark);
+
 /* Opaque recorded call sequence. */
 typedef struct tfk_program tfk_program;
 
@@ -515,7 +532,7 @@ TFK_API tfk_status tfk_program_create(tfk_program **prog);
 TFK_API void tfk_program_destroy(tfk_program *prog);
 /* Starts recording on the calling thread (previous contents are dropped).  Until
  * tfk_program_end, every tfk_* call on this thread that enqueues work (convolutions, bias/ReLU,
- * pooling, updates, losses, sampled-softmax ops, tfk_stream_wait) runs as usual and, when it
+ * pooling, updates, losses, sampled-softmax ops, tfk_stream_wait, marks) runs as usual and, when it
  * returns TFK_OK, is appended to the program with its arguments by value: the same pointers,
  * shapes, scalars and streams.  Calls that fail are not appended.  Queries
  * (*_workspace_bytes) are never recorded.  Errors: NULL; ARG (this thread already records). */

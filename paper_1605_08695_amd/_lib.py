@@ -24,7 +24,8 @@ EXPORTS = ["tfk_conv2d_fwd", "tfk_conv2d_fwd_bias_relu", "tfk_maxpool_bwd_relu_b
            "tfk_maxpool_fwd", "tfk_maxpool_bwd", "tfk_maxpool_fwd_taps", "tfk_maxpool_bwd_taps",
            "tfk_maxpool_bwd_relu_bwd_taps", "tfk_apply_sgd", "tfk_apply_sgd_multi",
            "tfk_apply_momentum", "tfk_apply_adam", "tfk_softmax_xent", "tfk_gather_rows_t",
-           "tfk_sampled_softmax_xent", "tfk_scatter_apply_sgd", "tfk_stream_wait", "tfk_program_create",
+           "tfk_sampled_softmax_xent", "tfk_scatter_apply_sgd", "tfk_stream_wait", "tfk_mark_create", "tfk_mark_destroy",
+           "tfk_mark_record", "tfk_stream_wait_mark", "tfk_program_create",
            "tfk_program_destroy", "tfk_program_begin", "tfk_program_end", "tfk_program_length", "tfk_program_run",
            "tfk_status_string", "tfk_last_error", "tfk_abi_version"]
 
@@ -101,6 +102,13 @@ def load(path: str = LIB_PATH):
     for name in ("tfk_last_bias_partials", "tfk_bias_grad_finish"):
         getattr(lib, name).restype = st
     lib.tfk_stream_wait.argtypes = [vp, vp]
+    lib.tfk_mark_create.argtypes = [ctypes.POINTER(vp)]
+    lib.tfk_mark_destroy.argtypes = [vp]
+    lib.tfk_mark_destroy.restype = None
+    lib.tfk_mark_record.argtypes = [vp, vp]
+    lib.tfk_stream_wait_mark.argtypes = [vp, vp]
+    for name in ("tfk_mark_create", "tfk_mark_record", "tfk_stream_wait_mark"):
+        getattr(lib, name).restype = st
     lib.tfk_program_create.argtypes = [ctypes.POINTER(vp)]
     lib.tfk_program_destroy.argtypes = [vp]
     lib.tfk_program_destroy.restype = None

@@ -12,6 +12,7 @@
 #include <algorithm>
 #include <functional>
 #include <memory>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -1089,6 +1090,43 @@ tfk_status tfk_stream_wait(void *waiter, void *producer) {
     const tfk_status s = join(e, (hipStream_t)waiter, (hipStream_t)producer);
     (void)hipEventDestroy(e);      // released once the recorded work completes
     return s;
+}
+
+// A point on one stream that work on other streams can wait for: the event of its latest record.
+struct tfk_mark {
+    hipEvent_t e = nullptr;
+};
+
+tfk_status tfk_mark_create(tfk_mark **mark) {
+    TRY(need_ptr(mark, "mark"));
+    *mark = nullptr;
+    tfk_mark *m = new (std::nothrow) tfk_mark();
+    if (m == nullptr) return fail(TFK_ERR_ARG, "tfk_mark_create: out of host memory");
+    const hipError_t r = hipEventCreateWithFlags(&m->e, kJoinEventFlags);
+    if (r != hipSuccess) {
+        delete m;
+        return hip_status(r, "mark_create");
+    }
+    *mark = m;
+    return ok();
+}
+
+void tfk_mark_destroy(tfk_mark *mark) {
+    if (mark == nullptr) return;
+    (void)hipEventDestroy(mark->e);
+    delete mark;
+}
+
+tfk_status tfk_mark_record(tfk_mark *mark, void *stream) {
+    TRY(need_ptr(mark, "mark"));
+    RECORDED(tfk_mark_record, mark, stream);
+    return hip_status(hipEventRecord(mark->e, (hipStream_t)stream), "mark_record");
+}
+
+tfk_status tfk_stream_wait_mark(void *waiter, tfk_mark *mark) {
+    TRY(need_ptr(mark, "mark"));
+    RECORDED(tfk_stream_wait_mark, waiter, mark);
+    return hip_status(hipStreamWaitEvent((hipStream_t)waiter, mark->e, 0), "stream_wait_mark");
 }
 
 tfk_status tfk_program_create(tfk_program **prog) {

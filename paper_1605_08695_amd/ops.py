@@ -507,6 +507,36 @@ def stream_wait(waiter, producer):
     check(load().tfk_stream_wait(ctypes.c_void_p(waiter.cuda_stream), ctypes.c_void_p(producer.cuda_stream)))
 
 
+class Mark:
+    """A point on one stream that other streams can wait for (``record`` then ``wait``): unlike
+    ``stream_wait``, work the producer enqueues after ``record`` is not waited for.  Recorded
+    into programs like the ops; a mark must outlive every program that uses it."""
+
+    def __init__(self):
+        self._lib = load()
+        h = ctypes.c_void_p()
+        check(self._lib.tfk_mark_create(ctypes.byref(h)))
+        self._h = h
+
+    def record(self, stream):
+        check(self._lib.tfk_mark_record(self._h, ctypes.c_void_p(stream.cuda_stream)))
+
+    def wait(self, waiter):
+        """Work enqueued on ``waiter`` afterwards starts once the latest ``record`` is reached."""
+        check(self._lib.tfk_stream_wait_mark(ctypes.c_void_p(waiter.cuda_stream), self._h))
+
+    def close(self):
+        if self._h is not None and self._h.value:
+            self._lib.tfk_mark_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 class Program:
     """A recorded sequence of library calls, issued again from C++ by ``run()``.
 

@@ -30,7 +30,7 @@ fused activation gradients); that convolution then skips its own ReLU backward.
 """
 from __future__ import annotations
 
-from typing import Dict, Optional
+from typing import Dict, List, Optional
 
 import numpy as np
 import torch
@@ -92,6 +92,63 @@ def _merge_groups(net: Net):
         groups.append({"op": mconv, "members": members, "offs": offs, "width": w, "cat": catt,
                        "at": pos[first.name]})
     return groups
+
+
+def lane_plan(nodes, outs, nlanes: int):
+    """Places ops, in issue order, on ``nlanes`` streams: an op continues the lane of an input's
+    producer when that producer is the lane's latest op, else takes the least recently used lane,
+    so an inception module's branches run side by side.  ``outs[i]`` names the tensors node i
+    writes (a concat has several writers: its readers need all of them); node i reads
+    ``nodes[i].src``.  Returns ``(plan, joins)``: plan entries ``(op, lane, waits)``, ``waits``
+    the earlier nodes (by index) on other lanes whose completion the op needs and its lane has
+    not yet waited for, directly or through another wait (vector clocks), at most one per lane;
+    "start" is lane 0 at the start, which every lane's first op must follow.  ``joins`` are the
+    nodes lane 0 waits for at the end, so that it follows every node."""
+    writers: Dict[str, List[int]] = {}
+    for i, o in enumerate(outs):
+        for t in o:
+            writers.setdefault(t, []).append(i)
+    lane_of: List[int] = []
+    tail = [None] * nlanes                   # latest node of each lane
+    used_at = [-1] * nlanes                  # when each lane was last given a node
+    clock = [dict() for _ in range(nlanes)]  # lane -> {lane: latest node known complete}
+    clock[0][0] = -1                         # lane 0 starts where the caller's stream is
+    node_clock, plan = [], []
+    for i, op in enumerate(nodes):
+        deps = sorted(j for j in writers.get(op.src, []) if j < i)
+        cont = [lane_of[j] for j in deps if tail[lane_of[j]] == j]
+        if i == 0:
+            lane = 0
+        elif cont:
+            lane = 0 if 0 in cont else cont[-1]
+        else:
+            lane = min(range(nlanes), key=lambda k: used_at[k])
+        waits = []
+        c = clock[lane]
+        latest = {}                          # per producing lane, its latest node among deps
+        for j in deps:
+            latest[lane_of[j]] = max(latest.get(lane_of[j], -1), j)
+        for a, j in sorted(latest.items(), key=lambda t: t[1]):
+            if a != lane and c.get(a, -2) < j:
+                waits.append(j)
+                for k, v in node_clock[j].items():
+                    c[k] = max(c.get(k, -2), v)
+        if c.get(0, -2) < -1:
+            waits.insert(0, "start")
+            c[0] = -1
+        c[lane] = i
+        lane_of.append(lane)
+        tail[lane] = i
+        used_at[lane] = i
+        node_clock.append(dict(c))
+        plan.append((op, lane, waits))
+    joins = []
+    for k in range(1, nlanes):
+        if tail[k] is not None and clock[0].get(k, -2) < tail[k]:
+            joins.append(tail[k])
+            for kk, v in node_clock[tail[k]].items():
+                clock[0][kk] = max(clock[0].get(kk, -2), v)
+    return plan, joins
 
 
 class Replica:
@@ -356,12 +413,46 @@ class Replica:
                                                         c.pads))
         self.ws_side = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=dev)
         self.side = torch.cuda.Stream(device=dev)
+        # ---- the forward pass's independent branches run on up to kFwdLanes streams (lane 0 is
+        # the step's stream, lane 1 the side stream, idle in the forward pass: with the step's
+        # stream, four streams, as many as the hardware queues a process gets by default), each
+        # lane with a workspace of its own (see _forward_plan)
+        self.fwd_plan = self._forward_plan(self.kFwdLanes)
+        used = sorted({lane for _, lane, _ in self.fwd_plan[0]} - {0})
+        self.lane_streams = {k: self.side if k == 1 else torch.cuda.Stream(device=dev) for k in used}
+        self.lane_ws = {k: torch.zeros_like(self.ws) for k in used}
+        self.marks = {}                          # node index (or "start") -> ops.Mark, made on first use
         # ---- bias gradients of an untraced step: each ReLU/bias backward leaves its per-block
         # partials in a workspace of its own, and one launch sums them all before the update
         self.defer_bias = True
         self.bias_ws: Dict[object, torch.Tensor] = {}
 
     # ------------------------------------------------------------------ helpers
+    kFwdLanes = 4
+
+    def _forward_plan(self, nlanes: int):
+        """The forward ops (a pool made inside its convolution left out) placed on ``nlanes``
+        streams by ``lane_plan``."""
+        nodes, outs = [], []
+        for op in self.ops:
+            if isinstance(op, Pool) and op.name in self.pool_in_conv:
+                continue
+            if op.name in self.merged:
+                o = {m.dst for m in self.merged[op.name]["members"]}
+            elif op.name in self.conv_pool:
+                o = {op.dst, self.conv_pool[op.name].dst}
+            else:
+                o = {op.dst}
+            nodes.append(op)
+            outs.append(o)
+        return lane_plan(nodes, outs, nlanes)
+
+    def _mark(self, key):
+        m = self.marks.get(key)
+        if m is None:
+            m = self.marks[key] = ops.Mark()
+        return m
+
     def place_filter(self, flat, name: str, w) -> None:
         """Writes filter ``w`` (HWIO) of convolution ``name`` where the flat variable layout keeps
         it: its own block, or its channels of its merged group's block."""
@@ -386,45 +477,66 @@ class Replica:
         return t[..., op.dst_c0:op.dst_c0 + self._width(op)]
 
     # ------------------------------------------------------------------ the step
-    def forward(self, trace=None, stream=None):
-        for op in self.ops:
-            x = self.act[op.src]
-            if op.name in self.merged:
-                y, w, b = self.m_act[op.name], self.mWlp[op.name], self.mb[op.name]
-                if trace: trace("conv_bias_relu_fwd", op, stream=stream, x=x, w=w, b=b, y=y)
-                ops.conv2d_fwd_bias_relu(x, w, b, (1, 1), op.pads, y=y, ws=self.ws, stream=stream)
-                if trace: trace("conv_bias_relu_fwd:end", op, stream=stream, y=y)
-                continue
-            y = self._slice(self.act, op)
-            if isinstance(op, Conv) and not op.relu:
-                # a classifier's logits: the bias is added inside the cross-entropy kernel
-                if trace: trace("conv_fwd", op, stream=stream, x=x, w=self.Wlp[op.name], y=y)
-                ops.conv2d_fwd(x, self.Wlp[op.name], (op.sh, op.sw), op.pads, y=y, ws=self.ws, stream=stream)
-                if trace: trace("conv_fwd:end", op, stream=stream, y=y)
-            elif isinstance(op, Conv) and op.name in self.conv_pool:
-                pool = self.conv_pool[op.name]
-                py, am = self._slice(self.act, pool), self.argmax[pool.name]
-                if trace: trace("conv_bias_relu_maxpool_fwd", op, stream=stream, x=x, w=self.Wlp[op.name],
-                                b=self.b[op.name], y=y, py=py, argmax=am)
-                ops.conv2d_fwd_bias_relu_maxpool(x, self.Wlp[op.name], self.b[op.name], (op.sh, op.sw), op.pads,
-                                                 (pool.kh, pool.kw), (pool.sh, pool.sw), pool.pads, y=y, py=py,
-                                                 taps=am, ws=self.ws, stream=stream)
-                if trace: trace("conv_bias_relu_maxpool_fwd:end", op, stream=stream, y=y, py=py, argmax=am)
-            elif isinstance(op, Pool) and op.name in self.pool_in_conv:
-                continue                         # produced with its convolution
-            elif isinstance(op, Conv):
-                if trace: trace("conv_bias_relu_fwd", op, stream=stream, x=x, w=self.Wlp[op.name],
-                                b=self.b[op.name], y=y)
-                ops.conv2d_fwd_bias_relu(x, self.Wlp[op.name], self.b[op.name], (op.sh, op.sw), op.pads, y=y,
-                                         ws=self.ws, stream=stream)
-                if trace: trace("conv_bias_relu_fwd:end", op, stream=stream, y=y)
-            else:
-                if trace: trace("maxpool_fwd", op, stream=stream, x=x, y=y, argmax=self.argmax[op.name])
-                ops.maxpool_fwd(x, (op.kh, op.kw), (op.sh, op.sw), op.pads, y=y, argmax=self.argmax[op.name],
-                                stream=stream)
-                if trace: trace("maxpool_fwd:end", op, stream=stream, y=y, argmax=self.argmax[op.name])
+    def forward(self, trace=None, stream=None, lanes=True):
+        """The forward pass on ``stream``; untraced, with ``lanes``, independent branches run on
+        the lane streams of the forward plan, which join ``stream`` before the loss."""
+        if trace is not None or not lanes or not self.lane_streams:
+            for op in self.ops:
+                self._forward_op(op, trace, stream, self.ws)
+        else:
+            cur = stream if stream is not None else torch.cuda.current_stream()
+            plan, joins = self.fwd_plan
+            needed = {j for _, _, waits in plan for j in waits} | set(joins)
+            if "start" in needed:
+                self._mark("start").record(cur)
+            for i, (op, lane, waits) in enumerate(plan):
+                st = cur if lane == 0 else self.lane_streams[lane]
+                for j in waits:
+                    self._mark(j).wait(st)
+                self._forward_op(op, None, st, self.ws if lane == 0 else self.lane_ws[lane])
+                if i in needed:
+                    self._mark(i).record(st)
+            for j in joins:
+                self._mark(j).wait(cur)
         if self.net.loss == "softmax_xent":
             self.loss_fwd_bwd(trace, stream)
+
+    def _forward_op(self, op, trace, stream, ws):
+        x = self.act[op.src]
+        if op.name in self.merged:
+            y, w, b = self.m_act[op.name], self.mWlp[op.name], self.mb[op.name]
+            if trace: trace("conv_bias_relu_fwd", op, stream=stream, x=x, w=w, b=b, y=y)
+            ops.conv2d_fwd_bias_relu(x, w, b, (1, 1), op.pads, y=y, ws=ws, stream=stream)
+            if trace: trace("conv_bias_relu_fwd:end", op, stream=stream, y=y)
+            return
+        y = self._slice(self.act, op)
+        if isinstance(op, Conv) and not op.relu:
+            # a classifier's logits: the bias is added inside the cross-entropy kernel
+            if trace: trace("conv_fwd", op, stream=stream, x=x, w=self.Wlp[op.name], y=y)
+            ops.conv2d_fwd(x, self.Wlp[op.name], (op.sh, op.sw), op.pads, y=y, ws=ws, stream=stream)
+            if trace: trace("conv_fwd:end", op, stream=stream, y=y)
+        elif isinstance(op, Conv) and op.name in self.conv_pool:
+            pool = self.conv_pool[op.name]
+            py, am = self._slice(self.act, pool), self.argmax[pool.name]
+            if trace: trace("conv_bias_relu_maxpool_fwd", op, stream=stream, x=x, w=self.Wlp[op.name],
+                            b=self.b[op.name], y=y, py=py, argmax=am)
+            ops.conv2d_fwd_bias_relu_maxpool(x, self.Wlp[op.name], self.b[op.name], (op.sh, op.sw), op.pads,
+                                             (pool.kh, pool.kw), (pool.sh, pool.sw), pool.pads, y=y, py=py,
+                                             taps=am, ws=ws, stream=stream)
+            if trace: trace("conv_bias_relu_maxpool_fwd:end", op, stream=stream, y=y, py=py, argmax=am)
+        elif isinstance(op, Pool) and op.name in self.pool_in_conv:
+            return                           # produced with its convolution
+        elif isinstance(op, Conv):
+            if trace: trace("conv_bias_relu_fwd", op, stream=stream, x=x, w=self.Wlp[op.name],
+                            b=self.b[op.name], y=y)
+            ops.conv2d_fwd_bias_relu(x, self.Wlp[op.name], self.b[op.name], (op.sh, op.sw), op.pads, y=y,
+                                     ws=ws, stream=stream)
+            if trace: trace("conv_bias_relu_fwd:end", op, stream=stream, y=y)
+        else:
+            if trace: trace("maxpool_fwd", op, stream=stream, x=x, y=y, argmax=self.argmax[op.name])
+            ops.maxpool_fwd(x, (op.kh, op.kw), (op.sh, op.sw), op.pads, y=y, argmax=self.argmax[op.name],
+                            stream=stream)
+            if trace: trace("maxpool_fwd:end", op, stream=stream, y=y, argmax=self.argmax[op.name])
 
     def loss_fwd_bwd(self, trace=None, stream=None):
         """Mean softmax cross-entropy of the logits (the logits layer's bias added here) and its
@@ -655,11 +767,12 @@ class Replica:
             if trace: trace("apply_adam:end", None, stream=stream, var=self.params)
 
     def step(self, trace=None, stream=None, concurrent=True):
-        """One training step on ``stream``; the filter gradients overlap the rest of the
-        backward pass on a second stream unless ``concurrent`` is false.  ``trace(event, op,
+        """One training step on ``stream``; unless ``concurrent`` is false, the forward pass's
+        independent branches run side by side on the lane streams and the filter gradients
+        overlap the rest of the backward pass on a second stream.  ``trace(event, op,
         stream=s, **tensors)`` is called before and after every op (``event`` ending in
         ``:end``), with the stream the op runs on (None: the current stream)."""
-        self.forward(trace, stream)
+        self.forward(trace, stream, lanes=concurrent)
         self.backward(trace, stream, side=self.side if concurrent else None)
         self.update(trace, stream)
 
@@ -671,7 +784,7 @@ class Replica:
         prog = ops.Program()
         prog.with_update = self.optimizer != "adam"
         with prog.recording():
-            self.forward(None, stream)
+            self.forward(None, stream, lanes=concurrent)
             self.backward(None, stream, side=self.side if concurrent else None)
             if prog.with_update:
                 self.update(None, stream)

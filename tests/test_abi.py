@@ -44,7 +44,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.tfk_abi_version() == 15
+    assert lib.tfk_abi_version() == 16
     assert lib.tfk_status_string(0) == b"ok"
     assert lib.tfk_status_string(6) == b"illegal aliasing"
     assert lib.tfk_status_string(99) == b"unknown status"
@@ -424,6 +424,11 @@ def test_program_state_errors(lib):
     assert lib.tfk_program_end(b._h) == OK
     assert lib.tfk_stream_wait(None, None) == OK                 # same stream: no-op
     b.close()
+    # marks: NULL checks only (creating one needs a HIP event)
+    assert lib.tfk_mark_create(None) == NULL
+    assert lib.tfk_mark_record(None, None) == NULL
+    assert lib.tfk_stream_wait_mark(None, None) == NULL
+    lib.tfk_mark_destroy(None)
 
 
 def test_deferred_bias_validation(lib):

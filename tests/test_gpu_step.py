@@ -29,7 +29,8 @@ pytestmark = pytest.mark.gpu
 
 
 def bitwise_equal(a, b):
-    return torch.equal(a.view(torch.int32), b.view(torch.int32))
+    bits = {2: torch.int16, 4: torch.int32}[a.element_size()]
+    return torch.equal(a.view(bits), b.view(bits))
 
 
 def _report(tr):
@@ -276,12 +277,13 @@ def test_step_deterministic_and_restorable(make):
     assert bitwise_equal(p1, rep.params) and bitwise_equal(g1, rep.grads)
 
 
-@pytest.mark.parametrize("make", [lambda: W.alexnet(batch=8), lambda: W.googlenet(batch=4)],
-                         ids=["alexnet_b8", "googlenet_b4"])
+@pytest.mark.parametrize("make", [lambda: W.alexnet(batch=8), lambda: W.googlenet(batch=4),
+                                  lambda: W.inception_v3(batch=2)],
+                         ids=["alexnet_b8", "googlenet_b4", "inception_v3_b2"])
 def test_two_stream_step_matches_one_stream(make):
-    """Filter gradients on the second stream (overlapping the input gradients) must give
-    bit-identical gradients and variables to the same step with every op on one stream,
-    over several steps in a row."""
+    """Forward branches on the lane streams and filter gradients on the second stream
+    (overlapping the input gradients) must give bit-identical activations, gradients and
+    variables to the same step with every op on one stream, over several steps in a row."""
     net = make()
     net.lr = 1e-6
     inp = W.make_inputs(net, seed=3)
@@ -293,6 +295,8 @@ def test_two_stream_step_matches_one_stream(make):
         assert bool(torch.isfinite(two.params).all()), r
         assert bitwise_equal(one.grads, two.grads), r
         assert bitwise_equal(one.params, two.params), r
+        for t in one.act:
+            assert bitwise_equal(one.act[t], two.act[t]), (r, t)
 
 
 def test_graph_capture_replays_match_eager():
@@ -325,8 +329,10 @@ def test_graph_capture_replays_match_eager():
 
 
 @pytest.mark.parametrize("make,opt", [(lambda: W.alexnet(batch=8), "sgd"), (lambda: W.googlenet(batch=4), "sgd"),
+                                      (lambda: W.inception_v3(batch=2), "sgd"),
                                       (lambda: W.alexnet(batch=8), "momentum"), (lambda: W.alexnet(batch=8), "adam")],
-                         ids=["alexnet_b8_sgd", "googlenet_b4_sgd", "alexnet_b8_momentum", "alexnet_b8_adam"])
+                         ids=["alexnet_b8_sgd", "googlenet_b4_sgd", "inception_v3_b2_sgd", "alexnet_b8_momentum",
+                              "alexnet_b8_adam"])
 def test_program_replays_match_eager(make, opt):
     """The step recorded once into a native program (its library calls, stream joins included)
     and issued again from C++: every replay, with eager steps and synchronisations in between,
