@@ -94,20 +94,27 @@ def _merge_groups(net: Net):
     return groups
 
 
-def lane_plan(nodes, outs, nlanes: int):
-    """Places ops, in issue order, on ``nlanes`` streams: an op continues the lane of an input's
-    producer when that producer is the lane's latest op, else takes the least recently used lane,
-    so an inception module's branches run side by side.  ``outs[i]`` names the tensors node i
-    writes (a concat has several writers: its readers need all of them); node i reads
-    ``nodes[i].src``.  Returns ``(plan, joins)``: plan entries ``(op, lane, waits)``, ``waits``
-    the earlier nodes (by index) on other lanes whose completion the op needs and its lane has
-    not yet waited for, directly or through another wait (vector clocks), at most one per lane;
-    "start" is lane 0 at the start, which every lane's first op must follow.  ``joins`` are the
-    nodes lane 0 waits for at the end, so that it follows every node."""
-    writers: Dict[str, List[int]] = {}
-    for i, o in enumerate(outs):
-        for t in o:
-            writers.setdefault(t, []).append(i)
+def access_deps(reads, writes, ordered_writes=True):
+    """For ops in issue order with the tensor names each reads and writes, the earlier ops each
+    must follow: a read after a write, a write after a read, and, with ``ordered_writes``, a
+    write after a write (gradient accumulation keeps its order; the forward pass's writers of
+    one concat write disjoint channel slices and need no order)."""
+    deps = []
+    for i in range(len(reads)):
+        deps.append([j for j in range(i) if (writes[j] & reads[i]) or (reads[j] & writes[i])
+                     or (ordered_writes and (writes[j] & writes[i]))])
+    return deps
+
+
+def lane_plan(nodes, deps, nlanes: int):
+    """Places ops, in issue order, on ``nlanes`` streams: an op continues the lane of a producer
+    it needs when that producer is the lane's latest op, else takes the least recently used lane,
+    so an inception module's branches run side by side.  ``deps[i]`` lists the earlier ops node i
+    must follow (see access_deps).  Returns ``(plan, joins)``: plan entries ``(op, lane, waits)``,
+    ``waits`` the earlier nodes (by index) on other lanes whose completion the op needs and its
+    lane has not yet waited for, directly or through another wait (vector clocks), at most one
+    per lane; "start" is lane 0 at the start, which every lane's first op must follow.
+    ``joins`` are the nodes lane 0 waits for at the end, so that it follows every node."""
     lane_of: List[int] = []
     tail = [None] * nlanes                   # latest node of each lane
     used_at = [-1] * nlanes                  # when each lane was last given a node
@@ -115,8 +122,8 @@ def lane_plan(nodes, outs, nlanes: int):
     clock[0][0] = -1                         # lane 0 starts where the caller's stream is
     node_clock, plan = [], []
     for i, op in enumerate(nodes):
-        deps = sorted(j for j in writers.get(op.src, []) if j < i)
-        cont = [lane_of[j] for j in deps if tail[lane_of[j]] == j]
+        need = sorted(deps[i])
+        cont = [lane_of[j] for j in need if tail[lane_of[j]] == j]
         if i == 0:
             lane = 0
         elif cont:
@@ -126,7 +133,7 @@ def lane_plan(nodes, outs, nlanes: int):
         waits = []
         c = clock[lane]
         latest = {}                          # per producing lane, its latest node among deps
-        for j in deps:
+        for j in need:
             latest[lane_of[j]] = max(latest.get(lane_of[j], -1), j)
         for a, j in sorted(latest.items(), key=lambda t: t[1]):
             if a != lane and c.get(a, -2) < j:
@@ -418,7 +425,11 @@ class Replica:
         # stream, four streams, as many as the hardware queues a process gets by default), each
         # lane with a workspace of its own (see _forward_plan)
         self.fwd_plan = self._forward_plan(self.kFwdLanes)
-        used = sorted({lane for _, lane, _ in self.fwd_plan[0]} - {0})
+        # ---- the backward pass's independent branches: up to kFwdLanes - 1 streams (the side
+        # stream carries the filter gradients there); backward lane k runs on lane stream k + 1
+        self.bwd_plan = self._backward_plan(self.kFwdLanes - 1)
+        used = sorted(({lane for _, lane, _ in self.fwd_plan[0]} | {lane + 1 for _, lane, _ in self.bwd_plan[0]
+                                                                    if lane > 0}) - {0})
         self.lane_streams = {k: self.side if k == 1 else torch.cuda.Stream(device=dev) for k in used}
         self.lane_ws = {k: torch.zeros_like(self.ws) for k in used}
         self.marks = {}                          # node index (or "start") -> ops.Mark, made on first use
@@ -445,7 +456,47 @@ class Replica:
                 o = {op.dst}
             nodes.append(op)
             outs.append(o)
-        return lane_plan(nodes, outs, nlanes)
+        return lane_plan(nodes, access_deps([{op.src} for op in nodes], outs, ordered_writes=False), nlanes)
+
+    def _backward_access(self):
+        """The backward nodes (reverse forward order) with the gradient tensors each reads and
+        writes: its output gradient (read; written too where its ReLU or bias backward runs in
+        place, which a concat's ReLU group does in its first node unless the concat's last
+        reader has done it) and its input's gradient (written, accumulated after earlier
+        writers)."""
+        net, grouped = self.net, set()
+        nodes, reads, writes = [], [], []
+        for op in reversed(self.ops):
+            src_grad = op.src != "x" or net.input_grad
+            r, w = set(), set()
+            if isinstance(op, Pool):
+                r.add(op.dst)
+                if op.name in self.pool_relu or src_grad:
+                    w.add(op.src)
+                if src_grad and op.name in self.relu_last:
+                    grouped.add(id(self.relu_last[op.name][1][2]))
+            else:
+                members = self.merged[op.name]["members"] if op.name in self.merged else [op]
+                for m in members:
+                    r.add(m.dst)
+                    if not m.relu or (m.name not in self.relu_fused and m.name not in self.relu_groups):
+                        # (the output's pre-activation gradient: a buffer slice of this op's own)
+                        w.add(m.dst if m.dst != net.output else "dpre_out:" + m.name)
+                    elif m.name in self.relu_groups and id(self.relu_groups[m.name][2]) not in grouped:
+                        grouped.add(id(self.relu_groups[m.name][2]))
+                        w.add(m.dst)
+                if src_grad:
+                    w.add(op.src)
+                    if op.name in self.relu_last:
+                        grouped.add(id(self.relu_last[op.name][1][2]))
+            nodes.append(op)
+            reads.append(r)
+            writes.append(w)
+        return nodes, reads, writes
+
+    def _backward_plan(self, nlanes: int):
+        nodes, reads, writes = self._backward_access()
+        return lane_plan(nodes, access_deps(reads, writes), nlanes)
 
     def _mark(self, key):
         m = self.marks.get(key)
@@ -462,10 +513,12 @@ class Replica:
 
     def _bias_ws(self, key, need: int) -> torch.Tensor:
         """The workspace of one deferred bias gradient, made at its first use and kept (a recorded
-        program finds its partials where its calls left them)."""
+        program finds its partials where its calls left them).  Left uninitialised: its producer
+        writes every partial it sums, and a fill on the allocating stream could land after a
+        producer on a lane stream has written it."""
         t = self.bias_ws.get(key)
         if t is None or t.numel() < need:
-            t = torch.zeros(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=self.params.device)
+            t = torch.empty(max(16, (need + 15) // 16 * 16), dtype=torch.uint8, device=self.params.device)
             self.bias_ws[key] = t
         return t
 
@@ -553,7 +606,7 @@ class Replica:
         """The last step's batch-mean cross-entropy (host copy; synchronises)."""
         return float(self.loss_rows.double().mean())
 
-    def _relu_backward(self, op, dy, trace, stream, defer, jobs, grouped):
+    def _relu_backward(self, op, dy, trace, stream, defer, jobs, grouped, lws):
         """The ReLU (or bias-only) backward of convolution ``op``'s output gradient ``dy``, unless a
         fused kernel forms it (a pool's or a consumer's input gradient); returns the gradient
         before the ReLU, the one its filter and input gradients read."""
@@ -566,7 +619,7 @@ class Replica:
                 jobs.append((ops.bias_relu_bwd(None, dy, dpre=dpre, ws=ws, stream=stream, defer=True)[1],
                              self.db[op.name]))
             else:
-                ops.bias_relu_bwd(None, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
+                ops.bias_relu_bwd(None, dy, dpre=dpre, dbias=self.db[op.name], ws=lws, stream=stream)
             if trace: trace("bias_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
         elif op.name in self.relu_fused:
             dpre = dy                        # written by the fused pool / input-gradient backward
@@ -583,7 +636,7 @@ class Replica:
                     jobs.append((ops.bias_relu_bwd(yg, dyg, dpre=dyg, ws=ws, stream=stream, defer=True)[1],
                                  dbg))
                 else:
-                    ops.bias_relu_bwd(yg, dyg, dpre=dyg, dbias=dbg, ws=self.ws, stream=stream)
+                    ops.bias_relu_bwd(yg, dyg, dpre=dyg, dbias=dbg, ws=lws, stream=stream)
                 if trace: trace("bias_relu_bwd:end", op, stream=stream, dpre=dyg, db=dbg)
         else:
             y = self._slice(self.act, op)
@@ -594,11 +647,11 @@ class Replica:
                 jobs.append((ops.bias_relu_bwd(y, dy, dpre=dpre, ws=ws, stream=stream, defer=True)[1],
                              self.db[op.name]))
             else:
-                ops.bias_relu_bwd(y, dy, dpre=dpre, dbias=self.db[op.name], ws=self.ws, stream=stream)
+                ops.bias_relu_bwd(y, dy, dpre=dpre, dbias=self.db[op.name], ws=lws, stream=stream)
             if trace: trace("bias_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[op.name])
         return dpre
 
-    def _input_grad_relu_last(self, op, dpre, w, beta, trace, stream, defer, jobs, grouped):
+    def _input_grad_relu_last(self, op, dpre, w, beta, trace, stream, defer, jobs, grouped, lws):
         """The input gradient of convolution ``op`` as the last of its input's readers, fused with
         the ReLU backward of the group of convolutions that produced the whole input."""
         t, (c0, width, run) = self.relu_last[op.name]
@@ -613,140 +666,162 @@ class Replica:
             jobs.append((ops.conv2d_bwd_input_relu_bwd(dpre, w, y, dx, (op.sh, op.sw), op.pads, ws=ws, stream=stream,
                                                        defer=True, beta=beta)[1], dbg))
         else:
-            ops.conv2d_bwd_input_relu_bwd(dpre, w, y, dx, (op.sh, op.sw), op.pads, dbias=dbg, ws=self.ws,
+            ops.conv2d_bwd_input_relu_bwd(dpre, w, y, dx, (op.sh, op.sw), op.pads, dbias=dbg, ws=lws,
                                           stream=stream, beta=beta)
         if trace: trace("conv_bwd_input_relu_bwd:end", op, stream=stream, dpre=dx, db=dbg)
 
-    def backward(self, trace=None, stream=None, side=None):
+    def backward(self, trace=None, stream=None, side=None, lanes=True):
         """Gradients of every variable.  With ``side`` (a second stream), the filter gradient
         of each convolution that also has an input gradient runs there, concurrently with that
         input gradient and everything after it on ``stream``: the two only read the same
         tensors, and the side stream joins back before this returns (the dataflow executor runs
         independent kernels on several GPU streams, Section 5)."""
-        net = self.net
-        written = set()
-        grouped = set()                          # ReLU groups whose backward has run
         cur = stream if stream is not None else torch.cuda.current_stream()
         # (traced steps form each bias gradient at once, so that the tracer can check it)
         defer = trace is None and self.defer_bias
         jobs = []                                # deferred bias gradients: (partials, dbias)
-        for op in reversed(self.ops):
-            dy = self._slice(self.grad, op) if op.name not in self.merged else None
-            src_grad = op.src != "x" or net.input_grad
-            beta = 1.0 if op.src in written else 0.0
-            if op.name in self.merged:
-                # each member's ReLU backward (most are fused into other kernels), then the merged
-                # filter and input gradients over the members' adjacent gradient channels
-                for m in self.merged[op.name]["members"]:
-                    self._relu_backward(m, self._slice(self.grad, m), trace, stream, defer, jobs, grouped)
-                dpre, x = self.m_grad[op.name], self.act[op.src]
-                on_side = side is not None and src_grad
-                if on_side:
-                    ops.stream_wait(side, cur)
-                fs = side if on_side else stream
-                dw = self.mdW[op.name]
-                if trace: trace("conv_bwd_filter", op, stream=fs, x=x, dy=dpre)
-                ops.conv2d_bwd_filter(x, dpre, (1, 1), (1, 1), op.pads, dw=dw,
-                                      ws=self.ws_side if on_side else self.ws, stream=fs)
-                if trace: trace("conv_bwd_filter:end", op, stream=fs, dw=dw)
-                if src_grad and op.name in self.relu_last:
-                    self._input_grad_relu_last(op, dpre, self.mWlp[op.name], beta, trace, stream, defer, jobs,
-                                               grouped)
-                    written.add(op.src)
-                elif src_grad:
-                    dx, w = self.grad[op.src], self.mWlp[op.name]
-                    if trace: trace("conv_bwd_input", op, stream=stream, dy=dpre, w=w, dx=dx, beta=beta)
-                    ops.conv2d_bwd_input(dpre, w, dx, (1, 1), op.pads, beta=beta, ws=self.ws, stream=stream)
-                    if trace: trace("conv_bwd_input:end", op, stream=stream, dx=dx)
-                    written.add(op.src)
-                continue
-            if isinstance(op, Conv):
-                dpre = self._relu_backward(op, dy, trace, stream, defer, jobs, grouped)
-                x = self.act[op.src]
-                # a filter gradient with no input gradient beside it (the first layer) stays
-                # on the main stream, where it is next on the critical path
-                on_side = side is not None and src_grad
-                if on_side:
-                    ops.stream_wait(side, cur)
-                fs = side if on_side else stream
-                if trace: trace("conv_bwd_filter", op, stream=fs, x=x, dy=dpre)
-                ops.conv2d_bwd_filter(x, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, dw=self.dW[op.name],
-                                      ws=self.ws_side if on_side else self.ws, stream=fs)
-                if trace: trace("conv_bwd_filter:end", op, stream=fs, dw=self.dW[op.name])
-                if src_grad and op.name in self.bwi_relu:
-                    prod = self.bwi_relu[op.name]
-                    dx, y = self.grad[op.src], self.act[op.src]
-                    if trace: trace("conv_bwd_input_relu_bwd", op, stream=stream, dy=dpre, w=self.Wlp[op.name],
-                                    y=y)
-                    if defer:
-                        ws = self._bias_ws(("bwi", op.name), ops.conv2d_workspace_bytes(
-                            3, y, op.cout, op.kh, op.kw, (op.sh, op.sw), op.pads))
-                        jobs.append((ops.conv2d_bwd_input_relu_bwd(dpre, self.Wlp[op.name], y, dx, (op.sh, op.sw),
-                                                                   op.pads, ws=ws, stream=stream, defer=True)[1],
-                                     self.db[prod.name]))
-                    else:
-                        ops.conv2d_bwd_input_relu_bwd(dpre, self.Wlp[op.name], y, dx, (op.sh, op.sw), op.pads,
-                                                      dbias=self.db[prod.name], ws=self.ws, stream=stream)
-                    if trace: trace("conv_bwd_input_relu_bwd:end", op, stream=stream, dpre=dx, db=self.db[prod.name])
-                elif src_grad and op.name in self.relu_last:
-                    self._input_grad_relu_last(op, dpre, self.Wlp[op.name], beta, trace, stream, defer, jobs,
-                                               grouped)
-                elif src_grad:
-                    dx = self.grad[op.src]
-                    if trace: trace("conv_bwd_input", op, stream=stream, dy=dpre, w=self.Wlp[op.name], dx=dx,
-                                    beta=beta)
-                    ops.conv2d_bwd_input(dpre, self.Wlp[op.name], dx, (op.sh, op.sw), op.pads, beta=beta,
-                                         ws=self.ws, stream=stream)
-                    if trace: trace("conv_bwd_input:end", op, stream=stream, dx=dx)
-            elif op.name in self.pool_relu:
-                conv = self.pool_relu[op.name]
-                y, dpre, am = self.act[op.src], self.grad[op.src], self.argmax[op.name]
-                py = self._slice(self.act, op)
-                if trace: trace("maxpool_relu_bwd", op, stream=stream, dy=dy, argmax=am, y=y, py=py, dpre=dpre,
-                                beta=beta)
-                # (the pool's output gives the ReLU mask where the gradient is not accumulated)
-                if defer:
-                    ws = self._bias_ws(("pool", op.name), ops.bias_relu_bwd_workspace_bytes(dpre))
-                    jobs.append((ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads,
-                                                          beta=beta, ws=ws, stream=stream, py=py, defer=True)[1],
-                                 self.db[conv.name]))
-                else:
-                    ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
-                                             dbias=self.db[conv.name], ws=self.ws, stream=stream, py=py)
-                if trace: trace("maxpool_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[conv.name])
-            elif src_grad and op.name in self.relu_last:
-                # the last reader of a concat: its pool gradient added, then the concat's ReLU backward
-                t, (c0, width, run) = self.relu_last[op.name]
-                y, dpre, am = self.act[t], self.grad[t], self.argmax[op.name]
-                bo = self._layout[run[0].name][2]
-                dbg = self.grads[bo:bo + width]
-                grouped.add(id(run))
-                py = self._slice(self.act, op)
-                if trace: trace("maxpool_relu_bwd", op, stream=stream, dy=dy, argmax=am, y=y, py=py, dpre=dpre,
-                                beta=beta)
-                if defer:
-                    ws = self._bias_ws(("last", op.name), ops.bias_relu_bwd_workspace_bytes(dpre))
-                    jobs.append((ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads,
-                                                          beta=beta, ws=ws, stream=stream, py=py, defer=True)[1],
-                                 dbg))
-                else:
-                    ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
-                                             dbias=dbg, ws=self.ws, stream=stream, py=py)
-                if trace: trace("maxpool_relu_bwd:end", op, stream=stream, dpre=dpre, db=dbg)
-            else:
-                if src_grad:
-                    dx = self.grad[op.src]
-                    am = self.argmax[op.name]
-                    if trace: trace("maxpool_bwd", op, stream=stream, dy=dy, argmax=am, dx=dx, beta=beta)
-                    ops.maxpool_bwd(dy, am, dx, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
-                                    stream=stream)
-                    if trace: trace("maxpool_bwd:end", op, stream=stream, dx=dx)
-            if src_grad:
-                written.add(op.src)
+        state = (set(), set(), jobs, defer)      # gradients written so far, ReLU groups done
+        if trace is not None or not lanes or not self.lane_streams:
+            for op in reversed(self.ops):
+                self._backward_node(op, trace, stream, side, self.ws, state)
+        else:
+            plan, joins = self.bwd_plan
+            needed = {j for _, _, waits in plan for j in waits} | set(joins)
+            if "start" in needed:
+                self._mark(("b", "start")).record(cur)
+            for i, (op, lane, waits) in enumerate(plan):
+                st = cur if lane == 0 else self.lane_streams[lane + 1]
+                for j in waits:
+                    self._mark(("b", j)).wait(st)
+                self._backward_node(op, None, st, side, self.ws if lane == 0 else self.lane_ws[lane + 1], state)
+                if i in needed:
+                    self._mark(("b", i)).record(st)
+            for j in joins:
+                self._mark(("b", j)).wait(cur)
         if jobs:
             ops.bias_grad_finish(jobs, stream=stream)
         if side is not None:
             ops.stream_wait(cur, side)
+
+    def _backward_node(self, op, trace, stream, side, ws, state):
+        """One op's gradients: its ReLU (or bias) backward, its filter gradient (on ``side`` when
+        given and the op has an input gradient too) and its input gradient, on ``stream`` with
+        workspace ``ws``."""
+        net = self.net
+        written, grouped, jobs, defer = state
+        cur = stream if stream is not None else torch.cuda.current_stream()
+        dy = self._slice(self.grad, op) if op.name not in self.merged else None
+        src_grad = op.src != "x" or net.input_grad
+        beta = 1.0 if op.src in written else 0.0
+        if op.name in self.merged:
+            # each member's ReLU backward (most are fused into other kernels), then the merged
+            # filter and input gradients over the members' adjacent gradient channels
+            for m in self.merged[op.name]["members"]:
+                self._relu_backward(m, self._slice(self.grad, m), trace, stream, defer, jobs, grouped, ws)
+            dpre, x = self.m_grad[op.name], self.act[op.src]
+            on_side = side is not None and src_grad
+            if on_side:
+                ops.stream_wait(side, cur)
+            fs = side if on_side else stream
+            dw = self.mdW[op.name]
+            if trace: trace("conv_bwd_filter", op, stream=fs, x=x, dy=dpre)
+            ops.conv2d_bwd_filter(x, dpre, (1, 1), (1, 1), op.pads, dw=dw,
+                                  ws=self.ws_side if on_side else ws, stream=fs)
+            if trace: trace("conv_bwd_filter:end", op, stream=fs, dw=dw)
+            if src_grad and op.name in self.relu_last:
+                self._input_grad_relu_last(op, dpre, self.mWlp[op.name], beta, trace, stream, defer, jobs,
+                                           grouped, ws)
+                written.add(op.src)
+            elif src_grad:
+                dx, w = self.grad[op.src], self.mWlp[op.name]
+                if trace: trace("conv_bwd_input", op, stream=stream, dy=dpre, w=w, dx=dx, beta=beta)
+                ops.conv2d_bwd_input(dpre, w, dx, (1, 1), op.pads, beta=beta, ws=ws, stream=stream)
+                if trace: trace("conv_bwd_input:end", op, stream=stream, dx=dx)
+                written.add(op.src)
+            return
+        if isinstance(op, Conv):
+            dpre = self._relu_backward(op, dy, trace, stream, defer, jobs, grouped, ws)
+            x = self.act[op.src]
+            # a filter gradient with no input gradient beside it (the first layer) stays
+            # on the main stream, where it is next on the critical path
+            on_side = side is not None and src_grad
+            if on_side:
+                ops.stream_wait(side, cur)
+            fs = side if on_side else stream
+            if trace: trace("conv_bwd_filter", op, stream=fs, x=x, dy=dpre)
+            ops.conv2d_bwd_filter(x, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, dw=self.dW[op.name],
+                                  ws=self.ws_side if on_side else ws, stream=fs)
+            if trace: trace("conv_bwd_filter:end", op, stream=fs, dw=self.dW[op.name])
+            if src_grad and op.name in self.bwi_relu:
+                prod = self.bwi_relu[op.name]
+                dx, y = self.grad[op.src], self.act[op.src]
+                if trace: trace("conv_bwd_input_relu_bwd", op, stream=stream, dy=dpre, w=self.Wlp[op.name],
+                                y=y)
+                if defer:
+                    ws = self._bias_ws(("bwi", op.name), ops.conv2d_workspace_bytes(
+                        3, y, op.cout, op.kh, op.kw, (op.sh, op.sw), op.pads))
+                    jobs.append((ops.conv2d_bwd_input_relu_bwd(dpre, self.Wlp[op.name], y, dx, (op.sh, op.sw),
+                                                               op.pads, ws=ws, stream=stream, defer=True)[1],
+                                 self.db[prod.name]))
+                else:
+                    ops.conv2d_bwd_input_relu_bwd(dpre, self.Wlp[op.name], y, dx, (op.sh, op.sw), op.pads,
+                                                  dbias=self.db[prod.name], ws=ws, stream=stream)
+                if trace: trace("conv_bwd_input_relu_bwd:end", op, stream=stream, dpre=dx, db=self.db[prod.name])
+            elif src_grad and op.name in self.relu_last:
+                self._input_grad_relu_last(op, dpre, self.Wlp[op.name], beta, trace, stream, defer, jobs,
+                                           grouped, ws)
+            elif src_grad:
+                dx = self.grad[op.src]
+                if trace: trace("conv_bwd_input", op, stream=stream, dy=dpre, w=self.Wlp[op.name], dx=dx,
+                                beta=beta)
+                ops.conv2d_bwd_input(dpre, self.Wlp[op.name], dx, (op.sh, op.sw), op.pads, beta=beta,
+                                     ws=ws, stream=stream)
+                if trace: trace("conv_bwd_input:end", op, stream=stream, dx=dx)
+        elif op.name in self.pool_relu:
+            conv = self.pool_relu[op.name]
+            y, dpre, am = self.act[op.src], self.grad[op.src], self.argmax[op.name]
+            py = self._slice(self.act, op)
+            if trace: trace("maxpool_relu_bwd", op, stream=stream, dy=dy, argmax=am, y=y, py=py, dpre=dpre,
+                            beta=beta)
+            # (the pool's output gives the ReLU mask where the gradient is not accumulated)
+            if defer:
+                ws = self._bias_ws(("pool", op.name), ops.bias_relu_bwd_workspace_bytes(dpre))
+                jobs.append((ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads,
+                                                      beta=beta, ws=ws, stream=stream, py=py, defer=True)[1],
+                             self.db[conv.name]))
+            else:
+                ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
+                                         dbias=self.db[conv.name], ws=ws, stream=stream, py=py)
+            if trace: trace("maxpool_relu_bwd:end", op, stream=stream, dpre=dpre, db=self.db[conv.name])
+        elif src_grad and op.name in self.relu_last:
+            # the last reader of a concat: its pool gradient added, then the concat's ReLU backward
+            t, (c0, width, run) = self.relu_last[op.name]
+            y, dpre, am = self.act[t], self.grad[t], self.argmax[op.name]
+            bo = self._layout[run[0].name][2]
+            dbg = self.grads[bo:bo + width]
+            grouped.add(id(run))
+            py = self._slice(self.act, op)
+            if trace: trace("maxpool_relu_bwd", op, stream=stream, dy=dy, argmax=am, y=y, py=py, dpre=dpre,
+                            beta=beta)
+            if defer:
+                ws = self._bias_ws(("last", op.name), ops.bias_relu_bwd_workspace_bytes(dpre))
+                jobs.append((ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads,
+                                                      beta=beta, ws=ws, stream=stream, py=py, defer=True)[1],
+                             dbg))
+            else:
+                ops.maxpool_bwd_relu_bwd(dy, am, y, dpre, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
+                                         dbias=dbg, ws=ws, stream=stream, py=py)
+            if trace: trace("maxpool_relu_bwd:end", op, stream=stream, dpre=dpre, db=dbg)
+        else:
+            if src_grad:
+                dx = self.grad[op.src]
+                am = self.argmax[op.name]
+                if trace: trace("maxpool_bwd", op, stream=stream, dy=dy, argmax=am, dx=dx, beta=beta)
+                ops.maxpool_bwd(dy, am, dx, (op.kh, op.kw), (op.sh, op.sw), op.pads, beta=beta,
+                                stream=stream)
+                if trace: trace("maxpool_bwd:end", op, stream=stream, dx=dx)
+        if src_grad:
+            written.add(op.src)
 
     def update(self, trace=None, stream=None):
         a = self.opt_args

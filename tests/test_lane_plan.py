@@ -8,7 +8,7 @@ order of each lane, and each wait) rather than the vector clocks the planner use
 import pytest
 
 from paper_1605_08695_amd import workloads as W
-from paper_1605_08695_amd.step import lane_plan, _merge_groups
+from paper_1605_08695_amd.step import access_deps, lane_plan, _merge_groups
 
 
 def _nodes(net, merge):
@@ -26,6 +26,10 @@ def _nodes(net, merge):
             nodes.append(g["op"])
             outs.append({m.dst for m in g["members"]})
     return nodes, outs
+
+
+def _deps(nodes, outs):
+    return access_deps([{op.src} for op in nodes], outs, ordered_writes=False)
 
 
 def _check(nodes, outs, plan, joins, nlanes):
@@ -74,7 +78,7 @@ NETS = [("alexnet", lambda: W.alexnet(batch=8)), ("vgg16", lambda: W.vgg16(batch
 @pytest.mark.parametrize("nlanes", [1, 2, 4])
 def test_lane_plan_orders_every_dependency(name, make, merge, nlanes):
     nodes, outs = _nodes(make(), merge)
-    plan, joins = lane_plan(nodes, outs, nlanes)
+    plan, joins = lane_plan(nodes, _deps(nodes, outs), nlanes)
     _check(nodes, outs, plan, joins, nlanes)
     if nlanes == 1:
         assert all(lane == 0 and not waits for _, lane, waits in plan) and not joins
@@ -83,10 +87,11 @@ def test_lane_plan_orders_every_dependency(name, make, merge, nlanes):
 def test_lane_plan_runs_branches_side_by_side():
     """Chains stay on one stream; an inception module's branches are spread over several."""
     for make in (lambda: W.alexnet(batch=8), lambda: W.vgg16(batch=2, hw=32)):
-        plan, joins = lane_plan(*_nodes(make(), True), 4)
+        nodes, outs = _nodes(make(), True)
+        plan, joins = lane_plan(nodes, _deps(nodes, outs), 4)
         assert {lane for _, lane, _ in plan} == {0} and not joins
     nodes, outs = _nodes(W.googlenet(batch=2), True)
-    plan, _ = lane_plan(nodes, outs, 4)
+    plan, _ = lane_plan(nodes, _deps(nodes, outs), 4)
     lane = {op.name: l for op, l, _ in plan}
     # module 3a: the 5x5 branch and the pooling branch beside the merged 1x1 / 3x3 chain
     assert lane["m3a_3x3"] == lane["merged_m3a_1x1"]
@@ -97,7 +102,7 @@ def test_lane_plan_runs_branches_side_by_side():
 def test_lane_plan_catches_a_missing_wait():
     """The checker itself: dropping one wait from a valid plan must fail it."""
     nodes, outs = _nodes(W.googlenet(batch=2), True)
-    plan, joins = lane_plan(nodes, outs, 4)
+    plan, joins = lane_plan(nodes, _deps(nodes, outs), 4)
     k = next(i for i, (_, _, w) in enumerate(plan) if any(j != "start" for j in w))
     op, lane, waits = plan[k]
     bad = list(plan)
