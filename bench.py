@@ -24,6 +24,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import faulthandler
 import json
 import os
 import sys
@@ -324,6 +325,7 @@ def measure_workloads(args, torch, W, Replica):
     out = {}
     for make in (W.single_layer, W.vgg16, W.googlenet, W.inception_v3):
         net = make()
+        print("bench: workload %s" % net.name, file=sys.stderr, flush=True)
         rep = Replica(net, W.make_inputs(net, seed=args.seed))
         for _ in range(2):
             rep.step()
@@ -531,6 +533,7 @@ def step_figures(net, rep, per_kind, per_layer, D):
 
 
 def main():
+    faulthandler.enable()            # a crash prints where every thread was
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs one replica on one GPU; multi-GPU data parallelism is not built "
@@ -636,6 +639,7 @@ def main():
     # step's real cache state), a 512 MiB fill for the cold ones (every cache flushed).
     reps = max(3, min(10, args.steps))
     pad = sleep_cycles_for(torch, 200.0)
+    print("bench: per-op pass (warm, cold)", file=sys.stderr, flush=True)
     warm = per_op_pass(torch, rep, EventTrace(torch, pad_cycles=pad), reps)
     flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
     cold = per_op_pass(torch, rep, EventTrace(torch, flush=flush), reps)
@@ -660,7 +664,10 @@ def main():
 
     classifier = None
     if args.classifier_steps > 0 and not args.metric_only:
+        print("bench: AlexNet with its classifier", file=sys.stderr, flush=True)
         classifier = measure_classifier(args, torch, W, Replica)
+    if not (args.no_sampled or args.metric_only):
+        print("bench: sampled softmax", file=sys.stderr, flush=True)
     sampled = None if args.no_sampled or args.metric_only else measure_sampled(args, torch, W)
     others = None if args.metric_only else measure_workloads(args, torch, W, Replica)
 

@@ -537,6 +537,25 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
         compute(stage(S_));
     };
 
+    // The forward bias of this lane's channels, loaded before the main loop so that its latency
+    // hides under the first copies instead of stalling the epilogue.
+    float bq[MI][4];
+#pragma unroll
+    for (int x = 0; x < MI; ++x)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) bq[x][q] = 0.f;
+    if constexpr (DIR == DIR_FWD) {
+        if (a.bias != nullptr && a.k_split == 0) {
+#pragma unroll
+            for (int x = 0; x < MI; ++x) {
+                const int i = i0 + wi * WI + x * 16 + 4 * lg;
+                if (i < a.NI)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) bq[x][q] = a.bias[i + q];
+            }
+        }
+    }
+
     if (nk > 0) {
         issue(0, lds0);
         if (NS == 3 && nk > 1) issue(1, lds1);
@@ -567,9 +586,14 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     for (int x = 0; x < MI; ++x)
 #pragma unroll
         for (int q = 0; q < 4; ++q) cs[x][q] = 0.f;
+    // Row offsets of this lane's output rows, then (input gradients accumulated with beta or
+    // masked by the ReLU) every old value and ReLU output the stores combine with, loaded
+    // together: one memory latency instead of one per 16 x 16 tile behind the stores.
+    int64_t roff[MJ];
 #pragma unroll
     for (int y = 0; y < MJ; ++y) {
         const int j = j0 + wj * WJ + y * 16 + ld;
+        roff[y] = 0;
         if (j >= MJ_ext) continue;
         int64_t rowoff;
         if constexpr (DIR == DIR_FWD) {
@@ -589,6 +613,34 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
         } else {
             rowoff = (int64_t)bz * a.split_stride + (int64_t)j * a.K;
         }
+        roff[y] = rowoff;
+    }
+    uint2 oldv[MJ][MI], yv[MJ][MI];
+    if constexpr (DIR == DIR_BWD_DATA) {
+        if (a.k_split == 0 && (a.beta != 0.f || relu)) {
+#pragma unroll
+            for (int y = 0; y < MJ; ++y) {
+                const int j = j0 + wj * WJ + y * 16 + ld;
+                if (j >= MJ_ext) continue;
+#pragma unroll
+                for (int x = 0; x < MI; ++x) {
+                    const int i = i0 + wi * WI + x * 16 + 4 * lg;
+                    if (i >= a.NI) continue;
+                    if (a.beta != 0.f)
+                        oldv[y][x] = *reinterpret_cast<const uint2 *>(reinterpret_cast<const bf16_t *>(a.out) +
+                                                                      roff[y] + i);
+                    if (relu)
+                        yv[y][x] = *reinterpret_cast<const uint2 *>(reinterpret_cast<const bf16_t *>(a.relu_y) +
+                                                                    roff[y] + i);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int y = 0; y < MJ; ++y) {
+        const int j = j0 + wj * WJ + y * 16 + ld;
+        if (j >= MJ_ext) continue;
+        const int64_t rowoff = roff[y];
 #pragma unroll
         for (int x = 0; x < MI; ++x) {
             const int i = i0 + wi * WI + x * 16 + 4 * lg;
@@ -609,17 +661,16 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
                 float r4[4] = {v[0], v[1], v[2], v[3]};
                 if constexpr (DIR == DIR_BWD_DATA) {
                     if (a.beta != 0.f) {
-                        const uint2 old = *reinterpret_cast<const uint2 *>(o);
+                        const uint2 old = oldv[y][x];
                         r4[0] += a.beta * bf16_to_f32(old.x & 0xffffu);
                         r4[1] += a.beta * bf16_to_f32(old.x >> 16);
                         r4[2] += a.beta * bf16_to_f32(old.y & 0xffffu);
                         r4[3] += a.beta * bf16_to_f32(old.y >> 16);
                     }
                     if (relu) {
-                        const uint2 yv = *reinterpret_cast<const uint2 *>(
-                            reinterpret_cast<const bf16_t *>(a.relu_y) + rowoff + i);
-                        const float yq[4] = {bf16_to_f32(yv.x & 0xffffu), bf16_to_f32(yv.x >> 16),
-                                             bf16_to_f32(yv.y & 0xffffu), bf16_to_f32(yv.y >> 16)};
+                        const uint2 yy = yv[y][x];
+                        const float yq[4] = {bf16_to_f32(yy.x & 0xffffu), bf16_to_f32(yy.x >> 16),
+                                             bf16_to_f32(yy.y & 0xffffu), bf16_to_f32(yy.y >> 16)};
 #pragma unroll
                         for (int q = 0; q < 4; ++q) r4[q] = yq[q] > 0.f ? r4[q] : 0.f;
                     }
@@ -628,7 +679,7 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
                     if (a.bias != nullptr) {      // fused bias + ReLU, rounded once (i + 3 < NI)
 #pragma unroll
                         for (int q = 0; q < 4; ++q) {
-                            const float v = r4[q] + a.bias[i + q];
+                            const float v = r4[q] + bq[x][q];
                             r4[q] = v > 0.f ? v : 0.f;
                         }
                     }

@@ -533,7 +533,9 @@ class Replica:
     def forward(self, trace=None, stream=None, lanes=True):
         """The forward pass on ``stream``; untraced, with ``lanes``, independent branches run on
         the lane streams of the forward plan, which join ``stream`` before the loss."""
-        if trace is not None or not lanes or not self.lane_streams:
+        if trace is not None or not lanes or not self.lane_streams or torch.cuda.is_current_stream_capturing():
+            # (under HIP stream capture the forward pass stays on one stream: the marks are
+            # persistent events, which are not recorded into captures)
             for op in self.ops:
                 self._forward_op(op, trace, stream, self.ws)
         else:
@@ -681,7 +683,7 @@ class Replica:
         defer = trace is None and self.defer_bias
         jobs = []                                # deferred bias gradients: (partials, dbias)
         state = (set(), set(), jobs, defer)      # gradients written so far, ReLU groups done
-        if trace is not None or not lanes or not self.lane_streams:
+        if trace is not None or not lanes or not self.lane_streams or torch.cuda.is_current_stream_capturing():
             for op in reversed(self.ops):
                 self._backward_node(op, trace, stream, side, self.ws, state)
         else:

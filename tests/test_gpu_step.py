@@ -299,10 +299,14 @@ def test_two_stream_step_matches_one_stream(make):
             assert bitwise_equal(one.act[t], two.act[t]), (r, t)
 
 
-def test_graph_capture_replays_match_eager():
+@pytest.mark.parametrize("make", [lambda: W.alexnet(batch=8), lambda: W.googlenet(batch=4)],
+                         ids=["alexnet_b8", "googlenet_b4"])
+def test_graph_capture_replays_match_eager(make):
     """The whole step captured once in a HIP graph; every replay (with eager steps and
-    synchronisations in between) must equal the eager step from the same state."""
-    net = W.alexnet(batch=8)
+    synchronisations in between) must equal the eager step from the same state.  (A network
+    with branches runs its forward and backward passes without the lane streams under capture;
+    its eager steps use them.)"""
+    net = make()
     net.lr = 1e-6            # keep the linear surrogate loss from driving values to inf
     inp = W.make_inputs(net, seed=2)
     eager = Replica(net, inp)
