@@ -299,6 +299,33 @@ def test_two_stream_step_matches_one_stream(make):
             assert bitwise_equal(one.act[t], two.act[t]), (r, t)
 
 
+@pytest.mark.parametrize("make", [lambda: W.googlenet(), lambda: W.inception_v3()],
+                         ids=["googlenet_b128", "inception_v3_b32"])
+def test_full_size_lanes_match_one_stream(make):
+    """At the benchmarked sizes, two steps with the forward and backward branches on the lane
+    streams -- the first recorded into a program, the second issued from it -- must give the
+    same bits as two steps with every op on one stream, from the same variables."""
+    net = make()
+    net.lr = 1e-6
+    rep = Replica(net, W.make_inputs(net, seed=6))
+    snap = rep.snapshot()
+    for _ in range(2):
+        rep.step(concurrent=False)
+    torch.cuda.synchronize()
+    p1, g1 = rep.params.clone(), rep.grads.clone()
+    a1 = {t: v.clone() for t, v in rep.act.items()}
+    rep.restore(snap)
+    prog = rep.record_step()
+    rep.run_program(prog)
+    torch.cuda.synchronize()
+    say("lanes", net.name, "recorded calls:", len(prog))
+    assert bool(torch.isfinite(rep.params).all())
+    assert bitwise_equal(g1, rep.grads) and bitwise_equal(p1, rep.params)
+    for t, v in a1.items():
+        assert bitwise_equal(v, rep.act[t]), t
+    prog.close()
+
+
 @pytest.mark.parametrize("make", [lambda: W.alexnet(batch=8), lambda: W.googlenet(batch=4)],
                          ids=["alexnet_b8", "googlenet_b4"])
 def test_graph_capture_replays_match_eager(make):
