@@ -430,6 +430,51 @@ __global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restric
                 v[q] = *reinterpret_cast<const U4 *>(x + (M::mul(pidx[q], (I)g.xs) + (I)(cv * EPC)));
             }
         }
+        const I opix = M::mul(M::mul((I)n, (I)g.OH) + (I)oh, (I)g.OW) + (I)ow;
+        if constexpr (std::is_same<T, bf16_t>::value && std::is_same<A, uint8_t>::value) {
+            // Chunks with no sign bit in any tap (a ReLU's output): there bf16 bit patterns order
+            // as their values, so each element keeps the largest (bits << 8 | 255 - tap) over its
+            // taps -- one byte permute and one integer max per element and tap -- and a tie goes
+            // to the first tap, as the strict > of the scan below gives it.  A sign bit (a
+            // negative value or -0) or a NaN maximum leaves the chunk to that scan.
+            uint32_t sg = 0;
+#pragma unroll
+            for (int q = 0; q < KH * KW; ++q)
+                if (ok[q]) sg |= v[q].x | v[q].y | v[q].z | v[q].w;
+            if ((sg & 0x80008000u) == 0) {
+                uint32_t kb[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) kb[e] = 0u;
+#pragma unroll
+                for (int q = 0; q < KH * KW; ++q) {
+                    if (!ok[q]) continue;
+                    const uint32_t c = 255u - (uint32_t)q;
+                    const uint32_t d[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) {
+                        // (bytes: the tap code, then the element's two bytes, then zero)
+                        kb[2 * w] = max(kb[2 * w], __builtin_amdgcn_perm(d[w], c, 0x0C050400u));
+                        kb[2 * w + 1] = max(kb[2 * w + 1], __builtin_amdgcn_perm(d[w], c, 0x0C070600u));
+                    }
+                }
+                uint32_t top = 0;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) top = max(top, kb[e]);
+                if ((top >> 8) <= 0x7F80u) {          // no NaN (+inf is 0x7F80)
+                    U4 o;
+                    o.x = __builtin_amdgcn_perm(kb[1], kb[0], 0x06050201u);
+                    o.y = __builtin_amdgcn_perm(kb[3], kb[2], 0x06050201u);
+                    o.z = __builtin_amdgcn_perm(kb[5], kb[4], 0x06050201u);
+                    o.w = __builtin_amdgcn_perm(kb[7], kb[6], 0x06050201u);
+                    int32_t tq[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) tq[e] = 255 - (int32_t)(kb[e] & 0xFFu);
+                    *reinterpret_cast<U4 *>(y + (M::mul(opix, (I)g.ys) + (I)(cv * EPC))) = o;
+                    arg_store<A, EPC>(argmax + (M::mul(opix, (I)g.C) + (I)(cv * EPC)), tq);
+                    continue;
+                }
+            }
+        }
         float best[EPC];
         int32_t bi[EPC];
         bool have = false;
@@ -448,7 +493,6 @@ __global__ __launch_bounds__(256) void maxpool_fwd_win_kernel(const T *__restric
             }
             have = true;
         }
-        const I opix = M::mul(M::mul((I)n, (I)g.OH) + (I)oh, (I)g.OW) + (I)ow;
         *reinterpret_cast<U4 *>(y + (M::mul(opix, (I)g.ys) + (I)(cv * EPC))) = f32_to_chunk<T>(best);
         arg_store<A, EPC>(argmax + (M::mul(opix, (I)g.C) + (I)(cv * EPC)), bi);
     }

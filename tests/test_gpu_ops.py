@@ -387,6 +387,33 @@ def test_maxpool(case, dtype, ties):
         assert torch.equal(dx, dx8), "the tap form routes exactly as the index form"
 
 
+@pytest.mark.parametrize("stride", [1, 2])
+def test_maxpool_bf16_special_values(stride):
+    """bf16 3x3 windows over non-negative values -- exact zeros, repeats, subnormals, the largest
+    finite value, +inf -- where the uint8-tap forward orders elements by their bit patterns, and
+    chunks with a NaN or a sign bit (-0, a negative) that it leaves to the float scan: outputs
+    (NaN where the oracle has one) and selections equal the oracle's, in both argmax forms."""
+    rng = np.random.default_rng(41)
+    shape, pads = (2, 9, 9, 32), (1, 1, 1, 1)
+    vals = np.array([0.0, 0.0, 1.0, 2.0, 2.0, 0.5, 1e-40, 3.0e38, np.inf])
+    a = rng.choice(vals, size=shape)
+    a[0, 2, 2, 0:8] = np.nan                                  # a NaN that a later tap cannot beat
+    a[0, 5, 5, 8] = np.nan
+    a[1, 3, 3, 16:24] = -0.0                                   # sign bits: the float scan
+    a[1, 6, 6, 24] = -1.0
+    x = torch.from_numpy(a).to(torch.bfloat16).to(DEV)
+    y, am = ops.maxpool_fwd(x, (3, 3), stride, pads)
+    y8, taps = ops.maxpool_fwd(x, (3, 3), stride, pads, taps=True)
+    torch.cuda.synchronize()
+    ref_y, ref_am = oracle.maxpool_fwd(f64(x), (3, 3), stride, pads)
+    for got in (y, y8):
+        g = f64(got)
+        assert np.array_equal(g, ref_y, equal_nan=True)
+        assert np.array_equal(np.signbit(g), np.signbit(ref_y))
+    assert np.array_equal(am.cpu().numpy(), ref_am)
+    assert np.array_equal(_taps_to_dense(taps, shape, 3, stride, pads), ref_am)
+
+
 @pytest.mark.parametrize("taps", [False, True], ids=["index", "taps"])
 @pytest.mark.parametrize("dtype", DTYPES, ids=["f32", "bf16"])
 @pytest.mark.parametrize("case", POOL_CASES, ids=[c[0] for c in POOL_CASES])
