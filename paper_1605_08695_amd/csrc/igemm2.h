@@ -534,7 +534,19 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
             wait_barrier<0>();
         }
         if (kt + NS - 1 < nk) issue(kt + NS - 1, stage(std::integral_constant<int, S + NS - 1>{}));
-        compute(stage(S_));
+        if constexpr (DIR != DIR_BWD_FILTER) {
+            // A CU runs two blocks of a launch side by side, and issue arbitration favours the
+            // older one's waves: it finishes well ahead and leaves the other alone on the CU for
+            // the launch's tail.  The two swap the higher wave priority every 1.28 us (the
+            // 100 MHz clock's bit 7; the blocks of the second dispatch round, ids 256 up, take
+            // the other phase), so both progress at the shared rate.  (Scheduling only.)
+            const uint64_t now = __builtin_amdgcn_s_memrealtime();
+            compute(stage(S_));
+            if ((((uint32_t)(now >> 7) ^ (uint32_t)(lin_hw >> 8)) & 1u) != 0) __builtin_amdgcn_s_setprio(1);
+            else __builtin_amdgcn_s_setprio(0);
+        } else {
+            compute(stage(S_));
+        }
     };
 
     // The forward bias of this lane's channels, loaded before the main loop so that its latency
