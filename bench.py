@@ -44,8 +44,10 @@ METRIC = "ms per training step + conv TFLOP/s (% bf16 MFMA peak), AlexNet-shape 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # (defaults: about 0.14 s of warm-up steps, by which the AlexNet step has reached its sustained
+    # rate -- the first hundred steps after start-up run a few per cent slower -- then 200 timed)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--batch", type=int, default=128)
     ap.add_argument("--launch", choices=("program", "streams", "graph", "serial"), default="program",
                     help="the two-stream step recorded once and issued again from C++ (default), two streams "
