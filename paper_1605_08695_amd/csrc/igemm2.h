@@ -598,9 +598,9 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
     for (int x = 0; x < MI; ++x)
 #pragma unroll
         for (int q = 0; q < 4; ++q) cs[x][q] = 0.f;
-    // Row offsets of this lane's output rows, then (input gradients accumulated with beta or
-    // masked by the ReLU) every old value and ReLU output the stores combine with, loaded
-    // together: one memory latency instead of one per 16 x 16 tile behind the stores.
+    // Row offsets of this lane's output rows.  (Loading an input gradient's old values and ReLU
+    // outputs for all of a wave's tiles before the first store ran its kernels faster alone but
+    // the two-stream step slower, about 1 %; they stay loaded tile by tile.)
     int64_t roff[MJ];
 #pragma unroll
     for (int y = 0; y < MJ; ++y) {
@@ -627,27 +627,6 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
         }
         roff[y] = rowoff;
     }
-    uint2 oldv[MJ][MI], yv[MJ][MI];
-    if constexpr (DIR == DIR_BWD_DATA) {
-        if (a.k_split == 0 && (a.beta != 0.f || relu)) {
-#pragma unroll
-            for (int y = 0; y < MJ; ++y) {
-                const int j = j0 + wj * WJ + y * 16 + ld;
-                if (j >= MJ_ext) continue;
-#pragma unroll
-                for (int x = 0; x < MI; ++x) {
-                    const int i = i0 + wi * WI + x * 16 + 4 * lg;
-                    if (i >= a.NI) continue;
-                    if (a.beta != 0.f)
-                        oldv[y][x] = *reinterpret_cast<const uint2 *>(reinterpret_cast<const bf16_t *>(a.out) +
-                                                                      roff[y] + i);
-                    if (relu)
-                        yv[y][x] = *reinterpret_cast<const uint2 *>(reinterpret_cast<const bf16_t *>(a.relu_y) +
-                                                                    roff[y] + i);
-                }
-            }
-        }
-    }
 #pragma unroll
     for (int y = 0; y < MJ; ++y) {
         const int j = j0 + wj * WJ + y * 16 + ld;
@@ -673,14 +652,15 @@ __global__ __launch_bounds__(NW * 64, 2) void igemm2_kernel(const IgArgs a) {
                 float r4[4] = {v[0], v[1], v[2], v[3]};
                 if constexpr (DIR == DIR_BWD_DATA) {
                     if (a.beta != 0.f) {
-                        const uint2 old = oldv[y][x];
+                        const uint2 old = *reinterpret_cast<const uint2 *>(o);
                         r4[0] += a.beta * bf16_to_f32(old.x & 0xffffu);
                         r4[1] += a.beta * bf16_to_f32(old.x >> 16);
                         r4[2] += a.beta * bf16_to_f32(old.y & 0xffffu);
                         r4[3] += a.beta * bf16_to_f32(old.y >> 16);
                     }
                     if (relu) {
-                        const uint2 yy = yv[y][x];
+                        const uint2 yy = *reinterpret_cast<const uint2 *>(
+                            reinterpret_cast<const bf16_t *>(a.relu_y) + rowoff + i);
                         const float yq[4] = {bf16_to_f32(yy.x & 0xffffu), bf16_to_f32(yy.x >> 16),
                                              bf16_to_f32(yy.y & 0xffffu), bf16_to_f32(yy.y >> 16)};
 #pragma unroll
