@@ -4,11 +4,12 @@
 
 namespace tfk {
 
-// 33-64 input channels over many pixels at stride 1: 64 x 192 tiles, which copy 48 flop per byte
-// against 64 x 128's 43 and still give about a round of two blocks per CU (AlexNet conv2, 93312
-// pixels: 486 blocks; 74.8 -> 71.3 us back to back)
+// The forward pass's tile rule.  (64 x 192 tiles for 33-64 input channels over many pixels copy
+// 48 flop per byte against 64 x 128's 43 and ran AlexNet conv2's input gradient faster alone,
+// 74.8 -> 71.3 us back to back, but the sustained two-stream step slower, 0.694 -> 0.705 ms, where
+// the filter gradient of the other stream shares the GPU with it; GoogLeNet and Inception-v3
+// steps are the same either way.)
 static Igemm2Tile bwd_data_tiles(int ni, int mj, int zdim) {
-    if (ni > 32 && ni <= 64 && zdim == 1 && (mj + 191) / 192 >= 384) return {64, 192, 4, 2};
     return igemm2_tiles_narrow(ni, mj, zdim);
 }
 

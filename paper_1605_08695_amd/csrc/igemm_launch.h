@@ -102,8 +102,8 @@ static bool igemm2_launch(IgArgs &a, int mj, int zdim, const Igemm2Tile &t, hipS
         else { igemm2_go<DIR, 128, 96, 4, 2>(a, grid, st); return true; }
     }
     if (t.bj == 192 && t.nw == 4 && t.ns == 2) {
-        // (192-row J tiles: the forward row bands of a fused max-pool, and input gradients over
-        // at most 64 channels; 192-row k-major tiles are not laid out)
+        // (192-row J tiles: the forward row bands of a fused max-pool and 64-channel forward
+        // tiles; 192-row k-major tiles are not laid out)
         if constexpr (DIR == DIR_BWD_FILTER) return false;
         else {
             if (t.bi == 64) { igemm2_go<DIR, 64, 192, 4, 2>(a, grid, st); return true; }

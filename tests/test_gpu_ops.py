@@ -63,7 +63,7 @@ CONV_CASES = [
     # 288 tiles of 128 x 128 (most CUs with one block): 128 x 96 tiles, forward and input gradient
     ("bj96_tiles_fwd", 36, 32, 32, 64, 128, 3, 3, 1, 1, (1, 1, 1, 1)),
     ("bj96_tiles_bwd", 36, 32, 32, 128, 64, 3, 3, 1, 1, (1, 1, 1, 1)),
-    # 64 input channels over 75264 pixels: 64 x 192 input-gradient tiles (392 blocks)
+    # 64 input channels over 75264 pixels (input gradients over many blocks of 64-channel tiles)
     ("c64_bwd_tiles_64x192", 96, 28, 28, 64, 32, 3, 3, 1, 1, (1, 1, 1, 1)),
     # fully connected layers as whole-window convolutions: AlexNet's fc6 (6x6x256 -> 4096) and
     # fc8 (4096 -> 1000 logits), at batch 4
