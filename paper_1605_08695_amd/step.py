@@ -425,9 +425,9 @@ class Replica:
         # stream, four streams, as many as the hardware queues a process gets by default), each
         # lane with a workspace of its own (see _forward_plan)
         self.fwd_plan = self._forward_plan(self.kFwdLanes)
-        # ---- the backward pass's independent branches: up to kFwdLanes - 1 streams (the side
-        # stream carries the filter gradients there); backward lane k runs on lane stream k + 1
-        self.bwd_plan = self._backward_plan(self.kFwdLanes - 1)
+        # ---- the backward pass's independent branches: kBwdLanes streams (the side stream carries
+        # the filter gradients there); backward lane k runs on lane stream k + 1
+        self.bwd_plan = self._backward_plan(self.kBwdLanes)
         used = sorted(({lane for _, lane, _ in self.fwd_plan[0]} | {lane + 1 for _, lane, _ in self.bwd_plan[0]
                                                                     if lane > 0}) - {0})
         self.lane_streams = {k: self.side if k == 1 else torch.cuda.Stream(device=dev) for k in used}
@@ -439,7 +439,11 @@ class Replica:
         self.bias_ws: Dict[object, torch.Tensor] = {}
 
     # ------------------------------------------------------------------ helpers
+    # lanes of the forward and backward passes (sustained program steps, forward / backward:
+    # 4 / 3 GoogLeNet 2.96-2.97 ms, Inception-v3 4.52; 4 / 2 2.95 and 4.48-4.50; 4 / 1 3.03 and
+    # 4.56; 3 / 2 2.93 and 5.33, where a three-stream forward lines Inception's branches up badly)
     kFwdLanes = 4
+    kBwdLanes = 2
 
     def _forward_plan(self, nlanes: int):
         """The forward ops (a pool made inside its convolution left out) placed on ``nlanes``
