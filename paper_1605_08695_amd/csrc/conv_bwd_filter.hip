@@ -15,14 +15,9 @@ struct BwfPlan {
 // shapes: 128 x 128 tiles (even for 192 output channels, where the second channel tile
 // is half empty) and the pixel reduction split into as many parts as keep the blocks within
 // one full round of two blocks per CU (512 blocks): a last round with only a few blocks
-// costs a whole block time, and more splits only add partial-sum traffic (AlexNet conv2-5
-// alone: 357 us with four-block rounds, 297 us with this rule).  A short launch (at most
-// kShortBwf tile x K-tile steps: AlexNet conv2-5) fills three quarters of that round: it runs
-// beside the input gradients of the step's other stream, which take the remaining block
-// slots, and writes and sums fewer fp32 partials (the sustained two-stream AlexNet step:
-// 0.699 ms with 512, 0.687 with 384, 0.692 with 320 or 448, 0.715 with 256); long ones (VGG-16's
-// first four blocks) keep the full round (with 384 everywhere the VGG-16 step took 8.40 ms, not
-// 7.68; with this rule 7.51 against 7.43).
+// costs a whole block time, and more splits only add partial-sum traffic (AlexNet conv2-5:
+// 357 us with four-block rounds, 297 us with this rule; the sustained two-stream AlexNet step
+// 0.686 ms, against 0.694 with 384 blocks for the short launches).
 // 64-channel layers take 64 x 128
 // tiles, layers of at most 32 output channels 32 x 128, multiples of 64 that are not of 128 64 x 128.  (192-channel tiles, which pay in the
 // forward pass, need more registers here than two waves per SIMD have and spill.)
@@ -46,9 +41,7 @@ BwfPlan bwf_plan(int dt, const ConvShape &s, bool v2) {
     const int tiles = ((s.K + p.bi - 1) / p.bi) * ((m + p.bj - 1) / p.bj);
     const int64_t ktot = (int64_t)s.N * s.OH * s.OW;
     const int64_t ktiles = (ktot + bk - 1) / bk;
-    constexpr int64_t kShortBwf = 60000;
-    const bool short_launch = (int64_t)tiles * ktiles <= kShortBwf;
-    const int target = (by64 ? 768 : 512) * (short_launch ? 3 : 4) / 4;
+    const int target = by64 ? 768 : 512;
     int64_t sp = target / tiles;
     const int64_t max_sp = std::max<int64_t>(1, ktiles / 8);   // at least 8 K tiles per split
     sp = std::max<int64_t>(1, std::min<int64_t>(sp, max_sp));
