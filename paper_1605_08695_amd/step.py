@@ -871,6 +871,8 @@ class Replica:
                 self.update(None, stream)
         if not prog.with_update:
             self.update(None, stream)
+        # (the recorded stream joins name this replica's marks by pointer: the program keeps them)
+        prog.marks = dict(self.marks)
         return prog
 
     def run_program(self, prog, stream=None):
