@@ -514,7 +514,10 @@ TFK_API tfk_status tfk_stream_wait(void *waiter, void *producer);
  * mark by pointer: it must outlive the program's use).  tfk_mark_create errors: NULL; ARG (out
  * of host memory); HIP (event creation).  tfk_mark_record / tfk_stream_wait_mark errors: NULL
  * (mark is NULL); HIP.  tfk_mark_destroy(NULL) is a no-op; a mark that work still waits for may
- * be destroyed (the runtime keeps the event until it completes). */
+ * be destroyed (the runtime keeps the event until it completes).  Waiting on a mark that was
+ * never recorded does not wait.  The step keeps marks out of HIP stream captures (a capture of
+ * a step whose branches waited on marks ended in a host fault of the process; not investigated
+ * further). */
 typedef struct tfk_mark tfk_mark;
 TFK_API tfk_status tfk_mark_create(tfk_mark **mark);
 TFK_API void tfk_mark_destroy(tfk_mark *mark);
